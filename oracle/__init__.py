@@ -1,0 +1,151 @@
+"""fp64 CPU oracle for the gated N-D FFT long convolution.
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  It shares no code
+with the HIP library and never imports it.
+
+The arithmetic lives in ``oracle.c`` (plain C, IEEE double):
+
+* :func:`conv_direct` / :func:`conv_direct_points` evaluate the operator's
+  definition (Def. A.2 and Def. A.3 of the appendix "Gated Hyena Computes
+  Separable Attention", with the long convolution of Eq. (HyenaND), section
+  3.2) as an explicit sum;
+* :func:`conv_fft` evaluates it through the convolution theorem with the C
+  file's own radix-2 FFT;
+* :func:`fft1d` exposes that FFT so it can be pinned against a naive DFT.
+
+Inputs are float64 arrays of shape [B, C, L1, ..., LN] (x1, x2, v, k) and [C]
+(D).  ``pad_mode`` is "linear" (zero-padded, cropped to the first L_d outputs
+on every axis) or "circular".
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_SO = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_f64p = ctypes.POINTER(ctypes.c_double)
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.c into liboracle.so with the host C compiler."""
+    if force or not os.path.exists(_SO) or os.path.getmtime(_SO) < os.path.getmtime(_SRC):
+        tmp = _SO + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC,
+               "-lm", "-lpthread"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _SO)
+    return _SO
+
+
+def lib():
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_SO):
+                build()
+            L = ctypes.CDLL(_SO)
+            sig = [_f64p] * 5
+            L.oracle_direct.argtypes = sig + [_f64p, ctypes.c_int, _i64p, ctypes.c_int, _i64p,
+                                              ctypes.c_int64, ctypes.c_int]
+            L.oracle_fft.argtypes = L.oracle_direct.argtypes
+            L.oracle_direct_points.argtypes = sig + [ctypes.c_int, _i64p, ctypes.c_int, _i64p,
+                                                     ctypes.c_int64, _f64p, ctypes.c_int]
+            L.oracle_fft1d.argtypes = [_f64p, ctypes.c_int64, ctypes.c_int]
+            for f in (L.oracle_direct, L.oracle_fft, L.oracle_direct_points, L.oracle_fft1d):
+                f.restype = ctypes.c_int
+            _lib = L
+        return _lib
+
+
+def default_threads() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def _prep(x1, x2, v, k, D):
+    arrs = [np.ascontiguousarray(a, dtype=np.float64) for a in (x1, x2, v, k, D)]
+    shp = arrs[0].shape
+    if len(shp) < 3 or len(shp) > 5:
+        raise ValueError("tensors must be [B, C, L1..LN] with N in 1..3")
+    for a in arrs[1:4]:
+        if a.shape != shp:
+            raise ValueError("x1, x2, v, k must share one shape")
+    if arrs[4].shape != (shp[1],):
+        raise ValueError("D must have shape [C]")
+    dims = np.asarray(shp, dtype=np.int64)
+    return arrs, dims, len(shp) - 2
+
+
+def _ptr(a):
+    return a.ctypes.data_as(_f64p)
+
+
+def _mode(pad_mode: str) -> int:
+    if pad_mode not in ("linear", "circular"):
+        raise ValueError(f"pad_mode must be 'linear' or 'circular', got {pad_mode!r}")
+    return 1 if pad_mode == "circular" else 0
+
+
+def _lines_arg(lines):
+    if lines is None:
+        return None, None, 0
+    la = np.ascontiguousarray(lines, dtype=np.int64)
+    return la, la.ctypes.data_as(_i64p), la.size
+
+
+def _run_lines(fn, x1, x2, v, k, D, pad_mode, lines, nthreads):
+    arrs, dims, nd = _prep(x1, x2, v, k, D)
+    y = np.zeros(arrs[0].shape, dtype=np.float64)
+    la, lp, nl = _lines_arg(lines)
+    rc = fn(*[_ptr(a) for a in arrs], _ptr(y), nd, dims.ctypes.data_as(_i64p), _mode(pad_mode),
+            lp, nl, int(nthreads or default_threads()))
+    if rc != 0:
+        raise RuntimeError(f"oracle returned {rc}")
+    return y
+
+
+def conv_direct(x1, x2, v, k, D, pad_mode="linear", lines=None, nthreads=None):
+    """y by the explicit sum. ``lines`` selects flat (b*C + c) indices; other
+    lines of the returned array are left at zero."""
+    return _run_lines(lib().oracle_direct, x1, x2, v, k, D, pad_mode, lines, nthreads)
+
+
+def conv_fft(x1, x2, v, k, D, pad_mode="linear", lines=None, nthreads=None):
+    """y through the convolution theorem with the oracle's own FFT."""
+    return _run_lines(lib().oracle_fft, x1, x2, v, k, D, pad_mode, lines, nthreads)
+
+
+def conv_direct_points(x1, x2, v, k, D, flat_idx, pad_mode="linear", nthreads=None):
+    """y at the given flat indices of the [B, C, L...] output, by the explicit sum."""
+    arrs, dims, nd = _prep(x1, x2, v, k, D)
+    idx = np.ascontiguousarray(flat_idx, dtype=np.int64)
+    out = np.zeros(idx.size, dtype=np.float64)
+    rc = lib().oracle_direct_points(*[_ptr(a) for a in arrs], nd, dims.ctypes.data_as(_i64p),
+                                    _mode(pad_mode), idx.ctypes.data_as(_i64p), idx.size,
+                                    _ptr(out), int(nthreads or default_threads()))
+    if rc != 0:
+        raise RuntimeError(f"oracle returned {rc}")
+    return out
+
+
+def fft1d(x, sign=-1):
+    """Unnormalised DFT of a complex vector (length a power of two) by the
+    oracle's radix-2 FFT: X[f] = sum_n x[n] exp(sign 2 pi i f n / N)."""
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.complex128).copy())
+    rc = lib().oracle_fft1d(a.ctypes.data_as(_f64p), a.size, int(sign))
+    if rc != 0:
+        raise RuntimeError(f"oracle_fft1d returned {rc}")
+    return a

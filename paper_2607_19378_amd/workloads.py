@@ -1,0 +1,258 @@
+"""Seeded synthetic workloads for the gated N-D FFT long convolution.
+
+This module only draws and quantises inputs.  It holds none of the operator's
+arithmetic, so both the HIP path and the CPU oracle can consume the very same
+bytes without sharing any code that computes the method.
+
+Five named workloads stand in for the paper's data (none of the paper's
+datasets is used):
+
+* ``conv1d_4k``   -- 1D linear, fp32, B=1, C=64, L=4096 (the 1D spatial-recall
+  canvas length of the controlled spatial-recall experiments).
+* ``conv2d_64``   -- 2D linear, fp32, B=8, C=256, 64x64 (image-like; the 2D
+  spatial-recall canvas size).
+* ``conv2d_512c`` -- 2D circular, fp32, B=4, C=128, 512x512 smooth periodic
+  fields (the periodic 512x512 PDE fields of the PDE-surrogate experiments).
+* ``conv3d_128``  -- 3D linear, bf16 storage, B=1, C=64, 128^3 (volumes).
+* ``conv1d_1m``   -- 1D linear, bf16 storage, B=1, C=256, L=2^20 (genomics-scale
+  long context, the 1M point of the context-length study).
+
+Draw recipe (identical for every workload): ``numpy.random.default_rng(seed)``
+(PCG64); draw order x1, x2, v, kernel noise, D, each a ``standard_normal`` array
+in C order of the stated shape.  Values are produced in float64 and rounded
+once, round-to-nearest-even, to the storage dtype.  The per-sample kernel is
+noise times a decay window evaluated in index units from index 0 (the
+zero-displacement tap):
+
+* 1D: ``exp(-l / tau) / sqrt(L)`` with ``l`` the index;
+* 2D/3D linear: ``exp(-r / tau)`` with ``r`` the Euclidean index distance from
+  the origin;
+* 2D circular: ``exp(-r / tau)`` with ``r`` the periodic (wrap-around) distance.
+
+The circular workload's x1, x2, v are smooth fields: white noise filtered with
+a periodic separable Gaussian (sigma = 4 px, taps truncated at +-16, weights
+normalised to sum 1), then standardised per (b, c) field to zero mean and unit
+(population) variance.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+LINEAR = "linear"
+CIRCULAR = "circular"
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    C: int
+    grid: Tuple[int, ...]
+    pad_mode: str
+    dtype: str  # "f32" or "bf16" (storage); compute is fp32 in the kernels
+    seed: int
+    tau: float  # decay length of the kernel window, in index units
+    kernel_norm: bool = False  # 1D windows carry an extra 1/sqrt(L)
+    smooth_sigma: Optional[float] = None  # Gaussian low-pass of x1, x2, v
+    description: str = ""
+
+    @property
+    def ndim(self) -> int:
+        return len(self.grid)
+
+    @property
+    def shape(self) -> Tuple[int, ...]:
+        return (self.B, self.C) + tuple(self.grid)
+
+    @property
+    def elems(self) -> int:
+        n = self.B * self.C
+        for g in self.grid:
+            n *= g
+        return n
+
+    @property
+    def storage_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+    def scaled(self, B: Optional[int] = None, C: Optional[int] = None,
+               grid: Optional[Tuple[int, ...]] = None, name: Optional[str] = None,
+               seed: Optional[int] = None) -> "Workload":
+        """Same recipe at another size (used for small parity cases)."""
+        return Workload(
+            name=name or (self.name + "_scaled"),
+            B=self.B if B is None else B,
+            C=self.C if C is None else C,
+            grid=self.grid if grid is None else tuple(grid),
+            pad_mode=self.pad_mode, dtype=self.dtype,
+            seed=self.seed if seed is None else seed,
+            tau=self.tau, kernel_norm=self.kernel_norm,
+            smooth_sigma=self.smooth_sigma, description=self.description)
+
+
+WORKLOADS: Dict[str, Workload] = {
+    "conv1d_4k": Workload(
+        "conv1d_4k", 1, 64, (4096,), LINEAR, "f32", 20261, 1024.0, kernel_norm=True,
+        description="1D linear gated FFT conv, fp32, B=1 C=64 L=4096, pad 8192, crop first L"),
+    "conv2d_64": Workload(
+        "conv2d_64", 8, 256, (64, 64), LINEAR, "f32", 20262, 16.0,
+        description="2D linear gated FFT conv, fp32, B=8 C=256 64x64, pad 128x128, crop 64x64"),
+    "conv2d_512c": Workload(
+        "conv2d_512c", 4, 128, (512, 512), CIRCULAR, "f32", 20263, 64.0, smooth_sigma=4.0,
+        description="2D circular gated FFT conv, fp32, B=4 C=128 512x512 smooth periodic fields"),
+    "conv3d_128": Workload(
+        "conv3d_128", 1, 64, (128, 128, 128), LINEAR, "bf16", 20264, 24.0,
+        description="3D linear gated FFT conv, bf16 storage, B=1 C=64 128^3, pad 256^3, crop 128^3"),
+    "conv1d_1m": Workload(
+        "conv1d_1m", 1, 256, (1 << 20,), LINEAR, "bf16", 20265, 65536.0, kernel_norm=True,
+        description="1D linear gated FFT conv, bf16 storage, B=1 C=256 L=2^20, pad 2^21, crop first L"),
+}
+
+# Order in which the workloads are listed (small 1D case first).
+ORDER = ["conv1d_4k", "conv2d_64", "conv2d_512c", "conv3d_128", "conv1d_1m"]
+
+
+# ----------------------------------------------------------------------------
+# Rounding to the storage dtype (one RNE rounding from float64)
+# ----------------------------------------------------------------------------
+
+def round_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float64 values once, to nearest-even, to bfloat16; return uint16 bits.
+
+    The significand is rounded to 8 bits with ``numpy.rint`` (half to even) on
+    the float64 value itself, so there is no intermediate float32 rounding.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)                      # x = m * 2**e, 0.5 <= |m| < 1
+    r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)   # exactly representable in bf16 (normal range)
+    f32 = r.astype(np.float32)              # exact
+    return (f32.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32).astype(np.float64)
+
+
+def quantise(x64: np.ndarray, dtype: str) -> np.ndarray:
+    """float64 -> storage array (float32 values, or uint16 bf16 bits)."""
+    if dtype == "f32":
+        return np.ascontiguousarray(x64, dtype=np.float32)
+    if dtype == "bf16":
+        return np.ascontiguousarray(round_to_bf16_bits(x64))
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def storage_to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact upcast of stored values to float64."""
+    if dtype == "f32":
+        return np.asarray(a, dtype=np.float32).astype(np.float64)
+    if dtype == "bf16":
+        return bf16_bits_to_f64(a)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+# ----------------------------------------------------------------------------
+# Windows and smoothing used to shape the synthetic data
+# ----------------------------------------------------------------------------
+
+def decay_window(grid: Tuple[int, ...], tau: float, periodic: bool) -> np.ndarray:
+    """exp(-r/tau) on the grid, r the (periodic) Euclidean index distance to 0."""
+    r2 = np.zeros(grid, dtype=np.float64)
+    for ax, n in enumerate(grid):
+        i = np.arange(n, dtype=np.float64)
+        if periodic:
+            i = np.minimum(i, n - i)
+        shp = [1] * len(grid)
+        shp[ax] = n
+        r2 = r2 + (i * i).reshape(shp)
+    return np.exp(-np.sqrt(r2) / tau)
+
+
+def _gaussian_taps(sigma: float, radius: int) -> np.ndarray:
+    t = np.arange(-radius, radius + 1, dtype=np.float64)
+    w = np.exp(-0.5 * (t / sigma) ** 2)
+    return w / w.sum()
+
+
+def _periodic_smoothing_matrix(n: int, sigma: float) -> np.ndarray:
+    """Dense circulant matrix G with (G x)[i] = sum_t w[t] x[(i + t) mod n]."""
+    radius = int(4.0 * sigma + 0.5)
+    w = _gaussian_taps(sigma, radius)
+    G = np.zeros((n, n), dtype=np.float64)
+    rows = np.arange(n)
+    for j, t in enumerate(range(-radius, radius + 1)):
+        np.add.at(G, (rows, (rows + t) % n), w[j])
+    return G
+
+
+def smooth_fields(noise: np.ndarray, sigma: float) -> np.ndarray:
+    """Periodic separable Gaussian low-pass over the last two axes, then
+    per-field standardisation to zero mean and unit population variance."""
+    *lead, H, W = noise.shape
+    GH = _periodic_smoothing_matrix(H, sigma)
+    GW = _periodic_smoothing_matrix(W, sigma)
+    flat = noise.reshape(-1, H, W)
+    out = np.empty_like(flat)
+    for i in range(flat.shape[0]):
+        f = GH @ flat[i] @ GW.T
+        f = f - f.mean()
+        out[i] = f / f.std()
+    return out.reshape(noise.shape)
+
+
+# ----------------------------------------------------------------------------
+# Generation
+# ----------------------------------------------------------------------------
+
+@dataclass
+class Inputs:
+    """Quantised inputs of one workload instance (storage arrays)."""
+    workload: Workload
+    x1: np.ndarray
+    x2: np.ndarray
+    v: np.ndarray
+    k: np.ndarray
+    D: np.ndarray
+    extra: dict = field(default_factory=dict)
+
+    def as_f64(self):
+        d = self.workload.dtype
+        return tuple(storage_to_f64(a, d) for a in (self.x1, self.x2, self.v, self.k, self.D))
+
+
+def generate(w: Workload) -> Inputs:
+    rng = np.random.default_rng(w.seed)
+    shp = w.shape
+    x1 = rng.standard_normal(shp)
+    x2 = rng.standard_normal(shp)
+    v = rng.standard_normal(shp)
+    kn = rng.standard_normal(shp)
+    D = rng.standard_normal((w.C,))
+    if w.smooth_sigma is not None:
+        x1 = smooth_fields(x1, w.smooth_sigma)
+        x2 = smooth_fields(x2, w.smooth_sigma)
+        v = smooth_fields(v, w.smooth_sigma)
+    win = decay_window(w.grid, w.tau, periodic=(w.pad_mode == CIRCULAR))
+    if w.kernel_norm:
+        L = 1
+        for g in w.grid:
+            L *= g
+        win = win / np.sqrt(L)
+    k = kn * win
+    q = lambda a: quantise(a, w.dtype)
+    return Inputs(w, q(x1), q(x2), q(v), q(k), q(D))
+
+
+def random_case(B: int, C: int, grid, pad_mode: str, dtype: str, seed: int,
+                tau: Optional[float] = None) -> Inputs:
+    """Small seeded case with the same recipe (N(0,1) data, decaying kernel)."""
+    grid = tuple(int(g) for g in grid)
+    if tau is None:
+        tau = max(1.0, max(grid) / 4.0)
+    w = Workload(f"case_{len(grid)}d_{pad_mode}_{dtype}_{seed}", B, C, grid, pad_mode,
+                 dtype, seed, tau, kernel_norm=(len(grid) == 1))
+    return generate(w)
