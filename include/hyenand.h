@@ -1,0 +1,111 @@
+/*
+ * hyenand.h -- C ABI of the MI355X (gfx950) gated N-D FFT long convolution.
+ *
+ * The operation is the long convolution at the heart of the HyenaND operator
+ * (Eq. (HyenaND), section 3.2 "The HyenaND Operator") together with its two
+ * gates and the per-channel shortcut of the gated Hyena mixer (Def. A.2
+ * "Hyena mixer" and Def. A.3 "Gated Hyena mixer" in the appendix "Gated Hyena
+ * Computes Separable Attention").  For every sample b, channel c and output
+ * index n of an L1 x ... x LN grid (N = 1, 2 or 3):
+ *
+ *     u = x1 * v                                            (inner gate)
+ *     linear:   conv[n] = sum_{m: 0 <= m_d <= n_d} k[b,c,m] u[b,c,n-m]
+ *     circular: conv[n] = sum_{m}   k[b,c,m] u[b,c,(n-m) mod L]
+ *     y[b,c,n] = x2[b,c,n] * (conv[n] + D[c] * u[b,c,n])    (shortcut, outer gate)
+ *
+ * Each sample carries its own kernel k[b, c] (section 3.2.2, "FFT path
+ * preservation": B kernels, one N-D FFT convolution per input).  "linear" is
+ * the non-circular convolution of section 3.2.1 ("Support for circular and
+ * non-circular convolutions"): zero-padding to a transform of 2 L_d per axis
+ * (at least 2L-1, as the appendix "Hardware Context and IO Profile" requires)
+ * and cropping the first L_d outputs of every axis; index 0 of k is the zero
+ * displacement.  "circular" treats the grid as a torus (transform L_d).
+ *
+ * The library computes this with fused FFT kernels on the GPU (fp32 compute);
+ * it allocates nothing on the call path and keeps no pointer after a call.
+ */
+#ifndef HYENAND_H
+#define HYENAND_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HYENAND_OK = 0,
+  HYENAND_ERR_INVALID_ARGUMENT = 1,  /* null pointer, bad enum, dims <= 0, y aliasing an input */
+  HYENAND_ERR_UNSUPPORTED = 2,       /* extent not a power of two, or beyond the implemented plans */
+  HYENAND_ERR_WORKSPACE_TOO_SMALL = 3,
+  HYENAND_ERR_HIP = 4                /* a HIP launch failed; see hyenand_last_error() */
+} hyenand_status;
+
+typedef enum { HYENAND_PAD_LINEAR = 0, HYENAND_PAD_CIRCULAR = 1 } hyenand_pad_mode;
+
+/* Storage type of x1, x2, v, k, D and y.  Compute is fp32 in both cases;
+ * bf16 values are widened on load and rounded to nearest-even on store. */
+typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
+
+/*
+ * hyenand_fftconv -- y = x2 * (k conv (x1*v) + D*(x1*v)) on the GPU.
+ *
+ * x1, x2, v, k, y : device pointers, contiguous row-major [B, C, L1, ..., LN]
+ *                   of `dtype` (fp32, or bf16 bits).  y must not overlap any
+ *                   input.
+ * D               : device pointer, [C] of `dtype`.
+ * ndim            : N in {1, 2, 3}.
+ * dims            : host pointer to ndim + 2 int64 values {B, C, L1, ..., LN},
+ *                   all >= 1; every L_d must be a power of two.  Supported
+ *                   transform extents: 1D up to 2^24 points, 2D/3D up to 4096
+ *                   per axis.
+ * pad_mode        : hyenand_pad_mode.
+ * dtype           : hyenand_dtype.
+ * workspace       : device scratch of workspace_bytes, owned by the caller; may
+ *                   be NULL when hyenand_fftconv_workspace_size() reports 0.
+ *                   A workspace smaller than the reported size but at least
+ *                   the minimum one is accepted (the work is then split into
+ *                   more passes).
+ * stream          : hipStream_t to enqueue on (NULL = default stream).
+ *
+ * Validation is synchronous and launches nothing on error.  On HYENAND_OK the
+ * work has been enqueued on `stream` and the call returns without waiting;
+ * every buffer must stay alive until the stream reaches that point.  Calls on
+ * distinct streams from distinct host threads are safe; two in-flight calls
+ * must not share a workspace.  Results are deterministic (no atomics).
+ */
+hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k,
+                               const void* D, void* y, int ndim, const int64_t* dims,
+                               int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                               void* stream);
+
+/* Recommended workspace size (bytes) for a call with these arguments; 0 for
+ * plans that keep everything on chip.  Pure host function. */
+hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, int pad_mode,
+                                              int dtype, size_t* bytes_out);
+
+/* Smallest workspace (bytes) hyenand_fftconv accepts for these arguments. */
+hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int pad_mode,
+                                             int dtype, size_t* bytes_out);
+
+/* Name of the plan the call would use ("fused1d", "fused2d", "multipass2d",
+ * "multipass3d", "fourstep1d"), written NUL-terminated into buf (at most n
+ * bytes).  Pure host function. */
+hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                         char* buf, size_t n);
+
+/* Static text for a status code. */
+const char* hyenand_status_string(int status);
+
+/* Detail of the last non-OK return on the calling host thread ("" if none). */
+const char* hyenand_last_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int hyenand_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HYENAND_H */

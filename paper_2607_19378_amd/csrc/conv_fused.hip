@@ -1,0 +1,386 @@
+// Single-pass kernels: the whole padded problem of one (b, c) line stays in
+// LDS, so HBM sees only the five tensors (x1, v, k read; x2 read; y written).
+//
+//  * conv1d_fused<P>: 1D line, transform length P <= 16384.
+//  * conv2d_fused<P0, P1>: 2D image whose half spectra fit in LDS.
+//
+// Real-to-complex transforms: a real line of length P is read as the complex
+// line of its even/odd sample pairs (length P/2), transformed, and untangled
+// with the mirror bin (r2c_pair).  u = x1 v and k are transformed separately,
+// so each spectrum keeps its own relative accuracy.  The product
+// U (K + D) is Hermitian; the inverse runs on the half spectrum: in 1D as a
+// length-P/2 complex transform of the even/odd packed output (c2r_pair), in
+// 2D as column transforms of the P1/2+1 half-spectrum columns followed by row
+// transforms that carry two real output rows each (row a in the real part,
+// row b in the imaginary part).  Zero padding is never stored: inputs beyond L
+// are compile-time zeros of the first pass, and outputs beyond the crop are
+// never written.
+#include "kernels.hpp"
+
+namespace hyenand {
+
+// ---------------------------------------------------------------------------
+// 1D
+// ---------------------------------------------------------------------------
+constexpr int fused1d_nt(int P) {
+  return imax(64, imax(2 * ((P / 2) / imin(16, P / 2)), (P / 2) / imin(8, P / 2)));
+}
+
+template <int P, bool CIRC, typename TS>
+struct Fused1D {
+  static constexpr int L = CIRC ? P : P / 2;
+  static constexpr int M = P / 2;          // complex length of the packed real line
+  static constexpr int MNZ = (L + 1) / 2;  // nonzero packed samples
+  static constexpr int EF = imin(16, M);   // forward: two lines (u, k)
+  static constexpr int TF = M / EF;
+  static constexpr int EI = imin(8, M);    // inverse: one line
+  static constexpr int TI = M / EI;
+  static constexpr int NT = fused1d_nt(P);
+  static_assert(NT >= 2 * TF && NT >= TI, "threads");
+  static constexpr int LDSN = pad16_size(M);
+};
+
+template <int P, bool CIRC, typename TS>
+__global__ void __launch_bounds__(fused1d_nt(P))
+    conv1d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
+                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C) {
+  using F = Fused1D<P, CIRC, TS>;
+  constexpr int L = F::L, M = F::M, MNZ = F::MNZ, NT = F::NT;
+  __shared__ float2 Ub[F::LDSN];
+  __shared__ float2 Kb[F::LDSN];
+  const int line = blockIdx.x;
+  const int c = line % C;
+  const size_t base = (size_t)line * L;
+  const int tid = threadIdx.x;
+
+  // stage the even/odd packed real lines u = x1 v and k
+  for (int m = tid; m < MNZ; m += NT) {
+    const int n = 2 * m;
+    const bool two = n + 1 < L;
+    const float u0 = ld1(x1 + base + n) * ld1(v + base + n);
+    const float u1 = two ? ld1(x1 + base + n + 1) * ld1(v + base + n + 1) : 0.f;
+    Ub[m + (m >> 4)] = make_float2(u0, u1);
+    Kb[m + (m >> 4)] = make_float2(ld1(k + base + n), two ? ld1(k + base + n + 1) : 0.f);
+  }
+  __syncthreads();
+
+  // forward half-length transforms of both packed lines
+  {
+    constexpr int E = F::EF, T = F::TF;
+    const int which = tid / T, t = tid % T;
+    const bool act = which < 2;
+    float2* buf = which == 0 ? Ub : Kb;
+    const ScrPad16 scr{buf};
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int m = t + T * e;
+      w[e] = (act && m < MNZ) ? *scr(m) : czero();
+    }
+    BlockFFT<M, E, false>::run(w, t, scr, act);
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) *scr(t + T * e) = w[e];
+    }
+  }
+  __syncthreads();
+
+  // untangle both spectra, gated product with the folded shortcut, and pack
+  // the Hermitian product for a half-length inverse:
+  //   bin g needs U, K at g and M-g, which come from packed bins g and M-g.
+  {
+    constexpr int E = F::EI, T = F::TI;
+    const float twoD = 2.f * ld1(Dp + c);
+    const float scale = 1.f / (4.f * (float)P);
+    const ScrPad16 su{Ub}, sk{Kb};
+    const int t = tid;
+    const bool act = t < T;
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int g = t + T * e;
+      w[e] = czero();
+      if (act) {
+        const int gm = (M - g) & (M - 1);
+        const float2 tw = twiddle<ilog2(P), false>(g);
+        float2 Ug, Umg, Kg, Kmg;
+        r2c_pair(*su(g), *su(gm), tw, Ug, Umg);
+        r2c_pair(*sk(g), *sk(gm), tw, Kg, Kmg);
+        const float2 Yg = gated_product(Ug, Kg, twoD);
+        const float2 Ymg = gated_product(Umg, Kmg, twoD);
+        w[e] = c_scale(c2r_pair(Yg, Ymg, tw), scale);
+      }
+    }
+    if constexpr (T == 1) __syncthreads();
+    BlockFFT<M, E, true>::run(w, t, su, act);
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int n = 2 * (t + T * e);
+        if (n < L) st1(y + base + n, ld1(x2 + base + n) * w[e].x);
+        if (n + 1 < L) st1(y + base + n + 1, ld1(x2 + base + n + 1) * w[e].y);
+      }
+    }
+  }
+}
+
+template <int P, bool CIRC, typename TS>
+static hipError_t launch_1d_fused_t(const FftConvArgs& a, hipStream_t s) {
+  using F = Fused1D<P, CIRC, TS>;
+  hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
+                     (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
+                     (const TS*)a.D, (TS*)a.y, (int)a.C);
+  return hipGetLastError();
+}
+
+template <int P>
+static hipError_t launch_1d_fused_p(const FftConvArgs& a, hipStream_t s) {
+  if (a.circular) {
+    return a.bf16 ? launch_1d_fused_t<P, true, uint16_t>(a, s) : launch_1d_fused_t<P, true, float>(a, s);
+  }
+  return a.bf16 ? launch_1d_fused_t<P, false, uint16_t>(a, s) : launch_1d_fused_t<P, false, float>(a, s);
+}
+
+bool fused1d_supported(int64_t P) { return P >= 2 && P <= 16384 && (P & (P - 1)) == 0; }
+
+hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s) {
+  switch (a.P[0]) {
+    case 2: return launch_1d_fused_p<2>(a, s);
+    case 4: return launch_1d_fused_p<4>(a, s);
+    case 8: return launch_1d_fused_p<8>(a, s);
+    case 16: return launch_1d_fused_p<16>(a, s);
+    case 32: return launch_1d_fused_p<32>(a, s);
+    case 64: return launch_1d_fused_p<64>(a, s);
+    case 128: return launch_1d_fused_p<128>(a, s);
+    case 256: return launch_1d_fused_p<256>(a, s);
+    case 512: return launch_1d_fused_p<512>(a, s);
+    case 1024: return launch_1d_fused_p<1024>(a, s);
+    case 2048: return launch_1d_fused_p<2048>(a, s);
+    case 4096: return launch_1d_fused_p<4096>(a, s);
+    case 8192: return launch_1d_fused_p<8192>(a, s);
+    case 16384: return launch_1d_fused_p<16384>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2D
+// ---------------------------------------------------------------------------
+template <int P0, int P1, bool CIRC, typename TS>
+struct Fused2D {
+  static constexpr int L0 = CIRC ? P0 : P0 / 2;
+  static constexpr int L1 = CIRC ? P1 : P1 / 2;
+  static constexpr int M1 = P1 / 2;          // packed complex row length
+  static constexpr int MNZ = (L1 + 1) / 2;   // nonzero packed samples per row
+  static constexpr int RP = M1 + 1;          // LDS row pitch (half spectrum + Nyquist)
+  static constexpr int NT = 1024;
+  // forward row transforms: 2 L0 lines (u rows, k rows) of M1 points
+  static constexpr int ER = imin(8, M1);
+  static constexpr int TR = M1 / ER;
+  static constexpr int LR = NT / TR;         // lines per round
+  // column transforms (length P0) of the M1 + 1 half-spectrum columns
+  static constexpr int EC = imin(16, P0);
+  static constexpr int TC = P0 / EC;
+  static constexpr int CR = NT / TC;         // columns per round
+  // inverse row transforms carrying two rows each
+  static constexpr int EI = imin(8, P1);
+  static constexpr int TI = P1 / EI;
+  static constexpr int PR = NT / TI;         // row pairs per round
+  // real-to-complex untangling items: rows x (M1/2 + 1)
+  static constexpr int NPOST = 2 * L0 * (M1 / 2 + 1);
+  static constexpr int IPT = (NPOST + NT - 1) / NT;
+  static_assert(2 * RP >= P1, "two-row scratch");
+};
+
+template <int P0, int P1, bool CIRC, typename TS>
+__global__ void __launch_bounds__(1024)
+    conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
+                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C) {
+  using F = Fused2D<P0, P1, CIRC, TS>;
+  constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
+  __shared__ float2 Uh[P0 * RP];
+  __shared__ float2 Kh[P0 * RP];
+  const int img = blockIdx.x;
+  const int c = img % C;
+  const size_t base = (size_t)img * L0 * L1;
+  const int tid = threadIdx.x;
+
+  // 0. stage the real rows of u = x1 v and k (coalesced along rows); row r of
+  //    Uh read as floats is u[r][0..P1), i.e. the even/odd packed line.
+  {
+    float* uf = reinterpret_cast<float*>(Uh);
+    float* kf = reinterpret_cast<float*>(Kh);
+    for (int i = tid; i < L0 * L1; i += NT) {
+      const int r = i / L1, col = i - r * L1;
+      uf[r * 2 * RP + col] = ld1(x1 + base + i) * ld1(v + base + i);
+      kf[r * 2 * RP + col] = ld1(k + base + i);
+    }
+    if constexpr (L1 % 2 == 1) {  // odd row length: zero the unpaired odd sample
+      for (int r = tid; r < L0; r += NT) {
+        uf[r * 2 * RP + L1] = 0.f;
+        kf[r * 2 * RP + L1] = 0.f;
+      }
+    }
+  }
+  __syncthreads();
+
+  // 1. forward row transforms (lanes run across rows), then untangle each row
+  {
+    constexpr int E = F::ER, T = F::TR, LR = F::LR;
+    for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
+      const int l = l0 + tid % LR, t = tid / LR;
+      const bool act = l < 2 * L0;
+      float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+      float2 w[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int m = t + T * e;
+        w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
+      }
+      BlockFFT<M1, E, false>::run(w, t, ScrStrided{row, 1}, act);
+      if (act) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
+      }
+    }
+    __syncthreads();
+    float2 xa[F::IPT], xb[F::IPT];
+#pragma unroll
+    for (int j = 0; j < F::IPT; ++j) {
+      const int it = tid + NT * j;
+      if (it < F::NPOST) {
+        const int l = it % (2 * L0), g = it / (2 * L0);
+        const float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+        r2c_pair(row[g], row[(M1 - g) & (M1 - 1)], twiddle<ilog2(P1), false>(g), xa[j], xb[j]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < F::IPT; ++j) {
+      const int it = tid + NT * j;
+      if (it < F::NPOST) {
+        const int l = it % (2 * L0), g = it / (2 * L0);
+        float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+        row[g] = xa[j];
+        row[M1 - g] = xb[j];  // g = 0 writes the Nyquist bin M1
+      }
+    }
+  }
+  __syncthreads();
+
+  // 2. columns 0..M1 of both half spectra: forward transforms, gated product
+  //    with the folded shortcut, inverse transform; keep rows < L0.
+  {
+    constexpr int E = F::EC, T = F::TC, CR = F::CR;
+    constexpr int NC = M1 + 1;
+    const float twoD = 2.f * ld1(Dp + c);
+    const float scale = 1.f / (4.f * (float)P0 * (float)P1);
+    for (int c0 = 0; c0 < NC; c0 += CR) {
+      const int col = c0 + tid % CR, t = tid / CR;
+      const bool act = col < NC;
+      float2 wu[E], wk[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int n = t + T * e;
+        const bool nz = act && (CIRC || n < L0);
+        wu[e] = nz ? Uh[n * RP + col] : czero();
+        wk[e] = nz ? Kh[n * RP + col] : czero();
+      }
+      BlockFFT<P0, E, false>::run(wu, t, ScrStrided{Uh + col, RP}, act);
+      BlockFFT<P0, E, false>::run(wk, t, ScrStrided{Kh + col, RP}, act);
+#pragma unroll
+      for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
+      BlockFFT<P0, E, true>::run(wu, t, ScrStrided{Uh + col, RP}, act);
+      if (act) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int n = t + T * e;
+          if (CIRC || n < L0) Uh[n * RP + col] = wu[e];
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // 3. inverse row transforms, two real rows per complex transform; the
+  //    scratch of pair (ra, ra+1) is the 2 RP >= P1 entries of those rows.
+  {
+    constexpr int E = F::EI, T = F::TI, PR = F::PR;
+    constexpr int NPAIR = L0 / 2;
+    for (int q0 = 0; q0 < NPAIR; q0 += PR) {
+      const int q = q0 + tid % PR, t = tid / PR;
+      const bool act = q < NPAIR;
+      float2* ra = Uh + 2 * q * RP;
+      const float2* rb = ra + RP;
+      float2 w[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int f = t + T * e;
+        float2 ya = czero(), yb = czero();
+        if (act) {
+          if (f <= M1) {
+            ya = ra[f];
+            yb = rb[f];
+          } else {
+            ya = c_conj(ra[P1 - f]);
+            yb = c_conj(rb[P1 - f]);
+          }
+        }
+        w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
+      }
+      if constexpr (T == 1) __syncthreads();
+      BlockFFT<P1, E, true>::run(w, t, ScrStrided{ra, 1}, act);
+      if (act) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int n = t + T * e;
+          if (CIRC || n < L1) ra[n] = w[e];
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // 4. outer gate and store (coalesced along rows)
+  for (int i = tid; i < L0 * L1; i += NT) {
+    const int r = i / L1, col = i - r * L1;
+    const float2 q = Uh[(r & ~1) * RP + col];
+    st1(y + base + i, ld1(x2 + base + i) * ((r & 1) ? q.y : q.x));
+  }
+}
+
+template <int P0, int P1, bool CIRC, typename TS>
+static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(1024), 0, s,
+                     (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
+                     (const TS*)a.D, (TS*)a.y, (int)a.C);
+  return hipGetLastError();
+}
+
+template <int P0, int P1>
+static hipError_t launch_2d_fused_p(const FftConvArgs& a, hipStream_t s) {
+  if (a.circular) {
+    return a.bf16 ? launch_2d_fused_t<P0, P1, true, uint16_t>(a, s) : launch_2d_fused_t<P0, P1, true, float>(a, s);
+  }
+  return a.bf16 ? launch_2d_fused_t<P0, P1, false, uint16_t>(a, s) : launch_2d_fused_t<P0, P1, false, float>(a, s);
+}
+
+// Instantiated sizes: squares 4..128 and the 2:1 shapes next to 64 and 128.
+#define HY_FUSED2D_SIZES(X) \
+  X(4, 4) X(8, 8) X(16, 16) X(32, 32) X(64, 64) X(128, 128) X(64, 128) X(128, 64) X(32, 64) X(64, 32)
+
+bool fused2d_supported(int64_t P0, int64_t P1) {
+#define HY_CASE(a, b) if (P0 == a && P1 == b) return true;
+  HY_FUSED2D_SIZES(HY_CASE)
+#undef HY_CASE
+  return false;
+}
+
+hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s) {
+#define HY_CASE(p0, p1) if (a.P[0] == p0 && a.P[1] == p1) return launch_2d_fused_p<p0, p1>(a, s);
+  HY_FUSED2D_SIZES(HY_CASE)
+#undef HY_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace hyenand

@@ -1,0 +1,255 @@
+// Device building blocks for the gated N-D FFT long convolution on gfx950.
+//
+// * complex fp32 helpers (float2 = re, im);
+// * twiddles exp(-2 pi i m / 2^s) from fp32 tables that were computed in fp64
+//   (coarse 2^12 table, and coarse x fine for s up to 24);
+// * radix-R DFTs held entirely in registers (R <= 32), natural order in and out;
+// * BlockFFT<N, E>: a length-N transform carried by T = N/E lanes that each hold
+//   E points in registers (lane t holds x[t + T e]).  Passes are Stockham
+//   autosort steps of radix min(E, remaining): each pass applies twiddles, a
+//   register DFT, and exchanges through LDS; the last pass leaves the output in
+//   registers in the same stride-T distribution, so no bit reversal is needed
+//   and a transform can feed the next step directly from registers.
+//
+// Transforms are unnormalised: forward X[f] = sum_n x[n] exp(-2 pi i f n / N),
+// inverse uses exp(+2 pi i f n / N).  The scaling by 1/prod(P) of the inverse
+// N-D transform is folded into the spectral product by the callers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hyenand {
+
+#include "twiddles.inc"
+
+constexpr int ilog2(int n) { return n <= 1 ? 0 : 1 + ilog2(n >> 1); }
+constexpr int imin(int a, int b) { return a < b ? a : b; }
+constexpr int imax(int a, int b) { return a > b ? a : b; }
+constexpr bool is_pow2(int n) { return n >= 1 && (n & (n - 1)) == 0; }
+constexpr int bitrev(int k, int nbits) {
+  int r = 0;
+  for (int i = 0; i < nbits; ++i) r |= ((k >> i) & 1) << (nbits - 1 - i);
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// complex arithmetic
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float2 c_add(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 c_sub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ float2 c_conj(float2 a) { return make_float2(a.x, -a.y); }
+__device__ __forceinline__ float2 c_scale(float2 a, float s) { return make_float2(a.x * s, a.y * s); }
+__device__ __forceinline__ float2 c_mul(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, -a.y * b.y), fmaf(a.x, b.y, a.y * b.x));
+}
+// a * conj(b)
+__device__ __forceinline__ float2 c_mulc(float2 a, float2 b) {
+  return make_float2(fmaf(a.x, b.x, a.y * b.y), fmaf(a.y, b.x, -a.x * b.y));
+}
+// quarter turn: * (-i) for the forward direction, * (+i) for the inverse
+template <bool INV>
+__device__ __forceinline__ float2 c_quarter(float2 a) {
+  return INV ? make_float2(-a.y, a.x) : make_float2(a.y, -a.x);
+}
+__device__ __forceinline__ float2 czero() { return make_float2(0.f, 0.f); }
+
+// ---------------------------------------------------------------------------
+// twiddles
+// ---------------------------------------------------------------------------
+// exp(-2 pi i m / 2^LOG) for 0 <= m < 2^LOG (conjugated when INV), LOG <= 24.
+template <int LOG, bool INV>
+__device__ __forceinline__ float2 twiddle(uint32_t m) {
+  static_assert(LOG >= 0 && LOG <= 24, "twiddle range");
+  float2 w;
+  if constexpr (LOG <= 12) {
+    w = kTwCoarse[m << (12 - LOG)];
+  } else {
+    const uint32_t b = m << (24 - LOG);
+    w = c_mul(kTwCoarse[b >> 12], kTwFine[b & 4095u]);
+  }
+  return INV ? c_conj(w) : w;
+}
+
+// Same with the size known at run time only (log2n <= 24).
+template <bool INV>
+__device__ __forceinline__ float2 twiddle_rt(uint32_t m, int log2n) {
+  float2 w;
+  if (log2n <= 12) {
+    w = kTwCoarse[m << (12 - log2n)];
+  } else {
+    const uint32_t b = m << (24 - log2n);
+    w = c_mul(kTwCoarse[b >> 12], kTwFine[b & 4095u]);
+  }
+  return INV ? c_conj(w) : w;
+}
+
+// a * exp(-+2 pi i n / R) with n a compile-time constant after unrolling.
+template <int R, bool INV>
+__device__ __forceinline__ float2 mul_root(float2 a, int n) {
+  n &= (R - 1);
+  if (n == 0) return a;
+  if (4 * n == R) return c_quarter<INV>(a);
+  if (2 * n == R) return make_float2(-a.x, -a.y);
+  if (4 * n == 3 * R) return c_quarter<!INV>(a);
+  const int j = (n * (32 / R)) & 31;
+  const float c = kCos32[j];
+  const float s = INV ? kSin32[j] : -kSin32[j];
+  return make_float2(fmaf(a.x, c, -a.y * s), fmaf(a.x, s, a.y * c));
+}
+
+// ---------------------------------------------------------------------------
+// register DFTs
+// ---------------------------------------------------------------------------
+// Radix-2 decimation in frequency over v[0], v[S], ..., v[(R-1)S]; leaves the
+// outputs in bit-reversed slot order.
+template <int R, bool INV, int S>
+struct DifStages {
+  static __device__ __forceinline__ void run(float2* v) {
+    if constexpr (R >= 2) {
+#pragma unroll
+      for (int n = 0; n < R / 2; ++n) {
+        const float2 a = v[n * S], b = v[(n + R / 2) * S];
+        v[n * S] = c_add(a, b);
+        v[(n + R / 2) * S] = mul_root<R, INV>(c_sub(a, b), n);
+      }
+      if constexpr (R > 2) {
+        DifStages<R / 2, INV, S>::run(v);
+        DifStages<R / 2, INV, S>::run(v + (R / 2) * S);
+      }
+    }
+  }
+};
+
+// In-register DFT of R points, natural order in and out.
+template <int R, bool INV>
+__device__ __forceinline__ void dft(float2 (&v)[R]) {
+  static_assert(is_pow2(R) && R <= 32, "radix");
+  if constexpr (R > 1) {
+    DifStages<R, INV, 1>::run(v);
+    float2 t[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) t[k] = v[bitrev(k, ilog2(R))];
+#pragma unroll
+    for (int k = 0; k < R; ++k) v[k] = t[k];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LDS scratch addressing for one line of a block transform
+// ---------------------------------------------------------------------------
+struct ScrStrided {  // element p at base[p * stride]
+  float2* base;
+  int stride;
+  __device__ __forceinline__ float2* operator()(int p) const { return base + p * stride; }
+};
+struct ScrPad16 {  // element p at base[p + p/16]: one pad slot per 16 entries
+  float2* base;
+  __device__ __forceinline__ float2* operator()(int p) const { return base + p + (p >> 4); }
+};
+__host__ __device__ constexpr int pad16_size(int n) { return n + (n >> 4) + 1; }
+
+// ---------------------------------------------------------------------------
+// Block transform: N points over T = N/E lanes, E points per lane.
+// All lanes of the workgroup must call run() the same number of times (it
+// contains workgroup barriers when N > E).  Inactive lanes pass active=false:
+// they take the barriers but touch no LDS.  The first exchange starts with a
+// barrier, so callers may read the scratch line right before calling run().
+// ---------------------------------------------------------------------------
+template <int N, int E, bool INV>
+struct BlockFFT {
+  static_assert(is_pow2(N) && is_pow2(E) && E <= N && E <= 32, "block fft shape");
+  static constexpr int T = N / E;
+
+  template <class Scr>
+  static __device__ __forceinline__ void run(float2 (&v)[E], int t, const Scr& scr, bool active) {
+    pass<1>(v, t, scr, active);
+  }
+
+  template <int NS, class Scr>
+  static __device__ __forceinline__ void pass(float2 (&v)[E], int t, const Scr& scr, bool active) {
+    constexpr int R = (N / NS >= E) ? E : N / NS;
+    constexpr int NB = E / R;  // butterflies per lane in this pass
+    constexpr int LOGW = ilog2(NS * R);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float2 x[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) x[r] = v[b + NB * r];
+      if constexpr (NS > 1) {
+        const uint32_t jm = (uint32_t)(t + T * b) & (NS - 1);
+#pragma unroll
+        for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], twiddle<LOGW, INV>(jm * r));
+      }
+      dft<R, INV>(x);
+#pragma unroll
+      for (int r = 0; r < R; ++r) v[b + NB * r] = x[r];
+    }
+    if constexpr (NS * R < N) {
+      __syncthreads();
+      if (active) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const int j = t + T * b;
+          const int jm = j & (NS - 1);
+          const int dst = (j - jm) * R + jm;
+#pragma unroll
+          for (int r = 0; r < R; ++r) *scr(dst + r * NS) = v[b + NB * r];
+        }
+      }
+      __syncthreads();
+      if (active) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) v[e] = *scr(t + T * e);
+      }
+      pass<NS * R>(v, t, scr, active);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// storage types: float (fp32) or uint16_t (bf16 bits); compute is fp32
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float ld1(const float* p) { return *p; }
+__device__ __forceinline__ float ld1(const uint16_t* p) { return __uint_as_float(((uint32_t)*p) << 16); }
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ void st1(float* p, float x) { *p = x; }
+__device__ __forceinline__ void st1(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
+
+// Real-to-complex post-pass.  A real line x[0..P) is read as the complex
+// line z[m] = x[2m] + i x[2m+1] of length M = P/2 and transformed; with
+// A = Z[g], B = Z[(M-g) mod M] and w = exp(-2 pi i g / P) this returns
+// Xg = 2 X[g] and Xmg = 2 X[M-g] of the length-P real transform
+// (X[f] = Xe[f] + w^f Xo[f], Xe/Xo the transforms of the even/odd samples).
+__device__ __forceinline__ void r2c_pair(float2 A, float2 B, float2 w, float2& Xg, float2& Xmg) {
+  const float2 e = make_float2(A.x + B.x, A.y - B.y);  // A + conj B      = 2 Xe[g]
+  const float2 o = make_float2(A.y + B.y, B.x - A.x);  // -i (A - conj B) = 2 Xo[g]
+  const float2 t = c_mul(w, o);
+  Xg = c_add(e, t);
+  Xmg = make_float2(e.x - t.x, t.y - e.y);  // conj(e - t)
+}
+
+// Complex-to-real pre-pass, the inverse of r2c_pair: from the Hermitian
+// spectrum values Yg = Y[g], Ymg = Y[M-g] of a real length-P signal y and
+// w = exp(-2 pi i g / P), returns  Yg + conj Ymg + i w^-1 (Yg - conj Ymg)
+// = 2 (E[g] + i O[g]), with E/O the length-M transforms of the even/odd
+// samples; the length-M inverse of these bins is 2M (y[2m] + i y[2m+1]).
+__device__ __forceinline__ float2 c2r_pair(float2 Yg, float2 Ymg, float2 w) {
+  const float2 s = make_float2(Yg.x + Ymg.x, Yg.y - Ymg.y);  // Yg + conj Ymg
+  const float2 d = make_float2(Yg.x - Ymg.x, Yg.y + Ymg.y);  // Yg - conj Ymg
+  const float2 rd = c_mulc(d, w);                            // d exp(+2 pi i g / P)
+  return make_float2(s.x - rd.y, s.y + rd.x);                // s + i rd
+}
+
+// Spectral product with the shortcut folded in: U (K + D), D times the
+// transform of a unit impulse (1 at every bin).  Inputs are 2U and 2K.
+__device__ __forceinline__ float2 gated_product(float2 U2, float2 K2, float twoD) {
+  return c_mul(U2, make_float2(K2.x + twoD, K2.y));
+}
+
+}  // namespace hyenand

@@ -1,0 +1,226 @@
+// C-ABI front end: argument validation, plan choice, workspace sizing and
+// launches.  Validation and sizing are pure host code; nothing here touches
+// the GPU before every check has passed.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/hyenand.h"
+#include "kernels.hpp"
+
+using namespace hyenand;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hyenand_status fail(hyenand_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP };
+
+const char* plan_name(Plan p, int ndim) {
+  switch (p) {
+    case PLAN_FUSED1D: return "fused1d";
+    case PLAN_FUSED2D: return "fused2d";
+    case PLAN_MULTIPASS: return ndim == 3 ? "multipass3d" : "multipass2d";
+    case PLAN_FOURSTEP: return "fourstep1d";
+    default: return "none";
+  }
+}
+
+bool pow2(int64_t n) { return n >= 1 && (n & (n - 1)) == 0; }
+
+// Shape checks shared by every entry point.  Fills a (pointers left null).
+hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtype, FftConvArgs* a) {
+  memset(a, 0, sizeof *a);
+  if (ndim < 1 || ndim > 3) return fail(HYENAND_ERR_INVALID_ARGUMENT, "ndim must be 1, 2 or 3 (got %d)", ndim);
+  if (!dims) return fail(HYENAND_ERR_INVALID_ARGUMENT, "dims is NULL");
+  if (pad_mode != HYENAND_PAD_LINEAR && pad_mode != HYENAND_PAD_CIRCULAR)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "pad_mode must be 0 (linear) or 1 (circular), got %d", pad_mode);
+  if (dtype != HYENAND_DTYPE_F32 && dtype != HYENAND_DTYPE_BF16)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "dtype must be 0 (f32) or 1 (bf16), got %d", dtype);
+  int64_t total = 1;
+  for (int i = 0; i < ndim + 2; ++i) {
+    if (dims[i] < 1) return fail(HYENAND_ERR_INVALID_ARGUMENT, "dims[%d] = %lld must be >= 1", i, (long long)dims[i]);
+    if (dims[i] > (int64_t(1) << 40) || total > (int64_t(1) << 46) / dims[i])
+      return fail(HYENAND_ERR_UNSUPPORTED, "tensor too large");
+    total *= dims[i];
+  }
+  a->lines = dims[0] * dims[1];
+  a->C = dims[1];
+  a->circular = pad_mode == HYENAND_PAD_CIRCULAR;
+  a->bf16 = dtype == HYENAND_DTYPE_BF16;
+  // squeeze unit axes: along an axis of extent 1 both modes reduce to the m = 0 term
+  int nd = 0;
+  for (int d = 0; d < ndim; ++d) {
+    const int64_t L = dims[2 + d];
+    if (!pow2(L)) return fail(HYENAND_ERR_UNSUPPORTED, "grid extent L%d = %lld is not a power of two", d + 1, (long long)L);
+    if (L > 1) a->L[nd++] = L;
+  }
+  if (nd == 0) {  // a single point: the linear transform of length 2 covers it
+    nd = 1;
+    a->L[0] = 1;
+    a->circular = false;
+  }
+  a->ndim = nd;
+  for (int d = 0; d < nd; ++d) a->P[d] = a->circular ? a->L[d] : 2 * a->L[d];
+  return HYENAND_OK;
+}
+
+Plan choose_plan(const FftConvArgs& a) {
+  const char* force = getenv("HYENAND_PLAN");
+  const bool no_fused = force && (strcmp(force, "multipass") == 0 || strcmp(force, "fourstep") == 0);
+  if (a.ndim == 1) {
+    if (!no_fused && fused1d_supported(a.P[0])) return PLAN_FUSED1D;
+    if (fourstep_supported(a)) return PLAN_FOURSTEP;
+    return PLAN_NONE;
+  }
+  if (a.ndim == 2 && !no_fused && fused2d_supported(a.P[0], a.P[1])) return PLAN_FUSED2D;
+  if (multipass_supported(a)) return PLAN_MULTIPASS;
+  return PLAN_NONE;
+}
+
+size_t bytes_per_line(const FftConvArgs& a, Plan p) {
+  if (p == PLAN_MULTIPASS) return multipass_bytes_per_line(a);
+  if (p == PLAN_FOURSTEP) return fourstep_bytes_per_line(a);
+  return 0;
+}
+
+// Recommended workspace: enough lines per chunk to keep the grid busy while
+// the chunk's spectra stay within a cache-sized budget (default 192 MiB,
+// below the 256 MiB Infinity Cache; HYENAND_WS_TARGET_MB overrides).
+size_t recommended_ws(const FftConvArgs& a, Plan p) {
+  const size_t per = bytes_per_line(a, p);
+  if (per == 0) return 0;
+  size_t target = (size_t)192 << 20;
+  if (const char* e = getenv("HYENAND_WS_TARGET_MB")) {
+    long mb = strtol(e, nullptr, 10);
+    if (mb > 0) target = (size_t)mb << 20;
+  }
+  int64_t chunk = (int64_t)(target / per);
+  if (chunk < 1) chunk = 1;
+  if (chunk > a.lines) chunk = a.lines;
+  return (size_t)chunk * per;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+}  // namespace
+
+extern "C" {
+
+hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                              size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  *bytes_out = recommended_ws(a, p);
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                             size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  *bytes_out = bytes_per_line(a, p);
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_mode, int dtype, char* buf,
+                                         size_t n) {
+  if (!buf || n == 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "buf is NULL or empty");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  snprintf(buf, n, "%s", plan_name(p, a.ndim));
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k, const void* D,
+                               void* y, int ndim, const int64_t* dims, int pad_mode, int dtype,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  if (!x1 || !x2 || !v || !k || !D || !y)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "a tensor pointer is NULL");
+  const size_t es = a.bf16 ? 2 : 4;
+  size_t n = (size_t)a.lines;
+  for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];
+  const size_t nb = n * es;
+  const void* ins[4] = {x1, x2, v, k};
+  const char* names[4] = {"x1", "x2", "v", "k"};
+  for (int i = 0; i < 4; ++i)
+    if (overlaps(y, nb, ins[i], nb)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", names[i]);
+  if (overlaps(y, nb, D, (size_t)a.C * es)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps D");
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  const size_t per = bytes_per_line(a, p);
+  int64_t chunk = 0;
+  if (per > 0) {
+    if (!workspace || workspace_bytes < per)
+      return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "plan %s needs at least %zu workspace bytes, got %zu",
+                  plan_name(p, a.ndim), per, workspace ? workspace_bytes : (size_t)0);
+    if (overlaps(workspace, workspace_bytes, y, nb)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps y");
+    for (int i = 0; i < 4; ++i)
+      if (overlaps(workspace, workspace_bytes, ins[i], nb))
+        return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", names[i]);
+    chunk = (int64_t)(workspace_bytes / per);
+    if (chunk > a.lines) chunk = a.lines;
+  }
+  a.x1 = x1; a.x2 = x2; a.v = v; a.k = k; a.D = D; a.y = y;
+  a.ws = workspace;
+  a.ws_bytes = workspace_bytes;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t err = hipSuccess;
+  switch (p) {
+    case PLAN_FUSED1D: err = launch_fused1d(a, s); break;
+    case PLAN_FUSED2D: err = launch_fused2d(a, s); break;
+    case PLAN_MULTIPASS: err = launch_multipass(a, chunk, s); break;
+    case PLAN_FOURSTEP: err = launch_fourstep(a, chunk, s); break;
+    default: return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  }
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
+}
+
+const char* hyenand_status_string(int status) {
+  switch (status) {
+    case HYENAND_OK: return "ok";
+    case HYENAND_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case HYENAND_ERR_UNSUPPORTED: return "unsupported shape";
+    case HYENAND_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case HYENAND_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* hyenand_last_error(void) { return g_last_error.c_str(); }
+
+int hyenand_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,43 @@
+// Internal interface between the C-ABI front end (hyenand.cpp) and the
+// kernel translation units.  Not part of the public header.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "fft_device.hpp"
+
+namespace hyenand {
+
+// One validated call, after unit axes have been squeezed out.
+struct FftConvArgs {
+  const void *x1, *x2, *v, *k, *D;
+  void* y;
+  int64_t lines;  // B * C
+  int64_t C;
+  int ndim;       // 1..3, every remaining axis has L >= 2 (or the 1D L = 1 case)
+  int64_t L[3];   // grid extents of the squeezed problem
+  int64_t P[3];   // transform extents: 2L (linear) or L (circular)
+  bool circular;
+  bool bf16;
+  void* ws;       // device workspace (multi-pass plans)
+  size_t ws_bytes;
+};
+
+// single pass (the padded problem of one line fits in LDS)
+bool fused1d_supported(int64_t P);
+hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s);
+bool fused2d_supported(int64_t P0, int64_t P1);
+hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s);
+
+// multi-pass 2D/3D (lines along each axis; spectra staged in the workspace)
+bool multipass_supported(const FftConvArgs& a);
+size_t multipass_bytes_per_line(const FftConvArgs& a);
+hipError_t launch_multipass(const FftConvArgs& a, int64_t chunk_lines, hipStream_t s);
+
+// multi-pass 1D (four-step split of the long line)
+bool fourstep_supported(const FftConvArgs& a);
+size_t fourstep_bytes_per_line(const FftConvArgs& a);
+hipError_t launch_fourstep(const FftConvArgs& a, int64_t chunk_lines, hipStream_t s);
+
+}  // namespace hyenand

@@ -1,0 +1,161 @@
+"""Python binding of libhyenand (ctypes): argument marshalling only.
+
+Every step of the operation runs in the HIP kernels behind the C ABI declared
+in include/hyenand.h; PyTorch only provides device memory and the stream.
+There is no fallback: if the library is missing or cannot be loaded, every
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional, Sequence
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhyenand.so")
+
+OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = range(5)
+PAD_LINEAR, PAD_CIRCULAR = 0, 1
+DTYPE_F32, DTYPE_BF16 = 0, 1
+
+EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min",
+            "hyenand_fftconv_plan_name", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
+
+_lock = threading.Lock()
+_lib = None
+
+
+class HyenandError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhyenand.so (built in-tree by paper_2607_19378_amd.build)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2607_19378_amd.build`")
+            L = ctypes.CDLL(LIB_PATH)
+            i64p = ctypes.POINTER(ctypes.c_int64)
+            vp = ctypes.c_void_p
+            L.hyenand_fftconv.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
+                                          ctypes.c_int, vp, ctypes.c_size_t, vp]
+            L.hyenand_fftconv.restype = ctypes.c_int
+            for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min"):
+                f = getattr(L, name)
+                f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
+                              ctypes.POINTER(ctypes.c_size_t)]
+                f.restype = ctypes.c_int
+            L.hyenand_fftconv_plan_name.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
+                                                    ctypes.c_char_p, ctypes.c_size_t]
+            L.hyenand_fftconv_plan_name.restype = ctypes.c_int
+            L.hyenand_status_string.argtypes = [ctypes.c_int]
+            L.hyenand_status_string.restype = ctypes.c_char_p
+            L.hyenand_last_error.argtypes = []
+            L.hyenand_last_error.restype = ctypes.c_char_p
+            L.hyenand_version.argtypes = []
+            L.hyenand_version.restype = ctypes.c_int
+            _lib = L
+        return _lib
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        L = lib()
+        detail = L.hyenand_last_error().decode()
+        raise HyenandError(status, f"{L.hyenand_status_string(status).decode()}: {detail}")
+
+
+def _dims(shape: Sequence[int]):
+    arr = (ctypes.c_int64 * len(shape))(*[int(s) for s in shape])
+    return len(shape) - 2, arr
+
+
+def _mode(pad_mode: str) -> int:
+    if pad_mode == "linear":
+        return PAD_LINEAR
+    if pad_mode == "circular":
+        return PAD_CIRCULAR
+    raise ValueError(f"pad_mode must be 'linear' or 'circular', got {pad_mode!r}")
+
+
+def _dtype_code(dtype) -> int:
+    import torch
+    if dtype in (torch.float32, "f32", "float32"):
+        return DTYPE_F32
+    if dtype in (torch.bfloat16, "bf16", "bfloat16"):
+        return DTYPE_BF16
+    raise ValueError(f"unsupported dtype {dtype}")
+
+
+def workspace_size(shape, pad_mode: str, dtype) -> int:
+    nd, dims = _dims(shape)
+    out = ctypes.c_size_t(0)
+    _check(lib().hyenand_fftconv_workspace_size(nd, dims, _mode(pad_mode), _dtype_code(dtype),
+                                                ctypes.byref(out)))
+    return int(out.value)
+
+
+def workspace_min(shape, pad_mode: str, dtype) -> int:
+    nd, dims = _dims(shape)
+    out = ctypes.c_size_t(0)
+    _check(lib().hyenand_fftconv_workspace_min(nd, dims, _mode(pad_mode), _dtype_code(dtype),
+                                               ctypes.byref(out)))
+    return int(out.value)
+
+
+def plan_name(shape, pad_mode: str, dtype) -> str:
+    nd, dims = _dims(shape)
+    buf = ctypes.create_string_buffer(64)
+    _check(lib().hyenand_fftconv_plan_name(nd, dims, _mode(pad_mode), _dtype_code(dtype), buf, 64))
+    return buf.value.decode()
+
+
+def version() -> int:
+    return int(lib().hyenand_version())
+
+
+def _ptr(t) -> int:
+    return int(t.data_ptr())
+
+
+def fftconv_into(y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None,
+                 stream=None) -> None:
+    """y <- x2 * (k conv (x1*v) + D*(x1*v)); all tensors already allocated on the GPU."""
+    import torch
+    ts = (x1, x2, v, k, y)
+    shape = tuple(x1.shape)
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("all tensors must be on the GPU")
+        if tuple(t.shape) != shape or t.dtype != x1.dtype:
+            raise ValueError("x1, x2, v, k, y must share shape and dtype")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous")
+    if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():
+        raise ValueError("D must be a contiguous [C] GPU tensor of the same dtype")
+    nd, dims = _dims(shape)
+    if stream is None:
+        stream = torch.cuda.current_stream(x1.device)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+    _check(lib().hyenand_fftconv(_ptr(x1), _ptr(x2), _ptr(v), _ptr(k), _ptr(D), _ptr(y), nd, dims,
+                                 _mode(pad_mode), _dtype_code(x1.dtype), ws_ptr, ws_bytes,
+                                 ctypes.c_void_p(stream.cuda_stream)))
+
+
+def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None):
+    """Allocate y (and, unless given, the workspace) with torch and run the op."""
+    import torch
+    y = torch.empty_like(x1)
+    if workspace is None:
+        nbytes = workspace_size(tuple(x1.shape), pad_mode, x1.dtype)
+        if nbytes:
+            workspace = torch.empty(nbytes, dtype=torch.uint8, device=x1.device)
+    fftconv_into(y, x1, x2, v, k, D, pad_mode, workspace, stream)
+    return y

@@ -1,0 +1,64 @@
+"""Helpers shared by the GPU parity tests: move seeded storage arrays to the
+GPU, run the HIP path through the C ABI, and compare with the fp64 oracle."""
+import sys
+
+import numpy as np
+
+from paper_2607_19378_amd import workloads as W
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}  # relative L2, fp32 compute in both cases
+
+
+def log(msg):
+    sys.stdout.write(msg + "\n")
+    sys.stdout.flush()
+
+
+def to_device(arr, dtype):
+    import torch
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).cuda()
+    t = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.uint16).view(np.int16)).cuda()
+    return t.view(torch.bfloat16)
+
+
+def from_device(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        bits = t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return W.bf16_bits_to_f64(bits)
+    return t.cpu().numpy().astype(np.float64)
+
+
+def run_gpu(inp, workspace_bytes=None, stream=None):
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    w = inp.workload
+    dev = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+    ws = None
+    if workspace_bytes is not None:
+        ws = torch.empty(max(1, workspace_bytes), dtype=torch.uint8, device="cuda")
+    y = H.fftconv(*dev, pad_mode=w.pad_mode, workspace=ws, stream=stream)
+    torch.cuda.synchronize()
+    return from_device(y)
+
+
+def oracle_ref(inp, lines=None, method="fft"):
+    import oracle
+    x1, x2, v, k, D = inp.as_f64()
+    fn = oracle.conv_fft if method == "fft" else oracle.conv_direct
+    return fn(x1, x2, v, k, D, inp.workload.pad_mode, lines=lines)
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, dtype=np.float64).ravel()
+    b = np.asarray(b, dtype=np.float64).ravel()
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def per_line_worst(a, b, nlines):
+    a = np.asarray(a, dtype=np.float64).reshape(nlines, -1)
+    b = np.asarray(b, dtype=np.float64).reshape(nlines, -1)
+    num = np.linalg.norm(a - b, axis=1)
+    den = np.maximum(np.linalg.norm(b, axis=1), 1e-300)
+    return float(np.max(num / den))
