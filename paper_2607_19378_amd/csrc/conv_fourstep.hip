@@ -1,0 +1,358 @@
+// Multi-pass 1D plan for lines longer than the single-pass limit.
+//
+// The real line of transform length P is read as its even/odd packed complex
+// line z[m] = x[2m] + i x[2m+1] of length M = P/2, and the length-M transform
+// is split four-step style as M = N1 x N2 with m = m1 N2 + m2 and
+// f = f1 + N1 f2 (the paper's three-kernel Cooley-Tukey treatment of long
+// lines, appendix "1D FFT Convolution"):
+//
+//   cols_fwd  per column m2: transform over m1 (length N1; zero half skipped
+//             in linear mode) for u = x1 v and for k, twiddle
+//             exp(-2 pi i m2 f1 / M); store A[f1][m2] (both signals).
+//   core      per row pair (f1, N1 - f1): transforms over m2 (length N2) give
+//             the packed spectra of u and k; bins g and M - g sit in this row
+//             pair, so the real spectra are untangled (r2c_pair), multiplied
+//             (gated product, shortcut folded in), and packed again for a
+//             half-length inverse (c2r_pair); inverse transforms over f2,
+//             twiddle exp(+2 pi i f1 m2 / M); store in place of A_u.
+//   cols_inv  per column m2: inverse transform over f1 (length N1), keep the
+//             cropped m1 < N1/2, unpack y[2m], y[2m+1], outer gate, store.
+//
+// Inputs are read once, y written once; the two complex spectra (16 B per
+// packed sample) round-trip through the workspace, chunked by lines.
+#include "kernels.hpp"
+
+namespace hyenand {
+
+namespace {
+
+constexpr int kN2 = 2048;
+constexpr int kMinN1 = 8;
+constexpr int kMaxN1 = 1024;
+
+// column tiles: NS signals of TL adjacent columns, N1 points each
+template <int N1, int NS>
+struct ColCfg {
+  static constexpr int E = imin(16, N1);
+  static constexpr int T = N1 / E;
+  static constexpr int NT = 1024;
+  static constexpr int TL0 = imin(32, imax(2, NT / (NS * T)));
+  static constexpr int TL = (NS * N1 * (TL0 + 1) * 8 <= 150 * 1024) ? TL0 : imax(1, TL0 / 2);
+  static constexpr int TLP = TL + 1;
+};
+
+template <int N1, bool CIRC, typename TS>
+__global__ void __launch_bounds__(1024)
+    fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
+                float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line) {
+  using Cf = ColCfg<N1, 2>;
+  constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
+  constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
+  __shared__ float2 tile[2][N1 * TLP];
+  const int ntile = N2 / TL;
+  const int64_t line = blockIdx.x / ntile;
+  const int c0 = (int)(blockIdx.x % ntile) * TL;
+  const int64_t M = (int64_t)N1 * N2;
+  const int64_t L = CIRC ? 2 * M : M;  // real samples per line
+  const size_t gbase = (size_t)(line0 + line) * L;
+  const int tid = threadIdx.x;
+
+  for (int i = tid; i < NZ * TL; i += NT) {
+    const int m1 = i / TL, cc = i - m1 * TL;
+    const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
+    const float2 a = ld2(x1 + n), b = ld2(v + n);
+    tile[0][m1 * TLP + cc] = make_float2(a.x * b.x, a.y * b.y);
+    tile[1][m1 * TLP + cc] = ld2(k + n);
+  }
+  __syncthreads();
+
+  constexpr int NL = 2 * TL;
+  for (int l0 = 0; l0 < NL; l0 += NT / T) {
+    const int l = l0 + tid % (NT / T), t = tid / (NT / T);
+    const bool act = l < NL;
+    const int s = (l / TL) & 1, cc = l % TL;
+    float2* col = tile[s] + cc;
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int m1 = t + T * e;
+      w[e] = (act && (CIRC || m1 < NZ)) ? col[m1 * TLP] : czero();
+    }
+    BlockFFT<N1, E, false>::run(w, t, ScrStrided{col, TLP}, act);
+    if (act) {
+      const uint32_t m2 = (uint32_t)(c0 + cc);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t f1 = (uint32_t)(t + T * e);
+        col[f1 * TLP] = c_mul(w[e], twiddle_rt<false>(m2 * f1, log2M));
+      }
+    }
+  }
+  __syncthreads();
+
+  float2* A = ws + line * per_line;
+  for (int i = tid; i < N1 * TL; i += NT) {
+    const int f1 = i / TL, cc = i - f1 * TL;
+    const size_t off = (size_t)f1 * N2 + c0 + cc;
+    A[off] = tile[0][f1 * TLP + cc];
+    A[M + off] = tile[1][f1 * TLP + cc];
+  }
+}
+
+template <bool CIRC>
+__global__ void __launch_bounds__(512)
+    fs_core(float2* __restrict__ ws, const void* __restrict__ Dp, int dbf16, int64_t line0, int C, int N1,
+            int log2M, int64_t per_line, float scale) {
+  constexpr int N2 = kN2;
+  constexpr int E = 16, T = N2 / E, NT = 512;
+  constexpr int RS = pad16_size(N2);
+  constexpr int IPT = N2 / NT;
+  __shared__ float2 R[4][RS];  // u row a, u row b, k row a, k row b
+  const int npair = N1 / 2 + 1;
+  const int64_t line = blockIdx.x / npair;
+  const int fa = (int)(blockIdx.x % npair);
+  const int fb = (N1 - fa) & (N1 - 1);
+  const bool single = fa == fb;  // rows 0 and N1/2 are their own mirrors
+  const int64_t M = (int64_t)N1 * N2;
+  const int c = (int)((line0 + line) % C);
+  const float twoD = 2.f * (dbf16 ? ld1((const uint16_t*)Dp + c) : ld1((const float*)Dp + c));
+  float2* A = ws + line * per_line;
+  const int tid = threadIdx.x;
+  // slots: 0 = u row fa, 1 = u row fb, 2 = k row fa, 3 = k row fb (a single
+  // self-mirrored row uses slots 0 and 2 only)
+  for (int i = tid; i < 4 * N2; i += NT) {
+    const int sl = i / N2, f2 = i - sl * N2;
+    if (!single || (sl & 1) == 0) {
+      const ScrPad16 sc{R[sl]};
+      const int64_t row = (sl & 1) ? fb : fa;
+      *sc(f2) = A[((sl >> 1) ? M : 0) + row * N2 + f2];
+    }
+  }
+  __syncthreads();
+
+  // forward transforms over m2 (lanes run along each row)
+  {
+    const int sl = tid / T, t = tid % T;
+    const bool act = sl < 4 && (!single || (sl & 1) == 0);
+    const ScrPad16 sc{R[sl & 3]};
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) w[e] = act ? *sc(t + T * e) : czero();
+    BlockFFT<N2, E, false>::run(w, t, sc, act);
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) *sc(t + T * e) = w[e];
+    }
+  }
+  __syncthreads();
+
+  // untangle, gated product, pack for the half-length inverse
+  const ScrPad16 ua{R[0]}, ub{R[single ? 0 : 1]}, ka{R[2]}, kb{R[single ? 2 : 3]};
+  float2 wg[IPT], wm[IPT];
+  int mcol[IPT];
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int f2 = tid + NT * j;
+    const int mc = fa == 0 ? ((N2 - f2) & (N2 - 1)) : (N2 - 1 - f2);
+    mcol[j] = mc;
+    const uint32_t g = (uint32_t)fa + (uint32_t)N1 * (uint32_t)f2;
+    const float2 om = twiddle_rt<false>(g, log2M + 1);  // exp(-2 pi i g / P)
+    float2 Ug, Umg, Kg, Kmg;
+    r2c_pair(*ua(f2), *ub(mc), om, Ug, Umg);
+    r2c_pair(*ka(f2), *kb(mc), om, Kg, Kmg);
+    const float2 Yg = gated_product(Ug, Kg, twoD);
+    const float2 Ymg = gated_product(Umg, Kmg, twoD);
+    wg[j] = c_scale(c2r_pair(Yg, Ymg, om), scale);
+    const float2 omm = make_float2(-om.x, om.y);  // exp(-2 pi i (M - g) / P) = -conj(om)
+    wm[j] = c_scale(c2r_pair(Ymg, Yg, omm), scale);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int f2 = tid + NT * j;
+    *ua(f2) = wg[j];
+    if (!single) *ub(mcol[j]) = wm[j];
+  }
+  __syncthreads();
+
+  // inverse transforms over f2, twiddle exp(+2 pi i f1 m2 / M), store over A_u
+  {
+    const int sl = tid / T, t = tid % T;
+    const bool act = sl < (single ? 1 : 2);
+    const ScrPad16 sc{R[sl & 1]};
+    const uint32_t f1 = (uint32_t)(sl == 0 ? fa : fb);
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) w[e] = act ? *sc(t + T * e) : czero();
+    BlockFFT<N2, E, true>::run(w, t, sc, act);
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const uint32_t m2 = (uint32_t)(t + T * e);
+        A[(int64_t)f1 * N2 + m2] = c_mul(w[e], twiddle_rt<true>(f1 * m2, log2M));
+      }
+    }
+  }
+}
+
+template <int N1, bool CIRC, typename TS>
+__global__ void __launch_bounds__(1024)
+    fs_cols_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0, int N2,
+                int64_t per_line) {
+  using Cf = ColCfg<N1, 1>;
+  constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
+  constexpr int NOUT = CIRC ? N1 : N1 / 2;  // cropped rows m1
+  __shared__ float2 tile[N1 * TLP];
+  const int ntile = N2 / TL;
+  const int64_t line = blockIdx.x / ntile;
+  const int c0 = (int)(blockIdx.x % ntile) * TL;
+  const int64_t M = (int64_t)N1 * N2;
+  const int64_t L = CIRC ? 2 * M : M;
+  const float2* B = ws + line * per_line;
+  const int tid = threadIdx.x;
+
+  for (int i = tid; i < N1 * TL; i += NT) {
+    const int f1 = i / TL, cc = i - f1 * TL;
+    tile[f1 * TLP + cc] = B[(int64_t)f1 * N2 + c0 + cc];
+  }
+  __syncthreads();
+
+  for (int l0 = 0; l0 < TL; l0 += NT / T) {
+    const int cc = l0 + tid % (NT / T), t = tid / (NT / T);
+    const bool act = cc < TL;
+    float2* col = tile + (act ? cc : 0);
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) w[e] = act ? col[(t + T * e) * TLP] : czero();
+    BlockFFT<N1, E, true>::run(w, t, ScrStrided{col, TLP}, act);
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int m1 = t + T * e;
+        if (CIRC || m1 < NOUT) col[m1 * TLP] = w[e];
+      }
+    }
+  }
+  __syncthreads();
+
+  const size_t gbase = (size_t)(line0 + line) * L;
+  for (int i = tid; i < NOUT * TL; i += NT) {
+    const int m1 = i / TL, cc = i - m1 * TL;
+    const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
+    const float2 q = tile[m1 * TLP + cc];
+    const float2 g = ld2(x2 + n);
+    st2(y + n, make_float2(g.x * q.x, g.y * q.y));
+  }
+}
+
+struct FsLaunch {
+  const FftConvArgs* a;
+  float2* ws;
+  int64_t line0;
+  int nl;
+  int N1, log2M;
+  int64_t per;
+  float scale;
+  hipStream_t s;
+};
+
+template <int N1>
+hipError_t cols_fwd(const FsLaunch& L) {
+  constexpr int TL = ColCfg<N1, 2>::TL;
+  const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL)));
+  const FftConvArgs& a = *L.a;
+#define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per
+  if (a.bf16) {
+    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
+    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
+  } else {
+    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
+    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
+  }
+#undef HY_ARGS
+  return hipGetLastError();
+}
+
+template <int N1>
+hipError_t cols_inv(const FsLaunch& L) {
+  constexpr int TL = ColCfg<N1, 1>::TL;
+  const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL)));
+  const FftConvArgs& a = *L.a;
+#define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, kN2, L.per
+  if (a.bf16) {
+    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
+    else hipLaunchKernelGGL((fs_cols_inv<N1, false, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
+  } else {
+    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
+    else hipLaunchKernelGGL((fs_cols_inv<N1, false, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
+  }
+#undef HY_ARGS
+  return hipGetLastError();
+}
+
+#define HY_N1_SWITCH(N, FN, ARG)           \
+  switch (N) {                             \
+    case 8: return FN<8>(ARG);             \
+    case 16: return FN<16>(ARG);           \
+    case 32: return FN<32>(ARG);           \
+    case 64: return FN<64>(ARG);           \
+    case 128: return FN<128>(ARG);         \
+    case 256: return FN<256>(ARG);         \
+    case 512: return FN<512>(ARG);         \
+    case 1024: return FN<1024>(ARG);       \
+    default: return hipErrorInvalidValue;  \
+  }
+
+hipError_t d_cols_fwd(const FsLaunch& L) { HY_N1_SWITCH(L.N1, cols_fwd, L) }
+hipError_t d_cols_inv(const FsLaunch& L) { HY_N1_SWITCH(L.N1, cols_inv, L) }
+
+int ilog2_rt(int64_t n) {
+  int r = 0;
+  while ((int64_t(1) << r) < n) ++r;
+  return r;
+}
+
+}  // namespace
+
+bool fourstep_supported(const FftConvArgs& a) {
+  if (a.ndim != 1) return false;
+  const int64_t M = a.P[0] / 2;
+  if (M % kN2 != 0) return false;
+  const int64_t N1 = M / kN2;
+  return N1 >= kMinN1 && N1 <= kMaxN1;
+}
+
+size_t fourstep_bytes_per_line(const FftConvArgs& a) {
+  return (size_t)(a.P[0] / 2) * 2 * sizeof(float2);  // A_u and A_k
+}
+
+hipError_t launch_fourstep(const FftConvArgs& a, int64_t chunk, hipStream_t s) {
+  if (!fourstep_supported(a) || chunk < 1) return hipErrorInvalidValue;
+  FsLaunch L;
+  L.a = &a;
+  L.ws = (float2*)a.ws;
+  const int64_t M = a.P[0] / 2;
+  L.N1 = (int)(M / kN2);
+  L.log2M = ilog2_rt(M);
+  L.per = 2 * M;
+  L.scale = (float)(1.0 / (4.0 * (double)a.P[0]));
+  L.s = s;
+  for (int64_t line0 = 0; line0 < a.lines; line0 += chunk) {
+    L.line0 = line0;
+    L.nl = (int)((a.lines - line0) < chunk ? (a.lines - line0) : chunk);
+    hipError_t e;
+    if ((e = d_cols_fwd(L)) != hipSuccess) return e;
+    const dim3 grid((unsigned)((int64_t)L.nl * (L.N1 / 2 + 1)));
+    if (a.circular)
+      hipLaunchKernelGGL((fs_core<true>), grid, dim3(512), 0, s, L.ws, a.D, (int)a.bf16, line0, (int)a.C, L.N1,
+                         L.log2M, L.per, L.scale);
+    else
+      hipLaunchKernelGGL((fs_core<false>), grid, dim3(512), 0, s, L.ws, a.D, (int)a.bf16, line0, (int)a.C, L.N1,
+                         L.log2M, L.per, L.scale);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = d_cols_inv(L)) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace hyenand

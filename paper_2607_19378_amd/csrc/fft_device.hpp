@@ -220,6 +220,16 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
 }
 __device__ __forceinline__ void st1(float* p, float x) { *p = x; }
 __device__ __forceinline__ void st1(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
+// two consecutive values (p must be aligned to two elements)
+__device__ __forceinline__ float2 ld2(const float* p) { return *reinterpret_cast<const float2*>(p); }
+__device__ __forceinline__ float2 ld2(const uint16_t* p) {
+  const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+  return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+}
+__device__ __forceinline__ void st2(float* p, float2 x) { *reinterpret_cast<float2*>(p) = x; }
+__device__ __forceinline__ void st2(uint16_t* p, float2 x) {
+  *reinterpret_cast<uint32_t*>(p) = (uint32_t)f32_to_bf16_rne(x.x) | ((uint32_t)f32_to_bf16_rne(x.y) << 16);
+}
 
 // Real-to-complex post-pass.  A real line x[0..P) is read as the complex
 // line z[m] = x[2m] + i x[2m+1] of length M = P/2 and transformed; with

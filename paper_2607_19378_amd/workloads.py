@@ -17,10 +17,13 @@ datasets is used):
 * ``conv1d_1m``   -- 1D linear, bf16 storage, B=1, C=256, L=2^20 (genomics-scale
   long context, the 1M point of the context-length study).
 
-Draw recipe (identical for every workload): ``numpy.random.default_rng(seed)``
-(PCG64); draw order x1, x2, v, kernel noise, D, each a ``standard_normal`` array
-in C order of the stated shape.  Values are produced in float64 and rounded
-once, round-to-nearest-even, to the storage dtype.  The per-sample kernel is
+Draw recipe (identical for every workload): ``numpy.random.SeedSequence(seed)``
+spawns one child per tensor in the order x1, x2, v, kernel noise, D; each
+tensor is drawn in C order in blocks of 2^22 elements, block j from a PCG64
+stream seeded by the j-th child of that tensor's sequence (so blocks can be
+filled in parallel and the bytes do not depend on the thread count).  Values
+are ``standard_normal`` float64, rounded once, round-to-nearest-even, to the
+storage dtype.  The per-sample kernel is
 noise times a decay window evaluated in index units from index 0 (the
 zero-displacement tap):
 
@@ -122,14 +125,19 @@ ORDER = ["conv1d_4k", "conv2d_64", "conv2d_512c", "conv3d_128", "conv1d_1m"]
 def round_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round float64 values once, to nearest-even, to bfloat16; return uint16 bits.
 
-    The significand is rounded to 8 bits with ``numpy.rint`` (half to even) on
-    the float64 value itself, so there is no intermediate float32 rounding.
+    The rounding is done on the float64 bit pattern: the 52-bit significand is
+    cut to bfloat16's 7 stored bits with a round-half-to-even bias (a carry
+    into the exponent is the correct result), so there is no intermediate
+    float32 rounding.  The result is exactly representable in float32, whose
+    upper 16 bits are the bfloat16 bits.  Finite, normal-range inputs.
     """
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)                      # x = m * 2**e, 0.5 <= |m| < 1
-    r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)   # exactly representable in bf16 (normal range)
-    f32 = r.astype(np.float32)              # exact
-    return (f32.view(np.uint32) >> 16).astype(np.uint16)
+    b = np.ascontiguousarray(x, dtype=np.float64).view(np.uint64)
+    drop = np.uint64(45)                     # 52 - 7 significand bits removed
+    half = np.uint64((1 << 44) - 1)
+    lsb = (b >> drop) & np.uint64(1)
+    r = ((b + half + lsb) >> drop) << drop
+    f32 = r.view(np.float64).astype(np.float32)   # exact
+    return (f32.view(np.uint32) >> np.uint32(16)).astype(np.uint16)
 
 
 def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
@@ -178,29 +186,25 @@ def _gaussian_taps(sigma: float, radius: int) -> np.ndarray:
     return w / w.sum()
 
 
-def _periodic_smoothing_matrix(n: int, sigma: float) -> np.ndarray:
-    """Dense circulant matrix G with (G x)[i] = sum_t w[t] x[(i + t) mod n]."""
-    radius = int(4.0 * sigma + 0.5)
-    w = _gaussian_taps(sigma, radius)
-    G = np.zeros((n, n), dtype=np.float64)
-    rows = np.arange(n)
-    for j, t in enumerate(range(-radius, radius + 1)):
-        np.add.at(G, (rows, (rows + t) % n), w[j])
-    return G
-
-
 def smooth_fields(noise: np.ndarray, sigma: float) -> np.ndarray:
-    """Periodic separable Gaussian low-pass over the last two axes, then
-    per-field standardisation to zero mean and unit population variance."""
+    """Periodic separable Gaussian low-pass over the last two axes (taps
+    truncated at +-round(4 sigma), weights normalised to sum 1, wrap-around
+    boundaries), then per-field standardisation to zero mean and unit
+    population variance.  Fields are processed independently, in threads."""
+    from scipy import ndimage
+    radius = int(4.0 * sigma + 0.5)
+    taps = _gaussian_taps(sigma, radius)
     *lead, H, W = noise.shape
-    GH = _periodic_smoothing_matrix(H, sigma)
-    GW = _periodic_smoothing_matrix(W, sigma)
-    flat = noise.reshape(-1, H, W)
-    out = np.empty_like(flat)
-    for i in range(flat.shape[0]):
-        f = GH @ flat[i] @ GW.T
-        f = f - f.mean()
-        out[i] = f / f.std()
+    src = np.ascontiguousarray(noise, dtype=np.float64).reshape(-1, H, W)
+    out = np.empty_like(src)
+
+    def one(i):
+        f = ndimage.correlate1d(src[i], taps, axis=1, mode="wrap")
+        f = ndimage.correlate1d(f, taps, axis=0, mode="wrap")
+        f -= f.mean()
+        f /= f.std()
+        out[i] = f
+    _parallel(one, src.shape[0])
     return out.reshape(noise.shape)
 
 
@@ -224,27 +228,79 @@ class Inputs:
         return tuple(storage_to_f64(a, d) for a in (self.x1, self.x2, self.v, self.k, self.D))
 
 
+_BLOCK = 1 << 22
+
+
+def _threads() -> int:
+    import os
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _parallel(fn, nblocks: int) -> None:
+    from concurrent.futures import ThreadPoolExecutor
+    if nblocks <= 1:
+        for j in range(nblocks):
+            fn(j)
+        return
+    with ThreadPoolExecutor(_threads()) as ex:
+        list(ex.map(fn, range(nblocks)))
+
+
+def _normals(seq: np.random.SeedSequence, shape) -> np.ndarray:
+    out = np.empty(shape, dtype=np.float64)
+    flat = out.reshape(-1)
+    nb = (flat.size + _BLOCK - 1) // _BLOCK
+    kids = seq.spawn(nb)
+
+    def fill(j):
+        g = np.random.Generator(np.random.PCG64(kids[j]))
+        g.standard_normal(out=flat[j * _BLOCK:(j + 1) * _BLOCK])
+    _parallel(fill, nb)
+    return out
+
+
+def _quantise_parallel(x64: np.ndarray, dtype: str) -> np.ndarray:
+    flat = x64.reshape(-1)
+    out = np.empty(flat.size, dtype=np.float32 if dtype == "f32" else np.uint16)
+    nb = (flat.size + _BLOCK - 1) // _BLOCK
+
+    def q(j):
+        sl = slice(j * _BLOCK, (j + 1) * _BLOCK)
+        out[sl] = quantise(flat[sl], dtype)
+    _parallel(q, nb)
+    return out.reshape(x64.shape)
+
+
 def generate(w: Workload) -> Inputs:
-    rng = np.random.default_rng(w.seed)
+    seqs = np.random.SeedSequence(w.seed).spawn(5)  # x1, x2, v, kernel noise, D
     shp = w.shape
-    x1 = rng.standard_normal(shp)
-    x2 = rng.standard_normal(shp)
-    v = rng.standard_normal(shp)
-    kn = rng.standard_normal(shp)
-    D = rng.standard_normal((w.C,))
-    if w.smooth_sigma is not None:
-        x1 = smooth_fields(x1, w.smooth_sigma)
-        x2 = smooth_fields(x2, w.smooth_sigma)
-        v = smooth_fields(v, w.smooth_sigma)
+    out = []
+    for i in range(3):
+        a = _normals(seqs[i], shp)
+        if w.smooth_sigma is not None:
+            a = smooth_fields(a, w.smooth_sigma)
+        out.append(_quantise_parallel(a, w.dtype))
+        del a
     win = decay_window(w.grid, w.tau, periodic=(w.pad_mode == CIRCULAR))
     if w.kernel_norm:
         L = 1
         for g in w.grid:
             L *= g
         win = win / np.sqrt(L)
-    k = kn * win
-    q = lambda a: quantise(a, w.dtype)
-    return Inputs(w, q(x1), q(x2), q(v), q(k), q(D))
+    kn = _normals(seqs[3], shp)
+    kv = kn.reshape((-1,) + tuple(w.grid))
+
+    def scale(j):
+        kv[j] *= win
+    _parallel(scale, kv.shape[0])
+    k = _quantise_parallel(kn, w.dtype)
+    del kn, kv
+    D = quantise(_normals(seqs[4], (w.C,)), w.dtype)
+    return Inputs(w, out[0], out[1], out[2], k, D)
 
 
 def random_case(B: int, C: int, grid, pad_mode: str, dtype: str, seed: int,

@@ -62,3 +62,20 @@ def per_line_worst(a, b, nlines):
     num = np.linalg.norm(a - b, axis=1)
     den = np.maximum(np.linalg.norm(b, axis=1), 1e-300)
     return float(np.max(num / den))
+
+
+def oracle_lines(inp, lines):
+    """Oracle output of selected flat (b*C + c) lines, shape [len(lines), grid...].
+
+    Each selected line becomes one channel of a B=1 sub-problem carrying its
+    own D[c], so only the selected lines are upcast and computed."""
+    import oracle
+    w = inp.workload
+    nl = w.B * w.C
+    lines = np.asarray(lines, dtype=np.int64)
+    sub = []
+    for a in (inp.x1, inp.x2, inp.v, inp.k):
+        flat = a.reshape((nl,) + tuple(w.grid))[lines]
+        sub.append(W.storage_to_f64(flat, w.dtype)[None])
+    Dsub = W.storage_to_f64(inp.D, w.dtype)[lines % w.C]
+    return oracle.conv_fft(sub[0], sub[1], sub[2], sub[3], Dsub, w.pad_mode)[0]

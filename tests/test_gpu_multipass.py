@@ -1,0 +1,141 @@
+"""Parity of the multi-pass plans (2D/3D lines per axis, 1D four-step) with
+the fp64 oracle, from small ragged cases to the full-size workloads (checked
+on sampled lines, in the launch configuration the benchmark uses)."""
+import numpy as np
+import pytest
+
+from paper_2607_19378_amd import workloads as W
+
+from gpu_util import TOL, log, oracle_lines, oracle_ref, rel_l2, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_19378_amd import hyenand as H
+    H.lib()
+
+
+def check_full(inp, tag, **kw):
+    w = inp.workload
+    log(f"[multipass] {tag}: shape={w.shape} mode={w.pad_mode} dtype={w.dtype}")
+    y = run_gpu(inp, **kw)
+    ref = oracle_ref(inp)
+    err = rel_l2(y, ref)
+    log(f"[multipass] {tag}: rel_l2={err:.3e}")
+    assert np.all(np.isfinite(y)) and err <= TOL[w.dtype], f"{tag}: {err:.3e}"
+    return y
+
+
+def plan(inp):
+    from paper_2607_19378_amd import hyenand as H
+    w = inp.workload
+    return H.plan_name(w.shape, w.pad_mode, w.dtype)
+
+
+MP2D = [(2, 2), (4, 8), (16, 4), (32, 32), (8, 64), (64, 16)]
+
+
+@pytest.mark.parametrize("grid", MP2D)
+@pytest.mark.parametrize("mode", ["linear", "circular"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_multipass2d_forced(monkeypatch, grid, mode, dtype):
+    monkeypatch.setenv("HYENAND_PLAN", "multipass")
+    inp = W.random_case(3, 3, grid, mode, dtype, seed=300 + grid[0] + 7 * grid[1])
+    assert plan(inp) == "multipass2d"
+    check_full(inp, f"mp2d {grid}")
+
+
+@pytest.mark.parametrize("grid,mode", [((256, 256), "linear"), ((512, 256), "circular"), ((1024, 64), "circular"),
+                                       ((128, 512), "linear")])
+def test_multipass2d_natural(grid, mode):
+    inp = W.random_case(1, 3, grid, mode, "f32", seed=17)
+    assert plan(inp) == "multipass2d"
+    check_full(inp, f"mp2d {grid}")
+
+
+MP3D = [(2, 2, 2), (4, 4, 4), (2, 8, 4), (8, 4, 16), (16, 16, 16), (32, 8, 64), (4, 64, 8)]
+
+
+@pytest.mark.parametrize("grid", MP3D)
+@pytest.mark.parametrize("mode", ["linear", "circular"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_multipass3d(grid, mode, dtype):
+    inp = W.random_case(2, 3, grid, mode, dtype, seed=400 + sum(grid))
+    assert plan(inp) == "multipass3d"
+    check_full(inp, f"mp3d {grid}")
+
+
+@pytest.mark.parametrize("L,mode", [(16384, "linear"), (32768, "circular"), (65536, "linear"),
+                                    (1 << 17, "circular")])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fourstep(L, mode, dtype):
+    inp = W.random_case(1, 3, (L,), mode, dtype, seed=500 + L % 97)
+    assert plan(inp) == "fourstep1d"
+    check_full(inp, f"fourstep L={L}")
+
+
+def test_chunked_workspace_matches_full():
+    """A workspace of one line per chunk gives bitwise the same result as the
+    recommended one (chunking only changes the launch order)."""
+    from paper_2607_19378_amd import hyenand as H
+    for grid, mode in (((8, 16, 8), "linear"), ((256, 128), "circular"), ((32768,), "linear")):
+        inp = W.random_case(2, 3, grid, mode, "f32", seed=21)
+        w = inp.workload
+        wmin = H.workspace_min(w.shape, w.pad_mode, w.dtype)
+        wrec = H.workspace_size(w.shape, w.pad_mode, w.dtype)
+        assert 0 < wmin <= wrec
+        log(f"[chunk] {grid}: min={wmin} rec={wrec}")
+        y1 = run_gpu(inp, workspace_bytes=wmin)
+        y2 = run_gpu(inp, workspace_bytes=wmin * 2 + 8)
+        y3 = run_gpu(inp)
+        assert np.array_equal(y1, y3) and np.array_equal(y2, y3)
+        assert rel_l2(y3, oracle_ref(inp)) <= TOL["f32"]
+
+
+def test_workspace_too_small_rejected():
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    inp = W.random_case(1, 2, (8, 8, 8), "linear", "f32", seed=1)
+    w = inp.workload
+    wmin = H.workspace_min(w.shape, w.pad_mode, w.dtype)
+    with pytest.raises(H.HyenandError) as e:
+        run_gpu(inp, workspace_bytes=wmin - 8)
+    assert e.value.status == H.ERR_WORKSPACE_TOO_SMALL
+    torch.cuda.synchronize()
+
+
+@pytest.fixture(scope="module")
+def full_inputs():
+    cache = {}
+
+    def get(name):
+        if name not in cache:
+            cache.clear()
+            log(f"[full] generating {name}")
+            cache[name] = W.generate(W.WORKLOADS[name])
+        return cache[name]
+    return get
+
+
+@pytest.mark.parametrize("name", ["conv2d_512c", "conv3d_128", "conv1d_1m"])
+def test_full_size_sampled_lines(full_inputs, name):
+    """Full workload on the GPU in the benchmark's launch configuration;
+    parity on sampled (b, c) lines, and finiteness everywhere."""
+    inp = full_inputs(name)
+    w = inp.workload
+    log(f"[full] {name}: plan={plan(inp)}")
+    y = run_gpu(inp)
+    nl = w.B * w.C
+    assert np.all(np.isfinite(y))
+    rng = np.random.default_rng(99)
+    lines = np.unique(np.concatenate([[0, nl - 1], rng.choice(nl, size=6, replace=False)]))
+    ref = oracle_lines(inp, lines)
+    got = y.reshape((nl,) + tuple(w.grid))[lines]
+    err = rel_l2(got, ref)
+    log(f"[full] {name}: lines={lines.tolist()} rel_l2={err:.3e} (tol {TOL[w.dtype]:.0e})")
+    assert err <= TOL[w.dtype]
