@@ -166,6 +166,13 @@ hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // 2D
 // ---------------------------------------------------------------------------
+// LDS holds the half spectra of the L0 nonzero rows only (linear mode: half
+// the padded rows), so two workgroups fit on a CU for the 128 x 128
+// transform.  Column transforms exchange through the column's own U and K
+// slots (2 L0 >= P0 entries).  Columns 0 and P1/2 of a real row transform are
+// real, so they travel together as one complex column (a + i b) and are
+// separated with the mirror bin; M1 = P1/2 column groups cover all M1 + 1
+// columns.
 template <int P0, int P1, bool CIRC, typename TS>
 struct Fused2D {
   static constexpr int L0 = CIRC ? P0 : P0 / 2;
@@ -173,33 +180,33 @@ struct Fused2D {
   static constexpr int M1 = P1 / 2;          // packed complex row length
   static constexpr int MNZ = (L1 + 1) / 2;   // nonzero packed samples per row
   static constexpr int RP = M1 + 1;          // LDS row pitch (half spectrum + Nyquist)
-  static constexpr int NT = 1024;
+  static constexpr int NT = 512;
   // forward row transforms: 2 L0 lines (u rows, k rows) of M1 points
-  static constexpr int ER = imin(8, M1);
+  static constexpr int ER = imin(16, M1);
   static constexpr int TR = M1 / ER;
   static constexpr int LR = NT / TR;         // lines per round
-  // column transforms (length P0) of the M1 + 1 half-spectrum columns
-  static constexpr int EC = imin(16, P0);
+  // column transforms (length P0): M1 groups
+  static constexpr int EC = imin(8, P0);
   static constexpr int TC = P0 / EC;
-  static constexpr int CR = NT / TC;         // columns per round
+  static constexpr int CR = NT / TC;         // column groups per round
   // inverse row transforms carrying two rows each
   static constexpr int EI = imin(8, P1);
   static constexpr int TI = P1 / EI;
   static constexpr int PR = NT / TI;         // row pairs per round
   // real-to-complex untangling items: rows x (M1/2 + 1)
   static constexpr int NPOST = 2 * L0 * (M1 / 2 + 1);
-  static constexpr int IPT = (NPOST + NT - 1) / NT;
   static_assert(2 * RP >= P1, "two-row scratch");
+  static_assert(2 * L0 >= P0, "column scratch");
 };
 
 template <int P0, int P1, bool CIRC, typename TS>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
                  const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C) {
   using F = Fused2D<P0, P1, CIRC, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
-  __shared__ float2 Uh[P0 * RP];
-  __shared__ float2 Kh[P0 * RP];
+  __shared__ float2 Uh[L0 * RP];
+  __shared__ float2 Kh[L0 * RP];
   const int img = blockIdx.x;
   const int c = img % C;
   const size_t base = (size_t)img * L0 * L1;
@@ -214,12 +221,6 @@ __global__ void __launch_bounds__(1024)
       const int r = i / L1, col = i - r * L1;
       uf[r * 2 * RP + col] = ld1(x1 + base + i) * ld1(v + base + i);
       kf[r * 2 * RP + col] = ld1(k + base + i);
-    }
-    if constexpr (L1 % 2 == 1) {  // odd row length: zero the unpaired odd sample
-      for (int r = tid; r < L0; r += NT) {
-        uf[r * 2 * RP + L1] = 0.f;
-        kf[r * 2 * RP + L1] = 0.f;
-      }
     }
   }
   __syncthreads();
@@ -244,58 +245,95 @@ __global__ void __launch_bounds__(1024)
       }
     }
     __syncthreads();
-    float2 xa[F::IPT], xb[F::IPT];
-#pragma unroll
-    for (int j = 0; j < F::IPT; ++j) {
-      const int it = tid + NT * j;
-      if (it < F::NPOST) {
-        const int l = it % (2 * L0), g = it / (2 * L0);
-        const float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
-        r2c_pair(row[g], row[(M1 - g) & (M1 - 1)], twiddle<ilog2(P1), false>(g), xa[j], xb[j]);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < F::IPT; ++j) {
-      const int it = tid + NT * j;
-      if (it < F::NPOST) {
-        const int l = it % (2 * L0), g = it / (2 * L0);
-        float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
-        row[g] = xa[j];
-        row[M1 - g] = xb[j];  // g = 0 writes the Nyquist bin M1
-      }
+    // item (row, g) owns bins g and M1 - g (g = 0 also writes the Nyquist
+    // slot M1), so the untangling is an in-place read-modify-write
+    for (int it = tid; it < F::NPOST; it += NT) {
+      const int l = it % (2 * L0), g = it / (2 * L0);
+      float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+      float2 xa, xb;
+      r2c_pair(row[g], row[(M1 - g) & (M1 - 1)], twiddle<ilog2(P1), false>(g), xa, xb);
+      row[g] = xa;
+      row[M1 - g] = xb;
     }
   }
   __syncthreads();
 
-  // 2. columns 0..M1 of both half spectra: forward transforms, gated product
-  //    with the folded shortcut, inverse transform; keep rows < L0.
+  // 2. column groups: forward transforms of U and K, gated product with the
+  //    folded shortcut, inverse transform; keep rows < L0.  Group 0 carries
+  //    the two real columns 0 and M1 as one complex column.
   {
     constexpr int E = F::EC, T = F::TC, CR = F::CR;
-    constexpr int NC = M1 + 1;
     const float twoD = 2.f * ld1(Dp + c);
     const float scale = 1.f / (4.f * (float)P0 * (float)P1);
-    for (int c0 = 0; c0 < NC; c0 += CR) {
-      const int col = c0 + tid % CR, t = tid / CR;
-      const bool act = col < NC;
+    for (int c0 = 0; c0 < M1; c0 += CR) {
+      const int grp = c0 + tid % CR, t = tid / CR;
+      const bool act = grp < M1;
+      const bool nyq = act && grp == 0;
+      const int col = act ? grp : 0;
       float2 wu[E], wk[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int n = t + T * e;
         const bool nz = act && (CIRC || n < L0);
-        wu[e] = nz ? Uh[n * RP + col] : czero();
-        wk[e] = nz ? Kh[n * RP + col] : czero();
+        wu[e] = czero();
+        wk[e] = czero();
+        if (nz) {
+          if (nyq) {
+            wu[e] = make_float2(Uh[n * RP].x, Uh[n * RP + M1].x);
+            wk[e] = make_float2(Kh[n * RP].x, Kh[n * RP + M1].x);
+          } else {
+            wu[e] = Uh[n * RP + col];
+            wk[e] = Kh[n * RP + col];
+          }
+        }
       }
-      BlockFFT<P0, E, false>::run(wu, t, ScrStrided{Uh + col, RP}, act);
-      BlockFFT<P0, E, false>::run(wk, t, ScrStrided{Kh + col, RP}, act);
+      const ScrSplit su{Uh + col, Kh + col, L0, RP};
+      BlockFFT<P0, E, false>::run(wu, t, su, act);
+      BlockFFT<P0, E, false>::run(wk, t, su, act);
+      // group 0: publish both spectra so the mirror bins can be read
+      const ScrSplit sk0{CIRC ? Kh : Uh + M1, CIRC ? Kh : Kh + M1, L0, RP};
+      __syncthreads();
+      if (nyq) {
 #pragma unroll
-      for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
-      BlockFFT<P0, E, true>::run(wu, t, ScrStrided{Uh + col, RP}, act);
+        for (int e = 0; e < E; ++e) {
+          *su(t + T * e) = wu[e];
+          *sk0(t + T * e) = wk[e];
+        }
+      }
+      __syncthreads();
+      if (nyq) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int fm = (P0 - (t + T * e)) & (P0 - 1);
+          const float2 bu = *su(fm), bk = *sk0(fm);
+          // a + i b packing: A = (Z + conj Zm)/2, B = -i (Z - conj Zm)/2
+          const float2 ua = c_scale(make_float2(wu[e].x + bu.x, wu[e].y - bu.y), 0.5f);
+          const float2 ub = c_scale(make_float2(wu[e].y + bu.y, bu.x - wu[e].x), 0.5f);
+          const float2 ka = c_scale(make_float2(wk[e].x + bk.x, wk[e].y - bk.y), 0.5f);
+          const float2 kb = c_scale(make_float2(wk[e].y + bk.y, bk.x - wk[e].x), 0.5f);
+          const float2 ya = c_scale(gated_product(ua, ka, twoD), scale);
+          const float2 yb = c_scale(gated_product(ub, kb, twoD), scale);
+          wu[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
+      }
+      if constexpr (T == 1) __syncthreads();
+      BlockFFT<P0, E, true>::run(wu, t, su, act);
+      __syncthreads();  // scratch reads of the last exchange are done
       if (act) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const int n = t + T * e;
-          if (CIRC || n < L0) Uh[n * RP + col] = wu[e];
+          if (CIRC || n < L0) {
+            if (nyq) {
+              Uh[n * RP] = make_float2(wu[e].x, 0.f);
+              Uh[n * RP + M1] = make_float2(wu[e].y, 0.f);
+            } else {
+              Uh[n * RP + col] = wu[e];
+            }
+          }
         }
       }
     }
@@ -310,7 +348,7 @@ __global__ void __launch_bounds__(1024)
     for (int q0 = 0; q0 < NPAIR; q0 += PR) {
       const int q = q0 + tid % PR, t = tid / PR;
       const bool act = q < NPAIR;
-      float2* ra = Uh + 2 * q * RP;
+      float2* ra = Uh + 2 * (act ? q : 0) * RP;
       const float2* rb = ra + RP;
       float2 w[E];
 #pragma unroll
@@ -351,7 +389,7 @@ __global__ void __launch_bounds__(1024)
 
 template <int P0, int P1, bool CIRC, typename TS>
 static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(1024), 0, s,
+  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(512), 0, s,
                      (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
                      (const TS*)a.D, (TS*)a.y, (int)a.C);
   return hipGetLastError();

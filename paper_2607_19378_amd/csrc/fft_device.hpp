@@ -143,6 +143,15 @@ struct ScrStrided {  // element p at base[p * stride]
   int stride;
   __device__ __forceinline__ float2* operator()(int p) const { return base + p * stride; }
 };
+struct ScrSplit {  // positions [0, n0) in column a, the rest in column b (same stride)
+  float2* a;
+  float2* b;
+  int n0;
+  int stride;
+  __device__ __forceinline__ float2* operator()(int p) const {
+    return p < n0 ? a + p * stride : b + (p - n0) * stride;
+  }
+};
 struct ScrPad16 {  // element p at base[p + p/16]: one pad slot per 16 entries
   float2* base;
   __device__ __forceinline__ float2* operator()(int p) const { return base + p + (p >> 4); }
@@ -171,19 +180,21 @@ struct BlockFFT {
     constexpr int R = (N / NS >= E) ? E : N / NS;
     constexpr int NB = E / R;  // butterflies per lane in this pass
     constexpr int LOGW = ilog2(NS * R);
+    if (active) {  // waves with no active lane skip the arithmetic
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      float2 x[R];
+      for (int b = 0; b < NB; ++b) {
+        float2 x[R];
 #pragma unroll
-      for (int r = 0; r < R; ++r) x[r] = v[b + NB * r];
-      if constexpr (NS > 1) {
-        const uint32_t jm = (uint32_t)(t + T * b) & (NS - 1);
+        for (int r = 0; r < R; ++r) x[r] = v[b + NB * r];
+        if constexpr (NS > 1) {
+          const uint32_t jm = (uint32_t)(t + T * b) & (NS - 1);
 #pragma unroll
-        for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], twiddle<LOGW, INV>(jm * r));
+          for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], twiddle<LOGW, INV>(jm * r));
+        }
+        dft<R, INV>(x);
+#pragma unroll
+        for (int r = 0; r < R; ++r) v[b + NB * r] = x[r];
       }
-      dft<R, INV>(x);
-#pragma unroll
-      for (int r = 0; r < R; ++r) v[b + NB * r] = x[r];
     }
     if constexpr (NS * R < N) {
       __syncthreads();
