@@ -52,18 +52,19 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  * hyenand_fftconv -- y = x2 * (k conv (x1*v) + D*(x1*v)) on the GPU.
  *
  * x1, x2, v, k, y : device pointers, contiguous row-major [B, C, L1, ..., LN]
- *                   of `dtype` (fp32, or bf16 bits).  y must not overlap any
- *                   input.
+ *                   of `dtype` (fp32, or bf16 bits), 16-byte aligned (fresh
+ *                   allocations are).  y must not overlap any input.
  * D               : device pointer, [C] of `dtype`.
  * ndim            : N in {1, 2, 3}.
  * dims            : host pointer to ndim + 2 int64 values {B, C, L1, ..., LN},
  *                   all >= 1; every L_d must be a power of two.  Supported
- *                   transform extents: 1D up to 2^24 points, 2D/3D up to 4096
- *                   per axis.
+ *                   transform extents (2 L_d linear, L_d circular): 1D up to
+ *                   2^22 points, 2D/3D up to 1024 per axis.
  * pad_mode        : hyenand_pad_mode.
  * dtype           : hyenand_dtype.
- * workspace       : device scratch of workspace_bytes, owned by the caller; may
- *                   be NULL when hyenand_fftconv_workspace_size() reports 0.
+ * workspace       : device scratch of workspace_bytes (16-byte aligned), owned
+ *                   by the caller; may be NULL when
+ *                   hyenand_fftconv_workspace_size() reports 0.
  *                   A workspace smaller than the reported size but at least
  *                   the minimum one is accepted (the work is then split into
  *                   more passes).

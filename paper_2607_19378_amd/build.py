@@ -24,7 +24,7 @@ ARCH = "gfx950"
 # v_pk_{add,mul,fma}_f32 from plain float code.
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-I", os.path.join(os.path.dirname(PKG), "include")]
+         "-Wno-pass-failed", "-I", os.path.join(os.path.dirname(PKG), "include")]
 
 
 def _compile(src: str) -> str:

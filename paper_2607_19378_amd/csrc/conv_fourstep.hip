@@ -30,28 +30,46 @@ constexpr int kN2 = 2048;
 constexpr int kMinN1 = 8;
 constexpr int kMaxN1 = 1024;
 
-// column tiles: NS signals of TL adjacent columns, N1 points each
-template <int N1, int NS>
+// column tiles: TL adjacent columns of one signal, N1 points each; TL is the
+// widest power of two (<= 32) whose tile fits in ~75 KB of LDS, E is chosen
+// so the tile keeps 512 lanes busy when it can.
+constexpr int fs_tl(int N1) {
+  int tl = 32;
+  while (tl > 1 && N1 * (tl + 1) * 8 > 76 * 1024) tl /= 2;
+  return tl;
+}
+template <int N1>
 struct ColCfg {
-  static constexpr int E = imin(16, N1);
+  static constexpr int NT = 512;
+  static constexpr int TL = fs_tl(N1);
+  static constexpr int E = imax(imin(16, N1), imin(N1, imax(2, (N1 * TL) / NT)));
   static constexpr int T = N1 / E;
-  static constexpr int NT = 1024;
-  static constexpr int TL0 = imin(32, imax(2, NT / (NS * T)));
-  static constexpr int TL = (NS * N1 * (TL0 + 1) * 8 <= 150 * 1024) ? TL0 : imax(1, TL0 / 2);
   static constexpr int TLP = TL + 1;
 };
 
+// w, w s, w s^2, ... (E values): twiddles of one lane by recurrence
+template <int E>
+__device__ __forceinline__ void twiddle_run(float2 (&v)[E], float2 w, float2 s) {
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    v[e] = c_mul(v[e], w);
+    w = c_mul(w, s);
+  }
+}
+
 template <int N1, bool CIRC, typename TS>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(512)
     fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line) {
-  using Cf = ColCfg<N1, 2>;
+  using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
-  __shared__ float2 tile[2][N1 * TLP];
+  __shared__ float2 tile[N1 * TLP];
   const int ntile = N2 / TL;
-  const int64_t line = blockIdx.x / ntile;
-  const int c0 = (int)(blockIdx.x % ntile) * TL;
+  const int sig = (int)(blockIdx.x & 1);  // 0: u = x1 v, 1: k
+  const int64_t rest = blockIdx.x >> 1;
+  const int64_t line = rest / ntile;
+  const int c0 = (int)(rest % ntile) * TL;
   const int64_t M = (int64_t)N1 * N2;
   const int64_t L = CIRC ? 2 * M : M;  // real samples per line
   const size_t gbase = (size_t)(line0 + line) * L;
@@ -60,18 +78,21 @@ __global__ void __launch_bounds__(1024)
   for (int i = tid; i < NZ * TL; i += NT) {
     const int m1 = i / TL, cc = i - m1 * TL;
     const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
-    const float2 a = ld2(x1 + n), b = ld2(v + n);
-    tile[0][m1 * TLP + cc] = make_float2(a.x * b.x, a.y * b.y);
-    tile[1][m1 * TLP + cc] = ld2(k + n);
+    float2 z;
+    if (sig == 0) {
+      const float2 a = ld2(x1 + n), b = ld2(v + n);
+      z = make_float2(a.x * b.x, a.y * b.y);
+    } else {
+      z = ld2(k + n);
+    }
+    tile[m1 * TLP + cc] = z;
   }
   __syncthreads();
 
-  constexpr int NL = 2 * TL;
-  for (int l0 = 0; l0 < NL; l0 += NT / T) {
-    const int l = l0 + tid % (NT / T), t = tid / (NT / T);
-    const bool act = l < NL;
-    const int s = (l / TL) & 1, cc = l % TL;
-    float2* col = tile[s] + cc;
+  for (int l0 = 0; l0 < TL; l0 += NT / T) {
+    const int cc = l0 + tid % (NT / T), t = tid / (NT / T);
+    const bool act = cc < TL;
+    float2* col = tile + (act ? cc : 0);
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -80,22 +101,19 @@ __global__ void __launch_bounds__(1024)
     }
     BlockFFT<N1, E, false>::run(w, t, ScrStrided{col, TLP}, act);
     if (act) {
+      // exp(-2 pi i m2 f1 / M) for f1 = t + T e
       const uint32_t m2 = (uint32_t)(c0 + cc);
+      twiddle_run<E>(w, twiddle_rt<false>(m2 * (uint32_t)t, log2M), twiddle_rt<false>(m2 * (uint32_t)T, log2M));
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint32_t f1 = (uint32_t)(t + T * e);
-        col[f1 * TLP] = c_mul(w[e], twiddle_rt<false>(m2 * f1, log2M));
-      }
+      for (int e = 0; e < E; ++e) col[(t + T * e) * TLP] = w[e];
     }
   }
   __syncthreads();
 
-  float2* A = ws + line * per_line;
+  float2* A = ws + line * per_line + (sig ? M : 0);
   for (int i = tid; i < N1 * TL; i += NT) {
     const int f1 = i / TL, cc = i - f1 * TL;
-    const size_t off = (size_t)f1 * N2 + c0 + cc;
-    A[off] = tile[0][f1 * TLP + cc];
-    A[M + off] = tile[1][f1 * TLP + cc];
+    A[(size_t)f1 * N2 + c0 + cc] = tile[f1 * TLP + cc];
   }
 }
 
@@ -118,6 +136,8 @@ __global__ void __launch_bounds__(512)
   const float twoD = 2.f * (dbf16 ? ld1((const uint16_t*)Dp + c) : ld1((const float*)Dp + c));
   float2* A = ws + line * per_line;
   const int tid = threadIdx.x;
+  // exp(-2 pi i g / P) for g = fa + N1 f2 is exp(-2 pi i fa / P) exp(-2 pi i f2 / (2 N2))
+  const float2 om_a = twiddle_rt<false>((uint32_t)fa, log2M + 1);
   // slots: 0 = u row fa, 1 = u row fb, 2 = k row fa, 3 = k row fb (a single
   // self-mirrored row uses slots 0 and 2 only)
   for (int i = tid; i < 4 * N2; i += NT) {
@@ -155,8 +175,8 @@ __global__ void __launch_bounds__(512)
     const int f2 = tid + NT * j;
     const int mc = fa == 0 ? ((N2 - f2) & (N2 - 1)) : (N2 - 1 - f2);
     mcol[j] = mc;
-    const uint32_t g = (uint32_t)fa + (uint32_t)N1 * (uint32_t)f2;
-    const float2 om = twiddle_rt<false>(g, log2M + 1);  // exp(-2 pi i g / P)
+    static_assert(2 * N2 == 4096, "the untangling twiddle uses the 4096-point table");
+    const float2 om = c_mul(om_a, kTwCoarse[f2]);  // exp(-2 pi i g / P)
     float2 Ug, Umg, Kg, Kmg;
     r2c_pair(*ua(f2), *ub(mc), om, Ug, Umg);
     r2c_pair(*ka(f2), *kb(mc), om, Kg, Kmg);
@@ -186,20 +206,19 @@ __global__ void __launch_bounds__(512)
     for (int e = 0; e < E; ++e) w[e] = act ? *sc(t + T * e) : czero();
     BlockFFT<N2, E, true>::run(w, t, sc, act);
     if (act) {
+      // exp(+2 pi i f1 m2 / M) for m2 = t + T e
+      twiddle_run<E>(w, twiddle_rt<true>(f1 * (uint32_t)t, log2M), twiddle_rt<true>(f1 * (uint32_t)T, log2M));
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const uint32_t m2 = (uint32_t)(t + T * e);
-        A[(int64_t)f1 * N2 + m2] = c_mul(w[e], twiddle_rt<true>(f1 * m2, log2M));
-      }
+      for (int e = 0; e < E; ++e) A[(int64_t)f1 * N2 + t + T * e] = w[e];
     }
   }
 }
 
 template <int N1, bool CIRC, typename TS>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(512)
     fs_cols_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0, int N2,
                 int64_t per_line) {
-  using Cf = ColCfg<N1, 1>;
+  using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NOUT = CIRC ? N1 : N1 / 2;  // cropped rows m1
   __shared__ float2 tile[N1 * TLP];
@@ -258,16 +277,16 @@ struct FsLaunch {
 
 template <int N1>
 hipError_t cols_fwd(const FsLaunch& L) {
-  constexpr int TL = ColCfg<N1, 2>::TL;
-  const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL)));
+  constexpr int TL = ColCfg<N1>::TL;
+  const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * 2));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per
   if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
+    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
   } else {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
+    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
   }
 #undef HY_ARGS
   return hipGetLastError();
@@ -275,16 +294,16 @@ hipError_t cols_fwd(const FsLaunch& L) {
 
 template <int N1>
 hipError_t cols_inv(const FsLaunch& L) {
-  constexpr int TL = ColCfg<N1, 1>::TL;
+  constexpr int TL = ColCfg<N1>::TL;
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL)));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, kN2, L.per
   if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((fs_cols_inv<N1, false, uint16_t>), grid, dim3(1024), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
+    else hipLaunchKernelGGL((fs_cols_inv<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
   } else {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((fs_cols_inv<N1, false, float>), grid, dim3(1024), 0, L.s, HY_ARGS(float));
+    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+    else hipLaunchKernelGGL((fs_cols_inv<N1, false, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
   }
 #undef HY_ARGS
   return hipGetLastError();

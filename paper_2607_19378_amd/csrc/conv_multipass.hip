@@ -1,7 +1,9 @@
 // Multi-pass 2D/3D plan for grids whose half spectra do not fit in LDS.
 //
 // Per (b, c) line the half spectra U, K of shape [L0][P1][H] (3D; 2D is the
-// same with P1 = L1 = 1) live in the workspace, H = Plast/2 + 1:
+// same with P1 = L1 = 1) live in the workspace, H = Plast/2 + 1 valid bins
+// per row stored with a row stride HS = H rounded up to 16 complex values
+// (128 B), so every row starts on a cache line:
 //
 //   rows_fwd   read x1, v, k rows; u = x1 v; real-to-complex transform of every
 //              nonzero row of u and of k along the last axis (length Plast).
@@ -14,10 +16,10 @@
 //              rows per complex transform; crop, outer gate x2, store y.
 //
 // Inputs are read once and y is written once; only the spectra round-trip
-// through the workspace, which is sized per chunk of lines so that a chunk's
-// spectra can stay in the Infinity Cache.  Strided axes are transformed in
-// tiles of TL adjacent columns, so every global access is a contiguous run of
-// TL complex values and no explicit transpose is ever stored.
+// through the workspace, which is sized per chunk of lines.  Strided axes are
+// transformed in tiles of TL adjacent columns, so every global access is a
+// contiguous run of TL complex values and no explicit transpose is stored.
+// Tiles are sized so that two 512-lane workgroups share a CU.
 #include "kernels.hpp"
 
 namespace hyenand {
@@ -27,9 +29,9 @@ namespace {
 constexpr int kMaxP = 1024;
 
 struct MpGeom {
-  int L0, P0, L1, P1, LL, PL, H;  // L1 = P1 = 1 in 2D
-  int rows;                       // nonzero rows per line: L0 * L1
-  int64_t half;                   // complex entries of U (or K) per line: L0 * P1 * H
+  int L0, P0, L1, P1, LL, PL, H, HS;  // L1 = P1 = 1 in 2D
+  int rows;                           // nonzero rows per line: L0 * L1
+  int64_t half;                       // complex entries of U (or K) per line: L0 * P1 * HS
 };
 
 MpGeom mp_geom(const FftConvArgs& a) {
@@ -45,14 +47,15 @@ MpGeom mp_geom(const FftConvArgs& a) {
   g.LL = (int)a.L[a.ndim - 1];
   g.PL = (int)a.P[a.ndim - 1];
   g.H = g.PL / 2 + 1;
+  g.HS = (g.H + 15) & ~15;
   g.rows = g.L0 * g.L1;
-  g.half = (int64_t)g.L0 * g.P1 * g.H;
+  g.half = (int64_t)g.L0 * g.P1 * g.HS;
   return g;
 }
 
-// workspace row of flat nonzero row r: (n0 * P1 + n1) * H
-__device__ __forceinline__ int64_t ws_row(int r, int L1, int P1, int H) {
-  return ((int64_t)(r / L1) * P1 + (r % L1)) * H;
+// workspace offset of flat nonzero row r: (n0 * P1 + n1) * HS
+__device__ __forceinline__ int64_t ws_row(int r, int L1, int P1, int HS) {
+  return ((int64_t)(r / L1) * P1 + (r % L1)) * HS;
 }
 
 // ---------------------------------------------------------------------------
@@ -61,17 +64,17 @@ __device__ __forceinline__ int64_t ws_row(int r, int L1, int P1, int H) {
 template <int PL>
 struct RowsCfg {
   static constexpr int ML = PL / 2;
-  static constexpr int HP = ML + 1;  // row pitch in LDS
+  static constexpr int HP = ML + 1;  // row pitch in LDS (odd for ML >= 2)
   static constexpr int E = imin(16, ML);
   static constexpr int T = ML / E;
   static constexpr int NT = 256;
-  static constexpr int RPW = imax(1, imin(NT / (2 * T), (32 * 1024) / (2 * HP * 8)));  // rows per workgroup
+  static constexpr int RPW = imax(1, imin(NT / (2 * T), (36 * 1024) / (2 * HP * 8)));  // rows per workgroup
 };
 
 template <int PL, bool CIRC, typename TS>
 __global__ void __launch_bounds__(256)
     mp_rows_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
-                float2* __restrict__ ws, int64_t line0, int nlines, int rows, int L1, int P1,
+                float2* __restrict__ ws, int64_t line0, int nlines, int rows, int L1, int P1, int HS,
                 int64_t half, int64_t per_line) {
   using Cf = RowsCfg<PL>;
   constexpr int ML = Cf::ML, HP = Cf::HP, E = Cf::E, T = Cf::T, NT = Cf::NT, RPW = Cf::RPW;
@@ -85,15 +88,33 @@ __global__ void __launch_bounds__(256)
   const int nrow = (int)((total_rows - row0) < RPW ? (total_rows - row0) : RPW);
   const int tid = threadIdx.x;
 
-  // stage real rows (the input rows of the chunk are contiguous)
+  // stage real rows (the input rows of the chunk are contiguous), 4 per load
   {
     float* uf = reinterpret_cast<float*>(Ur);
     float* kf = reinterpret_cast<float*>(Kr);
     const size_t gbase = (size_t)(line0 * rows + row0) * LL;
-    for (int i = tid; i < nrow * LL; i += NT) {
-      const int r = i / LL, col = i - r * LL;
-      uf[r * 2 * HP + col] = ld1(x1 + gbase + i) * ld1(v + gbase + i);
-      kf[r * 2 * HP + col] = ld1(k + gbase + i);
+    if constexpr (LL % 4 == 0) {
+      for (int i4 = tid; i4 < nrow * (LL / 4); i4 += NT) {
+        const int i = 4 * i4;
+        const int r = i / LL, col = i - r * LL;
+        const float4 a = ld4(x1 + gbase + i), b = ld4(v + gbase + i), kk = ld4(k + gbase + i);
+        float* du = uf + r * 2 * HP + col;
+        float* dk = kf + r * 2 * HP + col;
+        du[0] = a.x * b.x;
+        du[1] = a.y * b.y;
+        du[2] = a.z * b.z;
+        du[3] = a.w * b.w;
+        dk[0] = kk.x;
+        dk[1] = kk.y;
+        dk[2] = kk.z;
+        dk[3] = kk.w;
+      }
+    } else {
+      for (int i = tid; i < nrow * LL; i += NT) {
+        const int r = i / LL, col = i - r * LL;
+        uf[r * 2 * HP + col] = ld1(x1 + gbase + i) * ld1(v + gbase + i);
+        kf[r * 2 * HP + col] = ld1(k + gbase + i);
+      }
     }
   }
   __syncthreads();
@@ -104,7 +125,7 @@ __global__ void __launch_bounds__(256)
     const int l = l0 + tid % (NT / T), t = tid / (NT / T);
     const int r = l >> 1;
     const bool act = l < NLINE && r < nrow;
-    float2* row = ((l & 1) ? Kr : Ur) + r * HP;
+    float2* row = ((l & 1) ? Kr : Ur) + (act ? r : 0) * HP;
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -119,84 +140,74 @@ __global__ void __launch_bounds__(256)
   }
   __syncthreads();
 
-  // untangle: items (line, g), g in [0, ML/2]
+  // untangle in place: item (line, g) owns bins g and ML - g (g = 0 also
+  // writes the Nyquist slot ML)
   constexpr int NPOST = NLINE * (ML / 2 + 1);
-  constexpr int IPT = (NPOST + NT - 1) / NT;
-  float2 xa[IPT], xb[IPT];
-#pragma unroll
-  for (int j = 0; j < IPT; ++j) {
-    const int it = tid + NT * j;
+  for (int it = tid; it < NPOST; it += NT) {
     const int l = it % NLINE, g = it / NLINE;
-    if (it < NPOST && (l >> 1) < nrow) {
-      const float2* row = ((l & 1) ? Kr : Ur) + (l >> 1) * HP;
-      r2c_pair(row[g], row[(ML - g) & (ML - 1)], twiddle<ilog2(PL), false>(g), xa[j], xb[j]);
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < IPT; ++j) {
-    const int it = tid + NT * j;
-    const int l = it % NLINE, g = it / NLINE;
-    if (it < NPOST && (l >> 1) < nrow) {
+    if ((l >> 1) < nrow) {
       float2* row = ((l & 1) ? Kr : Ur) + (l >> 1) * HP;
-      row[g] = xa[j];
-      row[ML - g] = xb[j];
+      float2 xa, xb;
+      r2c_pair(row[g], row[(ML - g) & (ML - 1)], twiddle<ilog2(PL), false>(g), xa, xb);
+      row[g] = xa;
+      row[ML - g] = xb;
     }
   }
   __syncthreads();
 
-  // store the H bins of every row to U and K (contiguous runs per row)
+  // store the H bins of every row to U and K (rows start on cache lines)
   for (int i = tid; i < nrow * H; i += NT) {
     const int r = i / H, f = i - r * H;
     const int64_t gr = row0 + r;
     const int64_t line = gr / rows;
     const int rr = (int)(gr - line * rows);
     float2* U = ws + line * per_line;
-    const int64_t off = ws_row(rr, L1, P1, H) + f;
+    const int64_t off = ws_row(rr, L1, P1, HS) + f;
     U[off] = Ur[r * HP + f];
     U[half + off] = Kr[r * HP + f];
   }
 }
 
 // ---------------------------------------------------------------------------
-// strided tiles: TL adjacent columns of a [rows][ncols] complex matrix,
-// transformed along the rows index.  LDS tile [P][TLP].
+// strided tiles: TL adjacent columns of a [rows][stride] complex matrix,
+// transformed along the rows index.  LDS tile [P][TLP].  Columns whose index
+// modulo HS is >= H (row padding) are neither loaded nor stored.
 // ---------------------------------------------------------------------------
-template <int P, int NS>
-struct TileCfg {
-  static constexpr int E = imin(16, P);
-  static constexpr int T = P / E;
-  // enough columns for 512 lanes, at most 32, within ~150 KB of LDS
-  static constexpr int TL0 = imin(32, imax(4, 512 / (NS * T)));
-  static constexpr int TL = (NS * P * (TL0 + 1) * 8 <= 150 * 1024) ? TL0 : imax(1, TL0 / 2);
-  static constexpr int TLP = TL + 1;  // LDS pitch
-};
+constexpr int mp_tl(int P, int NS) {  // widest power of two <= 32 fitting ~76 KB
+  int tl = 32;
+  while (tl > 1 && NS * P * (tl + 1) * 8 > 76 * 1024) tl /= 2;
+  return tl;
+}
+// E for `lines` transforms of length P carried by 512 lanes
+constexpr int mp_e(int P, int lines) { return imin(P, imax(2, imin(16, P * lines / 512))); }
 
-// core tiles: each lane carries one column of both U and K
-template <int P>
-struct CoreCfg {
-  static constexpr int E = imin(16, P);
+template <int P, int NS>
+struct TileCfg {  // NS signal tiles, each column of each signal is one line
+  static constexpr int TL = mp_tl(P, NS);
+  static constexpr int E = mp_e(P, NS * TL);
   static constexpr int T = P / E;
-  static constexpr int TL0 = imin(32, imax(4, 512 / T));
-  static constexpr int TL = (2 * P * (TL0 + 1) * 8 <= 150 * 1024) ? TL0 : imax(1, TL0 / 2);
   static constexpr int TLP = TL + 1;
 };
 
-template <int P, int TLP>
+__device__ __forceinline__ bool col_valid(int col, int ncols, int HS, int H) {
+  return col < ncols && (col % HS) < H;
+}
+
+template <int TLP>
 __device__ __forceinline__ void tile_load(float2* tile, const float2* __restrict__ src, int64_t stride, int col0,
-                                          int ncols, int nrows_load, int TL, int tid, int nt) {
-  for (int i = tid; i < nrows_load * TL; i += nt) {
+                                          int ncols, int HS, int H, int nrows, int TL, int tid, int nt) {
+  for (int i = tid; i < nrows * TL; i += nt) {
     const int p = i / TL, cc = i - p * TL;
-    if (col0 + cc < ncols) tile[p * TLP + cc] = src[p * stride + col0 + cc];
+    if (col_valid(col0 + cc, ncols, HS, H)) tile[p * TLP + cc] = src[p * stride + col0 + cc];
   }
 }
 
-template <int P, int TLP>
+template <int TLP>
 __device__ __forceinline__ void tile_store(const float2* tile, float2* __restrict__ dst, int64_t stride, int col0,
-                                           int ncols, int nrows_store, int TL, int tid, int nt) {
-  for (int i = tid; i < nrows_store * TL; i += nt) {
+                                           int ncols, int HS, int H, int nrows, int TL, int tid, int nt) {
+  for (int i = tid; i < nrows * TL; i += nt) {
     const int p = i / TL, cc = i - p * TL;
-    if (col0 + cc < ncols) dst[p * stride + col0 + cc] = tile[p * TLP + cc];
+    if (col_valid(col0 + cc, ncols, HS, H)) dst[p * stride + col0 + cc] = tile[p * TLP + cc];
   }
 }
 
@@ -206,7 +217,7 @@ __device__ __forceinline__ void tile_store(const float2* tile, float2* __restric
 // ---------------------------------------------------------------------------
 template <int P1, bool CIRC, bool INV>
 __global__ void __launch_bounds__(512)
-    mp_axis1(float2* __restrict__ ws, int H, int L0, int64_t half, int64_t per_line) {
+    mp_axis1(float2* __restrict__ ws, int H, int HS, int L0, int64_t half, int64_t per_line) {
   constexpr int NS = INV ? 1 : 2;  // signals
   using Cf = TileCfg<P1, NS>;
   constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T;
@@ -221,11 +232,11 @@ __global__ void __launch_bounds__(512)
   const int64_t line = rest / L0;
   const int col0 = tl * TL;
   const int tid = threadIdx.x;
-  float2* base = ws + line * per_line + (int64_t)n0 * P1 * H;
+  float2* base = ws + line * per_line + (int64_t)n0 * P1 * HS;
 
   const int nload = INV ? P1 : L1;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) tile_load<P1, TLP>(tile[s], base + s * half, H, col0, H, nload, TL, tid, NT);
+  for (int s = 0; s < NS; ++s) tile_load<TLP>(tile[s], base + s * half, HS, col0, H, HS, H, nload, TL, tid, NT);
   __syncthreads();
 
   constexpr int NL = NS * TL;
@@ -233,7 +244,7 @@ __global__ void __launch_bounds__(512)
     const int l = l0 + tid % (NT / T), t = tid / (NT / T);
     const int s = l / TL, cc = l % TL;
     const bool act = l < NL && col0 + cc < H;
-    float2* col = tile[s < NS ? s : 0] + cc;
+    float2* col = tile[act ? s : 0] + cc;
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -249,22 +260,33 @@ __global__ void __launch_bounds__(512)
   __syncthreads();
   const int nstore = INV ? L1 : P1;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) tile_store<P1, TLP>(tile[s], base + s * half, H, col0, H, nstore, TL, tid, NT);
+  for (int s = 0; s < NS; ++s) tile_store<TLP>(tile[s], base + s * half, HS, col0, H, HS, H, nstore, TL, tid, NT);
 }
 
 // ---------------------------------------------------------------------------
 // core: along axis 0, forward U and K, gated product, inverse, crop.
-// One workgroup per (line, tile of TL adjacent columns of the [L0][ncols] view).
+// One workgroup per (line, tile of TL adjacent columns of the [L0][ncols]
+// view).  Only one signal tile lives in LDS: K's tile is prefetched into
+// registers while U's tile loads and transforms, then takes its place.
 // ---------------------------------------------------------------------------
+template <int P0, bool CIRC>
+struct CoreCfg {
+  static constexpr int NT = 512;
+  static constexpr int TL = mp_tl(P0, 1);
+  static constexpr int E = mp_e(P0, TL);
+  static constexpr int T = P0 / E;
+  static constexpr int TLP = TL + 1;
+  static constexpr int L0 = CIRC ? P0 : P0 / 2;
+  static constexpr int KPT = (L0 * TL + NT - 1) / NT;  // prefetched K values per lane
+};
+
 template <int P0, bool CIRC>
 __global__ void __launch_bounds__(512)
     mp_core(float2* __restrict__ ws, const void* __restrict__ Dp, int dbf16, int64_t line0, int C,
-            int ncols, int64_t half, int64_t per_line, float scale) {
-  using Cf = CoreCfg<P0>;
-  constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T;
-  constexpr int L0 = CIRC ? P0 : P0 / 2;
-  constexpr int NT = 512;
-  __shared__ float2 tile[2][P0 * TLP];
+            int ncols, int HS, int H, int64_t half, int64_t per_line, float scale) {
+  using Cf = CoreCfg<P0, CIRC>;
+  constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T, NT = Cf::NT, L0 = Cf::L0, KPT = Cf::KPT;
+  __shared__ float2 tile[P0 * TLP];
   const int ntile = (ncols + TL - 1) / TL;
   const int tl = (int)(blockIdx.x % ntile);
   const int64_t line = blockIdx.x / ntile;
@@ -274,39 +296,57 @@ __global__ void __launch_bounds__(512)
   const float Dv = dbf16 ? ld1((const uint16_t*)Dp + c) : ld1((const float*)Dp + c);
   const float twoD = 2.f * Dv;
   float2* U = ws + line * per_line;
+  const float2* K = U + half;
 
-  tile_load<P0, TLP>(tile[0], U, ncols, col0, ncols, L0, TL, tid, NT);
-  tile_load<P0, TLP>(tile[1], U + half, ncols, col0, ncols, L0, TL, tid, NT);
+  // K's tile into registers, U's tile into LDS
+  float2 kreg[KPT];
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const int i = tid + NT * j;
+    const int p = i / TL, cc = i - p * TL;
+    kreg[j] = (i < L0 * TL && col_valid(col0 + cc, ncols, HS, H)) ? K[(int64_t)p * ncols + col0 + cc] : czero();
+  }
+  tile_load<TLP>(tile, U, ncols, col0, ncols, HS, H, L0, TL, tid, NT);
   __syncthreads();
 
-  for (int l0 = 0; l0 < TL; l0 += NT / T) {
-    const int cc = l0 + tid % (NT / T), t = tid / (NT / T);
-    const bool act = cc < TL && col0 + cc < ncols;
-    float2* cu = tile[0] + (cc < TL ? cc : 0);
-    float2* ck = tile[1] + (cc < TL ? cc : 0);
-    float2 wu[E], wk[E];
+  static_assert(NT / T >= TL, "one round of columns");
+  const int cc = tid % TL, t = tid / TL;
+  const bool act = t < T;
+  float2* col = tile + cc;
+  const ScrStrided sc{col, TLP};
+  float2 wu[E], wk[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int n = t + T * e;
+    wu[e] = (act && (CIRC || n < L0)) ? col[n * TLP] : czero();
+  }
+  BlockFFT<P0, E, false>::run(wu, t, sc, act);
+  __syncthreads();  // every lane is done with U's tile
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const int i = tid + NT * j;
+    if (i < L0 * TL) tile[(i / TL) * TLP + (i % TL)] = kreg[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int n = t + T * e;
+    wk[e] = (act && (CIRC || n < L0)) ? col[n * TLP] : czero();
+  }
+  BlockFFT<P0, E, false>::run(wk, t, sc, act);
+#pragma unroll
+  for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
+  if constexpr (T == 1) __syncthreads();
+  BlockFFT<P0, E, true>::run(wu, t, sc, act);
+  if (act) {
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int n = t + T * e;
-      const bool nz = act && (CIRC || n < L0);
-      wu[e] = nz ? cu[n * TLP] : czero();
-      wk[e] = nz ? ck[n * TLP] : czero();
-    }
-    BlockFFT<P0, E, false>::run(wu, t, ScrStrided{cu, TLP}, act);
-    BlockFFT<P0, E, false>::run(wk, t, ScrStrided{ck, TLP}, act);
-#pragma unroll
-    for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
-    BlockFFT<P0, E, true>::run(wu, t, ScrStrided{cu, TLP}, act);
-    if (act) {
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int n = t + T * e;
-        if (CIRC || n < L0) cu[n * TLP] = wu[e];
-      }
+      if (CIRC || n < L0) col[n * TLP] = wu[e];
     }
   }
   __syncthreads();
-  tile_store<P0, TLP>(tile[0], U, ncols, col0, ncols, L0, TL, tid, NT);
+  tile_store<TLP>(tile, U, ncols, col0, ncols, HS, H, L0, TL, tid, NT);
 }
 
 // ---------------------------------------------------------------------------
@@ -326,7 +366,7 @@ struct RowsInvCfg {
 template <int PL, bool CIRC, typename TS>
 __global__ void __launch_bounds__(256)
     mp_rows_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0,
-                int nlines, int rows, int L1, int P1, int64_t per_line) {
+                int nlines, int rows, int L1, int P1, int HS, int64_t per_line) {
   using Cf = RowsInvCfg<PL>;
   constexpr int H = Cf::H, PRP = Cf::PRP, E = Cf::E, T = Cf::T, NT = Cf::NT, PPW = Cf::PPW;
   constexpr int LL = CIRC ? PL : PL / 2;
@@ -344,14 +384,14 @@ __global__ void __launch_bounds__(256)
     const int64_t gr = 2 * (pair0 + q) + ab;
     const int64_t line = gr / rows;
     const int rr = (int)(gr - line * rows);
-    reg[q * PRP + rem] = ws[line * per_line + ws_row(rr, L1, P1, H) + f];
+    reg[q * PRP + rem] = ws[line * per_line + ws_row(rr, L1, P1, HS) + f];
   }
   __syncthreads();
 
   for (int q0 = 0; q0 < PPW; q0 += NT / T) {
     const int q = q0 + tid % (NT / T), t = tid / (NT / T);
     const bool act = q < npair;
-    float2* R = reg + (q < PPW ? q : 0) * PRP;
+    float2* R = reg + (act ? q : 0) * PRP;
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -380,11 +420,27 @@ __global__ void __launch_bounds__(256)
   }
   __syncthreads();
 
+  // gate and store; the rows of a pair are consecutive in y, 4 values per access
   const size_t gbase = (size_t)(line0 * rows + 2 * pair0) * LL;
-  for (int i = tid; i < npair * 2 * LL; i += NT) {
-    const int row = i / LL, n = i - row * LL;
-    const float2 qv = reg[(row >> 1) * PRP + n];
-    st1(y + gbase + i, ld1(x2 + gbase + i) * ((row & 1) ? qv.y : qv.x));
+  if constexpr (LL % 4 == 0) {
+    for (int i4 = tid; i4 < npair * 2 * (LL / 4); i4 += NT) {
+      const int i = 4 * i4;
+      const int row = i / LL, n = i - row * LL;
+      const float2* R = reg + (row >> 1) * PRP + n;
+      const float4 g = ld4(x2 + gbase + i);
+      float4 o;
+      if (row & 1)
+        o = make_float4(g.x * R[0].y, g.y * R[1].y, g.z * R[2].y, g.w * R[3].y);
+      else
+        o = make_float4(g.x * R[0].x, g.y * R[1].x, g.z * R[2].x, g.w * R[3].x);
+      st4(y + gbase + i, o);
+    }
+  } else {
+    for (int i = tid; i < npair * 2 * LL; i += NT) {
+      const int row = i / LL, n = i - row * LL;
+      const float2 qv = reg[(row >> 1) * PRP + n];
+      st1(y + gbase + i, ld1(x2 + gbase + i) * ((row & 1) ? qv.y : qv.x));
+    }
   }
 }
 
@@ -408,7 +464,7 @@ hipError_t rows_fwd(const MpLaunch& L) {
   const dim3 grid((unsigned)((total + RowsCfg<PL>::RPW - 1) / RowsCfg<PL>::RPW));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, \
-                    L.g.half, L.per
+                    L.g.HS, L.g.half, L.per
   if (a.bf16) {
     if (a.circular) hipLaunchKernelGGL((mp_rows_fwd<PL, true, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
     else hipLaunchKernelGGL((mp_rows_fwd<PL, false, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
@@ -426,9 +482,11 @@ hipError_t axis1(const MpLaunch& L) {
   const int ntile = (L.g.H + TL - 1) / TL;
   const dim3 grid((unsigned)((int64_t)L.nl * L.g.L0 * ntile));
   if (L.a->circular)
-    hipLaunchKernelGGL((mp_axis1<P1, true, INV>), grid, dim3(512), 0, L.s, L.ws, L.g.H, L.g.L0, L.g.half, L.per);
+    hipLaunchKernelGGL((mp_axis1<P1, true, INV>), grid, dim3(512), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
+                       L.per);
   else
-    hipLaunchKernelGGL((mp_axis1<P1, false, INV>), grid, dim3(512), 0, L.s, L.ws, L.g.H, L.g.L0, L.g.half, L.per);
+    hipLaunchKernelGGL((mp_axis1<P1, false, INV>), grid, dim3(512), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
+                       L.per);
   return hipGetLastError();
 }
 template <int P1>
@@ -438,17 +496,19 @@ hipError_t axis1_inv(const MpLaunch& L) { return axis1<P1, true>(L); }
 
 template <int P0>
 hipError_t core(const MpLaunch& L) {
-  constexpr int TL = CoreCfg<P0>::TL;
-  const int ncols = L.g.P1 * L.g.H;
-  const int ntile = (ncols + TL - 1) / TL;
-  const dim3 grid((unsigned)((int64_t)L.nl * ntile));
   const FftConvArgs& a = *L.a;
-  if (a.circular)
+  const int ncols = L.g.P1 * L.g.HS;
+  if (a.circular) {
+    constexpr int TL = CoreCfg<P0, true>::TL;
+    const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
     hipLaunchKernelGGL((mp_core<P0, true>), grid, dim3(512), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
-                       ncols, L.g.half, L.per, L.scale);
-  else
+                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale);
+  } else {
+    constexpr int TL = CoreCfg<P0, false>::TL;
+    const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
     hipLaunchKernelGGL((mp_core<P0, false>), grid, dim3(512), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
-                       ncols, L.g.half, L.per, L.scale);
+                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale);
+  }
   return hipGetLastError();
 }
 
@@ -457,7 +517,7 @@ hipError_t rows_inv(const MpLaunch& L) {
   const int64_t pairs = (int64_t)L.nl * L.g.rows / 2;
   const dim3 grid((unsigned)((pairs + RowsInvCfg<PL>::PPW - 1) / RowsInvCfg<PL>::PPW));
   const FftConvArgs& a = *L.a;
-#define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, L.per
+#define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, L.g.HS, L.per
   if (a.bf16) {
     if (a.circular) hipLaunchKernelGGL((mp_rows_inv<PL, true, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
     else hipLaunchKernelGGL((mp_rows_inv<PL, false, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));

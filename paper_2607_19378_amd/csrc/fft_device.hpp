@@ -84,6 +84,16 @@ __device__ __forceinline__ float2 twiddle_rt(uint32_t m, int log2n) {
   return INV ? c_conj(w) : w;
 }
 
+// Stockham pass twiddle exp(-+2 pi i jm r / (NS R)) from the [r-1][jm] table
+// of that pass shape: lanes with consecutive jm read consecutive entries.
+template <int NS, int R, bool INV>
+__device__ __forceinline__ float2 pass_twiddle(uint32_t jm, int r) {
+  static_assert(NS >= 2 && R >= 2 && R <= 16 && NS * R <= 8192, "pass table range");
+  constexpr int off = kPassOff[ilog2(NS)][ilog2(R)];
+  const float2 w = kPassTw[off + (r - 1) * NS + (int)jm];
+  return INV ? c_conj(w) : w;
+}
+
 // a * exp(-+2 pi i n / R) with n a compile-time constant after unrolling.
 template <int R, bool INV>
 __device__ __forceinline__ float2 mul_root(float2 a, int n) {
@@ -179,7 +189,6 @@ struct BlockFFT {
   static __device__ __forceinline__ void pass(float2 (&v)[E], int t, const Scr& scr, bool active) {
     constexpr int R = (N / NS >= E) ? E : N / NS;
     constexpr int NB = E / R;  // butterflies per lane in this pass
-    constexpr int LOGW = ilog2(NS * R);
     if (active) {  // waves with no active lane skip the arithmetic
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
@@ -189,7 +198,7 @@ struct BlockFFT {
         if constexpr (NS > 1) {
           const uint32_t jm = (uint32_t)(t + T * b) & (NS - 1);
 #pragma unroll
-          for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], twiddle<LOGW, INV>(jm * r));
+          for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], pass_twiddle<NS, R, INV>(jm, r));
         }
         dft<R, INV>(x);
 #pragma unroll
@@ -231,6 +240,20 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
 }
 __device__ __forceinline__ void st1(float* p, float x) { *p = x; }
 __device__ __forceinline__ void st1(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
+// four consecutive values (p aligned to four elements)
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 ld4(const uint16_t* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+__device__ __forceinline__ void st4(float* p, float4 x) { *reinterpret_cast<float4*>(p) = x; }
+__device__ __forceinline__ void st4(uint16_t* p, float4 x) {
+  uint2 u;
+  u.x = (uint32_t)f32_to_bf16_rne(x.x) | ((uint32_t)f32_to_bf16_rne(x.y) << 16);
+  u.y = (uint32_t)f32_to_bf16_rne(x.z) | ((uint32_t)f32_to_bf16_rne(x.w) << 16);
+  *reinterpret_cast<uint2*>(p) = u;
+}
 // two consecutive values (p must be aligned to two elements)
 __device__ __forceinline__ float2 ld2(const float* p) { return *reinterpret_cast<const float2*>(p); }
 __device__ __forceinline__ float2 ld2(const uint16_t* p) {

@@ -168,6 +168,17 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
   if (st != HYENAND_OK) return st;
   if (!x1 || !x2 || !v || !k || !D || !y)
     return fail(HYENAND_ERR_INVALID_ARGUMENT, "a tensor pointer is NULL");
+  {
+    const void* tens[5] = {x1, x2, v, k, y};
+    const char* tn[5] = {"x1", "x2", "v", "k", "y"};
+    for (int i = 0; i < 5; ++i)
+      if ((uintptr_t)tens[i] % 16 != 0)
+        return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", tn[i]);
+    if ((uintptr_t)D % (dtype == HYENAND_DTYPE_BF16 ? 2 : 4) != 0)
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "D is not aligned to its element size");
+    if (workspace && (uintptr_t)workspace % 16 != 0)
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace is not 16-byte aligned");
+  }
   const size_t es = a.bf16 ? 2 : 4;
   size_t n = (size_t)a.lines;
   for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];

@@ -73,8 +73,16 @@ def test_aliasing_rejected(L):
                                      base + 2 * n + 16]) == H.ERR_INVALID_ARGUMENT
     assert b"y overlaps x2" in L.hyenand_last_error()
     assert call(L, (2, 3, 64), ptrs=[base, base + 2 * n, base + 4 * n, base + 6 * n, base + 10 * n,
-                                     base + 10 * n - 4]) == H.ERR_INVALID_ARGUMENT
+                                     base + 10 * n - 16]) == H.ERR_INVALID_ARGUMENT
     assert b"y overlaps D" in L.hyenand_last_error()
+
+
+def test_unaligned_pointer_rejected(L):
+    base = FAKE
+    n = 1 * 2 * 64 * 4
+    ptrs = [base + 4, base + 2 * n, base + 4 * n, base + 6 * n, base + 8 * n, base + 10 * n]
+    assert call(L, (1, 2, 64), ptrs=ptrs) == H.ERR_INVALID_ARGUMENT
+    assert b"x1 is not 16-byte aligned" in L.hyenand_last_error()
 
 
 def test_workspace_queries_are_host_only():
