@@ -75,18 +75,18 @@ __global__ void __launch_bounds__(512)
   const size_t gbase = (size_t)(line0 + line) * L;
   const int tid = threadIdx.x;
 
-  for (int i = tid; i < NZ * TL; i += NT) {
-    const int m1 = i / TL, cc = i - m1 * TL;
-    const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
-    float2 z;
-    if (sig == 0) {
-      const float2 a = ld2(x1 + n), b = ld2(v + n);
-      z = make_float2(a.x * b.x, a.y * b.y);
-    } else {
-      z = ld2(k + n);
-    }
-    tile[m1 * TLP + cc] = z;
-  }
+  batched_copy<NZ * TL, NT, 8>(
+      tid,
+      [&](int i) {
+        const int m1 = i / TL, cc = i - m1 * TL;
+        const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
+        if (sig == 0) {
+          const float2 a = ld2(x1 + n), b = ld2(v + n);
+          return make_float2(a.x * b.x, a.y * b.y);
+        }
+        return ld2(k + n);
+      },
+      [&](int i, float2 z) { tile[(i / TL) * TLP + (i % TL)] = z; });
   __syncthreads();
 
   for (int l0 = 0; l0 < TL; l0 += NT / T) {
@@ -99,7 +99,7 @@ __global__ void __launch_bounds__(512)
       const int m1 = t + T * e;
       w[e] = (act && (CIRC || m1 < NZ)) ? col[m1 * TLP] : czero();
     }
-    BlockFFT<N1, E, false>::run(w, t, ScrStrided{col, TLP}, act);
+    BlockFFT<N1, E, false>::run(w, t, ScrS<TLP>{col}, act);
     if (act) {
       // exp(-2 pi i m2 f1 / M) for f1 = t + T e
       const uint32_t m2 = (uint32_t)(c0 + cc);
@@ -111,10 +111,9 @@ __global__ void __launch_bounds__(512)
   __syncthreads();
 
   float2* A = ws + line * per_line + (sig ? M : 0);
-  for (int i = tid; i < N1 * TL; i += NT) {
-    const int f1 = i / TL, cc = i - f1 * TL;
-    A[(size_t)f1 * N2 + c0 + cc] = tile[f1 * TLP + cc];
-  }
+  batched_copy<N1 * TL, NT, 8>(
+      tid, [&](int i) { return tile[(i / TL) * TLP + (i % TL)]; },
+      [&](int i, float2 z) { A[(size_t)(i / TL) * N2 + c0 + (i % TL)] = z; });
 }
 
 template <bool CIRC>
@@ -140,14 +139,18 @@ __global__ void __launch_bounds__(512)
   const float2 om_a = twiddle_rt<false>((uint32_t)fa, log2M + 1);
   // slots: 0 = u row fa, 1 = u row fb, 2 = k row fa, 3 = k row fb (a single
   // self-mirrored row uses slots 0 and 2 only)
-  for (int i = tid; i < 4 * N2; i += NT) {
-    const int sl = i / N2, f2 = i - sl * N2;
-    if (!single || (sl & 1) == 0) {
-      const ScrPad16 sc{R[sl]};
-      const int64_t row = (sl & 1) ? fb : fa;
-      *sc(f2) = A[((sl >> 1) ? M : 0) + row * N2 + f2];
-    }
-  }
+  batched_copy<4 * N2, NT, 8>(
+      tid,
+      [&](int i) {
+        const int sl = i / N2, f2 = i - sl * N2;
+        float2 z = czero();
+        if (!single || (sl & 1) == 0) z = A[((sl >> 1) ? M : 0) + (int64_t)((sl & 1) ? fb : fa) * N2 + f2];
+        return z;
+      },
+      [&](int i, float2 z) {
+        const int sl = i / N2, f2 = i - sl * N2;
+        *ScrPad16{R[sl]}(f2) = z;
+      });
   __syncthreads();
 
   // forward transforms over m2 (lanes run along each row)
@@ -230,10 +233,9 @@ __global__ void __launch_bounds__(512)
   const float2* B = ws + line * per_line;
   const int tid = threadIdx.x;
 
-  for (int i = tid; i < N1 * TL; i += NT) {
-    const int f1 = i / TL, cc = i - f1 * TL;
-    tile[f1 * TLP + cc] = B[(int64_t)f1 * N2 + c0 + cc];
-  }
+  batched_copy<N1 * TL, NT, 8>(
+      tid, [&](int i) { return B[(int64_t)(i / TL) * N2 + c0 + (i % TL)]; },
+      [&](int i, float2 z) { tile[(i / TL) * TLP + (i % TL)] = z; });
   __syncthreads();
 
   for (int l0 = 0; l0 < TL; l0 += NT / T) {
@@ -243,7 +245,7 @@ __global__ void __launch_bounds__(512)
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) w[e] = act ? col[(t + T * e) * TLP] : czero();
-    BlockFFT<N1, E, true>::run(w, t, ScrStrided{col, TLP}, act);
+    BlockFFT<N1, E, true>::run(w, t, ScrS<TLP>{col}, act);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {
@@ -255,13 +257,12 @@ __global__ void __launch_bounds__(512)
   __syncthreads();
 
   const size_t gbase = (size_t)(line0 + line) * L;
-  for (int i = tid; i < NOUT * TL; i += NT) {
-    const int m1 = i / TL, cc = i - m1 * TL;
-    const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
-    const float2 q = tile[m1 * TLP + cc];
-    const float2 g = ld2(x2 + n);
-    st2(y + n, make_float2(g.x * q.x, g.y * q.y));
-  }
+  batched_copy<NOUT * TL, NT, 8>(
+      tid, [&](int i) { return ld2(x2 + gbase + 2 * ((size_t)(i / TL) * N2 + c0 + (i % TL))); },
+      [&](int i, float2 g) {
+        const float2 q = tile[(i / TL) * TLP + (i % TL)];
+        st2(y + gbase + 2 * ((size_t)(i / TL) * N2 + c0 + (i % TL)), make_float2(g.x * q.x, g.y * q.y));
+      });
 }
 
 struct FsLaunch {

@@ -54,13 +54,20 @@ __global__ void __launch_bounds__(fused1d_nt(P))
   const int tid = threadIdx.x;
 
   // stage the even/odd packed real lines u = x1 v and k
-  for (int m = tid; m < MNZ; m += NT) {
-    const int n = 2 * m;
-    const bool two = n + 1 < L;
-    const float u0 = ld1(x1 + base + n) * ld1(v + base + n);
-    const float u1 = two ? ld1(x1 + base + n + 1) * ld1(v + base + n + 1) : 0.f;
-    Ub[m + (m >> 4)] = make_float2(u0, u1);
-    Kb[m + (m >> 4)] = make_float2(ld1(k + base + n), two ? ld1(k + base + n + 1) : 0.f);
+  if constexpr (L >= 2) {
+    batched_copy<MNZ, NT, 8>(
+        tid,
+        [&](int m) {
+          const float2 a = ld2(x1 + base + 2 * m), b = ld2(v + base + 2 * m), kk = ld2(k + base + 2 * m);
+          return make_float4(a.x * b.x, a.y * b.y, kk.x, kk.y);
+        },
+        [&](int m, float4 z) {
+          Ub[m + (m >> 4)] = make_float2(z.x, z.y);
+          Kb[m + (m >> 4)] = make_float2(z.z, z.w);
+        });
+  } else if (tid == 0) {  // a single sample
+    Ub[0] = make_float2(ld1(x1 + base) * ld1(v + base), 0.f);
+    Kb[0] = make_float2(ld1(k + base), 0.f);
   }
   __syncthreads();
 
@@ -205,8 +212,11 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
                  const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C) {
   using F = Fused2D<P0, P1, CIRC, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
-  __shared__ float2 Uh[L0 * RP];
-  __shared__ float2 Kh[L0 * RP];
+  // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
+  // line of 2 L0 >= P0 slots, the exchange scratch of that column's transforms
+  __shared__ float2 UK[2 * L0 * RP];
+  float2* const Uh = UK;
+  float2* const Kh = UK + L0 * RP;
   const int img = blockIdx.x;
   const int c = img % C;
   const size_t base = (size_t)img * L0 * L1;
@@ -217,11 +227,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   {
     float* uf = reinterpret_cast<float*>(Uh);
     float* kf = reinterpret_cast<float*>(Kh);
-    for (int i = tid; i < L0 * L1; i += NT) {
-      const int r = i / L1, col = i - r * L1;
-      uf[r * 2 * RP + col] = ld1(x1 + base + i) * ld1(v + base + i);
-      kf[r * 2 * RP + col] = ld1(k + base + i);
-    }
+    batched_copy<L0 * L1, NT, 8>(
+        tid, [&](int i) { return make_float2(ld1(x1 + base + i) * ld1(v + base + i), ld1(k + base + i)); },
+        [&](int i, float2 z) {
+          const int r = i / L1, col = i - r * L1;
+          uf[r * 2 * RP + col] = z.x;
+          kf[r * 2 * RP + col] = z.y;
+        });
   }
   __syncthreads();
 
@@ -238,7 +250,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         const int m = t + T * e;
         w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
       }
-      BlockFFT<M1, E, false>::run(w, t, ScrStrided{row, 1}, act);
+      BlockFFT<M1, E, false>::run(w, t, ScrS<1>{row}, act);
       if (act) {
 #pragma unroll
         for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
@@ -287,11 +299,11 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
           }
         }
       }
-      const ScrSplit su{Uh + col, Kh + col, L0, RP};
+      const ScrS<RP> su{UK + col};
       BlockFFT<P0, E, false>::run(wu, t, su, act);
       BlockFFT<P0, E, false>::run(wk, t, su, act);
       // group 0: publish both spectra so the mirror bins can be read
-      const ScrSplit sk0{CIRC ? Kh : Uh + M1, CIRC ? Kh : Kh + M1, L0, RP};
+      const ScrS<RP> sk0{CIRC ? Kh : UK + M1};
       __syncthreads();
       if (nyq) {
 #pragma unroll
@@ -367,7 +379,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
       }
       if constexpr (T == 1) __syncthreads();
-      BlockFFT<P1, E, true>::run(w, t, ScrStrided{ra, 1}, act);
+      BlockFFT<P1, E, true>::run(w, t, ScrS<1>{ra}, act);
       if (act) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -380,11 +392,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   __syncthreads();
 
   // 4. outer gate and store (coalesced along rows)
-  for (int i = tid; i < L0 * L1; i += NT) {
-    const int r = i / L1, col = i - r * L1;
-    const float2 q = Uh[(r & ~1) * RP + col];
-    st1(y + base + i, ld1(x2 + base + i) * ((r & 1) ? q.y : q.x));
-  }
+  batched_copy<L0 * L1, NT, 8>(
+      tid, [&](int i) { return ld1(x2 + base + i); },
+      [&](int i, float g) {
+        const int r = i / L1, col = i - r * L1;
+        const float2 q = Uh[(r & ~1) * RP + col];
+        st1(y + base + i, g * ((r & 1) ? q.y : q.x));
+      });
 }
 
 template <int P0, int P1, bool CIRC, typename TS>

@@ -88,33 +88,55 @@ __global__ void __launch_bounds__(256)
   const int nrow = (int)((total_rows - row0) < RPW ? (total_rows - row0) : RPW);
   const int tid = threadIdx.x;
 
-  // stage real rows (the input rows of the chunk are contiguous), 4 per load
+  // stage real rows (the input rows of the chunk are contiguous), four
+  // samples per global load, written to LDS as two 8-byte pairs
   {
-    float* uf = reinterpret_cast<float*>(Ur);
-    float* kf = reinterpret_cast<float*>(Kr);
     const size_t gbase = (size_t)(line0 * rows + row0) * LL;
     if constexpr (LL % 4 == 0) {
-      for (int i4 = tid; i4 < nrow * (LL / 4); i4 += NT) {
-        const int i = 4 * i4;
-        const int r = i / LL, col = i - r * LL;
-        const float4 a = ld4(x1 + gbase + i), b = ld4(v + gbase + i), kk = ld4(k + gbase + i);
-        float* du = uf + r * 2 * HP + col;
-        float* dk = kf + r * 2 * HP + col;
-        du[0] = a.x * b.x;
-        du[1] = a.y * b.y;
-        du[2] = a.z * b.z;
-        du[3] = a.w * b.w;
-        dk[0] = kk.x;
-        dk[1] = kk.y;
-        dk[2] = kk.z;
-        dk[3] = kk.w;
-      }
+      struct In3 {
+        float4 a, b, k;
+      };
+      batched_copy<RPW * (LL / 4), NT, 4>(
+          tid,
+          [&](int i4) {
+            In3 z;
+            const int i = 4 * i4;
+            if (i / LL < nrow) {
+              z.a = ld4(x1 + gbase + i);
+              z.b = ld4(v + gbase + i);
+              z.k = ld4(k + gbase + i);
+            }
+            return z;
+          },
+          [&](int i4, const In3& z) {
+            const int i = 4 * i4;
+            const int r = i / LL, col = i - r * LL;
+            if (r < nrow) {
+              float2* du = Ur + r * HP + col / 2;
+              float2* dk = Kr + r * HP + col / 2;
+              du[0] = make_float2(z.a.x * z.b.x, z.a.y * z.b.y);
+              du[1] = make_float2(z.a.z * z.b.z, z.a.w * z.b.w);
+              dk[0] = make_float2(z.k.x, z.k.y);
+              dk[1] = make_float2(z.k.z, z.k.w);
+            }
+          });
     } else {
-      for (int i = tid; i < nrow * LL; i += NT) {
-        const int r = i / LL, col = i - r * LL;
-        uf[r * 2 * HP + col] = ld1(x1 + gbase + i) * ld1(v + gbase + i);
-        kf[r * 2 * HP + col] = ld1(k + gbase + i);
-      }
+      float* uf = reinterpret_cast<float*>(Ur);
+      float* kf = reinterpret_cast<float*>(Kr);
+      batched_copy<RPW * LL, NT, 8>(
+          tid,
+          [&](int i) {
+            float2 z = czero();
+            if (i / LL < nrow) z = make_float2(ld1(x1 + gbase + i) * ld1(v + gbase + i), ld1(k + gbase + i));
+            return z;
+          },
+          [&](int i, float2 z) {
+            const int r = i / LL, col = i - r * LL;
+            if (r < nrow) {
+              uf[r * 2 * HP + col] = z.x;
+              kf[r * 2 * HP + col] = z.y;
+            }
+          });
     }
   }
   __syncthreads();
@@ -132,7 +154,7 @@ __global__ void __launch_bounds__(256)
       const int m = t + T * e;
       w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
     }
-    BlockFFT<ML, E, false>::run(w, t, ScrStrided{row, 1}, act);
+    BlockFFT<ML, E, false>::run(w, t, ScrS<1>{row}, act);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
@@ -156,16 +178,24 @@ __global__ void __launch_bounds__(256)
   __syncthreads();
 
   // store the H bins of every row to U and K (rows start on cache lines)
-  for (int i = tid; i < nrow * H; i += NT) {
-    const int r = i / H, f = i - r * H;
-    const int64_t gr = row0 + r;
-    const int64_t line = gr / rows;
-    const int rr = (int)(gr - line * rows);
-    float2* U = ws + line * per_line;
-    const int64_t off = ws_row(rr, L1, P1, HS) + f;
-    U[off] = Ur[r * HP + f];
-    U[half + off] = Kr[r * HP + f];
-  }
+  batched_copy<RPW * H, NT, 8>(
+      tid,
+      [&](int i) {
+        const int r = i / H, f = i - r * H;
+        return make_float4(Ur[r * HP + f].x, Ur[r * HP + f].y, Kr[r * HP + f].x, Kr[r * HP + f].y);
+      },
+      [&](int i, float4 z) {
+        const int r = i / H, f = i - r * H;
+        if (r < nrow) {
+          const int64_t gr = row0 + r;
+          const int64_t line = gr / rows;
+          const int rr = (int)(gr - line * rows);
+          float2* U = ws + line * per_line;
+          const int64_t off = ws_row(rr, L1, P1, HS) + f;
+          U[off] = make_float2(z.x, z.y);
+          U[half + off] = make_float2(z.z, z.w);
+        }
+      });
 }
 
 // ---------------------------------------------------------------------------
@@ -193,22 +223,33 @@ __device__ __forceinline__ bool col_valid(int col, int ncols, int HS, int H) {
   return col < ncols && (col % HS) < H;
 }
 
-template <int TLP>
+// Each lane always handles the same column cc = tid % TL (NT is a multiple
+// of TL), so the column test runs once per lane; rows are copied in batches
+// with all loads of a batch in flight together.
+template <int NROWS, int TL, int TLP, int NT>
 __device__ __forceinline__ void tile_load(float2* tile, const float2* __restrict__ src, int64_t stride, int col0,
-                                          int ncols, int HS, int H, int nrows, int TL, int tid, int nt) {
-  for (int i = tid; i < nrows * TL; i += nt) {
-    const int p = i / TL, cc = i - p * TL;
-    if (col_valid(col0 + cc, ncols, HS, H)) tile[p * TLP + cc] = src[p * stride + col0 + cc];
-  }
+                                          int ncols, int HS, int H, int tid) {
+  static_assert(NT % TL == 0, "lanes keep their column");
+  const int cc = tid % TL;
+  const bool ok = col_valid(col0 + cc, ncols, HS, H);
+  const float2* s = src + col0 + cc;
+  batched_copy<NROWS * TL, NT, 8>(
+      tid, [&](int i) { return ok ? s[(int64_t)(i / TL) * stride] : czero(); },
+      [&](int i, float2 z) { tile[(i / TL) * TLP + cc] = z; });
 }
 
-template <int TLP>
+template <int NROWS, int TL, int TLP, int NT>
 __device__ __forceinline__ void tile_store(const float2* tile, float2* __restrict__ dst, int64_t stride, int col0,
-                                           int ncols, int HS, int H, int nrows, int TL, int tid, int nt) {
-  for (int i = tid; i < nrows * TL; i += nt) {
-    const int p = i / TL, cc = i - p * TL;
-    if (col_valid(col0 + cc, ncols, HS, H)) dst[p * stride + col0 + cc] = tile[p * TLP + cc];
-  }
+                                           int ncols, int HS, int H, int tid) {
+  static_assert(NT % TL == 0, "lanes keep their column");
+  const int cc = tid % TL;
+  const bool ok = col_valid(col0 + cc, ncols, HS, H);
+  float2* d = dst + col0 + cc;
+  batched_copy<NROWS * TL, NT, 8>(
+      tid, [&](int i) { return tile[(i / TL) * TLP + cc]; },
+      [&](int i, float2 z) {
+        if (ok) d[(int64_t)(i / TL) * stride] = z;
+      });
 }
 
 // ---------------------------------------------------------------------------
@@ -234,9 +275,9 @@ __global__ void __launch_bounds__(512)
   const int tid = threadIdx.x;
   float2* base = ws + line * per_line + (int64_t)n0 * P1 * HS;
 
-  const int nload = INV ? P1 : L1;
+  constexpr int NLOAD = INV ? P1 : L1;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) tile_load<TLP>(tile[s], base + s * half, HS, col0, H, HS, H, nload, TL, tid, NT);
+  for (int s = 0; s < NS; ++s) tile_load<NLOAD, TL, TLP, NT>(tile[s], base + s * half, HS, col0, H, HS, H, tid);
   __syncthreads();
 
   constexpr int NL = NS * TL;
@@ -251,16 +292,16 @@ __global__ void __launch_bounds__(512)
       const int n = t + T * e;
       w[e] = (act && (INV || CIRC || n < L1)) ? col[n * TLP] : czero();
     }
-    BlockFFT<P1, E, INV>::run(w, t, ScrStrided{col, TLP}, act);
+    BlockFFT<P1, E, INV>::run(w, t, ScrS<TLP>{col}, act);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) col[(t + T * e) * TLP] = w[e];
     }
   }
   __syncthreads();
-  const int nstore = INV ? L1 : P1;
+  constexpr int NSTORE = INV ? L1 : P1;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) tile_store<TLP>(tile[s], base + s * half, HS, col0, H, HS, H, nstore, TL, tid, NT);
+  for (int s = 0; s < NS; ++s) tile_store<NSTORE, TL, TLP, NT>(tile[s], base + s * half, HS, col0, H, HS, H, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -299,21 +340,25 @@ __global__ void __launch_bounds__(512)
   const float2* K = U + half;
 
   // K's tile into registers, U's tile into LDS
+  static_assert(NT % TL == 0, "lanes keep their column");
   float2 kreg[KPT];
+  {
+    const bool kv = col_valid(col0 + tid % TL, ncols, HS, H);
+    const float2* ks = K + col0 + tid % TL;
 #pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    const int i = tid + NT * j;
-    const int p = i / TL, cc = i - p * TL;
-    kreg[j] = (i < L0 * TL && col_valid(col0 + cc, ncols, HS, H)) ? K[(int64_t)p * ncols + col0 + cc] : czero();
+    for (int j = 0; j < KPT; ++j) {
+      const int p = tid / TL + (NT / TL) * j;
+      kreg[j] = (kv && p < L0) ? ks[(int64_t)p * ncols] : czero();
+    }
   }
-  tile_load<TLP>(tile, U, ncols, col0, ncols, HS, H, L0, TL, tid, NT);
+  tile_load<L0, TL, TLP, NT>(tile, U, ncols, col0, ncols, HS, H, tid);
   __syncthreads();
 
   static_assert(NT / T >= TL, "one round of columns");
   const int cc = tid % TL, t = tid / TL;
   const bool act = t < T;
   float2* col = tile + cc;
-  const ScrStrided sc{col, TLP};
+  const ScrS<TLP> sc{col};
   float2 wu[E], wk[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
@@ -324,8 +369,8 @@ __global__ void __launch_bounds__(512)
   __syncthreads();  // every lane is done with U's tile
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
-    const int i = tid + NT * j;
-    if (i < L0 * TL) tile[(i / TL) * TLP + (i % TL)] = kreg[j];
+    const int p = tid / TL + (NT / TL) * j;
+    if (p < L0) tile[p * TLP + tid % TL] = kreg[j];
   }
   __syncthreads();
 #pragma unroll
@@ -346,7 +391,7 @@ __global__ void __launch_bounds__(512)
     }
   }
   __syncthreads();
-  tile_store<TLP>(tile, U, ncols, col0, ncols, HS, H, L0, TL, tid, NT);
+  tile_store<L0, TL, TLP, NT>(tile, U, ncols, col0, ncols, HS, H, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -356,7 +401,7 @@ __global__ void __launch_bounds__(512)
 template <int PL>
 struct RowsInvCfg {
   static constexpr int H = PL / 2 + 1;
-  static constexpr int PRP = PL + 17;  // pair region pitch (holds 2H and the scratch)
+  static constexpr int PRP = PL + 18;  // pair region pitch (holds 2H and the scratch; = 2 mod 16)
   static constexpr int E = imin(16, PL);
   static constexpr int T = PL / E;
   static constexpr int NT = 256;
@@ -378,14 +423,24 @@ __global__ void __launch_bounds__(256)
   const int tid = threadIdx.x;
 
   // load the half-spectrum rows of each pair: row a at [0, H), row b at [H, 2H)
-  for (int i = tid; i < npair * 2 * H; i += NT) {
-    const int q = i / (2 * H), rem = i - q * 2 * H;
-    const int ab = rem / H, f = rem - ab * H;
-    const int64_t gr = 2 * (pair0 + q) + ab;
-    const int64_t line = gr / rows;
-    const int rr = (int)(gr - line * rows);
-    reg[q * PRP + rem] = ws[line * per_line + ws_row(rr, L1, P1, HS) + f];
-  }
+  batched_copy<PPW * 2 * H, NT, 8>(
+      tid,
+      [&](int i) {
+        const int q = i / (2 * H), rem = i - q * 2 * H;
+        const int ab = rem / H, f = rem - ab * H;
+        float2 z = czero();
+        if (q < npair) {
+          const int64_t gr = 2 * (pair0 + q) + ab;
+          const int64_t line = gr / rows;
+          const int rr = (int)(gr - line * rows);
+          z = ws[line * per_line + ws_row(rr, L1, P1, HS) + f];
+        }
+        return z;
+      },
+      [&](int i, float2 z) {
+        const int q = i / (2 * H);
+        reg[q * PRP + (i - q * 2 * H)] = z;
+      });
   __syncthreads();
 
   for (int q0 = 0; q0 < PPW; q0 += NT / T) {
@@ -409,7 +464,7 @@ __global__ void __launch_bounds__(256)
       w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
     }
     if constexpr (T == 1) __syncthreads();
-    BlockFFT<PL, E, true>::run(w, t, ScrStrided{R, 1}, act);
+    BlockFFT<PL, E, true>::run(w, t, ScrS<1>{R}, act);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {
@@ -423,18 +478,25 @@ __global__ void __launch_bounds__(256)
   // gate and store; the rows of a pair are consecutive in y, 4 values per access
   const size_t gbase = (size_t)(line0 * rows + 2 * pair0) * LL;
   if constexpr (LL % 4 == 0) {
-    for (int i4 = tid; i4 < npair * 2 * (LL / 4); i4 += NT) {
-      const int i = 4 * i4;
-      const int row = i / LL, n = i - row * LL;
-      const float2* R = reg + (row >> 1) * PRP + n;
-      const float4 g = ld4(x2 + gbase + i);
-      float4 o;
-      if (row & 1)
-        o = make_float4(g.x * R[0].y, g.y * R[1].y, g.z * R[2].y, g.w * R[3].y);
-      else
-        o = make_float4(g.x * R[0].x, g.y * R[1].x, g.z * R[2].x, g.w * R[3].x);
-      st4(y + gbase + i, o);
-    }
+    batched_copy<PPW * 2 * (LL / 4), NT, 8>(
+        tid,
+        [&](int i4) {
+          const int i = 4 * i4;
+          return (i / LL) < 2 * npair ? ld4(x2 + gbase + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+        },
+        [&](int i4, float4 g) {
+          const int i = 4 * i4;
+          const int row = i / LL, n = i - row * LL;
+          if (row < 2 * npair) {
+            const float2* R = reg + (row >> 1) * PRP + n;
+            float4 o;
+            if (row & 1)
+              o = make_float4(g.x * R[0].y, g.y * R[1].y, g.z * R[2].y, g.w * R[3].y);
+            else
+              o = make_float4(g.x * R[0].x, g.y * R[1].x, g.z * R[2].x, g.w * R[3].x);
+            st4(y + gbase + i, o);
+          }
+        });
   } else {
     for (int i = tid; i < npair * 2 * LL; i += NT) {
       const int row = i / LL, n = i - row * LL;

@@ -89,8 +89,8 @@ __device__ __forceinline__ float2 twiddle_rt(uint32_t m, int log2n) {
 template <int NS, int R, bool INV>
 __device__ __forceinline__ float2 pass_twiddle(uint32_t jm, int r) {
   static_assert(NS >= 2 && R >= 2 && R <= 16 && NS * R <= 8192, "pass table range");
-  constexpr int off = kPassOff[ilog2(NS)][ilog2(R)];
-  const float2 w = kPassTw[off + (r - 1) * NS + (int)jm];
+  constexpr uint32_t off = (uint32_t)kPassOff[ilog2(NS)][ilog2(R)];
+  const float2 w = kPassTw[off + (uint32_t)(r - 1) * NS + jm];
   return INV ? c_conj(w) : w;
 }
 
@@ -146,27 +146,44 @@ __device__ __forceinline__ void dft(float2 (&v)[R]) {
 }
 
 // ---------------------------------------------------------------------------
-// LDS scratch addressing for one line of a block transform
+// LDS scratch addressing for one line of a block transform.
+// kKind 1: element p at base[p * S] with S known at compile time;
+// kKind 2: element p at base[p + p/16] (one pad slot per 16 entries);
+// kKind 0: anything else (address computed per access).
+// For kinds 1 and 2 the block transform computes one address per lane and
+// reaches the other elements through compile-time offsets.
 // ---------------------------------------------------------------------------
-struct ScrStrided {  // element p at base[p * stride]
+template <int S>
+struct ScrS {
+  static constexpr int kKind = 1;
+  float2* base;
+  __device__ __forceinline__ float2* operator()(int p) const { return base + p * S; }
+};
+struct ScrPad16 {
+  static constexpr int kKind = 2;
+  float2* base;
+  __device__ __forceinline__ float2* operator()(int p) const { return base + p + (p >> 4); }
+};
+struct ScrStrided {  // element p at base[p * stride], stride known at run time
+  static constexpr int kKind = 0;
   float2* base;
   int stride;
   __device__ __forceinline__ float2* operator()(int p) const { return base + p * stride; }
 };
-struct ScrSplit {  // positions [0, n0) in column a, the rest in column b (same stride)
-  float2* a;
-  float2* b;
-  int n0;
-  int stride;
-  __device__ __forceinline__ float2* operator()(int p) const {
-    return p < n0 ? a + p * stride : b + (p - n0) * stride;
-  }
-};
-struct ScrPad16 {  // element p at base[p + p/16]: one pad slot per 16 entries
-  float2* base;
-  __device__ __forceinline__ float2* operator()(int p) const { return base + p + (p >> 4); }
-};
 __host__ __device__ constexpr int pad16_size(int n) { return n + (n >> 4) + 1; }
+
+// Offset, in float2 slots, between position p0 and p0 + d for the layouts
+// above; valid only where the caller has checked pad16_step_ok.
+template <class Scr, int S_UNUSED = 0>
+struct ScrOff;
+template <int S>
+struct ScrOff<ScrS<S>> {
+  static constexpr int off(int d) { return d * S; }
+};
+template <>
+struct ScrOff<ScrPad16> {
+  static constexpr int off(int d) { return d + d / 16; }
+};
 
 // ---------------------------------------------------------------------------
 // Block transform: N points over T = N/E lanes, E points per lane.
@@ -183,6 +200,16 @@ struct BlockFFT {
   template <class Scr>
   static __device__ __forceinline__ void run(float2 (&v)[E], int t, const Scr& scr, bool active) {
     pass<1>(v, t, scr, active);
+  }
+
+  // Pass-16 layout: positions dst + r*NS (r < R) reachable by constant offsets
+  // when NS is a multiple of 16, or when the R positions sit inside one
+  // 16-entry block (NS * R <= 16; dst is then aligned to NS * R).
+  static constexpr bool pad_write_ok(int NS, int R) { return NS % 16 == 0 || NS * R <= 16; }
+  // reads t + T e: constant offsets when T is a multiple of 16 or divides 16
+  static constexpr bool pad_read_ok() { return T % 16 == 0 || 16 % T == 0; }
+  static constexpr int pad_read_off(int e) {
+    return T % 16 == 0 ? (T * e) + (T * e) / 16 : T * (e % (16 / T)) + 17 * (e / (16 / T));
   }
 
   template <int NS, class Scr>
@@ -213,19 +240,62 @@ struct BlockFFT {
           const int j = t + T * b;
           const int jm = j & (NS - 1);
           const int dst = (j - jm) * R + jm;
+          if constexpr (Scr::kKind == 1 || (Scr::kKind == 2 && pad_write_ok(NS, R))) {
+            float2* pw = scr(dst);
 #pragma unroll
-          for (int r = 0; r < R; ++r) *scr(dst + r * NS) = v[b + NB * r];
+            for (int r = 0; r < R; ++r) pw[ScrOff<Scr>::off(r * NS)] = v[b + NB * r];
+          } else {
+#pragma unroll
+            for (int r = 0; r < R; ++r) *scr(dst + r * NS) = v[b + NB * r];
+          }
         }
       }
       __syncthreads();
       if (active) {
+        if constexpr (Scr::kKind == 1) {
+          const float2* pr = scr(t);
 #pragma unroll
-        for (int e = 0; e < E; ++e) v[e] = *scr(t + T * e);
+          for (int e = 0; e < E; ++e) v[e] = pr[ScrOff<Scr>::off(T * e)];
+        } else if constexpr (Scr::kKind == 2 && pad_read_ok()) {
+          const float2* pr = scr(t);
+#pragma unroll
+          for (int e = 0; e < E; ++e) v[e] = pr[pad_read_off(e)];
+        } else {
+#pragma unroll
+          for (int e = 0; e < E; ++e) v[e] = *scr(t + T * e);
+        }
       }
       pass<NS * R>(v, t, scr, active);
     }
   }
 };
+
+// ---------------------------------------------------------------------------
+// Staging copies.  Item i = tid + NT * j for j < ceil(COUNT / NT); a batch of
+// BATCH items is loaded (all loads issued) before any of them is stored, so
+// global-memory latency overlaps instead of serialising per item.  ld(i)
+// returns the value (it may return zero for skipped items); st(i, value)
+// stores it (it may ignore skipped items).
+// ---------------------------------------------------------------------------
+template <int COUNT, int NT, int BATCH, class Ld, class St>
+__device__ __forceinline__ void batched_copy(int tid, const Ld& ld, const St& st) {
+  constexpr int ITER = (COUNT + NT - 1) / NT;
+  using V = decltype(ld(0));
+#pragma unroll
+  for (int j0 = 0; j0 < ITER; j0 += BATCH) {
+    V tmp[BATCH];
+#pragma unroll
+    for (int b = 0; b < BATCH; ++b) {
+      const int i = tid + NT * (j0 + b);
+      if (j0 + b < ITER && (COUNT % NT == 0 || i < COUNT)) tmp[b] = ld(i);
+    }
+#pragma unroll
+    for (int b = 0; b < BATCH; ++b) {
+      const int i = tid + NT * (j0 + b);
+      if (j0 + b < ITER && (COUNT % NT == 0 || i < COUNT)) st(i, tmp[b]);
+    }
+  }
+}
 
 // ---------------------------------------------------------------------------
 // storage types: float (fp32) or uint16_t (bf16 bits); compute is fp32
