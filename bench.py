@@ -47,16 +47,8 @@ def to_device(arr, dtype):
 
 
 def kernel_source_hash() -> str:
-    """Hash of every HIP source of the library (the counters in profiles/ are
-    only valid for the kernels they were taken on)."""
-    import glob
-    import hashlib
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2607_19378_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
-        h.update(os.path.basename(f).encode())
-        h.update(open(f, "rb").read())
-    return h.hexdigest()[:16]
+    from paper_2607_19378_amd.build import source_hash
+    return source_hash()
 
 
 def stored_traffic(workload: str):

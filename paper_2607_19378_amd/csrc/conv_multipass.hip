@@ -19,7 +19,8 @@
 // through the workspace, which is sized per chunk of lines.  Strided axes are
 // transformed in tiles of TL adjacent columns, so every global access is a
 // contiguous run of TL complex values and no explicit transpose is stored.
-// Tiles are sized so that two 512-lane workgroups share a CU.
+// Tiles are sized so that two 512-lane (core pass: up to four 256-lane)
+// workgroups share a CU.
 #include "kernels.hpp"
 
 namespace hyenand {
@@ -203,18 +204,27 @@ __global__ void __launch_bounds__(256)
 // transformed along the rows index.  LDS tile [P][TLP].  Columns whose index
 // modulo HS is >= H (row padding) are neither loaded nor stored.
 // ---------------------------------------------------------------------------
-constexpr int mp_tl(int P, int NS) {  // widest power of two <= 32 fitting ~76 KB
+// Tiles: the widest power of two <= 32 whose NS signal tiles fit in KB
+// kilobytes of LDS, and E points per lane so that a tile keeps NT lanes busy.
+// The axis-1 passes use two 512-lane workgroups per CU (76 KB each); the core
+// pass, which holds one signal, uses four 256-lane workgroups (38 KB) where
+// that still leaves tiles 16 columns wide, since more resident workgroups
+// overlap the load, transform and store phases better.
+constexpr int mp_tl(int P, int NS, int KB) {
   int tl = 32;
-  while (tl > 1 && NS * P * (tl + 1) * 8 > 76 * 1024) tl /= 2;
+  while (tl > 1 && NS * P * (tl + 1) * 8 > KB * 1024) tl /= 2;
   return tl;
 }
-// E for `lines` transforms of length P carried by 512 lanes
-constexpr int mp_e(int P, int lines) { return imin(P, imax(2, imin(16, P * lines / 512))); }
+constexpr int mp_e(int P, int lines, int NT) { return imin(P, imax(2, imin(16, P * lines / NT))); }
+constexpr int kTileNT = 512;
+constexpr int kTileKB = 76;
+constexpr bool mp_core_small(int P0) { return mp_tl(P0, 1, kTileKB / 2) >= 16; }
+constexpr int mp_core_nt(int P0) { return mp_core_small(P0) ? kTileNT / 2 : kTileNT; }
 
 template <int P, int NS>
 struct TileCfg {  // NS signal tiles, each column of each signal is one line
-  static constexpr int TL = mp_tl(P, NS);
-  static constexpr int E = mp_e(P, NS * TL);
+  static constexpr int TL = mp_tl(P, NS, kTileKB);
+  static constexpr int E = mp_e(P, NS * TL, kTileNT);
   static constexpr int T = P / E;
   static constexpr int TLP = TL + 1;
 };
@@ -257,13 +267,13 @@ __device__ __forceinline__ void tile_store(const float2* tile, float2* __restric
 // inverse on Y (P1 in, L1 cropped rows out).  One workgroup per (line, n0, tile).
 // ---------------------------------------------------------------------------
 template <int P1, bool CIRC, bool INV>
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(kTileNT)
     mp_axis1(float2* __restrict__ ws, int H, int HS, int L0, int64_t half, int64_t per_line) {
   constexpr int NS = INV ? 1 : 2;  // signals
   using Cf = TileCfg<P1, NS>;
   constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T;
   constexpr int L1 = CIRC ? P1 : P1 / 2;
-  constexpr int NT = 512;
+  constexpr int NT = kTileNT;
   __shared__ float2 tile[NS][P1 * TLP];
   const int ntile = (H + TL - 1) / TL;
   const int64_t bid = blockIdx.x;
@@ -312,9 +322,9 @@ __global__ void __launch_bounds__(512)
 // ---------------------------------------------------------------------------
 template <int P0, bool CIRC>
 struct CoreCfg {
-  static constexpr int NT = 512;
-  static constexpr int TL = mp_tl(P0, 1);
-  static constexpr int E = mp_e(P0, TL);
+  static constexpr int NT = mp_core_nt(P0);
+  static constexpr int TL = mp_tl(P0, 1, mp_core_small(P0) ? kTileKB / 2 : kTileKB);
+  static constexpr int E = mp_e(P0, TL, NT);
   static constexpr int T = P0 / E;
   static constexpr int TLP = TL + 1;
   static constexpr int L0 = CIRC ? P0 : P0 / 2;
@@ -322,7 +332,7 @@ struct CoreCfg {
 };
 
 template <int P0, bool CIRC>
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(mp_core_nt(P0))
     mp_core(float2* __restrict__ ws, const void* __restrict__ Dp, int dbf16, int64_t line0, int C,
             int ncols, int HS, int H, int64_t half, int64_t per_line, float scale) {
   using Cf = CoreCfg<P0, CIRC>;
@@ -544,10 +554,10 @@ hipError_t axis1(const MpLaunch& L) {
   const int ntile = (L.g.H + TL - 1) / TL;
   const dim3 grid((unsigned)((int64_t)L.nl * L.g.L0 * ntile));
   if (L.a->circular)
-    hipLaunchKernelGGL((mp_axis1<P1, true, INV>), grid, dim3(512), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
+    hipLaunchKernelGGL((mp_axis1<P1, true, INV>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
                        L.per);
   else
-    hipLaunchKernelGGL((mp_axis1<P1, false, INV>), grid, dim3(512), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
+    hipLaunchKernelGGL((mp_axis1<P1, false, INV>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
                        L.per);
   return hipGetLastError();
 }
@@ -563,12 +573,12 @@ hipError_t core(const MpLaunch& L) {
   if (a.circular) {
     constexpr int TL = CoreCfg<P0, true>::TL;
     const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
-    hipLaunchKernelGGL((mp_core<P0, true>), grid, dim3(512), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
+    hipLaunchKernelGGL((mp_core<P0, true>), grid, dim3(CoreCfg<P0, true>::NT), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
                        ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale);
   } else {
     constexpr int TL = CoreCfg<P0, false>::TL;
     const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
-    hipLaunchKernelGGL((mp_core<P0, false>), grid, dim3(512), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
+    hipLaunchKernelGGL((mp_core<P0, false>), grid, dim3(CoreCfg<P0, false>::NT), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
                        ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale);
   }
   return hipGetLastError();

@@ -1,0 +1,161 @@
+"""Turn rocprofv3 runs of bench.py into the text summaries kept under profiles/.
+
+    python -m paper_2607_19378_amd.profile_summary --workload W --calls N \\
+        --trace DIR --fetch DIR --write DIR --copy-mib M \\
+        --cmd-trace "..." --cmd-fetch "..." --cmd-write "..."
+
+The three directories hold the CSV output of three rocprofv3 runs of one
+bench.py command: ``--kernel-trace --stats``, ``--pmc FETCH_SIZE`` and
+``--pmc WRITE_SIZE``.  N is the number of hyenand_fftconv calls the command
+made (bench.py: warmup + steps).  Writes
+
+* ``profiles/<plan>_<workload>.md``: per-kernel average durations, HBM bytes
+  per call against the algorithmic minimum, and the commands;
+* ``profiles/traffic_<workload>.json``: HBM bytes per call, which bench.py
+  reports as ``roofline.traffic`` while the kernel sources are unchanged.
+
+FETCH_SIZE and WRITE_SIZE count KiB per dispatch.  Each is scaled by
+known bytes / counter value of the plain device-to-device copy
+(``__amd_rocclr_copyBuffer`` of M MiB) that ``bench.py --copy-calibration-mb M``
+runs after its timed steps, so the figures are HBM bytes.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import json
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def _rows(d: str, suffix: str):
+    files = glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
+    if not files:
+        raise SystemExit(f"no *{suffix} under {d}")
+    out = []
+    for f in files:
+        with open(f) as fh:
+            out += list(csv.DictReader(fh))
+    return out
+
+
+def short_name(full: str) -> str:
+    """'void hyenand::(anonymous namespace)::mp_core<512, true>(...)' -> 'mp_core<512, true>'."""
+    n = full.strip('"')
+    if n.startswith("void "):
+        n = n[5:]
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0 and not n[i:].startswith("(anonymous"):
+            cut = i
+            break
+    n = n[:cut]
+    return n.split("::")[-1]
+
+
+def counter_per_call(rows, counter: str, calls: int):
+    """Sum of the counter over hyenand dispatches / calls, and the copy's value."""
+    op = 0.0
+    copy = 0.0
+    per_kernel = {}
+    for r in rows:
+        if r["Counter_Name"] != counter:
+            continue
+        v = float(r["Counter_Value"])
+        name = r["Kernel_Name"]
+        if "hyenand" in name:
+            op += v
+            k = short_name(name)
+            per_kernel[k] = per_kernel.get(k, 0.0) + v
+        elif COPY_KERNEL in name:
+            copy = max(copy, v)
+    return op / calls, copy, {k: v / calls for k, v in per_kernel.items()}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--calls", type=int, required=True)
+    ap.add_argument("--trace", required=True)
+    ap.add_argument("--fetch", required=True)
+    ap.add_argument("--write", required=True)
+    ap.add_argument("--copy-mib", type=int, required=True)
+    ap.add_argument("--cmd-trace", required=True)
+    ap.add_argument("--cmd-fetch", required=True)
+    ap.add_argument("--cmd-write", required=True)
+    ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
+    a = ap.parse_args(argv)
+
+    sys.path.insert(0, ROOT)
+    from paper_2607_19378_amd import workloads as W
+    from paper_2607_19378_amd.build import source_hash
+    from paper_2607_19378_amd import hyenand as H
+
+    w = W.WORKLOADS[a.workload]
+    plan = H.plan_name(w.shape, w.pad_mode, w.dtype)
+    alg = w.elems * 5 * w.storage_bytes
+
+    stats = [r for r in _rows(a.trace, "_kernel_stats.csv") if "hyenand" in r["Name"]]
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    total_ns = sum(float(r["TotalDurationNs"]) for r in stats)
+
+    f_call, f_copy, f_k = counter_per_call(_rows(a.fetch, "_counter_collection.csv"), "FETCH_SIZE", a.calls)
+    w_call, w_copy, w_k = counter_per_call(_rows(a.write, "_counter_collection.csv"), "WRITE_SIZE", a.calls)
+    copy_kib = a.copy_mib * 1024.0
+    if f_copy <= 0 or w_copy <= 0:
+        raise SystemExit("copy calibration dispatch not found in the counter runs")
+    f_scale = copy_kib / f_copy
+    w_scale = copy_kib / w_copy
+    fetch_b = f_call * 1024.0 * f_scale
+    write_b = w_call * 1024.0 * w_scale
+    h = source_hash()
+
+    lines = [f"# {plan} on {w.name}", "",
+             f"{w.description}.  Plan `{plan}`; kernel source hash `{h}`.", "",
+             "Commands (run from /tmp with TMPDIR=/tmp on the MI355X box; bench.py made "
+             f"{a.calls} hyenand_fftconv calls in each):", "",
+             "```", a.cmd_trace, a.cmd_fetch, a.cmd_write, "```", "",
+             "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",
+             "| kernel | dispatches | avg us | min us | max us | share of op time |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for r in stats:
+        lines.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{100.0 * float(r['TotalDurationNs']) / total_ns:.1f}% |")
+    lines += ["", f"Kernel time per call: {total_ns / a.calls / 1e3:.2f} us "
+                  f"({alg / (total_ns / a.calls) :.1f} GB/s of algorithmic bytes, "
+                  f"{100.0 * alg / (total_ns / a.calls) / 8000.0:.2f}% of 8 TB/s).", "",
+              "## HBM traffic per call (rocprofv3 --pmc)", "",
+              f"Copy calibration: {a.copy_mib} MiB device copy read {f_copy:.1f} KiB (FETCH_SIZE) and wrote "
+              f"{w_copy:.1f} KiB (WRITE_SIZE); scale factors {f_scale:.4f} and {w_scale:.4f}.", "",
+              "| kernel | FETCH MB/call | WRITE MB/call |", "|---|---:|---:|"]
+    for k in sorted(set(f_k) | set(w_k)):
+        lines.append(f"| `{k}` | {f_k.get(k, 0.0) * 1024.0 * f_scale / 1e6:.2f} | {w_k.get(k, 0.0) * 1024.0 * w_scale / 1e6:.2f} |")
+    lines += ["",
+              f"Total: read {fetch_b / 1e6:.2f} MB + write {write_b / 1e6:.2f} MB = {(fetch_b + write_b) / 1e6:.2f} MB "
+              f"per call; algorithmic minimum {alg / 1e6:.2f} MB (x1, x2, v, k read and y written once); "
+              f"ratio {(fetch_b + write_b) / alg:.3f}.", ""]
+    os.makedirs(a.out, exist_ok=True)
+    md = os.path.join(a.out, f"{plan}_{w.name}.md")
+    with open(md, "w") as fh:
+        fh.write("\n".join(lines))
+    rec = {"workload": w.name, "plan": plan, "source_hash": h, "bytes_per_call": round(fetch_b + write_b),
+           "fetch_bytes_per_call": round(fetch_b), "write_bytes_per_call": round(write_b),
+           "alg_bytes_per_call": alg, "fetch_scale": round(f_scale, 5), "write_scale": round(w_scale, 5),
+           "calls": a.calls, "commands": [a.cmd_fetch, a.cmd_write]}
+    with open(os.path.join(a.out, f"traffic_{w.name}.json"), "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(md)
+
+
+if __name__ == "__main__":
+    main()
