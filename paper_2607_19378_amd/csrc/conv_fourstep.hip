@@ -64,7 +64,8 @@ __global__ void __launch_bounds__(512)
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
-  __shared__ float2 tile[N1 * TLP];
+  static_assert(NT / T >= TL, "one round covers the tile");
+  __shared__ float2 tile[N1 * TLP];  // exchange scratch, one column per line
   const int ntile = N2 / TL;
   const int sig = (int)(blockIdx.x & 1);  // 0: u = x1 v, 1: k
   const int64_t rest = blockIdx.x >> 1;
@@ -74,46 +75,37 @@ __global__ void __launch_bounds__(512)
   const int64_t L = CIRC ? 2 * M : M;  // real samples per line
   const size_t gbase = (size_t)(line0 + line) * L;
   const int tid = threadIdx.x;
+  // lanes with consecutive ids take consecutive columns of one row, so every
+  // global access below is a contiguous run of TL values per row
+  const int cc = tid % (NT / T), t = tid / (NT / T);
+  const bool act = cc < TL;
 
-  batched_copy<NZ * TL, NT, 8>(
-      tid,
-      [&](int i) {
-        const int m1 = i / TL, cc = i - m1 * TL;
-        const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
-        if (sig == 0) {
-          const float2 a = ld2(x1 + n), b = ld2(v + n);
-          return make_float2(a.x * b.x, a.y * b.y);
-        }
-        return ld2(k + n);
-      },
-      [&](int i, float2 z) { tile[(i / TL) * TLP + (i % TL)] = z; });
-  __syncthreads();
-
-  for (int l0 = 0; l0 < TL; l0 += NT / T) {
-    const int cc = l0 + tid % (NT / T), t = tid / (NT / T);
-    const bool act = cc < TL;
-    float2* col = tile + (act ? cc : 0);
-    float2 w[E];
+  // column points straight from global memory into registers (lane t holds
+  // m1 = t + T e); rows at or beyond NZ are the zero padding
+  float2 w[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-      const int m1 = t + T * e;
-      w[e] = (act && (CIRC || m1 < NZ)) ? col[m1 * TLP] : czero();
-    }
-    BlockFFT<N1, E, false>::run(w, t, ScrS<TLP>{col}, act);
-    if (act) {
-      // exp(-2 pi i m2 f1 / M) for f1 = t + T e
-      const uint32_t m2 = (uint32_t)(c0 + cc);
-      twiddle_run<E>(w, twiddle_rt<false>(m2 * (uint32_t)t, log2M), twiddle_rt<false>(m2 * (uint32_t)T, log2M));
-#pragma unroll
-      for (int e = 0; e < E; ++e) col[(t + T * e) * TLP] = w[e];
+  for (int e = 0; e < E; ++e) {
+    const int m1 = t + T * e;
+    w[e] = czero();
+    if (act && (CIRC || m1 < NZ)) {
+      const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
+      if (sig == 0) {
+        const float2 a = ld2(x1 + n), b = ld2(v + n);
+        w[e] = make_float2(a.x * b.x, a.y * b.y);
+      } else {
+        w[e] = ld2(k + n);
+      }
     }
   }
-  __syncthreads();
-
-  float2* A = ws + line * per_line + (sig ? M : 0);
-  batched_copy<N1 * TL, NT, 8>(
-      tid, [&](int i) { return tile[(i / TL) * TLP + (i % TL)]; },
-      [&](int i, float2 z) { A[(size_t)(i / TL) * N2 + c0 + (i % TL)] = z; });
+  BlockFFT<N1, E, false>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act);
+  if (act) {
+    // exp(-2 pi i m2 f1 / M) for f1 = t + T e, then A[f1][m2]
+    const uint32_t m2 = (uint32_t)(c0 + cc);
+    twiddle_run<E>(w, twiddle_rt<false>(m2 * (uint32_t)t, log2M), twiddle_rt<false>(m2 * (uint32_t)T, log2M));
+    float2* A = ws + line * per_line + (sig ? M : 0) + c0 + cc;
+#pragma unroll
+    for (int e = 0; e < E; ++e) A[(size_t)(t + T * e) * N2] = w[e];
+  }
 }
 
 template <bool CIRC>
@@ -224,45 +216,42 @@ __global__ void __launch_bounds__(512)
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NOUT = CIRC ? N1 : N1 / 2;  // cropped rows m1
-  __shared__ float2 tile[N1 * TLP];
+  static_assert(NT / T >= TL, "one round covers the tile");
+  __shared__ float2 tile[N1 * TLP];  // exchange scratch, one column per line
   const int ntile = N2 / TL;
-  const int64_t line = blockIdx.x / ntile;
-  const int c0 = (int)(blockIdx.x % ntile) * TL;
+  // the x2/y runs of neighbouring tiles share cache lines: keep them on one XCD
+  const uint32_t bid = xcd_order(blockIdx.x, gridDim.x);
+  const int64_t line = bid / ntile;
+  const int c0 = (int)(bid % ntile) * TL;
   const int64_t M = (int64_t)N1 * N2;
   const int64_t L = CIRC ? 2 * M : M;
-  const float2* B = ws + line * per_line;
   const int tid = threadIdx.x;
+  const int cc = tid % (NT / T), t = tid / (NT / T);
+  const bool act = cc < TL;
 
-  batched_copy<N1 * TL, NT, 8>(
-      tid, [&](int i) { return B[(int64_t)(i / TL) * N2 + c0 + (i % TL)]; },
-      [&](int i, float2 z) { tile[(i / TL) * TLP + (i % TL)] = z; });
-  __syncthreads();
-
-  for (int l0 = 0; l0 < TL; l0 += NT / T) {
-    const int cc = l0 + tid % (NT / T), t = tid / (NT / T);
-    const bool act = cc < TL;
-    float2* col = tile + (act ? cc : 0);
-    float2 w[E];
+  const float2* B = ws + line * per_line + c0 + cc;
+  float2 w[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) w[e] = act ? col[(t + T * e) * TLP] : czero();
-    BlockFFT<N1, E, true>::run(w, t, ScrS<TLP>{col}, act);
-    if (act) {
+  for (int e = 0; e < E; ++e) w[e] = act ? B[(size_t)(t + T * e) * N2] : czero();
+  // outer gate values for the kept rows m1 = t + T e < NOUT, fetched before
+  // the transform so their latency hides behind it
+  const size_t gbase = (size_t)(line0 + line) * L + 2 * (size_t)(c0 + cc);
+  float2 g[E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int m1 = t + T * e;
-        if (CIRC || m1 < NOUT) col[m1 * TLP] = w[e];
-      }
+  for (int e = 0; e < E; ++e) {
+    const int m1 = t + T * e;
+    g[e] = (act && (CIRC || m1 < NOUT)) ? ld2(x2 + gbase + 2 * (size_t)m1 * N2) : czero();
+  }
+  BlockFFT<N1, E, true>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act);
+  if (act) {
+    // unpack y[2m], y[2m+1] and gate
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int m1 = t + T * e;
+      if (CIRC || m1 < NOUT)
+        st2(y + gbase + 2 * (size_t)m1 * N2, make_float2(g[e].x * w[e].x, g[e].y * w[e].y));
     }
   }
-  __syncthreads();
-
-  const size_t gbase = (size_t)(line0 + line) * L;
-  batched_copy<NOUT * TL, NT, 8>(
-      tid, [&](int i) { return ld2(x2 + gbase + 2 * ((size_t)(i / TL) * N2 + c0 + (i % TL))); },
-      [&](int i, float2 g) {
-        const float2 q = tile[(i / TL) * TLP + (i % TL)];
-        st2(y + gbase + 2 * ((size_t)(i / TL) * N2 + c0 + (i % TL)), make_float2(g.x * q.x, g.y * q.y));
-      });
 }
 
 struct FsLaunch {

@@ -193,7 +193,7 @@ struct Fused2D {
   static constexpr int TR = M1 / ER;
   static constexpr int LR = NT / TR;         // lines per round
   // column transforms (length P0): M1 groups
-  static constexpr int EC = imin(8, P0);
+  static constexpr int EC = imin(16, P0);
   static constexpr int TC = P0 / EC;
   static constexpr int CR = NT / TC;         // column groups per round
   // inverse row transforms carrying two rows each
@@ -241,7 +241,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   {
     constexpr int E = F::ER, T = F::TR, LR = F::LR;
     for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
-      const int l = l0 + tid % LR, t = tid / LR;
+      using Map = LaneMap<T, NT>;
+      static_assert(Map::kLines == LR, "lines per round");
+      const int l = l0 + Map::line(tid), t = Map::t(tid);
       const bool act = l < 2 * L0;
       float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
       float2 w[E];
@@ -257,28 +259,31 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       }
     }
     __syncthreads();
-    // item (row, g) owns bins g and M1 - g (g = 0 also writes the Nyquist
-    // slot M1), so the untangling is an in-place read-modify-write
+    // item (row, g) owns bins g and M1 - g, so the untangling is an in-place
+    // read-modify-write.  The DC and Nyquist bins of a real row are real:
+    // slot 0 keeps both, as DC + i Nyquist (column group 0 below).
     for (int it = tid; it < F::NPOST; it += NT) {
       const int l = it % (2 * L0), g = it / (2 * L0);
       float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
       float2 xa, xb;
       r2c_pair(row[g], row[(M1 - g) & (M1 - 1)], twiddle<ilog2(P1), false>(g), xa, xb);
-      row[g] = xa;
+      row[g] = g == 0 ? make_float2(xa.x, xb.x) : xa;
       row[M1 - g] = xb;
     }
   }
   __syncthreads();
 
   // 2. column groups: forward transforms of U and K, gated product with the
-  //    folded shortcut, inverse transform; keep rows < L0.  Group 0 carries
-  //    the two real columns 0 and M1 as one complex column.
+  //    folded shortcut, inverse transform; keep rows < L0.  Group 0 is the
+  //    complex column DC + i Nyquist of the two real columns 0 and M1.
   {
     constexpr int E = F::EC, T = F::TC, CR = F::CR;
     const float twoD = 2.f * ld1(Dp + c);
     const float scale = 1.f / (4.f * (float)P0 * (float)P1);
     for (int c0 = 0; c0 < M1; c0 += CR) {
-      const int grp = c0 + tid % CR, t = tid / CR;
+      using Map = LaneMap<T, NT>;
+      static_assert(Map::kLines == CR, "groups per round");
+      const int grp = c0 + Map::line(tid), t = Map::t(tid);
       const bool act = grp < M1;
       const bool nyq = act && grp == 0;
       const int col = act ? grp : 0;
@@ -287,65 +292,56 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       for (int e = 0; e < E; ++e) {
         const int n = t + T * e;
         const bool nz = act && (CIRC || n < L0);
-        wu[e] = czero();
-        wk[e] = czero();
-        if (nz) {
-          if (nyq) {
-            wu[e] = make_float2(Uh[n * RP].x, Uh[n * RP + M1].x);
-            wk[e] = make_float2(Kh[n * RP].x, Kh[n * RP + M1].x);
-          } else {
-            wu[e] = Uh[n * RP + col];
-            wk[e] = Kh[n * RP + col];
-          }
-        }
+        wu[e] = nz ? Uh[n * RP + col] : czero();
+        wk[e] = nz ? Kh[n * RP + col] : czero();
       }
       const ScrS<RP> su{UK + col};
       BlockFFT<P0, E, false>::run(wu, t, su, act);
       BlockFFT<P0, E, false>::run(wk, t, su, act);
-      // group 0: publish both spectra so the mirror bins can be read
-      const ScrS<RP> sk0{CIRC ? Kh : UK + M1};
-      __syncthreads();
+      // Group 0 holds A + i B with A, B the spectra of the real columns 0
+      // and M1: A = (Z[f] + conj Z[-f]) / 2, B = -i (Z[f] - conj Z[-f]) / 2
+      // need the mirror bin, so its spectra go through LDS and the bin pairs
+      // (f, P0 - f) are multiplied by lanes of the first two wavefronts; the
+      // other groups multiply in registers.
+      const ScrS<RP> u0{UK};
+      const ScrS<RP> k0{CIRC ? Kh : UK + M1};
+      __syncthreads();  // exchange reads of the forward transforms are done
       if (nyq) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          *su(t + T * e) = wu[e];
-          *sk0(t + T * e) = wk[e];
+          *u0(t + T * e) = wu[e];
+          *k0(t + T * e) = wk[e];
         }
+      }
+      __syncthreads();
+      if (c0 == 0 && tid <= P0 / 2) {
+        const int f = tid, fm = (P0 - f) & (P0 - 1);
+        const float2 zu = *u0(f), zum = *u0(fm), zk = *k0(f), zkm = *k0(fm);
+        const float2 ua = c_scale(make_float2(zu.x + zum.x, zu.y - zum.y), 0.5f);
+        const float2 ub = c_scale(make_float2(zu.y + zum.y, zum.x - zu.x), 0.5f);
+        const float2 ka = c_scale(make_float2(zk.x + zkm.x, zk.y - zkm.y), 0.5f);
+        const float2 kb = c_scale(make_float2(zk.y + zkm.y, zkm.x - zk.x), 0.5f);
+        const float2 ya = c_scale(gated_product(ua, ka, twoD), scale);
+        const float2 yb = c_scale(gated_product(ub, kb, twoD), scale);
+        // Y = Ya + i Yb; both products are Hermitian, so at -f it is conj Ya + i conj Yb
+        *u0(f) = make_float2(ya.x - yb.y, ya.y + yb.x);
+        if (fm != f) *u0(fm) = make_float2(ya.x + yb.y, yb.x - ya.y);
       }
       __syncthreads();
       if (nyq) {
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const int fm = (P0 - (t + T * e)) & (P0 - 1);
-          const float2 bu = *su(fm), bk = *sk0(fm);
-          // a + i b packing: A = (Z + conj Zm)/2, B = -i (Z - conj Zm)/2
-          const float2 ua = c_scale(make_float2(wu[e].x + bu.x, wu[e].y - bu.y), 0.5f);
-          const float2 ub = c_scale(make_float2(wu[e].y + bu.y, bu.x - wu[e].x), 0.5f);
-          const float2 ka = c_scale(make_float2(wk[e].x + bk.x, wk[e].y - bk.y), 0.5f);
-          const float2 kb = c_scale(make_float2(wk[e].y + bk.y, bk.x - wk[e].x), 0.5f);
-          const float2 ya = c_scale(gated_product(ua, ka, twoD), scale);
-          const float2 yb = c_scale(gated_product(ub, kb, twoD), scale);
-          wu[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
-        }
+        for (int e = 0; e < E; ++e) wu[e] = *u0(t + T * e);
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
       }
-      if constexpr (T == 1) __syncthreads();
       BlockFFT<P0, E, true>::run(wu, t, su, act);
       __syncthreads();  // scratch reads of the last exchange are done
       if (act) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           const int n = t + T * e;
-          if (CIRC || n < L0) {
-            if (nyq) {
-              Uh[n * RP] = make_float2(wu[e].x, 0.f);
-              Uh[n * RP + M1] = make_float2(wu[e].y, 0.f);
-            } else {
-              Uh[n * RP + col] = wu[e];
-            }
-          }
+          if (CIRC || n < L0) Uh[n * RP + col] = wu[e];
         }
       }
     }
@@ -358,7 +354,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     constexpr int E = F::EI, T = F::TI, PR = F::PR;
     constexpr int NPAIR = L0 / 2;
     for (int q0 = 0; q0 < NPAIR; q0 += PR) {
-      const int q = q0 + tid % PR, t = tid / PR;
+      using Map = LaneMap<T, NT>;
+      static_assert(Map::kLines == PR, "pairs per round");
+      const int q = q0 + Map::line(tid), t = Map::t(tid);
       const bool act = q < NPAIR;
       float2* ra = Uh + 2 * (act ? q : 0) * RP;
       const float2* rb = ra + RP;
@@ -366,14 +364,23 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int f = t + T * e;
+        // bins above M1 are conjugate mirrors; slot 0 holds DC + i Nyquist
         float2 ya = czero(), yb = czero();
         if (act) {
-          if (f <= M1) {
-            ya = ra[f];
-            yb = rb[f];
+          const int idx = f < M1 ? f : (f == M1 ? 0 : P1 - f);
+          const float2 a = ra[idx], b = rb[idx];
+          if (f == 0) {
+            ya = make_float2(a.x, 0.f);
+            yb = make_float2(b.x, 0.f);
+          } else if (f == M1) {
+            ya = make_float2(a.y, 0.f);
+            yb = make_float2(b.y, 0.f);
+          } else if (f < M1) {
+            ya = a;
+            yb = b;
           } else {
-            ya = c_conj(ra[P1 - f]);
-            yb = c_conj(rb[P1 - f]);
+            ya = c_conj(a);
+            yb = c_conj(b);
           }
         }
         w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb

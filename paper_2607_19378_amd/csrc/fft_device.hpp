@@ -271,6 +271,41 @@ struct BlockFFT {
 };
 
 // ---------------------------------------------------------------------------
+// Lanes of an NT-lane workgroup assigned to (line, t) for block transforms of
+// T lanes per line, NT / T lines per round.  When T * 64 <= NT every
+// wavefront holds a single t, made wave-uniform, and 64 consecutive lines:
+// pass twiddle indices and exchange offsets are then scalar, and the lanes of
+// a wavefront touch 64 consecutive lines at one position.  Otherwise
+// consecutive lanes take consecutive lines and t = tid / (NT / T).
+// ---------------------------------------------------------------------------
+template <int T, int NT>
+struct LaneMap {
+  static constexpr bool kUniform = T * 64 <= NT;
+  static constexpr int kLines = NT / T;
+  static __device__ __forceinline__ int t(int tid) {
+    if constexpr (kUniform) return __builtin_amdgcn_readfirstlane((tid >> 6) % T);
+    else return tid / kLines;
+  }
+  static __device__ __forceinline__ int line(int tid) {
+    if constexpr (kUniform) return ((tid >> 6) / T) * 64 + (tid & 63);
+    else return tid % kLines;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Workgroup renumbering.  The dispatcher hands workgroup b to XCD b % 8 (each
+// XCD has its own L2).  xcd_order(b, n) numbers the n workgroups so that each
+// XCD receives a contiguous range of logical ids in dispatch order: tiles with
+// consecutive logical ids then run together on one XCD and share the cache
+// lines they both touch (a bijection of [0, n)).
+// ---------------------------------------------------------------------------
+constexpr uint32_t kNumXcd = 8;
+__host__ __device__ __forceinline__ uint32_t xcd_order(uint32_t b, uint32_t n) {
+  const uint32_t x = b % kNumXcd, j = b / kNumXcd, per = n / kNumXcd, rem = n % kNumXcd;
+  return x * per + (x < rem ? x : rem) + j;
+}
+
+// ---------------------------------------------------------------------------
 // Staging copies.  Item i = tid + NT * j for j < ceil(COUNT / NT); a batch of
 // BATCH items is loaded (all loads issued) before any of them is stored, so
 // global-memory latency overlaps instead of serialising per item.  ld(i)
