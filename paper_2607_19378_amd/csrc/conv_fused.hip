@@ -196,13 +196,11 @@ struct Fused2D {
   static constexpr int EC = imin(16, P0);
   static constexpr int TC = P0 / EC;
   static constexpr int CR = NT / TC;         // column groups per round
-  // inverse row transforms carrying two rows each
-  static constexpr int EI = imin(8, P1);
-  static constexpr int TI = P1 / EI;
-  static constexpr int PR = NT / TI;         // row pairs per round
-  // real-to-complex untangling items: rows x (M1/2 + 1)
-  static constexpr int NPOST = 2 * L0 * (M1 / 2 + 1);
-  static_assert(2 * RP >= P1, "two-row scratch");
+  // inverse row transforms: one real row each, as the length-M1 transform
+  // of its even/odd output pairs
+  static constexpr int EI = imin(8, M1);
+  static constexpr int TI = M1 / EI;
+  static constexpr int RI = NT / TI;         // rows per round
   static_assert(2 * L0 >= P0, "column scratch");
 };
 
@@ -223,18 +221,18 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   const int tid = threadIdx.x;
 
   // 0. stage the real rows of u = x1 v and k (coalesced along rows); row r of
-  //    Uh read as floats is u[r][0..P1), i.e. the even/odd packed line.
-  {
-    float* uf = reinterpret_cast<float*>(Uh);
-    float* kf = reinterpret_cast<float*>(Kh);
-    batched_copy<L0 * L1, NT, 8>(
-        tid, [&](int i) { return make_float2(ld1(x1 + base + i) * ld1(v + base + i), ld1(k + base + i)); },
-        [&](int i, float2 z) {
-          const int r = i / L1, col = i - r * L1;
-          uf[r * 2 * RP + col] = z.x;
-          kf[r * 2 * RP + col] = z.y;
-        });
-  }
+  //    Uh holds the even/odd packed line u[r][2m] + i u[r][2m+1].
+  batched_copy<L0 * L1 / 2, NT, 8>(
+      tid,
+      [&](int i) {
+        const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i), kk = ld2(k + base + 2 * i);
+        return make_float4(a.x * b.x, a.y * b.y, kk.x, kk.y);
+      },
+      [&](int i, float4 z) {
+        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+        Uh[r * RP + m] = make_float2(z.x, z.y);
+        Kh[r * RP + m] = make_float2(z.z, z.w);
+      });
   __syncthreads();
 
   // 1. forward row transforms (lanes run across rows), then untangle each row
@@ -259,16 +257,31 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       }
     }
     __syncthreads();
-    // item (row, g) owns bins g and M1 - g, so the untangling is an in-place
-    // read-modify-write.  The DC and Nyquist bins of a real row are real:
-    // slot 0 keeps both, as DC + i Nyquist (column group 0 below).
-    for (int it = tid; it < F::NPOST; it += NT) {
-      const int l = it % (2 * L0), g = it / (2 * L0);
-      float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+    // Untangling, in place: item (row l, g) for 0 < g < M1/2 owns bins g and
+    // M1 - g; bins 0 and M1/2 are their own mirrors and share the item g = 0
+    // of their row.  The DC and Nyquist bins of a real row are real: slot 0
+    // keeps both, as DC + i Nyquist (column group 0 below).  Rows of U and K
+    // are contiguous (Kh = Uh + L0 RP); with 2 L0 a multiple of 64 every
+    // wavefront shares one g, so its twiddle is a scalar.
+    constexpr int NR = 2 * L0, NG = imax(1, M1 / 2);
+    for (int it = tid; it < NR * NG; it += NT) {
+      const int l = it % NR;
+      const int g = NR % 64 == 0 ? __builtin_amdgcn_readfirstlane(it / NR) : it / NR;
+      float2* row = Uh + l * RP;
       float2 xa, xb;
-      r2c_pair(row[g], row[(M1 - g) & (M1 - 1)], twiddle<ilog2(P1), false>(g), xa, xb);
-      row[g] = g == 0 ? make_float2(xa.x, xb.x) : xa;
-      row[M1 - g] = xb;
+      if (g == 0) {
+        r2c_pair(row[0], row[0], make_float2(1.f, 0.f), xa, xb);
+        row[0] = make_float2(xa.x, xb.x);
+        if constexpr (M1 >= 2) {
+          constexpr int h = M1 / 2;
+          r2c_pair(row[h], row[h], twiddle<ilog2(P1), false>(h), xa, xb);
+          row[h] = xa;
+        }
+      } else {
+        r2c_pair(row[g], row[M1 - g], twiddle<ilog2(P1), false>(g), xa, xb);
+        row[g] = xa;
+        row[M1 - g] = xb;
+      }
     }
   }
   __syncthreads();
@@ -348,50 +361,38 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   }
   __syncthreads();
 
-  // 3. inverse row transforms, two real rows per complex transform; the
-  //    scratch of pair (ra, ra+1) is the 2 RP >= P1 entries of those rows.
+  // 3. inverse row transforms: c2r_pair turns row r's half spectrum (slot 0
+  //    holding DC + i Nyquist) into the length-M1 transform of its even/odd
+  //    output pairs; the inverse leaves y[r][2m] + i y[r][2m+1] in slot m.
   {
-    constexpr int E = F::EI, T = F::TI, PR = F::PR;
-    constexpr int NPAIR = L0 / 2;
-    for (int q0 = 0; q0 < NPAIR; q0 += PR) {
+    constexpr int E = F::EI, T = F::TI, RI = F::RI;
+    for (int r0 = 0; r0 < L0; r0 += RI) {
       using Map = LaneMap<T, NT>;
-      static_assert(Map::kLines == PR, "pairs per round");
-      const int q = q0 + Map::line(tid), t = Map::t(tid);
-      const bool act = q < NPAIR;
-      float2* ra = Uh + 2 * (act ? q : 0) * RP;
-      const float2* rb = ra + RP;
+      static_assert(Map::kLines == RI, "rows per round");
+      const int r = r0 + Map::line(tid), t = Map::t(tid);
+      const bool act = r < L0;
+      float2* row = Uh + (act ? r : 0) * RP;
       float2 w[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
-        const int f = t + T * e;
-        // bins above M1 are conjugate mirrors; slot 0 holds DC + i Nyquist
-        float2 ya = czero(), yb = czero();
-        if (act) {
-          const int idx = f < M1 ? f : (f == M1 ? 0 : P1 - f);
-          const float2 a = ra[idx], b = rb[idx];
-          if (f == 0) {
-            ya = make_float2(a.x, 0.f);
-            yb = make_float2(b.x, 0.f);
-          } else if (f == M1) {
-            ya = make_float2(a.y, 0.f);
-            yb = make_float2(b.y, 0.f);
-          } else if (f < M1) {
-            ya = a;
-            yb = b;
-          } else {
-            ya = c_conj(a);
-            yb = c_conj(b);
-          }
+        const int g = t + T * e;
+        float2 Yg, Ym;
+        if (g == 0) {
+          const float2 s0 = row[0];
+          Yg = make_float2(s0.x, 0.f);
+          Ym = make_float2(s0.y, 0.f);
+        } else {
+          Yg = row[g];
+          Ym = row[M1 - g];
         }
-        w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
+        w[e] = act ? c2r_pair(Yg, Ym, twiddle<ilog2(P1), false>(g)) : czero();
       }
-      if constexpr (T == 1) __syncthreads();
-      BlockFFT<P1, E, true>::run(w, t, ScrS<1>{ra}, act);
+      BlockFFT<M1, E, true>::run(w, t, ScrS<1>{row}, act);
       if (act) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const int n = t + T * e;
-          if (CIRC || n < L1) ra[n] = w[e];
+          const int m = t + T * e;
+          if (CIRC || 2 * m < L1) row[m] = w[e];
         }
       }
     }
@@ -399,12 +400,12 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   __syncthreads();
 
   // 4. outer gate and store (coalesced along rows)
-  batched_copy<L0 * L1, NT, 8>(
-      tid, [&](int i) { return ld1(x2 + base + i); },
-      [&](int i, float g) {
-        const int r = i / L1, col = i - r * L1;
-        const float2 q = Uh[(r & ~1) * RP + col];
-        st1(y + base + i, g * ((r & 1) ? q.y : q.x));
+  batched_copy<L0 * L1 / 2, NT, 8>(
+      tid, [&](int i) { return ld2(x2 + base + 2 * i); },
+      [&](int i, float2 g) {
+        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+        const float2 q = Uh[r * RP + m];
+        st2(y + base + 2 * i, make_float2(g.x * q.x, g.y * q.y));
       });
 }
 
