@@ -220,13 +220,18 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   const size_t base = (size_t)img * L0 * L1;
   const int tid = threadIdx.x;
 
+  // The normalisation 1 / (4 P0 P1) of the two unnormalised inverses and of
+  // the doubled R2C outputs is a power of two: it is applied, exactly, to k
+  // and D on the way in.
+  constexpr float scale = 1.f / (4.f * (float)P0 * (float)P1);
+
   // 0. stage the real rows of u = x1 v and k (coalesced along rows); row r of
   //    Uh holds the even/odd packed line u[r][2m] + i u[r][2m+1].
   batched_copy<L0 * L1 / 2, NT, 8>(
       tid,
       [&](int i) {
         const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i), kk = ld2(k + base + 2 * i);
-        return make_float4(a.x * b.x, a.y * b.y, kk.x, kk.y);
+        return make_float4(a.x * b.x, a.y * b.y, kk.x * scale, kk.y * scale);
       },
       [&](int i, float4 z) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
@@ -242,7 +247,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       using Map = LaneMap<T, NT>;
       static_assert(Map::kLines == LR, "lines per round");
       const int l = l0 + Map::line(tid), t = Map::t(tid);
-      const bool act = l < 2 * L0;
+      const bool act = (2 * L0) % LR == 0 || l < 2 * L0;  // all lanes busy when rounds are full
       float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
       float2 w[E];
 #pragma unroll
@@ -291,13 +296,12 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   //    complex column DC + i Nyquist of the two real columns 0 and M1.
   {
     constexpr int E = F::EC, T = F::TC, CR = F::CR;
-    const float twoD = 2.f * ld1(Dp + c);
-    const float scale = 1.f / (4.f * (float)P0 * (float)P1);
+    const float twoD = 2.f * scale * ld1(Dp + c);
     for (int c0 = 0; c0 < M1; c0 += CR) {
       using Map = LaneMap<T, NT>;
       static_assert(Map::kLines == CR, "groups per round");
       const int grp = c0 + Map::line(tid), t = Map::t(tid);
-      const bool act = grp < M1;
+      const bool act = M1 % CR == 0 || grp < M1;
       const bool nyq = act && grp == 0;
       const int col = act ? grp : 0;
       float2 wu[E], wk[E];
@@ -334,8 +338,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         const float2 ub = c_scale(make_float2(zu.y + zum.y, zum.x - zu.x), 0.5f);
         const float2 ka = c_scale(make_float2(zk.x + zkm.x, zk.y - zkm.y), 0.5f);
         const float2 kb = c_scale(make_float2(zk.y + zkm.y, zkm.x - zk.x), 0.5f);
-        const float2 ya = c_scale(gated_product(ua, ka, twoD), scale);
-        const float2 yb = c_scale(gated_product(ub, kb, twoD), scale);
+        const float2 ya = gated_product(ua, ka, twoD);
+        const float2 yb = gated_product(ub, kb, twoD);
         // Y = Ya + i Yb; both products are Hermitian, so at -f it is conj Ya + i conj Yb
         *u0(f) = make_float2(ya.x - yb.y, ya.y + yb.x);
         if (fm != f) *u0(fm) = make_float2(ya.x + yb.y, yb.x - ya.y);
@@ -346,7 +350,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         for (int e = 0; e < E; ++e) wu[e] = *u0(t + T * e);
       } else {
 #pragma unroll
-        for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
+        for (int e = 0; e < E; ++e) wu[e] = gated_product(wu[e], wk[e], twoD);
       }
       BlockFFT<P0, E, true>::run(wu, t, su, act);
       __syncthreads();  // scratch reads of the last exchange are done
@@ -370,7 +374,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       using Map = LaneMap<T, NT>;
       static_assert(Map::kLines == RI, "rows per round");
       const int r = r0 + Map::line(tid), t = Map::t(tid);
-      const bool act = r < L0;
+      const bool act = L0 % RI == 0 || r < L0;
       float2* row = Uh + (act ? r : 0) * RP;
       float2 w[E];
 #pragma unroll
