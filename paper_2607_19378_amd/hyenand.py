@@ -123,30 +123,46 @@ def _ptr(t) -> int:
     return int(t.data_ptr())
 
 
+class Prepared:
+    """One hyenand_fftconv call with its arguments checked and marshalled
+    once; calling the object enqueues the work again on the same buffers and
+    stream (for loops that repeat a call, where per-call Python work would
+    otherwise delay the launches)."""
+
+    def __init__(self, y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None):
+        import torch
+        ts = (x1, x2, v, k, y)
+        shape = tuple(x1.shape)
+        for t in ts:
+            if not t.is_cuda:
+                raise ValueError("all tensors must be on the GPU")
+            if tuple(t.shape) != shape or t.dtype != x1.dtype:
+                raise ValueError("x1, x2, v, k, y must share shape and dtype")
+            if not t.is_contiguous():
+                raise ValueError("tensors must be contiguous")
+        if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():
+            raise ValueError("D must be a contiguous [C] GPU tensor of the same dtype")
+        nd, dims = _dims(shape)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        ws_ptr, ws_bytes = None, 0
+        if workspace is not None:
+            ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
+        self._fn = lib().hyenand_fftconv
+        self._args = (_ptr(x1), _ptr(x2), _ptr(v), _ptr(k), _ptr(D), _ptr(y), nd, dims, _mode(pad_mode),
+                      _dtype_code(x1.dtype), ws_ptr, ws_bytes, ctypes.c_void_p(stream.cuda_stream))
+        self._keep = (y, x1, x2, v, k, D, workspace, stream)  # the buffers outlive the object
+
+    def __call__(self) -> None:
+        status = self._fn(*self._args)
+        if status != OK:
+            _check(status)
+
+
 def fftconv_into(y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None,
                  stream=None) -> None:
     """y <- x2 * (k conv (x1*v) + D*(x1*v)); all tensors already allocated on the GPU."""
-    import torch
-    ts = (x1, x2, v, k, y)
-    shape = tuple(x1.shape)
-    for t in ts:
-        if not t.is_cuda:
-            raise ValueError("all tensors must be on the GPU")
-        if tuple(t.shape) != shape or t.dtype != x1.dtype:
-            raise ValueError("x1, x2, v, k, y must share shape and dtype")
-        if not t.is_contiguous():
-            raise ValueError("tensors must be contiguous")
-    if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():
-        raise ValueError("D must be a contiguous [C] GPU tensor of the same dtype")
-    nd, dims = _dims(shape)
-    if stream is None:
-        stream = torch.cuda.current_stream(x1.device)
-    ws_ptr, ws_bytes = None, 0
-    if workspace is not None:
-        ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
-    _check(lib().hyenand_fftconv(_ptr(x1), _ptr(x2), _ptr(v), _ptr(k), _ptr(D), _ptr(y), nd, dims,
-                                 _mode(pad_mode), _dtype_code(x1.dtype), ws_ptr, ws_bytes,
-                                 ctypes.c_void_p(stream.cuda_stream)))
+    Prepared(y, x1, x2, v, k, D, pad_mode, workspace, stream)()
 
 
 def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None):

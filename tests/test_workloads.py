@@ -70,3 +70,22 @@ def test_random_case_dtypes(dtype):
     for a in (inp.x1, inp.x2, inp.v, inp.k):
         assert a.dtype == want and a.shape == (2, 3, 8, 4)
     assert inp.D.shape == (3,)
+
+
+def test_bench_algorithmic_flops():
+    """Per-call flop count used for the ALU roofline: three pruned real FFTs
+    (5 n log2 n complex, 2.5 n log2 n real), 6 flops per half-spectrum
+    product, 4 per output.  The 64x64 image (128x128 padded) written out:
+    forward rows 64 x 2.5*128*7, forward columns 65 x 5*128*7 (u and k),
+    inverse columns 65 x 5*128*7, inverse rows 64 x 2.5*128*7."""
+    import bench
+    w = W.WORKLOADS["conv2d_64"]
+    fwd = 64 * 2.5 * 128 * 7 + 65 * 5 * 128 * 7
+    inv = 65 * 5 * 128 * 7 + 64 * 2.5 * 128 * 7
+    per_img = 2 * fwd + inv + 6 * 128 * 65 + 4 * 64 * 64
+    assert bench.alg_flops(w) == per_img * 8 * 256
+    # 1D 2^20 linear: real transforms of 2^21 points
+    w = W.WORKLOADS["conv1d_1m"]
+    n = 2 ** 21
+    per_line = 3 * 2.5 * n * 21 + 6 * (n // 2 + 1) + 4 * 2 ** 20
+    assert abs(bench.alg_flops(w) - per_line * 256) < 1e-6 * per_line
