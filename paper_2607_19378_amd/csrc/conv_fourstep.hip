@@ -66,6 +66,8 @@ __global__ void __launch_bounds__(512)
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
   static_assert(NT / T >= TL, "one round covers the tile");
   __shared__ float2 tile[N1 * TLP];  // exchange scratch, one column per line
+  __shared__ float2 twl[imax(1, PassTw<N1, E>::kCount)];
+  PassTw<N1, E>::fill(twl, threadIdx.x, NT);
   const int ntile = N2 / TL;
   const int sig = (int)(blockIdx.x & 1);  // 0: u = x1 v, 1: k
   const int64_t rest = blockIdx.x >> 1;
@@ -97,7 +99,7 @@ __global__ void __launch_bounds__(512)
       }
     }
   }
-  BlockFFT<N1, E, false>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act);
+  BlockFFT<N1, E, false>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act, twl);
   if (act) {
     // exp(-2 pi i m2 f1 / M) for f1 = t + T e, then A[f1][m2]
     const uint32_t m2 = (uint32_t)(c0 + cc);
@@ -117,6 +119,8 @@ __global__ void __launch_bounds__(512)
   constexpr int RS = pad16_size(N2);
   constexpr int IPT = N2 / NT;
   __shared__ float2 R[4][RS];  // u row a, u row b, k row a, k row b
+  __shared__ float2 twl[PassTw<N2, E>::kCount];
+  PassTw<N2, E>::fill(twl, threadIdx.x, NT);
   const int npair = N1 / 2 + 1;
   const int64_t line = blockIdx.x / npair;
   const int fa = (int)(blockIdx.x % npair);
@@ -153,7 +157,7 @@ __global__ void __launch_bounds__(512)
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) w[e] = act ? *sc(t + T * e) : czero();
-    BlockFFT<N2, E, false>::run(w, t, sc, act);
+    BlockFFT<N2, E, false>::run(w, t, sc, act, twl);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) *sc(t + T * e) = w[e];
@@ -199,7 +203,7 @@ __global__ void __launch_bounds__(512)
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) w[e] = act ? *sc(t + T * e) : czero();
-    BlockFFT<N2, E, true>::run(w, t, sc, act);
+    BlockFFT<N2, E, true>::run(w, t, sc, act, twl);
     if (act) {
       // exp(+2 pi i f1 m2 / M) for m2 = t + T e
       twiddle_run<E>(w, twiddle_rt<true>(f1 * (uint32_t)t, log2M), twiddle_rt<true>(f1 * (uint32_t)T, log2M));
@@ -218,6 +222,8 @@ __global__ void __launch_bounds__(512)
   constexpr int NOUT = CIRC ? N1 : N1 / 2;  // cropped rows m1
   static_assert(NT / T >= TL, "one round covers the tile");
   __shared__ float2 tile[N1 * TLP];  // exchange scratch, one column per line
+  __shared__ float2 twl[imax(1, PassTw<N1, E>::kCount)];
+  PassTw<N1, E>::fill(twl, threadIdx.x, NT);
   const int ntile = N2 / TL;
   // the x2/y runs of neighbouring tiles share cache lines: keep them on one XCD
   const uint32_t bid = xcd_order(blockIdx.x, gridDim.x);
@@ -242,7 +248,7 @@ __global__ void __launch_bounds__(512)
     const int m1 = t + T * e;
     g[e] = (act && (CIRC || m1 < NOUT)) ? ld2(x2 + gbase + 2 * (size_t)m1 * N2) : czero();
   }
-  BlockFFT<N1, E, true>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act);
+  BlockFFT<N1, E, true>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act, twl);
   if (act) {
     // unpack y[2m], y[2m+1] and gate
 #pragma unroll

@@ -48,10 +48,20 @@ __global__ void __launch_bounds__(fused1d_nt(P))
   constexpr int L = F::L, M = F::M, MNZ = F::MNZ, NT = F::NT;
   __shared__ float2 Ub[F::LDSN];
   __shared__ float2 Kb[F::LDSN];
+  // pass twiddles in LDS where they fit beside the two lines
+  using TwF = PassTw<M, F::EF>;
+  using TwI = PassTw<M, F::EI>;
+  constexpr bool kTwl = (2 * F::LDSN + TwF::kCount + TwI::kCount) * 8 <= 150 * 1024;
+  __shared__ float2 twf[kTwl ? imax(1, TwF::kCount) : 1];
+  __shared__ float2 twi[kTwl ? imax(1, TwI::kCount) : 1];
   const int line = blockIdx.x;
   const int c = line % C;
   const size_t base = (size_t)line * L;
   const int tid = threadIdx.x;
+  if constexpr (kTwl) {
+    TwF::fill(twf, tid, NT);
+    TwI::fill(twi, tid, NT);
+  }
 
   // stage the even/odd packed real lines u = x1 v and k
   if constexpr (L >= 2) {
@@ -84,7 +94,8 @@ __global__ void __launch_bounds__(fused1d_nt(P))
       const int m = t + T * e;
       w[e] = (act && m < MNZ) ? *scr(m) : czero();
     }
-    BlockFFT<M, E, false>::run(w, t, scr, act);
+    if constexpr (kTwl) BlockFFT<M, E, false>::run(w, t, scr, act, twf);
+    else BlockFFT<M, E, false>::run(w, t, scr, act);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) *scr(t + T * e) = w[e];
@@ -119,7 +130,8 @@ __global__ void __launch_bounds__(fused1d_nt(P))
       }
     }
     if constexpr (T == 1) __syncthreads();
-    BlockFFT<M, E, true>::run(w, t, su, act);
+    if constexpr (kTwl) BlockFFT<M, E, true>::run(w, t, su, act, twi);
+    else BlockFFT<M, E, true>::run(w, t, su, act);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {

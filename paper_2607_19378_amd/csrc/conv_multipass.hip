@@ -84,10 +84,12 @@ __global__ void __launch_bounds__(256)
   constexpr int MNZ = (LL + 1) / 2;
   __shared__ float2 Ur[RPW * HP];
   __shared__ float2 Kr[RPW * HP];
+  __shared__ float2 twl[imax(1, PassTw<ML, E>::kCount)];
   const int64_t total_rows = (int64_t)nlines * rows;
   const int64_t row0 = (int64_t)blockIdx.x * RPW;
   const int nrow = (int)((total_rows - row0) < RPW ? (total_rows - row0) : RPW);
   const int tid = threadIdx.x;
+  PassTw<ML, E>::fill(twl, tid, NT);
 
   // stage real rows (the input rows of the chunk are contiguous), four
   // samples per global load, written to LDS as two 8-byte pairs
@@ -155,7 +157,7 @@ __global__ void __launch_bounds__(256)
       const int m = t + T * e;
       w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
     }
-    BlockFFT<ML, E, false>::run(w, t, ScrS<1>{row}, act);
+    BlockFFT<ML, E, false>::run(w, t, ScrS<1>{row}, act, twl);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
@@ -275,6 +277,8 @@ __global__ void __launch_bounds__(kTileNT)
   constexpr int L1 = CIRC ? P1 : P1 / 2;
   constexpr int NT = kTileNT;
   __shared__ float2 tile[NS][P1 * TLP];
+  __shared__ float2 twl[imax(1, PassTw<P1, E>::kCount)];
+  PassTw<P1, E>::fill(twl, threadIdx.x, NT);
   const int ntile = (H + TL - 1) / TL;
   const int64_t bid = blockIdx.x;
   const int tl = (int)(bid % ntile);
@@ -302,7 +306,7 @@ __global__ void __launch_bounds__(kTileNT)
       const int n = t + T * e;
       w[e] = (act && (INV || CIRC || n < L1)) ? col[n * TLP] : czero();
     }
-    BlockFFT<P1, E, INV>::run(w, t, ScrS<TLP>{col}, act);
+    BlockFFT<P1, E, INV>::run(w, t, ScrS<TLP>{col}, act, twl);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) col[(t + T * e) * TLP] = w[e];
@@ -338,11 +342,13 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
   using Cf = CoreCfg<P0, CIRC>;
   constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T, NT = Cf::NT, L0 = Cf::L0, KPT = Cf::KPT;
   __shared__ float2 tile[P0 * TLP];
+  __shared__ float2 twl[imax(1, PassTw<P0, E>::kCount)];
   const int ntile = (ncols + TL - 1) / TL;
   const int tl = (int)(blockIdx.x % ntile);
   const int64_t line = blockIdx.x / ntile;
   const int col0 = tl * TL;
   const int tid = threadIdx.x;
+  PassTw<P0, E>::fill(twl, tid, NT);
   const int c = (int)((line0 + line) % C);
   const float Dv = dbf16 ? ld1((const uint16_t*)Dp + c) : ld1((const float*)Dp + c);
   const float twoD = 2.f * Dv;
@@ -375,7 +381,7 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
     const int n = t + T * e;
     wu[e] = (act && (CIRC || n < L0)) ? col[n * TLP] : czero();
   }
-  BlockFFT<P0, E, false>::run(wu, t, sc, act);
+  BlockFFT<P0, E, false>::run(wu, t, sc, act, twl);
   __syncthreads();  // every lane is done with U's tile
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
@@ -388,11 +394,11 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
     const int n = t + T * e;
     wk[e] = (act && (CIRC || n < L0)) ? col[n * TLP] : czero();
   }
-  BlockFFT<P0, E, false>::run(wk, t, sc, act);
+  BlockFFT<P0, E, false>::run(wk, t, sc, act, twl);
 #pragma unroll
   for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
   if constexpr (T == 1) __syncthreads();
-  BlockFFT<P0, E, true>::run(wu, t, sc, act);
+  BlockFFT<P0, E, true>::run(wu, t, sc, act, twl);
   if (act) {
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -427,10 +433,12 @@ __global__ void __launch_bounds__(256)
   constexpr int LL = CIRC ? PL : PL / 2;
   constexpr int ML = PL / 2;
   __shared__ float2 reg[PPW * PRP];
+  __shared__ float2 twl[imax(1, PassTw<PL, E>::kCount)];
   const int64_t total_pairs = (int64_t)nlines * rows / 2;
   const int64_t pair0 = (int64_t)blockIdx.x * PPW;
   const int npair = (int)((total_pairs - pair0) < PPW ? (total_pairs - pair0) : PPW);
   const int tid = threadIdx.x;
+  PassTw<PL, E>::fill(twl, tid, NT);
 
   // load the half-spectrum rows of each pair: row a at [0, H), row b at [H, 2H)
   batched_copy<PPW * 2 * H, NT, 8>(
@@ -474,7 +482,7 @@ __global__ void __launch_bounds__(256)
       w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
     }
     if constexpr (T == 1) __syncthreads();
-    BlockFFT<PL, E, true>::run(w, t, ScrS<1>{R}, act);
+    BlockFFT<PL, E, true>::run(w, t, ScrS<1>{R}, act, twl);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {

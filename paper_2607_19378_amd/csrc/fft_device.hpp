@@ -186,6 +186,78 @@ struct ScrOff<ScrPad16> {
 };
 
 // ---------------------------------------------------------------------------
+// Pass twiddles of BlockFFT<N, E> staged in LDS.  When the lanes of a
+// wavefront need different twiddles, reading them from the global pass table
+// costs a vector-memory round trip per pass; a workgroup instead copies the
+// tables of all its passes into LDS once.  Pass (NS, R) keeps rows r = 1..R-1
+// ([r-1][jm], as in the global table) when that is at most kFullMax entries,
+// else only rows r = 1, 2, 4, 8 ([log2 r][jm]); the other rows are then formed
+// as products of those (at most three roundings more).
+// ---------------------------------------------------------------------------
+template <int N, int E>
+struct PassTw {
+  static constexpr int kFullMax = 512;
+  static constexpr int radix(int ns) { return (N / ns >= E) ? E : N / ns; }
+  static constexpr bool full(int ns) { return (radix(ns) - 1) * ns <= kFullMax; }
+  static constexpr int rows(int ns) { return full(ns) ? radix(ns) - 1 : ilog2(radix(ns)); }
+  static constexpr int offset(int ns) {  // entries before the pass of stride ns
+    int off = 0;
+    for (int s = 1; s < ns; s *= radix(s))
+      if (s > 1) off += rows(s) * s;
+    return off;
+  }
+  static constexpr int kCount = offset(N);
+
+  // Copy from the global tables; every lane of the workgroup calls it with
+  // its id and the workgroup size, and the caller synchronises afterwards.
+  template <int NS = 1>
+  static __device__ __forceinline__ void fill(float2* lds, int tid, int nt) {
+    if constexpr (NS < N) {
+      constexpr int R = radix(NS);
+      if constexpr (NS > 1) {
+        constexpr int off = offset(NS), cnt = rows(NS) * NS;
+        constexpr uint32_t g = (uint32_t)kPassOff[ilog2(NS)][ilog2(R)];
+        for (int i = tid; i < cnt; i += nt) {
+          const int q = i / NS, jm = i - q * NS;
+          const int r = full(NS) ? q + 1 : (1 << q);
+          lds[off + i] = kPassTw[g + (uint32_t)(r - 1) * NS + jm];
+        }
+      }
+      fill<NS * R>(lds, tid, nt);
+    }
+  }
+
+  // x[r] *= W^(jm r), r = 1..R-1, W = exp(-+2 pi i / (NS R))
+  template <int NS, int R, bool INV>
+  static __device__ __forceinline__ void apply(const float2* lds, uint32_t jm, float2 (&x)[R]) {
+    constexpr int off = offset(NS);
+    if constexpr (full(NS)) {
+#pragma unroll
+      for (int r = 1; r < R; ++r) {
+        const float2 w = lds[off + (r - 1) * NS + jm];
+        x[r] = c_mul(x[r], INV ? c_conj(w) : w);
+      }
+    } else {
+      float2 p[R];
+#pragma unroll
+      for (int q = 0; (1 << q) < R; ++q) {
+        const float2 w = lds[off + q * NS + jm];
+        p[1 << q] = INV ? c_conj(w) : w;
+      }
+#pragma unroll
+      for (int r = 3; r < R; ++r) {
+        if ((r & (r - 1)) != 0) {
+          const int hi = 1 << ilog2(r);
+          p[r] = c_mul(p[hi], p[r - hi]);
+        }
+      }
+#pragma unroll
+      for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], p[r]);
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
 // Block transform: N points over T = N/E lanes, E points per lane.
 // All lanes of the workgroup must call run() the same number of times (it
 // contains workgroup barriers when N > E).  Inactive lanes pass active=false:
@@ -199,7 +271,13 @@ struct BlockFFT {
 
   template <class Scr>
   static __device__ __forceinline__ void run(float2 (&v)[E], int t, const Scr& scr, bool active) {
-    pass<1>(v, t, scr, active);
+    pass<1>(v, t, scr, active, nullptr);
+  }
+  // Same, with the pass twiddles read from PassTw<N, E> tables in LDS.
+  template <class Scr>
+  static __device__ __forceinline__ void run(float2 (&v)[E], int t, const Scr& scr, bool active,
+                                             const float2* lds_tw) {
+    pass<1, Scr, true>(v, t, scr, active, lds_tw);
   }
 
   // Pass-16 layout: positions dst + r*NS (r < R) reachable by constant offsets
@@ -212,8 +290,9 @@ struct BlockFFT {
     return T % 16 == 0 ? (T * e) + (T * e) / 16 : T * (e % (16 / T)) + 17 * (e / (16 / T));
   }
 
-  template <int NS, class Scr>
-  static __device__ __forceinline__ void pass(float2 (&v)[E], int t, const Scr& scr, bool active) {
+  template <int NS, class Scr, bool LTW = false>
+  static __device__ __forceinline__ void pass(float2 (&v)[E], int t, const Scr& scr, bool active,
+                                              const float2* lds_tw) {
     constexpr int R = (N / NS >= E) ? E : N / NS;
     constexpr int NB = E / R;  // butterflies per lane in this pass
     if (active) {  // waves with no active lane skip the arithmetic
@@ -224,8 +303,12 @@ struct BlockFFT {
         for (int r = 0; r < R; ++r) x[r] = v[b + NB * r];
         if constexpr (NS > 1) {
           const uint32_t jm = (uint32_t)(t + T * b) & (NS - 1);
+          if constexpr (LTW) {
+            PassTw<N, E>::template apply<NS, R, INV>(lds_tw, jm, x);
+          } else {
 #pragma unroll
-          for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], pass_twiddle<NS, R, INV>(jm, r));
+            for (int r = 1; r < R; ++r) x[r] = c_mul(x[r], pass_twiddle<NS, R, INV>(jm, r));
+          }
         }
         dft<R, INV>(x);
 #pragma unroll
@@ -265,7 +348,7 @@ struct BlockFFT {
           for (int e = 0; e < E; ++e) v[e] = *scr(t + T * e);
         }
       }
-      pass<NS * R>(v, t, scr, active);
+      pass<NS * R, Scr, LTW>(v, t, scr, active, lds_tw);
     }
   }
 };
@@ -282,9 +365,11 @@ template <int T, int NT>
 struct LaneMap {
   static constexpr bool kUniform = T * 64 <= NT;
   static constexpr int kLines = NT / T;
+  // the final mask tells the compiler that t < T (tid < NT), so positions
+  // t + T e known to be padding or outside the crop are compile-time facts
   static __device__ __forceinline__ int t(int tid) {
-    if constexpr (kUniform) return __builtin_amdgcn_readfirstlane((tid >> 6) % T);
-    else return tid / kLines;
+    if constexpr (kUniform) return __builtin_amdgcn_readfirstlane((tid >> 6) % T) & (T - 1);
+    else return (tid / kLines) & (T - 1);
   }
   static __device__ __forceinline__ int line(int tid) {
     if constexpr (kUniform) return ((tid >> 6) / T) * 64 + (tid & 63);
