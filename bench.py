@@ -147,6 +147,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true", help="skip the sampled oracle check (profiling runs)")
+    ap.add_argument("--no-stream-peak", action="store_true", help="skip the 1 GiB copy that measures the stream peak")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -229,6 +230,26 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+
+    # measured stream peak: a 1 GiB device-to-device copy (read + write), best of 5
+    stream_gbs = None
+    if not args.no_stream_peak:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        best = None
+        for _ in range(6):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            dst.copy_(src)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            best = ms if best is None else min(best, ms)
+        stream_gbs = 2.0 * src.numel() * 4 / (best * 1e-3) / 1e9
+        del src, dst
+        roofline["stream_peak_gbs"] = round(stream_gbs, 1)
+        roofline["hbm_frac_of_stream_peak"] = round(hbm_gbs / stream_gbs, 4)
 
     parity = None
     if not args.no_parity:
