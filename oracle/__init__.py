@@ -12,7 +12,10 @@ The arithmetic lives in ``oracle.c`` (plain C, IEEE double):
   3.2) as an explicit sum;
 * :func:`conv_fft` evaluates it through the convolution theorem with the C
   file's own radix-2 FFT;
-* :func:`fft1d` exposes that FFT so it can be pinned against a naive DFT.
+* :func:`fft1d` exposes that FFT so it can be pinned against a naive DFT;
+* :func:`backward_direct` / :func:`backward_fft` give the gradients of a
+  scalar loss through y (gx1, gx2, gv, gk, gD for a given gy = dLoss/dy), as
+  explicit sums and through the FFT.
 
 Inputs are float64 arrays of shape [B, C, L1, ..., LN] (x1, x2, v, k) and [C]
 (D).  ``pad_mode`` is "linear" (zero-padded, cropped to the first L_d outputs
@@ -62,7 +65,11 @@ def lib():
             L.oracle_direct_points.argtypes = sig + [ctypes.c_int, _i64p, ctypes.c_int, _i64p,
                                                      ctypes.c_int64, _f64p, ctypes.c_int]
             L.oracle_fft1d.argtypes = [_f64p, ctypes.c_int64, ctypes.c_int]
-            for f in (L.oracle_direct, L.oracle_fft, L.oracle_direct_points, L.oracle_fft1d):
+            bsig = [_f64p] * 11 + [ctypes.c_int, _i64p, ctypes.c_int, ctypes.c_int]
+            L.oracle_backward_direct.argtypes = bsig
+            L.oracle_backward_fft.argtypes = bsig
+            for f in (L.oracle_direct, L.oracle_fft, L.oracle_direct_points, L.oracle_fft1d,
+                      L.oracle_backward_direct, L.oracle_backward_fft):
                 f.restype = ctypes.c_int
             _lib = L
         return _lib
@@ -149,3 +156,28 @@ def fft1d(x, sign=-1):
     if rc != 0:
         raise RuntimeError(f"oracle_fft1d returned {rc}")
     return a
+
+
+def _backward(fn, x1, x2, v, k, D, gy, pad_mode, nthreads):
+    arrs, dims, nd = _prep(x1, x2, v, k, D)
+    g = np.ascontiguousarray(gy, dtype=np.float64)
+    if g.shape != arrs[0].shape:
+        raise ValueError("gy must have the shape of y")
+    outs = [np.zeros(arrs[0].shape, dtype=np.float64) for _ in range(4)]
+    gD = np.zeros(arrs[4].shape, dtype=np.float64)
+    rc = fn(*[_ptr(a) for a in arrs], _ptr(g), *[_ptr(o) for o in outs], _ptr(gD), nd,
+            dims.ctypes.data_as(_i64p), _mode(pad_mode), int(nthreads or default_threads()))
+    if rc != 0:
+        raise RuntimeError(f"oracle returned {rc}")
+    gx1, gx2, gv, gk = outs
+    return gx1, gx2, gv, gk, gD
+
+
+def backward_direct(x1, x2, v, k, D, gy, pad_mode="linear", nthreads=None):
+    """(gx1, gx2, gv, gk, gD) for dLoss/dy = gy, by explicit sums (any extents)."""
+    return _backward(lib().oracle_backward_direct, x1, x2, v, k, D, gy, pad_mode, nthreads)
+
+
+def backward_fft(x1, x2, v, k, D, gy, pad_mode="linear", nthreads=None):
+    """(gx1, gx2, gv, gk, gD) through the convolution theorem (power-of-two extents)."""
+    return _backward(lib().oracle_backward_fft, x1, x2, v, k, D, gy, pad_mode, nthreads)

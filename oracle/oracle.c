@@ -34,6 +34,26 @@
  * Layout: every tensor is contiguous row-major [B, C, L1, ..., LN]; D is [C].
  * dims = {B, C, L1, ..., LN}, ndim = N in {1, 2, 3}.
  *
+ * Backward (gradients of a scalar loss through y; the derivatives of the
+ * definition above, written out -- the paper trains HyenaND end to end through
+ * this operator but prints no backward formulas): with gy = dLoss/dy,
+ *
+ *   z   = conv + D[c] u                 (pre-gate output)
+ *   gx2 = gy * z
+ *   h   = gy * x2                       (dLoss/dz)
+ *   gu[j] = sum_n k[n - j] h[n] + D[c] h[j]      (adjoint of u -> k * u;
+ *           linear: n_d >= j_d, n_d < L_d; circular: (n - j) mod L)
+ *   gk[m] = sum_n h[n] u[n - m]                  (linear: n_d >= m_d;
+ *           circular: u[(n - m) mod L])
+ *   gx1 = gu * v,  gv = gu * x1,  gD[c] = sum_{b, n} h[b,c,n] u[b,c,n]
+ *
+ *   oracle_backward_direct : these sums written out (any extents).
+ *   oracle_backward_fft    : the same through this file's FFT: on the
+ *       transform grid the adjoint of a convolution with k is the product
+ *       with conj(K) (k real), so gu = crop(IFFT(conj(K) H)) + D h and
+ *       gk = crop(IFFT(conj(U) H)); zero padding to 2 L_d makes the cyclic
+ *       sums equal the linear ones on the cropped range.
+ *
  * Return codes: 0 ok, 1 bad argument, 2 out of memory, 3 the inverse
  * transform left an imaginary residue above 1e-9 of the real part (a broken
  * FFT), 4 a thread could not be started.
@@ -411,4 +431,268 @@ int oracle_fft(const double *x1, const double *x2, const double *v, const double
     return rc;
 }
 
-int oracle_version(void) { return 1; }
+/* ------------------------------------------------------------------------- */
+/* Backward                                                                   */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+    const double *x1, *x2, *v, *k, *D, *gy;
+    double *gx1, *gx2, *gv, *gk, *hu; /* hu: per-line sum of h u */
+    const geom *g;
+    int circular;
+    int tid, nthreads;
+    int status;
+    const cplx *const *tw_fwd;
+    const cplx *const *tw_inv;
+} bjob;
+
+static void unflat(const geom *g, int64_t r, int64_t n[3]) {
+    n[2] = r % g->L[2];
+    n[1] = (r / g->L[2]) % g->L[1];
+    n[0] = r / (g->L[2] * g->L[1]);
+}
+
+/* Index of a - b on the grid: linear requires a_d >= b_d (else -1);
+ * circular wraps each axis. */
+static int64_t diff_index(const geom *g, const int64_t a[3], const int64_t b[3], int circular) {
+    int64_t r = 0;
+    for (int d = 0; d < 3; ++d) {
+        int64_t x = a[d] - b[d];
+        if (circular)
+            x = (x % g->L[d] + g->L[d]) % g->L[d];
+        else if (x < 0)
+            return -1;
+        r = r * g->L[d] + x;
+    }
+    return r;
+}
+
+static void *backward_direct_worker(void *arg) {
+    bjob *J = (bjob *)arg;
+    const geom *g = J->g;
+    const int64_t box = g->box;
+    double *u = (double *)malloc((size_t)box * sizeof(double));
+    double *h = (double *)malloc((size_t)box * sizeof(double));
+    if (!u || !h) {
+        free(u); free(h);
+        J->status = 2;
+        return NULL;
+    }
+    for (int64_t line = J->tid; line < g->B * g->C; line += J->nthreads) {
+        const int64_t base = line * box, c = line % g->C;
+        const double *K = J->k + base;
+        for (int64_t i = 0; i < box; ++i) {
+            u[i] = J->x1[base + i] * J->v[base + i];
+            h[i] = J->gy[base + i] * J->x2[base + i];
+        }
+        double hu = 0.0;
+        for (int64_t i = 0; i < box; ++i) hu += h[i] * u[i];
+        J->hu[line] = hu;
+        for (int64_t i = 0; i < box; ++i) {
+            int64_t p[3], q[3];
+            unflat(g, i, p);
+            /* z[i] = sum_m k[m] u[i - m] + D u[i] */
+            double conv = 0.0, gu = 0.0, gk = 0.0;
+            for (int64_t m = 0; m < box; ++m) {
+                unflat(g, m, q);
+                int64_t im = diff_index(g, p, q, J->circular); /* i - m */
+                if (im >= 0) conv += K[m] * u[im];
+            }
+            /* gu[i] = sum_n k[n - i] h[n];  gk[i] = sum_n h[n] u[n - i] */
+            for (int64_t n = 0; n < box; ++n) {
+                unflat(g, n, q);
+                int64_t ni = diff_index(g, q, p, J->circular); /* n - i */
+                if (ni >= 0) {
+                    gu += K[ni] * h[n];
+                    gk += h[n] * u[ni];
+                }
+            }
+            const double z = conv + J->D[c] * u[i];
+            J->gx2[base + i] = J->gy[base + i] * z;
+            gu += J->D[c] * h[i];
+            J->gx1[base + i] = gu * J->v[base + i];
+            J->gv[base + i] = gu * J->x1[base + i];
+            J->gk[base + i] = gk;
+        }
+    }
+    free(u);
+    free(h);
+    return NULL;
+}
+
+static void *backward_fft_worker(void *arg) {
+    bjob *J = (bjob *)arg;
+    const geom *g = J->g;
+    int64_t P[3];
+    int64_t tot = 1, maxP = 1;
+    transform_extents(g, J->circular, P);
+    for (int d = 0; d < 3; ++d) {
+        tot *= P[d];
+        if (P[d] > maxP) maxP = P[d];
+    }
+    cplx *U = (cplx *)malloc((size_t)tot * sizeof(cplx));
+    cplx *K = (cplx *)malloc((size_t)tot * sizeof(cplx));
+    cplx *H = (cplx *)malloc((size_t)tot * sizeof(cplx));
+    cplx *Z = (cplx *)malloc((size_t)tot * sizeof(cplx));
+    cplx *tmp = (cplx *)malloc((size_t)maxP * sizeof(cplx));
+    if (!U || !K || !H || !Z || !tmp) {
+        free(U); free(K); free(H); free(Z); free(tmp);
+        J->status = 2;
+        return NULL;
+    }
+    const double scale = 1.0 / (double)tot;
+    for (int64_t line = J->tid; line < g->B * g->C; line += J->nthreads) {
+        const int64_t base = line * g->box, c = line % g->C;
+        memset(U, 0, (size_t)tot * sizeof(cplx));
+        memset(K, 0, (size_t)tot * sizeof(cplx));
+        memset(H, 0, (size_t)tot * sizeof(cplx));
+        double hu = 0.0;
+        for (int64_t n0 = 0; n0 < g->L[0]; ++n0)
+            for (int64_t n1 = 0; n1 < g->L[1]; ++n1)
+                for (int64_t n2 = 0; n2 < g->L[2]; ++n2) {
+                    int64_t src = base + (n0 * g->L[1] + n1) * g->L[2] + n2;
+                    int64_t dst = (n0 * P[1] + n1) * P[2] + n2;
+                    U[dst].re = J->x1[src] * J->v[src];
+                    K[dst].re = J->k[src];
+                    H[dst].re = J->gy[src] * J->x2[src];
+                    hu += H[dst].re * U[dst].re;
+                }
+        J->hu[line] = hu;
+        for (int ax = 0; ax < 3; ++ax) {
+            fft_axis(U, P, ax, J->tw_fwd[ax], tmp);
+            fft_axis(K, P, ax, J->tw_fwd[ax], tmp);
+            fft_axis(H, P, ax, J->tw_fwd[ax], tmp);
+        }
+        /* Z = U K, then H <- conj(K) H (for gu) and K <- conj(U) H (for gk) */
+        for (int64_t i = 0; i < tot; ++i) {
+            cplx a = U[i], b = K[i], e = H[i];
+            Z[i].re = a.re * b.re - a.im * b.im;
+            Z[i].im = a.re * b.im + a.im * b.re;
+            H[i].re = b.re * e.re + b.im * e.im;
+            H[i].im = b.re * e.im - b.im * e.re;
+            K[i].re = a.re * e.re + a.im * e.im;
+            K[i].im = a.re * e.im - a.im * e.re;
+        }
+        for (int ax = 0; ax < 3; ++ax) {
+            fft_axis(Z, P, ax, J->tw_inv[ax], tmp);
+            fft_axis(H, P, ax, J->tw_inv[ax], tmp);
+            fft_axis(K, P, ax, J->tw_inv[ax], tmp);
+        }
+        double maxre = 0.0, maxim = 0.0;
+        for (int64_t n0 = 0; n0 < g->L[0]; ++n0)
+            for (int64_t n1 = 0; n1 < g->L[1]; ++n1)
+                for (int64_t n2 = 0; n2 < g->L[2]; ++n2) {
+                    int64_t src = base + (n0 * g->L[1] + n1) * g->L[2] + n2;
+                    int64_t pos = (n0 * P[1] + n1) * P[2] + n2;
+                    const cplx *outs[3] = {&Z[pos], &H[pos], &K[pos]};
+                    for (int o = 0; o < 3; ++o) {
+                        double re = fabs(outs[o]->re * scale), im = fabs(outs[o]->im * scale);
+                        if (re > maxre) maxre = re;
+                        if (im > maxim) maxim = im;
+                    }
+                    const double u = J->x1[src] * J->v[src];
+                    const double hh = J->gy[src] * J->x2[src];
+                    const double z = Z[pos].re * scale + J->D[c] * u;
+                    const double gu = H[pos].re * scale + J->D[c] * hh;
+                    J->gx2[src] = J->gy[src] * z;
+                    J->gx1[src] = gu * J->v[src];
+                    J->gv[src] = gu * J->x1[src];
+                    J->gk[src] = K[pos].re * scale;
+                }
+        if (maxim > 1e-9 * (maxre > 1e-300 ? maxre : 1e-300) && maxim > 1e-200) J->status = 3;
+    }
+    free(U); free(K); free(H); free(Z); free(tmp);
+    return NULL;
+}
+
+static int run_bjobs(bjob *proto, int nthreads, void *(*fn)(void *)) {
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > 256) nthreads = 256;
+    bjob jobs[256];
+    pthread_t th[256];
+    int started[256];
+    int rc = 0;
+    for (int t = 0; t < nthreads; ++t) {
+        jobs[t] = *proto;
+        jobs[t].tid = t;
+        jobs[t].nthreads = nthreads;
+        jobs[t].status = 0;
+        started[t] = 0;
+    }
+    for (int t = 1; t < nthreads; ++t) {
+        if (pthread_create(&th[t], NULL, fn, &jobs[t]) == 0)
+            started[t] = 1;
+        else
+            rc = 4;
+    }
+    fn(&jobs[0]);
+    for (int t = 1; t < nthreads; ++t)
+        if (started[t]) pthread_join(th[t], NULL);
+    if (rc) return rc;
+    for (int t = 0; t < nthreads; ++t)
+        if (jobs[t].status) return jobs[t].status;
+    return 0;
+}
+
+static int backward_common(const double *x1, const double *x2, const double *v, const double *k,
+                           const double *D, const double *gy, double *gx1, double *gx2, double *gv,
+                           double *gk, double *gD, int ndim, const int64_t *dims, int circular,
+                           int nthreads, int use_fft) {
+    geom g;
+    if (!x1 || !x2 || !v || !k || !D || !gy || !gx1 || !gx2 || !gv || !gk || !gD ||
+        make_geom(ndim, dims, &g))
+        return 1;
+    if (use_fft)
+        for (int d = 0; d < 3; ++d)
+            if (!is_pow2(g.L[d])) return 1;
+    double *hu = (double *)calloc((size_t)(g.B * g.C), sizeof(double));
+    if (!hu) return 2;
+    int64_t P[3];
+    transform_extents(&g, circular, P);
+    cplx *twf[3] = {NULL, NULL, NULL}, *twi[3] = {NULL, NULL, NULL};
+    int rc = 0;
+    if (use_fft)
+        for (int d = 0; d < 3; ++d) {
+            twf[d] = make_twiddles(P[d], -1);
+            twi[d] = make_twiddles(P[d], +1);
+            if (!twf[d] || !twi[d]) rc = 2;
+        }
+    if (!rc) {
+        bjob J;
+        memset(&J, 0, sizeof J);
+        J.x1 = x1; J.x2 = x2; J.v = v; J.k = k; J.D = D; J.gy = gy;
+        J.gx1 = gx1; J.gx2 = gx2; J.gv = gv; J.gk = gk; J.hu = hu; J.g = &g;
+        J.circular = circular ? 1 : 0;
+        J.tw_fwd = (const cplx *const *)twf;
+        J.tw_inv = (const cplx *const *)twi;
+        rc = run_bjobs(&J, nthreads, use_fft ? backward_fft_worker : backward_direct_worker);
+    }
+    if (!rc) /* gD[c] = sum over samples, in sample order */
+        for (int64_t c = 0; c < g.C; ++c) {
+            double s = 0.0;
+            for (int64_t b = 0; b < g.B; ++b) s += hu[b * g.C + c];
+            gD[c] = s;
+        }
+    for (int d = 0; d < 3; ++d) {
+        free(twf[d]);
+        free(twi[d]);
+    }
+    free(hu);
+    return rc;
+}
+
+int oracle_backward_direct(const double *x1, const double *x2, const double *v, const double *k,
+                           const double *D, const double *gy, double *gx1, double *gx2, double *gv,
+                           double *gk, double *gD, int ndim, const int64_t *dims, int circular,
+                           int nthreads) {
+    return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 0);
+}
+
+int oracle_backward_fft(const double *x1, const double *x2, const double *v, const double *k,
+                        const double *D, const double *gy, double *gx1, double *gx2, double *gv,
+                        double *gk, double *gD, int ndim, const int64_t *dims, int circular,
+                        int nthreads) {
+    return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 1);
+}
+
+int oracle_version(void) { return 2; }
