@@ -76,6 +76,117 @@ def alg_flops(w: W.Workload) -> float:
     return per_line * w.B * w.C
 
 
+def alg_flops_backward(w: W.Workload) -> float:
+    """Backward: three forward and three inverse pruned real transforms (u, k,
+    h in; z, gu, gk out), three half-spectrum products, 8 flops per element
+    (u, h, gx2, gx1, gv and the h u sum)."""
+    import math
+    n = w.ndim
+    L = list(w.grid)
+    P = [2 * x if w.pad_mode == "linear" else x for x in L]
+    H = P[-1] // 2 + 1
+
+    def cplx(m):
+        return 5.0 * m * math.log2(m) if m > 1 else 0.0
+
+    def real(m):
+        return 2.5 * m * math.log2(m) if m > 1 else 0.0
+
+    ext = L[:-1] + [H]
+    fwd = real(P[-1]) * math.prod(L[:-1])
+    for d in range(n - 2, -1, -1):
+        fwd += cplx(P[d]) * math.prod(ext[:d] + ext[d + 1:])
+        ext[d] = P[d]
+    ext = P[:-1] + [H]
+    inv = 0.0
+    for d in range(n - 1):
+        inv += cplx(P[d]) * math.prod(ext[:d] + ext[d + 1:])
+        ext[d] = L[d]
+    inv += real(P[-1]) * math.prod(L[:-1])
+    per_line = 3 * fwd + 3 * inv + 3 * 6.0 * math.prod(P[:-1]) * H + 8.0 * math.prod(L)
+    return per_line * w.B * w.C
+
+
+def bench_backward(args, w, inp):
+    """Time hyenand_fftconv_backward on the workload (dLoss/dy a seeded
+    normal tensor); prints one JSON line of the same form as the forward's."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    rng = np.random.default_rng(w.seed + 7)
+    gy_host = W.quantise(rng.standard_normal(w.shape), w.dtype)
+    elem_bytes = 9 * w.storage_bytes  # read x1, x2, v, k, gy; write gx1, gx2, gv, gk
+    set_bytes = w.elems * elem_bytes
+    rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
+    dev = torch.device("cuda:0")
+    base = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D, gy_host)]
+    sets = [base] + [[t.clone() for t in base] for _ in range(1, rot)]
+    outs = [[torch.empty_like(base[0]) for _ in range(4)] + [torch.empty_like(base[4])] for _ in range(rot)]
+    ws = torch.empty(H.backward_workspace_size(w.shape, w.pad_mode, w.dtype), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    calls = [H.PreparedBackward(*o, *st, w.pad_mode, ws, stream) for o, st in zip(outs, sets)]
+    for i in range(args.warmup):
+        calls[i % rot]()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        calls[i % rot]()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    avg_s = ev0.elapsed_time(ev1) * 1e-3 / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    flops = alg_flops_backward(w)
+    hbm_gbs = set_bytes / avg_s / 1e9
+    alu_tflops = flops / avg_s / 1e12
+    alu_bound = flops / (FP32_VALU_TFLOPS * 1e12) > set_bytes / (HBM_PEAK_GBS * 1e9)
+    if alu_bound:
+        roofline = {"bound": "alu", "achieved": round(alu_tflops, 3), "peak": FP32_VALU_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(alu_tflops / FP32_VALU_TFLOPS, 4)}
+    else:
+        roofline = {"bound": "hbm", "achieved": round(hbm_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(hbm_gbs / HBM_PEAK_GBS, 4)}
+    roofline.update({"traffic": None, "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
+                     "alu_frac": round(alu_tflops / FP32_VALU_TFLOPS, 4), "alg_bytes_per_call": set_bytes,
+                     "alg_flops_per_call": round(flops), "avg_call_us": round(avg_s * 1e6, 3)})
+    parity = None
+    cpu = None
+    if not args.no_parity or not args.no_cpu_baseline:
+        import oracle
+        f64 = [W.storage_to_f64(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D, gy_host)]
+        t0 = time.perf_counter()
+        ref = oracle.backward_fft(*f64[:5], f64[5], w.pad_mode)
+        dt = time.perf_counter() - t0
+        if not args.no_parity:
+            got = outs[(args.steps - 1) % rot]
+            errs = []
+            for g, r in zip(got, ref):
+                if g.dtype == torch.bfloat16:
+                    gh = W.bf16_bits_to_f64(g.view(torch.int16).cpu().numpy().view(np.uint16))
+                else:
+                    gh = g.cpu().numpy().astype(np.float64)
+                errs.append(float(np.linalg.norm(gh - r) / max(np.linalg.norm(r), 1e-300)))
+            parity = max(errs)
+        if not args.no_cpu_baseline:
+            cpu = {"value": round(w.elems / dt / 1e9, 6), "unit": "GElem/s", "cores": oracle.default_threads(),
+                   "kind": "oracle", "sample": f"one pass over all {w.B * w.C} (b,c) lines of {w.name} "
+                                               f"(fp64 FFT oracle backward, {dt:.2f} s wall)"}
+    out = {
+        "metric": "gated N-D FFT-conv backward GElem/s and % of roofline on 1 MI355X",
+        "value": round(w.elems / (ms_per_step * 1e-3) / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded, shapes and distributions of the paper's workloads; gy seeded normal)",
+        "config": {"workload": w.name, "pass": "backward", "B": w.B, "C": w.C, "grid": list(w.grid),
+                   "pad_mode": w.pad_mode, "storage": w.dtype, "rotated_input_sets": rot},
+        "roofline": roofline, "cpu_baseline": cpu, "parity_rel_l2_worst_tensor": parity,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out))
+
+
 def to_device(arr, dtype):
     import torch
     if dtype == "f32":
@@ -148,6 +259,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true", help="skip the sampled oracle check (profiling runs)")
     ap.add_argument("--no-stream-peak", action="store_true", help="skip the 1 GiB copy that measures the stream peak")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward (gradients for x1, x2, v, k, D) instead of the forward")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -161,6 +274,9 @@ def main():
 
     w = W.WORKLOADS[args.workload]
     inp = W.generate(w)
+    if args.backward:
+        bench_backward(args, w, inp)
+        return
     set_bytes = w.elems * alg_bytes_per_elem(w)
     rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
     dev = torch.device("cuda:0")

@@ -96,6 +96,39 @@ hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int 
 hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_mode, int dtype,
                                          char* buf, size_t n);
 
+/*
+ * hyenand_fftconv_backward -- gradients of a scalar loss through
+ * y = x2 * (k conv (x1*v) + D*(x1*v)), given gy = dLoss/dy.
+ *
+ * With u = x1*v, h = gy*x2 and z = k conv u + D*u (the pre-gate output):
+ *
+ *     gx2 = gy*z,    gu[j] = sum_n k[n-j] h[n] + D[c]*h[j]   (adjoint of the
+ *                    convolution: linear n_d >= j_d, circular (n-j) mod L),
+ *     gk[m] = sum_n h[n] u[n-m]  (linear n_d >= m_d, circular mod L),
+ *     gx1 = gu*v,    gv = gu*x1,    gD[c] = sum over b and n of h*u.
+ *
+ * These are the derivatives of the operator of Eq. (HyenaND), section 3.2,
+ * with the gates and shortcut of Def. A.2 / A.3 (the paper trains through
+ * it).  Same layouts, dtype, pad_mode and stream semantics as
+ * hyenand_fftconv; gy and the outputs gx1, gx2, gv, gk are [B, C, L...]
+ * (16-byte aligned), gD is [C].  No output may overlap an input or another
+ * output.  workspace: device scratch of at least
+ * hyenand_fftconv_backward_workspace_size() bytes (one float per (b, c)
+ * line; contents are overwritten).  gD is reduced over b in a fixed order, so
+ * results are deterministic.  Supported: 1D transforms up to 8192 points and
+ * 2D grids whose three half spectra fit on chip (linear up to 64x64,
+ * circular up to 64x128 / 128x64); other shapes return
+ * HYENAND_ERR_UNSUPPORTED.
+ */
+hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,
+                                        const void* D, const void* gy, void* gx1, void* gx2, void* gv,
+                                        void* gk, void* gD, int ndim, const int64_t* dims, int pad_mode,
+                                        int dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes hyenand_fftconv_backward needs for these arguments. */
+hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, int pad_mode,
+                                                       int dtype, size_t* bytes_out);
+
 /* Static text for a status code. */
 const char* hyenand_status_string(int status);
 

@@ -455,6 +455,25 @@ __device__ __forceinline__ void st2(uint16_t* p, float2 x) {
   *reinterpret_cast<uint32_t*>(p) = (uint32_t)f32_to_bf16_rne(x.x) | ((uint32_t)f32_to_bf16_rne(x.y) << 16);
 }
 
+// Raw pairs: the storage bits of two consecutive values, widened to fp32 only
+// where they are used, so that a load issued early is waited for late.
+template <typename TS>
+struct Raw2;
+template <>
+struct Raw2<float> {
+  using type = float2;
+};
+template <>
+struct Raw2<uint16_t> {
+  using type = uint32_t;
+};
+__device__ __forceinline__ float2 ld2_raw(const float* p) { return *reinterpret_cast<const float2*>(p); }
+__device__ __forceinline__ uint32_t ld2_raw(const uint16_t* p) { return *reinterpret_cast<const uint32_t*>(p); }
+__device__ __forceinline__ float2 widen2(float2 r) { return r; }
+__device__ __forceinline__ float2 widen2(uint32_t u) {
+  return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+}
+
 // Real-to-complex post-pass.  A real line x[0..P) is read as the complex
 // line z[m] = x[2m] + i x[2m+1] of length M = P/2 and transformed; with
 // A = Z[g], B = Z[(M-g) mod M] and w = exp(-2 pi i g / P) this returns

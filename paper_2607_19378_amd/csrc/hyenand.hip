@@ -219,6 +219,76 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
   return HYENAND_OK;
 }
 
+hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                                       size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  if (!backward_supported(a)) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  *bytes_out = ((size_t)a.lines * sizeof(float) + 15) / 16 * 16;
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,
+                                        const void* D, const void* gy, void* gx1, void* gx2, void* gv, void* gk,
+                                        void* gD, int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const void* ins[6] = {x1, x2, v, k, gy, D};
+  const char* in_names[6] = {"x1", "x2", "v", "k", "gy", "D"};
+  void* outs[5] = {gx1, gx2, gv, gk, gD};
+  const char* out_names[5] = {"gx1", "gx2", "gv", "gk", "gD"};
+  for (int i = 0; i < 6; ++i)
+    if (!ins[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", in_names[i]);
+  for (int i = 0; i < 5; ++i)
+    if (!outs[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", out_names[i]);
+  const size_t es = a.bf16 ? 2 : 4;
+  size_t n = (size_t)a.lines;
+  for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];
+  size_t in_bytes[6], out_bytes[5];
+  for (int i = 0; i < 6; ++i) in_bytes[i] = i == 5 ? (size_t)a.C * es : n * es;
+  for (int i = 0; i < 5; ++i) out_bytes[i] = i == 4 ? (size_t)a.C * es : n * es;
+  for (int i = 0; i < 6; ++i)
+    if ((uintptr_t)ins[i] % (i == 5 ? es : 16) != 0)
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not aligned", in_names[i]);
+  for (int i = 0; i < 5; ++i)
+    if ((uintptr_t)outs[i] % (i == 4 ? es : 16) != 0)
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not aligned", out_names[i]);
+  for (int i = 0; i < 5; ++i) {
+    for (int j = 0; j < 6; ++j)
+      if (overlaps(outs[i], out_bytes[i], ins[j], in_bytes[j]))
+        return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s overlaps %s", out_names[i], in_names[j]);
+    for (int j = 0; j < i; ++j)
+      if (overlaps(outs[i], out_bytes[i], outs[j], out_bytes[j]))
+        return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s overlaps %s", out_names[i], out_names[j]);
+  }
+  if (!backward_supported(a)) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  const size_t need = (size_t)a.lines * sizeof(float);
+  if (!workspace || workspace_bytes < need)
+    return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "backward needs at least %zu workspace bytes, got %zu", need,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16 != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace is not 16-byte aligned");
+  for (int j = 0; j < 6; ++j)
+    if (overlaps(workspace, workspace_bytes, ins[j], in_bytes[j]))
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", in_names[j]);
+  for (int j = 0; j < 5; ++j)
+    if (overlaps(workspace, workspace_bytes, outs[j], out_bytes[j]))
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", out_names[j]);
+  FftConvBwdArgs b;
+  b.f = a;
+  b.f.x1 = x1; b.f.x2 = x2; b.f.v = v; b.f.k = k; b.f.D = D;
+  b.gy = gy;
+  b.gx1 = gx1; b.gx2 = gx2; b.gv = gv; b.gk = gk; b.gD = gD;
+  b.partial = (float*)workspace;
+  const hipError_t err = launch_backward(b, (hipStream_t)stream);
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
+}
+
 const char* hyenand_status_string(int status) {
   switch (status) {
     case HYENAND_OK: return "ok";
@@ -232,6 +302,6 @@ const char* hyenand_status_string(int status) {
 
 const char* hyenand_last_error(void) { return g_last_error.c_str(); }
 
-int hyenand_version(void) { return 100; }
+int hyenand_version(void) { return 200; }
 
 }  // extern "C"

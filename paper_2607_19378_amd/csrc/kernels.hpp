@@ -35,6 +35,17 @@ bool multipass_supported(const FftConvArgs& a);
 size_t multipass_bytes_per_line(const FftConvArgs& a);
 hipError_t launch_multipass(const FftConvArgs& a, int64_t chunk_lines, hipStream_t s);
 
+// backward (single pass per line: 1D up to P = 8192, 2D where the half
+// spectra of u, k and h fit in LDS)
+struct FftConvBwdArgs {
+  FftConvArgs f;  // shapes and the forward inputs (f.y unused)
+  const void* gy;
+  void *gx1, *gx2, *gv, *gk, *gD;
+  float* partial;  // workspace: one float per line (sum of h u)
+};
+bool backward_supported(const FftConvArgs& a);
+hipError_t launch_backward(const FftConvBwdArgs& b, hipStream_t s);
+
 // multi-pass 1D (four-step split of the long line)
 bool fourstep_supported(const FftConvArgs& a);
 size_t fourstep_bytes_per_line(const FftConvArgs& a);

@@ -20,7 +20,8 @@ PAD_LINEAR, PAD_CIRCULAR = 0, 1
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
 EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min",
-            "hyenand_fftconv_plan_name", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
+            "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
+            "hyenand_status_string", "hyenand_last_error", "hyenand_version")
 
 _lock = threading.Lock()
 _lib = None
@@ -50,6 +51,12 @@ def lib() -> ctypes.CDLL:
                 f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                               ctypes.POINTER(ctypes.c_size_t)]
                 f.restype = ctypes.c_int
+            L.hyenand_fftconv_backward.argtypes = [vp] * 11 + [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int, vp,
+                                                           ctypes.c_size_t, vp]
+            L.hyenand_fftconv_backward.restype = ctypes.c_int
+            L.hyenand_fftconv_backward_workspace_size.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
+                                                                  ctypes.POINTER(ctypes.c_size_t)]
+            L.hyenand_fftconv_backward_workspace_size.restype = ctypes.c_int
             L.hyenand_fftconv_plan_name.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_char_p, ctypes.c_size_t]
             L.hyenand_fftconv_plan_name.restype = ctypes.c_int
@@ -175,3 +182,60 @@ def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=No
             workspace = torch.empty(nbytes, dtype=torch.uint8, device=x1.device)
     fftconv_into(y, x1, x2, v, k, D, pad_mode, workspace, stream)
     return y
+
+
+def backward_workspace_size(shape, pad_mode: str, dtype) -> int:
+    nd, dims = _dims(shape)
+    out = ctypes.c_size_t(0)
+    _check(lib().hyenand_fftconv_backward_workspace_size(nd, dims, _mode(pad_mode), _dtype_code(dtype),
+                                                         ctypes.byref(out)))
+    return int(out.value)
+
+
+class PreparedBackward:
+    """One hyenand_fftconv_backward call with its arguments checked and
+    marshalled once (see Prepared)."""
+
+    def __init__(self, gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None,
+                 stream=None):
+        import torch
+        shape = tuple(x1.shape)
+        for t in (x1, x2, v, k, gy, gx1, gx2, gv, gk):
+            if not t.is_cuda or tuple(t.shape) != shape or t.dtype != x1.dtype or not t.is_contiguous():
+                raise ValueError("x1, x2, v, k, gy and the four gradients must be contiguous GPU tensors "
+                                 "of one shape and dtype")
+        for t in (D, gD):
+            if not t.is_cuda or t.dtype != x1.dtype or tuple(t.shape) != (shape[1],) or not t.is_contiguous():
+                raise ValueError("D and gD must be contiguous [C] GPU tensors of the same dtype")
+        if workspace is None:
+            workspace = torch.empty(backward_workspace_size(shape, pad_mode, x1.dtype), dtype=torch.uint8,
+                                    device=x1.device)
+        nd, dims = _dims(shape)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        self._fn = lib().hyenand_fftconv_backward
+        self._args = (_ptr(x1), _ptr(x2), _ptr(v), _ptr(k), _ptr(D), _ptr(gy), _ptr(gx1), _ptr(gx2), _ptr(gv),
+                      _ptr(gk), _ptr(gD), nd, dims, _mode(pad_mode), _dtype_code(x1.dtype), _ptr(workspace),
+                      workspace.numel() * workspace.element_size(), ctypes.c_void_p(stream.cuda_stream))
+        self._keep = (gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, workspace, stream)
+
+    def __call__(self) -> None:
+        status = self._fn(*self._args)
+        if status != OK:
+            _check(status)
+
+
+def backward_into(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None,
+                  stream=None) -> None:
+    """Gradients of a loss through y for dLoss/dy = gy, written into gx1, gx2,
+    gv, gk ([B, C, L...]) and gD ([C]); all tensors already on the GPU."""
+    PreparedBackward(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode, workspace, stream)()
+
+
+def backward(x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None, stream=None):
+    """(gx1, gx2, gv, gk, gD) with torch-allocated outputs."""
+    import torch
+    gx1, gx2, gv, gk = (torch.empty_like(x1) for _ in range(4))
+    gD = torch.empty_like(D)
+    backward_into(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode, workspace, stream)
+    return gx1, gx2, gv, gk, gD

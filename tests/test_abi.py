@@ -94,3 +94,41 @@ def test_workspace_queries_are_host_only():
     with pytest.raises(H.HyenandError) as e:
         H.workspace_size((1, 1, 3), "linear", "f32")
     assert e.value.status == H.ERR_UNSUPPORTED
+
+
+def bcall(L, shape, mode=0, dtype=0, ptrs=None, ws=FAKE + (40 << 36), ws_bytes=1 << 20):
+    nd = len(shape) - 2
+    dims = (ctypes.c_int64 * len(shape))(*shape)
+    p = ptrs or [FAKE + i * (1 << 36) for i in range(11)]
+    return L.hyenand_fftconv_backward(*[ctypes.c_void_p(x) for x in p], nd, dims, mode, dtype,
+                                      ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+def test_backward_validation(L):
+    p = [FAKE + i * (1 << 36) for i in range(11)]
+    q = list(p)
+    q[6] = 0  # gx1
+    assert bcall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+    assert b"gx1 is NULL" in L.hyenand_last_error()
+    q = list(p)
+    q[7] = p[0] + 16  # gx2 inside x1
+    assert bcall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+    assert b"overlaps" in L.hyenand_last_error()
+    q = list(p)
+    q[8] = q[9]  # gv == gk
+    assert bcall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+    q = list(p)
+    q[6] = p[6] + 4  # misaligned output
+    assert bcall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+    assert bcall(L, (2, 3, 16), ws=None, ws_bytes=0) == H.ERR_WORKSPACE_TOO_SMALL
+    assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
+    assert bcall(L, (1, 2, 1 << 20)) == H.ERR_UNSUPPORTED      # beyond the single-pass 1D backward
+    assert bcall(L, (1, 2, 128, 128), mode=1) == H.ERR_UNSUPPORTED  # three 128x128 half spectra exceed LDS
+    assert bcall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED            # not a power of two
+
+
+def test_backward_workspace_size(L):
+    assert H.backward_workspace_size((8, 256, 64, 64), "linear", "f32") == 8 * 256 * 4
+    assert H.backward_workspace_size((3, 5, 16), "circular", "bf16") == 64  # 15 floats, rounded to 16 bytes
+    with pytest.raises(H.HyenandError):
+        H.backward_workspace_size((1, 1, 2048, 2048), "linear", "f32")
