@@ -134,29 +134,17 @@ __global__ void __launch_bounds__(512)
   // exp(-2 pi i g / P) for g = fa + N1 f2 is exp(-2 pi i fa / P) exp(-2 pi i f2 / (2 N2))
   const float2 om_a = twiddle_rt<false>((uint32_t)fa, log2M + 1);
   // slots: 0 = u row fa, 1 = u row fb, 2 = k row fa, 3 = k row fb (a single
-  // self-mirrored row uses slots 0 and 2 only)
-  batched_copy<4 * N2, NT, 8>(
-      tid,
-      [&](int i) {
-        const int sl = i / N2, f2 = i - sl * N2;
-        float2 z = czero();
-        if (!single || (sl & 1) == 0) z = A[((sl >> 1) ? M : 0) + (int64_t)((sl & 1) ? fb : fa) * N2 + f2];
-        return z;
-      },
-      [&](int i, float2 z) {
-        const int sl = i / N2, f2 = i - sl * N2;
-        *ScrPad16{R[sl]}(f2) = z;
-      });
-  __syncthreads();
-
-  // forward transforms over m2 (lanes run along each row)
+  // self-mirrored row uses slots 0 and 2 only).  Forward transforms over m2,
+  // lanes along each row; lane t holds f2 = t + T e straight from global
+  // memory (consecutive lanes, consecutive addresses).
   {
     const int sl = tid / T, t = tid % T;
     const bool act = sl < 4 && (!single || (sl & 1) == 0);
     const ScrPad16 sc{R[sl & 3]};
+    const float2* src = A + ((sl >> 1) ? M : 0) + (int64_t)((sl & 1) ? fb : fa) * N2 + t;
     float2 w[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) w[e] = act ? *sc(t + T * e) : czero();
+    for (int e = 0; e < E; ++e) w[e] = act ? src[T * e] : czero();
     BlockFFT<N2, E, false>::run(w, t, sc, act, twl);
     if (act) {
 #pragma unroll
