@@ -332,7 +332,6 @@ struct CoreCfg {
   static constexpr int T = P0 / E;
   static constexpr int TLP = TL + 1;
   static constexpr int L0 = CIRC ? P0 : P0 / 2;
-  static constexpr int KPT = (L0 * TL + NT - 1) / NT;  // prefetched K values per lane
 };
 
 template <int P0, bool CIRC>
@@ -340,7 +339,7 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
     mp_core(float2* __restrict__ ws, const void* __restrict__ Dp, int dbf16, int64_t line0, int C,
             int ncols, int HS, int H, int64_t half, int64_t per_line, float scale) {
   using Cf = CoreCfg<P0, CIRC>;
-  constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T, NT = Cf::NT, L0 = Cf::L0, KPT = Cf::KPT;
+  constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T, NT = Cf::NT, L0 = Cf::L0;
   __shared__ float2 tile[P0 * TLP];
   __shared__ float2 twl[imax(1, PassTw<P0, E>::kCount)];
   const int ntile = (ncols + TL - 1) / TL;
@@ -355,59 +354,41 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
   float2* U = ws + line * per_line;
   const float2* K = U + half;
 
-  // K's tile into registers, U's tile into LDS
-  static_assert(NT % TL == 0, "lanes keep their column");
-  float2 kreg[KPT];
-  {
-    const bool kv = col_valid(col0 + tid % TL, ncols, HS, H);
-    const float2* ks = K + col0 + tid % TL;
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-      const int p = tid / TL + (NT / TL) * j;
-      kreg[j] = (kv && p < L0) ? ks[(int64_t)p * ncols] : czero();
-    }
-  }
-  tile_load<L0, TL, TLP, NT>(tile, U, ncols, col0, ncols, HS, H, tid);
-  __syncthreads();
-
+  // Column points of U and K straight from global memory into registers
+  // (lane (cc, t) holds rows n = t + T e of column col0 + cc; consecutive
+  // lanes read consecutive columns).  K's loads are issued right after U's
+  // and arrive while U is transformed.  The LDS tile is only the exchange
+  // scratch; the result goes back to U's rows straight from registers.
   static_assert(NT / T >= TL, "one round of columns");
   const int cc = tid % TL, t = tid / TL;
   const bool act = t < T;
-  float2* col = tile + cc;
-  const ScrS<TLP> sc{col};
+  const bool cv = act && col_valid(col0 + cc, ncols, HS, H);
+  float2* const uc = U + col0 + cc;
+  const float2* const kc = K + col0 + cc;
+  const ScrS<TLP> sc{tile + cc};
   float2 wu[E], wk[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int n = t + T * e;
-    wu[e] = (act && (CIRC || n < L0)) ? col[n * TLP] : czero();
+    wu[e] = (cv && (CIRC || n < L0)) ? uc[(int64_t)n * ncols] : czero();
   }
-  BlockFFT<P0, E, false>::run(wu, t, sc, act, twl);
-  __syncthreads();  // every lane is done with U's tile
-#pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    const int p = tid / TL + (NT / TL) * j;
-    if (p < L0) tile[p * TLP + tid % TL] = kreg[j];
-  }
-  __syncthreads();
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int n = t + T * e;
-    wk[e] = (act && (CIRC || n < L0)) ? col[n * TLP] : czero();
+    wk[e] = (cv && (CIRC || n < L0)) ? kc[(int64_t)n * ncols] : czero();
   }
+  BlockFFT<P0, E, false>::run(wu, t, sc, act, twl);
   BlockFFT<P0, E, false>::run(wk, t, sc, act, twl);
 #pragma unroll
   for (int e = 0; e < E; ++e) wu[e] = c_scale(gated_product(wu[e], wk[e], twoD), scale);
-  if constexpr (T == 1) __syncthreads();
   BlockFFT<P0, E, true>::run(wu, t, sc, act, twl);
-  if (act) {
+  if (cv) {
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int n = t + T * e;
-      if (CIRC || n < L0) col[n * TLP] = wu[e];
+      if (CIRC || n < L0) uc[(int64_t)n * ncols] = wu[e];
     }
   }
-  __syncthreads();
-  tile_store<L0, TL, TLP, NT>(tile, U, ncols, col0, ncols, HS, H, tid);
 }
 
 // ---------------------------------------------------------------------------
