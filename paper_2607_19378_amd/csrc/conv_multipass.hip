@@ -289,33 +289,35 @@ __global__ void __launch_bounds__(kTileNT)
   const int tid = threadIdx.x;
   float2* base = ws + line * per_line + (int64_t)n0 * P1 * HS;
 
-  constexpr int NLOAD = INV ? P1 : L1;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) tile_load<NLOAD, TL, TLP, NT>(tile[s], base + s * half, HS, col0, H, HS, H, tid);
-  __syncthreads();
-
+  // Lines are (signal, column) pairs; lane (line, t) moves rows t + T e of
+  // its column straight between global memory and registers (consecutive
+  // lanes, consecutive columns), in place: the forward reads the L1 nonzero
+  // rows and writes all P1, the inverse reads P1 rows and keeps L1.  The LDS
+  // tile is only the exchange scratch.
   constexpr int NL = NS * TL;
+  constexpr int NLOAD = INV ? P1 : L1;
+  constexpr int NSTORE = INV ? L1 : P1;
   for (int l0 = 0; l0 < NL; l0 += NT / T) {
     const int l = l0 + tid % (NT / T), t = tid / (NT / T);
     const int s = l / TL, cc = l % TL;
-    const bool act = l < NL && col0 + cc < H;
-    float2* col = tile[act ? s : 0] + cc;
+    const bool act = l < NL;
+    const bool cv = act && col0 + cc < H;
+    float2* const g = base + (act ? s : 0) * half + col0 + cc;
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int n = t + T * e;
-      w[e] = (act && (INV || CIRC || n < L1)) ? col[n * TLP] : czero();
+      w[e] = (cv && n < NLOAD) ? g[(int64_t)n * HS] : czero();
     }
-    BlockFFT<P1, E, INV>::run(w, t, ScrS<TLP>{col}, act, twl);
-    if (act) {
+    BlockFFT<P1, E, INV>::run(w, t, ScrS<TLP>{tile[act ? s : 0] + cc}, act, twl);
+    if (cv) {
 #pragma unroll
-      for (int e = 0; e < E; ++e) col[(t + T * e) * TLP] = w[e];
+      for (int e = 0; e < E; ++e) {
+        const int n = t + T * e;
+        if (n < NSTORE) g[(int64_t)n * HS] = w[e];
+      }
     }
   }
-  __syncthreads();
-  constexpr int NSTORE = INV ? L1 : P1;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) tile_store<NSTORE, TL, TLP, NT>(tile[s], base + s * half, HS, col0, H, HS, H, tid);
 }
 
 // ---------------------------------------------------------------------------
