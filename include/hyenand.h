@@ -81,6 +81,19 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
                                int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
                                void* stream);
 
+/*
+ * hyenand_fftconv_shared_k -- as hyenand_fftconv, with one kernel per channel
+ * shared by every sample: the Hyena operator's global kernel K of one row per
+ * channel (Eq. (hyena), section "Background: Hyena and CKConv"), before
+ * HyenaND makes the kernel input-dependent.  k is [C, L1, ..., LN] and sample
+ * b, channel c uses k[c].  Everything else, including the workspace sizes
+ * below, is as for hyenand_fftconv.
+ */
+hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const void* v, const void* k,
+                                        const void* D, void* y, int ndim, const int64_t* dims,
+                                        int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                                        void* stream);
+
 /* Recommended workspace size (bytes) for a call with these arguments; 0 for
  * plans that keep everything on chip.  Pure host function. */
 hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, int pad_mode,

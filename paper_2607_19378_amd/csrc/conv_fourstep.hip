@@ -60,7 +60,7 @@ __device__ __forceinline__ void twiddle_run(float2 (&v)[E], float2 w, float2 s) 
 template <int N1, bool CIRC, typename TS>
 __global__ void __launch_bounds__(512)
     fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
-                float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line) {
+                float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int kC) {
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
@@ -76,6 +76,7 @@ __global__ void __launch_bounds__(512)
   const int64_t M = (int64_t)N1 * N2;
   const int64_t L = CIRC ? 2 * M : M;  // real samples per line
   const size_t gbase = (size_t)(line0 + line) * L;
+  const size_t kbase = (size_t)k_line(line0 + line, kC) * L;
   const int tid = threadIdx.x;
   // lanes with consecutive ids take consecutive columns of one row, so every
   // global access below is a contiguous run of TL values per row
@@ -95,7 +96,7 @@ __global__ void __launch_bounds__(512)
         const float2 a = ld2(x1 + n), b = ld2(v + n);
         w[e] = make_float2(a.x * b.x, a.y * b.y);
       } else {
-        w[e] = ld2(k + n);
+        w[e] = ld2(k + n - gbase + kbase);
       }
     }
   }
@@ -264,7 +265,7 @@ hipError_t cols_fwd(const FsLaunch& L) {
   constexpr int TL = ColCfg<N1>::TL;
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * 2));
   const FftConvArgs& a = *L.a;
-#define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per
+#define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC
   if (a.bf16) {
     if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
     else hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));

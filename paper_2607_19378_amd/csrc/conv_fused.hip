@@ -43,7 +43,7 @@ struct Fused1D {
 template <int P, bool CIRC, typename TS>
 __global__ void __launch_bounds__(fused1d_nt(P))
     conv1d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
-                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C) {
+                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
   using F = Fused1D<P, CIRC, TS>;
   constexpr int L = F::L, M = F::M, MNZ = F::MNZ, NT = F::NT;
   __shared__ float2 Ub[F::LDSN];
@@ -57,6 +57,7 @@ __global__ void __launch_bounds__(fused1d_nt(P))
   const int line = blockIdx.x;
   const int c = line % C;
   const size_t base = (size_t)line * L;
+  const size_t kbase = (size_t)k_line(line, kC) * L;
   const int tid = threadIdx.x;
   if constexpr (kTwl) {
     TwF::fill(twf, tid, NT);
@@ -68,7 +69,7 @@ __global__ void __launch_bounds__(fused1d_nt(P))
     batched_copy<MNZ, NT, 8>(
         tid,
         [&](int m) {
-          const float2 a = ld2(x1 + base + 2 * m), b = ld2(v + base + 2 * m), kk = ld2(k + base + 2 * m);
+          const float2 a = ld2(x1 + base + 2 * m), b = ld2(v + base + 2 * m), kk = ld2(k + kbase + 2 * m);
           return make_float4(a.x * b.x, a.y * b.y, kk.x, kk.y);
         },
         [&](int m, float4 z) {
@@ -77,7 +78,7 @@ __global__ void __launch_bounds__(fused1d_nt(P))
         });
   } else if (tid == 0) {  // a single sample
     Ub[0] = make_float2(ld1(x1 + base) * ld1(v + base), 0.f);
-    Kb[0] = make_float2(ld1(k + base), 0.f);
+    Kb[0] = make_float2(ld1(k + kbase), 0.f);
   }
   __syncthreads();
 
@@ -148,7 +149,7 @@ static hipError_t launch_1d_fused_t(const FftConvArgs& a, hipStream_t s) {
   using F = Fused1D<P, CIRC, TS>;
   hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
                      (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
-                     (const TS*)a.D, (TS*)a.y, (int)a.C);
+                     (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
   return hipGetLastError();
 }
 
@@ -219,7 +220,7 @@ struct Fused2D {
 template <int P0, int P1, bool CIRC, typename TS>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
-                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C) {
+                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
   using F = Fused2D<P0, P1, CIRC, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
   // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
@@ -230,6 +231,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   const int img = blockIdx.x;
   const int c = img % C;
   const size_t base = (size_t)img * L0 * L1;
+  const size_t kbase = (size_t)k_line(img, kC) * L0 * L1;
   const int tid = threadIdx.x;
 
   // The normalisation 1 / (4 P0 P1) of the two unnormalised inverses and of
@@ -242,7 +244,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   batched_copy<L0 * L1 / 2, NT, 8>(
       tid,
       [&](int i) {
-        const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i), kk = ld2(k + base + 2 * i);
+        const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i), kk = ld2(k + kbase + 2 * i);
         return make_float4(a.x * b.x, a.y * b.y, kk.x * scale, kk.y * scale);
       },
       [&](int i, float4 z) {
@@ -429,7 +431,7 @@ template <int P0, int P1, bool CIRC, typename TS>
 static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(512), 0, s,
                      (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
-                     (const TS*)a.D, (TS*)a.y, (int)a.C);
+                     (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
   return hipGetLastError();
 }
 

@@ -76,7 +76,7 @@ template <int PL, bool CIRC, typename TS>
 __global__ void __launch_bounds__(256)
     mp_rows_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int nlines, int rows, int L1, int P1, int HS,
-                int64_t half, int64_t per_line) {
+                int64_t half, int64_t per_line, int kC) {
   using Cf = RowsCfg<PL>;
   constexpr int ML = Cf::ML, HP = Cf::HP, E = Cf::E, T = Cf::T, NT = Cf::NT, RPW = Cf::RPW;
   constexpr int LL = CIRC ? PL : PL / 2;
@@ -95,6 +95,12 @@ __global__ void __launch_bounds__(256)
   // samples per global load, written to LDS as two 8-byte pairs
   {
     const size_t gbase = (size_t)(line0 * rows + row0) * LL;
+    // element e of the chunk's input reads k at kidx(e): the same element
+    // of line k_line(e / (rows LL)) (rows and LL are powers of two)
+    const size_t per = (size_t)rows * LL;
+    auto kidx = [&](size_t e) -> size_t {
+      return kC ? (size_t)k_line((int64_t)(e / per), kC) * per + (e & (per - 1)) : e;
+    };
     if constexpr (LL % 4 == 0) {
       struct In3 {
         float4 a, b, k;
@@ -107,7 +113,7 @@ __global__ void __launch_bounds__(256)
             if (i / LL < nrow) {
               z.a = ld4(x1 + gbase + i);
               z.b = ld4(v + gbase + i);
-              z.k = ld4(k + gbase + i);
+              z.k = ld4(k + kidx(gbase + i));
             }
             return z;
           },
@@ -130,7 +136,7 @@ __global__ void __launch_bounds__(256)
           tid,
           [&](int i) {
             float2 z = czero();
-            if (i / LL < nrow) z = make_float2(ld1(x1 + gbase + i) * ld1(v + gbase + i), ld1(k + gbase + i));
+            if (i / LL < nrow) z = make_float2(ld1(x1 + gbase + i) * ld1(v + gbase + i), ld1(k + kidx(gbase + i)));
             return z;
           },
           [&](int i, float2 z) {
@@ -527,7 +533,7 @@ hipError_t rows_fwd(const MpLaunch& L) {
   const dim3 grid((unsigned)((total + RowsCfg<PL>::RPW - 1) / RowsCfg<PL>::RPW));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, \
-                    L.g.HS, L.g.half, L.per
+                    L.g.HS, L.g.half, L.per, a.kC
   if (a.bf16) {
     if (a.circular) hipLaunchKernelGGL((mp_rows_fwd<PL, true, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
     else hipLaunchKernelGGL((mp_rows_fwd<PL, false, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));

@@ -455,6 +455,10 @@ __device__ __forceinline__ void st2(uint16_t* p, float2 x) {
   *reinterpret_cast<uint32_t*>(p) = (uint32_t)f32_to_bf16_rne(x.x) | ((uint32_t)f32_to_bf16_rne(x.y) << 16);
 }
 
+// Line of k that line `line` (= b C + c) uses: its own, or with one kernel
+// per channel (kC = C) the kernel of channel c.
+__device__ __forceinline__ int64_t k_line(int64_t line, int kC) { return kC ? line % kC : line; }
+
 // Raw pairs: the storage bits of two consecutive values, widened to fp32 only
 // where they are used, so that a load issued early is waited for late.
 template <typename TS>

@@ -159,13 +159,18 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_
   return HYENAND_OK;
 }
 
-hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k, const void* D,
-                               void* y, int ndim, const int64_t* dims, int pad_mode, int dtype,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+hyenand_status forward(const void* x1, const void* x2, const void* v, const void* k, const void* D, void* y,
+                       int ndim, const int64_t* dims, int pad_mode, int dtype, void* workspace,
+                       size_t workspace_bytes, void* stream, bool shared_k) {
   g_last_error.clear();
   FftConvArgs a;
   hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
   if (st != HYENAND_OK) return st;
+  a.kC = shared_k ? (int)a.C : 0;
   if (!x1 || !x2 || !v || !k || !D || !y)
     return fail(HYENAND_ERR_INVALID_ARGUMENT, "a tensor pointer is NULL");
   {
@@ -183,10 +188,12 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
   size_t n = (size_t)a.lines;
   for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];
   const size_t nb = n * es;
+  const size_t kb = shared_k ? nb / (size_t)(a.lines / a.C) : nb;  // [C, L...] or [B, C, L...]
   const void* ins[4] = {x1, x2, v, k};
+  const size_t in_bytes[4] = {nb, nb, nb, kb};
   const char* names[4] = {"x1", "x2", "v", "k"};
   for (int i = 0; i < 4; ++i)
-    if (overlaps(y, nb, ins[i], nb)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", names[i]);
+    if (overlaps(y, nb, ins[i], in_bytes[i])) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", names[i]);
   if (overlaps(y, nb, D, (size_t)a.C * es)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps D");
   const Plan p = choose_plan(a);
   if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
@@ -198,7 +205,7 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
                   plan_name(p, a.ndim), per, workspace ? workspace_bytes : (size_t)0);
     if (overlaps(workspace, workspace_bytes, y, nb)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps y");
     for (int i = 0; i < 4; ++i)
-      if (overlaps(workspace, workspace_bytes, ins[i], nb))
+      if (overlaps(workspace, workspace_bytes, ins[i], in_bytes[i]))
         return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", names[i]);
     chunk = (int64_t)(workspace_bytes / per);
     if (chunk > a.lines) chunk = a.lines;
@@ -217,6 +224,22 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
   }
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
   return HYENAND_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k, const void* D,
+                               void* y, int ndim, const int64_t* dims, int pad_mode, int dtype,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  return forward(x1, x2, v, k, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, false);
+}
+
+hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const void* v, const void* k,
+                                        const void* D, void* y, int ndim, const int64_t* dims, int pad_mode,
+                                        int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  return forward(x1, x2, v, k, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, true);
 }
 
 hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,

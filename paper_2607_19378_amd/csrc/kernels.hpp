@@ -20,6 +20,7 @@ struct FftConvArgs {
   int64_t P[3];   // transform extents: 2L (linear) or L (circular)
   bool circular;
   bool bf16;
+  int kC;         // 0: k is [B, C, L...]; C: one kernel per channel, k is [C, L...]
   void* ws;       // device workspace (multi-pass plans)
   size_t ws_bytes;
 };

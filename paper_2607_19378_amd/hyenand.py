@@ -19,7 +19,8 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = ra
 PAD_LINEAR, PAD_CIRCULAR = 0, 1
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
-EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min",
+EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_workspace_size",
+            "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_status_string", "hyenand_last_error", "hyenand_version")
 
@@ -46,6 +47,8 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
                                           ctypes.c_int, vp, ctypes.c_size_t, vp]
             L.hyenand_fftconv.restype = ctypes.c_int
+            L.hyenand_fftconv_shared_k.argtypes = L.hyenand_fftconv.argtypes
+            L.hyenand_fftconv_shared_k.restype = ctypes.c_int
             for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min"):
                 f = getattr(L, name)
                 f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
@@ -136,15 +139,17 @@ class Prepared:
     stream (for loops that repeat a call, where per-call Python work would
     otherwise delay the launches)."""
 
-    def __init__(self, y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None):
+    def __init__(self, y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None,
+                 shared_k: bool = False):
         import torch
-        ts = (x1, x2, v, k, y)
         shape = tuple(x1.shape)
-        for t in ts:
+        kshape = (shape[1],) + shape[2:] if shared_k else shape
+        for t, want in ((x1, shape), (x2, shape), (v, shape), (k, kshape), (y, shape)):
             if not t.is_cuda:
                 raise ValueError("all tensors must be on the GPU")
-            if tuple(t.shape) != shape or t.dtype != x1.dtype:
-                raise ValueError("x1, x2, v, k, y must share shape and dtype")
+            if tuple(t.shape) != want or t.dtype != x1.dtype:
+                raise ValueError("x1, x2, v, y must share shape and dtype; k is the same shape "
+                                 "(or [C, L...] with shared_k)")
             if not t.is_contiguous():
                 raise ValueError("tensors must be contiguous")
         if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():
@@ -155,7 +160,7 @@ class Prepared:
         ws_ptr, ws_bytes = None, 0
         if workspace is not None:
             ws_ptr, ws_bytes = _ptr(workspace), workspace.numel() * workspace.element_size()
-        self._fn = lib().hyenand_fftconv
+        self._fn = lib().hyenand_fftconv_shared_k if shared_k else lib().hyenand_fftconv
         self._args = (_ptr(x1), _ptr(x2), _ptr(v), _ptr(k), _ptr(D), _ptr(y), nd, dims, _mode(pad_mode),
                       _dtype_code(x1.dtype), ws_ptr, ws_bytes, ctypes.c_void_p(stream.cuda_stream))
         self._keep = (y, x1, x2, v, k, D, workspace, stream)  # the buffers outlive the object
@@ -167,12 +172,13 @@ class Prepared:
 
 
 def fftconv_into(y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None,
-                 stream=None) -> None:
-    """y <- x2 * (k conv (x1*v) + D*(x1*v)); all tensors already allocated on the GPU."""
-    Prepared(y, x1, x2, v, k, D, pad_mode, workspace, stream)()
+                 stream=None, shared_k: bool = False) -> None:
+    """y <- x2 * (k conv (x1*v) + D*(x1*v)); all tensors already allocated on
+    the GPU.  shared_k: k is [C, L...], one kernel per channel for every sample."""
+    Prepared(y, x1, x2, v, k, D, pad_mode, workspace, stream, shared_k)()
 
 
-def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None):
+def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None, shared_k: bool = False):
     """Allocate y (and, unless given, the workspace) with torch and run the op."""
     import torch
     y = torch.empty_like(x1)
@@ -180,7 +186,7 @@ def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=No
         nbytes = workspace_size(tuple(x1.shape), pad_mode, x1.dtype)
         if nbytes:
             workspace = torch.empty(nbytes, dtype=torch.uint8, device=x1.device)
-    fftconv_into(y, x1, x2, v, k, D, pad_mode, workspace, stream)
+    fftconv_into(y, x1, x2, v, k, D, pad_mode, workspace, stream, shared_k)
     return y
 
 

@@ -132,3 +132,17 @@ def test_backward_workspace_size(L):
     assert H.backward_workspace_size((3, 5, 16), "circular", "bf16") == 64  # 15 floats, rounded to 16 bytes
     with pytest.raises(H.HyenandError):
         H.backward_workspace_size((1, 1, 2048, 2048), "linear", "f32")
+
+
+def test_shared_kernel_validation(L):
+    """hyenand_fftconv_shared_k takes k as [C, L...]: y inside that smaller
+    region still overlaps k; null pointers are rejected."""
+    shape = (4, 3, 64)
+    dims = (ctypes.c_int64 * 3)(*shape)
+    p = [FAKE + i * (1 << 36) for i in range(6)]
+    p[5] = p[3] + 3 * 64 * 4 - 16  # y starts 16 bytes before the end of k[C, L]
+    args = [ctypes.c_void_p(x) for x in p]
+    assert L.hyenand_fftconv_shared_k(*args, 1, dims, 0, 0, None, 0, None) == H.ERR_INVALID_ARGUMENT
+    assert b"y overlaps k" in L.hyenand_last_error()
+    q = [ctypes.c_void_p(x) for x in p[:3]] + [None] + [ctypes.c_void_p(x) for x in p[4:]]
+    assert L.hyenand_fftconv_shared_k(*q, 1, dims, 0, 0, None, 0, None) == H.ERR_INVALID_ARGUMENT
