@@ -74,7 +74,16 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  * work has been enqueued on `stream` and the call returns without waiting;
  * every buffer must stay alive until the stream reaches that point.  Calls on
  * distinct streams from distinct host threads are safe; two in-flight calls
- * must not share a workspace.  Results are deterministic (no atomics).
+ * must not share a workspace.  Results are deterministic (no atomics) and do
+ * not depend on the workspace size.
+ *
+ * The multi-pass plans (the ones with a nonzero workspace) fork onto two or
+ * three side streams of the library (created once per device, default
+ * priority, kept until the process ends) that wait for `stream` and that
+ * `stream` waits for before anything enqueued after the call; a graph
+ * captured on `stream` therefore takes them in.  Calls from several host
+ * threads share those side streams: they stay correct but their multi-pass
+ * work runs one call after the other.
  */
 hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k,
                                const void* D, void* y, int ndim, const int64_t* dims,

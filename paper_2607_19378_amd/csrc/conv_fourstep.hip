@@ -330,33 +330,30 @@ size_t fourstep_bytes_per_line(const FftConvArgs& a) {
   return (size_t)(a.P[0] / 2) * 2 * sizeof(float2);  // A_u and A_k
 }
 
-hipError_t launch_fourstep(const FftConvArgs& a, int64_t chunk, hipStream_t s) {
-  if (!fourstep_supported(a) || chunk < 1) return hipErrorInvalidValue;
+hipError_t launch_fourstep(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s) {
+  if (!fourstep_supported(a) || nl < 1 || line0 < 0 || line0 + nl > a.lines) return hipErrorInvalidValue;
   FsLaunch L;
   L.a = &a;
-  L.ws = (float2*)a.ws;
+  L.ws = (float2*)ws;
   const int64_t M = a.P[0] / 2;
   L.N1 = (int)(M / kN2);
   L.log2M = ilog2_rt(M);
   L.per = 2 * M;
   L.scale = (float)(1.0 / (4.0 * (double)a.P[0]));
   L.s = s;
-  for (int64_t line0 = 0; line0 < a.lines; line0 += chunk) {
-    L.line0 = line0;
-    L.nl = (int)((a.lines - line0) < chunk ? (a.lines - line0) : chunk);
-    hipError_t e;
-    if ((e = d_cols_fwd(L)) != hipSuccess) return e;
-    const dim3 grid((unsigned)((int64_t)L.nl * (L.N1 / 2 + 1)));
-    if (a.circular)
-      hipLaunchKernelGGL((fs_core<true>), grid, dim3(512), 0, s, L.ws, a.D, (int)a.bf16, line0, (int)a.C, L.N1,
-                         L.log2M, L.per, L.scale);
-    else
-      hipLaunchKernelGGL((fs_core<false>), grid, dim3(512), 0, s, L.ws, a.D, (int)a.bf16, line0, (int)a.C, L.N1,
-                         L.log2M, L.per, L.scale);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = d_cols_inv(L)) != hipSuccess) return e;
-  }
-  return hipSuccess;
+  L.line0 = line0;
+  L.nl = (int)nl;
+  hipError_t e;
+  if ((e = d_cols_fwd(L)) != hipSuccess) return e;
+  const dim3 grid((unsigned)((int64_t)L.nl * (L.N1 / 2 + 1)));
+  if (a.circular)
+    hipLaunchKernelGGL((fs_core<true>), grid, dim3(512), 0, s, L.ws, a.D, (int)a.bf16, line0, (int)a.C, L.N1,
+                       L.log2M, L.per, L.scale);
+  else
+    hipLaunchKernelGGL((fs_core<false>), grid, dim3(512), 0, s, L.ws, a.D, (int)a.bf16, line0, (int)a.C, L.N1,
+                       L.log2M, L.per, L.scale);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return d_cols_inv(L);
 }
 
 }  // namespace hyenand

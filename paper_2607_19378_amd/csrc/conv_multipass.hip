@@ -633,27 +633,24 @@ size_t multipass_bytes_per_line(const FftConvArgs& a) {
   return (size_t)(2 * g.half) * sizeof(float2);
 }
 
-hipError_t launch_multipass(const FftConvArgs& a, int64_t chunk, hipStream_t s) {
-  if (!multipass_supported(a) || chunk < 1) return hipErrorInvalidValue;
+hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s) {
+  if (!multipass_supported(a) || nl < 1 || line0 < 0 || line0 + nl > a.lines) return hipErrorInvalidValue;
   MpLaunch L;
   L.a = &a;
   L.g = mp_geom(a);
-  L.ws = (float2*)a.ws;
+  L.ws = (float2*)ws;
   L.per = 2 * L.g.half;
   L.scale = (float)(1.0 / (4.0 * (double)L.g.P0 * (double)L.g.P1 * (double)L.g.PL));
   L.s = s;
+  L.line0 = line0;
+  L.nl = (int)nl;
   const bool three = a.ndim == 3;
-  for (int64_t line0 = 0; line0 < a.lines; line0 += chunk) {
-    L.line0 = line0;
-    L.nl = (int)((a.lines - line0) < chunk ? (a.lines - line0) : chunk);
-    hipError_t e;
-    if ((e = d_rows_fwd(L.g.PL, L)) != hipSuccess) return e;
-    if (three && (e = d_axis1_fwd(L.g.P1, L)) != hipSuccess) return e;
-    if ((e = d_core(L.g.P0, L)) != hipSuccess) return e;
-    if (three && (e = d_axis1_inv(L.g.P1, L)) != hipSuccess) return e;
-    if ((e = d_rows_inv(L.g.PL, L)) != hipSuccess) return e;
-  }
-  return hipSuccess;
+  hipError_t e;
+  if ((e = d_rows_fwd(L.g.PL, L)) != hipSuccess) return e;
+  if (three && (e = d_axis1_fwd(L.g.P1, L)) != hipSuccess) return e;
+  if ((e = d_core(L.g.P0, L)) != hipSuccess) return e;
+  if (three && (e = d_axis1_inv(L.g.P1, L)) != hipSuccess) return e;
+  return d_rows_inv(L.g.PL, L);
 }
 
 }  // namespace hyenand

@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/hyenand.h"
@@ -97,21 +98,150 @@ size_t bytes_per_line(const FftConvArgs& a, Plan p) {
   return 0;
 }
 
-// Recommended workspace: enough lines per chunk to keep the grid busy while
-// the chunk's spectra stay within a cache-sized budget (default 192 MiB,
-// below the 256 MiB Infinity Cache; HYENAND_WS_TARGET_MB overrides).
-size_t recommended_ws(const FftConvArgs& a, Plan p) {
-  const size_t per = bytes_per_line(a, p);
-  if (per == 0) return 0;
-  size_t target = (size_t)192 << 20;
+// Chunking of the multi-pass plans.  Their spectra go through the caller's
+// workspace a chunk of lines at a time.  Consecutive chunks rotate over S
+// side streams, each with its own part of the workspace, so that the passes
+// of one chunk run in the launch tails of the others'; a chunk's spectra are
+// kept near 1/S of a 160 MiB budget so that the next pass over them still
+// finds most of them in the 256 MiB Infinity Cache.  S is 2, or 3 where a
+// chunk is a single line (measured best on the MI355X for 512^2, 2^20 and
+// 128^3 lines).  The recommended workspace is S such chunks;
+// HYENAND_WS_TARGET_MB sets the budget and HYENAND_CHUNK_STREAMS fixes S.
+size_t ws_target_bytes() {
+  size_t target = (size_t)160 << 20;
   if (const char* e = getenv("HYENAND_WS_TARGET_MB")) {
     long mb = strtol(e, nullptr, 10);
     if (mb > 0) target = (size_t)mb << 20;
   }
-  int64_t chunk = (int64_t)(target / per);
-  if (chunk < 1) chunk = 1;
-  if (chunk > a.lines) chunk = a.lines;
-  return (size_t)chunk * per;
+  return target;
+}
+
+// side streams for lines of `per` workspace bytes: 1 (the caller's stream
+// only) up to kMaxSide
+constexpr int kMaxSide = 4;
+int chunk_streams(size_t per) {
+  if (const char* e = getenv("HYENAND_CHUNK_STREAMS")) {
+    const long n = strtol(e, nullptr, 10);
+    if (n >= 1 && n <= kMaxSide) return (int)n;
+  }
+  return ws_target_bytes() / 2 / per < 2 ? 3 : 2;
+}
+
+struct ChunkPlan {
+  int64_t chunk;    // lines per chunk (the last one may hold fewer)
+  int64_t nchunks;
+  int streams;      // 1: everything on the caller's stream
+};
+
+ChunkPlan plan_chunks(int64_t lines, size_t per, size_t ws_bytes) {
+  ChunkPlan c;
+  const int64_t fit = (int64_t)(ws_bytes / per);  // >= 1, checked by the caller
+  const int want = chunk_streams(per);
+  c.streams = want;
+  if (c.streams > fit) c.streams = (int)fit;
+  if (c.streams > lines) c.streams = (int)lines;
+  int64_t target = (int64_t)(ws_target_bytes() / (size_t)want / per);
+  if (target < 1) target = 1;
+  int64_t chunk = fit / c.streams;
+  if (chunk > target) chunk = target;
+  if (chunk > lines) chunk = lines;
+  c.nchunks = (lines + chunk - 1) / chunk;
+  c.chunk = (lines + c.nchunks - 1) / c.nchunks;  // balanced
+  if (c.nchunks < c.streams) c.streams = (int)c.nchunks;
+  return c;
+}
+
+size_t recommended_ws(const FftConvArgs& a, Plan p) {
+  const size_t per = bytes_per_line(a, p);
+  if (per == 0) return 0;
+  const int ns = chunk_streams(per);
+  int64_t n = (int64_t)(ws_target_bytes() / (size_t)ns / per);
+  if (n < 1) n = 1;
+  n *= ns;
+  if (n > a.lines) n = a.lines;
+  return (size_t)n * per;
+}
+
+// Non-blocking side streams per device, created on first use and kept for
+// the life of the process (default priority).
+constexpr int kMaxDevices = 64;
+struct SideStreams {
+  std::once_flag once;
+  hipError_t err = hipSuccess;
+  hipStream_t s[kMaxSide] = {};
+};
+SideStreams g_side[kMaxDevices];
+
+hipError_t side_streams(hipStream_t caller, hipStream_t** out) {
+  int dev = 0;
+  hipError_t e = caller ? hipStreamGetDevice(caller, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  SideStreams& sd = g_side[dev];
+  std::call_once(sd.once, [&sd, dev] {
+    int prev = 0;
+    sd.err = hipGetDevice(&prev);
+    if (sd.err == hipSuccess && prev != dev) sd.err = hipSetDevice(dev);
+    for (int i = 0; i < kMaxSide && sd.err == hipSuccess; ++i)
+      sd.err = hipStreamCreateWithFlags(&sd.s[i], hipStreamNonBlocking);
+    if (prev != dev) {
+      const hipError_t r = hipSetDevice(prev);
+      if (sd.err == hipSuccess) sd.err = r;
+    }
+  });
+  if (sd.err != hipSuccess) return sd.err;
+  *out = sd.s;
+  return hipSuccess;
+}
+
+// Run a multi-pass plan chunk by chunk.  With side streams: they wait for
+// the caller's stream, chunk j runs on side stream j % S with workspace part
+// j % S, and the caller's stream waits for all S before any later work.
+template <class Launch>
+hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Launch launch) {
+  const ChunkPlan c = plan_chunks(a.lines, per, a.ws_bytes);
+  if (c.streams == 1) {
+    for (int64_t j = 0; j < c.nchunks; ++j) {
+      const int64_t line0 = j * c.chunk;
+      const int64_t nl = a.lines - line0 < c.chunk ? a.lines - line0 : c.chunk;
+      if (nl <= 0) break;
+      const hipError_t e = launch(line0, nl, a.ws, caller);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  const int S = c.streams;
+  hipStream_t* side = nullptr;
+  hipError_t e = side_streams(caller, &side);
+  if (e != hipSuccess) return e;
+  hipEvent_t ev[1 + kMaxSide] = {};
+  for (int i = 0; i <= S && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventRecord(ev[0], caller);
+  for (int i = 0; i < S && e == hipSuccess; ++i) e = hipStreamWaitEvent(side[i], ev[0], 0);
+  if (e == hipSuccess) {
+    for (int64_t j = 0; j < c.nchunks; ++j) {
+      const int64_t line0 = j * c.chunk;
+      const int64_t nl = a.lines - line0 < c.chunk ? a.lines - line0 : c.chunk;
+      if (nl <= 0) break;
+      const int q = (int)(j % S);
+      void* ws = (char*)a.ws + (size_t)q * (size_t)c.chunk * per;
+      e = launch(line0, nl, ws, side[q]);
+      if (e != hipSuccess) break;
+    }
+    // join even after a failed launch, so that no work is left unordered
+    // with the caller's stream
+    for (int i = 0; i < S; ++i) {
+      hipError_t r = hipEventRecord(ev[1 + i], side[i]);
+      if (r == hipSuccess) r = hipStreamWaitEvent(caller, ev[1 + i], 0);
+      if (e == hipSuccess) e = r;
+    }
+  }
+  for (int i = 0; i <= S; ++i)
+    if (ev[i]) {
+      const hipError_t r = hipEventDestroy(ev[i]);
+      if (e == hipSuccess) e = r;
+    }
+  return e;
 }
 
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -198,7 +328,6 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   const Plan p = choose_plan(a);
   if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
   const size_t per = bytes_per_line(a, p);
-  int64_t chunk = 0;
   if (per > 0) {
     if (!workspace || workspace_bytes < per)
       return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "plan %s needs at least %zu workspace bytes, got %zu",
@@ -207,8 +336,6 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
     for (int i = 0; i < 4; ++i)
       if (overlaps(workspace, workspace_bytes, ins[i], in_bytes[i]))
         return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", names[i]);
-    chunk = (int64_t)(workspace_bytes / per);
-    if (chunk > a.lines) chunk = a.lines;
   }
   a.x1 = x1; a.x2 = x2; a.v = v; a.k = k; a.D = D; a.y = y;
   a.ws = workspace;
@@ -218,8 +345,16 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   switch (p) {
     case PLAN_FUSED1D: err = launch_fused1d(a, s); break;
     case PLAN_FUSED2D: err = launch_fused2d(a, s); break;
-    case PLAN_MULTIPASS: err = launch_multipass(a, chunk, s); break;
-    case PLAN_FOURSTEP: err = launch_fourstep(a, chunk, s); break;
+    case PLAN_MULTIPASS:
+      err = run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
+        return launch_multipass(a, l0, nl, ws, st);
+      });
+      break;
+    case PLAN_FOURSTEP:
+      err = run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
+        return launch_fourstep(a, l0, nl, ws, st);
+      });
+      break;
     default: return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
   }
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));

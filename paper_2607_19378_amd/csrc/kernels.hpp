@@ -31,10 +31,12 @@ hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s);
 bool fused2d_supported(int64_t P0, int64_t P1);
 hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s);
 
-// multi-pass 2D/3D (lines along each axis; spectra staged in the workspace)
+// multi-pass 2D/3D (lines along each axis; spectra staged in the workspace).
+// One call runs every pass over lines [line0, line0 + nl) with their spectra
+// in ws (nl times the bytes per line), all on stream s.
 bool multipass_supported(const FftConvArgs& a);
 size_t multipass_bytes_per_line(const FftConvArgs& a);
-hipError_t launch_multipass(const FftConvArgs& a, int64_t chunk_lines, hipStream_t s);
+hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s);
 
 // backward (single pass per line: 1D up to P = 8192, 2D where the half
 // spectra of u, k and h fit in LDS)
@@ -47,9 +49,10 @@ struct FftConvBwdArgs {
 bool backward_supported(const FftConvArgs& a);
 hipError_t launch_backward(const FftConvBwdArgs& b, hipStream_t s);
 
-// multi-pass 1D (four-step split of the long line)
+// multi-pass 1D (four-step split of the long line); one call per chunk of
+// lines, as for launch_multipass
 bool fourstep_supported(const FftConvArgs& a);
 size_t fourstep_bytes_per_line(const FftConvArgs& a);
-hipError_t launch_fourstep(const FftConvArgs& a, int64_t chunk_lines, hipStream_t s);
+hipError_t launch_fourstep(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s);
 
 }  // namespace hyenand

@@ -97,6 +97,69 @@ def test_chunked_workspace_matches_full():
         assert rel_l2(y3, oracle_ref(inp)) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("grid,mode,dtype", [((64, 32), "circular", "f32"), ((8, 8, 16), "linear", "bf16"),
+                                             ((16384,), "linear", "f32")])
+def test_side_streams_match_caller_stream(monkeypatch, grid, mode, dtype):
+    """Chunks rotating over two or three side streams (7 lines, 3 lines of
+    workspace: chunks of one line each) give bitwise the result of every
+    chunk on the caller's stream.  The caller's stream is a non-default one
+    whose next kernel reads y at once, so a missing join would show."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    from gpu_util import to_device
+    inp = W.random_case(1, 7, grid, mode, dtype, seed=33)
+    w = inp.workload
+    wmin = H.workspace_min(w.shape, w.pad_mode, w.dtype)
+    dev = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+    ws = torch.empty(3 * wmin, dtype=torch.uint8, device="cuda")
+    outs = []
+    for streams in ("1", "2", "3"):
+        monkeypatch.setenv("HYENAND_CHUNK_STREAMS", streams)
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            y = torch.full_like(dev[0], float("nan"))
+            H.fftconv_into(y, *dev, pad_mode=w.pad_mode, workspace=ws, stream=s)
+            y2 = y.float() * 2.0  # consumer on the caller's stream
+        s.synchronize()
+        outs.append((y.float().cpu().numpy(), y2.cpu().numpy()))
+    log(f"[side streams] {grid} {mode} {dtype}")
+    a, a2 = outs[0]
+    for b, b2 in outs[1:]:
+        assert np.array_equal(a, b) and np.array_equal(a2, b2) and np.array_equal(b2, 2.0 * b)
+    assert rel_l2(a, oracle_ref(inp)) <= TOL[dtype]
+
+
+def test_graph_capture_with_side_streams():
+    """A multi-pass call captured into a graph (chunks on two side streams)
+    replays to the eager result, three times, with eager calls in between."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    from gpu_util import to_device
+    inp = W.random_case(1, 5, (64, 32), "circular", "f32", seed=44)
+    w = inp.workload
+    wmin = H.workspace_min(w.shape, w.pad_mode, w.dtype)
+    dev = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+    ws = torch.empty(2 * wmin, dtype=torch.uint8, device="cuda")
+    y = torch.empty_like(dev[0])
+    H.fftconv_into(y, *dev, pad_mode=w.pad_mode, workspace=ws)
+    torch.cuda.synchronize()
+    ref = y.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        H.fftconv_into(y, *dev, pad_mode=w.pad_mode, workspace=ws)
+    other = torch.empty_like(y)
+    for i in range(3):
+        y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        log(f"[graph] replay {i}")
+        assert torch.equal(y, ref)
+        H.fftconv_into(other, *dev, pad_mode=w.pad_mode, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(other, ref)
+
+
 def test_workspace_too_small_rejected():
     import torch
     from paper_2607_19378_amd import hyenand as H
