@@ -135,21 +135,31 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_
  * hyenand_fftconv; gy and the outputs gx1, gx2, gv, gk are [B, C, L...]
  * (16-byte aligned), gD is [C].  No output may overlap an input or another
  * output.  workspace: device scratch of at least
- * hyenand_fftconv_backward_workspace_size() bytes (one float per (b, c)
- * line; contents are overwritten).  gD is reduced over b in a fixed order, so
- * results are deterministic.  Supported: 1D transforms up to 8192 points and
- * 2D grids whose three half spectra fit on chip (linear up to 64x64,
- * circular up to 64x128 / 128x64); other shapes return
- * HYENAND_ERR_UNSUPPORTED.
+ * hyenand_fftconv_backward_workspace_min() bytes, 16-byte aligned, contents
+ * overwritten: per-line sums of h*u for gD, then (for the multi-pass plans)
+ * the three half spectra of u, k and h of a chunk of lines, as in the
+ * forward; hyenand_fftconv_backward_workspace_size() is the recommended
+ * size.  gD is reduced in a fixed order, so results are deterministic and do
+ * not depend on the workspace size.  Supported: 1D transforms up to 8192
+ * points and 2^15..2^22 points, 2D/3D transforms up to 1024 per axis (the
+ * forward's shapes except 1D lines of 16384 points); other shapes return
+ * HYENAND_ERR_UNSUPPORTED.  The multi-pass plans use the library's side
+ * streams as hyenand_fftconv does.
  */
 hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,
                                         const void* D, const void* gy, void* gx1, void* gx2, void* gv,
                                         void* gk, void* gD, int ndim, const int64_t* dims, int pad_mode,
                                         int dtype, void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes hyenand_fftconv_backward needs for these arguments. */
+/* Recommended workspace bytes for hyenand_fftconv_backward with these
+ * arguments. */
 hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, int pad_mode,
                                                        int dtype, size_t* bytes_out);
+
+/* Smallest workspace (bytes) hyenand_fftconv_backward accepts for these
+ * arguments. */
+hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, int pad_mode,
+                                                      int dtype, size_t* bytes_out);
 
 /* Static text for a status code. */
 const char* hyenand_status_string(int status);

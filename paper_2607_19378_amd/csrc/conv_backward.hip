@@ -539,7 +539,7 @@ hipError_t launch_typed(const FftConvBwdArgs& b, hipStream_t s) {
 
 }  // namespace
 
-bool backward_supported(const FftConvArgs& a) {
+bool fused_backward_supported(const FftConvArgs& a) {
   if (a.ndim == 1) {
     if (a.L[0] == 1) return true;
 #define HY_CASE(p) \

@@ -244,6 +244,50 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
   return e;
 }
 
+// Backward plans: single pass per line where the three spectra fit in LDS,
+// else the multi-pass (2D/3D) or four-step (1D) structure of the forward
+// with three signals.  The workspace holds the gD sums (256-byte aligned
+// block) and then the spectra of a chunk of lines per side stream.
+enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP };
+
+BwdPlan choose_bwd_plan(const FftConvArgs& a) {
+  if (fused_backward_supported(a)) return BWD_FUSED;
+  if ((a.ndim == 2 || a.ndim == 3) && multipass_supported(a)) return BWD_MULTIPASS;
+  if (a.ndim == 1 && fourstep_supported(a)) return BWD_FOURSTEP;
+  return BWD_NONE;
+}
+
+int64_t bwd_partials_per_line(const FftConvArgs& a, BwdPlan p) {
+  switch (p) {
+    case BWD_FUSED: return 1;
+    case BWD_MULTIPASS: return backward_mp_partials_per_line(a);
+    case BWD_FOURSTEP: return backward_fs_partials_per_line(a);
+    default: return 0;
+  }
+}
+
+size_t bwd_partial_bytes(const FftConvArgs& a, BwdPlan p) {
+  const size_t n = (size_t)a.lines * (size_t)bwd_partials_per_line(a, p) * sizeof(float);
+  return (n + 255) / 256 * 256;
+}
+
+size_t bwd_bytes_per_line(const FftConvArgs& a, BwdPlan p) {
+  if (p == BWD_MULTIPASS) return backward_mp_bytes_per_line(a);
+  if (p == BWD_FOURSTEP) return backward_fs_bytes_per_line(a);
+  return 0;
+}
+
+size_t bwd_recommended_spectra(const FftConvArgs& a, BwdPlan p) {
+  const size_t per = bwd_bytes_per_line(a, p);
+  if (per == 0) return 0;
+  const int ns = chunk_streams(per);
+  int64_t n = (int64_t)(ws_target_bytes() / (size_t)ns / per);
+  if (n < 1) n = 1;
+  n *= ns;
+  if (n > a.lines) n = a.lines;
+  return (size_t)n * per;
+}
+
 bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
   return a0 < b0 + nb && b0 < a0 + na;
@@ -383,8 +427,21 @@ hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* 
   FftConvArgs a;
   hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
   if (st != HYENAND_OK) return st;
-  if (!backward_supported(a)) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
-  *bytes_out = ((size_t)a.lines * sizeof(float) + 15) / 16 * 16;
+  const BwdPlan p = choose_bwd_plan(a);
+  if (p == BWD_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  *bytes_out = bwd_partial_bytes(a, p) + bwd_recommended_spectra(a, p);
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                                      size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const BwdPlan p = choose_bwd_plan(a);
+  if (p == BWD_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  *bytes_out = bwd_partial_bytes(a, p) + bwd_bytes_per_line(a, p);
   return HYENAND_OK;
 }
 
@@ -424,8 +481,10 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
       if (overlaps(outs[i], out_bytes[i], outs[j], out_bytes[j]))
         return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s overlaps %s", out_names[i], out_names[j]);
   }
-  if (!backward_supported(a)) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
-  const size_t need = (size_t)a.lines * sizeof(float);
+  const BwdPlan p = choose_bwd_plan(a);
+  if (p == BWD_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  const size_t pbytes = bwd_partial_bytes(a, p);
+  const size_t need = pbytes + bwd_bytes_per_line(a, p);
   if (!workspace || workspace_bytes < need)
     return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "backward needs at least %zu workspace bytes, got %zu", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -442,7 +501,26 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
   b.gy = gy;
   b.gx1 = gx1; b.gx2 = gx2; b.gv = gv; b.gk = gk; b.gD = gD;
   b.partial = (float*)workspace;
-  const hipError_t err = launch_backward(b, (hipStream_t)stream);
+  const hipStream_t s = (hipStream_t)stream;
+  hipError_t err = hipSuccess;
+  if (p == BWD_FUSED) {
+    err = launch_backward(b, s);
+  } else {
+    // the spectra of each chunk follow the gD sums in the workspace
+    FftConvArgs sa = b.f;
+    sa.ws = (char*)workspace + pbytes;
+    sa.ws_bytes = workspace_bytes - pbytes;
+    const size_t per = bwd_bytes_per_line(a, p);
+    if (p == BWD_MULTIPASS)
+      err = run_chunked(sa, per, s, [&b](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
+        return launch_backward_mp(b, l0, nl, ws, st);
+      });
+    else
+      err = run_chunked(sa, per, s, [&b](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
+        return launch_backward_fs(b, l0, nl, ws, st);
+      });
+    if (err == hipSuccess) err = launch_backward_reduce(b, bwd_partials_per_line(a, p), s);
+  }
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
   return HYENAND_OK;
 }

@@ -38,16 +38,27 @@ bool multipass_supported(const FftConvArgs& a);
 size_t multipass_bytes_per_line(const FftConvArgs& a);
 hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s);
 
-// backward (single pass per line: 1D up to P = 8192, 2D where the half
-// spectra of u, k and h fit in LDS)
+// backward
 struct FftConvBwdArgs {
   FftConvArgs f;  // shapes and the forward inputs (f.y unused)
   const void* gy;
   void *gx1, *gx2, *gv, *gk, *gD;
-  float* partial;  // workspace: one float per line (sum of h u)
+  float* partial;  // workspace: the sums of h u for gD
 };
-bool backward_supported(const FftConvArgs& a);
+// single pass per line (1D up to P = 8192, 2D where the half spectra of u, k
+// and h fit in LDS); one float of partial per line; launches the gD reduction
+bool fused_backward_supported(const FftConvArgs& a);
 hipError_t launch_backward(const FftConvBwdArgs& b, hipStream_t s);
+// multi-pass 2D/3D and four-step 1D: one call per chunk of lines [line0,
+// line0 + nl) with their three spectra in ws; partial holds the given number
+// of sums per line; launch_backward_reduce adds them into gD afterwards
+size_t backward_mp_bytes_per_line(const FftConvArgs& a);
+int64_t backward_mp_partials_per_line(const FftConvArgs& a);
+hipError_t launch_backward_mp(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s);
+size_t backward_fs_bytes_per_line(const FftConvArgs& a);
+int64_t backward_fs_partials_per_line(const FftConvArgs& a);
+hipError_t launch_backward_fs(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s);
+hipError_t launch_backward_reduce(const FftConvBwdArgs& b, int64_t partials_per_line, hipStream_t s);
 
 // multi-pass 1D (four-step split of the long line); one call per chunk of
 // lines, as for launch_multipass

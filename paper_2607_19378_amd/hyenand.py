@@ -22,7 +22,7 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_workspace_size",
             "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
-            "hyenand_status_string", "hyenand_last_error", "hyenand_version")
+            "hyenand_fftconv_backward_workspace_min", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
 
 _lock = threading.Lock()
 _lib = None
@@ -60,6 +60,9 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv_backward_workspace_size.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                                   ctypes.POINTER(ctypes.c_size_t)]
             L.hyenand_fftconv_backward_workspace_size.restype = ctypes.c_int
+            L.hyenand_fftconv_backward_workspace_min.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
+                                                                 ctypes.POINTER(ctypes.c_size_t)]
+            L.hyenand_fftconv_backward_workspace_min.restype = ctypes.c_int
             L.hyenand_fftconv_plan_name.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_char_p, ctypes.c_size_t]
             L.hyenand_fftconv_plan_name.restype = ctypes.c_int
@@ -195,6 +198,14 @@ def backward_workspace_size(shape, pad_mode: str, dtype) -> int:
     out = ctypes.c_size_t(0)
     _check(lib().hyenand_fftconv_backward_workspace_size(nd, dims, _mode(pad_mode), _dtype_code(dtype),
                                                          ctypes.byref(out)))
+    return int(out.value)
+
+
+def backward_workspace_min(shape, pad_mode: str, dtype) -> int:
+    nd, dims = _dims(shape)
+    out = ctypes.c_size_t(0)
+    _check(lib().hyenand_fftconv_backward_workspace_min(nd, dims, _mode(pad_mode), _dtype_code(dtype),
+                                                        ctypes.byref(out)))
     return int(out.value)
 
 

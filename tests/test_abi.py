@@ -122,14 +122,27 @@ def test_backward_validation(L):
     assert bcall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
     assert bcall(L, (2, 3, 16), ws=None, ws_bytes=0) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
-    assert bcall(L, (1, 2, 1 << 20)) == H.ERR_UNSUPPORTED      # beyond the single-pass 1D backward
-    assert bcall(L, (1, 2, 128, 128), mode=1) == H.ERR_UNSUPPORTED  # three 128x128 half spectra exceed LDS
+    assert bcall(L, (1, 2, 8192)) == H.ERR_UNSUPPORTED          # 16384-point lines: no backward plan
+    assert bcall(L, (1, 2, 2048, 4)) == H.ERR_UNSUPPORTED       # 4096 points on an axis of a 2D grid
     assert bcall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED            # not a power of two
+    # multi-pass plans: the gD sums plus one line of three spectra at least
+    assert bcall(L, (1, 2, 1 << 20)) == H.ERR_WORKSPACE_TOO_SMALL
+    assert bcall(L, (1, 2, 128, 128), mode=1, ws_bytes=4096) == H.ERR_WORKSPACE_TOO_SMALL
+    assert b"backward needs at least" in L.hyenand_last_error()
 
 
 def test_backward_workspace_size(L):
+    # single pass: one float per line, in a block rounded to 256 bytes
     assert H.backward_workspace_size((8, 256, 64, 64), "linear", "f32") == 8 * 256 * 4
-    assert H.backward_workspace_size((3, 5, 16), "circular", "bf16") == 64  # 15 floats, rounded to 16 bytes
+    assert H.backward_workspace_size((3, 5, 16), "circular", "bf16") == 256
+    assert H.backward_workspace_min((3, 5, 16), "circular", "bf16") == 256
+    # multi-pass 2D, 512^2 transform grid: 32 sums per line (8 rows per
+    # workgroup), then U, K, H of 256 rows x 272 (257 bins padded to 16)
+    per = 3 * 256 * 272 * 8
+    assert H.backward_workspace_min((1, 3, 256, 256), "linear", "f32") == 512 + per
+    assert H.backward_workspace_size((1, 3, 256, 256), "linear", "f32") == 512 + 3 * per
+    # four-step 1D, 2^21 points: 128 column tiles per line, three spectra of 2^20
+    assert H.backward_workspace_min((1, 2, 1 << 20), "linear", "f32") == 1024 + 3 * (1 << 20) * 8
     with pytest.raises(H.HyenandError):
         H.backward_workspace_size((1, 1, 2048, 2048), "linear", "f32")
 
