@@ -140,10 +140,9 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_
  * the three half spectra of u, k and h of a chunk of lines, as in the
  * forward; hyenand_fftconv_backward_workspace_size() is the recommended
  * size.  gD is reduced in a fixed order, so results are deterministic and do
- * not depend on the workspace size.  Supported: 1D transforms up to 8192
- * points and 2^15..2^22 points, 2D/3D transforms up to 1024 per axis (the
- * forward's shapes except 1D lines of 16384 points); other shapes return
- * HYENAND_ERR_UNSUPPORTED.  The multi-pass plans use the library's side
+ * not depend on the workspace size.  Supported: every shape the forward
+ * supports (1D transforms up to 2^22 points, 2D/3D up to 1024 per axis);
+ * other shapes return HYENAND_ERR_UNSUPPORTED.  The multi-pass plans use the library's side
  * streams as hyenand_fftconv does.
  */
 hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,

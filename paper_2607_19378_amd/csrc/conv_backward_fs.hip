@@ -1,6 +1,7 @@
 // Backward of the gated long convolution for 1D lines beyond the single-pass
-// limit: the four-step structure of the forward plan (M = P/2 = N1 x N2,
-// m = m1 N2 + m2, f = f1 + N1 f2) carried over to three signals.
+// limit (2^14 to 2^22 transform points): the four-step structure of the
+// forward plan (M = P/2 = N1 x N2, m = m1 N2 + m2, f = f1 + N1 f2) carried
+// over to three signals.
 //
 // With u = x1 v and h = gy x2 the gradients come from the spectral products
 // Z = U (K + D), GU = conj(K + D) H and GK = conj(U) H (gx2 = gy z,
@@ -299,6 +300,7 @@ hipError_t b_cols_inv(const FsbLaunch& L) {
 
 #define HY_BN1_SWITCH(N, FN, ARG)          \
   switch (N) {                             \
+    case 4: return FN<4>(ARG);             \
     case 8: return FN<8>(ARG);             \
     case 16: return FN<16>(ARG);           \
     case 32: return FN<32>(ARG);           \
@@ -317,13 +319,24 @@ int cols_tile(int N1) {
   switch (N1) {
 #define HY_CASE(n) \
   case n: return ColCfg<n>::TL;
-    HY_CASE(8) HY_CASE(16) HY_CASE(32) HY_CASE(64) HY_CASE(128) HY_CASE(256) HY_CASE(512) HY_CASE(1024)
+    HY_CASE(4) HY_CASE(8) HY_CASE(16) HY_CASE(32) HY_CASE(64) HY_CASE(128) HY_CASE(256) HY_CASE(512)
+    HY_CASE(1024)
 #undef HY_CASE
     default: return 1;
   }
 }
 
 }  // namespace
+
+// the forward's four-step shapes and one more: N1 = 4 (16384-point lines,
+// which the forward runs in a single pass)
+bool backward_fs_supported(const FftConvArgs& a) {
+  if (a.ndim != 1) return false;
+  const int64_t M = a.P[0] / 2;
+  if (M % kN2 != 0) return false;
+  const int64_t N1 = M / kN2;
+  return N1 >= 4 && N1 <= kMaxN1;
+}
 
 size_t backward_fs_bytes_per_line(const FftConvArgs& a) {
   return (size_t)(a.P[0] / 2) * 3 * sizeof(float2);  // A_u, A_k, A_h
@@ -336,7 +349,7 @@ int64_t backward_fs_partials_per_line(const FftConvArgs& a) {
 
 hipError_t launch_backward_fs(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s) {
   const FftConvArgs& a = b.f;
-  if (!fourstep_supported(a) || nl < 1 || line0 < 0 || line0 + nl > a.lines) return hipErrorInvalidValue;
+  if (!backward_fs_supported(a) || nl < 1 || line0 < 0 || line0 + nl > a.lines) return hipErrorInvalidValue;
   FsbLaunch L;
   L.b = &b;
   L.ws = (float2*)ws;

@@ -253,7 +253,7 @@ enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP };
 BwdPlan choose_bwd_plan(const FftConvArgs& a) {
   if (fused_backward_supported(a)) return BWD_FUSED;
   if ((a.ndim == 2 || a.ndim == 3) && multipass_supported(a)) return BWD_MULTIPASS;
-  if (a.ndim == 1 && fourstep_supported(a)) return BWD_FOURSTEP;
+  if (a.ndim == 1 && backward_fs_supported(a)) return BWD_FOURSTEP;
   return BWD_NONE;
 }
 

@@ -55,6 +55,7 @@ hipError_t launch_backward(const FftConvBwdArgs& b, hipStream_t s);
 size_t backward_mp_bytes_per_line(const FftConvArgs& a);
 int64_t backward_mp_partials_per_line(const FftConvArgs& a);
 hipError_t launch_backward_mp(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s);
+bool backward_fs_supported(const FftConvArgs& a);
 size_t backward_fs_bytes_per_line(const FftConvArgs& a);
 int64_t backward_fs_partials_per_line(const FftConvArgs& a);
 hipError_t launch_backward_fs(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s);

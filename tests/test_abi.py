@@ -122,7 +122,7 @@ def test_backward_validation(L):
     assert bcall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
     assert bcall(L, (2, 3, 16), ws=None, ws_bytes=0) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
-    assert bcall(L, (1, 2, 8192)) == H.ERR_UNSUPPORTED          # 16384-point lines: no backward plan
+    assert bcall(L, (1, 2, 1 << 22)) == H.ERR_UNSUPPORTED       # 2^23 transform points
     assert bcall(L, (1, 2, 2048, 4)) == H.ERR_UNSUPPORTED       # 4096 points on an axis of a 2D grid
     assert bcall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED            # not a power of two
     # multi-pass plans: the gD sums plus one line of three spectra at least

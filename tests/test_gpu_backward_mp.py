@@ -53,6 +53,7 @@ CASES = [
     ((1, 2, 512, 512), "circular", "f32"), ((3, 2, 8, 4), "linear", "f32"), ((1, 2, 1024, 8), "circular", "bf16"),
     ((2, 2, 8, 16, 32), "linear", "f32"), ((1, 2, 32, 32, 32), "circular", "bf16"), ((1, 2, 16, 8, 64), "linear", "bf16"),
     ((2, 3, 4, 2, 8), "circular", "f32"), ((1, 2, 64, 64, 64), "linear", "f32"),
+    ((1, 3, 8192), "linear", "f32"), ((2, 2, 16384), "circular", "bf16"),
     ((1, 3, 16384), "linear", "f32"), ((2, 2, 32768), "circular", "f32"), ((1, 2, 65536), "linear", "bf16"),
     ((1, 2, 1 << 20), "linear", "f32"),
 ]
