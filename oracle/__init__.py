@@ -19,7 +19,10 @@ The arithmetic lives in ``oracle.c`` (plain C, IEEE double):
 
 Inputs are float64 arrays of shape [B, C, L1, ..., LN] (x1, x2, v, k) and [C]
 (D).  ``pad_mode`` is "linear" (zero-padded, cropped to the first L_d outputs
-on every axis) or "circular".
+on every axis), "circular", or "centered" (forward only): the paper's kernel
+on the double grid, k of shape [B, C, 2 L1 - 1, ..., 2 LN - 1] with index
+L_d - 1 the zero displacement, input zero-padded and output cropped as in
+"linear".
 """
 from __future__ import annotations
 
@@ -82,14 +85,24 @@ def default_threads() -> int:
         return os.cpu_count() or 1
 
 
-def _prep(x1, x2, v, k, D):
+def kernel_shape(shape, pad_mode):
+    """Shape of k for a call on tensors of `shape` ([B, C, L1..LN])."""
+    shape = tuple(int(s) for s in shape)
+    if pad_mode == "centered":
+        return shape[:2] + tuple(2 * s - 1 for s in shape[2:])
+    return shape
+
+
+def _prep(x1, x2, v, k, D, pad_mode="linear"):
     arrs = [np.ascontiguousarray(a, dtype=np.float64) for a in (x1, x2, v, k, D)]
     shp = arrs[0].shape
     if len(shp) < 3 or len(shp) > 5:
         raise ValueError("tensors must be [B, C, L1..LN] with N in 1..3")
-    for a in arrs[1:4]:
+    for a in arrs[1:3]:
         if a.shape != shp:
-            raise ValueError("x1, x2, v, k must share one shape")
+            raise ValueError("x1, x2, v must share one shape")
+    if arrs[3].shape != kernel_shape(shp, pad_mode):
+        raise ValueError(f"k must have shape {kernel_shape(shp, pad_mode)} for pad_mode {pad_mode!r}")
     if arrs[4].shape != (shp[1],):
         raise ValueError("D must have shape [C]")
     dims = np.asarray(shp, dtype=np.int64)
@@ -100,10 +113,13 @@ def _ptr(a):
     return a.ctypes.data_as(_f64p)
 
 
+_MODES = {"linear": 0, "circular": 1, "centered": 2}
+
+
 def _mode(pad_mode: str) -> int:
-    if pad_mode not in ("linear", "circular"):
-        raise ValueError(f"pad_mode must be 'linear' or 'circular', got {pad_mode!r}")
-    return 1 if pad_mode == "circular" else 0
+    if pad_mode not in _MODES:
+        raise ValueError(f"pad_mode must be 'linear', 'circular' or 'centered', got {pad_mode!r}")
+    return _MODES[pad_mode]
 
 
 def _lines_arg(lines):
@@ -114,7 +130,7 @@ def _lines_arg(lines):
 
 
 def _run_lines(fn, x1, x2, v, k, D, pad_mode, lines, nthreads):
-    arrs, dims, nd = _prep(x1, x2, v, k, D)
+    arrs, dims, nd = _prep(x1, x2, v, k, D, pad_mode)
     y = np.zeros(arrs[0].shape, dtype=np.float64)
     la, lp, nl = _lines_arg(lines)
     rc = fn(*[_ptr(a) for a in arrs], _ptr(y), nd, dims.ctypes.data_as(_i64p), _mode(pad_mode),
@@ -137,7 +153,7 @@ def conv_fft(x1, x2, v, k, D, pad_mode="linear", lines=None, nthreads=None):
 
 def conv_direct_points(x1, x2, v, k, D, flat_idx, pad_mode="linear", nthreads=None):
     """y at the given flat indices of the [B, C, L...] output, by the explicit sum."""
-    arrs, dims, nd = _prep(x1, x2, v, k, D)
+    arrs, dims, nd = _prep(x1, x2, v, k, D, pad_mode)
     idx = np.ascontiguousarray(flat_idx, dtype=np.int64)
     out = np.zeros(idx.size, dtype=np.float64)
     rc = lib().oracle_direct_points(*[_ptr(a) for a in arrs], nd, dims.ctypes.data_as(_i64p),
@@ -159,7 +175,9 @@ def fft1d(x, sign=-1):
 
 
 def _backward(fn, x1, x2, v, k, D, gy, pad_mode, nthreads):
-    arrs, dims, nd = _prep(x1, x2, v, k, D)
+    if pad_mode == "centered":
+        raise ValueError("the backward takes pad_mode 'linear' or 'circular'")
+    arrs, dims, nd = _prep(x1, x2, v, k, D, pad_mode)
     g = np.ascontiguousarray(gy, dtype=np.float64)
     if g.shape != arrs[0].shape:
         raise ValueError("gy must have the shape of y")

@@ -13,6 +13,7 @@
  *   u = x1 * v                                   (inner gate, elementwise)
  *   linear:   conv[n] = sum_{m : 0 <= m_d <= n_d}  k[m] u[n - m]
  *   circular: conv[n] = sum_{m in box}            k[m] u[(n - m) mod L]
+ *   centered: conv[n] = sum_{m in box}            kc[n - m + (L - 1)] u[m]
  *   y[n]     = x2[n] * (conv[n] + D[c] u[n])     (shortcut, then outer gate)
  *
  * for every sample b, channel c and output index n of the L1 x ... x LN grid,
@@ -20,7 +21,12 @@
  * preservation": one kernel per input).  "linear" is the non-circular
  * convolution of section 3.2.1 ("Support for circular and non-circular
  * convolutions"): zero-pad and crop, with index 0 of k the zero displacement;
- * "circular" treats the grid as a torus.
+ * "circular" treats the grid as a torus.  "centered" is the same section's
+ * kernel on the double grid: kc has 2 L_d - 1 points per axis, index L_d - 1
+ * is the zero displacement, so every displacement -(L_d - 1) .. L_d - 1
+ * between two points of the input grid has its own weight; the input is
+ * zero-padded to 2 L_d and the output cropped to the first L_d.  kc is
+ * [B, C, 2 L1 - 1, ..., 2 LN - 1].
  *
  * Two independent evaluations are provided:
  *   oracle_direct / oracle_direct_points : the sum above written out.
@@ -53,6 +59,9 @@
  *       with conj(K) (k real), so gu = crop(IFFT(conj(K) H)) + D h and
  *       gk = crop(IFFT(conj(U) H)); zero padding to 2 L_d makes the cyclic
  *       sums equal the linear ones on the cropped range.
+ *
+ * The mode argument: 0 linear, 1 circular, 2 centered (forward only; the
+ * backward takes 0 and 1).
  *
  * Return codes: 0 ok, 1 bad argument, 2 out of memory, 3 the inverse
  * transform left an imaginary residue above 1e-9 of the real part (a broken
@@ -94,13 +103,22 @@ static int make_geom(int ndim, const int64_t *dims, geom *g) {
     return 0;
 }
 
-/* Transform extents: 2 L_d on the real axes in linear mode, L_d in circular
- * mode; the virtual leading axes of a 1D/2D problem stay at extent 1. */
-static void transform_extents(const geom *g, int circular, int64_t P[3]) {
+enum { MODE_LINEAR = 0, MODE_CIRCULAR = 1, MODE_CENTERED = 2 };
+
+/* Transform extents: 2 L_d on the real axes in linear and centered mode, L_d
+ * in circular mode; the virtual leading axes of a 1D/2D problem stay at
+ * extent 1. */
+static void transform_extents(const geom *g, int mode, int64_t P[3]) {
     for (int d = 0; d < 3; ++d) {
         int real_axis = d >= 3 - g->ndim;
-        P[d] = (real_axis && !circular) ? 2 * g->L[d] : g->L[d];
+        P[d] = (real_axis && mode != MODE_CIRCULAR) ? 2 * g->L[d] : g->L[d];
     }
+}
+
+/* Points of the centered kernel per line: prod (2 L_d - 1) (1 on the virtual
+ * axes). */
+static int64_t centered_box(const geom *g) {
+    return (2 * g->L[0] - 1) * (2 * g->L[1] - 1) * (2 * g->L[2] - 1);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -110,13 +128,23 @@ static void transform_extents(const geom *g, int circular, int64_t P[3]) {
 /* One output element of line `line` (= b*C + c) at grid index (n0,n1,n2). */
 static double direct_one(const double *x1, const double *x2, const double *v,
                          const double *k, const double *D, const geom *g,
-                         int circular, int64_t line, int64_t n0, int64_t n1,
+                         int mode, int64_t line, int64_t n0, int64_t n1,
                          int64_t n2) {
     const int64_t L0 = g->L[0], L1 = g->L[1], L2 = g->L[2];
     const int64_t base = line * g->box;
     const double *X1 = x1 + base, *V = v + base, *K = k + base;
     double conv = 0.0;
-    if (!circular) {
+    if (mode == MODE_CENTERED) {
+        const int64_t K1 = 2 * L1 - 1, K2 = 2 * L2 - 1;
+        const double *KC = k + line * centered_box(g);
+        for (int64_t m0 = 0; m0 < L0; ++m0)
+            for (int64_t m1 = 0; m1 < L1; ++m1)
+                for (int64_t m2 = 0; m2 < L2; ++m2) {
+                    int64_t j0 = n0 - m0 + L0 - 1, j1 = n1 - m1 + L1 - 1, j2 = n2 - m2 + L2 - 1;
+                    int64_t un = (m0 * L1 + m1) * L2 + m2;
+                    conv += KC[(j0 * K1 + j1) * K2 + j2] * (X1[un] * V[un]);
+                }
+    } else if (mode == MODE_LINEAR) {
         for (int64_t m0 = 0; m0 <= n0; ++m0)
             for (int64_t m1 = 0; m1 <= n1; ++m1)
                 for (int64_t m2 = 0; m2 <= n2; ++m2) {
@@ -146,7 +174,7 @@ typedef struct {
     const double *x1, *x2, *v, *k, *D;
     double *y;
     const geom *g;
-    int circular;
+    int circular; /* the mode: MODE_LINEAR, MODE_CIRCULAR or MODE_CENTERED */
     /* work split */
     const int64_t *items; /* line ids (direct/fft) or flat output indices (points) */
     int64_t nitems;
@@ -225,8 +253,9 @@ int oracle_direct(const double *x1, const double *x2, const double *v, const dou
     if (!x1 || !x2 || !v || !k || !D || !y || make_geom(ndim, dims, &g)) return 1;
     job J;
     memset(&J, 0, sizeof J);
+    if (circular < 0 || circular > 2) return 1;
     J.x1 = x1; J.x2 = x2; J.v = v; J.k = k; J.D = D; J.y = y; J.g = &g;
-    J.circular = circular ? 1 : 0;
+    J.circular = circular;
     J.items = lines;
     J.nitems = lines ? nlines : g.B * g.C;
     return run_jobs(&J, nthreads, direct_lines_worker);
@@ -242,8 +271,9 @@ int oracle_direct_points(const double *x1, const double *x2, const double *v, co
         if (idx[i] < 0 || idx[i] >= g.B * g.C * g.box) return 1;
     job J;
     memset(&J, 0, sizeof J);
+    if (circular < 0 || circular > 2) return 1;
     J.x1 = x1; J.x2 = x2; J.v = v; J.k = k; J.D = D; J.y = out; J.g = &g;
-    J.circular = circular ? 1 : 0;
+    J.circular = circular;
     J.items = idx;
     J.nitems = npts;
     return run_jobs(&J, nthreads, direct_points_worker);
@@ -360,8 +390,22 @@ static void *fft_lines_worker(void *arg) {
                     int64_t src = base + (n0 * g->L[1] + n1) * g->L[2] + n2;
                     int64_t dst = (n0 * P[1] + n1) * P[2] + n2;
                     U[dst].re = J->x1[src] * J->v[src];
-                    K[dst].re = J->k[src];
+                    if (J->circular != MODE_CENTERED) K[dst].re = J->k[src];
                 }
+        if (J->circular == MODE_CENTERED) {
+            /* displacement j_d - (L_d - 1) of kc goes to grid index
+             * (j_d - (L_d - 1)) mod P_d */
+            const int64_t K0 = 2 * g->L[0] - 1, K1 = 2 * g->L[1] - 1, K2 = 2 * g->L[2] - 1;
+            const double *KC = J->k + line * centered_box(g);
+            for (int64_t j0 = 0; j0 < K0; ++j0)
+                for (int64_t j1 = 0; j1 < K1; ++j1)
+                    for (int64_t j2 = 0; j2 < K2; ++j2) {
+                        int64_t g0 = (j0 - (g->L[0] - 1) + P[0]) % P[0];
+                        int64_t g1 = (j1 - (g->L[1] - 1) + P[1]) % P[1];
+                        int64_t g2 = (j2 - (g->L[2] - 1) + P[2]) % P[2];
+                        K[(g0 * P[1] + g1) * P[2] + g2].re = KC[(j0 * K1 + j1) * K2 + j2];
+                    }
+        }
         /* 2. forward transforms along every axis */
         for (int ax = 0; ax < 3; ++ax) {
             fft_axis(U, P, ax, J->tw_fwd[ax], tmp);
@@ -402,6 +446,7 @@ int oracle_fft(const double *x1, const double *x2, const double *v, const double
                const int64_t *lines, int64_t nlines, int nthreads) {
     geom g;
     if (!x1 || !x2 || !v || !k || !D || !y || make_geom(ndim, dims, &g)) return 1;
+    if (circular < 0 || circular > 2) return 1;
     for (int d = 0; d < 3; ++d)
         if (!is_pow2(g.L[d])) return 1;
     int64_t P[3];
@@ -417,7 +462,7 @@ int oracle_fft(const double *x1, const double *x2, const double *v, const double
         job J;
         memset(&J, 0, sizeof J);
         J.x1 = x1; J.x2 = x2; J.v = v; J.k = k; J.D = D; J.y = y; J.g = &g;
-        J.circular = circular ? 1 : 0;
+        J.circular = circular;
         J.items = lines;
         J.nitems = lines ? nlines : g.B * g.C;
         J.tw_fwd = (const cplx *const *)twf;
@@ -642,6 +687,7 @@ static int backward_common(const double *x1, const double *x2, const double *v, 
     if (!x1 || !x2 || !v || !k || !D || !gy || !gx1 || !gx2 || !gv || !gk || !gD ||
         make_geom(ndim, dims, &g))
         return 1;
+    if (circular != MODE_LINEAR && circular != MODE_CIRCULAR) return 1;
     if (use_fft)
         for (int d = 0; d < 3; ++d)
             if (!is_pow2(g.L[d])) return 1;
@@ -695,4 +741,4 @@ int oracle_backward_fft(const double *x1, const double *x2, const double *v, con
     return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 1);
 }
 
-int oracle_version(void) { return 2; }
+int oracle_version(void) { return 3; }
