@@ -37,9 +37,11 @@ MALL_BYTES = 256 << 20
 DEFAULT_WORKLOAD = "conv2d_64"
 
 
-def alg_bytes_per_elem(w: W.Workload) -> int:
-    # read x1, v, k, x2 and write y once; D is C values
-    return 5 * w.storage_bytes
+def alg_bytes(w: W.Workload) -> int:
+    """Read x1, v, x2 and k and write y once (D is C values); k has the grid's
+    points, or 2 L_d - 1 per axis in the centered mode."""
+    kelems = int(np.prod(w.kernel_shape))
+    return (4 * w.elems + kelems) * w.storage_bytes
 
 
 def alg_flops(w: W.Workload) -> float:
@@ -50,7 +52,7 @@ def alg_flops(w: W.Workload) -> float:
     import math
     n = w.ndim
     L = list(w.grid)
-    P = [2 * x if w.pad_mode == "linear" else x for x in L]
+    P = [x if w.pad_mode == "circular" else 2 * x for x in L]
     H = P[-1] // 2 + 1
 
     def cplx(m):
@@ -72,7 +74,15 @@ def alg_flops(w: W.Workload) -> float:
         inv += cplx(P[d]) * math.prod(ext[:d] + ext[d + 1:])
         ext[d] = L[d]
     inv += real(P[-1]) * math.prod(L[:-1])
-    per_line = 2 * fwd + inv + 6.0 * math.prod(P[:-1]) * H + 4.0 * math.prod(L)
+    # k: the same pruned transform, or (centered) every line of the full grid
+    if w.pad_mode == "centered":
+        ext = P[:-1] + [H]
+        fwd_k = real(P[-1]) * math.prod(P[:-1])
+        for d in range(n - 1):
+            fwd_k += cplx(P[d]) * math.prod(ext[:d] + ext[d + 1:])
+    else:
+        fwd_k = fwd
+    per_line = fwd + fwd_k + inv + 6.0 * math.prod(P[:-1]) * H + 4.0 * math.prod(L)
     return per_line * w.B * w.C
 
 
@@ -83,7 +93,7 @@ def alg_flops_backward(w: W.Workload) -> float:
     import math
     n = w.ndim
     L = list(w.grid)
-    P = [2 * x if w.pad_mode == "linear" else x for x in L]
+    P = [x if w.pad_mode == "circular" else 2 * x for x in L]
     H = P[-1] // 2 + 1
 
     def cplx(m):
@@ -266,7 +276,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=W.ORDER)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=list(W.WORKLOADS))
     ap.add_argument("--rotate", type=int, default=0, help="input sets to rotate (0: enough to exceed 2x the MALL)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -290,7 +300,7 @@ def main():
     if args.backward:
         bench_backward(args, w, inp)
         return
-    set_bytes = w.elems * alg_bytes_per_elem(w)
+    set_bytes = alg_bytes(w)
     rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
     dev = torch.device("cuda:0")
     base = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
@@ -386,7 +396,7 @@ def main():
         import oracle
         nl = w.B * w.C
         chk = np.array(sorted(set([0, nl // 2, nl - 1])), dtype=np.int64)
-        sub = [W.storage_to_f64(a.reshape((nl,) + tuple(w.grid))[chk], w.dtype)[None]
+        sub = [W.storage_to_f64(a.reshape((nl, -1))[chk].reshape((len(chk),) + a.shape[2:]), w.dtype)[None]
                for a in (inp.x1, inp.x2, inp.v, inp.k)]
         Dsub = W.storage_to_f64(inp.D, w.dtype)[chk % w.C]
         ref = oracle.conv_fft(*sub, Dsub, w.pad_mode)[0].reshape(len(chk), -1)
@@ -410,7 +420,7 @@ def main():
                    "pad_mode": w.pad_mode, "storage": w.dtype, "plan": plan, "rotated_input_sets": rot},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "hbm_frac_alg": round(w.elems * alg_bytes_per_elem(w) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "hbm_frac_alg": round(alg_bytes(w) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "parity_rel_l2_sampled": parity,
         "kernel_source_hash": kernel_source_hash(),
     }

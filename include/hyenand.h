@@ -20,6 +20,12 @@
  * (at least 2L-1, as the appendix "Hardware Context and IO Profile" requires)
  * and cropping the first L_d outputs of every axis; index 0 of k is the zero
  * displacement.  "circular" treats the grid as a torus (transform L_d).
+ * "centered" is the paper's own non-circular form (section 3.2.1): k is
+ * evaluated on the double grid of 2 L_d - 1 points per axis, index L_d - 1 is
+ * the zero displacement, and
+ *     conv[n] = sum_m k[n - m + (L - 1)] u[m]      (every m of the grid),
+ * so every displacement between two grid points has its own weight; the
+ * transform is 2 L_d per axis and the output is cropped as in "linear".
  *
  * The library computes this with fused FFT kernels on the GPU (fp32 compute);
  * it allocates nothing on the call path and keeps no pointer after a call.
@@ -42,7 +48,7 @@ typedef enum {
   HYENAND_ERR_HIP = 4                /* a HIP launch failed; see hyenand_last_error() */
 } hyenand_status;
 
-typedef enum { HYENAND_PAD_LINEAR = 0, HYENAND_PAD_CIRCULAR = 1 } hyenand_pad_mode;
+typedef enum { HYENAND_PAD_LINEAR = 0, HYENAND_PAD_CIRCULAR = 1, HYENAND_PAD_CENTERED = 2 } hyenand_pad_mode;
 
 /* Storage type of x1, x2, v, k, D and y.  Compute is fp32 in both cases;
  * bf16 values are widened on load and rounded to nearest-even on store. */
@@ -53,13 +59,16 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  *
  * x1, x2, v, k, y : device pointers, contiguous row-major [B, C, L1, ..., LN]
  *                   of `dtype` (fp32, or bf16 bits), 16-byte aligned (fresh
- *                   allocations are).  y must not overlap any input.
+ *                   allocations are); with pad_mode centered k is
+ *                   [B, C, 2 L1 - 1, ..., 2 LN - 1].  y must not overlap any
+ *                   input.
  * D               : device pointer, [C] of `dtype`.
  * ndim            : N in {1, 2, 3}.
  * dims            : host pointer to ndim + 2 int64 values {B, C, L1, ..., LN},
  *                   all >= 1; every L_d must be a power of two.  Supported
- *                   transform extents (2 L_d linear, L_d circular): 1D up to
- *                   2^22 points, 2D/3D up to 1024 per axis.
+ *                   transform extents (2 L_d linear and centered, L_d
+ *                   circular): 1D up to 2^22 points, 2D/3D up to 1024 per
+ *                   axis.
  * pad_mode        : hyenand_pad_mode.
  * dtype           : hyenand_dtype.
  * workspace       : device scratch of workspace_bytes (16-byte aligned), owned
@@ -94,8 +103,8 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
  * hyenand_fftconv_shared_k -- as hyenand_fftconv, with one kernel per channel
  * shared by every sample: the Hyena operator's global kernel K of one row per
  * channel (Eq. (hyena), section "Background: Hyena and CKConv"), before
- * HyenaND makes the kernel input-dependent.  k is [C, L1, ..., LN] and sample
- * b, channel c uses k[c].  Everything else, including the workspace sizes
+ * HyenaND makes the kernel input-dependent.  k is [C, L1, ..., LN] (centered:
+ * [C, 2 L1 - 1, ...]) and sample b, channel c uses k[c].  Everything else, including the workspace sizes
  * below, is as for hyenand_fftconv.
  */
 hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const void* v, const void* k,

@@ -490,12 +490,13 @@ hipError_t b_axis1(const MpbLaunch& L) {
   constexpr int TL = TileCfg<P1, 3>::TL;
   const int ntile = (L.g.H + TL - 1) / TL;
   const dim3 grid((unsigned)((int64_t)L.nl * L.g.L0 * ntile));
+  const int nload = INV ? P1 : L.g.L1;
   if (L.b->f.circular)
     hipLaunchKernelGGL((mp_axis1<P1, true, INV, 3>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0,
-                       L.g.half, L.per);
+                       L.g.half, L.per, nload, (int64_t)0);
   else
     hipLaunchKernelGGL((mp_axis1<P1, false, INV, 3>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0,
-                       L.g.half, L.per);
+                       L.g.half, L.per, nload, (int64_t)0);
   return hipGetLastError();
 }
 template <int P1>

@@ -26,13 +26,16 @@ namespace hyenand {
 
 namespace {
 
-template <int N1, bool CIRC, typename TS>
+// KC: k is the centered kernel of 2L - 1 points (linear transform grid); its
+// column lines have no zero half.
+template <int N1, bool CIRC, typename TS, bool KC = false>
 __global__ void __launch_bounds__(512)
     fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int kC) {
+  static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
-  constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
+  constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1 of u (and of k unless centered)
   static_assert(NT / T >= TL, "one round covers the tile");
   __shared__ float2 tile[N1 * TLP];  // exchange scratch, one column per line
   __shared__ float2 twl[imax(1, PassTw<N1, E>::kCount)];
@@ -55,17 +58,33 @@ __global__ void __launch_bounds__(512)
   // column points straight from global memory into registers (lane t holds
   // m1 = t + T e); rows at or beyond NZ are the zero padding
   float2 w[E];
+  if (KC && sig == 1) {
+    // grid points 2m, 2m + 1 (m = m1 N2 + m2) from the 2L - 1 centered points
+    const TS* kl = k + (size_t)k_line(line0 + line, kC) * (size_t)(2 * L - 1);
+    const int Li = (int)L;
 #pragma unroll
-  for (int e = 0; e < E; ++e) {
-    const int m1 = t + T * e;
-    w[e] = czero();
-    if (act && (CIRC || m1 < NZ)) {
-      const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
-      if (sig == 0) {
-        const float2 a = ld2(x1 + n), b = ld2(v + n);
-        w[e] = make_float2(a.x * b.x, a.y * b.y);
-      } else {
-        w[e] = ld2(k + n - gbase + kbase);
+    for (int e = 0; e < E; ++e) {
+      const int m1 = t + T * e;
+      w[e] = czero();
+      if (act) {
+        const int g = 2 * (m1 * N2 + c0 + cc);
+        const int ja = centered_index(g, Li), jb = centered_index(g + 1, Li);
+        w[e] = make_float2(ja >= 0 ? ld1(kl + ja) : 0.f, jb >= 0 ? ld1(kl + jb) : 0.f);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int m1 = t + T * e;
+      w[e] = czero();
+      if (act && (CIRC || m1 < NZ)) {
+        const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
+        if (sig == 0) {
+          const float2 a = ld2(x1 + n), b = ld2(v + n);
+          w[e] = make_float2(a.x * b.x, a.y * b.y);
+        } else {
+          w[e] = ld2(k + n - gbase + kbase);
+        }
       }
     }
   }
@@ -235,7 +254,10 @@ hipError_t cols_fwd(const FsLaunch& L) {
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * 2));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC
-  if (a.bf16) {
+  if (a.centered) {
+    if (a.bf16) hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t, true>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
+    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, float, true>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+  } else if (a.bf16) {
     if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
     else hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
   } else {

@@ -40,10 +40,13 @@ struct Fused1D {
   static constexpr int LDSN = pad16_size(M);
 };
 
-template <int P, bool CIRC, typename TS>
+// KC: k is the centered kernel of 2L - 1 points (linear transform grid); its
+// packed line has no zero half.
+template <int P, bool CIRC, typename TS, bool KC = false>
 __global__ void __launch_bounds__(fused1d_nt(P))
     conv1d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
                  const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
+  static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
   using F = Fused1D<P, CIRC, TS>;
   constexpr int L = F::L, M = F::M, MNZ = F::MNZ, NT = F::NT;
   __shared__ float2 Ub[F::LDSN];
@@ -65,7 +68,25 @@ __global__ void __launch_bounds__(fused1d_nt(P))
   }
 
   // stage the even/odd packed real lines u = x1 v and k
-  if constexpr (L >= 2) {
+  if constexpr (KC) {
+    static_assert(L >= 2, "centered lines have two or more points");
+    batched_copy<MNZ, NT, 8>(
+        tid,
+        [&](int m) {
+          const float2 a = ld2(x1 + base + 2 * m), b = ld2(v + base + 2 * m);
+          return make_float2(a.x * b.x, a.y * b.y);
+        },
+        [&](int m, float2 z) { Ub[m + (m >> 4)] = z; });
+    // grid points 2m, 2m + 1 of k from the 2L - 1 centered points
+    const TS* kl = k + (size_t)k_line(line, kC) * (2 * L - 1);
+    batched_copy<M, NT, 8>(
+        tid,
+        [&](int m) {
+          const int j0 = centered_index(2 * m, L), j1 = centered_index(2 * m + 1, L);
+          return make_float2(j0 >= 0 ? ld1(kl + j0) : 0.f, j1 >= 0 ? ld1(kl + j1) : 0.f);
+        },
+        [&](int m, float2 z) { Kb[m + (m >> 4)] = z; });
+  } else if constexpr (L >= 2) {
     batched_copy<MNZ, NT, 8>(
         tid,
         [&](int m) {
@@ -89,11 +110,12 @@ __global__ void __launch_bounds__(fused1d_nt(P))
     const bool act = which < 2;
     float2* buf = which == 0 ? Ub : Kb;
     const ScrPad16 scr{buf};
+    const int nz = (KC && which == 1) ? M : MNZ;  // a centered k line is full
     float2 w[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       const int m = t + T * e;
-      w[e] = (act && m < MNZ) ? *scr(m) : czero();
+      w[e] = (act && m < nz) ? *scr(m) : czero();
     }
     if constexpr (kTwl) BlockFFT<M, E, false>::run(w, t, scr, act, twf);
     else BlockFFT<M, E, false>::run(w, t, scr, act);
@@ -144,10 +166,10 @@ __global__ void __launch_bounds__(fused1d_nt(P))
   }
 }
 
-template <int P, bool CIRC, typename TS>
+template <int P, bool CIRC, typename TS, bool KC = false>
 static hipError_t launch_1d_fused_t(const FftConvArgs& a, hipStream_t s) {
   using F = Fused1D<P, CIRC, TS>;
-  hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
+  hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS, KC>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
                      (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
                      (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
   return hipGetLastError();
@@ -155,6 +177,12 @@ static hipError_t launch_1d_fused_t(const FftConvArgs& a, hipStream_t s) {
 
 template <int P>
 static hipError_t launch_1d_fused_p(const FftConvArgs& a, hipStream_t s) {
+  if constexpr (P >= 4) {
+    if (a.centered)
+      return a.bf16 ? launch_1d_fused_t<P, false, uint16_t, true>(a, s) : launch_1d_fused_t<P, false, float, true>(a, s);
+  } else {
+    if (a.centered) return hipErrorInvalidValue;
+  }
   if (a.circular) {
     return a.bf16 ? launch_1d_fused_t<P, true, uint16_t>(a, s) : launch_1d_fused_t<P, true, float>(a, s);
   }
@@ -193,15 +221,16 @@ hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s) {
 // real, so they travel together as one complex column (a + i b) and are
 // separated with the mirror bin; M1 = P1/2 column groups cover all M1 + 1
 // columns.
-template <int P0, int P1, bool CIRC, typename TS>
+template <int P0, int P1, bool CIRC, typename TS, bool KC = false>
 struct Fused2D {
   static constexpr int L0 = CIRC ? P0 : P0 / 2;
+  static constexpr int KR = KC ? P0 : L0;    // rows of K held (a centered k fills the grid)
   static constexpr int L1 = CIRC ? P1 : P1 / 2;
   static constexpr int M1 = P1 / 2;          // packed complex row length
   static constexpr int MNZ = (L1 + 1) / 2;   // nonzero packed samples per row
   static constexpr int RP = M1 + 1;          // LDS row pitch (half spectrum + Nyquist)
   static constexpr int NT = 512;
-  // forward row transforms: 2 L0 lines (u rows, k rows) of M1 points
+  // forward row transforms: L0 + KR lines (u rows, k rows) of M1 points
   static constexpr int ER = imin(16, M1);
   static constexpr int TR = M1 / ER;
   static constexpr int LR = NT / TR;         // lines per round
@@ -214,18 +243,22 @@ struct Fused2D {
   static constexpr int EI = imin(8, M1);
   static constexpr int TI = M1 / EI;
   static constexpr int RI = NT / TI;         // rows per round
-  static_assert(2 * L0 >= P0, "column scratch");
+  static_assert(L0 + KR >= P0, "column scratch");
 };
 
-template <int P0, int P1, bool CIRC, typename TS>
+// KC: k is the centered kernel of (2 L0 - 1) x (2 L1 - 1) points on the
+// linear transform grid; K then has P0 nonzero rows and full rows.
+template <int P0, int P1, bool CIRC, typename TS, bool KC = false>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
                  const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
-  using F = Fused2D<P0, P1, CIRC, TS>;
-  constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
-  // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
-  // line of 2 L0 >= P0 slots, the exchange scratch of that column's transforms
-  __shared__ float2 UK[2 * L0 * RP];
+  static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
+  using F = Fused2D<P0, P1, CIRC, TS, KC>;
+  constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT, KR = F::KR;
+  // U half spectrum rows [0, L0), then K's rows [0, KR): column c of both is
+  // one stride-RP line of L0 + KR >= P0 slots, the exchange scratch of that
+  // column's transforms
+  __shared__ float2 UK[(L0 + KR) * RP];
   float2* const Uh = UK;
   float2* const Kh = UK + L0 * RP;
   const int img = blockIdx.x;
@@ -241,6 +274,34 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
   // 0. stage the real rows of u = x1 v and k (coalesced along rows); row r of
   //    Uh holds the even/odd packed line u[r][2m] + i u[r][2m+1].
+  if constexpr (KC) {
+    batched_copy<L0 * L1 / 2, NT, 8>(
+        tid,
+        [&](int i) {
+          const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i);
+          return make_float2(a.x * b.x, a.y * b.y);
+        },
+        [&](int i, float2 z) {
+          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+          Uh[r * RP + m] = z;
+        });
+    // K grid rows from the (2 L0 - 1) x (2 L1 - 1) centered points
+    const TS* kl = k + (size_t)k_line(img, kC) * (2 * L0 - 1) * (2 * L1 - 1);
+    batched_copy<P0 * M1, NT, 8>(
+        tid,
+        [&](int i) {
+          const int g0 = i / M1, m = i - g0 * M1;
+          const int j0 = centered_index(g0, L0);
+          const int ja = centered_index(2 * m, L1), jb = centered_index(2 * m + 1, L1);
+          const TS* kr = kl + (size_t)j0 * (2 * L1 - 1);
+          return make_float2((j0 >= 0 && ja >= 0) ? ld1(kr + ja) * scale : 0.f,
+                             (j0 >= 0 && jb >= 0) ? ld1(kr + jb) * scale : 0.f);
+        },
+        [&](int i, float2 z) {
+          const int g0 = i / M1, m = i - g0 * M1;
+          Kh[g0 * RP + m] = z;
+        });
+  } else {
   batched_copy<L0 * L1 / 2, NT, 8>(
       tid,
       [&](int i) {
@@ -252,22 +313,24 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         Uh[r * RP + m] = make_float2(z.x, z.y);
         Kh[r * RP + m] = make_float2(z.z, z.w);
       });
+  }
   __syncthreads();
 
   // 1. forward row transforms (lanes run across rows), then untangle each row
   {
     constexpr int E = F::ER, T = F::TR, LR = F::LR;
-    for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
+    for (int l0 = 0; l0 < L0 + KR; l0 += LR) {
       using Map = LaneMap<T, NT>;
       static_assert(Map::kLines == LR, "lines per round");
       const int l = l0 + Map::line(tid), t = Map::t(tid);
-      const bool act = (2 * L0) % LR == 0 || l < 2 * L0;  // all lanes busy when rounds are full
+      const bool act = (L0 + KR) % LR == 0 || l < L0 + KR;  // all lanes busy when rounds are full
       float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+      const int nz = (KC && l >= L0) ? M1 : MNZ;  // centered K rows are full
       float2 w[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int m = t + T * e;
-        w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
+        w[e] = (act && (CIRC || m < nz)) ? row[m] : czero();
       }
       BlockFFT<M1, E, false>::run(w, t, ScrS<1>{row}, act);
       if (act) {
@@ -282,7 +345,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     // keeps both, as DC + i Nyquist (column group 0 below).  Rows of U and K
     // are contiguous (Kh = Uh + L0 RP); with 2 L0 a multiple of 64 every
     // wavefront shares one g, so its twiddle is a scalar.
-    constexpr int NR = 2 * L0, NG = imax(1, M1 / 2);
+    constexpr int NR = L0 + KR, NG = imax(1, M1 / 2);
     for (int it = tid; it < NR * NG; it += NT) {
       const int l = it % NR;
       const int g = NR % 64 == 0 ? __builtin_amdgcn_readfirstlane(it / NR) : it / NR;
@@ -324,7 +387,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         const int n = t + T * e;
         const bool nz = act && (CIRC || n < L0);
         wu[e] = nz ? Uh[n * RP + col] : czero();
-        wk[e] = nz ? Kh[n * RP + col] : czero();
+        wk[e] = (act && (CIRC || n < KR)) ? Kh[n * RP + col] : czero();
       }
       const ScrS<RP> su{UK + col};
       BlockFFT<P0, E, false>::run(wu, t, su, act);
@@ -427,9 +490,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       });
 }
 
-template <int P0, int P1, bool CIRC, typename TS>
+template <int P0, int P1, bool CIRC, typename TS, bool KC = false>
 static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(512), 0, s,
+  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, KC>), dim3((unsigned)a.lines), dim3(512), 0, s,
                      (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
                      (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
   return hipGetLastError();
@@ -437,6 +500,10 @@ static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
 
 template <int P0, int P1>
 static hipError_t launch_2d_fused_p(const FftConvArgs& a, hipStream_t s) {
+  if (a.centered) {
+    return a.bf16 ? launch_2d_fused_t<P0, P1, false, uint16_t, true>(a, s)
+                  : launch_2d_fused_t<P0, P1, false, float, true>(a, s);
+  }
   if (a.circular) {
     return a.bf16 ? launch_2d_fused_t<P0, P1, true, uint16_t>(a, s) : launch_2d_fused_t<P0, P1, true, float>(a, s);
   }

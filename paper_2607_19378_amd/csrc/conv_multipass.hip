@@ -44,7 +44,7 @@ template <int PL, bool CIRC, typename TS>
 __global__ void __launch_bounds__(256)
     mp_rows_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int nlines, int rows, int L1, int P1, int HS,
-                int64_t half, int64_t per_line, int kC) {
+                int64_t half, int64_t per_line, int kC, int nsig) {
   using Cf = RowsCfg<PL>;
   constexpr int ML = Cf::ML, HP = Cf::HP, E = Cf::E, T = Cf::T, NT = Cf::NT, RPW = Cf::RPW;
   constexpr int LL = CIRC ? PL : PL / 2;
@@ -81,7 +81,7 @@ __global__ void __launch_bounds__(256)
             if (i / LL < nrow) {
               z.a = ld4(x1 + gbase + i);
               z.b = ld4(v + gbase + i);
-              z.k = ld4(k + kidx(gbase + i));
+              z.k = nsig > 1 ? ld4(k + kidx(gbase + i)) : make_float4(0.f, 0.f, 0.f, 0.f);
             }
             return z;
           },
@@ -104,7 +104,8 @@ __global__ void __launch_bounds__(256)
           tid,
           [&](int i) {
             float2 z = czero();
-            if (i / LL < nrow) z = make_float2(ld1(x1 + gbase + i) * ld1(v + gbase + i), ld1(k + kidx(gbase + i)));
+            if (i / LL < nrow)
+              z = make_float2(ld1(x1 + gbase + i) * ld1(v + gbase + i), nsig > 1 ? ld1(k + kidx(gbase + i)) : 0.f);
             return z;
           },
           [&](int i, float2 z) {
@@ -123,7 +124,7 @@ __global__ void __launch_bounds__(256)
   for (int l0 = 0; l0 < NLINE; l0 += NT / T) {
     const int l = l0 + tid % (NT / T), t = tid / (NT / T);
     const int r = l >> 1;
-    const bool act = l < NLINE && r < nrow;
+    const bool act = l < NLINE && r < nrow && (l & 1) < nsig;
     float2* row = ((l & 1) ? Kr : Ur) + (act ? r : 0) * HP;
     float2 w[E];
 #pragma unroll
@@ -144,7 +145,7 @@ __global__ void __launch_bounds__(256)
   constexpr int NPOST = NLINE * (ML / 2 + 1);
   for (int it = tid; it < NPOST; it += NT) {
     const int l = it % NLINE, g = it / NLINE;
-    if ((l >> 1) < nrow) {
+    if ((l >> 1) < nrow && (l & 1) < nsig) {
       float2* row = ((l & 1) ? Kr : Ur) + (l >> 1) * HP;
       float2 xa, xb;
       r2c_pair(row[g], row[(ML - g) & (ML - 1)], twiddle<ilog2(PL), false>(g), xa, xb);
@@ -170,7 +171,99 @@ __global__ void __launch_bounds__(256)
           float2* U = ws + line * per_line;
           const int64_t off = ws_row(rr, L1, P1, HS) + f;
           U[off] = make_float2(z.x, z.y);
-          U[half + off] = make_float2(z.z, z.w);
+          if (nsig > 1) U[half + off] = make_float2(z.z, z.w);
+        }
+      });
+}
+
+// ---------------------------------------------------------------------------
+// rows of a centered kernel: K holds all P0 x P1 grid rows, each a full real
+// row of PL points gathered from the (2 L0 - 1) x (2 L1 - 1) x (2 LL - 1)
+// centered points (grid index g of an axis holds displacement g or g - 2L);
+// real-to-complex along the last axis, stored at koff + row * HS.
+// ---------------------------------------------------------------------------
+template <int PL, typename TS>
+__global__ void __launch_bounds__(256)
+    mp_rows_kc(const TS* __restrict__ k, float2* __restrict__ ws, int64_t line0, int nlines, int krows, int L0,
+               int L1, int P1, int HS, int64_t koff, int64_t per_line, int kC) {
+  using Cf = RowsCfg<PL>;
+  constexpr int ML = Cf::ML, HP = Cf::HP, E = Cf::E, T = Cf::T, NT = Cf::NT;
+  constexpr int RPW = 2 * Cf::RPW;  // one signal: the two-signal pass's LDS holds twice the rows
+  constexpr int LL = PL / 2;
+  constexpr int H = ML + 1;
+  __shared__ float2 Kr[RPW * HP];
+  __shared__ float2 twl[imax(1, PassTw<ML, E>::kCount)];
+  const int64_t total_rows = (int64_t)nlines * krows;
+  const int64_t row0 = (int64_t)blockIdx.x * RPW;
+  const int nrow = (int)((total_rows - row0) < RPW ? (total_rows - row0) : RPW);
+  const int tid = threadIdx.x;
+  PassTw<ML, E>::fill(twl, tid, NT);
+  const int K1 = 2 * L1 - 1;
+  constexpr int K2 = 2 * LL - 1;
+  const int64_t kpts = (int64_t)(2 * L0 - 1) * K1 * K2;
+
+  // gather the grid points 2m, 2m + 1 of every row
+  batched_copy<RPW * ML, NT, 8>(
+      tid,
+      [&](int i) {
+        const int r = i / ML, m = i - r * ML;
+        float2 z = czero();
+        if (r < nrow) {
+          const int64_t gr = row0 + r;
+          const int64_t line = gr / krows;
+          const int rr = (int)(gr - line * krows);
+          const int j0 = centered_index(rr / P1, L0), j1 = centered_index(rr % P1, L1);
+          if (j0 >= 0 && j1 >= 0) {
+            const TS* kr = k + (size_t)k_line(line0 + line, kC) * kpts + ((size_t)j0 * K1 + j1) * K2;
+            const int ja = centered_index(2 * m, LL), jb = centered_index(2 * m + 1, LL);
+            z = make_float2(ja >= 0 ? ld1(kr + ja) : 0.f, jb >= 0 ? ld1(kr + jb) : 0.f);
+          }
+        }
+        return z;
+      },
+      [&](int i, float2 z) {
+        const int r = i / ML, m = i - r * ML;
+        Kr[r * HP + m] = z;
+      });
+  __syncthreads();
+
+  for (int l0 = 0; l0 < RPW; l0 += NT / T) {
+    const int l = l0 + tid % (NT / T), t = tid / (NT / T);
+    const bool act = l < RPW && l < nrow;
+    float2* row = Kr + (act ? l : 0) * HP;
+    float2 w[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) w[e] = act ? row[t + T * e] : czero();
+    BlockFFT<ML, E, false>::run(w, t, ScrS<1>{row}, act, twl);
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
+    }
+  }
+  __syncthreads();
+
+  constexpr int NPOST = RPW * (ML / 2 + 1);
+  for (int it = tid; it < NPOST; it += NT) {
+    const int l = it % RPW, g = it / RPW;
+    if (l < nrow) {
+      float2* row = Kr + l * HP;
+      float2 xa, xb;
+      r2c_pair(row[g], row[(ML - g) & (ML - 1)], twiddle<ilog2(PL), false>(g), xa, xb);
+      row[g] = xa;
+      row[ML - g] = xb;
+    }
+  }
+  __syncthreads();
+
+  batched_copy<RPW * H, NT, 8>(
+      tid, [&](int i) { return Kr[(i / H) * HP + (i % H)]; },
+      [&](int i, float2 z) {
+        const int r = i / H, f = i - r * H;
+        if (r < nrow) {
+          const int64_t gr = row0 + r;
+          const int64_t line = gr / krows;
+          const int rr = (int)(gr - line * krows);
+          ws[line * per_line + koff + (int64_t)rr * HS + f] = z;
         }
       });
 }
@@ -194,7 +287,7 @@ struct CoreCfg {
 template <int P0, bool CIRC>
 __global__ void __launch_bounds__(mp_core_nt(P0))
     mp_core(float2* __restrict__ ws, const void* __restrict__ Dp, int dbf16, int64_t line0, int C,
-            int ncols, int HS, int H, int64_t half, int64_t per_line, float scale) {
+            int ncols, int HS, int H, int64_t half, int64_t per_line, float scale, int krows) {
   using Cf = CoreCfg<P0, CIRC>;
   constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T, NT = Cf::NT, L0 = Cf::L0;
   __shared__ float2 tile[P0 * TLP];
@@ -232,7 +325,7 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int n = t + T * e;
-    wk[e] = (cv && (CIRC || n < L0)) ? kc[(int64_t)n * ncols] : czero();
+    wk[e] = (cv && (CIRC || n < krows)) ? kc[(int64_t)n * ncols] : czero();
   }
   BlockFFT<P0, E, false>::run(wu, t, sc, act, twl);
   BlockFFT<P0, E, false>::run(wk, t, sc, act, twl);
@@ -381,8 +474,9 @@ hipError_t rows_fwd(const MpLaunch& L) {
   const int64_t total = (int64_t)L.nl * L.g.rows;
   const dim3 grid((unsigned)((total + RowsCfg<PL>::RPW - 1) / RowsCfg<PL>::RPW));
   const FftConvArgs& a = *L.a;
+  const int nsig = L.g.kc ? 1 : 2;  // a centered K has rows of its own (rows_kc)
 #define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, \
-                    L.g.HS, L.g.half, L.per, a.kC
+                    L.g.HS, L.g.half, L.per, a.kC, nsig
   if (a.bf16) {
     if (a.circular) hipLaunchKernelGGL((mp_rows_fwd<PL, true, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
     else hipLaunchKernelGGL((mp_rows_fwd<PL, false, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
@@ -394,19 +488,45 @@ hipError_t rows_fwd(const MpLaunch& L) {
   return hipGetLastError();
 }
 
-template <int P1, bool INV>
-hipError_t axis1(const MpLaunch& L) {
-  constexpr int NS = INV ? 1 : 2;  // U and K forward, Y inverse
+template <int PL>
+hipError_t rows_kc(const MpLaunch& L) {
+  const FftConvArgs& a = *L.a;
+  constexpr int RPW = 2 * RowsCfg<PL>::RPW;
+  const int krows = L.g.P0 * L.g.P1;
+  const int64_t total = (int64_t)L.nl * krows;
+  const dim3 grid((unsigned)((total + RPW - 1) / RPW));
+  if (a.bf16)
+    hipLaunchKernelGGL((mp_rows_kc<PL, uint16_t>), grid, dim3(256), 0, L.s, (const uint16_t*)a.k, L.ws, L.line0, L.nl,
+                       krows, L.g.L0, L.g.L1, L.g.P1, L.g.HS, L.g.half, L.per, a.kC);
+  else
+    hipLaunchKernelGGL((mp_rows_kc<PL, float>), grid, dim3(256), 0, L.s, (const float*)a.k, L.ws, L.line0, L.nl,
+                       krows, L.g.L0, L.g.L1, L.g.P1, L.g.HS, L.g.half, L.per, a.kC);
+  return hipGetLastError();
+}
+
+template <int P1, bool INV, int NS>
+hipError_t axis1_sig(const MpLaunch& L, int planes, int nload, int64_t sig_off) {
   constexpr int TL = TileCfg<P1, NS>::TL;
   const int ntile = (L.g.H + TL - 1) / TL;
-  const dim3 grid((unsigned)((int64_t)L.nl * L.g.L0 * ntile));
+  const dim3 grid((unsigned)((int64_t)L.nl * planes * ntile));
   if (L.a->circular)
-    hipLaunchKernelGGL((mp_axis1<P1, true, INV, NS>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
-                       L.per);
+    hipLaunchKernelGGL((mp_axis1<P1, true, INV, NS>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, planes,
+                       L.g.half, L.per, nload, sig_off);
   else
-    hipLaunchKernelGGL((mp_axis1<P1, false, INV, NS>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, L.g.L0, L.g.half,
-                       L.per);
+    hipLaunchKernelGGL((mp_axis1<P1, false, INV, NS>), grid, dim3(kTileNT), 0, L.s, L.ws, L.g.H, L.g.HS, planes,
+                       L.g.half, L.per, nload, sig_off);
   return hipGetLastError();
+}
+
+// forward: U and K in one pass (a centered K, with P0 planes of P1 nonzero
+// rows, in a pass of its own); inverse: Y
+template <int P1, bool INV>
+hipError_t axis1(const MpLaunch& L) {
+  if (INV) return axis1_sig<P1, true, 1>(L, L.g.L0, P1, 0);
+  if (!L.g.kc) return axis1_sig<P1, false, 2>(L, L.g.L0, L.g.L1, 0);
+  hipError_t e = axis1_sig<P1, false, 1>(L, L.g.L0, L.g.L1, 0);
+  if (e != hipSuccess) return e;
+  return axis1_sig<P1, false, 1>(L, L.g.P0, P1, L.g.half);
 }
 template <int P1>
 hipError_t axis1_fwd(const MpLaunch& L) { return axis1<P1, false>(L); }
@@ -421,12 +541,12 @@ hipError_t core(const MpLaunch& L) {
     constexpr int TL = CoreCfg<P0, true>::TL;
     const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
     hipLaunchKernelGGL((mp_core<P0, true>), grid, dim3(CoreCfg<P0, true>::NT), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
-                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale);
+                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale, L.g.krows0);
   } else {
     constexpr int TL = CoreCfg<P0, false>::TL;
     const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
     hipLaunchKernelGGL((mp_core<P0, false>), grid, dim3(CoreCfg<P0, false>::NT), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
-                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale);
+                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale, L.g.krows0);
   }
   return hipGetLastError();
 }
@@ -464,6 +584,7 @@ hipError_t rows_inv(const MpLaunch& L) {
   }
 
 hipError_t d_rows_fwd(int P, const MpLaunch& L) { HY_SIZE_SWITCH(P, rows_fwd, L) }
+hipError_t d_rows_kc(int P, const MpLaunch& L) { HY_SIZE_SWITCH(P, rows_kc, L) }
 hipError_t d_axis1_fwd(int P, const MpLaunch& L) { HY_SIZE_SWITCH(P, axis1_fwd, L) }
 hipError_t d_core(int P, const MpLaunch& L) { HY_SIZE_SWITCH(P, core, L) }
 hipError_t d_axis1_inv(int P, const MpLaunch& L) { HY_SIZE_SWITCH(P, axis1_inv, L) }
@@ -480,7 +601,7 @@ bool multipass_supported(const FftConvArgs& a) {
 
 size_t multipass_bytes_per_line(const FftConvArgs& a) {
   const MpGeom g = mp_geom(a);
-  return (size_t)(2 * g.half) * sizeof(float2);
+  return (size_t)(g.half + g.halfK) * sizeof(float2);
 }
 
 hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s) {
@@ -489,7 +610,7 @@ hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, voi
   L.a = &a;
   L.g = mp_geom(a);
   L.ws = (float2*)ws;
-  L.per = 2 * L.g.half;
+  L.per = L.g.half + L.g.halfK;
   L.scale = (float)(1.0 / (4.0 * (double)L.g.P0 * (double)L.g.P1 * (double)L.g.PL));
   L.s = s;
   L.line0 = line0;
@@ -497,6 +618,7 @@ hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, voi
   const bool three = a.ndim == 3;
   hipError_t e;
   if ((e = d_rows_fwd(L.g.PL, L)) != hipSuccess) return e;
+  if (L.g.kc && (e = d_rows_kc(L.g.PL, L)) != hipSuccess) return e;
   if (three && (e = d_axis1_fwd(L.g.P1, L)) != hipSuccess) return e;
   if ((e = d_core(L.g.P0, L)) != hipSuccess) return e;
   if (three && (e = d_axis1_inv(L.g.P1, L)) != hipSuccess) return e;

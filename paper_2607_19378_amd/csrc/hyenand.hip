@@ -47,8 +47,9 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   memset(a, 0, sizeof *a);
   if (ndim < 1 || ndim > 3) return fail(HYENAND_ERR_INVALID_ARGUMENT, "ndim must be 1, 2 or 3 (got %d)", ndim);
   if (!dims) return fail(HYENAND_ERR_INVALID_ARGUMENT, "dims is NULL");
-  if (pad_mode != HYENAND_PAD_LINEAR && pad_mode != HYENAND_PAD_CIRCULAR)
-    return fail(HYENAND_ERR_INVALID_ARGUMENT, "pad_mode must be 0 (linear) or 1 (circular), got %d", pad_mode);
+  if (pad_mode != HYENAND_PAD_LINEAR && pad_mode != HYENAND_PAD_CIRCULAR && pad_mode != HYENAND_PAD_CENTERED)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "pad_mode must be 0 (linear), 1 (circular) or 2 (centered), got %d",
+                pad_mode);
   if (dtype != HYENAND_DTYPE_F32 && dtype != HYENAND_DTYPE_BF16)
     return fail(HYENAND_ERR_INVALID_ARGUMENT, "dtype must be 0 (f32) or 1 (bf16), got %d", dtype);
   int64_t total = 1;
@@ -61,8 +62,10 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   a->lines = dims[0] * dims[1];
   a->C = dims[1];
   a->circular = pad_mode == HYENAND_PAD_CIRCULAR;
+  a->centered = pad_mode == HYENAND_PAD_CENTERED;
   a->bf16 = dtype == HYENAND_DTYPE_BF16;
-  // squeeze unit axes: along an axis of extent 1 both modes reduce to the m = 0 term
+  // squeeze unit axes: along an axis of extent 1 every mode reduces to the
+  // zero-displacement term (the centered kernel has 2 * 1 - 1 = 1 point there)
   int nd = 0;
   for (int d = 0; d < ndim; ++d) {
     const int64_t L = dims[2 + d];
@@ -73,6 +76,7 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
     nd = 1;
     a->L[0] = 1;
     a->circular = false;
+    a->centered = false;
   }
   a->ndim = nd;
   for (int d = 0; d < nd; ++d) a->P[d] = a->circular ? a->L[d] : 2 * a->L[d];
@@ -251,6 +255,7 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
 enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP };
 
 BwdPlan choose_bwd_plan(const FftConvArgs& a) {
+  if (a.centered) return BWD_NONE;  // the backward takes the linear and circular modes
   if (fused_backward_supported(a)) return BWD_FUSED;
   if ((a.ndim == 2 || a.ndim == 3) && multipass_supported(a)) return BWD_MULTIPASS;
   if (a.ndim == 1 && backward_fs_supported(a)) return BWD_FOURSTEP;
@@ -362,7 +367,9 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   size_t n = (size_t)a.lines;
   for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];
   const size_t nb = n * es;
-  const size_t kb = shared_k ? nb / (size_t)(a.lines / a.C) : nb;  // [C, L...] or [B, C, L...]
+  size_t kpts = 1;  // kernel points per line: prod L_d, or prod (2 L_d - 1) centered
+  for (int d = 0; d < a.ndim; ++d) kpts *= (size_t)(a.centered ? 2 * a.L[d] - 1 : a.L[d]);
+  const size_t kb = (size_t)(shared_k ? a.C : a.lines) * kpts * es;  // [C, K...] or [B, C, K...]
   const void* ins[4] = {x1, x2, v, k};
   const size_t in_bytes[4] = {nb, nb, nb, kb};
   const char* names[4] = {"x1", "x2", "v", "k"};

@@ -19,6 +19,7 @@ struct FftConvArgs {
   int64_t L[3];   // grid extents of the squeezed problem
   int64_t P[3];   // transform extents: 2L (linear) or L (circular)
   bool circular;
+  bool centered;  // linear transform grid, k on the double grid of 2 L_d - 1 points per axis
   bool bf16;
   int kC;         // 0: k is [B, C, L...]; C: one kernel per channel, k is [C, L...]
   void* ws;       // device workspace (multi-pass plans)

@@ -17,7 +17,10 @@ constexpr int kMaxP = 1024;
 struct MpGeom {
   int L0, P0, L1, P1, LL, PL, H, HS;  // L1 = P1 = 1 in 2D
   int rows;                           // nonzero rows per line: L0 * L1
-  int64_t half;                       // complex entries of U (or K) per line: L0 * P1 * HS
+  int64_t half;                       // complex entries of U (and of K) per line: L0 * P1 * HS
+  bool kc;                            // centered kernel: K holds P0 * P1 rows
+  int krows0;                         // planes n0 of K: L0, or P0 centered
+  int64_t halfK;                      // complex entries of K per line: krows0 * P1 * HS
 };
 
 MpGeom mp_geom(const FftConvArgs& a) {
@@ -36,6 +39,9 @@ MpGeom mp_geom(const FftConvArgs& a) {
   g.HS = (g.H + 15) & ~15;
   g.rows = g.L0 * g.L1;
   g.half = (int64_t)g.L0 * g.P1 * g.HS;
+  g.kc = a.centered;
+  g.krows0 = g.kc ? g.P0 : g.L0;
+  g.halfK = (int64_t)g.krows0 * g.P1 * g.HS;
   return g;
 }
 
@@ -109,13 +115,15 @@ __device__ __forceinline__ void tile_store(const float2* tile, float2* __restric
 }
 
 // ---------------------------------------------------------------------------
-// axis-1 transforms (3D): forward on NS signals (L1 nonzero rows in, P1
-// out), inverse on NS signals (P1 in, L1 cropped rows out); signal s of a
-// line starts at s * half.  One workgroup per (line, n0, tile).
+// axis-1 transforms (3D): forward on NS signals (nload nonzero rows in: L1,
+// or P1 for a centered kernel; P1 out), inverse on NS signals (P1 in, L1
+// cropped rows out).  Signal s of a line starts at sig_off + s * half and
+// has `planes` planes n0.  One workgroup per (line, n0, tile).
 // ---------------------------------------------------------------------------
 template <int P1, bool CIRC, bool INV, int NS>
 __global__ void __launch_bounds__(kTileNT)
-    mp_axis1(float2* __restrict__ ws, int H, int HS, int L0, int64_t half, int64_t per_line) {
+    mp_axis1(float2* __restrict__ ws, int H, int HS, int planes, int64_t half, int64_t per_line, int nload,
+             int64_t sig_off) {
   using Cf = TileCfg<P1, NS>;
   constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T;
   constexpr int L1 = CIRC ? P1 : P1 / 2;
@@ -127,19 +135,19 @@ __global__ void __launch_bounds__(kTileNT)
   const int64_t bid = blockIdx.x;
   const int tl = (int)(bid % ntile);
   const int64_t rest = bid / ntile;
-  const int n0 = (int)(rest % L0);
-  const int64_t line = rest / L0;
+  const int n0 = (int)(rest % planes);
+  const int64_t line = rest / planes;
   const int col0 = tl * TL;
   const int tid = threadIdx.x;
-  float2* base = ws + line * per_line + (int64_t)n0 * P1 * HS;
+  float2* base = ws + line * per_line + sig_off + (int64_t)n0 * P1 * HS;
 
   // Lines are (signal, column) pairs; lane (line, t) moves rows t + T e of
   // its column straight between global memory and registers (consecutive
-  // lanes, consecutive columns), in place: the forward reads the L1 nonzero
-  // rows and writes all P1, the inverse reads P1 rows and keeps L1.  The LDS
-  // tile is only the exchange scratch.
+  // lanes, consecutive columns), in place: the forward reads the nload
+  // nonzero rows and writes all P1, the inverse reads P1 rows and keeps L1.
+  // The LDS tile is only the exchange scratch.
   constexpr int NL = NS * TL;
-  constexpr int NLOAD = INV ? P1 : L1;
+  const int NLOAD = INV ? P1 : nload;
   constexpr int NSTORE = INV ? L1 : P1;
   for (int l0 = 0; l0 < NL; l0 += NT / T) {
     const int l = l0 + tid % (NT / T), t = tid / (NT / T);

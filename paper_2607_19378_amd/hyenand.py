@@ -88,12 +88,21 @@ def _dims(shape: Sequence[int]):
     return len(shape) - 2, arr
 
 
+_MODES = {"linear": 0, "circular": 1, "centered": 2}
+
+
 def _mode(pad_mode: str) -> int:
-    if pad_mode == "linear":
-        return PAD_LINEAR
-    if pad_mode == "circular":
-        return PAD_CIRCULAR
-    raise ValueError(f"pad_mode must be 'linear' or 'circular', got {pad_mode!r}")
+    if pad_mode not in _MODES:
+        raise ValueError(f"pad_mode must be 'linear', 'circular' or 'centered', got {pad_mode!r}")
+    return _MODES[pad_mode]
+
+
+def kernel_shape(shape, pad_mode: str, shared_k: bool = False):
+    """Shape of k for tensors of `shape` ([B, C, L1..LN]): the same, or
+    [B, C, 2 L1 - 1, ...] centered; without B with shared_k."""
+    shape = tuple(int(x) for x in shape)
+    grid = tuple(2 * x - 1 for x in shape[2:]) if pad_mode == "centered" else shape[2:]
+    return (shape[1],) + grid if shared_k else shape[:2] + grid
 
 
 def _dtype_code(dtype) -> int:
@@ -146,13 +155,13 @@ class Prepared:
                  shared_k: bool = False):
         import torch
         shape = tuple(x1.shape)
-        kshape = (shape[1],) + shape[2:] if shared_k else shape
+        kshape = kernel_shape(shape, pad_mode, shared_k)
         for t, want in ((x1, shape), (x2, shape), (v, shape), (k, kshape), (y, shape)):
             if not t.is_cuda:
                 raise ValueError("all tensors must be on the GPU")
             if tuple(t.shape) != want or t.dtype != x1.dtype:
-                raise ValueError("x1, x2, v, y must share shape and dtype; k is the same shape "
-                                 "(or [C, L...] with shared_k)")
+                raise ValueError(f"x1, x2, v, y must share shape and dtype; k must be {kshape} "
+                                 f"(pad_mode {pad_mode!r}, shared_k {shared_k})")
             if not t.is_contiguous():
                 raise ValueError("tensors must be contiguous")
         if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():

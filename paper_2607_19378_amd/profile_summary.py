@@ -25,6 +25,8 @@ import argparse
 import csv
 import glob
 import json
+
+import numpy as np
 import os
 import sys
 
@@ -101,7 +103,7 @@ def main(argv=None):
 
     w = W.WORKLOADS[a.workload]
     plan = H.plan_name(w.shape, w.pad_mode, w.dtype)
-    alg = w.elems * 5 * w.storage_bytes
+    alg = (4 * w.elems + int(np.prod(w.kernel_shape))) * w.storage_bytes  # x1, v, x2, k in; y out
 
     stats = [r for r in _rows(a.trace, "_kernel_stats.csv") if "hyenand" in r["Name"]]
     stats.sort(key=lambda r: -float(r["TotalDurationNs"]))

@@ -17,6 +17,10 @@ datasets is used):
 * ``conv1d_1m``   -- 1D linear, bf16 storage, B=1, C=256, L=2^20 (genomics-scale
   long context, the 1M point of the context-length study).
 
+One more, outside the five: ``conv2d_64_centered`` -- the image workload with
+the paper's own non-circular kernel, evaluated on the double grid (127 x 127
+points per 64 x 64 image, pad mode "centered").
+
 Draw recipe (identical for every workload): ``numpy.random.SeedSequence(seed)``
 spawns one child per tensor in the order x1, x2, v, kernel noise, D; each
 tensor is drawn in C order in blocks of 2^22 elements, block j from a PCG64
@@ -30,7 +34,9 @@ zero-displacement tap):
 * 1D: ``exp(-l / tau) / sqrt(L)`` with ``l`` the index;
 * 2D/3D linear: ``exp(-r / tau)`` with ``r`` the Euclidean index distance from
   the origin;
-* 2D circular: ``exp(-r / tau)`` with ``r`` the periodic (wrap-around) distance.
+* 2D circular: ``exp(-r / tau)`` with ``r`` the periodic (wrap-around) distance;
+* centered: ``exp(-r / tau)`` on the 2 L_d - 1 points per axis, ``r`` the
+  Euclidean distance of the displacement (index minus L_d - 1) from zero.
 
 The circular workload's x1, x2, v are smooth fields: white noise filtered with
 a periodic separable Gaussian (sigma = 4 px, taps truncated at +-16, weights
@@ -46,6 +52,7 @@ import numpy as np
 
 LINEAR = "linear"
 CIRCULAR = "circular"
+CENTERED = "centered"
 
 
 @dataclass(frozen=True)
@@ -76,6 +83,13 @@ class Workload:
         for g in self.grid:
             n *= g
         return n
+
+    @property
+    def kernel_shape(self) -> Tuple[int, ...]:
+        """[B, C, K...]: the grid, or 2 L_d - 1 points per axis centered."""
+        if self.pad_mode == CENTERED:
+            return (self.B, self.C) + tuple(2 * g - 1 for g in self.grid)
+        return self.shape
 
     @property
     def storage_bytes(self) -> int:
@@ -112,6 +126,9 @@ WORKLOADS: Dict[str, Workload] = {
     "conv1d_1m": Workload(
         "conv1d_1m", 1, 256, (1 << 20,), LINEAR, "bf16", 20265, 65536.0, kernel_norm=True,
         description="1D linear gated FFT conv, bf16 storage, B=1 C=256 L=2^20, pad 2^21, crop first L"),
+    "conv2d_64_centered": Workload(
+        "conv2d_64_centered", 8, 256, (64, 64), CENTERED, "f32", 20266, 16.0,
+        description="2D gated FFT conv with 127x127 centered kernels, fp32, B=8 C=256 64x64, pad 128x128"),
 }
 
 # Order in which the workloads are listed (small 1D case first).
@@ -167,13 +184,18 @@ def storage_to_f64(a: np.ndarray, dtype: str) -> np.ndarray:
 # Windows and smoothing used to shape the synthetic data
 # ----------------------------------------------------------------------------
 
-def decay_window(grid: Tuple[int, ...], tau: float, periodic: bool) -> np.ndarray:
-    """exp(-r/tau) on the grid, r the (periodic) Euclidean index distance to 0."""
+def decay_window(grid: Tuple[int, ...], tau: float, periodic: bool, centered: bool = False) -> np.ndarray:
+    """exp(-r/tau) on the grid, r the (periodic) Euclidean index distance to 0;
+    centered: on 2 n - 1 points per axis, r the distance of the displacement."""
+    if centered:
+        grid = tuple(2 * n - 1 for n in grid)
     r2 = np.zeros(grid, dtype=np.float64)
     for ax, n in enumerate(grid):
         i = np.arange(n, dtype=np.float64)
         if periodic:
             i = np.minimum(i, n - i)
+        if centered:
+            i = i - (n - 1) / 2
         shp = [1] * len(grid)
         shp[ax] = n
         r2 = r2 + (i * i).reshape(shp)
@@ -285,14 +307,14 @@ def generate(w: Workload) -> Inputs:
             a = smooth_fields(a, w.smooth_sigma)
         out.append(_quantise_parallel(a, w.dtype))
         del a
-    win = decay_window(w.grid, w.tau, periodic=(w.pad_mode == CIRCULAR))
+    win = decay_window(w.grid, w.tau, periodic=(w.pad_mode == CIRCULAR), centered=(w.pad_mode == CENTERED))
     if w.kernel_norm:
         L = 1
         for g in w.grid:
             L *= g
         win = win / np.sqrt(L)
-    kn = _normals(seqs[3], shp)
-    kv = kn.reshape((-1,) + tuple(w.grid))
+    kn = _normals(seqs[3], w.kernel_shape)
+    kv = kn.reshape((-1,) + win.shape)
 
     def scale(j):
         kv[j] *= win

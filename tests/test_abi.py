@@ -59,7 +59,7 @@ def test_invalid_arguments(L):
     assert call(L, (1, 1, 16), ndim=0) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 1, 1, 1, 16), ndim=4) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 0, 16)) == H.ERR_INVALID_ARGUMENT
-    assert call(L, (1, 1, 16), mode=2) == H.ERR_INVALID_ARGUMENT
+    assert call(L, (1, 1, 16), mode=3) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), dtype=5) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 12)) == H.ERR_UNSUPPORTED  # not a power of two
     assert b"power of two" in L.hyenand_last_error()
@@ -145,6 +145,37 @@ def test_backward_workspace_size(L):
     assert H.backward_workspace_min((1, 2, 1 << 20), "linear", "f32") == 1024 + 3 * (1 << 20) * 8
     with pytest.raises(H.HyenandError):
         H.backward_workspace_size((1, 1, 2048, 2048), "linear", "f32")
+
+
+def test_centered_mode_queries():
+    """pad_mode 2: the transform grid of the linear mode, a workspace that
+    holds U (L0 rows) and a centered K (P0 rows) per line, no backward."""
+    assert H.plan_name((8, 256, 64, 64), "centered", "f32") == "fused2d"
+    assert H.plan_name((1, 64, 4096), "centered", "f32") == "fused1d"
+    assert H.plan_name((1, 4, 1 << 20), "centered", "bf16") == "fourstep1d"
+    assert H.plan_name((1, 2, 128, 128, 128), "centered", "bf16") == "multipass3d"
+    assert H.workspace_min((1, 3, 256, 256), "centered", "f32") == (256 + 512) * 272 * 8
+    assert H.workspace_min((1, 3, 256, 256), "linear", "f32") == 2 * 256 * 272 * 8
+    assert H.workspace_min((1, 2, 1 << 20), "centered", "f32") == 2 * (1 << 20) * 8
+    with pytest.raises(H.HyenandError) as e:
+        H.backward_workspace_size((1, 2, 64), "centered", "f32")
+    assert e.value.status == H.ERR_UNSUPPORTED
+    assert H.kernel_shape((2, 3, 8, 4), "centered") == (2, 3, 15, 7)
+    assert H.kernel_shape((2, 3, 8, 4), "centered", shared_k=True) == (3, 15, 7)
+
+
+def test_centered_kernel_overlap_uses_double_grid(L):
+    """y placed just past the [B, C, L] extent of k but inside its centered
+    [B, C, 2L - 1] extent is rejected."""
+    shape = (1, 2, 64)
+    dims = (ctypes.c_int64 * 3)(*shape)
+    p = [FAKE + i * (1 << 36) for i in range(6)]
+    p[5] = p[3] + 2 * 64 * 4  # past 2 x 64 floats, inside 2 x 127
+    args = [ctypes.c_void_p(x) for x in p]
+    assert L.hyenand_fftconv(*args, 1, dims, 2, 0, None, 0, None) == H.ERR_INVALID_ARGUMENT
+    assert b"y overlaps k" in L.hyenand_last_error()
+    assert L.hyenand_fftconv(*args, 1, dims, 3, 0, None, 0, None) == H.ERR_INVALID_ARGUMENT
+    assert b"pad_mode" in L.hyenand_last_error()
 
 
 def test_shared_kernel_validation(L):
