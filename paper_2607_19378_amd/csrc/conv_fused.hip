@@ -15,6 +15,8 @@
 // row b in the imaginary part).  Zero padding is never stored: inputs beyond L
 // are compile-time zeros of the first pass, and outputs beyond the crop are
 // never written.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace hyenand {
@@ -221,16 +223,15 @@ hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s) {
 // real, so they travel together as one complex column (a + i b) and are
 // separated with the mirror bin; M1 = P1/2 column groups cover all M1 + 1
 // columns.
-template <int P0, int P1, bool CIRC, typename TS, bool KC = false>
+template <int P0, int P1, bool CIRC, typename TS>
 struct Fused2D {
   static constexpr int L0 = CIRC ? P0 : P0 / 2;
-  static constexpr int KR = KC ? P0 : L0;    // rows of K held (a centered k fills the grid)
   static constexpr int L1 = CIRC ? P1 : P1 / 2;
   static constexpr int M1 = P1 / 2;          // packed complex row length
   static constexpr int MNZ = (L1 + 1) / 2;   // nonzero packed samples per row
   static constexpr int RP = M1 + 1;          // LDS row pitch (half spectrum + Nyquist)
   static constexpr int NT = 512;
-  // forward row transforms: L0 + KR lines (u rows, k rows) of M1 points
+  // forward row transforms: 2 L0 lines (u rows, k rows) of M1 points
   static constexpr int ER = imin(16, M1);
   static constexpr int TR = M1 / ER;
   static constexpr int LR = NT / TR;         // lines per round
@@ -243,22 +244,18 @@ struct Fused2D {
   static constexpr int EI = imin(8, M1);
   static constexpr int TI = M1 / EI;
   static constexpr int RI = NT / TI;         // rows per round
-  static_assert(L0 + KR >= P0, "column scratch");
+  static_assert(2 * L0 >= P0, "column scratch");
 };
 
-// KC: k is the centered kernel of (2 L0 - 1) x (2 L1 - 1) points on the
-// linear transform grid; K then has P0 nonzero rows and full rows.
-template <int P0, int P1, bool CIRC, typename TS, bool KC = false>
+template <int P0, int P1, bool CIRC, typename TS>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
                  const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
-  static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
-  using F = Fused2D<P0, P1, CIRC, TS, KC>;
-  constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT, KR = F::KR;
-  // U half spectrum rows [0, L0), then K's rows [0, KR): column c of both is
-  // one stride-RP line of L0 + KR >= P0 slots, the exchange scratch of that
-  // column's transforms
-  __shared__ float2 UK[(L0 + KR) * RP];
+  using F = Fused2D<P0, P1, CIRC, TS>;
+  constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
+  // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
+  // line of 2 L0 >= P0 slots, the exchange scratch of that column's transforms
+  __shared__ float2 UK[2 * L0 * RP];
   float2* const Uh = UK;
   float2* const Kh = UK + L0 * RP;
   const int img = blockIdx.x;
@@ -274,34 +271,6 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
   // 0. stage the real rows of u = x1 v and k (coalesced along rows); row r of
   //    Uh holds the even/odd packed line u[r][2m] + i u[r][2m+1].
-  if constexpr (KC) {
-    batched_copy<L0 * L1 / 2, NT, 8>(
-        tid,
-        [&](int i) {
-          const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i);
-          return make_float2(a.x * b.x, a.y * b.y);
-        },
-        [&](int i, float2 z) {
-          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-          Uh[r * RP + m] = z;
-        });
-    // K grid rows from the (2 L0 - 1) x (2 L1 - 1) centered points
-    const TS* kl = k + (size_t)k_line(img, kC) * (2 * L0 - 1) * (2 * L1 - 1);
-    batched_copy<P0 * M1, NT, 8>(
-        tid,
-        [&](int i) {
-          const int g0 = i / M1, m = i - g0 * M1;
-          const int j0 = centered_index(g0, L0);
-          const int ja = centered_index(2 * m, L1), jb = centered_index(2 * m + 1, L1);
-          const TS* kr = kl + (size_t)j0 * (2 * L1 - 1);
-          return make_float2((j0 >= 0 && ja >= 0) ? ld1(kr + ja) * scale : 0.f,
-                             (j0 >= 0 && jb >= 0) ? ld1(kr + jb) * scale : 0.f);
-        },
-        [&](int i, float2 z) {
-          const int g0 = i / M1, m = i - g0 * M1;
-          Kh[g0 * RP + m] = z;
-        });
-  } else {
   batched_copy<L0 * L1 / 2, NT, 8>(
       tid,
       [&](int i) {
@@ -313,24 +282,22 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         Uh[r * RP + m] = make_float2(z.x, z.y);
         Kh[r * RP + m] = make_float2(z.z, z.w);
       });
-  }
   __syncthreads();
 
   // 1. forward row transforms (lanes run across rows), then untangle each row
   {
     constexpr int E = F::ER, T = F::TR, LR = F::LR;
-    for (int l0 = 0; l0 < L0 + KR; l0 += LR) {
+    for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
       using Map = LaneMap<T, NT>;
       static_assert(Map::kLines == LR, "lines per round");
       const int l = l0 + Map::line(tid), t = Map::t(tid);
-      const bool act = (L0 + KR) % LR == 0 || l < L0 + KR;  // all lanes busy when rounds are full
+      const bool act = (2 * L0) % LR == 0 || l < 2 * L0;  // all lanes busy when rounds are full
       float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
-      const int nz = (KC && l >= L0) ? M1 : MNZ;  // centered K rows are full
       float2 w[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int m = t + T * e;
-        w[e] = (act && (CIRC || m < nz)) ? row[m] : czero();
+        w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
       }
       BlockFFT<M1, E, false>::run(w, t, ScrS<1>{row}, act);
       if (act) {
@@ -345,7 +312,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     // keeps both, as DC + i Nyquist (column group 0 below).  Rows of U and K
     // are contiguous (Kh = Uh + L0 RP); with 2 L0 a multiple of 64 every
     // wavefront shares one g, so its twiddle is a scalar.
-    constexpr int NR = L0 + KR, NG = imax(1, M1 / 2);
+    constexpr int NR = 2 * L0, NG = imax(1, M1 / 2);
     for (int it = tid; it < NR * NG; it += NT) {
       const int l = it % NR;
       const int g = NR % 64 == 0 ? __builtin_amdgcn_readfirstlane(it / NR) : it / NR;
@@ -387,7 +354,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         const int n = t + T * e;
         const bool nz = act && (CIRC || n < L0);
         wu[e] = nz ? Uh[n * RP + col] : czero();
-        wk[e] = (act && (CIRC || n < KR)) ? Kh[n * RP + col] : czero();
+        wk[e] = nz ? Kh[n * RP + col] : czero();
       }
       const ScrS<RP> su{UK + col};
       BlockFFT<P0, E, false>::run(wu, t, su, act);
@@ -490,9 +457,231 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       });
 }
 
-template <int P0, int P1, bool CIRC, typename TS, bool KC = false>
+// Centered kernel, single pass: the K half spectrum fills all P0 rows, so U
+// does not sit beside it in LDS.  U's rows are transformed first in the same
+// region, and each lane keeps the U values of its column group (the nonzero
+// rows n < L0 of its column transform) in registers while K's rows take the
+// region: one P0 x (P1/2 + 1) region per image, as in the linear kernel, and
+// two workgroups per CU for the 128 x 128 grid.
+template <int P0, int P1, typename TS>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
+    conv2d_fused_kc(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
+                    const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
+  using F = Fused2D<P0, P1, false, TS>;
+  constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
+  __shared__ float2 S[P0 * RP];  // U rows [0, L0), then K rows [0, P0); column exchange scratch
+  const int img = blockIdx.x;
+  const int c = img % C;
+  const size_t base = (size_t)img * L0 * L1;
+  const TS* kl = k + (size_t)k_line(img, kC) * (2 * L0 - 1) * (2 * L1 - 1);
+  const int tid = threadIdx.x;
+  constexpr float scale = 1.f / (4.f * (float)P0 * (float)P1);
+
+  // row transforms of NR rows in place (the first nz packed samples of each
+  // row nonzero), then untangling with DC + i Nyquist in slot 0
+  auto rows_r2c = [&](auto nr_c, int nz) {
+    constexpr int NR = decltype(nr_c)::value;
+    constexpr int E = F::ER, T = F::TR, LR = F::LR;
+    for (int l0 = 0; l0 < NR; l0 += LR) {
+      using Map = LaneMap<T, NT>;
+      const int l = l0 + Map::line(tid), t = Map::t(tid);
+      const bool act = NR % LR == 0 || l < NR;
+      float2* row = S + (act ? l : 0) * RP;
+      float2 w[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int m = t + T * e;
+        w[e] = (act && m < nz) ? row[m] : czero();
+      }
+      BlockFFT<M1, E, false>::run(w, t, ScrS<1>{row}, act);
+      if (act) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
+      }
+    }
+    __syncthreads();
+    constexpr int NG = imax(1, M1 / 2);
+    for (int it = tid; it < NR * NG; it += NT) {
+      const int l = it % NR;
+      const int g = NR % 64 == 0 ? __builtin_amdgcn_readfirstlane(it / NR) : it / NR;
+      float2* row = S + l * RP;
+      float2 xa, xb;
+      if (g == 0) {
+        r2c_pair(row[0], row[0], make_float2(1.f, 0.f), xa, xb);
+        row[0] = make_float2(xa.x, xb.x);
+        if constexpr (M1 >= 2) {
+          constexpr int h = M1 / 2;
+          r2c_pair(row[h], row[h], twiddle<ilog2(P1), false>(h), xa, xb);
+          row[h] = xa;
+        }
+      } else {
+        r2c_pair(row[g], row[M1 - g], twiddle<ilog2(P1), false>(g), xa, xb);
+        row[g] = xa;
+        row[M1 - g] = xb;
+      }
+    }
+    __syncthreads();
+  };
+
+  // 0-1. u = x1 v rows, their transforms
+  batched_copy<L0 * L1 / 2, NT, 8>(
+      tid,
+      [&](int i) {
+        const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i);
+        return make_float2(a.x * b.x, a.y * b.y);
+      },
+      [&](int i, float2 z) {
+        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+        S[r * RP + m] = z;
+      });
+  __syncthreads();
+  rows_r2c(std::integral_constant<int, L0>{}, MNZ);
+
+  // 2. each lane keeps the U values of its column transform (rows n < L0)
+  constexpr int E = F::EC, T = F::TC, CR = F::CR;
+  static_assert(M1 <= CR, "one round of column groups");
+  static_assert(L0 % T == 0, "the nonzero rows are the first points of every lane");
+  constexpr int EU = L0 / T;  // nonzero points per lane
+  using Map = LaneMap<T, NT>;
+  const int grp = Map::line(tid), t = Map::t(tid);
+  const bool act = M1 % CR == 0 || grp < M1;
+  const bool nyq = act && grp == 0;
+  const int col = act ? grp : 0;
+  float2 uh[EU];
+#pragma unroll
+  for (int e = 0; e < EU; ++e) uh[e] = act ? S[(t + T * e) * RP + col] : czero();
+  __syncthreads();
+
+  // 3. K grid rows from the centered points, their transforms (full rows)
+  batched_copy<P0 * M1, NT, 8>(
+      tid,
+      [&](int i) {
+        const int g0 = i / M1, m = i - g0 * M1;
+        const int j0 = centered_index(g0, L0);
+        const int ja = centered_index(2 * m, L1), jb = centered_index(2 * m + 1, L1);
+        const TS* kr = kl + (size_t)(j0 >= 0 ? j0 : 0) * (2 * L1 - 1);
+        return make_float2((j0 >= 0 && ja >= 0) ? ld1(kr + ja) * scale : 0.f,
+                           (j0 >= 0 && jb >= 0) ? ld1(kr + jb) * scale : 0.f);
+      },
+      [&](int i, float2 z) {
+        const int g0 = i / M1, m = i - g0 * M1;
+        S[g0 * RP + m] = z;
+      });
+  __syncthreads();
+  rows_r2c(std::integral_constant<int, P0>{}, M1);
+
+  // 4. column groups: forward U (from registers) and K, product with the
+  //    folded shortcut, inverse; keep rows < L0.  Group 0 is the complex
+  //    column DC + i Nyquist, multiplied through LDS as in the linear kernel.
+  {
+    const float twoD = 2.f * scale * ld1(Dp + c);
+    float2 wu[E], wk[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      wu[e] = e < EU ? uh[e] : czero();
+      wk[e] = act ? S[(t + T * e) * RP + col] : czero();
+    }
+    const ScrS<RP> su{S + col};
+    BlockFFT<P0, E, false>::run(wu, t, su, act);
+    BlockFFT<P0, E, false>::run(wk, t, su, act);
+    const ScrS<RP> u0{S};
+    const ScrS<RP> k0{S + M1};
+    __syncthreads();  // exchange reads of the forward transforms are done
+    if (nyq) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        *u0(t + T * e) = wu[e];
+        *k0(t + T * e) = wk[e];
+      }
+    }
+    __syncthreads();
+    if (tid <= P0 / 2) {
+      const int f = tid, fm = (P0 - f) & (P0 - 1);
+      const float2 zu = *u0(f), zum = *u0(fm), zk = *k0(f), zkm = *k0(fm);
+      const float2 ua = c_scale(make_float2(zu.x + zum.x, zu.y - zum.y), 0.5f);
+      const float2 ub = c_scale(make_float2(zu.y + zum.y, zum.x - zu.x), 0.5f);
+      const float2 ka = c_scale(make_float2(zk.x + zkm.x, zk.y - zkm.y), 0.5f);
+      const float2 kb = c_scale(make_float2(zk.y + zkm.y, zkm.x - zk.x), 0.5f);
+      const float2 ya = gated_product(ua, ka, twoD);
+      const float2 yb = gated_product(ub, kb, twoD);
+      *u0(f) = make_float2(ya.x - yb.y, ya.y + yb.x);
+      if (fm != f) *u0(fm) = make_float2(ya.x + yb.y, yb.x - ya.y);
+    }
+    __syncthreads();
+    if (nyq) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) wu[e] = *u0(t + T * e);
+    } else {
+#pragma unroll
+      for (int e = 0; e < E; ++e) wu[e] = gated_product(wu[e], wk[e], twoD);
+    }
+    BlockFFT<P0, E, true>::run(wu, t, su, act);
+    __syncthreads();  // scratch reads of the last exchange are done
+    if (act) {
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const int n = t + T * e;
+        if (n < L0) S[n * RP + col] = wu[e];
+      }
+    }
+  }
+  __syncthreads();
+
+  // 5. inverse row transforms (two real output values per complex point)
+  {
+    constexpr int EI = F::EI, TI = F::TI, RI = F::RI;
+    for (int r0 = 0; r0 < L0; r0 += RI) {
+      using MapI = LaneMap<TI, NT>;
+      const int r = r0 + MapI::line(tid), ti = MapI::t(tid);
+      const bool acti = L0 % RI == 0 || r < L0;
+      float2* row = S + (acti ? r : 0) * RP;
+      float2 w[EI];
+#pragma unroll
+      for (int e = 0; e < EI; ++e) {
+        const int g = ti + TI * e;
+        float2 Yg, Ym;
+        if (g == 0) {
+          const float2 s0 = row[0];
+          Yg = make_float2(s0.x, 0.f);
+          Ym = make_float2(s0.y, 0.f);
+        } else {
+          Yg = row[g];
+          Ym = row[M1 - g];
+        }
+        w[e] = acti ? c2r_pair(Yg, Ym, twiddle<ilog2(P1), false>(g)) : czero();
+      }
+      BlockFFT<M1, EI, true>::run(w, ti, ScrS<1>{row}, acti);
+      if (acti) {
+#pragma unroll
+        for (int e = 0; e < EI; ++e) {
+          const int m = ti + TI * e;
+          if (2 * m < L1) row[m] = w[e];
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // 6. outer gate and store
+  batched_copy<L0 * L1 / 2, NT, 8>(
+      tid, [&](int i) { return ld2(x2 + base + 2 * i); },
+      [&](int i, float2 g) {
+        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+        const float2 q = S[r * RP + m];
+        st2(y + base + 2 * i, make_float2(g.x * q.x, g.y * q.y));
+      });
+}
+
+template <int P0, int P1, typename TS>
+static hipError_t launch_2d_fused_kc_t(const FftConvArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((conv2d_fused_kc<P0, P1, TS>), dim3((unsigned)a.lines), dim3(512), 0, s, (const TS*)a.x1,
+                     (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
+  return hipGetLastError();
+}
+
+template <int P0, int P1, bool CIRC, typename TS>
 static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, KC>), dim3((unsigned)a.lines), dim3(512), 0, s,
+  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(512), 0, s,
                      (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
                      (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
   return hipGetLastError();
@@ -500,10 +689,8 @@ static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
 
 template <int P0, int P1>
 static hipError_t launch_2d_fused_p(const FftConvArgs& a, hipStream_t s) {
-  if (a.centered) {
-    return a.bf16 ? launch_2d_fused_t<P0, P1, false, uint16_t, true>(a, s)
-                  : launch_2d_fused_t<P0, P1, false, float, true>(a, s);
-  }
+  if (a.centered)
+    return a.bf16 ? launch_2d_fused_kc_t<P0, P1, uint16_t>(a, s) : launch_2d_fused_kc_t<P0, P1, float>(a, s);
   if (a.circular) {
     return a.bf16 ? launch_2d_fused_t<P0, P1, true, uint16_t>(a, s) : launch_2d_fused_t<P0, P1, true, float>(a, s);
   }

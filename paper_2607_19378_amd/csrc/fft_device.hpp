@@ -503,8 +503,6 @@ __device__ __forceinline__ float2 c2r_pair(float2 Yg, float2 Ymg, float2 w) {
   return make_float2(s.x - rd.y, s.y + rd.x);                // s + i rd
 }
 
-// Spectral product with the shortcut folded in: U (K + D), D times the
-// transform of a unit impulse (1 at every bin).  Inputs are 2U and 2K.
 // Centered kernels (pad mode "centered"): 2L - 1 points per axis, index
 // L - 1 the zero displacement, transformed on the grid of 2L points.  Grid
 // index g holds displacement g (g < L) or g - 2L (g > L); g = L holds no
@@ -513,6 +511,8 @@ __device__ __forceinline__ int centered_index(int g, int L) {
   return g < L ? g + L - 1 : (g == L ? -1 : g - L - 1);
 }
 
+// Spectral product with the shortcut folded in: U (K + D), D times the
+// transform of a unit impulse (1 at every bin).  Inputs are 2U and 2K.
 __device__ __forceinline__ float2 gated_product(float2 U2, float2 K2, float twoD) {
   return c_mul(U2, make_float2(K2.x + twoD, K2.y));
 }
