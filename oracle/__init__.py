@@ -13,6 +13,9 @@ The arithmetic lives in ``oracle.c`` (plain C, IEEE double):
 * :func:`conv_fft` evaluates it through the convolution theorem with the C
   file's own radix-2 FFT;
 * :func:`fft1d` exposes that FFT so it can be pinned against a naive DFT;
+* :func:`operator` evaluates the whole HyenaND operator of Eq. (HyenaND):
+  l2-normalised q times SiLU(kin), RMSNorm across channels, the gated long
+  convolution with Sigmoid(vin), RMSNorm across channels;
 * :func:`backward_direct` / :func:`backward_fft` give the gradients of a
   scalar loss through y (gx1, gx2, gv, gk, gD for a given gy = dLoss/dy), as
   explicit sums and through the FFT.
@@ -71,8 +74,10 @@ def lib():
             bsig = [_f64p] * 11 + [ctypes.c_int, _i64p, ctypes.c_int, ctypes.c_int]
             L.oracle_backward_direct.argtypes = bsig
             L.oracle_backward_fft.argtypes = bsig
+            L.oracle_operator.argtypes = [_f64p] * 7 + [ctypes.c_double, ctypes.c_double, _f64p, ctypes.c_int,
+                                                        _i64p, ctypes.c_int, ctypes.c_int]
             for f in (L.oracle_direct, L.oracle_fft, L.oracle_direct_points, L.oracle_fft1d,
-                      L.oracle_backward_direct, L.oracle_backward_fft):
+                      L.oracle_backward_direct, L.oracle_backward_fft, L.oracle_operator):
                 f.restype = ctypes.c_int
             _lib = L
         return _lib
@@ -199,3 +204,22 @@ def backward_direct(x1, x2, v, k, D, gy, pad_mode="linear", nthreads=None):
 def backward_fft(x1, x2, v, k, D, gy, pad_mode="linear", nthreads=None):
     """(gx1, gx2, gv, gk, gD) through the convolution theorem (power-of-two extents)."""
     return _backward(lib().oracle_backward_fft, x1, x2, v, k, D, gy, pad_mode, nthreads)
+
+
+def operator(q, kin, vin, k, D, w_in, w_out, eps_l2=1e-6, eps_rms=1e-6, pad_mode="linear", nthreads=None):
+    """The HyenaND operator, Eq. (HyenaND): y = RMSNorm(Sigmoid(vin) * (k conv
+    RMSNorm(l2(q) * SiLU(kin)) + D * that)), both norms across the C channels
+    of every (b, grid point), with per-channel weights w_in and w_out."""
+    arrs, dims, nd = _prep(q, vin, kin, k, D, pad_mode)
+    qa, va, ka, kk, Da = arrs
+    wi = np.ascontiguousarray(w_in, dtype=np.float64)
+    wo = np.ascontiguousarray(w_out, dtype=np.float64)
+    if wi.shape != Da.shape or wo.shape != Da.shape:
+        raise ValueError("w_in and w_out must have shape [C]")
+    y = np.zeros(qa.shape, dtype=np.float64)
+    rc = lib().oracle_operator(_ptr(qa), _ptr(ka), _ptr(va), _ptr(kk), _ptr(Da), _ptr(wi), _ptr(wo),
+                               float(eps_l2), float(eps_rms), _ptr(y), nd, dims.ctypes.data_as(_i64p),
+                               _mode(pad_mode), int(nthreads or default_threads()))
+    if rc != 0:
+        raise RuntimeError(f"oracle returned {rc}")
+    return y

@@ -63,6 +63,19 @@
  * The mode argument: 0 linear, 1 circular, 2 centered (forward only; the
  * backward takes 0 and 1).
  *
+ * The HyenaND operator, Eq. (HyenaND) of section 3.2 (oracle_operator):
+ * with q, kin, vin the three projections [B, C, L...], per sample b and grid
+ * point p, the channel vectors are normalised across the C channels:
+ *
+ *   a[c]  = q[c] / max(||q[:]||_2, eps_l2) * SiLU(kin[c])   (l2 norm of q)
+ *   u[c]  = a[c] / sqrt(mean_c a^2 + eps_rms) * w_in[c]      (RMSNorm)
+ *   z     = Sigmoid(vin) * (conv(k, u) + D[c] u)             (long conv,
+ *           shortcut and outer gate; conv in the given mode)
+ *   y[c]  = z[c] / sqrt(mean_c z^2 + eps_rms) * w_out[c]     (RMSNorm)
+ *
+ * with SiLU(x) = x / (1 + exp(-x)), Sigmoid(x) = 1 / (1 + exp(-x)).  The
+ * paper writes the operator without the shortcut; D = 0 gives it exactly.
+ *
  * Return codes: 0 ok, 1 bad argument, 2 out of memory, 3 the inverse
  * transform left an imaginary residue above 1e-9 of the real part (a broken
  * FFT), 4 a thread could not be started.
@@ -741,4 +754,77 @@ int oracle_backward_fft(const double *x1, const double *x2, const double *v, con
     return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 1);
 }
 
-int oracle_version(void) { return 3; }
+int oracle_version(void) { return 4; }
+
+/* ------------------------------------------------------------------------- */
+/* HyenaND operator: normalised prologue, long convolution, normalised       */
+/* epilogue                                                                  */
+/* ------------------------------------------------------------------------- */
+
+static double silu(double x) { return x / (1.0 + exp(-x)); }
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+int oracle_operator(const double *q, const double *kin, const double *vin, const double *k,
+                    const double *D, const double *w_in, const double *w_out, double eps_l2,
+                    double eps_rms, double *y, int ndim, const int64_t *dims, int mode,
+                    int nthreads) {
+    geom g;
+    if (!q || !kin || !vin || !k || !D || !w_in || !w_out || !y || make_geom(ndim, dims, &g)) return 1;
+    if (mode < 0 || mode > 2 || !(eps_l2 >= 0.0) || !(eps_rms >= 0.0)) return 1;
+    const int64_t B = g.B, C = g.C, box = g.box, n = B * C * box;
+    double *u = (double *)malloc((size_t)n * sizeof(double));
+    double *gate = (double *)malloc((size_t)n * sizeof(double));
+    double *ones = (double *)malloc((size_t)n * sizeof(double));
+    if (!u || !gate || !ones) {
+        free(u); free(gate); free(ones);
+        return 2;
+    }
+    /* 1. prologue, one channel vector per (b, p) */
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t p = 0; p < box; ++p) {
+            double qq = 0.0;
+            for (int64_t c = 0; c < C; ++c) {
+                double x = q[(b * C + c) * box + p];
+                qq += x * x;
+            }
+            double qn = sqrt(qq);
+            if (qn < eps_l2) qn = eps_l2;
+            double aa = 0.0;
+            for (int64_t c = 0; c < C; ++c) {
+                int64_t i = (b * C + c) * box + p;
+                double a = (qn > 0.0 ? q[i] / qn : 0.0) * silu(kin[i]);
+                u[i] = a;
+                aa += a * a;
+            }
+            double r = sqrt(aa / (double)C + eps_rms);
+            for (int64_t c = 0; c < C; ++c) {
+                int64_t i = (b * C + c) * box + p;
+                u[i] = (r > 0.0 ? u[i] / r : 0.0) * w_in[c];
+            }
+        }
+    for (int64_t i = 0; i < n; ++i) {
+        gate[i] = sigmoid(vin[i]);
+        ones[i] = 1.0;
+    }
+    /* 2. the gated long convolution of u (x1 = u, v = 1, x2 = the gate) */
+    int rc = oracle_fft(u, gate, ones, k, D, y, ndim, dims, mode, NULL, 0, nthreads);
+    /* 3. epilogue RMSNorm across channels */
+    if (!rc)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t p = 0; p < box; ++p) {
+                double zz = 0.0;
+                for (int64_t c = 0; c < C; ++c) {
+                    double z = y[(b * C + c) * box + p];
+                    zz += z * z;
+                }
+                double r = sqrt(zz / (double)C + eps_rms);
+                for (int64_t c = 0; c < C; ++c) {
+                    int64_t i = (b * C + c) * box + p;
+                    y[i] = (r > 0.0 ? y[i] / r : 0.0) * w_out[c];
+                }
+            }
+    free(u);
+    free(gate);
+    free(ones);
+    return rc;
+}
