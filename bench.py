@@ -210,6 +210,66 @@ def bench_backward(args, w, inp):
     print(json.dumps(out))
 
 
+def bench_operator(args, w, inp):
+    """Time hyenand_operator (the whole HyenaND operator: normalised prologue,
+    the gated long convolution, output RMSNorm) on the workload's shape, with
+    x1, v, x2 as q, kin, vin; prints one JSON line."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    rng = np.random.default_rng(w.seed + 11)
+    w_in = W.quantise(1.0 + 0.2 * rng.standard_normal(w.C), w.dtype)
+    w_out = W.quantise(1.0 + 0.2 * rng.standard_normal(w.C), w.dtype)
+    set_bytes = alg_bytes(w)  # q, kin, vin, k in and y out once: the fused minimum
+    rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
+    dev = torch.device("cuda:0")
+    base = [to_device(a, w.dtype) for a in (inp.x1, inp.v, inp.x2, inp.k, inp.D, w_in, w_out)]
+    sets = [base] + [[t.clone() for t in base] for _ in range(1, rot)]
+    ys = [torch.empty_like(base[0]) for _ in range(rot)]
+    ws = torch.empty(H.operator_workspace_size(w.shape, w.pad_mode, w.dtype), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    calls = [H.PreparedOperator(y, *st, 1e-6, 1e-6, w.pad_mode, ws, stream) for y, st in zip(ys, sets)]
+    for i in range(args.warmup):
+        calls[i % rot]()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        calls[i % rot]()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    avg_s = ev0.elapsed_time(ev1) * 1e-3 / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    hbm_gbs = set_bytes / avg_s / 1e9
+    parity = None
+    if not args.no_parity:
+        import oracle
+        f64 = [W.storage_to_f64(a, w.dtype) for a in (inp.x1, inp.v, inp.x2, inp.k, inp.D, w_in, w_out)]
+        ref = oracle.operator(*f64, eps_l2=1e-6, eps_rms=1e-6, pad_mode=w.pad_mode)
+        yv = ys[(args.steps - 1) % rot]
+        if yv.dtype == torch.bfloat16:
+            got = W.bf16_bits_to_f64(yv.view(torch.int16).cpu().numpy().view(np.uint16))
+        else:
+            got = yv.cpu().numpy().astype(np.float64)
+        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    out = {
+        "metric": "HyenaND operator (Eq. HyenaND) GElem/s on 1 MI355X",
+        "value": round(w.elems / (ms_per_step * 1e-3) / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
+        "config": {"workload": w.name, "pass": "operator", "B": w.B, "C": w.C, "grid": list(w.grid),
+                   "pad_mode": w.pad_mode, "storage": w.dtype, "rotated_input_sets": rot},
+        "roofline": {"bound": "hbm", "achieved": round(hbm_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(hbm_gbs / HBM_PEAK_GBS, 4), "traffic": None, "alg_bytes_per_call": set_bytes,
+                     "avg_call_us": round(avg_s * 1e6, 3)},
+        "cpu_baseline": None, "parity_rel_l2": parity, "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out))
+
+
 def to_device(arr, dtype):
     import torch
     if dtype == "f32":
@@ -284,6 +344,8 @@ def main():
     ap.add_argument("--no-stream-peak", action="store_true", help="skip the 1 GiB copy that measures the stream peak")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward (gradients for x1, x2, v, k, D) instead of the forward")
+    ap.add_argument("--operator", action="store_true",
+                    help="time the whole HyenaND operator (norms and activations around the convolution)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -299,6 +361,9 @@ def main():
     inp = W.generate(w)
     if args.backward:
         bench_backward(args, w, inp)
+        return
+    if args.operator:
+        bench_operator(args, w, inp)
         return
     set_bytes = alg_bytes(w)
     rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))

@@ -169,6 +169,38 @@ hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* 
 hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, int pad_mode,
                                                       int dtype, size_t* bytes_out);
 
+/*
+ * hyenand_operator -- the whole HyenaND operator of Eq. (HyenaND), section
+ * 3.2, around the same long convolution:
+ *
+ *     a   = l2(q) * SiLU(kin),  l2(q) = q / max(||q[b, :, p]||_2, eps_l2)
+ *     u   = a / sqrt(mean_c a^2 + eps_rms) * w_in[c]            (RMSNorm)
+ *     z   = Sigmoid(vin) * (k conv u + D[c] * u)                 (as y above)
+ *     y   = z / sqrt(mean_c z^2 + eps_rms) * w_out[c]            (RMSNorm)
+ *
+ * with SiLU(x) = x / (1 + exp(-x)) and Sigmoid(x) = 1 / (1 + exp(-x)); the
+ * norms and means run across the C channels of every sample b and grid point
+ * p.  The paper writes the operator without the shortcut: pass D = 0.
+ * q, kin, vin, y : [B, C, L...] of dtype (16-byte aligned); k as for
+ * hyenand_fftconv (its shape follows pad_mode); D, w_in, w_out : [C] of dtype.
+ * eps_l2, eps_rms: finite, >= 0.  C is at most 16384.  y must not overlap an
+ * input.  workspace: at least the normalisation scales (B * prod L floats, in
+ * a 256-byte block) plus hyenand_fftconv_workspace_min() bytes;
+ * hyenand_operator_workspace_size() is the recommended size.  Three stages
+ * on `stream`: a pass over q and kin for the per-point scale, the transform
+ * kernels with the gates applied as they stage and store, and an in-place
+ * RMSNorm of y (one read, one write).  Stream, determinism and error
+ * conventions as for hyenand_fftconv.
+ */
+hyenand_status hyenand_operator(const void* q, const void* kin, const void* vin, const void* k, const void* D,
+                                const void* w_in, const void* w_out, float eps_l2, float eps_rms, void* y,
+                                int ndim, const int64_t* dims, int pad_mode, int dtype, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* Recommended workspace bytes for hyenand_operator. */
+hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                               size_t* bytes_out);
+
 /* Static text for a status code. */
 const char* hyenand_status_string(int status);
 

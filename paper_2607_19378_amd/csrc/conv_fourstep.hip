@@ -28,10 +28,11 @@ namespace {
 
 // KC: k is the centered kernel of 2L - 1 points (linear transform grid); its
 // column lines have no zero half.
-template <int N1, bool CIRC, typename TS, bool KC = false>
+template <int N1, bool CIRC, typename TS, bool KC = false, bool ACT = false>
 __global__ void __launch_bounds__(512)
     fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
-                float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int kC) {
+                float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int kC, ActIn ain,
+                int C) {
   static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
@@ -80,8 +81,7 @@ __global__ void __launch_bounds__(512)
       if (act && (CIRC || m1 < NZ)) {
         const size_t n = gbase + 2 * ((size_t)m1 * N2 + c0 + cc);
         if (sig == 0) {
-          const float2 a = ld2(x1 + n), b = ld2(v + n);
-          w[e] = make_float2(a.x * b.x, a.y * b.y);
+          w[e] = line_gates<ACT, TS>(ain, line0 + line, C).u2(ld2(x1 + n), ld2(v + n), (int64_t)(n - gbase));
         } else {
           w[e] = ld2(k + n - gbase + kbase);
         }
@@ -190,7 +190,7 @@ __global__ void __launch_bounds__(512)
   }
 }
 
-template <int N1, bool CIRC, typename TS>
+template <int N1, bool CIRC, typename TS, bool ACT = false>
 __global__ void __launch_bounds__(512)
     fs_cols_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0, int N2,
                 int64_t per_line) {
@@ -223,7 +223,7 @@ __global__ void __launch_bounds__(512)
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int m1 = t + T * e;
-    g[e] = (act && (CIRC || m1 < NOUT)) ? ld2(x2 + gbase + 2 * (size_t)m1 * N2) : czero();
+    g[e] = (act && (CIRC || m1 < NOUT)) ? Gates<ACT>{}.g2(ld2(x2 + gbase + 2 * (size_t)m1 * N2)) : czero();
   }
   BlockFFT<N1, E, true>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act, twl);
   if (act) {
@@ -253,17 +253,19 @@ hipError_t cols_fwd(const FsLaunch& L) {
   constexpr int TL = ColCfg<N1>::TL;
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * 2));
   const FftConvArgs& a = *L.a;
-#define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC
+#define HY_ARGS(TS) \
+  (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC, a.act_in, (int)a.C
+#define HY_LAUNCH(CI, TS, KC)                                                                                     \
+  if (a.act) hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, true>), grid, dim3(512), 0, L.s, HY_ARGS(TS)); \
+  else hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, false>), grid, dim3(512), 0, L.s, HY_ARGS(TS));
   if (a.centered) {
-    if (a.bf16) hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t, true>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, float, true>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+    if (a.bf16) { HY_LAUNCH(false, uint16_t, true) } else { HY_LAUNCH(false, float, true) }
   } else if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) { HY_LAUNCH(true, uint16_t, false) } else { HY_LAUNCH(false, uint16_t, false) }
   } else {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_fwd<N1, true, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((fs_cols_fwd<N1, false, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+    if (a.circular) { HY_LAUNCH(true, float, false) } else { HY_LAUNCH(false, float, false) }
   }
+#undef HY_LAUNCH
 #undef HY_ARGS
   return hipGetLastError();
 }
@@ -274,13 +276,15 @@ hipError_t cols_inv(const FsLaunch& L) {
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL)));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, kN2, L.per
+#define HY_LAUNCH(CI, TS)                                                                                  \
+  if (a.act) hipLaunchKernelGGL((fs_cols_inv<N1, CI, TS, true>), grid, dim3(512), 0, L.s, HY_ARGS(TS)); \
+  else hipLaunchKernelGGL((fs_cols_inv<N1, CI, TS, false>), grid, dim3(512), 0, L.s, HY_ARGS(TS));
   if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((fs_cols_inv<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) { HY_LAUNCH(true, uint16_t) } else { HY_LAUNCH(false, uint16_t) }
   } else {
-    if (a.circular) hipLaunchKernelGGL((fs_cols_inv<N1, true, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((fs_cols_inv<N1, false, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+    if (a.circular) { HY_LAUNCH(true, float) } else { HY_LAUNCH(false, float) }
   }
+#undef HY_LAUNCH
 #undef HY_ARGS
   return hipGetLastError();
 }

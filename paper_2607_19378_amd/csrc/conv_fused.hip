@@ -44,10 +44,12 @@ struct Fused1D {
 
 // KC: k is the centered kernel of 2L - 1 points (linear transform grid); its
 // packed line has no zero half.
-template <int P, bool CIRC, typename TS, bool KC = false>
+// ACT: the HyenaND operator's gates (Gates).
+template <int P, bool CIRC, typename TS, bool KC = false, bool ACT = false>
 __global__ void __launch_bounds__(fused1d_nt(P))
     conv1d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
-                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
+                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC,
+                 ActIn ain) {
   static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
   using F = Fused1D<P, CIRC, TS>;
   constexpr int L = F::L, M = F::M, MNZ = F::MNZ, NT = F::NT;
@@ -64,6 +66,7 @@ __global__ void __launch_bounds__(fused1d_nt(P))
   const size_t base = (size_t)line * L;
   const size_t kbase = (size_t)k_line(line, kC) * L;
   const int tid = threadIdx.x;
+  const Gates<ACT> G = line_gates<ACT, TS>(ain, line, C);
   if constexpr (kTwl) {
     TwF::fill(twf, tid, NT);
     TwI::fill(twi, tid, NT);
@@ -74,10 +77,7 @@ __global__ void __launch_bounds__(fused1d_nt(P))
     static_assert(L >= 2, "centered lines have two or more points");
     batched_copy<MNZ, NT, 8>(
         tid,
-        [&](int m) {
-          const float2 a = ld2(x1 + base + 2 * m), b = ld2(v + base + 2 * m);
-          return make_float2(a.x * b.x, a.y * b.y);
-        },
+        [&](int m) { return G.u2(ld2(x1 + base + 2 * m), ld2(v + base + 2 * m), 2 * m); },
         [&](int m, float2 z) { Ub[m + (m >> 4)] = z; });
     // grid points 2m, 2m + 1 of k from the 2L - 1 centered points
     const TS* kl = k + (size_t)k_line(line, kC) * (2 * L - 1);
@@ -92,15 +92,16 @@ __global__ void __launch_bounds__(fused1d_nt(P))
     batched_copy<MNZ, NT, 8>(
         tid,
         [&](int m) {
-          const float2 a = ld2(x1 + base + 2 * m), b = ld2(v + base + 2 * m), kk = ld2(k + kbase + 2 * m);
-          return make_float4(a.x * b.x, a.y * b.y, kk.x, kk.y);
+          const float2 u = G.u2(ld2(x1 + base + 2 * m), ld2(v + base + 2 * m), 2 * m);
+          const float2 kk = ld2(k + kbase + 2 * m);
+          return make_float4(u.x, u.y, kk.x, kk.y);
         },
         [&](int m, float4 z) {
           Ub[m + (m >> 4)] = make_float2(z.x, z.y);
           Kb[m + (m >> 4)] = make_float2(z.z, z.w);
         });
   } else if (tid == 0) {  // a single sample
-    Ub[0] = make_float2(ld1(x1 + base) * ld1(v + base), 0.f);
+    Ub[0] = make_float2(G.u1(ld1(x1 + base), ld1(v + base), 0), 0.f);
     Kb[0] = make_float2(ld1(k + kbase), 0.f);
   }
   __syncthreads();
@@ -161,8 +162,8 @@ __global__ void __launch_bounds__(fused1d_nt(P))
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int n = 2 * (t + T * e);
-        if (n < L) st1(y + base + n, ld1(x2 + base + n) * w[e].x);
-        if (n + 1 < L) st1(y + base + n + 1, ld1(x2 + base + n + 1) * w[e].y);
+        if (n < L) st1(y + base + n, G.g1(ld1(x2 + base + n)) * w[e].x);
+        if (n + 1 < L) st1(y + base + n + 1, G.g1(ld1(x2 + base + n + 1)) * w[e].y);
       }
     }
   }
@@ -171,9 +172,14 @@ __global__ void __launch_bounds__(fused1d_nt(P))
 template <int P, bool CIRC, typename TS, bool KC = false>
 static hipError_t launch_1d_fused_t(const FftConvArgs& a, hipStream_t s) {
   using F = Fused1D<P, CIRC, TS>;
-  hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS, KC>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
-                     (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
-                     (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
+  if (a.act)
+    hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS, KC, true>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
+                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                       (int)a.C, a.kC, a.act_in);
+  else
+    hipLaunchKernelGGL((conv1d_fused<P, CIRC, TS, KC, false>), dim3((unsigned)a.lines), dim3(F::NT), 0, s,
+                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                       (int)a.C, a.kC, a.act_in);
   return hipGetLastError();
 }
 
@@ -247,10 +253,11 @@ struct Fused2D {
   static_assert(2 * L0 >= P0, "column scratch");
 };
 
-template <int P0, int P1, bool CIRC, typename TS>
+template <int P0, int P1, bool CIRC, typename TS, bool ACT = false>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
-                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
+                 const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC,
+                 ActIn ain) {
   using F = Fused2D<P0, P1, CIRC, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
   // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
@@ -263,6 +270,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   const size_t base = (size_t)img * L0 * L1;
   const size_t kbase = (size_t)k_line(img, kC) * L0 * L1;
   const int tid = threadIdx.x;
+  const Gates<ACT> G = line_gates<ACT, TS>(ain, img, C);
 
   // The normalisation 1 / (4 P0 P1) of the two unnormalised inverses and of
   // the doubled R2C outputs is a power of two: it is applied, exactly, to k
@@ -274,8 +282,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   batched_copy<L0 * L1 / 2, NT, 8>(
       tid,
       [&](int i) {
-        const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i), kk = ld2(k + kbase + 2 * i);
-        return make_float4(a.x * b.x, a.y * b.y, kk.x * scale, kk.y * scale);
+        const float2 u = G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i);
+        const float2 kk = ld2(k + kbase + 2 * i);
+        return make_float4(u.x, u.y, kk.x * scale, kk.y * scale);
       },
       [&](int i, float4 z) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
@@ -449,7 +458,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
   // 4. outer gate and store (coalesced along rows)
   batched_copy<L0 * L1 / 2, NT, 8>(
-      tid, [&](int i) { return ld2(x2 + base + 2 * i); },
+      tid, [&](int i) { return G.g2(ld2(x2 + base + 2 * i)); },
       [&](int i, float2 g) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
         const float2 q = Uh[r * RP + m];
@@ -463,10 +472,11 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 // rows n < L0 of its column transform) in registers while K's rows take the
 // region: one P0 x (P1/2 + 1) region per image, as in the linear kernel, and
 // two workgroups per CU for the 128 x 128 grid.
-template <int P0, int P1, typename TS>
+template <int P0, int P1, typename TS, bool ACT = false>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused_kc(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
-                    const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC) {
+                    const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC,
+                    ActIn ain) {
   using F = Fused2D<P0, P1, false, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
   __shared__ float2 S[P0 * RP];  // U rows [0, L0), then K rows [0, P0); column exchange scratch
@@ -475,6 +485,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   const size_t base = (size_t)img * L0 * L1;
   const TS* kl = k + (size_t)k_line(img, kC) * (2 * L0 - 1) * (2 * L1 - 1);
   const int tid = threadIdx.x;
+  const Gates<ACT> G = line_gates<ACT, TS>(ain, img, C);
   constexpr float scale = 1.f / (4.f * (float)P0 * (float)P1);
 
   // row transforms of NR rows in place (the first nz packed samples of each
@@ -525,11 +536,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
   // 0-1. u = x1 v rows, their transforms
   batched_copy<L0 * L1 / 2, NT, 8>(
-      tid,
-      [&](int i) {
-        const float2 a = ld2(x1 + base + 2 * i), b = ld2(v + base + 2 * i);
-        return make_float2(a.x * b.x, a.y * b.y);
-      },
+      tid, [&](int i) { return G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i); },
       [&](int i, float2 z) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
         S[r * RP + m] = z;
@@ -664,7 +671,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
   // 6. outer gate and store
   batched_copy<L0 * L1 / 2, NT, 8>(
-      tid, [&](int i) { return ld2(x2 + base + 2 * i); },
+      tid, [&](int i) { return G.g2(ld2(x2 + base + 2 * i)); },
       [&](int i, float2 g) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
         const float2 q = S[r * RP + m];
@@ -674,16 +681,27 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
 template <int P0, int P1, typename TS>
 static hipError_t launch_2d_fused_kc_t(const FftConvArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((conv2d_fused_kc<P0, P1, TS>), dim3((unsigned)a.lines), dim3(512), 0, s, (const TS*)a.x1,
-                     (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
+  if (a.act)
+    hipLaunchKernelGGL((conv2d_fused_kc<P0, P1, TS, true>), dim3((unsigned)a.lines), dim3(512), 0, s, (const TS*)a.x1,
+                       (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC,
+                       a.act_in);
+  else
+    hipLaunchKernelGGL((conv2d_fused_kc<P0, P1, TS, false>), dim3((unsigned)a.lines), dim3(512), 0, s, (const TS*)a.x1,
+                       (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC,
+                       a.act_in);
   return hipGetLastError();
 }
 
 template <int P0, int P1, bool CIRC, typename TS>
 static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS>), dim3((unsigned)a.lines), dim3(512), 0, s,
-                     (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k,
-                     (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC);
+  if (a.act)
+    hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, true>), dim3((unsigned)a.lines), dim3(512), 0, s,
+                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                       (int)a.C, a.kC, a.act_in);
+  else
+    hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false>), dim3((unsigned)a.lines), dim3(512), 0, s,
+                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                       (int)a.C, a.kC, a.act_in);
   return hipGetLastError();
 }
 

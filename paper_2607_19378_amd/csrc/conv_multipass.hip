@@ -40,11 +40,11 @@ struct RowsCfg {
   static constexpr int RPW = imax(1, imin(NT / (2 * T), (36 * 1024) / (2 * HP * 8)));  // rows per workgroup
 };
 
-template <int PL, bool CIRC, typename TS>
+template <int PL, bool CIRC, typename TS, bool ACT = false>
 __global__ void __launch_bounds__(256)
     mp_rows_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int nlines, int rows, int L1, int P1, int HS,
-                int64_t half, int64_t per_line, int kC, int nsig) {
+                int64_t half, int64_t per_line, int kC, int nsig, ActIn ain, int C) {
   using Cf = RowsCfg<PL>;
   constexpr int ML = Cf::ML, HP = Cf::HP, E = Cf::E, T = Cf::T, NT = Cf::NT, RPW = Cf::RPW;
   constexpr int LL = CIRC ? PL : PL / 2;
@@ -82,6 +82,12 @@ __global__ void __launch_bounds__(256)
               z.a = ld4(x1 + gbase + i);
               z.b = ld4(v + gbase + i);
               z.k = nsig > 1 ? ld4(k + kidx(gbase + i)) : make_float4(0.f, 0.f, 0.f, 0.f);
+              if constexpr (ACT) {  // the operator's inner gate; a line's points are contiguous
+                const size_t e = gbase + i;
+                const int64_t line = (int64_t)(e / per);
+                z.a = line_gates<true, TS>(ain, line, C).u4(z.a, z.b, (int64_t)(e - (size_t)line * per));
+                z.b = make_float4(1.f, 1.f, 1.f, 1.f);
+              }
             }
             return z;
           },
@@ -104,8 +110,12 @@ __global__ void __launch_bounds__(256)
           tid,
           [&](int i) {
             float2 z = czero();
-            if (i / LL < nrow)
-              z = make_float2(ld1(x1 + gbase + i) * ld1(v + gbase + i), nsig > 1 ? ld1(k + kidx(gbase + i)) : 0.f);
+            if (i / LL < nrow) {
+              const size_t e = gbase + i;
+              const int64_t line = (int64_t)(e / per);
+              const float u = line_gates<ACT, TS>(ain, line, C).u1(ld1(x1 + e), ld1(v + e), (int64_t)(e - (size_t)line * per));
+              z = make_float2(u, nsig > 1 ? ld1(k + kidx(e)) : 0.f);
+            }
             return z;
           },
           [&](int i, float2 z) {
@@ -355,7 +365,7 @@ struct RowsInvCfg {
   static constexpr int PPW = imax(1, imin(NT / T, (48 * 1024) / (PRP * 8)));  // pairs per workgroup
 };
 
-template <int PL, bool CIRC, typename TS>
+template <int PL, bool CIRC, typename TS, bool ACT = false>
 __global__ void __launch_bounds__(256)
     mp_rows_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0,
                 int nlines, int rows, int L1, int P1, int HS, int64_t per_line) {
@@ -431,7 +441,7 @@ __global__ void __launch_bounds__(256)
         tid,
         [&](int i4) {
           const int i = 4 * i4;
-          return (i / LL) < 2 * npair ? ld4(x2 + gbase + i) : make_float4(0.f, 0.f, 0.f, 0.f);
+          return (i / LL) < 2 * npair ? Gates<ACT>{}.g4(ld4(x2 + gbase + i)) : make_float4(0.f, 0.f, 0.f, 0.f);
         },
         [&](int i4, float4 g) {
           const int i = 4 * i4;
@@ -450,7 +460,7 @@ __global__ void __launch_bounds__(256)
     for (int i = tid; i < npair * 2 * LL; i += NT) {
       const int row = i / LL, n = i - row * LL;
       const float2 qv = reg[(row >> 1) * PRP + n];
-      st1(y + gbase + i, ld1(x2 + gbase + i) * ((row & 1) ? qv.y : qv.x));
+      st1(y + gbase + i, Gates<ACT>{}.g1(ld1(x2 + gbase + i)) * ((row & 1) ? qv.y : qv.x));
     }
   }
 }
@@ -476,14 +486,16 @@ hipError_t rows_fwd(const MpLaunch& L) {
   const FftConvArgs& a = *L.a;
   const int nsig = L.g.kc ? 1 : 2;  // a centered K has rows of its own (rows_kc)
 #define HY_ARGS(TS) (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, \
-                    L.g.HS, L.g.half, L.per, a.kC, nsig
+                    L.g.HS, L.g.half, L.per, a.kC, nsig, a.act_in, (int)a.C
+#define HY_LAUNCH(CI, TS)                                                                                     \
+  if (a.act) hipLaunchKernelGGL((mp_rows_fwd<PL, CI, TS, true>), grid, dim3(256), 0, L.s, HY_ARGS(TS)); \
+  else hipLaunchKernelGGL((mp_rows_fwd<PL, CI, TS, false>), grid, dim3(256), 0, L.s, HY_ARGS(TS));
   if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((mp_rows_fwd<PL, true, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((mp_rows_fwd<PL, false, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) { HY_LAUNCH(true, uint16_t) } else { HY_LAUNCH(false, uint16_t) }
   } else {
-    if (a.circular) hipLaunchKernelGGL((mp_rows_fwd<PL, true, float>), grid, dim3(256), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((mp_rows_fwd<PL, false, float>), grid, dim3(256), 0, L.s, HY_ARGS(float));
+    if (a.circular) { HY_LAUNCH(true, float) } else { HY_LAUNCH(false, float) }
   }
+#undef HY_LAUNCH
 #undef HY_ARGS
   return hipGetLastError();
 }
@@ -557,13 +569,15 @@ hipError_t rows_inv(const MpLaunch& L) {
   const dim3 grid((unsigned)((pairs + RowsInvCfg<PL>::PPW - 1) / RowsInvCfg<PL>::PPW));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, L.nl, L.g.rows, L.g.L1, L.g.P1, L.g.HS, L.per
+#define HY_LAUNCH(CI, TS)                                                                                     \
+  if (a.act) hipLaunchKernelGGL((mp_rows_inv<PL, CI, TS, true>), grid, dim3(256), 0, L.s, HY_ARGS(TS)); \
+  else hipLaunchKernelGGL((mp_rows_inv<PL, CI, TS, false>), grid, dim3(256), 0, L.s, HY_ARGS(TS));
   if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((mp_rows_inv<PL, true, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((mp_rows_inv<PL, false, uint16_t>), grid, dim3(256), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) { HY_LAUNCH(true, uint16_t) } else { HY_LAUNCH(false, uint16_t) }
   } else {
-    if (a.circular) hipLaunchKernelGGL((mp_rows_inv<PL, true, float>), grid, dim3(256), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((mp_rows_inv<PL, false, float>), grid, dim3(256), 0, L.s, HY_ARGS(float));
+    if (a.circular) { HY_LAUNCH(true, float) } else { HY_LAUNCH(false, float) }
   }
+#undef HY_LAUNCH
 #undef HY_ARGS
   return hipGetLastError();
 }

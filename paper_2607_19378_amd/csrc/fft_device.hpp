@@ -511,6 +511,76 @@ __device__ __forceinline__ int centered_index(int g, int L) {
   return g < L ? g + L - 1 : (g == L ? -1 : g - L - 1);
 }
 
+// ---------------------------------------------------------------------------
+// Inner and outer gates of one (b, c) line.  Plain call: u = x1 v and the
+// gate is x2.  HyenaND operator (ACT): x1, v and x2 hold the projections q,
+// kin and vin, u = q SiLU(kin) s[p] w_in[c] -- s[p] the l2 normalisation of
+// q and the RMSNorm across channels at grid point p, precomputed per sample
+// -- and the gate is Sigmoid(vin) (Eq. (HyenaND), section 3.2).
+// ---------------------------------------------------------------------------
+struct ActIn {
+  const float* s;    // [B, npos] normalisation scale per (sample, grid point)
+  const void* w_in;  // [C] RMSNorm weights, storage type
+  int64_t npos;      // grid points per line
+};
+
+// exp through the hardware exp2 (__expf): a few ulp, well inside fp32 parity
+__device__ __forceinline__ float silu_f(float x) { return x / (1.f + __expf(-x)); }
+__device__ __forceinline__ float sigmoid_f(float x) { return 1.f / (1.f + __expf(-x)); }
+
+template <bool ACT>
+struct Gates {
+  const float* s;  // this sample's row of s (ACT)
+  float w;         // w_in[c] (ACT)
+  // u at grid points p, p + 1 (p even) / p .. p + 3 (p a multiple of 4) / p
+  __device__ __forceinline__ float2 u2(float2 a, float2 b, int64_t p) const {
+    if constexpr (ACT) {
+      const float2 sc = *reinterpret_cast<const float2*>(s + p);
+      return make_float2(a.x * silu_f(b.x) * (sc.x * w), a.y * silu_f(b.y) * (sc.y * w));
+    } else {
+      return make_float2(a.x * b.x, a.y * b.y);
+    }
+  }
+  __device__ __forceinline__ float4 u4(float4 a, float4 b, int64_t p) const {
+    if constexpr (ACT) {
+      const float4 sc = *reinterpret_cast<const float4*>(s + p);
+      return make_float4(a.x * silu_f(b.x) * (sc.x * w), a.y * silu_f(b.y) * (sc.y * w),
+                         a.z * silu_f(b.z) * (sc.z * w), a.w * silu_f(b.w) * (sc.w * w));
+    } else {
+      return make_float4(a.x * b.x, a.y * b.y, a.z * b.z, a.w * b.w);
+    }
+  }
+  __device__ __forceinline__ float u1(float a, float b, int64_t p) const {
+    if constexpr (ACT) return a * silu_f(b) * (s[p] * w);
+    else return a * b;
+  }
+  __device__ __forceinline__ float2 g2(float2 x) const {
+    if constexpr (ACT) return make_float2(sigmoid_f(x.x), sigmoid_f(x.y));
+    else return x;
+  }
+  __device__ __forceinline__ float4 g4(float4 x) const {
+    if constexpr (ACT) return make_float4(sigmoid_f(x.x), sigmoid_f(x.y), sigmoid_f(x.z), sigmoid_f(x.w));
+    else return x;
+  }
+  __device__ __forceinline__ float g1(float x) const {
+    if constexpr (ACT) return sigmoid_f(x);
+    else return x;
+  }
+};
+
+template <bool ACT, typename TS>
+__device__ __forceinline__ Gates<ACT> line_gates(const ActIn& act, int64_t line, int C) {
+  Gates<ACT> g;
+  if constexpr (ACT) {
+    g.s = act.s + (line / C) * act.npos;
+    g.w = ld1(reinterpret_cast<const TS*>(act.w_in) + line % C);
+  } else {
+    g.s = nullptr;
+    g.w = 1.f;
+  }
+  return g;
+}
+
 // Spectral product with the shortcut folded in: U (K + D), D times the
 // transform of a unit impulse (1 at every bin).  Inputs are 2U and 2K.
 __device__ __forceinline__ float2 gated_product(float2 U2, float2 K2, float twoD) {

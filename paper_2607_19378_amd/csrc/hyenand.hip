@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <cmath>
 #include <mutex>
 #include <string>
 
@@ -342,6 +343,24 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_
 
 namespace {
 
+// Every step of the path for a validated call: the plan's kernels, chunked
+// over side streams for the multi-pass plans.
+hipError_t launch_plan(const FftConvArgs& a, Plan p, size_t per, hipStream_t s) {
+  switch (p) {
+    case PLAN_FUSED1D: return launch_fused1d(a, s);
+    case PLAN_FUSED2D: return launch_fused2d(a, s);
+    case PLAN_MULTIPASS:
+      return run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
+        return launch_multipass(a, l0, nl, ws, st);
+      });
+    case PLAN_FOURSTEP:
+      return run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
+        return launch_fourstep(a, l0, nl, ws, st);
+      });
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hyenand_status forward(const void* x1, const void* x2, const void* v, const void* k, const void* D, void* y,
                        int ndim, const int64_t* dims, int pad_mode, int dtype, void* workspace,
                        size_t workspace_bytes, void* stream, bool shared_k) {
@@ -391,23 +410,75 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   a.x1 = x1; a.x2 = x2; a.v = v; a.k = k; a.D = D; a.y = y;
   a.ws = workspace;
   a.ws_bytes = workspace_bytes;
-  hipStream_t s = (hipStream_t)stream;
-  hipError_t err = hipSuccess;
-  switch (p) {
-    case PLAN_FUSED1D: err = launch_fused1d(a, s); break;
-    case PLAN_FUSED2D: err = launch_fused2d(a, s); break;
-    case PLAN_MULTIPASS:
-      err = run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
-        return launch_multipass(a, l0, nl, ws, st);
-      });
-      break;
-    case PLAN_FOURSTEP:
-      err = run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
-        return launch_fourstep(a, l0, nl, ws, st);
-      });
-      break;
-    default: return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  const hipError_t err = launch_plan(a, p, per, (hipStream_t)stream);
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
+}
+
+// HyenaND operator: prologue scale s (B * npos floats, first in the
+// workspace, 256-byte block), the plan's kernels with the operator's gates,
+// the output RMSNorm in place.
+size_t op_scale_bytes(const FftConvArgs& a) {
+  int64_t npos = 1;
+  for (int d = 0; d < a.ndim; ++d) npos *= a.L[d];
+  return ((size_t)(a.lines / a.C) * (size_t)npos * sizeof(float) + 255) / 256 * 256;
+}
+
+hyenand_status operator_fwd(const void* q, const void* kin, const void* vin, const void* k, const void* D,
+                            const void* w_in, const void* w_out, float eps_l2, float eps_rms, void* y, int ndim,
+                            const int64_t* dims, int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  g_last_error.clear();
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const void* ptrs[8] = {q, kin, vin, k, D, w_in, w_out, y};
+  const char* pn[8] = {"q", "kin", "vin", "k", "D", "w_in", "w_out", "y"};
+  for (int i = 0; i < 8; ++i)
+    if (!ptrs[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", pn[i]);
+  const size_t es = a.bf16 ? 2 : 4;
+  for (int i = 0; i < 8; ++i) {
+    const bool vec = i < 4 || i == 7;
+    if ((uintptr_t)ptrs[i] % (vec ? 16 : es) != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not aligned", pn[i]);
   }
+  if (!(eps_l2 >= 0.f) || !(eps_rms >= 0.f) || !std::isfinite(eps_l2) || !std::isfinite(eps_rms))
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "eps_l2 and eps_rms must be finite and >= 0");
+  if (a.C > (int64_t(1) << 30) || op_rmsnorm_points((int)a.C) < 1)
+    return fail(HYENAND_ERR_UNSUPPORTED, "C = %lld channels exceed the output norm's tile", (long long)a.C);
+  size_t n = (size_t)a.lines;
+  for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];
+  const size_t nb = n * es;
+  size_t kpts = 1;
+  for (int d = 0; d < a.ndim; ++d) kpts *= (size_t)(a.centered ? 2 * a.L[d] - 1 : a.L[d]);
+  const size_t bytes[8] = {nb, nb, nb, (size_t)a.lines * kpts * es, (size_t)a.C * es, (size_t)a.C * es,
+                           (size_t)a.C * es, nb};
+  for (int i = 0; i < 7; ++i)
+    if (overlaps(y, nb, ptrs[i], bytes[i])) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", pn[i]);
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  const size_t sb = op_scale_bytes(a);
+  const size_t per = bytes_per_line(a, p);
+  if (!workspace || workspace_bytes < sb + per)
+    return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "the operator needs at least %zu workspace bytes, got %zu", sb + per,
+                workspace ? workspace_bytes : (size_t)0);
+  if ((uintptr_t)workspace % 16 != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace is not 16-byte aligned");
+  for (int i = 0; i < 8; ++i)
+    if (overlaps(workspace, workspace_bytes, ptrs[i], bytes[i]))
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", pn[i]);
+  const int64_t npos = (int64_t)(n / (size_t)a.lines);
+  const int64_t B = a.lines / a.C;
+  float* sc = (float*)workspace;
+  a.x1 = q; a.v = kin; a.x2 = vin; a.k = k; a.D = D; a.y = y;
+  a.ws = (char*)workspace + sb;
+  a.ws_bytes = workspace_bytes - sb;
+  a.act = true;
+  a.act_in.s = sc;
+  a.act_in.w_in = w_in;
+  a.act_in.npos = npos;
+  const hipStream_t s = (hipStream_t)stream;
+  hipError_t err = launch_op_prologue(q, kin, sc, B, (int)a.C, npos, a.bf16, eps_l2, eps_rms, s);
+  if (err == hipSuccess) err = launch_plan(a, p, per, s);
+  if (err == hipSuccess) err = launch_op_rmsnorm(y, w_out, B, (int)a.C, npos, a.bf16, eps_rms, s);
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
   return HYENAND_OK;
 }
@@ -544,6 +615,26 @@ const char* hyenand_status_string(int status) {
 }
 
 const char* hyenand_last_error(void) { return g_last_error.c_str(); }
+
+hyenand_status hyenand_operator(const void* q, const void* kin, const void* vin, const void* k, const void* D,
+                                const void* w_in, const void* w_out, float eps_l2, float eps_rms, void* y, int ndim,
+                                const int64_t* dims, int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  return operator_fwd(q, kin, vin, k, D, w_in, w_out, eps_l2, eps_rms, y, ndim, dims, pad_mode, dtype, workspace,
+                      workspace_bytes, stream);
+}
+
+hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                               size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  *bytes_out = op_scale_bytes(a) + recommended_ws(a, p);
+  return HYENAND_OK;
+}
 
 int hyenand_version(void) { return 200; }
 

@@ -24,6 +24,8 @@ struct FftConvArgs {
   int kC;         // 0: k is [B, C, L...]; C: one kernel per channel, k is [C, L...]
   void* ws;       // device workspace (multi-pass plans)
   size_t ws_bytes;
+  bool act;       // HyenaND operator: x1, v, x2 are q, kin, vin (see Gates)
+  ActIn act_in;
 };
 
 // single pass (the padded problem of one line fits in LDS)
@@ -67,5 +69,14 @@ hipError_t launch_backward_reduce(const FftConvBwdArgs& b, int64_t partials_per_
 bool fourstep_supported(const FftConvArgs& a);
 size_t fourstep_bytes_per_line(const FftConvArgs& a);
 hipError_t launch_fourstep(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s);
+
+// HyenaND operator: the normalisations across channels (op_norm.hip).
+// op_rmsnorm_points: grid points per rmsnorm workgroup for C channels (0 if C
+// is too large for the LDS tile).
+int op_rmsnorm_points(int C);
+hipError_t launch_op_prologue(const void* q, const void* kin, float* s, int64_t B, int C, int64_t npos, bool bf16,
+                              float eps_l2, float eps_rms, hipStream_t st);
+hipError_t launch_op_rmsnorm(void* y, const void* w_out, int64_t B, int C, int64_t npos, bool bf16, float eps_rms,
+                             hipStream_t st);
 
 }  // namespace hyenand

@@ -22,7 +22,8 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_workspace_size",
             "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
-            "hyenand_fftconv_backward_workspace_min", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
+            "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
+            "hyenand_status_string", "hyenand_last_error", "hyenand_version")
 
 _lock = threading.Lock()
 _lib = None
@@ -63,6 +64,12 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv_backward_workspace_min.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                                  ctypes.POINTER(ctypes.c_size_t)]
             L.hyenand_fftconv_backward_workspace_min.restype = ctypes.c_int
+            L.hyenand_operator.argtypes = [vp] * 7 + [ctypes.c_float, ctypes.c_float, vp, ctypes.c_int, i64p,
+                                                      ctypes.c_int, ctypes.c_int, vp, ctypes.c_size_t, vp]
+            L.hyenand_operator.restype = ctypes.c_int
+            L.hyenand_operator_workspace_size.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
+                                                          ctypes.POINTER(ctypes.c_size_t)]
+            L.hyenand_operator_workspace_size.restype = ctypes.c_int
             L.hyenand_fftconv_plan_name.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_char_p, ctypes.c_size_t]
             L.hyenand_fftconv_plan_name.restype = ctypes.c_int
@@ -265,3 +272,54 @@ def backward(x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None, stre
     gD = torch.empty_like(D)
     backward_into(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode, workspace, stream)
     return gx1, gx2, gv, gk, gD
+
+
+def operator_workspace_size(shape, pad_mode: str, dtype) -> int:
+    nd, dims = _dims(shape)
+    out = ctypes.c_size_t(0)
+    _check(lib().hyenand_operator_workspace_size(nd, dims, _mode(pad_mode), _dtype_code(dtype), ctypes.byref(out)))
+    return int(out.value)
+
+
+class PreparedOperator:
+    """One hyenand_operator call with its arguments checked and marshalled
+    once (see Prepared)."""
+
+    def __init__(self, y, q, kin, vin, k, D, w_in, w_out, eps_l2: float = 1e-6, eps_rms: float = 1e-6,
+                 pad_mode: str = "linear", workspace=None, stream=None):
+        import torch
+        shape = tuple(q.shape)
+        for t, want in ((q, shape), (kin, shape), (vin, shape), (y, shape),
+                        (k, kernel_shape(shape, pad_mode))):
+            if not t.is_cuda or tuple(t.shape) != want or t.dtype != q.dtype or not t.is_contiguous():
+                raise ValueError("q, kin, vin, y must be contiguous GPU tensors of one shape and dtype; "
+                                 f"k must be {kernel_shape(shape, pad_mode)}")
+        for t in (D, w_in, w_out):
+            if not t.is_cuda or t.dtype != q.dtype or tuple(t.shape) != (shape[1],) or not t.is_contiguous():
+                raise ValueError("D, w_in and w_out must be contiguous [C] GPU tensors of the same dtype")
+        if workspace is None:
+            workspace = torch.empty(operator_workspace_size(shape, pad_mode, q.dtype), dtype=torch.uint8,
+                                    device=q.device)
+        nd, dims = _dims(shape)
+        if stream is None:
+            stream = torch.cuda.current_stream(q.device)
+        self._fn = lib().hyenand_operator
+        self._args = (_ptr(q), _ptr(kin), _ptr(vin), _ptr(k), _ptr(D), _ptr(w_in), _ptr(w_out), float(eps_l2),
+                      float(eps_rms), _ptr(y), nd, dims, _mode(pad_mode), _dtype_code(q.dtype), _ptr(workspace),
+                      workspace.numel() * workspace.element_size(), ctypes.c_void_p(stream.cuda_stream))
+        self._keep = (y, q, kin, vin, k, D, w_in, w_out, workspace, stream)
+
+    def __call__(self) -> None:
+        status = self._fn(*self._args)
+        if status != OK:
+            _check(status)
+
+
+def operator(q, kin, vin, k, D, w_in, w_out, eps_l2: float = 1e-6, eps_rms: float = 1e-6,
+             pad_mode: str = "linear", workspace=None, stream=None):
+    """The HyenaND operator, Eq. (HyenaND): RMSNorm(Sigmoid(vin) * (k conv
+    RMSNorm(l2(q) * SiLU(kin)) + D * .)) with torch-allocated y."""
+    import torch
+    y = torch.empty_like(q)
+    PreparedOperator(y, q, kin, vin, k, D, w_in, w_out, eps_l2, eps_rms, pad_mode, workspace, stream)()
+    return y

@@ -178,6 +178,47 @@ def test_centered_kernel_overlap_uses_double_grid(L):
     assert b"pad_mode" in L.hyenand_last_error()
 
 
+def ocall(L, shape, mode=0, dtype=0, ptrs=None, eps=(1e-6, 1e-6), ws=FAKE + (40 << 36), ws_bytes=1 << 20):
+    nd = len(shape) - 2
+    dims = (ctypes.c_int64 * len(shape))(*shape)
+    p = ptrs or [FAKE + i * (1 << 36) for i in range(8)]
+    a = [ctypes.c_void_p(x) for x in p]
+    return L.hyenand_operator(*a[:7], ctypes.c_float(eps[0]), ctypes.c_float(eps[1]), a[7], nd, dims, mode, dtype,
+                              ctypes.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+def test_operator_validation(L):
+    """hyenand_operator rejects bad arguments before launching anything (every
+    call here stops at validation)."""
+    p = [FAKE + i * (1 << 36) for i in range(8)]
+    for i in range(8):
+        q = list(p)
+        q[i] = 0
+        assert ocall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+        assert b"is NULL" in L.hyenand_last_error()
+    assert ocall(L, (2, 3, 16), eps=(-1.0, 1e-6)) == H.ERR_INVALID_ARGUMENT
+    assert ocall(L, (2, 3, 16), eps=(1e-6, float("nan"))) == H.ERR_INVALID_ARGUMENT
+    q = list(p)
+    q[7] = p[2] + 32  # y inside vin
+    assert ocall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+    assert b"y overlaps vin" in L.hyenand_last_error()
+    q = list(p)
+    q[5] = p[5] + 2  # w_in not aligned to a float
+    assert ocall(L, (2, 3, 16), ptrs=q) == H.ERR_INVALID_ARGUMENT
+    assert ocall(L, (2, 3, 16), ws=None, ws_bytes=0) == H.ERR_WORKSPACE_TOO_SMALL
+    assert ocall(L, (2, 3, 16), ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL  # 2 x 16 scales need 256 bytes
+    assert ocall(L, (1, 1 << 15, 2)) == H.ERR_UNSUPPORTED  # more channels than the output norm's tile
+    assert ocall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED
+
+
+def test_operator_workspace_size(L):
+    # scales [B, prod L] floats in a 256-byte block, then the convolution's workspace
+    assert H.operator_workspace_size((8, 256, 64, 64), "linear", "f32") == 8 * 64 * 64 * 4
+    assert H.operator_workspace_size((1, 3, 256, 256), "linear", "f32") == (
+        256 * 256 * 4 + H.workspace_size((1, 3, 256, 256), "linear", "f32"))
+    assert H.operator_workspace_size((2, 2, 4), "circular", "bf16") == 256
+
+
 def test_shared_kernel_validation(L):
     """hyenand_fftconv_shared_k takes k as [C, L...]: y inside that smaller
     region still overlaps k; null pointers are rejected."""
