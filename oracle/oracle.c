@@ -118,13 +118,24 @@ static int make_geom(int ndim, const int64_t *dims, geom *g) {
 
 enum { MODE_LINEAR = 0, MODE_CIRCULAR = 1, MODE_CENTERED = 2 };
 
-/* Transform extents: 2 L_d on the real axes in linear and centered mode, L_d
- * in circular mode; the virtual leading axes of a 1D/2D problem stay at
- * extent 1. */
+/* Transform extents: in linear and centered mode the smallest power of two
+ * >= 2 L_d - 1 on the real axes (2 L_d when L_d is a power of two; any length
+ * >= 2 L_d - 1 holds every displacement between two grid points without
+ * wrap-around), L_d in circular mode; the virtual leading axes of a 1D/2D
+ * problem stay at extent 1. */
+static int64_t pow2_at_least(int64_t n) {
+    int64_t p = 1;
+    while (p < n) p *= 2;
+    return p;
+}
+
 static void transform_extents(const geom *g, int mode, int64_t P[3]) {
     for (int d = 0; d < 3; ++d) {
         int real_axis = d >= 3 - g->ndim;
-        P[d] = (real_axis && mode != MODE_CIRCULAR) ? 2 * g->L[d] : g->L[d];
+        if (real_axis && mode != MODE_CIRCULAR)
+            P[d] = g->L[d] > 1 ? pow2_at_least(2 * g->L[d] - 1) : 2;
+        else
+            P[d] = g->L[d];
     }
 }
 
@@ -460,8 +471,9 @@ int oracle_fft(const double *x1, const double *x2, const double *v, const double
     geom g;
     if (!x1 || !x2 || !v || !k || !D || !y || make_geom(ndim, dims, &g)) return 1;
     if (circular < 0 || circular > 2) return 1;
-    for (int d = 0; d < 3; ++d)
-        if (!is_pow2(g.L[d])) return 1;
+    if (circular == MODE_CIRCULAR)
+        for (int d = 0; d < 3; ++d)
+            if (!is_pow2(g.L[d])) return 1;
     int64_t P[3];
     transform_extents(&g, circular, P);
     cplx *twf[3] = {NULL, NULL, NULL}, *twi[3] = {NULL, NULL, NULL};
@@ -701,7 +713,7 @@ static int backward_common(const double *x1, const double *x2, const double *v, 
         make_geom(ndim, dims, &g))
         return 1;
     if (circular != MODE_LINEAR && circular != MODE_CIRCULAR) return 1;
-    if (use_fft)
+    if (use_fft && circular == MODE_CIRCULAR)
         for (int d = 0; d < 3; ++d)
             if (!is_pow2(g.L[d])) return 1;
     double *hu = (double *)calloc((size_t)(g.B * g.C), sizeof(double));
