@@ -69,7 +69,7 @@ __global__ void __launch_bounds__(512)
       w[e] = czero();
       if (act) {
         const int g = 2 * (m1 * N2 + c0 + cc);
-        const int ja = centered_index(g, Li), jb = centered_index(g + 1, Li);
+        const int ja = centered_index(g, Li, 2 * Li), jb = centered_index(g + 1, Li, 2 * Li);
         w[e] = make_float2(ja >= 0 ? ld1(kl + ja) : 0.f, jb >= 0 ? ld1(kl + jb) : 0.f);
       }
     }

@@ -84,7 +84,7 @@ __global__ void __launch_bounds__(fused1d_nt(P))
     batched_copy<M, NT, 8>(
         tid,
         [&](int m) {
-          const int j0 = centered_index(2 * m, L), j1 = centered_index(2 * m + 1, L);
+          const int j0 = centered_index(2 * m, L, P), j1 = centered_index(2 * m + 1, L, P);
           return make_float2(j0 >= 0 ? ld1(kl + j0) : 0.f, j1 >= 0 ? ld1(kl + j1) : 0.f);
         },
         [&](int m, float2 z) { Kb[m + (m >> 4)] = z; });
@@ -564,8 +564,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       tid,
       [&](int i) {
         const int g0 = i / M1, m = i - g0 * M1;
-        const int j0 = centered_index(g0, L0);
-        const int ja = centered_index(2 * m, L1), jb = centered_index(2 * m + 1, L1);
+        const int j0 = centered_index(g0, L0, P0);
+        const int ja = centered_index(2 * m, L1, P1), jb = centered_index(2 * m + 1, L1, P1);
         const TS* kr = kl + (size_t)(j0 >= 0 ? j0 : 0) * (2 * L1 - 1);
         return make_float2((j0 >= 0 && ja >= 0) ? ld1(kr + ja) * scale : 0.f,
                            (j0 >= 0 && jb >= 0) ? ld1(kr + jb) * scale : 0.f);

@@ -222,10 +222,10 @@ __global__ void __launch_bounds__(256)
           const int64_t gr = row0 + r;
           const int64_t line = gr / krows;
           const int rr = (int)(gr - line * krows);
-          const int j0 = centered_index(rr / P1, L0), j1 = centered_index(rr % P1, L1);
+          const int j0 = centered_index(rr / P1, L0, 2 * L0), j1 = centered_index(rr % P1, L1, 2 * L1);
           if (j0 >= 0 && j1 >= 0) {
             const TS* kr = k + (size_t)k_line(line0 + line, kC) * kpts + ((size_t)j0 * K1 + j1) * K2;
-            const int ja = centered_index(2 * m, LL), jb = centered_index(2 * m + 1, LL);
+            const int ja = centered_index(2 * m, LL, PL), jb = centered_index(2 * m + 1, LL, PL);
             z = make_float2(ja >= 0 ? ld1(kr + ja) : 0.f, jb >= 0 ? ld1(kr + jb) : 0.f);
           }
         }

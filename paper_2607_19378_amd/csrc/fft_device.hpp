@@ -504,11 +504,11 @@ __device__ __forceinline__ float2 c2r_pair(float2 Yg, float2 Ymg, float2 w) {
 }
 
 // Centered kernels (pad mode "centered"): 2L - 1 points per axis, index
-// L - 1 the zero displacement, transformed on the grid of 2L points.  Grid
-// index g holds displacement g (g < L) or g - 2L (g > L); g = L holds no
-// displacement of the L grid and stays zero (-1).
-__device__ __forceinline__ int centered_index(int g, int L) {
-  return g < L ? g + L - 1 : (g == L ? -1 : g - L - 1);
+// L - 1 the zero displacement, transformed on a grid of P >= 2L points.  Grid
+// index g holds displacement g (g < L) or g - P (g > P - L); the indices in
+// between hold no displacement of the L grid and stay zero (-1).
+__device__ __forceinline__ int centered_index(int g, int L, int P) {
+  return g < L ? g + L - 1 : (g > P - L ? g - P + L - 1 : -1);
 }
 
 // ---------------------------------------------------------------------------

@@ -29,7 +29,7 @@ hyenand_status fail(hyenand_status s, const char* fmt, ...) {
   return s;
 }
 
-enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP };
+enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP, PLAN_FUSED_RL };
 
 const char* plan_name(Plan p, int ndim) {
   switch (p) {
@@ -37,6 +37,7 @@ const char* plan_name(Plan p, int ndim) {
     case PLAN_FUSED2D: return "fused2d";
     case PLAN_MULTIPASS: return ndim == 3 ? "multipass3d" : "multipass2d";
     case PLAN_FOURSTEP: return "fourstep1d";
+    case PLAN_FUSED_RL: return ndim == 1 ? "fused1d_any" : "fused2d_any";
     default: return "none";
   }
 }
@@ -70,7 +71,13 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   int nd = 0;
   for (int d = 0; d < ndim; ++d) {
     const int64_t L = dims[2 + d];
-    if (!pow2(L)) return fail(HYENAND_ERR_UNSUPPORTED, "grid extent L%d = %lld is not a power of two", d + 1, (long long)L);
+    if (!pow2(L)) {
+      if (a->circular)
+        return fail(HYENAND_ERR_UNSUPPORTED, "circular grid extent L%d = %lld is not a power of two", d + 1,
+                    (long long)L);
+      if (L > (int64_t(1) << 24)) return fail(HYENAND_ERR_UNSUPPORTED, "grid extent too large");
+      a->rl = true;
+    }
     if (L > 1) a->L[nd++] = L;
   }
   if (nd == 0) {  // a single point: the linear transform of length 2 covers it
@@ -80,11 +87,17 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
     a->centered = false;
   }
   a->ndim = nd;
-  for (int d = 0; d < nd; ++d) a->P[d] = a->circular ? a->L[d] : 2 * a->L[d];
+  for (int d = 0; d < nd; ++d) {
+    // non-circular: the smallest power of two >= 2L - 1 (2L for a power of two)
+    int64_t p = 2;
+    while (p < 2 * a->L[d] - 1) p *= 2;
+    a->P[d] = a->circular ? a->L[d] : p;
+  }
   return HYENAND_OK;
 }
 
 Plan choose_plan(const FftConvArgs& a) {
+  if (a.rl) return fused_rl_supported(a) ? PLAN_FUSED_RL : PLAN_NONE;
   const char* force = getenv("HYENAND_PLAN");
   const bool no_fused = force && (strcmp(force, "multipass") == 0 || strcmp(force, "fourstep") == 0);
   if (a.ndim == 1) {
@@ -256,7 +269,7 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
 enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP };
 
 BwdPlan choose_bwd_plan(const FftConvArgs& a) {
-  if (a.centered) return BWD_NONE;  // the backward takes the linear and circular modes
+  if (a.centered || a.rl) return BWD_NONE;  // linear and circular modes, power-of-two extents
   if (fused_backward_supported(a)) return BWD_FUSED;
   if ((a.ndim == 2 || a.ndim == 3) && multipass_supported(a)) return BWD_MULTIPASS;
   if (a.ndim == 1 && backward_fs_supported(a)) return BWD_FOURSTEP;
@@ -357,6 +370,7 @@ hipError_t launch_plan(const FftConvArgs& a, Plan p, size_t per, hipStream_t s) 
       return run_chunked(a, per, s, [&a](int64_t l0, int64_t nl, void* ws, hipStream_t st) {
         return launch_fourstep(a, l0, nl, ws, st);
       });
+    case PLAN_FUSED_RL: return launch_fused_rl(a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -20,6 +20,7 @@ struct FftConvArgs {
   int64_t P[3];   // transform extents: 2L (linear) or L (circular)
   bool circular;
   bool centered;  // linear transform grid, k on the double grid of 2 L_d - 1 points per axis
+  bool rl;        // some L_d is not a power of two (linear or centered; P_d = pow2 >= 2 L_d - 1)
   bool bf16;
   int kC;         // 0: k is [B, C, L...]; C: one kernel per channel, k is [C, L...]
   void* ws;       // device workspace (multi-pass plans)
@@ -33,6 +34,11 @@ bool fused1d_supported(int64_t P);
 hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s);
 bool fused2d_supported(int64_t P0, int64_t P1);
 hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s);
+
+// single pass for grid extents that are not powers of two (linear and
+// centered modes, transform P_d = the smallest power of two >= 2 L_d - 1)
+bool fused_rl_supported(const FftConvArgs& a);
+hipError_t launch_fused_rl(const FftConvArgs& a, hipStream_t s);
 
 // multi-pass 2D/3D (lines along each axis; spectra staged in the workspace).
 // One call runs every pass over lines [line0, line0 + nl) with their spectra

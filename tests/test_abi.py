@@ -61,8 +61,10 @@ def test_invalid_arguments(L):
     assert call(L, (1, 0, 16)) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), mode=3) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), dtype=5) == H.ERR_INVALID_ARGUMENT
-    assert call(L, (1, 1, 12)) == H.ERR_UNSUPPORTED  # not a power of two
+    assert call(L, (1, 1, 12), mode=1) == H.ERR_UNSUPPORTED  # circular: not a power of two
     assert b"power of two" in L.hyenand_last_error()
+    assert call(L, (1, 1, 300, 300)) == H.ERR_UNSUPPORTED  # 512 x 512 transform beyond the single pass
+    assert b"no plan" in L.hyenand_last_error()
 
 
 def test_aliasing_rejected(L):
@@ -92,8 +94,16 @@ def test_workspace_queries_are_host_only():
     assert H.plan_name((2, 2, 1, 64), "linear", "bf16") == "fused1d"      # unit axis squeezed
     assert H.plan_name((2, 2, 1, 1, 1), "circular", "f32") == "fused1d"  # single point
     with pytest.raises(H.HyenandError) as e:
-        H.workspace_size((1, 1, 3), "linear", "f32")
+        H.workspace_size((1, 1, 3), "circular", "f32")
     assert e.value.status == H.ERR_UNSUPPORTED
+    # other extents in the non-circular modes: transforms on the smallest power
+    # of two >= 2L - 1, single pass
+    assert H.plan_name((1, 1, 3), "linear", "f32") == "fused1d_any"
+    assert H.plan_name((2, 4, 14, 14), "centered", "f32") == "fused2d_any"
+    assert H.plan_name((2, 4, 14, 16), "linear", "bf16") == "fused2d_any"
+    assert H.workspace_size((2, 4, 14, 14), "linear", "f32") == 0
+    with pytest.raises(H.HyenandError):
+        H.plan_name((1, 1, 100, 100), "linear", "f32")  # 256 x 256: beyond the single pass
 
 
 def bcall(L, shape, mode=0, dtype=0, ptrs=None, ws=FAKE + (40 << 36), ws_bytes=1 << 20):
@@ -124,7 +134,7 @@ def test_backward_validation(L):
     assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 1 << 22)) == H.ERR_UNSUPPORTED       # 2^23 transform points
     assert bcall(L, (1, 2, 2048, 4)) == H.ERR_UNSUPPORTED       # 4096 points on an axis of a 2D grid
-    assert bcall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED            # not a power of two
+    assert bcall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED            # no backward for other extents
     # multi-pass plans: the gD sums plus one line of three spectra at least
     assert bcall(L, (1, 2, 1 << 20)) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 128, 128), mode=1, ws_bytes=4096) == H.ERR_WORKSPACE_TOO_SMALL
@@ -208,7 +218,7 @@ def test_operator_validation(L):
     assert ocall(L, (2, 3, 16), ws=None, ws_bytes=0) == H.ERR_WORKSPACE_TOO_SMALL
     assert ocall(L, (2, 3, 16), ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL  # 2 x 16 scales need 256 bytes
     assert ocall(L, (1, 1 << 15, 2)) == H.ERR_UNSUPPORTED  # more channels than the output norm's tile
-    assert ocall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED
+    assert ocall(L, (1, 2, 12), mode=1) == H.ERR_UNSUPPORTED  # circular, not a power of two
 
 
 def test_operator_workspace_size(L):

@@ -1,0 +1,95 @@
+"""Grid extents that are not powers of two (linear and centered modes): the
+single-pass kernels transform on the smallest power of two >= 2L - 1 and crop
+L points; parity with the fp64 oracle (which takes any extent) on 1D and 2D
+grids, fp32 and bf16, one kernel per channel and the HyenaND operator."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_19378_amd import workloads as W
+
+from gpu_util import TOL, from_device, log, rel_l2, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _case(B, C, grid, mode, dtype, seed, shared=False):
+    rng = np.random.default_rng(seed)
+    shape = (B, C) + tuple(grid)
+    x1, x2, v = (W.quantise(rng.standard_normal(shape), dtype) for _ in range(3))
+    kshape = oracle.kernel_shape(shape, mode)
+    if shared:
+        kshape = kshape[1:]
+    k = W.quantise(rng.standard_normal(kshape) / np.sqrt(np.prod(kshape[-len(grid):])), dtype)
+    D = W.quantise(rng.standard_normal(C), dtype)
+    return shape, x1, x2, v, k, D
+
+
+def _check(tag, B, C, grid, mode, dtype, seed, shared=False):
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    shape, x1, x2, v, k, D = _case(B, C, grid, mode, dtype, seed, shared)
+    plan = H.plan_name(shape, mode, dtype)
+    dev = [to_device(a, dtype) for a in (x1, x2, v, k, D)]
+    y = H.fftconv(*dev, pad_mode=mode, shared_k=shared)
+    torch.cuda.synchronize()
+    got = from_device(y)
+    f = [W.storage_to_f64(a, dtype) for a in (x1, x2, v, k, D)]
+    if shared:
+        f[3] = np.broadcast_to(f[3][None], (B,) + f[3].shape)
+    ref = oracle.conv_fft(*f, mode)
+    err = rel_l2(got, ref)
+    log(f"[any] {tag} {shape} {mode} {dtype} plan={plan}: rel_l2={err:.3e}")
+    assert np.all(np.isfinite(got)) and err <= TOL[dtype]
+    return plan
+
+
+@pytest.mark.parametrize("mode", ["linear", "centered"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("L", [3, 5, 7, 12, 100, 1000, 3000, 8191])
+def test_1d(L, mode, dtype):
+    assert _check("1d", 2, 3, (L,), mode, dtype, L) == "fused1d_any"
+
+
+@pytest.mark.parametrize("mode", ["linear", "centered"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("grid", [(3, 5), (14, 14), (7, 30), (50, 60), (64, 33), (33, 64), (2, 3), (24, 40)])
+def test_2d(grid, mode, dtype):
+    assert _check("2d", 2, 3, grid, mode, dtype, sum(grid)) == "fused2d_any"
+
+
+@pytest.mark.parametrize("grid", [(100,), (14, 14)])
+def test_shared_kernel(grid):
+    _check("shared", 3, 2, grid, "centered", "f32", 7, shared=True)
+
+
+def test_image_patch_grid_batch():
+    """A batch of 14 x 14 patch grids (the paper's ImageNet models' grid) with
+    centered kernels: 16 x 384 lines."""
+    _check("patches", 16, 384, (14, 14), "centered", "f32", 11)
+
+
+@pytest.mark.parametrize("grid,mode", [((14, 14), "centered"), ((300,), "linear")])
+def test_operator(grid, mode):
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    rng = np.random.default_rng(5)
+    shape = (2, 6) + grid
+    q, kin, vin = (rng.standard_normal(shape).astype(np.float32) for _ in range(3))
+    kshape = oracle.kernel_shape(shape, mode)
+    k = (rng.standard_normal(kshape) / np.sqrt(np.prod(kshape[2:]))).astype(np.float32)
+    D, wi, wo = (rng.standard_normal(6).astype(np.float32) for _ in range(3))
+    dev = [to_device(a, "f32") for a in (q, kin, vin, k, D, wi, wo)]
+    y = H.operator(*dev, pad_mode=mode)
+    torch.cuda.synchronize()
+    ref = oracle.operator(*[a.astype(np.float64) for a in (q, kin, vin, k, D, wi, wo)], pad_mode=mode)
+    err = rel_l2(from_device(y), ref)
+    log(f"[any] operator {shape} {mode}: rel_l2={err:.3e}")
+    assert err <= TOL["f32"]
