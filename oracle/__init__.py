@@ -16,6 +16,9 @@ The arithmetic lives in ``oracle.c`` (plain C, IEEE double):
 * :func:`operator` evaluates the whole HyenaND operator of Eq. (HyenaND):
   l2-normalised q times SiLU(kin), RMSNorm across channels, the gated long
   convolution with Sigmoid(vin), RMSNorm across channels;
+* :func:`kernel_synth` evaluates the implicit, input-dependent kernel K(x) of
+  sections 3.2.1-3.2.2 (a SIREN over the grid coordinates, FiLM-modulated per
+  sample, times a per-channel window) on a convolution's kernel grid;
 * :func:`backward_direct` / :func:`backward_fft` give the gradients of a
   scalar loss through y (gx1, gx2, gv, gk, gD for a given gy = dLoss/dy), as
   explicit sums and through the FFT.
@@ -76,8 +79,11 @@ def lib():
             L.oracle_backward_fft.argtypes = bsig
             L.oracle_operator.argtypes = [_f64p] * 7 + [ctypes.c_double, ctypes.c_double, _f64p, ctypes.c_int,
                                                         _i64p, ctypes.c_int, ctypes.c_int]
+            L.oracle_kernel_synth.argtypes = [_f64p] * 8 + [ctypes.c_int, _f64p, ctypes.c_int, _i64p,
+                                                            ctypes.c_int, ctypes.c_int, ctypes.c_int]
             for f in (L.oracle_direct, L.oracle_fft, L.oracle_direct_points, L.oracle_fft1d,
-                      L.oracle_backward_direct, L.oracle_backward_fft, L.oracle_operator):
+                      L.oracle_backward_direct, L.oracle_backward_fft, L.oracle_operator,
+                      L.oracle_kernel_synth):
                 f.restype = ctypes.c_int
             _lib = L
         return _lib
@@ -223,3 +229,67 @@ def operator(q, kin, vin, k, D, w_in, w_out, eps_l2=1e-6, eps_rms=1e-6, pad_mode
     if rc != 0:
         raise RuntimeError(f"oracle returned {rc}")
     return y
+
+
+WINDOWS = {"gaussian": 0, "exponential": 1}
+
+
+def synth_grid(shape, pad_mode):
+    """Kernel-grid extents that kernel synthesis evaluates for a convolution
+    on tensors of `shape` ([B, C, L1..LN])."""
+    return kernel_shape(shape, pad_mode)[2:]
+
+
+def kernel_synth(shape, omega0, W1, Wh, Wout, window, gamma=None, beta=None, bias=None,
+                 window_kind="gaussian", pad_mode="linear"):
+    """The HyenaND kernel K(x) on the kernel grid of a convolution of `shape`
+    ([B, C, L1..LN]): a J-layer SIREN of width Hf over the normalised grid
+    coordinates (Eq. (kernel)), each sine's output FiLM-modulated by the
+    sample's (gamma_j, beta_j) (Eq. (film)), projected to the C channels and
+    multiplied by the channel's window (Eq. (mask): Gaussian, win = sigma
+    [N, C]; or exponential, win = alpha [C]).
+
+    omega0 [Hf], W1 [N, Hf], Wh [J-1, Hf, Hf] (rows = input units), Wout
+    [Hf, C], bias [J, Hf] or None, gamma / beta [B, J, Hf] or both None.
+    Returns [B, C, grid...] (modulated) or [C, grid...] (both None)."""
+    shape = tuple(int(s) for s in shape)
+    nd = len(shape) - 2
+    if nd < 1 or nd > 3:
+        raise ValueError("shape must be [B, C, L1..LN] with N in 1..3")
+    B, C = shape[:2]
+    om = np.ascontiguousarray(omega0, dtype=np.float64)
+    Hf = om.size
+    w1 = np.ascontiguousarray(W1, dtype=np.float64)
+    wo = np.ascontiguousarray(Wout, dtype=np.float64)
+    wh = np.ascontiguousarray(Wh if Wh is not None else np.zeros((0, Hf, Hf)), dtype=np.float64)
+    J = wh.shape[0] + 1
+    if om.shape != (Hf,) or w1.shape != (nd, Hf) or wo.shape != (Hf, C) or wh.shape != (J - 1, Hf, Hf):
+        raise ValueError("weight shapes do not match (omega0 [Hf], W1 [N, Hf], Wh [J-1, Hf, Hf], Wout [Hf, C])")
+    if window_kind not in WINDOWS:
+        raise ValueError(f"window_kind must be one of {sorted(WINDOWS)}")
+    win = np.ascontiguousarray(window, dtype=np.float64)
+    if win.shape != ((nd, C) if window_kind == "gaussian" else (C,)):
+        raise ValueError("window must be sigma [N, C] (gaussian) or alpha [C] (exponential)")
+    if (gamma is None) != (beta is None):
+        raise ValueError("gamma and beta go together")
+    mods = [None, None]
+    if gamma is not None:
+        mods = [np.ascontiguousarray(a, dtype=np.float64) for a in (gamma, beta)]
+        if any(m.shape != (B, J, Hf) for m in mods):
+            raise ValueError("gamma and beta must be [B, J, Hf]")
+    bi = None
+    if bias is not None:
+        bi = np.ascontiguousarray(bias, dtype=np.float64)
+        if bi.shape != (J, Hf):
+            raise ValueError("bias must be [J, Hf]")
+    grid = synth_grid(shape, pad_mode)
+    out = np.zeros(((B,) if gamma is not None else ()) + (C,) + tuple(grid), dtype=np.float64)
+    dims = np.asarray(shape, dtype=np.int64)
+    null = ctypes.cast(None, _f64p)
+    p = lambda a: null if a is None else _ptr(a)
+    rc = lib().oracle_kernel_synth(_ptr(om), _ptr(w1), _ptr(wh), p(bi), p(mods[0]), p(mods[1]), _ptr(wo),
+                                   _ptr(win), WINDOWS[window_kind], _ptr(out), nd,
+                                   dims.ctypes.data_as(_i64p), _mode(pad_mode), Hf, J)
+    if rc != 0:
+        raise RuntimeError(f"oracle returned {rc}")
+    return out

@@ -766,7 +766,7 @@ int oracle_backward_fft(const double *x1, const double *x2, const double *v, con
     return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 1);
 }
 
-int oracle_version(void) { return 4; }
+int oracle_version(void) { return 5; }
 
 /* ------------------------------------------------------------------------- */
 /* HyenaND operator: normalised prologue, long convolution, normalised       */
@@ -839,4 +839,127 @@ int oracle_operator(const double *q, const double *kin, const double *vin, const
     free(gate);
     free(ones);
     return rc;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Kernel synthesis: the implicit, input-dependent kernel K(x)               */
+/* ------------------------------------------------------------------------- */
+/*
+ * oracle_kernel_synth -- the HyenaND kernel evaluated on the kernel grid of a
+ * convolution (section 3.2.1 "Multi-Dimensional Continuous Convolutional
+ * Kernels", Eq. (kernel); section 3.2.2 "Input-Dependent Kernels via
+ * Registers and FiLM", Eq. (film); the appendix "HyenaND Design Details:
+ * Masking and Initialization", Eq. (mask)):
+ *
+ *   h_1 = sin(omega0 * (r W1) + b_1)          r in [-1, 1]^N, W1 [N, Hf]
+ *   h_j = sin(h_{j-1} W_j + b_j)              j = 2 .. J, W_j [Hf, Hf]
+ *   after each sine: h_j <- gamma_j[b] * h_j + beta_j[b]   (FiLM, per sample)
+ *   f   = h_J Wout                            Wout [Hf, C]
+ *   K[b, c, i] = w_c(r_i) f[c]
+ *
+ * Window w_c: kind 0, the Gaussian of Eq. (mask), exp(-1/2 sum_d (r_d /
+ * sigma[d, c])^2) with win = sigma [N, C]; kind 1, the exponential decay
+ * exp(-alpha[c] sum_d |r_d|) of the original Hyena window (one axis: Hyena's
+ * exp(-alpha |r|)) with win = alpha [C].
+ *
+ * The grid follows the convolution's kernel layout: per axis L_d points in
+ * the linear and circular modes, 2 L_d - 1 in the centered mode.  The point's
+ * displacement is i (linear), i - (L_d - 1) (centered), i for i <= L_d / 2
+ * and i - L_d beyond (circular, the signed periodic displacement), and its
+ * coordinate r_d = displacement / (L_d - 1) (0 when L_d = 1): the double
+ * grid of the centered mode spans [-1, 1] exactly, and every mode gives one
+ * displacement the same coordinate.
+ *
+ * Readings: the hidden-layer frequency of the appendix's SIREN definition is
+ * taken as folded into W_j; the bias is that definition's (one per layer, may
+ * be NULL for none); FiLM acts on the sine's output, the hidden activation.
+ * gamma and beta are [B, J, Hf]; both NULL gives the unmodulated kernel of
+ * section 3.2.1, written once as [C, grid] (a kernel shared by the batch).
+ * Wh is [J - 1, Hf, Hf], row = input unit.  k is [B, C, grid] or [C, grid].
+ */
+static double synth_coord(int64_t i, int64_t L, int mode) {
+    if (L <= 1) return 0.0;
+    int64_t d;
+    if (mode == MODE_CENTERED)
+        d = i - (L - 1);
+    else if (mode == MODE_CIRCULAR)
+        d = i <= L / 2 ? i : i - L;
+    else
+        d = i;
+    return (double)d / (double)(L - 1);
+}
+
+int oracle_kernel_synth(const double *omega0, const double *W1, const double *Wh, const double *bias,
+                        const double *gamma, const double *beta, const double *Wout, const double *win,
+                        int wkind, double *k, int ndim, const int64_t *dims, int mode, int hidden,
+                        int layers) {
+    geom g;
+    if (!omega0 || !W1 || !Wout || !win || !k || make_geom(ndim, dims, &g)) return 1;
+    if (mode < 0 || mode > 2 || wkind < 0 || wkind > 1 || hidden < 1 || layers < 1) return 1;
+    if ((gamma == NULL) != (beta == NULL) || (layers > 1 && !Wh)) return 1;
+    const int64_t C = g.C, H = hidden, J = layers;
+    const int64_t nb = gamma ? g.B : 1;
+    int64_t KL[3];
+    for (int d = 0; d < 3; ++d) KL[d] = (mode == MODE_CENTERED) ? 2 * g.L[d] - 1 : g.L[d];
+    const int64_t npos = KL[0] * KL[1] * KL[2];
+    double *h = (double *)malloc((size_t)H * sizeof(double));
+    double *t = (double *)malloc((size_t)H * sizeof(double));
+    if (!h || !t) {
+        free(h);
+        free(t);
+        return 2;
+    }
+    for (int64_t b = 0; b < nb; ++b)
+        for (int64_t p = 0; p < npos; ++p) {
+            /* coordinates of the grid point; axis a of the N real axes is
+               axis 3 - N + a of the padded three */
+            int64_t idx[3] = {p / (KL[1] * KL[2]), (p / KL[2]) % KL[1], p % KL[2]};
+            double r[3];
+            for (int a = 0; a < ndim; ++a) {
+                int d = 3 - ndim + a;
+                r[a] = synth_coord(idx[d], g.L[d], mode);
+            }
+            /* first layer */
+            for (int64_t o = 0; o < H; ++o) {
+                double s = 0.0;
+                for (int a = 0; a < ndim; ++a) s += r[a] * W1[a * H + o];
+                s = omega0[o] * s + (bias ? bias[o] : 0.0);
+                h[o] = sin(s);
+                if (gamma) h[o] = gamma[(b * J + 0) * H + o] * h[o] + beta[(b * J + 0) * H + o];
+            }
+            /* hidden layers 2 .. J */
+            for (int64_t j = 1; j < J; ++j) {
+                const double *W = Wh + (j - 1) * H * H;
+                for (int64_t o = 0; o < H; ++o) {
+                    double s = 0.0;
+                    for (int64_t i = 0; i < H; ++i) s += h[i] * W[i * H + o];
+                    s += bias ? bias[j * H + o] : 0.0;
+                    t[o] = sin(s);
+                    if (gamma) t[o] = gamma[(b * J + j) * H + o] * t[o] + beta[(b * J + j) * H + o];
+                }
+                memcpy(h, t, (size_t)H * sizeof(double));
+            }
+            /* output projection and window */
+            for (int64_t c = 0; c < C; ++c) {
+                double f = 0.0;
+                for (int64_t i = 0; i < H; ++i) f += h[i] * Wout[i * C + c];
+                double w;
+                if (wkind == 0) {
+                    double e = 0.0;
+                    for (int a = 0; a < ndim; ++a) {
+                        double z = r[a] / win[a * C + c];
+                        e += z * z;
+                    }
+                    w = exp(-0.5 * e);
+                } else {
+                    double e = 0.0;
+                    for (int a = 0; a < ndim; ++a) e += fabs(r[a]);
+                    w = exp(-win[c] * e);
+                }
+                k[(b * C + c) * npos + p] = w * f;
+            }
+        }
+    free(h);
+    free(t);
+    return 0;
 }
