@@ -204,6 +204,51 @@ hyenand_status hyenand_operator(const void* q, const void* kin, const void* vin,
 hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
                                                size_t* bytes_out);
 
+/*
+ * hyenand_kernel_synth -- the HyenaND kernel K(x) = w(r) * f_theta(r; z(x))
+ * written on the kernel grid of a convolution, ready for hyenand_fftconv
+ * (section 3.2.1 "Multi-Dimensional Continuous Convolutional Kernels",
+ * Eq. (kernel); section 3.2.2 "Input-Dependent Kernels via Registers and
+ * FiLM", Eq. (film); the appendix "HyenaND Design Details: Masking and
+ * Initialization", Eq. (mask)).  For every sample b, channel c and grid point
+ * with normalised coordinates r in [-1, 1]^N:
+ *
+ *     h_1 = sin(omega0 * (r W1) + bias_1)          then FiLM
+ *     h_j = sin(h_{j-1} W_j + bias_j), j = 2..J    then FiLM
+ *     FiLM: h_j <- gamma[b, j] * h_j + beta[b, j]  (after the sine)
+ *     k[b, c, point] = w_c(r) * (h_J Wout)[c]
+ *
+ * Window: window_kind 0 is the Gaussian exp(-1/2 sum_d (r_d / sigma[d, c])^2)
+ * with window = sigma [N, C] (every sigma > 0); window_kind 1 is the
+ * exponential exp(-alpha[c] sum_d |r_d|) with window = alpha [C].
+ *
+ * The grid is the kernel layout that hyenand_fftconv takes for the same dims
+ * and pad_mode: L_d points per axis (linear, circular) or 2 L_d - 1
+ * (centered).  A point's displacement along axis d is its index i (linear),
+ * i - (L_d - 1) (centered), or the signed periodic one, i for i <= L_d / 2
+ * and i - L_d above (circular); r_d = displacement / (L_d - 1), and 0 when
+ * L_d = 1.  The centered double grid thus spans [-1, 1] exactly.
+ *
+ * Parameters (device pointers, fp32, row-major, 4-byte aligned):
+ *   omega0 [Hf], W1 [N, Hf], Wh [J - 1, Hf, Hf] (layer j + 1's matrix, rows =
+ *   input units; NULL allowed when J = 1), bias [J, Hf] or NULL (no biases),
+ *   gamma, beta [B, J, Hf] (the sample's FiLM scales and shifts) or both NULL
+ *   (the unmodulated kernel), Wout [Hf, C].
+ * hidden = Hf in {32, 64, 128}; layers = J in 1..16.
+ * k (output, device, `dtype`, aligned to its element size): [B, C, grid...]
+ *   with FiLM, [C, grid...] without (the kernel hyenand_fftconv_shared_k
+ *   takes); must not overlap a parameter.
+ * dims = {B, C, L1, ..., LN} of the convolution (host pointer), ndim = N.
+ * The hidden layers and the output projection run as fp32 matrix-core
+ * products; the sine and exponential use the hardware approximations after
+ * an exact-to-fp32 argument reduction.  Validation, stream and error
+ * conventions as for hyenand_fftconv; no workspace.
+ */
+hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const float* Wh, const float* bias,
+                                    const float* gamma, const float* beta, const float* Wout, const float* window,
+                                    int window_kind, int hidden, int layers, void* k, int ndim,
+                                    const int64_t* dims, int pad_mode, int dtype, void* stream);
+
 /* Static text for a status code. */
 const char* hyenand_status_string(int status);
 

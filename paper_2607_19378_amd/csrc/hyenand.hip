@@ -650,6 +650,79 @@ hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, in
   return HYENAND_OK;
 }
 
-int hyenand_version(void) { return 200; }
+hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const float* Wh, const float* bias,
+                                    const float* gamma, const float* beta, const float* Wout, const float* window,
+                                    int window_kind, int hidden, int layers, void* k, int ndim, const int64_t* dims,
+                                    int pad_mode, int dtype, void* stream) {
+  if (ndim < 1 || ndim > 3) return fail(HYENAND_ERR_INVALID_ARGUMENT, "ndim must be 1, 2 or 3 (got %d)", ndim);
+  if (!dims) return fail(HYENAND_ERR_INVALID_ARGUMENT, "dims is NULL");
+  if (pad_mode != HYENAND_PAD_LINEAR && pad_mode != HYENAND_PAD_CIRCULAR && pad_mode != HYENAND_PAD_CENTERED)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "pad_mode must be 0, 1 or 2, got %d", pad_mode);
+  if (dtype != HYENAND_DTYPE_F32 && dtype != HYENAND_DTYPE_BF16)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "dtype must be 0 (f32) or 1 (bf16), got %d", dtype);
+  if (window_kind != 0 && window_kind != 1)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "window_kind must be 0 (gaussian) or 1 (exponential), got %d",
+                window_kind);
+  if (!synth_hidden_supported(hidden))
+    return fail(HYENAND_ERR_UNSUPPORTED, "hidden width must be 32, 64 or 128 (got %d)", hidden);
+  if (layers < 1 || layers > 16) return fail(HYENAND_ERR_UNSUPPORTED, "layers must be 1..16 (got %d)", layers);
+  if (!omega0 || !W1 || !Wout || !window || !k || (layers > 1 && !Wh))
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if ((gamma == nullptr) != (beta == nullptr))
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "gamma and beta must both be given or both be NULL");
+  SynthArgs a;
+  memset(&a, 0, sizeof a);
+  int64_t total = 1;
+  for (int i = 0; i < ndim + 2; ++i) {
+    if (dims[i] < 1) return fail(HYENAND_ERR_INVALID_ARGUMENT, "dims[%d] = %lld must be >= 1", i, (long long)dims[i]);
+    if (dims[i] > (int64_t(1) << 30)) return fail(HYENAND_ERR_UNSUPPORTED, "extent too large");
+  }
+  if (dims[1] > (1 << 20)) return fail(HYENAND_ERR_UNSUPPORTED, "C = %lld is too large", (long long)dims[1]);
+  a.nd = ndim;
+  a.npos = 1;
+  for (int d = 0; d < ndim; ++d) {
+    a.Lc[d] = dims[2 + d];
+    a.KL[d] = pad_mode == HYENAND_PAD_CENTERED ? 2 * dims[2 + d] - 1 : dims[2 + d];
+    if (a.npos > (int64_t(1) << 40) / a.KL[d]) return fail(HYENAND_ERR_UNSUPPORTED, "kernel grid too large");
+    a.npos *= a.KL[d];
+  }
+  a.C = (int)dims[1];
+  a.nb = gamma ? dims[0] : 1;
+  total = a.nb * a.C;
+  if (total > (int64_t(1) << 46) / a.npos) return fail(HYENAND_ERR_UNSUPPORTED, "kernel tensor too large");
+  total *= a.npos;
+  if ((a.npos + 31) / 32 * a.nb / 4 >= (int64_t(1) << 31)) return fail(HYENAND_ERR_UNSUPPORTED, "grid too large");
+  const size_t es = dtype == HYENAND_DTYPE_BF16 ? 2 : 4;
+  const float* ptrs[] = {omega0, W1, Wh, bias, gamma, beta, Wout, window};
+  const char* names[] = {"omega0", "W1", "Wh", "bias", "gamma", "beta", "Wout", "window"};
+  const size_t H = (size_t)hidden, J = (size_t)layers, C = (size_t)a.C;
+  const size_t counts[] = {H, (size_t)ndim * H, (J - 1) * H * H, J * H, (size_t)a.nb * J * H,
+                           (size_t)a.nb * J * H, H * C, window_kind == 0 ? (size_t)ndim * C : C};
+  if ((uintptr_t)k % es != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "k is not aligned to its element size");
+  for (int i = 0; i < 8; ++i) {
+    if (!ptrs[i] || counts[i] == 0) continue;
+    if ((uintptr_t)ptrs[i] % 4 != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not 4-byte aligned", names[i]);
+    if (overlaps(k, (size_t)total * es, ptrs[i], counts[i] * 4))
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "k overlaps %s", names[i]);
+  }
+  a.omega0 = omega0;
+  a.W1 = W1;
+  a.Wh = layers > 1 ? Wh : nullptr;
+  a.bias = bias;
+  a.gamma = gamma;
+  a.beta = beta;
+  a.Wout = Wout;
+  a.win = window;
+  a.k = k;
+  a.mode = pad_mode;
+  a.J = layers;
+  a.wkind = window_kind;
+  a.hidden = hidden;
+  hipError_t err = launch_synth(a, dtype == HYENAND_DTYPE_BF16, (hipStream_t)stream);
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
+}
+
+int hyenand_version(void) { return 300; }
 
 }  // extern "C"

@@ -85,4 +85,20 @@ hipError_t launch_op_prologue(const void* q, const void* kin, float* s, int64_t 
 hipError_t launch_op_rmsnorm(void* y, const void* w_out, int64_t B, int C, int64_t npos, bool bf16, float eps_rms,
                              hipStream_t st);
 
+// Kernel synthesis (synth.hip): the SIREN + FiLM + window kernel on the kernel
+// grid of a convolution, k [nb, C, KL...] in the storage type.
+struct SynthArgs {
+  const float *omega0, *W1, *Wh, *bias, *gamma, *beta, *Wout, *win;
+  void* k;
+  int nd;         // axes of the grid, 1..3 (unit axes kept)
+  int64_t KL[3];  // kernel-grid extents: L (linear, circular) or 2L - 1 (centered)
+  int64_t Lc[3];  // convolution grid extents, which fix the coordinates
+  int mode;       // 0 linear, 1 circular, 2 centered
+  int C, J, wkind, hidden;
+  int64_t npos;   // prod KL
+  int64_t nb;     // kernels written: B (FiLM given) or 1
+};
+bool synth_hidden_supported(int hidden);
+hipError_t launch_synth(const SynthArgs& a, bool bf16, hipStream_t s);
+
 }  // namespace hyenand

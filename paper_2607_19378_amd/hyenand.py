@@ -23,7 +23,7 @@ EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_work
             "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
-            "hyenand_status_string", "hyenand_last_error", "hyenand_version")
+            "hyenand_kernel_synth", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
 
 _lock = threading.Lock()
 _lib = None
@@ -70,6 +70,9 @@ def lib() -> ctypes.CDLL:
             L.hyenand_operator_workspace_size.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                           ctypes.POINTER(ctypes.c_size_t)]
             L.hyenand_operator_workspace_size.restype = ctypes.c_int
+            L.hyenand_kernel_synth.argtypes = [vp] * 8 + [ctypes.c_int] * 3 + [vp, ctypes.c_int, i64p, ctypes.c_int,
+                                                                       ctypes.c_int, vp]
+            L.hyenand_kernel_synth.restype = ctypes.c_int
             L.hyenand_fftconv_plan_name.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_char_p, ctypes.c_size_t]
             L.hyenand_fftconv_plan_name.restype = ctypes.c_int
@@ -323,3 +326,66 @@ def operator(q, kin, vin, k, D, w_in, w_out, eps_l2: float = 1e-6, eps_rms: floa
     y = torch.empty_like(q)
     PreparedOperator(y, q, kin, vin, k, D, w_in, w_out, eps_l2, eps_rms, pad_mode, workspace, stream)()
     return y
+
+
+WINDOWS = {"gaussian": 0, "exponential": 1}
+
+
+class PreparedSynth:
+    """One hyenand_kernel_synth call with its arguments checked and
+    marshalled once (see Prepared).  k is [B, C, grid...] when gamma and beta
+    are given, else [C, grid...]; the grid is kernel_shape(shape, pad_mode)'s."""
+
+    def __init__(self, k, shape, omega0, W1, Wh, Wout, window, gamma=None, beta=None, bias=None,
+                 window_kind: str = "gaussian", pad_mode: str = "linear", stream=None):
+        import torch
+        shape = tuple(int(x) for x in shape)
+        nd = len(shape) - 2
+        B, C = shape[:2]
+        Hf = int(omega0.shape[0])
+        J = 1 if Wh is None else int(Wh.shape[0]) + 1
+        if window_kind not in WINDOWS:
+            raise ValueError(f"window_kind must be one of {sorted(WINDOWS)}")
+        want = [(omega0, (Hf,)), (W1, (nd, Hf)), (Wout, (Hf, C)),
+                (window, (nd, C) if window_kind == "gaussian" else (C,))]
+        if Wh is not None:
+            want.append((Wh, (J - 1, Hf, Hf)))
+        if bias is not None:
+            want.append((bias, (J, Hf)))
+        if (gamma is None) != (beta is None):
+            raise ValueError("gamma and beta go together")
+        if gamma is not None:
+            want += [(gamma, (B, J, Hf)), (beta, (B, J, Hf))]
+        for t, sh in want:
+            if not t.is_cuda or t.dtype != torch.float32 or tuple(t.shape) != sh or not t.is_contiguous():
+                raise ValueError(f"parameters must be contiguous fp32 GPU tensors; expected shape {sh}, "
+                                 f"got {tuple(t.shape)}")
+        kshape = kernel_shape(shape, pad_mode, shared_k=gamma is None)
+        if not k.is_cuda or tuple(k.shape) != kshape or not k.is_contiguous():
+            raise ValueError(f"k must be a contiguous GPU tensor of shape {kshape}")
+        nd_, dims = _dims(shape)
+        if stream is None:
+            stream = torch.cuda.current_stream(k.device)
+        opt = lambda t: None if t is None else _ptr(t)
+        self._fn = lib().hyenand_kernel_synth
+        self._args = (_ptr(omega0), _ptr(W1), opt(Wh), opt(bias), opt(gamma), opt(beta), _ptr(Wout), _ptr(window),
+                      WINDOWS[window_kind], Hf, J, _ptr(k), nd_, dims, _mode(pad_mode), _dtype_code(k.dtype),
+                      ctypes.c_void_p(stream.cuda_stream))
+        self._keep = (k, omega0, W1, Wh, Wout, window, gamma, beta, bias, stream)
+
+    def __call__(self) -> None:
+        status = self._fn(*self._args)
+        if status != OK:
+            _check(status)
+
+
+def kernel_synth(shape, omega0, W1, Wh, Wout, window, gamma=None, beta=None, bias=None,
+                 window_kind: str = "gaussian", pad_mode: str = "linear", dtype=None, stream=None):
+    """The HyenaND kernel K(x) for a convolution on tensors of `shape`
+    ([B, C, L...]), with a torch-allocated k of `dtype` (fp32 by default)."""
+    import torch
+    dtype = dtype or torch.float32
+    kshape = kernel_shape(shape, pad_mode, shared_k=gamma is None)
+    k = torch.empty(kshape, dtype=dtype, device=omega0.device)
+    PreparedSynth(k, shape, omega0, W1, Wh, Wout, window, gamma, beta, bias, window_kind, pad_mode, stream)()
+    return k

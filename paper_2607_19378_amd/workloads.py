@@ -334,3 +334,61 @@ def random_case(B: int, C: int, grid, pad_mode: str, dtype: str, seed: int,
     w = Workload(f"case_{len(grid)}d_{pad_mode}_{dtype}_{seed}", B, C, grid, pad_mode,
                  dtype, seed, tau, kernel_norm=(len(grid) == 1))
     return generate(w)
+
+
+def siren_params(seed: int, ndim: int, hidden: int, layers: int, C: int, B: int, modulated: bool = True,
+                 bias: bool = True, window_kind: str = "gaussian", blocks: int = 4,
+                 omega_range: Tuple[float, float] = (1.0, 30.0), scale_range: Tuple[float, float] = (0.5, 1.5),
+                 rho: float = 0.1, sigma_range: Tuple[float, float] = (1.0, 0.05),
+                 film_spread: float = 0.1) -> Dict[str, Optional[np.ndarray]]:
+    """Seeded fp32 parameters of the kernel-synthesis network, drawn the way
+    the paper initialises it (section 3.2.1 and the masking/initialisation
+    appendix), with FiLM moved away from its identity start as training would:
+
+    * omega0: ``blocks`` equal blocks of hidden units with base frequencies on
+      a linear schedule over ``omega_range``, each unit's base scaled by
+      s ~ U(``scale_range``);
+    * W1 ~ U(-1/sqrt(N), 1/sqrt(N)) (the N-D first-layer correction);
+    * hidden W_j and Wout ~ U(-sqrt(6/Hf), sqrt(6/Hf)) (SIREN's hidden-layer
+      range), near-block-diagonal: entries linking different blocks (channels
+      are assigned to blocks in order) scaled by ``rho``;
+    * biases ~ U(-1/sqrt(fan_in), 1/sqrt(fan_in));
+    * Gaussian window: sigma[d, c] on a log-spaced ramp over the channels from
+      ``sigma_range[0]`` (channel 0, paired with the lowest-frequency block)
+      to ``sigma_range[1]``, times a per-axis factor U(0.8, 1.25);
+      exponential window: alpha[c] log-spaced over [0.5, 8];
+    * gamma = 1 + film_spread N(0, 1), beta = film_spread N(0, 1), per (b, j, unit).
+
+    The draw order is fixed (one child SeedSequence per array, in the order of
+    the keys below); arrays that are switched off are None."""
+    seqs = np.random.SeedSequence(seed).spawn(9)
+    rng = [np.random.Generator(np.random.PCG64(s)) for s in seqs]
+    H, J = hidden, layers
+    f32 = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    ublock = (np.arange(H) * blocks) // H
+    cblock = (np.arange(C) * blocks) // C
+    lo, hi = omega_range
+    base = lo + (hi - lo) * ublock / max(1, blocks - 1)
+    omega0 = base * rng[0].uniform(*scale_range, H)
+    W1 = rng[1].uniform(-1.0, 1.0, (ndim, H)) / np.sqrt(ndim)
+    lim = np.sqrt(6.0 / H)
+    Wh = rng[2].uniform(-lim, lim, (J - 1, H, H))
+    Wh *= np.where(ublock[:, None] == ublock[None, :], 1.0, rho)[None]
+    Wout = rng[3].uniform(-lim, lim, (H, C)) * np.where(ublock[:, None] == cblock[None, :], 1.0, rho)
+    b = None
+    if bias:
+        b = np.empty((J, H))
+        b[0] = rng[4].uniform(-1.0, 1.0, H) / np.sqrt(ndim)
+        b[1:] = rng[4].uniform(-1.0, 1.0, (J - 1, H)) / np.sqrt(H)
+    if window_kind == "gaussian":
+        ramp = np.geomspace(sigma_range[0], sigma_range[1], C)
+        window = ramp[None, :] * rng[5].uniform(0.8, 1.25, (ndim, 1))
+    else:
+        window = np.geomspace(0.5, 8.0, C)
+    gamma = beta = None
+    if modulated:
+        gamma = 1.0 + film_spread * rng[6].standard_normal((B, J, H))
+        beta = film_spread * rng[7].standard_normal((B, J, H))
+    return dict(omega0=f32(omega0), W1=f32(W1), Wh=f32(Wh) if J > 1 else None, Wout=f32(Wout),
+                window=f32(window), bias=None if b is None else f32(b), gamma=None if gamma is None else f32(gamma),
+                beta=None if beta is None else f32(beta))

@@ -241,3 +241,40 @@ def test_shared_kernel_validation(L):
     assert b"y overlaps k" in L.hyenand_last_error()
     q = [ctypes.c_void_p(x) for x in p[:3]] + [None] + [ctypes.c_void_p(x) for x in p[4:]]
     assert L.hyenand_fftconv_shared_k(*q, 1, dims, 0, 0, None, 0, None) == H.ERR_INVALID_ARGUMENT
+
+
+def synth(L, shape=(2, 4, 16), hidden=32, layers=1, wkind=0, mode=0, dtype=0, ptrs=None, k=None):
+    """hyenand_kernel_synth with fake pointers: every call here must fail
+    validation (nothing may launch)."""
+    dims = (ctypes.c_int64 * len(shape))(*shape)
+    p = ptrs or [FAKE + i * (1 << 36) for i in range(8)]
+    kp = FAKE + (9 << 36) if k is None else k
+    return L.hyenand_kernel_synth(*[ctypes.c_void_p(x) if x else None for x in p], wkind, hidden, layers,
+                                  ctypes.c_void_p(kp), len(shape) - 2, dims, mode, dtype, None)
+
+
+def test_synth_validation(L):
+    base = [FAKE + i * (1 << 36) for i in range(8)]
+    assert synth(L, hidden=48) == H.ERR_UNSUPPORTED
+    assert b"hidden width" in L.hyenand_last_error()
+    assert synth(L, layers=0) == H.ERR_UNSUPPORTED
+    assert synth(L, layers=17) == H.ERR_UNSUPPORTED
+    assert synth(L, wkind=2) == H.ERR_INVALID_ARGUMENT
+    assert synth(L, mode=3) == H.ERR_INVALID_ARGUMENT
+    assert synth(L, dtype=4) == H.ERR_INVALID_ARGUMENT
+    assert synth(L, shape=(2, 0, 16)) == H.ERR_INVALID_ARGUMENT
+    assert synth(L, shape=(2, 4, 16), ptrs=[0] + base[1:]) == H.ERR_INVALID_ARGUMENT  # omega0 NULL
+    assert synth(L, layers=2, ptrs=base[:2] + [0] + base[3:]) == H.ERR_INVALID_ARGUMENT  # Wh NULL
+    assert synth(L, ptrs=base[:5] + [0] + base[6:]) == H.ERR_INVALID_ARGUMENT  # gamma without beta
+    assert b"gamma and beta" in L.hyenand_last_error()
+    assert synth(L, ptrs=base[:1] + [base[1] + 2] + base[2:]) == H.ERR_INVALID_ARGUMENT  # W1 misaligned
+    assert b"W1" in L.hyenand_last_error()
+    assert synth(L, dtype=1, k=FAKE + (9 << 36) + 1) == H.ERR_INVALID_ARGUMENT  # bf16 k misaligned
+    # k (2 x 4 x 16 fp32 = 512 bytes) running into Wout
+    assert synth(L, k=base[6] - 256) == H.ERR_INVALID_ARGUMENT
+    assert b"k overlaps Wout" in L.hyenand_last_error()
+    # without FiLM k is [C, grid]: 4 x 16 fp32 = 256 bytes, so starting 252 bytes below Wout overlaps it
+    nofilm = base[:4] + [0, 0] + base[6:]
+    assert synth(L, ptrs=nofilm, k=base[6] - 252) == H.ERR_INVALID_ARGUMENT
+    # centered: the grid has 2L - 1 = 31 points, so 4 x 31 floats reach Wout from 496 bytes below it
+    assert synth(L, ptrs=nofilm, mode=2, k=base[6] - 492) == H.ERR_INVALID_ARGUMENT
