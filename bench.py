@@ -270,6 +270,90 @@ def bench_operator(args, w, inp):
     print(json.dumps(out))
 
 
+SYNTH_HIDDEN, SYNTH_LAYERS = 64, 3
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+
+def synth_flops(w: W.Workload, hidden: int, layers: int) -> float:
+    """Multiply-adds of kernel synthesis, 2 flops each: per grid point and
+    sample the first layer (N x Hf), the hidden layers ((J - 1) x Hf x Hf) and
+    the output projection (Hf x C); sines, FiLM and the window are not counted."""
+    npos = int(np.prod(w.kernel_shape[2:]))
+    per = len(w.grid) * hidden + (layers - 1) * hidden * hidden + hidden * w.C
+    return 2.0 * w.B * npos * per
+
+
+def bench_synth(args, w, inp):
+    """Time hyenand_kernel_synth (the FiLM-modulated SIREN kernel and its
+    window, Hf = 64, J = 3) on the workload's kernel grid, alone and followed
+    by the gated convolution that consumes it; prints one JSON line."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    p = W.siren_params(w.seed + 21, len(w.grid), SYNTH_HIDDEN, SYNTH_LAYERS, w.C, w.B)
+    d = {k: (None if v is None else torch.from_numpy(v).to(dev)) for k, v in p.items()}
+    k = torch.empty(H.kernel_shape(w.shape, w.pad_mode), dtype=tdt, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    synth = H.PreparedSynth(k, w.shape, d["omega0"], d["W1"], d["Wh"], d["Wout"], d["window"], d["gamma"],
+                            d["beta"], d["bias"], "gaussian", w.pad_mode, stream)
+    x1, x2, v, D = (to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.D))
+    y = torch.empty_like(x1)
+    ws_bytes = H.workspace_size(w.shape, w.pad_mode, w.dtype)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    conv = H.Prepared(y, x1, x2, v, k, D, w.pad_mode, ws, stream)
+
+    def timed(fns, steps):
+        for _ in range(args.warmup):
+            for f in fns:
+                f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(steps):
+            for f in fns:
+                f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / steps, (time.perf_counter() - t0) / steps
+
+    synth_s, _ = timed([synth], args.steps)
+    conv_s, _ = timed([conv], args.steps)
+    both_s, both_wall = timed([synth, conv], args.steps)
+    flops = synth_flops(w, SYNTH_HIDDEN, SYNTH_LAYERS)
+    tflops = flops / synth_s / 1e12
+    parity = None
+    if not args.no_parity:
+        import oracle
+        f = {kk: (None if vv is None else vv.astype(np.float64)) for kk, vv in p.items()}
+        kb = min(w.B, 2)  # the first samples' kernels, every channel and point
+        ref = oracle.kernel_synth((kb,) + w.shape[1:], f["omega0"], f["W1"], f["Wh"], f["Wout"], f["window"],
+                                  gamma=f["gamma"][:kb], beta=f["beta"][:kb], bias=f["bias"], pad_mode=w.pad_mode)
+        got = k[:kb]
+        got = (W.bf16_bits_to_f64(got.view(torch.int16).cpu().numpy().view(np.uint16)) if got.dtype == torch.bfloat16
+               else got.cpu().numpy().astype(np.float64))
+        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    out = {
+        "metric": "input-dependent kernel synthesis + gated N-D FFT conv GElem/s on 1 MI355X",
+        "value": round(w.elems / both_wall / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(both_wall * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded parameters drawn by the paper's initialisation recipe)",
+        "config": {"workload": w.name, "pass": "synth+conv", "B": w.B, "C": w.C, "grid": list(w.grid),
+                   "kernel_grid": list(w.kernel_shape[2:]), "pad_mode": w.pad_mode, "storage": w.dtype,
+                   "hidden": SYNTH_HIDDEN, "layers": SYNTH_LAYERS, "film": True, "window": "gaussian"},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": MFMA_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / MFMA_F32_PEAK_TFLOPS, 4), "traffic": None, "kernel": "siren_synth",
+                     "alg_flops_per_call": flops, "avg_call_us": round(synth_s * 1e6, 3),
+                     "k_bytes_written": int(k.numel() * k.element_size())},
+        "synth_us": round(synth_s * 1e6, 3), "conv_us": round(conv_s * 1e6, 3),
+        "synth_then_conv_us": round(both_s * 1e6, 3),
+        "cpu_baseline": None, "parity_rel_l2": parity, "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out))
+
+
 def to_device(arr, dtype):
     import torch
     if dtype == "f32":
@@ -346,6 +430,8 @@ def main():
                     help="time the backward (gradients for x1, x2, v, k, D) instead of the forward")
     ap.add_argument("--operator", action="store_true",
                     help="time the whole HyenaND operator (norms and activations around the convolution)")
+    ap.add_argument("--synth", action="store_true",
+                    help="time kernel synthesis (FiLM-modulated SIREN + window) alone and followed by the conv")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -364,6 +450,9 @@ def main():
         return
     if args.operator:
         bench_operator(args, w, inp)
+        return
+    if args.synth:
+        bench_synth(args, w, inp)
         return
     set_bytes = alg_bytes(w)
     rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))

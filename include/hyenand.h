@@ -229,7 +229,8 @@ hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, in
  * and i - L_d above (circular); r_d = displacement / (L_d - 1), and 0 when
  * L_d = 1.  The centered double grid thus spans [-1, 1] exactly.
  *
- * Parameters (device pointers, fp32, row-major, 4-byte aligned):
+ * Parameters (device pointers, fp32, row-major; Wh, gamma and beta 16-byte
+ * aligned, the others 4-byte aligned):
  *   omega0 [Hf], W1 [N, Hf], Wh [J - 1, Hf, Hf] (layer j + 1's matrix, rows =
  *   input units; NULL allowed when J = 1), bias [J, Hf] or NULL (no biases),
  *   gamma, beta [B, J, Hf] (the sample's FiLM scales and shifts) or both NULL

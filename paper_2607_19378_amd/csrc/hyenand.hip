@@ -691,7 +691,7 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
   total = a.nb * a.C;
   if (total > (int64_t(1) << 46) / a.npos) return fail(HYENAND_ERR_UNSUPPORTED, "kernel tensor too large");
   total *= a.npos;
-  if ((a.npos + 31) / 32 * a.nb / 4 >= (int64_t(1) << 31)) return fail(HYENAND_ERR_UNSUPPORTED, "grid too large");
+  if ((a.npos + 15) / 16 * a.nb / 8 >= (int64_t(1) << 31)) return fail(HYENAND_ERR_UNSUPPORTED, "grid too large");
   const size_t es = dtype == HYENAND_DTYPE_BF16 ? 2 : 4;
   const float* ptrs[] = {omega0, W1, Wh, bias, gamma, beta, Wout, window};
   const char* names[] = {"omega0", "W1", "Wh", "bias", "gamma", "beta", "Wout", "window"};
@@ -701,7 +701,10 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
   if ((uintptr_t)k % es != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "k is not aligned to its element size");
   for (int i = 0; i < 8; ++i) {
     if (!ptrs[i] || counts[i] == 0) continue;
-    if ((uintptr_t)ptrs[i] % 4 != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not 4-byte aligned", names[i]);
+    // Wh, gamma and beta are read four floats at a time
+    const size_t align = (i == 2 || i == 4 || i == 5) ? 16 : 4;
+    if ((uintptr_t)ptrs[i] % align != 0)
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not %zu-byte aligned", names[i], align);
     if (overlaps(k, (size_t)total * es, ptrs[i], counts[i] * 4))
       return fail(HYENAND_ERR_INVALID_ARGUMENT, "k overlaps %s", names[i]);
   }

@@ -97,6 +97,10 @@ struct SynthArgs {
   int C, J, wkind, hidden;
   int64_t npos;   // prod KL
   int64_t nb;     // kernels written: B (FiLM given) or 1
+  int resident;   // set by launch_synth: every weight staged in LDS at once
+  int cc;         // set by launch_synth: output channels per streamed chunk
+  int stream_floats;  // set by launch_synth: LDS floats of the streamed region
+  int film_lds;   // set by launch_synth: FiLM rows of every sample kept in LDS
 };
 bool synth_hidden_supported(int hidden);
 hipError_t launch_synth(const SynthArgs& a, bool bf16, hipStream_t s);

@@ -6,30 +6,33 @@
 // the exponential decay of the original Hyena).
 //
 // The hidden layers and the output projection are dense contractions over the
-// hidden width Hf, so they run on v_mfma_f32_32x32x2_f32 (fp32 in, fp32
-// accumulate).  One wave owns 32 grid points of one sample and carries them
-// through every layer without leaving registers: the matrix product is taken
+// hidden width Hf, so they run on v_mfma_f32_16x16x4_f32 (fp32 in, fp32
+// accumulate).  One wave owns 16 grid points of one sample and carries them
+// through every layer without leaving registers: the product is taken
 // transposed, out[unit, point] = sum_k W[k, unit] h[point, k], so the points
-// are the 32 columns (lane % 32) and the units the 32 rows of each tile.  The
-// accumulator layout of one tile (lane l, register e: row 8 (e / 4) +
-// 4 (l / 32) + e % 4, column l % 32) then already is the operand layout of
-// the next layer, because a contraction may visit its k index in any order:
-// at the step of register e the two lane halves contribute units
-// 8 (e / 4) + e % 4 and that + 4, and the weight operand is read for exactly
-// those units.  Only weights are loaded (from L1/L2, shared by every wave);
-// the points' coordinates are generated from their index; K is written once.
+// are the 16 columns (lane % 16) and the units the 16 rows of each tile.  The
+// accumulator layout of a tile (lane l, register r: row 4 (l / 16) + r,
+// column l % 16) already is the operand layout of the next layer, because a
+// contraction may visit its k index in any order: at step r of a 16-unit
+// block the four lane groups contribute units 4 g + r (g = l / 16), and the
+// weight operand is read for exactly those units.  The weights sit in LDS,
+// transposed (row = output unit or channel), so that the four steps of a
+// block take one 16-byte read per lane.  Points' coordinates are generated
+// from their index; K is written once.
+#include <algorithm>
+#include <mutex>
+
 #include "kernels.hpp"
 
 namespace hyenand {
 
 namespace {
 
-typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int kSynthWaves = 4;  // independent waves per workgroup
-
-// the hidden unit (within a 32-unit tile) a lane of half g holds in register e
-__device__ __forceinline__ int tile_unit(int e, int g) { return 8 * (e >> 2) + 4 * g + (e & 3); }
+constexpr int kSynthWaves = 8;  // waves per workgroup, one 16-point tile each
+constexpr int kThreads = 64 * kSynthWaves;
+constexpr float kLog2e = 1.4426950408889634f;
 
 // sin(x): two-constant Cody-Waite reduction to [-pi, pi], then the hardware
 // sine (which takes its argument in turns)
@@ -40,127 +43,365 @@ __device__ __forceinline__ float sin_reduced(float x) {
   return __builtin_amdgcn_sinf(r * 0.15915494309189535f);
 }
 
-template <int HF, typename TS>
-__global__ void __launch_bounds__(64 * kSynthWaves) siren_synth(SynthArgs a) {
-  constexpr int OT = HF / 32;  // 32-unit tiles of the hidden width
-  const int lane = threadIdx.x & 63, g = lane >> 5, pl = lane & 31;
-  const int64_t tiles = (a.npos + 31) / 32;
-  const int64_t tile = (int64_t)blockIdx.x * kSynthWaves + (threadIdx.x >> 6);
-  if (tile >= tiles * a.nb) return;  // uniform across the wave
-  const int64_t b = tile / tiles;
-  const int64_t p = (tile - b * tiles) * 32 + pl;
-  const bool valid = p < a.npos;
+// LDS layout (floats).  A parameter block at 0: omega0 [HF], W1 [3][HF] (rows
+// past N zero), bias [J][HF] (zero without biases).  Then the matrices,
+// transposed (row = output unit or channel, row stride HF + 4 floats: the pad
+// spreads consecutive rows over the banks).  With every weight resident:
+// W_2 .. W_J back to back (HF rows each), then Wout (ldo rows, zero past the
+// last channel) and the window exponents q [3][ldo]; streamed, one region
+// that holds one hidden matrix or a chunk of ldo = cc output channels at a
+// time.  The window exponent of channel c on axis d is q[d][c] s_d, with
+// s_d = r_d^2 and q = -log2(e) / (2 sigma^2) for the Gaussian, s_d = |r_d|
+// and q = -log2(e) alpha for the exponential, so that
+// w = 2^(sum_d q[d][c] s_d).
+__device__ __forceinline__ int par_floats(int HF, int J) { return (4 + J) * HF; }
 
-  // coordinates of grid point p (last axis fastest)
-  float r[3] = {0.f, 0.f, 0.f};
-  {
-    int64_t q = valid ? p : 0;
-    for (int d = a.nd - 1; d >= 0; --d) {
-      const int64_t i = q % a.KL[d];
-      q /= a.KL[d];
-      const int64_t L = a.Lc[d];
-      int64_t disp = i;
-      if (a.mode == 2) disp = i - (L - 1);
-      else if (a.mode == 1 && i > L / 2) disp = i - L;
-      r[d] = L > 1 ? (float)disp / (float)(L - 1) : 0.f;
+__device__ void stage_params(const SynthArgs& a, float* lds, int HF) {
+  for (int i = threadIdx.x; i < par_floats(HF, a.J); i += kThreads) {
+    float v = 0.f;
+    if (i < HF) v = a.omega0[i];
+    else if (i < 4 * HF) {
+      const int d = i / HF - 1;
+      if (d < a.nd) v = a.W1[d * HF + i % HF];
+    } else if (a.bias) {
+      v = a.bias[i - 4 * HF];
+    }
+    lds[i] = v;
+  }
+}
+
+// Staging: wave w copies rows w, w + 8, ... of a matrix for 64 consecutive
+// output columns at a time, one column per lane: global reads coalesced, no
+// division, HF / 8 loads in flight per lane before its LDS stores.
+// W_j [k][o] -> dst[o][k]
+template <int HF>
+__device__ void stage_hidden(const SynthArgs& a, float* dst, int j) {
+  const float* W = a.Wh + (int64_t)(j - 1) * HF * HF;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int o0 = 0; o0 < HF; o0 += 64) {
+    const int o = o0 + lane;
+    if (o < HF) {
+      float v[HF / kSynthWaves];
+#pragma unroll
+      for (int kk = 0; kk < HF / kSynthWaves; ++kk) v[kk] = W[(w + kSynthWaves * kk) * HF + o];
+#pragma unroll
+      for (int kk = 0; kk < HF / kSynthWaves; ++kk) dst[o * (HF + 4) + w + kSynthWaves * kk] = v[kk];
     }
   }
-  const float* gam = a.gamma ? a.gamma + b * a.J * HF : nullptr;
-  const float* bet = a.beta ? a.beta + b * a.J * HF : nullptr;
+}
 
-  // layer 1 straight into the operand layout
-  float h[OT][16];
+// window exponents of channels c0 .. c0 + n - 1 -> q[3][ld] (zero past n)
+__device__ void stage_q(const SynthArgs& a, float* q, int c0, int n, int ld) {
+  const int C = a.C;
+  for (int i = threadIdx.x; i < 3 * ld; i += kThreads) {
+    const int d = i / ld, c = i - d * ld;
+    float v = 0.f;
+    if (c < n && d < a.nd) {
+      if (a.wkind == 0) {
+        const float sg = a.win[d * C + c0 + c];
+        v = -0.5f * kLog2e / (sg * sg);
+      } else {
+        v = -kLog2e * a.win[c0 + c];
+      }
+    }
+    q[i] = v;
+  }
+}
+
+// Wout[:, c0 : c0 + n] -> dst[c][k] for c < ld (ld a multiple of 64; rows
+// past n zero), then q[3][ld]
+template <int HF>
+__device__ void stage_out(const SynthArgs& a, float* dst, int c0, int n, int ld) {
+  const int C = a.C;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int cb = 0; cb < ld; cb += 64) {
+    const int c = cb + lane;
+    const bool in = c < n;
+    const float* src = a.Wout + c0 + (in ? c : 0);
+    float v[HF / kSynthWaves];
 #pragma unroll
-  for (int t = 0; t < OT; ++t)
+    for (int kk = 0; kk < HF / kSynthWaves; ++kk) v[kk] = in ? src[(int64_t)(w + kSynthWaves * kk) * C] : 0.f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int o = t * 32 + tile_unit(e, g);
-      float s = 0.f;
-      for (int d = 0; d < a.nd; ++d) s = fmaf(r[d], a.W1[d * HF + o], s);
-      s = fmaf(a.omega0[o], s, a.bias ? a.bias[o] : 0.f);
-      float v = sin_reduced(s);
-      if (gam) v = fmaf(gam[o], v, bet[o]);
-      h[t][e] = v;
+    for (int kk = 0; kk < HF / kSynthWaves; ++kk) dst[c * (HF + 4) + w + kSynthWaves * kk] = v[kk];
+  }
+  stage_q(a, dst + ld * (HF + 4), c0, n, ld);
+}
+
+// FiLM scale and shift of layer j for this lane's units t * 16 + 4 g + r,
+// from src = gamma and beta of every sample, interleaved per (b, j) as
+// [gamma row, beta row] (LDS copy) or from the caller's arrays
+template <int HF, bool FILM>
+__device__ __forceinline__ void film_load(const SynthArgs& a, const float* film_lds, int64_t b, int j, int g,
+                                          v4f (&gm)[HF / 16], v4f (&bt)[HF / 16]) {
+  if constexpr (FILM) {
+    const float *G, *Bt;
+    if (film_lds) {
+      G = film_lds + (b * a.J + j) * 2 * HF + 4 * g;
+      Bt = G + HF;
+    } else {
+      G = a.gamma + (b * a.J + j) * HF + 4 * g;
+      Bt = a.beta + (b * a.J + j) * HF + 4 * g;
+    }
+#pragma unroll
+    for (int t = 0; t < HF / 16; ++t) {
+      gm[t] = *reinterpret_cast<const v4f*>(G + t * 16);
+      bt[t] = *reinterpret_cast<const v4f*>(Bt + t * 16);
+    }
+  }
+}
+
+// NT output tiles of 16 rows (weights in LDS at rows[i] = this lane's row of
+// tile i): acc[i] = sum over the hidden width of weight x activation; the
+// products of the NT tiles alternate, the operands of one 16-unit block are
+// read one block ahead
+template <int HF, int NT>
+__device__ __forceinline__ void chains(const float* const (&rows)[NT], const v4f (&h)[HF / 16], int g, v4f (&acc)[NT]) {
+  v4f w[2][NT];
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    acc[i] = v4f{};
+    w[0][i] = *reinterpret_cast<const v4f*>(rows[i] + 4 * g);
+  }
+#pragma unroll
+  for (int kt = 0; kt < HF / 16; ++kt) {
+    if (kt + 1 < HF / 16)
+#pragma unroll
+      for (int i = 0; i < NT; ++i) w[(kt + 1) & 1][i] = *reinterpret_cast<const v4f*>(rows[i] + (kt + 1) * 16 + 4 * g);
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int i = 0; i < NT; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[kt & 1][i][r], h[kt][r], acc[i], 0, 0, 0);
+  }
+}
+
+// window and store of one 16-channel tile: channels cb + 4 g + r of point p
+// (CHECK: skip channels at or past n; tbase points at channel c0)
+template <typename TS, bool CHECK>
+__device__ __forceinline__ void store_tile(const v4f& acc, TS* tbase, int64_t npos, int64_t p, const float* q, int ld,
+                                           int cb, int n, int g, const float (&sd)[3]) {
+  const int cr = cb + 4 * g;
+  const v4f q0 = *reinterpret_cast<const v4f*>(q + cr);
+  const v4f q1 = *reinterpret_cast<const v4f*>(q + ld + cr);
+  const v4f q2 = *reinterpret_cast<const v4f*>(q + 2 * ld + cr);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (!CHECK || cr + r < n) {
+      const float ex = fmaf(q2[r], sd[2], fmaf(q1[r], sd[1], q0[r] * sd[0]));
+      st1(tbase + (int64_t)(cr + r) * npos + p, __builtin_amdgcn_exp2f(ex) * acc[r]);
+    }
+  }
+}
+
+template <int HF, bool FILM, typename TS>
+__global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
+  constexpr int OT = HF / 16;  // 16-unit blocks of the hidden width
+  constexpr int LDW = HF + 4;  // row stride of a staged matrix
+  constexpr int NT = HF >= 128 ? 2 : 4;  // output tiles per group
+  extern __shared__ float lds[];
+  const int lane = threadIdx.x & 63, g = lane >> 4, pl = lane & 15;
+  const int wave = threadIdx.x >> 6;
+  const int J = a.J, C = a.C;
+  const int64_t tiles = (a.npos + 15) / 16;
+  const int64_t total = tiles * a.nb;
+  const int M0 = (par_floats(HF, J) + 3) & ~3;
+  const bool resident = a.resident;
+  const int ldo = resident ? (C + 63) & ~63 : a.cc;  // staged output channels
+  const int out_off = M0 + (resident ? (J - 1) * HF * LDW : 0);
+
+  // FiLM of every sample in LDS when the launch reserved room for it
+  const float* film_lds = nullptr;
+  if (FILM && a.film_lds) {
+    float* f = lds + out_off + (resident ? ldo * (LDW + 3) : a.stream_floats);
+    for (int i = threadIdx.x; i < (int)(a.nb * J * HF); i += kThreads) {
+      const int row = i / HF, u = i - row * HF;  // row = b * J + j
+      f[row * 2 * HF + u] = a.gamma[i];
+      f[row * 2 * HF + HF + u] = a.beta[i];
+    }
+    film_lds = f;
+  }
+  stage_params(a, lds, HF);
+  if (resident) {
+    for (int j = 1; j < J; ++j) stage_hidden<HF>(a, lds + M0 + (j - 1) * HF * LDW, j);
+    stage_out<HF>(a, lds + out_off, 0, C, ldo);
+  }
+  __syncthreads();
+
+  for (int64_t base = (int64_t)blockIdx.x * kSynthWaves; base < total; base += (int64_t)gridDim.x * kSynthWaves) {
+    const int64_t tile = base + wave;
+    const bool live = tile < total;  // uniform across the wave
+    const int64_t b = live ? tile / tiles : 0;
+    const int64_t p0 = (tile - b * tiles) * 16;  // first point of the tile
+    const int64_t p = p0 + pl;
+    const bool valid = live && p < a.npos;
+
+    // coordinates of grid point p (last axis fastest)
+    float r[3] = {0.f, 0.f, 0.f};
+    {
+      int64_t q = valid ? p : 0;
+      for (int d = a.nd - 1; d >= 0; --d) {
+        const int64_t i = q % a.KL[d];
+        q /= a.KL[d];
+        const int64_t L = a.Lc[d];
+        int64_t disp = i;
+        if (a.mode == 2) disp = i - (L - 1);
+        else if (a.mode == 1 && i > L / 2) disp = i - L;
+        r[d] = L > 1 ? (float)disp / (float)(L - 1) : 0.f;
+      }
     }
 
-  // hidden layers 2 .. J on the matrix cores
-  for (int j = 1; j < a.J; ++j) {
-    const float* W = a.Wh + (int64_t)(j - 1) * HF * HF;
-    v16f acc[OT];
+    // layer 1 straight into the operand layout: h[t][r] is unit t * 16 +
+    // 4 g + r of point p
+    v4f h[OT];
+    if (live) {
+      v4f gm[OT], bt[OT];
+      film_load<HF, FILM>(a, film_lds, b, 0, g, gm, bt);
 #pragma unroll
-    for (int t = 0; t < OT; ++t) acc[t] = v16f{};
+      for (int t = 0; t < OT; ++t)
 #pragma unroll
-    for (int kt = 0; kt < OT; ++kt)
+        for (int k = 0; k < 4; ++k) {
+          const int o = t * 16 + 4 * g + k;
+          float s = r[0] * lds[HF + o];
+          s = fmaf(r[1], lds[2 * HF + o], s);
+          s = fmaf(r[2], lds[3 * HF + o], s);
+          float v = sin_reduced(fmaf(lds[o], s, lds[4 * HF + o]));
+          if constexpr (FILM) v = fmaf(gm[t][k], v, bt[t][k]);
+          h[t][k] = v;
+        }
+    }
+
+    // hidden layers 2 .. J on the matrix cores, weights from LDS
+    for (int j = 1; j < J; ++j) {
+      const float* W = lds + M0 + (resident ? (j - 1) * HF * LDW : 0);
+      if (!resident) {
+        __syncthreads();
+        stage_hidden<HF>(a, lds + M0, j);
+        __syncthreads();
+      }
+      if (live) {
+        v4f gm[OT], bt[OT];
+        film_load<HF, FILM>(a, film_lds, b, j, g, gm, bt);
+        constexpr int NH = OT < NT ? OT : NT;  // hidden tiles per group
+        v4f acc[OT];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float* Wk = W + (kt * 32 + tile_unit(e, g)) * HF + pl;
+        for (int t0 = 0; t0 < OT; t0 += NH) {
+          const float* rows[NH];
+          v4f part[NH];
+#pragma unroll
+          for (int i = 0; i < NH; ++i) rows[i] = W + ((t0 + i) * 16 + pl) * LDW;
+          chains<HF, NH>(rows, h, g, part);
+#pragma unroll
+          for (int i = 0; i < NH; ++i) acc[t0 + i] = part[i];
+        }
+        const float* bias = lds + (4 + j) * HF;
 #pragma unroll
         for (int t = 0; t < OT; ++t)
-          acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(Wk[t * 32], h[kt][e], acc[t], 0, 0, 0);
-      }
 #pragma unroll
-    for (int t = 0; t < OT; ++t)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int o = t * 32 + tile_unit(e, g);
-        float v = sin_reduced(acc[t][e] + (a.bias ? a.bias[j * HF + o] : 0.f));
-        if (gam) v = fmaf(gam[j * HF + o], v, bet[j * HF + o]);
-        h[t][e] = v;
-      }
-  }
-
-  // output projection, window, store: 32 channels per step
-  const int C = a.C;
-  TS* out = reinterpret_cast<TS*>(a.k) + b * C * a.npos;
-  float rr[3], ra = 0.f;
-  for (int d = 0; d < 3; ++d) {
-    rr[d] = r[d] * r[d];
-    ra += fabsf(r[d]);
-  }
-  for (int c0 = 0; c0 < C; c0 += 32) {
-    const bool cok = c0 + pl < C;
-    const float* Wc = a.Wout + c0 + pl;
-    v16f acc = v16f{};
-#pragma unroll
-    for (int kt = 0; kt < OT; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float w = cok ? Wc[(int64_t)(kt * 32 + tile_unit(e, g)) * C] : 0.f;
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(w, h[kt][e], acc, 0, 0, 0);
-      }
-    if (valid) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int c = c0 + tile_unit(e, g);
-        if (c < C) {
-          float ex;
-          if (a.wkind == 0) {
-            ex = 0.f;
-            for (int d = 0; d < a.nd; ++d) {
-              const float s = a.win[d * C + c];
-              ex = fmaf(rr[d], __fdividef(-0.5f, s * s), ex);
-            }
-          } else {
-            ex = -a.win[c] * ra;
+          for (int k = 0; k < 4; ++k) {
+            float v = sin_reduced(acc[t][k] + bias[t * 16 + 4 * g + k]);
+            if constexpr (FILM) v = fmaf(gm[t][k], v, bt[t][k]);
+            h[t][k] = v;
           }
-          st1(out + (int64_t)c * a.npos + p, __expf(ex) * acc[e]);
+      }
+    }
+
+    // output projection, window, store: chunks of staged channels, NT
+    // 16-channel tiles per group (rows past the last channel are zero, so
+    // every tile of a group exists)
+    TS* out = reinterpret_cast<TS*>(a.k) + b * C * a.npos;
+    float sd[3];
+#pragma unroll
+    for (int d = 0; d < 3; ++d) sd[d] = a.wkind == 0 ? r[d] * r[d] : fabsf(r[d]);
+    for (int c0 = 0; c0 < C; c0 += ldo) {
+      const int n = min(ldo, C - c0);
+      if (!resident) {
+        __syncthreads();
+        stage_out<HF>(a, lds + M0, c0, n, ldo);
+        __syncthreads();
+      }
+      if (!live) continue;
+      const float* Wo = lds + out_off;
+      const float* q = Wo + ldo * LDW;
+      TS* cbase = out + (int64_t)c0 * a.npos;
+      const bool full = p0 + 16 <= a.npos && n % (16 * NT) == 0;  // uniform
+      for (int ct = 0; ct < n; ct += 16 * NT) {
+        const float* rows[NT];
+#pragma unroll
+        for (int i = 0; i < NT; ++i) rows[i] = Wo + (ct + 16 * i + pl) * LDW;
+        v4f acc[NT];
+        chains<HF, NT>(rows, h, g, acc);
+        if (full) {
+#pragma unroll
+          for (int i = 0; i < NT; ++i) store_tile<TS, false>(acc[i], cbase, a.npos, p, q, ldo, ct + 16 * i, n, g, sd);
+        } else if (valid) {
+#pragma unroll
+          for (int i = 0; i < NT; ++i) store_tile<TS, true>(acc[i], cbase, a.npos, p, q, ldo, ct + 16 * i, n, g, sd);
         }
       }
     }
   }
 }
 
-template <typename TS>
-hipError_t launch_typed(const SynthArgs& a, hipStream_t s) {
-  const int64_t waves = (a.npos + 31) / 32 * a.nb;
-  const dim3 grid((unsigned)((waves + kSynthWaves - 1) / kSynthWaves)), block(64 * kSynthWaves);
+// LDS floats of a launch: the parameter block plus either every weight
+// (resident) or one streamed region, plus the FiLM block when kept in LDS
+size_t lds_floats(const SynthArgs& a, bool resident) {
+  const size_t H = a.hidden, J = a.J, C = ((size_t)a.C + 63) & ~size_t(63), LDW = H + 4;
+  const size_t par = ((4 + J) * H + 3) & ~size_t(3);
+  const size_t film = a.film_lds ? 2 * (size_t)a.nb * J * H : 0;
+  if (resident) return par + (J - 1) * H * LDW + (LDW + 3) * C + film;
+  return par + (size_t)a.stream_floats + film;
+}
+
+constexpr size_t kLdsLimit = 160 * 1024;
+
+// one launch; the kernel's dynamic LDS limit is raised to the CU's 160 KB
+// once per kernel
+template <typename K>
+hipError_t launch_one(K kernel, int64_t grid, dim3 block, size_t bytes, hipStream_t s, const SynthArgs& a) {
+  static std::once_flag once;
+  static hipError_t attr = hipSuccess;
+  std::call_once(once, [&] {
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)kLdsLimit);
+  });
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)grid), block, bytes, s, a);
+  return hipGetLastError();
+}
+
+template <typename TS, bool FILM>
+hipError_t launch_film(SynthArgs a, hipStream_t s) {
+  // stream the weights when they do not all fit next to each other
+  a.cc = 64 * std::max(1, (int)(16384 / a.hidden / 64));  // output channels per streamed chunk
+  const int LDW = a.hidden + 4;
+  a.stream_floats = (int)std::max(a.hidden * LDW, (LDW + 3) * a.cc);
+  // FiLM rows of every sample in LDS when they take at most 32 KiB
+  a.film_lds = FILM && 2 * a.nb * a.J * a.hidden * 4 <= 32 * 1024;
+  const size_t res_bytes = lds_floats(a, true) * 4;
+  a.resident = res_bytes <= kLdsLimit - 8 * 1024;
+  const size_t bytes = lds_floats(a, a.resident) * 4;
+  static int ncu = 0;
+  if (ncu == 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                  hipSuccess || ncu <= 0)
+      ncu = 256;
+  }
+  const int per_cu = std::max<int>(1, (int)(kLdsLimit / bytes));
+  const int64_t groups = ((a.npos + 15) / 16 * a.nb + kSynthWaves - 1) / kSynthWaves;
+  const int64_t grid = std::min<int64_t>(groups, (int64_t)ncu * std::min(per_cu, 2));
+  const dim3 block(64 * kSynthWaves);
   switch (a.hidden) {
-    case 32: hipLaunchKernelGGL((siren_synth<32, TS>), grid, block, 0, s, a); break;
-    case 64: hipLaunchKernelGGL((siren_synth<64, TS>), grid, block, 0, s, a); break;
-    case 128: hipLaunchKernelGGL((siren_synth<128, TS>), grid, block, 0, s, a); break;
+    case 32: return launch_one(siren_synth<32, FILM, TS>, grid, block, bytes, s, a);
+    case 64: return launch_one(siren_synth<64, FILM, TS>, grid, block, bytes, s, a);
+    case 128: return launch_one(siren_synth<128, FILM, TS>, grid, block, bytes, s, a);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+}
+
+template <typename TS>
+hipError_t launch_typed(const SynthArgs& a, hipStream_t s) {
+  return a.gamma ? launch_film<TS, true>(a, s) : launch_film<TS, false>(a, s);
 }
 
 }  // namespace

@@ -269,6 +269,8 @@ def test_synth_validation(L):
     assert b"gamma and beta" in L.hyenand_last_error()
     assert synth(L, ptrs=base[:1] + [base[1] + 2] + base[2:]) == H.ERR_INVALID_ARGUMENT  # W1 misaligned
     assert b"W1" in L.hyenand_last_error()
+    assert synth(L, layers=2, ptrs=base[:2] + [base[2] + 4] + base[3:]) == H.ERR_INVALID_ARGUMENT  # Wh: 16 bytes
+    assert b"Wh is not 16-byte aligned" in L.hyenand_last_error()
     assert synth(L, dtype=1, k=FAKE + (9 << 36) + 1) == H.ERR_INVALID_ARGUMENT  # bf16 k misaligned
     # k (2 x 4 x 16 fp32 = 512 bytes) running into Wout
     assert synth(L, k=base[6] - 256) == H.ERR_INVALID_ARGUMENT

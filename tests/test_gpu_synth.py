@@ -70,6 +70,13 @@ def test_channel_counts(C):
     _check("channels", (2, C, 9, 11), 32, 2, "linear", "f32", C)
 
 
+@pytest.mark.parametrize("hidden,C", [(64, 1200), (32, 3000), (128, 300)])
+def test_streamed_weights(hidden, C):
+    """Weights too large to stay in LDS together: hidden matrices and chunks
+    of output channels are staged one at a time (the last chunk ragged)."""
+    _check("streamed", (2, C, 8, 8), hidden, 3, "centered", "f32", C + hidden)
+
+
 def test_unmodulated_is_shared():
     _check("shared", (4, 16, 30, 17), 64, 3, "centered", "f32", 9, modulated=False)
 
