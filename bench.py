@@ -321,6 +321,7 @@ def bench_synth(args, w, inp):
     synth_s, _ = timed([synth], args.steps)
     conv_s, _ = timed([conv], args.steps)
     both_s, both_wall = timed([synth, conv], args.steps)
+    copy_calibration(args, dev)
     flops = synth_flops(w, SYNTH_HIDDEN, SYNTH_LAYERS)
     tflops = flops / synth_s / 1e12
     parity = None
@@ -352,6 +353,18 @@ def bench_synth(args, w, inp):
         "cpu_baseline": None, "parity_rel_l2": parity, "kernel_source_hash": kernel_source_hash(),
     }
     print(json.dumps(out))
+
+
+def copy_calibration(args, dev):
+    """One plain device copy of --copy-calibration-mb MiB, whose FETCH_SIZE and
+    WRITE_SIZE counters scale the library's own to HBM bytes."""
+    import torch
+    if args.copy_calibration_mb > 0:
+        src = torch.ones(args.copy_calibration_mb << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
 
 def to_device(arr, dtype):
@@ -517,12 +530,7 @@ def main():
         "kernel_plan": plan, "launches_per_call": "1" if plan.startswith("fused") else "3-5 (chunked)",
         "avg_call_us": round(avg_call_s * 1e6, 3)})
 
-    if args.copy_calibration_mb > 0:
-        src = torch.ones(args.copy_calibration_mb << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+    copy_calibration(args, dev)
 
     # measured stream peak: a 1 GiB device-to-device copy (read + write), best of 5
     stream_gbs = None

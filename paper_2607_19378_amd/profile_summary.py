@@ -6,7 +6,9 @@
 
 The three directories hold the CSV output of three rocprofv3 runs of one
 bench.py command: ``--kernel-trace --stats``, ``--pmc FETCH_SIZE`` and
-``--pmc WRITE_SIZE``.  N is the number of hyenand_fftconv calls the command
+``--pmc WRITE_SIZE``.  With ``--synth`` the runs are of ``bench.py --synth``
+and the summary, ``profiles/siren_synth_<workload>.md``, covers the kernel
+synthesis kernel.  N is the number of hyenand_fftconv calls the command
 made (bench.py: warmup + steps).  Writes
 
 * ``profiles/<plan>_<workload>.md``: per-kernel average durations, HBM bytes
@@ -82,6 +84,68 @@ def counter_per_call(rows, counter: str, calls: int):
     return op / calls, copy, {k: v / calls for k, v in per_kernel.items()}
 
 
+def synth_summary(a, W, source_hash):
+    """profiles/siren_synth_<workload>.md from rocprofv3 runs of
+    ``bench.py --synth``: the synthesis kernel's duration, HBM bytes and
+    matrix-core rate, beside the convolution kernels of the same run."""
+    sys.path.insert(0, ROOT)
+    import bench
+    w = W.WORKLOADS[a.workload]
+    stats = [r for r in _rows(a.trace, "_kernel_stats.csv") if "hyenand" in r["Name"]]
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    syn = [r for r in stats if "siren_synth" in r["Name"]]
+    if not syn:
+        raise SystemExit("no siren_synth dispatches in the trace")
+    avg_ns = float(syn[0]["AverageNs"])
+    flops = bench.synth_flops(w, bench.SYNTH_HIDDEN, bench.SYNTH_LAYERS)
+    tf = flops / (avg_ns * 1e-9) / 1e12
+    npos = int(np.prod(w.kernel_shape[2:]))
+    k_bytes = w.B * w.C * npos * w.storage_bytes
+
+    def per_dispatch(rows, counter):
+        tot, n, copy = 0.0, set(), 0.0
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            if "siren_synth" in r["Kernel_Name"]:
+                tot += float(r["Counter_Value"])
+                n.add(r["Dispatch_Id"])
+            elif COPY_KERNEL in r["Kernel_Name"]:
+                copy = max(copy, float(r["Counter_Value"]))
+        return tot / max(1, len(n)), copy
+
+    f_d, f_copy = per_dispatch(_rows(a.fetch, "_counter_collection.csv"), "FETCH_SIZE")
+    w_d, w_copy = per_dispatch(_rows(a.write, "_counter_collection.csv"), "WRITE_SIZE")
+    if f_copy <= 0 or w_copy <= 0:
+        raise SystemExit("copy calibration dispatch not found in the counter runs")
+    copy_kib = a.copy_mib * 1024.0
+    fb = f_d * 1024.0 * copy_kib / f_copy
+    wb = w_d * 1024.0 * copy_kib / w_copy
+    lines = [f"# siren_synth on {w.name}", "",
+             f"Kernel synthesis (FiLM-modulated SIREN, Hf = {bench.SYNTH_HIDDEN}, J = {bench.SYNTH_LAYERS}, "
+             f"Gaussian window) on the kernel grid of {w.description}: {w.B} x {w.C} x {npos} points.  "
+             f"Kernel source hash `{source_hash()}`.", "",
+             "Commands (run from /tmp with TMPDIR=/tmp on the MI355X box):", "",
+             "```", a.cmd_trace, a.cmd_fetch, a.cmd_write, "```", "",
+             "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",
+             "| kernel | dispatches | avg us | min us | max us |", "|---|---:|---:|---:|---:|"]
+    for r in stats:
+        lines.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    lines += ["", f"siren_synth: {flops / 1e9:.3f} GFLOP of matrix-core multiply-adds per call in "
+                  f"{avg_ns / 1e3:.2f} us = {tf:.1f} TFLOP/s, {100 * tf / bench.MFMA_F32_PEAK_TFLOPS:.1f}% of the "
+                  f"{bench.MFMA_F32_PEAK_TFLOPS} TFLOP/s fp32 matrix peak.", "",
+              "## HBM traffic per siren_synth dispatch (rocprofv3 --pmc)", "",
+              f"Copy calibration: {a.copy_mib} MiB device copy read {f_copy:.1f} KiB (FETCH_SIZE) and wrote "
+              f"{w_copy:.1f} KiB (WRITE_SIZE).", "",
+              f"Read {fb / 1e6:.2f} MB (the weights, by every workgroup, mostly from the caches), write "
+              f"{wb / 1e6:.2f} MB; the kernel tensor is {k_bytes / 1e6:.2f} MB (written once).", ""]
+    md = os.path.join(a.out, f"siren_synth_{w.name}.md")
+    with open(md, "w") as fh:
+        fh.write("\n".join(lines))
+    print(md)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", required=True)
@@ -94,12 +158,16 @@ def main(argv=None):
     ap.add_argument("--cmd-fetch", required=True)
     ap.add_argument("--cmd-write", required=True)
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
+    ap.add_argument("--synth", action="store_true", help="runs of bench.py --synth: summarise the synthesis kernel")
     a = ap.parse_args(argv)
 
     sys.path.insert(0, ROOT)
     from paper_2607_19378_amd import workloads as W
     from paper_2607_19378_amd.build import source_hash
     from paper_2607_19378_amd import hyenand as H
+    if a.synth:
+        synth_summary(a, W, source_hash)
+        return
 
     w = W.WORKLOADS[a.workload]
     plan = H.plan_name(w.shape, w.pad_mode, w.dtype)
