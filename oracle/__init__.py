@@ -19,6 +19,8 @@ The arithmetic lives in ``oracle.c`` (plain C, IEEE double):
 * :func:`kernel_synth` evaluates the implicit, input-dependent kernel K(x) of
   sections 3.2.1-3.2.2 (a SIREN over the grid coordinates, FiLM-modulated per
   sample, times a per-channel window) on a convolution's kernel grid;
+* :func:`modal_filter` evaluates the implicit modal filter of order M (the
+  appendix "Filter Generation"): k[c, t] = Re sum_m R[c, m] lambda[c, m]^t;
 * :func:`backward_direct` / :func:`backward_fft` give the gradients of a
   scalar loss through y (gx1, gx2, gv, gk, gD for a given gy = dLoss/dy), as
   explicit sums and through the FFT.
@@ -81,9 +83,10 @@ def lib():
                                                         _i64p, ctypes.c_int, ctypes.c_int]
             L.oracle_kernel_synth.argtypes = [_f64p] * 8 + [ctypes.c_int, _f64p, ctypes.c_int, _i64p,
                                                             ctypes.c_int, ctypes.c_int, ctypes.c_int]
+            L.oracle_modal_filter.argtypes = [_f64p] * 5 + [ctypes.c_int64] * 3
             for f in (L.oracle_direct, L.oracle_fft, L.oracle_direct_points, L.oracle_fft1d,
                       L.oracle_backward_direct, L.oracle_backward_fft, L.oracle_operator,
-                      L.oracle_kernel_synth):
+                      L.oracle_kernel_synth, L.oracle_modal_filter):
                 f.restype = ctypes.c_int
             _lib = L
         return _lib
@@ -293,3 +296,18 @@ def kernel_synth(shape, omega0, W1, Wh, Wout, window, gamma=None, beta=None, bia
     if rc != 0:
         raise RuntimeError(f"oracle returned {rc}")
     return out
+
+
+def modal_filter(log_mag, angle, res_re, res_im, L):
+    """k [C, L] with k[c, t] = Re sum_m (res_re + i res_im)[c, m] *
+    exp((log_mag + i angle)[c, m] * t): a sum of M damped complex exponentials
+    per channel.  Parameters are [C, M]."""
+    arrs = [np.ascontiguousarray(x, dtype=np.float64) for x in (log_mag, angle, res_re, res_im)]
+    if arrs[0].ndim != 2 or any(x.shape != arrs[0].shape for x in arrs):
+        raise ValueError("log_mag, angle, res_re and res_im must share one [C, M] shape")
+    C, M = arrs[0].shape
+    k = np.zeros((C, int(L)), dtype=np.float64)
+    rc = lib().oracle_modal_filter(*[_ptr(x) for x in arrs], _ptr(k), C, M, int(L))
+    if rc != 0:
+        raise RuntimeError(f"oracle returned {rc}")
+    return k

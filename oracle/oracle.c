@@ -766,7 +766,7 @@ int oracle_backward_fft(const double *x1, const double *x2, const double *v, con
     return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 1);
 }
 
-int oracle_version(void) { return 5; }
+int oracle_version(void) { return 6; }
 
 /* ------------------------------------------------------------------------- */
 /* HyenaND operator: normalised prologue, long convolution, normalised       */
@@ -961,5 +961,39 @@ int oracle_kernel_synth(const double *omega0, const double *W1, const double *Wh
         }
     free(h);
     free(t);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Modal filter generation                                                   */
+/* ------------------------------------------------------------------------- */
+/*
+ * oracle_modal_filter -- the implicit modal filter of order M of the long
+ * convolution layers (appendix "Filter Generation"): per channel c a sum of
+ * M damped complex exponentials, taken as its real part,
+ *
+ *   k[c, t] = Re sum_m R[c, m] lambda[c, m]^t,   t = 0 .. L - 1,
+ *   lambda = exp(a + i theta),  R = re + i im,
+ *
+ * so k[c, t] = sum_m exp(t a) (re cos(t theta) - im sin(t theta)).  The
+ * paper gives the order (16) and the form only by name; this is the modal
+ * (sum of poles and residues) form with the pole given by its log-magnitude
+ * a and angle theta.  a, theta, re, im are [C, M]; k is [C, L].  t * theta
+ * is formed in double, which holds the product of an fp32 angle and t < 2^29
+ * exactly.
+ */
+int oracle_modal_filter(const double *a, const double *theta, const double *re, const double *im, double *k,
+                        int64_t C, int64_t M, int64_t L) {
+    if (!a || !theta || !re || !im || !k || C < 1 || M < 1 || L < 1) return 1;
+    for (int64_t c = 0; c < C; ++c)
+        for (int64_t t = 0; t < L; ++t) {
+            double s = 0.0;
+            for (int64_t m = 0; m < M; ++m) {
+                const int64_t i = c * M + m;
+                const double ph = (double)t * theta[i];
+                s += exp((double)t * a[i]) * (re[i] * cos(ph) - im[i] * sin(ph));
+            }
+            k[c * L + t] = s;
+        }
     return 0;
 }
