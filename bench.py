@@ -355,6 +355,82 @@ def bench_synth(args, w, inp):
     print(json.dumps(out))
 
 
+MODAL_ORDER = 16
+
+
+def bench_modal(args, w, inp):
+    """Time hyenand_modal_filter (order-16 modal filters, one per channel, over
+    the workload's 1D length) alone and followed by the one-kernel-per-channel
+    convolution that consumes it; prints one JSON line."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    if len(w.grid) != 1 or w.pad_mode != W.LINEAR:
+        raise SystemExit("--modal takes a 1D linear workload")
+    dev = torch.device("cuda:0")
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    L = w.grid[0]
+    p = W.modal_params(w.seed + 31, w.C, MODAL_ORDER, L)
+    d = [torch.from_numpy(p[n]).to(dev) for n in ("log_mag", "angle", "res_re", "res_im")]
+    k = torch.empty((w.C, L), dtype=tdt, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    gen = H.PreparedModal(k, *d, stream=stream)
+    x1, x2, v, D = (to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.D))
+    y = torch.empty_like(x1)
+    ws_bytes = H.workspace_size(w.shape, w.pad_mode, w.dtype)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    conv = H.Prepared(y, x1, x2, v, k, D, w.pad_mode, ws, stream, shared_k=True)
+
+    def timed(fns):
+        for _ in range(args.warmup):
+            for f in fns:
+                f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            for f in fns:
+                f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / args.steps, (time.perf_counter() - t0) / args.steps
+
+    gen_s, _ = timed([gen])
+    conv_s, _ = timed([conv])
+    both_s, both_wall = timed([gen, conv])
+    copy_calibration(args, dev)
+    # per point and mode: one complex product (6 flops) and one accumulation
+    flops = 7.0 * MODAL_ORDER * w.C * L
+    tflops = flops / gen_s / 1e12
+    k_bytes = k.numel() * k.element_size()
+    parity = None
+    if not args.no_parity:
+        import oracle
+        rows = [0, w.C // 2, w.C - 1]
+        ref = oracle.modal_filter(*[p[n][rows].astype(np.float64) for n in ("log_mag", "angle", "res_re", "res_im")], L)
+        got = k[rows]
+        got = (W.bf16_bits_to_f64(got.view(torch.int16).cpu().numpy().view(np.uint16)) if got.dtype == torch.bfloat16
+               else got.cpu().numpy().astype(np.float64))
+        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    out = {
+        "metric": "modal filter generation + gated 1D FFT conv GElem/s on 1 MI355X",
+        "value": round(w.elems / both_wall / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(both_wall * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded poles and residues)",
+        "config": {"workload": w.name, "pass": "modal+conv", "B": w.B, "C": w.C, "L": L, "order": MODAL_ORDER,
+                   "storage": w.dtype},
+        "roofline": {"bound": "alu", "achieved": round(tflops, 3), "peak": FP32_VALU_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / FP32_VALU_TFLOPS, 4), "traffic": None, "kernel": "modal_filter_kernel",
+                     "alg_flops_per_call": flops, "avg_call_us": round(gen_s * 1e6, 3),
+                     "k_bytes_written": k_bytes, "hbm_frac_of_k_write": round(k_bytes / gen_s / 1e9 / HBM_PEAK_GBS, 4)},
+        "modal_us": round(gen_s * 1e6, 3), "conv_us": round(conv_s * 1e6, 3),
+        "modal_then_conv_us": round(both_s * 1e6, 3),
+        "cpu_baseline": None, "parity_rel_l2_sampled_channels": parity, "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out))
+
+
 def copy_calibration(args, dev):
     """One plain device copy of --copy-calibration-mb MiB, whose FETCH_SIZE and
     WRITE_SIZE counters scale the library's own to HBM bytes."""
@@ -445,6 +521,8 @@ def main():
                     help="time the whole HyenaND operator (norms and activations around the convolution)")
     ap.add_argument("--synth", action="store_true",
                     help="time kernel synthesis (FiLM-modulated SIREN + window) alone and followed by the conv")
+    ap.add_argument("--modal", action="store_true",
+                    help="time modal filter generation (order 16, one filter per channel) alone and with the conv")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -466,6 +544,9 @@ def main():
         return
     if args.synth:
         bench_synth(args, w, inp)
+        return
+    if args.modal:
+        bench_modal(args, w, inp)
         return
     set_bytes = alg_bytes(w)
     rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))

@@ -250,6 +250,30 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
                                     int window_kind, int hidden, int layers, void* k, int ndim,
                                     const int64_t* dims, int pad_mode, int dtype, void* stream);
 
+/*
+ * hyenand_modal_filter -- the implicit long filter of order M of the appendix
+ * "Filter Generation", written as the [C, L] kernel that
+ * hyenand_fftconv_shared_k takes (one filter per channel):
+ *
+ *     k[c, t] = Re sum_{m < M} R[c, m] lambda[c, m]^t,   t = 0 .. L - 1,
+ *     lambda = exp(log_mag + i angle),  R = res_re + i res_im,
+ *
+ * i.e. sum_m exp(t log_mag) (res_re cos(t angle) - res_im sin(t angle)).
+ * The M complex terms per point are never stored.  log_mag <= 0 keeps every
+ * term bounded; a positive one grows and may overflow as the formula does.
+ * log_mag, angle, res_re, res_im : device pointers, [C, M] fp32, 4-byte
+ *   aligned; order = M in 1..256.
+ * k (output, device, `dtype`, aligned to its element size) : [C, L]; must not
+ *   overlap a parameter.  C in 1..65535, L in 1..2^29.
+ * Accuracy: each point is generated from an exact (double) phase and
+ * magnitude at most 31 fp32 steps back, so errors stay at a few fp32
+ * roundings per mode.  Validation, stream and error conventions as for
+ * hyenand_fftconv; no workspace.
+ */
+hyenand_status hyenand_modal_filter(const float* log_mag, const float* angle, const float* res_re,
+                                    const float* res_im, int order, void* k, int64_t C, int64_t L, int dtype,
+                                    void* stream);
+
 /* Static text for a status code. */
 const char* hyenand_status_string(int status);
 

@@ -726,6 +726,33 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
   return HYENAND_OK;
 }
 
-int hyenand_version(void) { return 300; }
+hyenand_status hyenand_modal_filter(const float* log_mag, const float* angle, const float* res_re,
+                                    const float* res_im, int order, void* k, int64_t C, int64_t L, int dtype,
+                                    void* stream) {
+  if (dtype != HYENAND_DTYPE_F32 && dtype != HYENAND_DTYPE_BF16)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "dtype must be 0 (f32) or 1 (bf16), got %d", dtype);
+  if (C < 1 || L < 1 || order < 1)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "C, L and order must be >= 1 (got %lld, %lld, %d)", (long long)C,
+                (long long)L, order);
+  if (order > 256 || C > 65535 || L > (int64_t(1) << 29))
+    return fail(HYENAND_ERR_UNSUPPORTED, "order <= 256, C <= 65535 and L <= 2^29 are supported");
+  const float* ptrs[] = {log_mag, angle, res_re, res_im};
+  const char* names[] = {"log_mag", "angle", "res_re", "res_im"};
+  const size_t es = dtype == HYENAND_DTYPE_BF16 ? 2 : 4;
+  if (!k) return fail(HYENAND_ERR_INVALID_ARGUMENT, "k is NULL");
+  if ((uintptr_t)k % es != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "k is not aligned to its element size");
+  for (int i = 0; i < 4; ++i) {
+    if (!ptrs[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", names[i]);
+    if ((uintptr_t)ptrs[i] % 4 != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not 4-byte aligned", names[i]);
+    if (overlaps(k, (size_t)C * L * es, ptrs[i], (size_t)C * order * 4))
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "k overlaps %s", names[i]);
+  }
+  hipError_t err = launch_modal(log_mag, angle, res_re, res_im, k, C, order, L, dtype == HYENAND_DTYPE_BF16,
+                                (hipStream_t)stream);
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
+}
+
+int hyenand_version(void) { return 400; }
 
 }  // extern "C"

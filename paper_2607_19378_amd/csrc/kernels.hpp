@@ -103,6 +103,11 @@ struct SynthArgs {
   int film_lds;   // set by launch_synth: FiLM rows of every sample kept in LDS
 };
 bool synth_hidden_supported(int hidden);
+
+// Modal filter generation (modal.hip): k[c, t] = Re sum_m R lambda^t,
+// parameters [C, M], k [C, L] in the storage type.
+hipError_t launch_modal(const float* a, const float* th, const float* re, const float* im, void* k, int64_t C,
+                        int M, int64_t L, bool bf16, hipStream_t s);
 hipError_t launch_synth(const SynthArgs& a, bool bf16, hipStream_t s);
 
 }  // namespace hyenand

@@ -23,7 +23,7 @@ EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_work
             "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
-            "hyenand_kernel_synth", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
+            "hyenand_kernel_synth", "hyenand_modal_filter", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
 
 _lock = threading.Lock()
 _lib = None
@@ -73,6 +73,9 @@ def lib() -> ctypes.CDLL:
             L.hyenand_kernel_synth.argtypes = [vp] * 8 + [ctypes.c_int] * 3 + [vp, ctypes.c_int, i64p, ctypes.c_int,
                                                                        ctypes.c_int, vp]
             L.hyenand_kernel_synth.restype = ctypes.c_int
+            L.hyenand_modal_filter.argtypes = [vp] * 4 + [ctypes.c_int, vp, ctypes.c_int64, ctypes.c_int64,
+                                                       ctypes.c_int, vp]
+            L.hyenand_modal_filter.restype = ctypes.c_int
             L.hyenand_fftconv_plan_name.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                                                     ctypes.c_char_p, ctypes.c_size_t]
             L.hyenand_fftconv_plan_name.restype = ctypes.c_int
@@ -388,4 +391,38 @@ def kernel_synth(shape, omega0, W1, Wh, Wout, window, gamma=None, beta=None, bia
     kshape = kernel_shape(shape, pad_mode, shared_k=gamma is None)
     k = torch.empty(kshape, dtype=dtype, device=omega0.device)
     PreparedSynth(k, shape, omega0, W1, Wh, Wout, window, gamma, beta, bias, window_kind, pad_mode, stream)()
+    return k
+
+
+class PreparedModal:
+    """One hyenand_modal_filter call with its arguments checked and marshalled
+    once (see Prepared): k [C, L] from the [C, M] poles and residues."""
+
+    def __init__(self, k, log_mag, angle, res_re, res_im, stream=None):
+        import torch
+        C, M = (int(x) for x in log_mag.shape)
+        for t in (log_mag, angle, res_re, res_im):
+            if not t.is_cuda or t.dtype != torch.float32 or tuple(t.shape) != (C, M) or not t.is_contiguous():
+                raise ValueError("log_mag, angle, res_re, res_im must be contiguous fp32 GPU tensors of one [C, M] shape")
+        if not k.is_cuda or k.dim() != 2 or k.shape[0] != C or not k.is_contiguous():
+            raise ValueError("k must be a contiguous [C, L] GPU tensor")
+        if stream is None:
+            stream = torch.cuda.current_stream(k.device)
+        self._fn = lib().hyenand_modal_filter
+        self._args = (_ptr(log_mag), _ptr(angle), _ptr(res_re), _ptr(res_im), M, _ptr(k), C, int(k.shape[1]),
+                      _dtype_code(k.dtype), ctypes.c_void_p(stream.cuda_stream))
+        self._keep = (k, log_mag, angle, res_re, res_im, stream)
+
+    def __call__(self) -> None:
+        status = self._fn(*self._args)
+        if status != OK:
+            _check(status)
+
+
+def modal_filter(log_mag, angle, res_re, res_im, L: int, dtype=None, stream=None):
+    """k [C, L] = Re sum_m R lambda^t (the modal long filter) with a
+    torch-allocated k of `dtype` (fp32 by default)."""
+    import torch
+    k = torch.empty((log_mag.shape[0], int(L)), dtype=dtype or torch.float32, device=log_mag.device)
+    PreparedModal(k, log_mag, angle, res_re, res_im, stream)()
     return k

@@ -392,3 +392,19 @@ def siren_params(seed: int, ndim: int, hidden: int, layers: int, C: int, B: int,
     return dict(omega0=f32(omega0), W1=f32(W1), Wh=f32(Wh) if J > 1 else None, Wout=f32(Wout),
                 window=f32(window), bias=None if b is None else f32(b), gamma=None if gamma is None else f32(gamma),
                 beta=None if beta is None else f32(beta))
+
+
+def modal_params(seed: int, C: int, M: int, L: int) -> Dict[str, np.ndarray]:
+    """Seeded fp32 poles and residues of a modal long filter of order M per
+    channel, spread the way a trained long-convolution filter bank spans its
+    context: decay rates log-uniform between one e-fold over the whole
+    length (-1/L) and over two points (-0.5), angles uniform in [0, pi),
+    residues N(0, 1 / M).  Draw order: log_mag, angle, res_re, res_im."""
+    seqs = np.random.SeedSequence(seed).spawn(4)
+    rng = [np.random.Generator(np.random.PCG64(s)) for s in seqs]
+    f32 = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    log_mag = -np.exp(rng[0].uniform(np.log(1.0 / max(L, 2)), np.log(0.5), (C, M)))
+    angle = rng[1].uniform(0.0, np.pi, (C, M))
+    re = rng[2].standard_normal((C, M)) / np.sqrt(M)
+    im = rng[3].standard_normal((C, M)) / np.sqrt(M)
+    return dict(log_mag=f32(log_mag), angle=f32(angle), res_re=f32(re), res_im=f32(im))

@@ -280,3 +280,30 @@ def test_synth_validation(L):
     assert synth(L, ptrs=nofilm, k=base[6] - 252) == H.ERR_INVALID_ARGUMENT
     # centered: the grid has 2L - 1 = 31 points, so 4 x 31 floats reach Wout from 496 bytes below it
     assert synth(L, ptrs=nofilm, mode=2, k=base[6] - 492) == H.ERR_INVALID_ARGUMENT
+
+
+def modal(L, C=4, Lt=64, order=16, dtype=0, ptrs=None, k=None):
+    """hyenand_modal_filter with fake pointers: every call here must fail
+    validation (nothing may launch)."""
+    p = ptrs or [FAKE + i * (1 << 36) for i in range(4)]
+    kp = FAKE + (9 << 36) if k is None else k
+    return L.hyenand_modal_filter(*[ctypes.c_void_p(x) if x else None for x in p], order, ctypes.c_void_p(kp) if kp else None,
+                                  C, Lt, dtype, None)
+
+
+def test_modal_validation(L):
+    base = [FAKE + i * (1 << 36) for i in range(4)]
+    assert modal(L, C=0) == H.ERR_INVALID_ARGUMENT
+    assert modal(L, Lt=0) == H.ERR_INVALID_ARGUMENT
+    assert modal(L, order=0) == H.ERR_INVALID_ARGUMENT
+    assert modal(L, order=257) == H.ERR_UNSUPPORTED
+    assert modal(L, Lt=(1 << 29) + 1) == H.ERR_UNSUPPORTED
+    assert modal(L, dtype=3) == H.ERR_INVALID_ARGUMENT
+    assert modal(L, ptrs=[base[0], 0, base[2], base[3]]) == H.ERR_INVALID_ARGUMENT
+    assert b"angle is NULL" in L.hyenand_last_error()
+    assert modal(L, k=0) == H.ERR_INVALID_ARGUMENT
+    assert modal(L, ptrs=[base[0] + 2] + base[1:]) == H.ERR_INVALID_ARGUMENT
+    assert modal(L, dtype=1, k=FAKE + (9 << 36) + 1) == H.ERR_INVALID_ARGUMENT
+    # k (4 x 64 fp32 = 1024 bytes) running into res_im
+    assert modal(L, k=base[3] - 1020) == H.ERR_INVALID_ARGUMENT
+    assert b"k overlaps res_im" in L.hyenand_last_error()

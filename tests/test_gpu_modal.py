@@ -1,0 +1,91 @@
+"""Modal filter generation on the GPU (hyenand_modal_filter: per channel a
+sum of M damped complex exponentials) against the fp64 oracle on the same
+fp32 poles and residues; and the generated filter fed to the
+one-kernel-per-channel convolution, against the oracle's filter through the
+oracle's convolution."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_19378_amd import workloads as W
+
+from gpu_util import TOL, from_device, log, rel_l2, to_device
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run(C, M, L, dtype, seed, rows=None):
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    p = W.modal_params(seed, C, M, L)
+    d = [torch.from_numpy(p[n]).cuda() for n in ("log_mag", "angle", "res_re", "res_im")]
+    k = H.modal_filter(*d, L, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32)
+    torch.cuda.synchronize()
+    got = from_device(k)
+    sel = np.arange(C) if rows is None else np.asarray(rows)
+    ref = oracle.modal_filter(*[p[n][sel].astype(np.float64) for n in ("log_mag", "angle", "res_re", "res_im")], L)
+    return got[sel], ref, k, p
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C,M,L", [(1, 1, 1), (3, 16, 63), (3, 16, 64), (5, 16, 100), (2, 64, 8193),
+                                   (16, 16, 4096), (1, 256, 777)])
+def test_modal(C, M, L, dtype):
+    got, ref, _, _ = _run(C, M, L, dtype, C * 1000 + M + L)
+    err = rel_l2(got, ref)
+    log(f"[modal] C={C} M={M} L={L} {dtype}: rel_l2={err:.3e}")
+    assert np.all(np.isfinite(got)) and err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_genomics_length(dtype):
+    """256 channels of order-16 filters over 2^20 points (the 1M-context
+    configuration); channels 0, 77, 200 and 255 against the oracle."""
+    rows = [0, 77, 200, 255]
+    got, ref, _, _ = _run(256, 16, 1 << 20, dtype, 5, rows)
+    err = rel_l2(got, ref)
+    worst = max(rel_l2(g, r) for g, r in zip(got, ref))
+    log(f"[modal] 256 x 2^20 order 16 {dtype}: rel_l2={err:.3e} worst channel {worst:.3e}")
+    assert err <= TOL[dtype] and worst <= TOL[dtype]
+
+
+def test_undamped_pole_keeps_phase():
+    """|lambda| = 1 over 2^20 points: the phase must not drift (each point is
+    at most 31 fp32 steps from an exact double-precision phase)."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    L = 1 << 20
+    a = np.zeros((2, 1), np.float32)
+    th = np.array([[2 * np.pi / 1000.0], [3.0]], np.float32)
+    one = np.ones((2, 1), np.float32)
+    d = [torch.from_numpy(x).cuda() for x in (a, th, one, 0 * one)]
+    got = from_device(H.modal_filter(*d, L))
+    ref = oracle.modal_filter(a.astype(np.float64), th.astype(np.float64), one.astype(np.float64),
+                              0 * one.astype(np.float64), L)
+    err = np.max(np.abs(got - ref))
+    log(f"[modal] undamped 2^20: max abs err {err:.3e}")
+    assert err < 2e-5
+
+
+def test_filter_through_the_convolution():
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    B, C, L = 2, 6, 4096
+    got, kref, k, _ = _run(C, 16, L, "f32", 9)
+    rng = np.random.default_rng(10)
+    x1, x2, v = (rng.standard_normal((B, C, L)).astype(np.float32) for _ in range(3))
+    D = rng.standard_normal(C).astype(np.float32)
+    y = H.fftconv(*[to_device(a, "f32") for a in (x1, x2, v)], k, to_device(D, "f32"), shared_k=True)
+    torch.cuda.synchronize()
+    kb = np.broadcast_to(kref[None], (B, C, L))
+    ref = oracle.conv_fft(x1.astype(np.float64), x2.astype(np.float64), v.astype(np.float64), kb, D.astype(np.float64))
+    err = rel_l2(from_device(y), ref)
+    log(f"[modal] through the convolution: rel_l2={err:.3e}")
+    assert err <= TOL["f32"]
