@@ -189,13 +189,12 @@ def fft1d(x, sign=-1):
 
 
 def _backward(fn, x1, x2, v, k, D, gy, pad_mode, nthreads):
-    if pad_mode == "centered":
-        raise ValueError("the backward takes pad_mode 'linear' or 'circular'")
     arrs, dims, nd = _prep(x1, x2, v, k, D, pad_mode)
     g = np.ascontiguousarray(gy, dtype=np.float64)
     if g.shape != arrs[0].shape:
         raise ValueError("gy must have the shape of y")
-    outs = [np.zeros(arrs[0].shape, dtype=np.float64) for _ in range(4)]
+    outs = [np.zeros(arrs[0].shape, dtype=np.float64) for _ in range(3)]
+    outs.append(np.zeros(arrs[3].shape, dtype=np.float64))  # gk, shaped like k
     gD = np.zeros(arrs[4].shape, dtype=np.float64)
     rc = fn(*[_ptr(a) for a in arrs], _ptr(g), *[_ptr(o) for o in outs], _ptr(gD), nd,
             dims.ctypes.data_as(_i64p), _mode(pad_mode), int(nthreads or default_threads()))
@@ -206,12 +205,16 @@ def _backward(fn, x1, x2, v, k, D, gy, pad_mode, nthreads):
 
 
 def backward_direct(x1, x2, v, k, D, gy, pad_mode="linear", nthreads=None):
-    """(gx1, gx2, gv, gk, gD) for dLoss/dy = gy, by explicit sums (any extents)."""
+    """(gx1, gx2, gv, gk, gD) for dLoss/dy = gy, by explicit sums (any extents,
+    every pad mode; centred gk has the shape of the centred k)."""
     return _backward(lib().oracle_backward_direct, x1, x2, v, k, D, gy, pad_mode, nthreads)
 
 
 def backward_fft(x1, x2, v, k, D, gy, pad_mode="linear", nthreads=None):
-    """(gx1, gx2, gv, gk, gD) through the convolution theorem (power-of-two extents)."""
+    """(gx1, gx2, gv, gk, gD) through the convolution theorem (linear and
+    circular modes; circular needs power-of-two extents)."""
+    if pad_mode == "centered":
+        raise ValueError("the FFT backward takes pad_mode 'linear' or 'circular'")
     return _backward(lib().oracle_backward_fft, x1, x2, v, k, D, gy, pad_mode, nthreads)
 
 

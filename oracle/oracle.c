@@ -60,8 +60,11 @@
  *       gk = crop(IFFT(conj(U) H)); zero padding to 2 L_d makes the cyclic
  *       sums equal the linear ones on the cropped range.
  *
- * The mode argument: 0 linear, 1 circular, 2 centered (forward only; the
- * backward takes 0 and 1).
+ * The mode argument: 0 linear, 1 circular, 2 centered (the FFT backward
+ * takes 0 and 1; the direct backward all three, centred as
+ *   gu[j] = sum_n kc[n - j + (L - 1)] h[n] + D[c] h[j],
+ *   gk[i] = sum_n h[n] u[n - i + (L - 1)]  over n with that index on the grid,
+ * kc and gk on the 2 L_d - 1 point grid).
  *
  * The HyenaND operator, Eq. (HyenaND) of section 3.2 (oracle_operator):
  * with q, kin, vin the three projections [B, C, L...], per sample b and grid
@@ -475,7 +478,7 @@ int oracle_fft(const double *x1, const double *x2, const double *v, const double
         for (int d = 0; d < 3; ++d)
             if (!is_pow2(g.L[d])) return 1;
     int64_t P[3];
-    transform_extents(&g, circular, P);
+    transform_extents(&g, circular == MODE_CIRCULAR ? MODE_CIRCULAR : MODE_LINEAR, P);
     cplx *twf[3] = {NULL, NULL, NULL}, *twi[3] = {NULL, NULL, NULL};
     int rc = 0;
     for (int d = 0; d < 3; ++d) {
@@ -583,6 +586,77 @@ static void *backward_direct_worker(void *arg) {
             J->gx1[base + i] = gu * J->v[base + i];
             J->gv[base + i] = gu * J->x1[base + i];
             J->gk[base + i] = gk;
+        }
+    }
+    free(u);
+    free(h);
+    return NULL;
+}
+
+/* centred mode: conv[n] = sum_m kc[n - m + (L - 1)] u[m], kc on the 2 L_d - 1
+ * point grid, so gu[j] = sum_n kc[n - j + (L - 1)] h[n] + D h[j] and
+ * gk[i] = sum_n h[n] u[n - i + (L - 1)] (where that index is on the grid) */
+static int64_t kc_index(const geom *g, const int64_t a[3], const int64_t b[3]) {
+    int64_t r = 0;
+    for (int d = 0; d < 3; ++d) r = r * (2 * g->L[d] - 1) + (a[d] - b[d] + g->L[d] - 1);
+    return r;
+}
+
+static void *backward_centered_worker(void *arg) {
+    bjob *J = (bjob *)arg;
+    const geom *g = J->g;
+    const int64_t box = g->box, kbox = centered_box(g);
+    double *u = (double *)malloc((size_t)box * sizeof(double));
+    double *h = (double *)malloc((size_t)box * sizeof(double));
+    if (!u || !h) {
+        free(u); free(h);
+        J->status = 2;
+        return NULL;
+    }
+    for (int64_t line = J->tid; line < g->B * g->C; line += J->nthreads) {
+        const int64_t base = line * box, kbase = line * kbox, c = line % g->C;
+        const double *K = J->k + kbase;
+        double hu = 0.0;
+        for (int64_t i = 0; i < box; ++i) {
+            u[i] = J->x1[base + i] * J->v[base + i];
+            h[i] = J->gy[base + i] * J->x2[base + i];
+            hu += h[i] * u[i];
+        }
+        J->hu[line] = hu;
+        for (int64_t i = 0; i < box; ++i) {
+            int64_t p[3], q[3];
+            unflat(g, i, p);
+            double conv = 0.0, gu = 0.0;
+            for (int64_t m = 0; m < box; ++m) {
+                unflat(g, m, q);
+                conv += K[kc_index(g, p, q)] * u[m];  /* kc[i - m + L - 1] u[m] */
+                gu += K[kc_index(g, q, p)] * h[m];    /* kc[m - i + L - 1] h[m] */
+            }
+            const double z = conv + J->D[c] * u[i];
+            J->gx2[base + i] = J->gy[base + i] * z;
+            gu += J->D[c] * h[i];
+            J->gx1[base + i] = gu * J->v[base + i];
+            J->gv[base + i] = gu * J->x1[base + i];
+        }
+        for (int64_t ki = 0; ki < kbox; ++ki) {
+            /* kernel point ki: displacement e_d = index_d - (L_d - 1) */
+            int64_t e[3], r = ki;
+            for (int d = 2; d >= 0; --d) {
+                e[d] = r % (2 * g->L[d] - 1) - (g->L[d] - 1);
+                r /= 2 * g->L[d] - 1;
+            }
+            double s = 0.0;
+            for (int64_t n = 0; n < box; ++n) {
+                int64_t q[3], m = 0, ok = 1;
+                unflat(g, n, q);
+                for (int d = 0; d < 3; ++d) {
+                    const int64_t x = q[d] - e[d];
+                    if (x < 0 || x >= g->L[d]) ok = 0;
+                    m = m * g->L[d] + x;
+                }
+                if (ok) s += h[n] * u[m];
+            }
+            J->gk[kbase + ki] = s;
         }
     }
     free(u);
@@ -712,14 +786,15 @@ static int backward_common(const double *x1, const double *x2, const double *v, 
     if (!x1 || !x2 || !v || !k || !D || !gy || !gx1 || !gx2 || !gv || !gk || !gD ||
         make_geom(ndim, dims, &g))
         return 1;
-    if (circular != MODE_LINEAR && circular != MODE_CIRCULAR) return 1;
+    if (circular != MODE_LINEAR && circular != MODE_CIRCULAR && circular != MODE_CENTERED) return 1;
+    if (use_fft && circular == MODE_CENTERED) return 1; /* the centred backward is the direct sums */
     if (use_fft && circular == MODE_CIRCULAR)
         for (int d = 0; d < 3; ++d)
             if (!is_pow2(g.L[d])) return 1;
     double *hu = (double *)calloc((size_t)(g.B * g.C), sizeof(double));
     if (!hu) return 2;
     int64_t P[3];
-    transform_extents(&g, circular, P);
+    transform_extents(&g, circular == MODE_CIRCULAR ? MODE_CIRCULAR : MODE_LINEAR, P);
     cplx *twf[3] = {NULL, NULL, NULL}, *twi[3] = {NULL, NULL, NULL};
     int rc = 0;
     if (use_fft)
@@ -733,10 +808,12 @@ static int backward_common(const double *x1, const double *x2, const double *v, 
         memset(&J, 0, sizeof J);
         J.x1 = x1; J.x2 = x2; J.v = v; J.k = k; J.D = D; J.gy = gy;
         J.gx1 = gx1; J.gx2 = gx2; J.gv = gv; J.gk = gk; J.hu = hu; J.g = &g;
-        J.circular = circular ? 1 : 0;
+        J.circular = circular == MODE_CIRCULAR ? 1 : 0;
         J.tw_fwd = (const cplx *const *)twf;
         J.tw_inv = (const cplx *const *)twi;
-        rc = run_bjobs(&J, nthreads, use_fft ? backward_fft_worker : backward_direct_worker);
+        rc = run_bjobs(&J, nthreads,
+                       use_fft ? backward_fft_worker
+                               : (circular == MODE_CENTERED ? backward_centered_worker : backward_direct_worker));
     }
     if (!rc) /* gD[c] = sum over samples, in sample order */
         for (int64_t c = 0; c < g.C; ++c) {
@@ -766,7 +843,7 @@ int oracle_backward_fft(const double *x1, const double *x2, const double *v, con
     return backward_common(x1, x2, v, k, D, gy, gx1, gx2, gv, gk, gD, ndim, dims, circular, nthreads, 1);
 }
 
-int oracle_version(void) { return 6; }
+int oracle_version(void) { return 7; }
 
 /* ------------------------------------------------------------------------- */
 /* HyenaND operator: normalised prologue, long convolution, normalised       */
