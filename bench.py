@@ -124,13 +124,16 @@ def bench_backward(args, w, inp):
     from paper_2607_19378_amd import hyenand as H
     rng = np.random.default_rng(w.seed + 7)
     gy_host = W.quantise(rng.standard_normal(w.shape), w.dtype)
-    elem_bytes = 9 * w.storage_bytes  # read x1, x2, v, k, gy; write gx1, gx2, gv, gk
-    set_bytes = w.elems * elem_bytes
+    # read x1, x2, v, gy and k; write gx1, gx2, gv and gk (k and gk have the
+    # kernel's shape: 2 L - 1 points per axis in the centred mode)
+    kelems = int(np.prod(w.kernel_shape))
+    set_bytes = (7 * w.elems + 2 * kelems) * w.storage_bytes
     rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
     dev = torch.device("cuda:0")
     base = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D, gy_host)]
     sets = [base] + [[t.clone() for t in base] for _ in range(1, rot)]
-    outs = [[torch.empty_like(base[0]) for _ in range(4)] + [torch.empty_like(base[4])] for _ in range(rot)]
+    outs = [[torch.empty_like(base[0]) for _ in range(3)] + [torch.empty_like(base[3]), torch.empty_like(base[4])]
+            for _ in range(rot)]
     ws = torch.empty(H.backward_workspace_size(w.shape, w.pad_mode, w.dtype), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     calls = [H.PreparedBackward(*o, *st, w.pad_mode, ws, stream) for o, st in zip(outs, sets)]
@@ -168,15 +171,18 @@ def bench_backward(args, w, inp):
         # all of them for small workloads
         import oracle
         nl = w.B * w.C
-        chans = list(range(w.C)) if w.elems <= (1 << 24) else sorted({0, w.C - 1})
+        centred = w.pad_mode == W.CENTERED  # the oracle's centred backward is the direct sums
+        chans = list(range(w.C)) if w.elems <= (1 << 24) and not centred else sorted({0, w.C - 1})
         lines = np.array([b * w.C + c for b in range(w.B) for c in chans], dtype=np.int64)
         sub = []
         for a in (inp.x1, inp.x2, inp.v, inp.k, gy_host):
-            flat = a.reshape((nl,) + tuple(w.grid))[lines]
-            sub.append(W.storage_to_f64(flat, w.dtype).reshape((w.B, len(chans)) + tuple(w.grid)))
+            g = tuple(a.shape[2:])
+            flat = a.reshape((nl,) + g)[lines]
+            sub.append(W.storage_to_f64(flat, w.dtype).reshape((w.B, len(chans)) + g))
         Dsub = W.storage_to_f64(inp.D, w.dtype)[chans]
         t0 = time.perf_counter()
-        ref = oracle.backward_fft(sub[0], sub[1], sub[2], sub[3], Dsub, sub[4], w.pad_mode)
+        ref = (oracle.backward_direct if centred else oracle.backward_fft)(sub[0], sub[1], sub[2], sub[3], Dsub,
+                                                                          sub[4], w.pad_mode)
         dt = time.perf_counter() - t0
         if not args.no_parity:
             got = outs[(args.steps - 1) % rot]
@@ -194,8 +200,8 @@ def bench_backward(args, w, inp):
         if not args.no_cpu_baseline:
             cpu = {"value": round(len(lines) * (w.elems // nl) / dt / 1e9, 6), "unit": "GElem/s",
                    "cores": oracle.default_threads(), "kind": "oracle",
-                   "sample": f"{len(lines)} of the {nl} (b,c) lines of {w.name} (fp64 FFT oracle backward, "
-                             f"{dt:.2f} s wall)"}
+                   "sample": f"{len(lines)} of the {nl} (b,c) lines of {w.name} (fp64 "
+                             f"{'direct-sum' if centred else 'FFT'} oracle backward, {dt:.2f} s wall)"}
     out = {
         "metric": "gated N-D FFT-conv backward GElem/s and % of roofline on 1 MI355X",
         "value": round(w.elems / (ms_per_step * 1e-3) / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,

@@ -266,10 +266,45 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
 // else the multi-pass (2D/3D) or four-step (1D) structure of the forward
 // with three signals.  The workspace holds the gD sums (256-byte aligned
 // block) and then the spectra of a chunk of lines per side stream.
-enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP };
+//
+// The centred mode and extents that are not powers of two (BWD_EMBED) run the
+// circular backward on their transform grid (P_d >= 2 L_d - 1, a power of
+// two): the five inputs are embedded in that grid and the four gradient
+// tensors extracted from it (conv_embed.hip); gD comes out directly.  Their
+// workspace holds the nine embedded tensors (each 256-byte aligned) and then
+// the circular backward's own.
+enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP, BWD_EMBED };
+
+BwdPlan choose_bwd_plan(const FftConvArgs& a);
+
+struct Embedded {
+  FftConvArgs e;  // the circular problem on the transform grid
+  BwdPlan p;      // its plan
+  int nd;
+  int64_t dims[5];
+  size_t tensor;  // bytes of one embedded tensor
+};
+
+bool embedded_problem(const FftConvArgs& a, Embedded* m) {
+  m->nd = a.ndim;
+  m->dims[0] = a.lines / a.C;
+  m->dims[1] = a.C;
+  for (int d = 0; d < a.ndim; ++d) m->dims[2 + d] = a.P[d];
+  const std::string keep = g_last_error;
+  const hyenand_status st = parse_shape(m->nd, m->dims, HYENAND_PAD_CIRCULAR,
+                                        a.bf16 ? HYENAND_DTYPE_BF16 : HYENAND_DTYPE_F32, &m->e);
+  g_last_error = keep;
+  if (st != HYENAND_OK) return false;
+  m->p = choose_bwd_plan(m->e);
+  m->tensor = ((size_t)embed_grid_elems(a) * (a.bf16 ? 2 : 4) + 255) / 256 * 256;
+  return m->p != BWD_NONE && m->p != BWD_EMBED;
+}
 
 BwdPlan choose_bwd_plan(const FftConvArgs& a) {
-  if (a.centered || a.rl) return BWD_NONE;  // linear and circular modes, power-of-two extents
+  if (a.centered || a.rl) {
+    Embedded m;
+    return embedded_problem(a, &m) ? BWD_EMBED : BWD_NONE;
+  }
   if (fused_backward_supported(a)) return BWD_FUSED;
   if ((a.ndim == 2 || a.ndim == 3) && multipass_supported(a)) return BWD_MULTIPASS;
   if (a.ndim == 1 && backward_fs_supported(a)) return BWD_FOURSTEP;
@@ -521,6 +556,12 @@ hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* 
   if (st != HYENAND_OK) return st;
   const BwdPlan p = choose_bwd_plan(a);
   if (p == BWD_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  if (p == BWD_EMBED) {
+    Embedded m;
+    embedded_problem(a, &m);
+    *bytes_out = 9 * m.tensor + bwd_partial_bytes(m.e, m.p) + bwd_recommended_spectra(m.e, m.p);
+    return HYENAND_OK;
+  }
   *bytes_out = bwd_partial_bytes(a, p) + bwd_recommended_spectra(a, p);
   return HYENAND_OK;
 }
@@ -533,6 +574,12 @@ hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* d
   if (st != HYENAND_OK) return st;
   const BwdPlan p = choose_bwd_plan(a);
   if (p == BWD_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
+  if (p == BWD_EMBED) {
+    Embedded m;
+    embedded_problem(a, &m);
+    *bytes_out = 9 * m.tensor + bwd_partial_bytes(m.e, m.p) + bwd_bytes_per_line(m.e, m.p);
+    return HYENAND_OK;
+  }
   *bytes_out = bwd_partial_bytes(a, p) + bwd_bytes_per_line(a, p);
   return HYENAND_OK;
 }
@@ -554,11 +601,14 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
   for (int i = 0; i < 5; ++i)
     if (!outs[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", out_names[i]);
   const size_t es = a.bf16 ? 2 : 4;
-  size_t n = (size_t)a.lines;
-  for (int d = 0; d < a.ndim; ++d) n *= (size_t)a.L[d];
+  size_t n = (size_t)a.lines, kn = (size_t)a.lines;  // elements of the data and of the kernel
+  for (int d = 0; d < a.ndim; ++d) {
+    n *= (size_t)a.L[d];
+    kn *= (size_t)(a.centered ? 2 * a.L[d] - 1 : a.L[d]);
+  }
   size_t in_bytes[6], out_bytes[5];
-  for (int i = 0; i < 6; ++i) in_bytes[i] = i == 5 ? (size_t)a.C * es : n * es;
-  for (int i = 0; i < 5; ++i) out_bytes[i] = i == 4 ? (size_t)a.C * es : n * es;
+  for (int i = 0; i < 6; ++i) in_bytes[i] = i == 5 ? (size_t)a.C * es : (i == 3 ? kn : n) * es;
+  for (int i = 0; i < 5; ++i) out_bytes[i] = i == 4 ? (size_t)a.C * es : (i == 3 ? kn : n) * es;
   for (int i = 0; i < 6; ++i)
     if ((uintptr_t)ins[i] % (i == 5 ? es : 16) != 0)
       return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not aligned", in_names[i]);
@@ -575,8 +625,11 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
   }
   const BwdPlan p = choose_bwd_plan(a);
   if (p == BWD_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no backward plan for this shape");
-  const size_t pbytes = bwd_partial_bytes(a, p);
-  const size_t need = pbytes + bwd_bytes_per_line(a, p);
+  Embedded m;
+  if (p == BWD_EMBED) embedded_problem(a, &m);
+  const size_t pbytes = p == BWD_EMBED ? 0 : bwd_partial_bytes(a, p);
+  const size_t need = p == BWD_EMBED ? 9 * m.tensor + bwd_partial_bytes(m.e, m.p) + bwd_bytes_per_line(m.e, m.p)
+                                     : pbytes + bwd_bytes_per_line(a, p);
   if (!workspace || workspace_bytes < need)
     return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "backward needs at least %zu workspace bytes, got %zu", need,
                 workspace ? workspace_bytes : (size_t)0);
@@ -595,7 +648,20 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
   b.partial = (float*)workspace;
   const hipStream_t s = (hipStream_t)stream;
   hipError_t err = hipSuccess;
-  if (p == BWD_FUSED) {
+  if (p == BWD_EMBED) {
+    char* w = (char*)workspace;
+    void* e[9];
+    for (int i = 0; i < 9; ++i) e[i] = w + i * m.tensor;
+    void* const ein[5] = {e[0], e[1], e[2], e[3], e[4]};  // x1, x2, v, gy, k
+    void* const eout[4] = {e[5], e[6], e[7], e[8]};       // gx1, gx2, gv, gk
+    err = launch_embed(b.f, gy, ein, s);
+    if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+    const hyenand_status inner =
+        hyenand_fftconv_backward(e[0], e[1], e[2], e[4], D, e[3], e[5], e[6], e[7], e[8], gD, m.nd, m.dims,
+                                 HYENAND_PAD_CIRCULAR, dtype, w + 9 * m.tensor, workspace_bytes - 9 * m.tensor, stream);
+    if (inner != HYENAND_OK) return inner;
+    err = launch_extract(b.f, eout, gx1, gx2, gv, gk, s);
+  } else if (p == BWD_FUSED) {
     err = launch_backward(b, s);
   } else {
     // the spectra of each chunk follow the gD sums in the workspace

@@ -69,6 +69,13 @@ size_t backward_fs_bytes_per_line(const FftConvArgs& a);
 int64_t backward_fs_partials_per_line(const FftConvArgs& a);
 hipError_t launch_backward_fs(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s);
 hipError_t launch_backward_reduce(const FftConvBwdArgs& b, int64_t partials_per_line, hipStream_t s);
+// centred and non-power-of-two extents (conv_embed.hip): embed x1, x2, v, gy
+// and k in the transform grid (e[0..4], lines * prod P elements each), run
+// the circular backward there, extract gx1, gx2, gv, gk (from e[0..3])
+int64_t embed_grid_elems(const FftConvArgs& a);
+hipError_t launch_embed(const FftConvArgs& a, const void* gy, void* const (&e)[5], hipStream_t s);
+hipError_t launch_extract(const FftConvArgs& a, void* const (&e)[4], void* gx1, void* gx2, void* gv, void* gk,
+                          hipStream_t s);
 
 // multi-pass 1D (four-step split of the long line); one call per chunk of
 // lines, as for launch_multipass

@@ -239,10 +239,12 @@ class PreparedBackward:
                  stream=None):
         import torch
         shape = tuple(x1.shape)
+        kshape = kernel_shape(shape, pad_mode)
         for t in (x1, x2, v, k, gy, gx1, gx2, gv, gk):
-            if not t.is_cuda or tuple(t.shape) != shape or t.dtype != x1.dtype or not t.is_contiguous():
-                raise ValueError("x1, x2, v, k, gy and the four gradients must be contiguous GPU tensors "
-                                 "of one shape and dtype")
+            want = kshape if (t is k or t is gk) else shape
+            if not t.is_cuda or tuple(t.shape) != want or t.dtype != x1.dtype or not t.is_contiguous():
+                raise ValueError("x1, x2, v, gy, gx1, gx2, gv must be contiguous GPU tensors of one shape and "
+                                 f"dtype; k and gk {kshape} (pad_mode {pad_mode!r})")
         for t in (D, gD):
             if not t.is_cuda or t.dtype != x1.dtype or tuple(t.shape) != (shape[1],) or not t.is_contiguous():
                 raise ValueError("D and gD must be contiguous [C] GPU tensors of the same dtype")
@@ -267,14 +269,16 @@ class PreparedBackward:
 def backward_into(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None,
                   stream=None) -> None:
     """Gradients of a loss through y for dLoss/dy = gy, written into gx1, gx2,
-    gv, gk ([B, C, L...]) and gD ([C]); all tensors already on the GPU."""
+    gv ([B, C, L...]), gk (shaped like k) and gD ([C]); all tensors already on
+    the GPU."""
     PreparedBackward(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode, workspace, stream)()
 
 
 def backward(x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None, stream=None):
     """(gx1, gx2, gv, gk, gD) with torch-allocated outputs."""
     import torch
-    gx1, gx2, gv, gk = (torch.empty_like(x1) for _ in range(4))
+    gx1, gx2, gv = (torch.empty_like(x1) for _ in range(3))
+    gk = torch.empty_like(k)
     gD = torch.empty_like(D)
     backward_into(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode, workspace, stream)
     return gx1, gx2, gv, gk, gD

@@ -134,7 +134,10 @@ def test_backward_validation(L):
     assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 1 << 22)) == H.ERR_UNSUPPORTED       # 2^23 transform points
     assert bcall(L, (1, 2, 2048, 4)) == H.ERR_UNSUPPORTED       # 4096 points on an axis of a 2D grid
-    assert bcall(L, (1, 2, 12)) == H.ERR_UNSUPPORTED            # no backward for other extents
+    assert bcall(L, (1, 2, 12), mode=1) == H.ERR_UNSUPPORTED    # circular needs powers of two
+    # other extents (linear) run embedded in their transform grid: nine
+    # embedded tensors of 2 x 32 floats (256 bytes each) plus the gD sums
+    assert bcall(L, (1, 2, 12), ws_bytes=9 * 256) == H.ERR_WORKSPACE_TOO_SMALL
     # multi-pass plans: the gD sums plus one line of three spectra at least
     assert bcall(L, (1, 2, 1 << 20)) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 128, 128), mode=1, ws_bytes=4096) == H.ERR_WORKSPACE_TOO_SMALL
@@ -159,7 +162,8 @@ def test_backward_workspace_size(L):
 
 def test_centered_mode_queries():
     """pad_mode 2: the transform grid of the linear mode, a workspace that
-    holds U (L0 rows) and a centered K (P0 rows) per line, no backward."""
+    holds U (L0 rows) and a centered K (P0 rows) per line; the backward runs
+    embedded in the transform grid."""
     assert H.plan_name((8, 256, 64, 64), "centered", "f32") == "fused2d"
     assert H.plan_name((1, 64, 4096), "centered", "f32") == "fused1d"
     assert H.plan_name((1, 4, 1 << 20), "centered", "bf16") == "fourstep1d"
@@ -167,9 +171,10 @@ def test_centered_mode_queries():
     assert H.workspace_min((1, 3, 256, 256), "centered", "f32") == (256 + 512) * 272 * 8
     assert H.workspace_min((1, 3, 256, 256), "linear", "f32") == 2 * 256 * 272 * 8
     assert H.workspace_min((1, 2, 1 << 20), "centered", "f32") == 2 * (1 << 20) * 8
-    with pytest.raises(H.HyenandError) as e:
-        H.backward_workspace_size((1, 2, 64), "centered", "f32")
-    assert e.value.status == H.ERR_UNSUPPORTED
+    # backward: nine tensors embedded in the 2 x 128 transform grid (1 KiB
+    # each) and the circular backward's gD sums (one 256-byte block)
+    assert H.backward_workspace_size((1, 2, 64), "centered", "f32") == 9 * 1024 + 256
+    assert H.backward_workspace_min((1, 2, 64), "centered", "f32") == 9 * 1024 + 256
     assert H.kernel_shape((2, 3, 8, 4), "centered") == (2, 3, 15, 7)
     assert H.kernel_shape((2, 3, 8, 4), "centered", shared_k=True) == (3, 15, 7)
 
@@ -307,3 +312,17 @@ def test_modal_validation(L):
     # k (4 x 64 fp32 = 1024 bytes) running into res_im
     assert modal(L, k=base[3] - 1020) == H.ERR_INVALID_ARGUMENT
     assert b"k overlaps res_im" in L.hyenand_last_error()
+
+
+def test_embedded_backward_validation(L):
+    """Centred and other-extent backward: k and gk take the kernel's shape in
+    the overlap checks, and every call here fails validation."""
+    p = [FAKE + i * (1 << 36) for i in range(11)]
+    # centred [1, 2, 8]: gk is 2 x 15 floats = 120 bytes; placed 112 bytes
+    # below gD's start it runs into gD (a data-sized gk, 64 bytes, would not)
+    q = list(p)
+    q[9] = p[10] - 112
+    assert bcall(L, (1, 2, 8), mode=2, ptrs=q) == H.ERR_INVALID_ARGUMENT
+    assert b"gD overlaps gk" in L.hyenand_last_error() or b"gk overlaps" in L.hyenand_last_error()
+    assert bcall(L, (1, 2, 8), mode=2, ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL
+    assert bcall(L, (1, 2, 5, 7), mode=0, ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL
