@@ -67,11 +67,13 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  * dims            : host pointer to ndim + 2 int64 values {B, C, L1, ..., LN},
  *                   all >= 1.  Transform extents: L_d circular, 2 L_d
  *                   linear and centered; supported up to 2^22 points in 1D
- *                   and 1024 per axis in 2D/3D.  Circular mode needs powers
- *                   of two.  In the linear and centered modes other extents
- *                   run on the smallest power of two >= 2 L_d - 1 (exact for
- *                   a non-circular convolution), in one pass per line: 1D up
- *                   to L = 8192, 2D up to 128-point transforms per axis.
+ *                   and 1024 per axis in 2D/3D.  Other extents run on the
+ *                   smallest power of two >= 2 L_d - 1 (exact for a
+ *                   non-circular convolution; in circular mode the kernel is
+ *                   repeated periodically over the displacements
+ *                   -(L_d - 1) .. L_d - 1, which makes the circular
+ *                   convolution a non-circular one), in one pass per line:
+ *                   1D up to L = 8192, 2D up to 128-point transforms per axis.
  * pad_mode        : hyenand_pad_mode.
  * dtype           : hyenand_dtype.
  * workspace       : device scratch of workspace_bytes (16-byte aligned), owned

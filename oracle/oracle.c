@@ -895,8 +895,14 @@ int oracle_operator(const double *q, const double *kin, const double *vin, const
         gate[i] = sigmoid(vin[i]);
         ones[i] = 1.0;
     }
-    /* 2. the gated long convolution of u (x1 = u, v = 1, x2 = the gate) */
-    int rc = oracle_fft(u, gate, ones, k, D, y, ndim, dims, mode, NULL, 0, nthreads);
+    /* 2. the gated long convolution of u (x1 = u, v = 1, x2 = the gate);
+       the circular mode on extents that are not powers of two takes the
+       direct sums (this file's FFT is radix 2) */
+    int pow2_grid = 1;
+    for (int d = 0; d < 3; ++d) pow2_grid = pow2_grid && is_pow2(g.L[d]);
+    int rc = (mode == MODE_CIRCULAR && !pow2_grid)
+                 ? oracle_direct(u, gate, ones, k, D, y, ndim, dims, mode, NULL, 0, nthreads)
+                 : oracle_fft(u, gate, ones, k, D, y, ndim, dims, mode, NULL, 0, nthreads);
     /* 3. epilogue RMSNorm across channels */
     if (!rc)
         for (int64_t b = 0; b < B; ++b)

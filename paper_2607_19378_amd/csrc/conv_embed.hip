@@ -1,14 +1,17 @@
-// Backward of the centred and the non-power-of-two (linear) modes through the
-// circular backward on their transform grid.
+// Backward of the centred mode and of extents that are not powers of two
+// through the circular backward on their transform grid.
 //
-// Both modes are a non-circular convolution computed on a grid of P_d >=
+// These calls are a non-circular convolution computed on a grid of P_d >=
 // 2 L_d - 1 points per axis (a power of two): u is zero beyond its L_d
 // points, the kernel sits at its displacements taken modulo P_d (index m of a
 // linear kernel at m; index i of a centred kernel, displacement
-// i - (L_d - 1), at that displacement mod P_d).  On that grid the operation
-// is exactly the circular one of the embedded tensors, and so is its
-// backward: the correlations gu and gk of the circular backward never wrap
-// onto a nonzero value because P_d >= 2 L_d - 1.  So
+// i - (L_d - 1), at that displacement mod P_d; a circular kernel of other
+// extents, repeated periodically, at displacements -(L_d - 1) .. L_d - 1).
+// On that grid the operation is exactly the circular one of the embedded
+// tensors, and so is its backward: the correlations gu and gk of the circular
+// backward never wrap onto a nonzero value because P_d >= 2 L_d - 1.  The
+// periodic kernel's gradient gathers the two displacements m and m - L_d that
+// hold k[m] (m >= 1) on every axis.  So
 //
 //   embed     x1, x2, v, gy into the first L_d points of every axis of a
 //             P-grid (zeros elsewhere), k at its displacements;
@@ -33,6 +36,7 @@ struct EmbedGeom {
   int64_t box;    // prod L_d
   int64_t kbox;   // prod KL_d
   bool centered;
+  bool periodic;  // circular kernel repeated over the displacements -(L-1) .. L-1
 };
 
 EmbedGeom embed_geom(const FftConvArgs& a) {
@@ -40,6 +44,7 @@ EmbedGeom embed_geom(const FftConvArgs& a) {
   g.nd = a.ndim;
   g.grid = g.box = g.kbox = 1;
   g.centered = a.centered;
+  g.periodic = a.periodic;
   for (int d = 0; d < 3; ++d) {
     g.lp[d] = 0;
     g.L[d] = g.KL[d] = 1;
@@ -58,8 +63,9 @@ EmbedGeom embed_geom(const FftConvArgs& a) {
 }
 
 // kernel index of grid position q along one axis, or -1 where the kernel has
-// no point (linear: q < L; centred: displacement q or q - P)
-__device__ __forceinline__ int64_t kernel_pos(int64_t q, int64_t L, int64_t P, bool centered) {
+// no point (linear: q < L; centred and periodic: displacement q or q - P)
+__device__ __forceinline__ int64_t kernel_pos(int64_t q, int64_t L, int64_t P, bool centered, bool periodic) {
+  if (periodic) return q < L ? q : (q > P - L ? q - P + L : -1);
   if (!centered) return q < L ? q : -1;
   return q < L ? q + L - 1 : (q > P - L ? q - P + L - 1 : -1);
 }
@@ -83,7 +89,7 @@ __global__ void __launch_bounds__(256)
     const int64_t P = int64_t(1) << g.lp[d];
     in = in && q < g.L[d];
     src = src * g.L[d] + (q < g.L[d] ? q : 0);
-    const int64_t kp = kernel_pos(q, g.L[d], P, g.centered);
+    const int64_t kp = kernel_pos(q, g.L[d], P, g.centered, g.periodic);
     kin = kin && kp >= 0;
     ksrc = ksrc * g.KL[d] + (kp >= 0 ? kp : 0);
   }
@@ -116,23 +122,35 @@ __global__ void __launch_bounds__(256)
   o3[i] = e3[e];
 }
 
-// gk back from the kernel's displacements
+// gk back from the kernel's displacements (periodic: the sum over the one or
+// two displacements of every axis that hold the point, in a fixed order)
 template <typename TS>
 __global__ void __launch_bounds__(256)
     extract_kernel(const TS* __restrict__ ek, TS* __restrict__ gk, EmbedGeom g, int64_t total) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= total) return;
   const int64_t line = i / g.kbox;
-  int64_t r = i - line * g.kbox, q[3] = {0, 0, 0};
+  int64_t r = i - line * g.kbox, q[3] = {0, 0, 0}, q2[3] = {-1, -1, -1};
   for (int d = g.nd - 1; d >= 0; --d) {
     const int64_t m = r % g.KL[d];
     r /= g.KL[d];
     const int64_t P = int64_t(1) << g.lp[d];
     q[d] = g.centered ? (m - (g.L[d] - 1) + P) & (P - 1) : m;
+    if (g.periodic && m >= 1) q2[d] = m - g.L[d] + P;  // displacement m - L
   }
-  int64_t e = line;
-  for (int d = 0; d < g.nd; ++d) e = (e << g.lp[d]) + q[d];
-  gk[i] = ek[e];
+  float acc = 0.f;
+  const int nc = g.periodic ? 1 << g.nd : 1;
+  for (int cmb = 0; cmb < nc; ++cmb) {
+    int64_t e = line;
+    bool ok = true;
+    for (int d = 0; d < g.nd; ++d) {
+      const int64_t qd = (cmb >> d) & 1 ? q2[d] : q[d];
+      ok = ok && qd >= 0;
+      e = (e << g.lp[d]) + (qd >= 0 ? qd : 0);
+    }
+    if (ok) acc += ld1(ek + e);
+  }
+  st1(gk + i, acc);
 }
 
 unsigned blocks(int64_t n) { return (unsigned)((n + 255) / 256); }

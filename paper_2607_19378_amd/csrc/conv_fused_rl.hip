@@ -10,17 +10,28 @@
 //  * conv1d_rl<P>: 1D lines, P <= 16384.
 //  * conv2d_rl<P0, P1>: 2D images whose U and K half spectra fit in LDS side
 //    by side (linear: L0 + L0 rows; centered: L0 + P0 rows).
+//
+// The circular mode takes these kernels too: a circular convolution of L
+// points equals the centred one whose kernel holds k[d mod L] at every
+// displacement d = -(L-1) .. L-1 (n - m covers exactly that range), so KC
+// with per = true gathers k periodically onto the grid.
 #include "kernels.hpp"
 
 namespace hyenand {
 
 namespace {
 
-// value of the centered kernel at grid point g of a line of L points on a
-// transform of P (0 where no displacement lands)
+// index of the kernel value at grid point g of a line of L points on a
+// transform of P: centred kernel (per = false) or circular kernel repeated
+// periodically (per = true); -1 where no displacement lands
+__device__ __forceinline__ int kmap(int g, int L, int P, bool per) {
+  return per ? periodic_index(g, L, P) : centered_index(g, L, P);
+}
+
+// value of that kernel at grid point g (0 where no displacement lands)
 template <typename TS>
-__device__ __forceinline__ float kc_at(const TS* kl, int g, int L, int P) {
-  const int j = centered_index(g, L, P);
+__device__ __forceinline__ float kc_at(const TS* kl, int g, int L, int P, bool per) {
+  const int j = kmap(g, L, P, per);
   return j >= 0 ? ld1(kl + j) : 0.f;
 }
 
@@ -30,7 +41,7 @@ template <int P, bool KC, typename TS, bool ACT>
 __global__ void __launch_bounds__(rl1d_nt(P))
     conv1d_rl(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
               const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC, int L,
-              ActIn ain) {
+              ActIn ain, bool per) {
   constexpr int M = P / 2;
   constexpr int EF = imin(16, M), TF = M / EF;
   constexpr int EI = imin(8, M), TI = M / EI;
@@ -45,7 +56,7 @@ __global__ void __launch_bounds__(rl1d_nt(P))
   const Gates<ACT> G = line_gates<ACT, TS>(ain, line, C);
   const int MNZ = (L + 1) / 2;
   const int KNZ = KC ? M : MNZ;  // packed points of k that can be nonzero
-  const TS* kl = k + (size_t)k_line(line, kC) * (KC ? 2 * L - 1 : L);
+  const TS* kl = k + (size_t)k_line(line, kC) * (KC && !per ? 2 * L - 1 : L);
 
   // stage u = x1 v and k as even/odd packed lines, point by point
   for (int m = tid; m < M; m += NT) {
@@ -56,7 +67,7 @@ __global__ void __launch_bounds__(rl1d_nt(P))
       if (n + 1 < L) u.y = G.u1(ld1(x1 + base + n + 1), ld1(v + base + n + 1), n + 1);
     }
     if (KC) {
-      kk = make_float2(kc_at(kl, 2 * m, L, P), kc_at(kl, 2 * m + 1, L, P));
+      kk = make_float2(kc_at(kl, 2 * m, L, P, per), kc_at(kl, 2 * m + 1, L, P, per));
     } else if (m < MNZ) {
       kk.x = ld1(kl + 2 * m);
       if (2 * m + 1 < L) kk.y = ld1(kl + 2 * m + 1);
@@ -126,7 +137,7 @@ template <int P0, int P1, bool KC, typename TS, bool ACT>
 __global__ void __launch_bounds__(512)
     conv2d_rl(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
               const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC, int L0,
-              int L1, ActIn ain) {
+              int L1, ActIn ain, bool per) {
   constexpr int M1 = P1 / 2, RP = M1 + 1, NT = 512;
   constexpr int L0M = P0 / 2;
   constexpr int KRM = KC ? P0 : L0M;
@@ -145,7 +156,8 @@ __global__ void __launch_bounds__(512)
   const int MNZ = (L1 + 1) / 2;        // packed points per nonzero row
   const int KR = KC ? P0 : L0;         // K rows that can be nonzero
   const int KNZ = KC ? M1 : MNZ;
-  const TS* kl = k + (size_t)k_line(img, kC) * (KC ? (2 * L0 - 1) * (2 * L1 - 1) : L0 * L1);
+  const int KL1 = KC && !per ? 2 * L1 - 1 : L1;  // kernel row length
+  const TS* kl = k + (size_t)k_line(img, kC) * (KC && !per ? (2 * L0 - 1) * (2 * L1 - 1) : L0 * L1);
   constexpr float scale = 1.f / (4.f * (float)P0 * (float)P1);
 
   // 0. stage u and k rows as packed pairs (k scaled by the normalisation)
@@ -165,11 +177,11 @@ __global__ void __launch_bounds__(512)
   if constexpr (KC) {
     for (int i = tid; i < P0 * M1; i += NT) {
       const int g0 = i / M1, m = i - g0 * M1;
-      const int j0 = centered_index(g0, L0, P0);
+      const int j0 = kmap(g0, L0, P0, per);
       float2 z = czero();
       if (j0 >= 0) {
-        const TS* kr = kl + (size_t)j0 * (2 * L1 - 1);
-        z = make_float2(kc_at(kr, 2 * m, L1, P1) * scale, kc_at(kr, 2 * m + 1, L1, P1) * scale);
+        const TS* kr = kl + (size_t)j0 * KL1;
+        z = make_float2(kc_at(kr, 2 * m, L1, P1, per) * scale, kc_at(kr, 2 * m + 1, L1, P1, per) * scale);
       }
       Kh[g0 * RP + m] = z;
     }
@@ -326,17 +338,18 @@ hipError_t launch_1d_t(const FftConvArgs& a, hipStream_t s) {
   if (a.act)
     hipLaunchKernelGGL((conv1d_rl<P, KC, TS, true>), dim3((unsigned)a.lines), dim3(rl1d_nt(P)), 0, s,
                        (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, L, a.act_in);
+                       (int)a.C, a.kC, L, a.act_in, a.periodic);
   else
     hipLaunchKernelGGL((conv1d_rl<P, KC, TS, false>), dim3((unsigned)a.lines), dim3(rl1d_nt(P)), 0, s,
                        (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, L, a.act_in);
+                       (int)a.C, a.kC, L, a.act_in, a.periodic);
   return hipGetLastError();
 }
 
 template <int P>
 hipError_t launch_1d_p(const FftConvArgs& a, hipStream_t s) {
-  if (a.centered) return a.bf16 ? launch_1d_t<P, true, uint16_t>(a, s) : launch_1d_t<P, true, float>(a, s);
+  if (a.centered || a.periodic)
+    return a.bf16 ? launch_1d_t<P, true, uint16_t>(a, s) : launch_1d_t<P, true, float>(a, s);
   return a.bf16 ? launch_1d_t<P, false, uint16_t>(a, s) : launch_1d_t<P, false, float>(a, s);
 }
 
@@ -346,17 +359,17 @@ hipError_t launch_2d_t(const FftConvArgs& a, hipStream_t s) {
   if (a.act)
     hipLaunchKernelGGL((conv2d_rl<P0, P1, KC, TS, true>), dim3((unsigned)a.lines), dim3(512), 0, s, (const TS*)a.x1,
                        (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int)a.C, a.kC, L0,
-                       L1, a.act_in);
+                       L1, a.act_in, a.periodic);
   else
     hipLaunchKernelGGL((conv2d_rl<P0, P1, KC, TS, false>), dim3((unsigned)a.lines), dim3(512), 0, s,
                        (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, L0, L1, a.act_in);
+                       (int)a.C, a.kC, L0, L1, a.act_in, a.periodic);
   return hipGetLastError();
 }
 
 template <int P0, int P1>
 hipError_t launch_2d_p(const FftConvArgs& a, hipStream_t s) {
-  if (a.centered)
+  if (a.centered || a.periodic)
     return a.bf16 ? launch_2d_t<P0, P1, true, uint16_t>(a, s) : launch_2d_t<P0, P1, true, float>(a, s);
   return a.bf16 ? launch_2d_t<P0, P1, false, uint16_t>(a, s) : launch_2d_t<P0, P1, false, float>(a, s);
 }

@@ -511,6 +511,12 @@ __device__ __forceinline__ int centered_index(int g, int L, int P) {
   return g < L ? g + L - 1 : (g > P - L ? g - P + L - 1 : -1);
 }
 
+// Same for a circular kernel of L points repeated periodically over the
+// displacements -(L-1) .. L-1: displacement d takes k[d mod L].
+__device__ __forceinline__ int periodic_index(int g, int L, int P) {
+  return g < L ? g : (g > P - L ? g - P + L : -1);
+}
+
 // ---------------------------------------------------------------------------
 // Inner and outer gates of one (b, c) line.  Plain call: u = x1 v and the
 // gate is x2.  HyenaND operator (ACT): x1, v and x2 hold the projections q,

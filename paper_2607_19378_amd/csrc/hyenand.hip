@@ -72,9 +72,6 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   for (int d = 0; d < ndim; ++d) {
     const int64_t L = dims[2 + d];
     if (!pow2(L)) {
-      if (a->circular)
-        return fail(HYENAND_ERR_UNSUPPORTED, "circular grid extent L%d = %lld is not a power of two", d + 1,
-                    (long long)L);
       if (L > (int64_t(1) << 24)) return fail(HYENAND_ERR_UNSUPPORTED, "grid extent too large");
       a->rl = true;
     }
@@ -87,6 +84,13 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
     a->centered = false;
   }
   a->ndim = nd;
+  if (a->rl && a->circular) {
+    // a circular convolution of L points is the centred one whose kernel
+    // repeats k periodically over the displacements -(L-1) .. L-1, so it runs
+    // on the non-circular transform grid with that kernel
+    a->circular = false;
+    a->periodic = true;
+  }
   for (int d = 0; d < nd; ++d) {
     // non-circular: the smallest power of two >= 2L - 1 (2L for a power of two)
     int64_t p = 2;

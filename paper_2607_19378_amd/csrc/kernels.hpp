@@ -20,7 +20,8 @@ struct FftConvArgs {
   int64_t P[3];   // transform extents: 2L (linear) or L (circular)
   bool circular;
   bool centered;  // linear transform grid, k on the double grid of 2 L_d - 1 points per axis
-  bool rl;        // some L_d is not a power of two (linear or centered; P_d = pow2 >= 2 L_d - 1)
+  bool rl;        // some L_d is not a power of two (P_d = pow2 >= 2 L_d - 1)
+  bool periodic;  // circular mode with rl: k repeated periodically on the non-circular grid
   bool bf16;
   int kC;         // 0: k is [B, C, L...]; C: one kernel per channel, k is [C, L...]
   void* ws;       // device workspace (multi-pass plans)

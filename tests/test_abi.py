@@ -61,8 +61,10 @@ def test_invalid_arguments(L):
     assert call(L, (1, 0, 16)) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), mode=3) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), dtype=5) == H.ERR_INVALID_ARGUMENT
-    assert call(L, (1, 1, 12), mode=1) == H.ERR_UNSUPPORTED  # circular: not a power of two
-    assert b"power of two" in L.hyenand_last_error()
+    # circular, not a power of two: single pass only (transform >= 2L - 1 <= 16384)
+    assert call(L, (1, 1, 10000), mode=1) == H.ERR_UNSUPPORTED
+    assert b"no plan" in L.hyenand_last_error()
+    assert call(L, (1, 1, 12, 12, 12), mode=1) == H.ERR_UNSUPPORTED  # 3D: no single-pass plan
     assert call(L, (1, 1, 300, 300)) == H.ERR_UNSUPPORTED  # 512 x 512 transform beyond the single pass
     assert b"no plan" in L.hyenand_last_error()
 
@@ -93,8 +95,12 @@ def test_workspace_queries_are_host_only():
     assert H.plan_name((8, 256, 64, 64), "linear", "f32") == "fused2d"
     assert H.plan_name((2, 2, 1, 64), "linear", "bf16") == "fused1d"      # unit axis squeezed
     assert H.plan_name((2, 2, 1, 1, 1), "circular", "f32") == "fused1d"  # single point
+    # circular, not a power of two: the periodic kernel on the centred grid
+    assert H.plan_name((1, 1, 3), "circular", "f32") == "fused1d_any"
+    assert H.plan_name((2, 4, 14, 14), "circular", "f32") == "fused2d_any"
+    assert H.workspace_size((1, 1, 3), "circular", "f32") == 0
     with pytest.raises(H.HyenandError) as e:
-        H.workspace_size((1, 1, 3), "circular", "f32")
+        H.workspace_size((1, 1, 10000), "circular", "f32")
     assert e.value.status == H.ERR_UNSUPPORTED
     # other extents in the non-circular modes: transforms on the smallest power
     # of two >= 2L - 1, single pass
@@ -134,7 +140,9 @@ def test_backward_validation(L):
     assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 1 << 22)) == H.ERR_UNSUPPORTED       # 2^23 transform points
     assert bcall(L, (1, 2, 2048, 4)) == H.ERR_UNSUPPORTED       # 4096 points on an axis of a 2D grid
-    assert bcall(L, (1, 2, 12), mode=1) == H.ERR_UNSUPPORTED    # circular needs powers of two
+    # circular, not a power of two: embedded in the 32-point grid (nine
+    # tensors of 2 x 32 floats, 256 bytes each, then the gD sums)
+    assert bcall(L, (1, 2, 12), mode=1, ws_bytes=9 * 256) == H.ERR_WORKSPACE_TOO_SMALL
     # other extents (linear) run embedded in their transform grid: nine
     # embedded tensors of 2 x 32 floats (256 bytes each) plus the gD sums
     assert bcall(L, (1, 2, 12), ws_bytes=9 * 256) == H.ERR_WORKSPACE_TOO_SMALL
@@ -223,7 +231,7 @@ def test_operator_validation(L):
     assert ocall(L, (2, 3, 16), ws=None, ws_bytes=0) == H.ERR_WORKSPACE_TOO_SMALL
     assert ocall(L, (2, 3, 16), ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL  # 2 x 16 scales need 256 bytes
     assert ocall(L, (1, 1 << 15, 2)) == H.ERR_UNSUPPORTED  # more channels than the output norm's tile
-    assert ocall(L, (1, 2, 12), mode=1) == H.ERR_UNSUPPORTED  # circular, not a power of two
+    assert ocall(L, (1, 2, 10000), mode=1) == H.ERR_UNSUPPORTED  # circular, no single-pass plan
 
 
 def test_operator_workspace_size(L):

@@ -1,7 +1,9 @@
-"""Grid extents that are not powers of two (linear and centered modes): the
-single-pass kernels transform on the smallest power of two >= 2L - 1 and crop
-L points; parity with the fp64 oracle (which takes any extent) on 1D and 2D
-grids, fp32 and bf16, one kernel per channel and the HyenaND operator."""
+"""Grid extents that are not powers of two: the single-pass kernels transform
+on the smallest power of two >= 2L - 1 and crop L points (linear and centered
+modes; the circular mode as the centred convolution of the periodically
+repeated kernel); parity with the fp64 oracle (which takes any extent) on 1D
+and 2D grids, fp32 and bf16, one kernel per channel and the HyenaND
+operator."""
 import numpy as np
 import pytest
 
@@ -44,7 +46,7 @@ def _check(tag, B, C, grid, mode, dtype, seed, shared=False):
     f = [W.storage_to_f64(a, dtype) for a in (x1, x2, v, k, D)]
     if shared:
         f[3] = np.broadcast_to(f[3][None], (B,) + f[3].shape)
-    ref = oracle.conv_fft(*f, mode)
+    ref = (oracle.conv_direct if mode == "circular" else oracle.conv_fft)(*f, mode)
     err = rel_l2(got, ref)
     log(f"[any] {tag} {shape} {mode} {dtype} plan={plan}: rel_l2={err:.3e}")
     assert np.all(np.isfinite(got)) and err <= TOL[dtype]
@@ -65,6 +67,23 @@ def test_2d(grid, mode, dtype):
     assert _check("2d", 2, 3, grid, mode, dtype, sum(grid)) == "fused2d_any"
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("L", [3, 5, 12, 100, 1000, 3000])
+def test_1d_circular(L, dtype):
+    assert _check("1d-circ", 2, 3, (L,), "circular", dtype, 50 + L) == "fused1d_any"
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("grid", [(3, 5), (14, 14), (7, 30), (50, 60), (16, 14), (2, 3)])
+def test_2d_circular(grid, dtype):
+    assert _check("2d-circ", 2, 3, grid, "circular", dtype, 60 + sum(grid)) == "fused2d_any"
+
+
+@pytest.mark.parametrize("grid", [(100,), (14, 14)])
+def test_shared_kernel_circular(grid):
+    _check("shared-circ", 3, 2, grid, "circular", "f32", 8, shared=True)
+
+
 @pytest.mark.parametrize("grid", [(100,), (14, 14)])
 def test_shared_kernel(grid):
     _check("shared", 3, 2, grid, "centered", "f32", 7, shared=True)
@@ -76,7 +95,7 @@ def test_image_patch_grid_batch():
     _check("patches", 16, 384, (14, 14), "centered", "f32", 11)
 
 
-@pytest.mark.parametrize("grid,mode", [((14, 14), "centered"), ((300,), "linear")])
+@pytest.mark.parametrize("grid,mode", [((14, 14), "centered"), ((300,), "linear"), ((14, 14), "circular")])
 def test_operator(grid, mode):
     import torch
     from paper_2607_19378_amd import hyenand as H

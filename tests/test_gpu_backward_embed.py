@@ -1,6 +1,6 @@
 """Backward of the centred mode and of grid extents that are not powers of
-two (hyenand_fftconv_backward running the circular backward on the transform
-grid of the embedded tensors) against the oracle's direct-sum backward, every
+two, every pad mode (hyenand_fftconv_backward running the circular backward
+on the transform grid of the embedded tensors) against the oracle's direct-sum backward, every
 gradient, fp32 and bf16, 1D/2D/3D, and each circular plan underneath (single
 pass, multi-pass, four-step)."""
 import numpy as np
@@ -55,6 +55,15 @@ def test_centered(shape, dtype):
                                    (1, 2, 5, 6, 7)])
 def test_other_extents(shape, dtype):
     _check(shape, "linear", dtype, 21 + sum(shape))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 3, 3), (2, 3, 12), (1, 2, 1000), (2, 2, 14, 14), (1, 2, 7, 30),
+                                   (1, 2, 5, 6, 7)])
+def test_circular_other_extents(shape, dtype):
+    """Circular mode on extents that are not powers of two: the periodic
+    kernel embedded on the centred grid; gk gathers both displacements."""
+    _check(shape, "circular", dtype, 41 + sum(shape))
 
 
 def test_centered_long_line_four_step():

@@ -55,3 +55,36 @@ def test_circular_fft_needs_powers_of_two():
     x1, x2, v, k, D = _case(1, 1, (6,), 0, "circular")
     with pytest.raises(RuntimeError):
         oracle.conv_fft(x1, x2, v, k, D, "circular")
+
+
+@pytest.mark.parametrize("grid", [(3,), (6,), (12,), (3, 5), (14, 14), (5, 6, 7)])
+def test_circular_direct_matches_numpy_fft(grid):
+    """The circular mode on any extents (the direct sums) against numpy's
+    FFT of the same length: circular convolution = ifftn(fftn(u) fftn(k))."""
+    x1, x2, v, k, D = _case(2, 2, grid, 41 + sum(grid), "circular")
+    got = oracle.conv_direct(x1, x2, v, k, D, "circular")
+    ax = tuple(range(2, 2 + len(grid)))
+    u = x1 * v
+    conv = np.real(np.fft.ifftn(np.fft.fftn(u, axes=ax) * np.fft.fftn(k, axes=ax), axes=ax))
+    want = x2 * (conv + D.reshape((1, 2) + (1,) * len(grid)) * u)
+    assert np.allclose(got, want, rtol=1e-11, atol=1e-11)
+
+
+@pytest.mark.parametrize("grid", [(6,), (3, 5)])
+def test_circular_backward_direct_matches_numpy_fft(grid):
+    """Circular gradients on any extents against numpy FFT correlations:
+    gu = ifft(conj(K) H) + D h, gk = ifft(conj(U) H)."""
+    x1, x2, v, k, D = _case(1, 2, grid, 51 + sum(grid), "circular")
+    gy = np.random.default_rng(9).standard_normal(x1.shape)
+    gx1, gx2, gv, gk, gD = oracle.backward_direct(x1, x2, v, k, D, gy, "circular")
+    ax = tuple(range(2, 2 + len(grid)))
+    F = lambda a: np.fft.fftn(a, axes=ax)
+    iF = lambda a: np.real(np.fft.ifftn(a, axes=ax))
+    u, h = x1 * v, gy * x2
+    Dc = D.reshape((1, 2) + (1,) * len(grid))
+    gu = iF(np.conj(F(k)) * F(h)) + Dc * h
+    assert np.allclose(gx1, gu * v, rtol=1e-11, atol=1e-11)
+    assert np.allclose(gv, gu * x1, rtol=1e-11, atol=1e-11)
+    assert np.allclose(gk, iF(np.conj(F(u)) * F(h)), rtol=1e-11, atol=1e-11)
+    assert np.allclose(gx2, gy * (iF(F(u) * F(k)) + Dc * u), rtol=1e-11, atol=1e-11)
+    assert np.allclose(gD, (h * u).sum(axis=(0,) + ax), rtol=1e-11, atol=1e-11)
