@@ -19,6 +19,13 @@
 // transposed (row = output unit or channel), so that the four steps of a
 // block take one 16-byte read per lane.  Points' coordinates are generated
 // from their index; K is written once.
+//
+// For a bf16 kernel tensor the products run on v_mfma_f32_16x16x32_bf16
+// instead (weights and activations rounded to bf16, fp32 accumulate; the
+// sines, FiLM and window stay fp32): step s of the contraction takes units
+// (2 s + hi) * 16 + 4 g + r (hi, r < 2, 4) from lane group g, i.e. two of the
+// lane's own register quads, and the weights sit in LDS as bf16 in that
+// order, eight per 16-byte read.
 #include <algorithm>
 #include <mutex>
 
@@ -29,6 +36,7 @@ namespace hyenand {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 constexpr int kSynthWaves = 8;  // waves per workgroup, one 16-point tile each
 constexpr int kThreads = 64 * kSynthWaves;
@@ -73,8 +81,30 @@ __device__ void stage_params(const SynthArgs& a, float* lds, int HF) {
 // Staging: wave w copies rows w, w + 8, ... of a matrix for 64 consecutive
 // output columns at a time, one column per lane: global reads coalesced, no
 // division, HF / 8 loads in flight per lane before its LDS stores.
+// Row stride (in floats) of a staged matrix: HF fp32 values + 4, or HF bf16
+// values + 8 (16 bytes of pad either way).
+template <int HF, bool BF>
+constexpr int row_floats() {
+  return BF ? HF / 2 + 4 : HF + 4;
+}
+
+// Position of input unit k within a bf16 row: step s = k / 32 of the
+// contraction, lane group g = (k % 16) / 4, then the unit's quad (hi = which
+// 16-unit block of the step) and r = k % 4.
+__device__ __forceinline__ int bf_pos(int k) { return (k >> 5) * 32 + ((k >> 2) & 3) * 8 + ((k >> 4) & 1) * 4 + (k & 3); }
+
+// value v of input unit k in row o of a staged matrix
+template <int HF, bool BF>
+__device__ __forceinline__ void stage_put(float* dst, int o, int k, float v) {
+  if constexpr (BF) {
+    reinterpret_cast<__bf16*>(dst)[o * 2 * row_floats<HF, BF>() + bf_pos(k)] = (__bf16)v;
+  } else {
+    dst[o * row_floats<HF, BF>() + k] = v;
+  }
+}
+
 // W_j [k][o] -> dst[o][k]
-template <int HF>
+template <int HF, bool BF>
 __device__ void stage_hidden(const SynthArgs& a, float* dst, int j) {
   const float* W = a.Wh + (int64_t)(j - 1) * HF * HF;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -86,7 +116,7 @@ __device__ void stage_hidden(const SynthArgs& a, float* dst, int j) {
 #pragma unroll
       for (int kk = 0; kk < HF / kSynthWaves; ++kk) v[kk] = W[(w + kSynthWaves * kk) * HF + o];
 #pragma unroll
-      for (int kk = 0; kk < HF / kSynthWaves; ++kk) dst[o * (HF + 4) + w + kSynthWaves * kk] = v[kk];
+      for (int kk = 0; kk < HF / kSynthWaves; ++kk) stage_put<HF, BF>(dst, o, w + kSynthWaves * kk, v[kk]);
     }
   }
 }
@@ -111,7 +141,7 @@ __device__ void stage_q(const SynthArgs& a, float* q, int c0, int n, int ld) {
 
 // Wout[:, c0 : c0 + n] -> dst[c][k] for c < ld (ld a multiple of 64; rows
 // past n zero), then q[3][ld]
-template <int HF>
+template <int HF, bool BF>
 __device__ void stage_out(const SynthArgs& a, float* dst, int c0, int n, int ld) {
   const int C = a.C;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -123,9 +153,9 @@ __device__ void stage_out(const SynthArgs& a, float* dst, int c0, int n, int ld)
 #pragma unroll
     for (int kk = 0; kk < HF / kSynthWaves; ++kk) v[kk] = in ? src[(int64_t)(w + kSynthWaves * kk) * C] : 0.f;
 #pragma unroll
-    for (int kk = 0; kk < HF / kSynthWaves; ++kk) dst[c * (HF + 4) + w + kSynthWaves * kk] = v[kk];
+    for (int kk = 0; kk < HF / kSynthWaves; ++kk) stage_put<HF, BF>(dst, c, w + kSynthWaves * kk, v[kk]);
   }
-  stage_q(a, dst + ld * (HF + 4), c0, n, ld);
+  stage_q(a, dst + ld * row_floats<HF, BF>(), c0, n, ld);
 }
 
 // FiLM scale and shift of layer j for this lane's units t * 16 + 4 g + r,
@@ -175,6 +205,48 @@ __device__ __forceinline__ void chains(const float* const (&rows)[NT], const v4f
   }
 }
 
+// the same on the bf16 matrix cores: hb[s] holds the lane's units of step s
+// (register quads 2 s and 2 s + 1) in bf16; rows[i] points at this lane's
+// bf16 row of tile i
+template <int HF, int NT>
+__device__ __forceinline__ void chains_bf(const float* const (&rows)[NT], const v8bf (&hb)[HF / 32], int g,
+                                          v4f (&acc)[NT]) {
+  v8bf w[2][NT];
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    acc[i] = v4f{};
+    w[0][i] = *reinterpret_cast<const v8bf*>(reinterpret_cast<const __bf16*>(rows[i]) + 8 * g);
+  }
+#pragma unroll
+  for (int st = 0; st < HF / 32; ++st) {
+    if (st + 1 < HF / 32)
+#pragma unroll
+      for (int i = 0; i < NT; ++i)
+        w[(st + 1) & 1][i] = *reinterpret_cast<const v8bf*>(reinterpret_cast<const __bf16*>(rows[i]) + (st + 1) * 32 + 8 * g);
+#pragma unroll
+    for (int i = 0; i < NT; ++i) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[st & 1][i], hb[st], acc[i], 0, 0, 0);
+  }
+}
+
+template <int HF>
+__device__ __forceinline__ void to_bf(const v4f (&h)[HF / 16], v8bf (&hb)[HF / 32]) {
+#pragma unroll
+  for (int st = 0; st < HF / 32; ++st)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      hb[st][r] = (__bf16)h[2 * st][r];
+      hb[st][4 + r] = (__bf16)h[2 * st + 1][r];
+    }
+}
+
+// NT output tiles through the fp32 or the bf16 products
+template <int HF, int NT, bool BF>
+__device__ __forceinline__ void tile_products(const float* const (&rows)[NT], const v4f (&h)[HF / 16], const v8bf (&hb)[HF / 32],
+                                      int g, v4f (&acc)[NT]) {
+  if constexpr (BF) chains_bf<HF, NT>(rows, hb, g, acc);
+  else chains<HF, NT>(rows, h, g, acc);
+}
+
 // window and store of one 16-channel tile: channels cb + 4 g + r of point p
 // (CHECK: skip channels at or past n; tbase points at channel c0)
 template <typename TS, bool CHECK>
@@ -193,10 +265,10 @@ __device__ __forceinline__ void store_tile(const v4f& acc, TS* tbase, int64_t np
   }
 }
 
-template <int HF, bool FILM, typename TS>
+template <int HF, bool FILM, typename TS, bool BF>
 __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
   constexpr int OT = HF / 16;  // 16-unit blocks of the hidden width
-  constexpr int LDW = HF + 4;  // row stride of a staged matrix
+  constexpr int LDW = row_floats<HF, BF>();  // row stride of a staged matrix
   constexpr int NT = HF >= 128 ? 2 : 4;  // output tiles per group
   extern __shared__ float lds[];
   const int lane = threadIdx.x & 63, g = lane >> 4, pl = lane & 15;
@@ -222,8 +294,8 @@ __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
   }
   stage_params(a, lds, HF);
   if (resident) {
-    for (int j = 1; j < J; ++j) stage_hidden<HF>(a, lds + M0 + (j - 1) * HF * LDW, j);
-    stage_out<HF>(a, lds + out_off, 0, C, ldo);
+    for (int j = 1; j < J; ++j) stage_hidden<HF, BF>(a, lds + M0 + (j - 1) * HF * LDW, j);
+    stage_out<HF, BF>(a, lds + out_off, 0, C, ldo);
   }
   __syncthreads();
 
@@ -275,7 +347,7 @@ __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
       const float* W = lds + M0 + (resident ? (j - 1) * HF * LDW : 0);
       if (!resident) {
         __syncthreads();
-        stage_hidden<HF>(a, lds + M0, j);
+        stage_hidden<HF, BF>(a, lds + M0, j);
         __syncthreads();
       }
       if (live) {
@@ -283,13 +355,15 @@ __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
         film_load<HF, FILM>(a, film_lds, b, j, g, gm, bt);
         constexpr int NH = OT < NT ? OT : NT;  // hidden tiles per group
         v4f acc[OT];
+        v8bf hb[HF / 32];
+        if constexpr (BF) to_bf<HF>(h, hb);
 #pragma unroll
         for (int t0 = 0; t0 < OT; t0 += NH) {
           const float* rows[NH];
           v4f part[NH];
 #pragma unroll
           for (int i = 0; i < NH; ++i) rows[i] = W + ((t0 + i) * 16 + pl) * LDW;
-          chains<HF, NH>(rows, h, g, part);
+          tile_products<HF, NH, BF>(rows, h, hb, g, part);
 #pragma unroll
           for (int i = 0; i < NH; ++i) acc[t0 + i] = part[i];
         }
@@ -316,7 +390,7 @@ __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
       const int n = min(ldo, C - c0);
       if (!resident) {
         __syncthreads();
-        stage_out<HF>(a, lds + M0, c0, n, ldo);
+        stage_out<HF, BF>(a, lds + M0, c0, n, ldo);
         __syncthreads();
       }
       if (!live) continue;
@@ -324,12 +398,14 @@ __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
       const float* q = Wo + ldo * LDW;
       TS* cbase = out + (int64_t)c0 * a.npos;
       const bool full = p0 + 16 <= a.npos && n % (16 * NT) == 0;  // uniform
+      v8bf hb[HF / 32];
+      if constexpr (BF) to_bf<HF>(h, hb);
       for (int ct = 0; ct < n; ct += 16 * NT) {
         const float* rows[NT];
 #pragma unroll
         for (int i = 0; i < NT; ++i) rows[i] = Wo + (ct + 16 * i + pl) * LDW;
         v4f acc[NT];
-        chains<HF, NT>(rows, h, g, acc);
+        tile_products<HF, NT, BF>(rows, h, hb, g, acc);
         if (full) {
 #pragma unroll
           for (int i = 0; i < NT; ++i) store_tile<TS, false>(acc[i], cbase, a.npos, p, q, ldo, ct + 16 * i, n, g, sd);
@@ -344,8 +420,8 @@ __global__ void __launch_bounds__(kThreads) siren_synth(SynthArgs a) {
 
 // LDS floats of a launch: the parameter block plus either every weight
 // (resident) or one streamed region, plus the FiLM block when kept in LDS
-size_t lds_floats(const SynthArgs& a, bool resident) {
-  const size_t H = a.hidden, J = a.J, C = ((size_t)a.C + 63) & ~size_t(63), LDW = H + 4;
+size_t lds_floats(const SynthArgs& a, bool resident, bool bf) {
+  const size_t H = a.hidden, J = a.J, C = ((size_t)a.C + 63) & ~size_t(63), LDW = bf ? H / 2 + 4 : H + 4;
   const size_t par = ((4 + J) * H + 3) & ~size_t(3);
   const size_t film = a.film_lds ? 2 * (size_t)a.nb * J * H : 0;
   if (resident) return par + (J - 1) * H * LDW + (LDW + 3) * C + film;
@@ -371,15 +447,16 @@ hipError_t launch_one(K kernel, int64_t grid, dim3 block, size_t bytes, hipStrea
 
 template <typename TS, bool FILM>
 hipError_t launch_film(SynthArgs a, hipStream_t s) {
+  constexpr bool BF = sizeof(TS) == 2;  // bf16 output: bf16 products
   // stream the weights when they do not all fit next to each other
   a.cc = 64 * std::max(1, (int)(16384 / a.hidden / 64));  // output channels per streamed chunk
-  const int LDW = a.hidden + 4;
+  const int LDW = BF ? a.hidden / 2 + 4 : a.hidden + 4;
   a.stream_floats = (int)std::max(a.hidden * LDW, (LDW + 3) * a.cc);
   // FiLM rows of every sample in LDS when they take at most 32 KiB
   a.film_lds = FILM && 2 * a.nb * a.J * a.hidden * 4 <= 32 * 1024;
-  const size_t res_bytes = lds_floats(a, true) * 4;
+  const size_t res_bytes = lds_floats(a, true, BF) * 4;
   a.resident = res_bytes <= kLdsLimit - 8 * 1024;
-  const size_t bytes = lds_floats(a, a.resident) * 4;
+  const size_t bytes = lds_floats(a, a.resident, BF) * 4;
   static int ncu = 0;
   if (ncu == 0) {
     int dev = 0;
@@ -392,9 +469,9 @@ hipError_t launch_film(SynthArgs a, hipStream_t s) {
   const int64_t grid = std::min<int64_t>(groups, (int64_t)ncu * std::min(per_cu, 2));
   const dim3 block(64 * kSynthWaves);
   switch (a.hidden) {
-    case 32: return launch_one(siren_synth<32, FILM, TS>, grid, block, bytes, s, a);
-    case 64: return launch_one(siren_synth<64, FILM, TS>, grid, block, bytes, s, a);
-    case 128: return launch_one(siren_synth<128, FILM, TS>, grid, block, bytes, s, a);
+    case 32: return launch_one(siren_synth<32, FILM, TS, BF>, grid, block, bytes, s, a);
+    case 64: return launch_one(siren_synth<64, FILM, TS, BF>, grid, block, bytes, s, a);
+    case 128: return launch_one(siren_synth<128, FILM, TS, BF>, grid, block, bytes, s, a);
     default: return hipErrorInvalidValue;
   }
 }

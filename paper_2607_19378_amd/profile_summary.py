@@ -132,9 +132,12 @@ def synth_summary(a, W, source_hash):
     for r in stats:
         lines.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    mpeak, mkind = ((bench.MFMA_BF16_PEAK_TFLOPS, "bf16") if w.dtype == "bf16"
+                    else (bench.MFMA_F32_PEAK_TFLOPS, "fp32"))
     lines += ["", f"siren_synth: {flops / 1e9:.3f} GFLOP of matrix-core multiply-adds per call in "
-                  f"{avg_ns / 1e3:.2f} us = {tf:.1f} TFLOP/s, {100 * tf / bench.MFMA_F32_PEAK_TFLOPS:.1f}% of the "
-                  f"{bench.MFMA_F32_PEAK_TFLOPS} TFLOP/s fp32 matrix peak.", "",
+                  f"{avg_ns / 1e3:.2f} us = {tf:.1f} TFLOP/s, {100 * tf / mpeak:.1f}% of the "
+                  f"{mpeak} TFLOP/s {mkind} matrix peak; the k write alone takes {k_bytes / 8e12 * 1e6:.1f} us "
+                  f"at 8 TB/s ({100 * k_bytes / (avg_ns * 1e-9) / 8e12:.1f}% of it achieved).", "",
               "## HBM traffic per siren_synth dispatch (rocprofv3 --pmc)", "",
               f"Copy calibration: {a.copy_mib} MiB device copy read {f_copy:.1f} KiB (FETCH_SIZE) and wrote "
               f"{w_copy:.1f} KiB (WRITE_SIZE).", "",
