@@ -72,8 +72,16 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  *                   non-circular convolution; in circular mode the kernel is
  *                   repeated periodically over the displacements
  *                   -(L_d - 1) .. L_d - 1, which makes the circular
- *                   convolution a non-circular one), in one pass per line:
- *                   1D up to L = 8192, 2D up to 128-point transforms per axis.
+ *                   convolution a non-circular one): in one pass per line
+ *                   for 1D up to L = 8192 and 2D up to 128-point transforms
+ *                   per axis; beyond that (and in 3D) embedded in the
+ *                   transform grid, where the call is the circular
+ *                   convolution of the zero-padded inputs and of k placed at
+ *                   its displacements: x1, x2, v and k are copied into the
+ *                   workspace on that grid, the circular plan runs there and
+ *                   y is copied back (the workspace queries include the five
+ *                   embedded tensors).  The operator takes the single-pass
+ *                   shapes only.
  * pad_mode        : hyenand_pad_mode.
  * dtype           : hyenand_dtype.
  * workspace       : device scratch of workspace_bytes (16-byte aligned), owned
@@ -127,8 +135,9 @@ hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int 
                                              int dtype, size_t* bytes_out);
 
 /* Name of the plan the call would use ("fused1d", "fused2d", "multipass2d",
- * "multipass3d", "fourstep1d"), written NUL-terminated into buf (at most n
- * bytes).  Pure host function. */
+ * "multipass3d", "fourstep1d"; for extents that are not powers of two
+ * "fused1d_any", "fused2d_any" or "embedded1d/2d/3d"), written
+ * NUL-terminated into buf (at most n bytes).  Pure host function. */
 hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_mode, int dtype,
                                          char* buf, size_t n);
 

@@ -16,6 +16,8 @@
 //   embed     x1, x2, v, gy into the first L_d points of every axis of a
 //             P-grid (zeros elsewhere), k at its displacements;
 //   circular backward on the P-grid (every plan of the circular mode);
+//   (the forward of shapes without a single-pass plan takes the same route:
+//   x1, x2, v and k embedded, the circular forward, y extracted)
 //   extract   gx1, gx2, gv from the first L_d points, gk from the kernel's
 //             displacements; gD comes straight from the circular backward
 //             (the zeros add nothing).
@@ -98,11 +100,12 @@ __global__ void __launch_bounds__(256)
   ex1[i] = in ? x1[s] : zero;
   ex2[i] = in ? x2[s] : zero;
   ev[i] = in ? v[s] : zero;
-  egy[i] = in ? gy[s] : zero;
+  if (egy) egy[i] = in ? gy[s] : zero;  // the backward's gy (none for the forward)
   ek[i] = kin ? k[(shared_k ? line % C : line) * g.kbox + ksrc] : zero;
 }
 
-// gx1, gx2, gv back from the first L_d points of every axis
+// gx1, gx2, gv (or the forward's y alone) back from the first L_d points of
+// every axis
 template <typename TS>
 __global__ void __launch_bounds__(256)
     extract_data(const TS* __restrict__ e1, const TS* __restrict__ e2, const TS* __restrict__ e3,
@@ -118,8 +121,8 @@ __global__ void __launch_bounds__(256)
   int64_t e = line;
   for (int d = 0; d < g.nd; ++d) e = (e << g.lp[d]) + q[d];
   o1[i] = e1[e];
-  o2[i] = e2[e];
-  o3[i] = e3[e];
+  if (o2) o2[i] = e2[e];
+  if (o3) o3[i] = e3[e];
 }
 
 // gk back from the kernel's displacements (periodic: the sum over the one or
@@ -173,6 +176,39 @@ hipError_t launch_embed(const FftConvArgs& a, const void* gy, void* const (&e)[5
     hipLaunchKernelGGL(embed_inputs<T>, dim3(blocks(total)), dim3(256), 0, s, (const T*)a.x1, (const T*)a.x2,
                        (const T*)a.v, (const T*)gy, (const T*)a.k, (T*)e[0], (T*)e[1], (T*)e[2], (T*)e[3], (T*)e[4],
                        g, total, shared, a.C);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_fwd(const FftConvArgs& a, void* const (&e)[4], hipStream_t s) {
+  const EmbedGeom g = embed_geom(a);
+  const int64_t total = a.lines * g.grid;
+  const bool shared = a.kC != 0;
+  if (a.bf16) {
+    using T = uint16_t;
+    hipLaunchKernelGGL(embed_inputs<T>, dim3(blocks(total)), dim3(256), 0, s, (const T*)a.x1, (const T*)a.x2,
+                       (const T*)a.v, (const T*)nullptr, (const T*)a.k, (T*)e[0], (T*)e[1], (T*)e[2], (T*)nullptr,
+                       (T*)e[3], g, total, shared, a.C);
+  } else {
+    using T = float;
+    hipLaunchKernelGGL(embed_inputs<T>, dim3(blocks(total)), dim3(256), 0, s, (const T*)a.x1, (const T*)a.x2,
+                       (const T*)a.v, (const T*)nullptr, (const T*)a.k, (T*)e[0], (T*)e[1], (T*)e[2], (T*)nullptr,
+                       (T*)e[3], g, total, shared, a.C);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_extract_y(const FftConvArgs& a, const void* ey, void* y, hipStream_t s) {
+  const EmbedGeom g = embed_geom(a);
+  const int64_t nd = a.lines * g.box;
+  if (a.bf16) {
+    using T = uint16_t;
+    hipLaunchKernelGGL(extract_data<T>, dim3(blocks(nd)), dim3(256), 0, s, (const T*)ey, (const T*)nullptr,
+                       (const T*)nullptr, (T*)y, (T*)nullptr, (T*)nullptr, g, nd);
+  } else {
+    using T = float;
+    hipLaunchKernelGGL(extract_data<T>, dim3(blocks(nd)), dim3(256), 0, s, (const T*)ey, (const T*)nullptr,
+                       (const T*)nullptr, (T*)y, (T*)nullptr, (T*)nullptr, g, nd);
   }
   return hipGetLastError();
 }

@@ -29,7 +29,7 @@ hyenand_status fail(hyenand_status s, const char* fmt, ...) {
   return s;
 }
 
-enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP, PLAN_FUSED_RL };
+enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP, PLAN_FUSED_RL, PLAN_EMBED };
 
 const char* plan_name(Plan p, int ndim) {
   switch (p) {
@@ -38,6 +38,7 @@ const char* plan_name(Plan p, int ndim) {
     case PLAN_MULTIPASS: return ndim == 3 ? "multipass3d" : "multipass2d";
     case PLAN_FOURSTEP: return "fourstep1d";
     case PLAN_FUSED_RL: return ndim == 1 ? "fused1d_any" : "fused2d_any";
+    case PLAN_EMBED: return ndim == 1 ? "embedded1d" : (ndim == 2 ? "embedded2d" : "embedded3d");
     default: return "none";
   }
 }
@@ -100,8 +101,48 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   return HYENAND_OK;
 }
 
+// A shape whose extents are not powers of two and that no single-pass kernel
+// takes runs embedded in its transform grid (P_d >= 2 L_d - 1, a power of
+// two): on that grid the call is the circular convolution of the zero-padded
+// inputs and of k placed at its displacements (conv_embed.hip), so x1, x2, v
+// and k are embedded, the circular plan of the grid runs, and y is extracted.
+// The workspace holds the five embedded tensors (x1, x2, v, k, y; each
+// 256-byte aligned) and then the circular plan's own.
+struct GridProblem {
+  FftConvArgs e;  // the circular problem on the transform grid
+  int nd;
+  int64_t dims[5];
+  size_t tensor;  // bytes of one embedded tensor
+};
+
+bool grid_problem(const FftConvArgs& a, GridProblem* m) {
+  m->nd = a.ndim;
+  m->dims[0] = a.lines / a.C;
+  m->dims[1] = a.C;
+  for (int d = 0; d < a.ndim; ++d) m->dims[2 + d] = a.P[d];
+  const std::string keep = g_last_error;
+  const hyenand_status st = parse_shape(m->nd, m->dims, HYENAND_PAD_CIRCULAR,
+                                        a.bf16 ? HYENAND_DTYPE_BF16 : HYENAND_DTYPE_F32, &m->e);
+  g_last_error = keep;
+  m->tensor = ((size_t)embed_grid_elems(a) * (a.bf16 ? 2 : 4) + 255) / 256 * 256;
+  return st == HYENAND_OK;
+}
+
+Plan choose_plan(const FftConvArgs& a);
+
+// the circular plan of the grid problem of an embedded forward
+Plan embedded_inner_plan(const FftConvArgs& a, GridProblem* m) {
+  if (!grid_problem(a, m)) return PLAN_NONE;
+  const Plan p = choose_plan(m->e);
+  return p == PLAN_EMBED ? PLAN_NONE : p;
+}
+
 Plan choose_plan(const FftConvArgs& a) {
-  if (a.rl) return fused_rl_supported(a) ? PLAN_FUSED_RL : PLAN_NONE;
+  if (a.rl) {
+    if (fused_rl_supported(a)) return PLAN_FUSED_RL;
+    GridProblem m;
+    return embedded_inner_plan(a, &m) != PLAN_NONE ? PLAN_EMBED : PLAN_NONE;
+  }
   const char* force = getenv("HYENAND_PLAN");
   const bool no_fused = force && (strcmp(force, "multipass") == 0 || strcmp(force, "fourstep") == 0);
   if (a.ndim == 1) {
@@ -114,9 +155,16 @@ Plan choose_plan(const FftConvArgs& a) {
   return PLAN_NONE;
 }
 
+size_t bytes_per_line(const FftConvArgs& a, Plan p);
+
+// workspace of an embedded forward: the five tensors, then the inner plan's
+// least (or recommended) workspace
+size_t embed_fwd_ws(const FftConvArgs& a, bool recommended);
+
 size_t bytes_per_line(const FftConvArgs& a, Plan p) {
   if (p == PLAN_MULTIPASS) return multipass_bytes_per_line(a);
   if (p == PLAN_FOURSTEP) return fourstep_bytes_per_line(a);
+  if (p == PLAN_EMBED) return embed_fwd_ws(a, false);  // the least workspace of the whole call
   return 0;
 }
 
@@ -174,6 +222,7 @@ ChunkPlan plan_chunks(int64_t lines, size_t per, size_t ws_bytes) {
 }
 
 size_t recommended_ws(const FftConvArgs& a, Plan p) {
+  if (p == PLAN_EMBED) return embed_fwd_ws(a, true);
   const size_t per = bytes_per_line(a, p);
   if (per == 0) return 0;
   const int ns = chunk_streams(per);
@@ -182,6 +231,13 @@ size_t recommended_ws(const FftConvArgs& a, Plan p) {
   n *= ns;
   if (n > a.lines) n = a.lines;
   return (size_t)n * per;
+}
+
+size_t embed_fwd_ws(const FftConvArgs& a, bool recommended) {
+  GridProblem m;
+  const Plan pi = embedded_inner_plan(a, &m);
+  if (pi == PLAN_NONE) return 0;
+  return 5 * m.tensor + (recommended ? recommended_ws(m.e, pi) : bytes_per_line(m.e, pi));
 }
 
 // Non-blocking side streams per device, created on first use and kept for
@@ -463,6 +519,22 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   a.x1 = x1; a.x2 = x2; a.v = v; a.k = k; a.D = D; a.y = y;
   a.ws = workspace;
   a.ws_bytes = workspace_bytes;
+  if (p == PLAN_EMBED) {
+    // x1, x2, v, k into the transform grid, the circular plan there, y back
+    GridProblem m;
+    embedded_inner_plan(a, &m);
+    char* w = (char*)workspace;
+    void* const e[4] = {w, w + m.tensor, w + 2 * m.tensor, w + 3 * m.tensor};
+    void* const ey = w + 4 * m.tensor;
+    hipError_t err = launch_embed_fwd(a, e, (hipStream_t)stream);
+    if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+    const hyenand_status inner = forward(e[0], e[1], e[2], e[3], D, ey, m.nd, m.dims, HYENAND_PAD_CIRCULAR, dtype,
+                                         w + 5 * m.tensor, workspace_bytes - 5 * m.tensor, stream, false);
+    if (inner != HYENAND_OK) return inner;
+    err = launch_extract_y(a, ey, y, (hipStream_t)stream);
+    if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+    return HYENAND_OK;
+  }
   const hipError_t err = launch_plan(a, p, per, (hipStream_t)stream);
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
   return HYENAND_OK;
@@ -508,7 +580,8 @@ hyenand_status operator_fwd(const void* q, const void* kin, const void* vin, con
   for (int i = 0; i < 7; ++i)
     if (overlaps(y, nb, ptrs[i], bytes[i])) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", pn[i]);
   const Plan p = choose_plan(a);
-  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  if (p == PLAN_NONE || p == PLAN_EMBED)
+    return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape in the operator");
   const size_t sb = op_scale_bytes(a);
   const size_t per = bytes_per_line(a, p);
   if (!workspace || workspace_bytes < sb + per)
@@ -715,7 +788,8 @@ hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, in
   hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
   if (st != HYENAND_OK) return st;
   const Plan p = choose_plan(a);
-  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  if (p == PLAN_NONE || p == PLAN_EMBED)
+    return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape in the operator");
   *bytes_out = op_scale_bytes(a) + recommended_ws(a, p);
   return HYENAND_OK;
 }

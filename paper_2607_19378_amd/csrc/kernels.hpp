@@ -77,6 +77,9 @@ int64_t embed_grid_elems(const FftConvArgs& a);
 hipError_t launch_embed(const FftConvArgs& a, const void* gy, void* const (&e)[5], hipStream_t s);
 hipError_t launch_extract(const FftConvArgs& a, void* const (&e)[4], void* gx1, void* gx2, void* gv, void* gk,
                           hipStream_t s);
+// forward of the same shapes: x1, x2, v, k embedded (e[0..3]), y extracted
+hipError_t launch_embed_fwd(const FftConvArgs& a, void* const (&e)[4], hipStream_t s);
+hipError_t launch_extract_y(const FftConvArgs& a, const void* ey, void* y, hipStream_t s);
 
 // multi-pass 1D (four-step split of the long line); one call per chunk of
 // lines, as for launch_multipass

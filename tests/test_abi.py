@@ -61,11 +61,13 @@ def test_invalid_arguments(L):
     assert call(L, (1, 0, 16)) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), mode=3) == H.ERR_INVALID_ARGUMENT
     assert call(L, (1, 1, 16), dtype=5) == H.ERR_INVALID_ARGUMENT
-    # circular, not a power of two: single pass only (transform >= 2L - 1 <= 16384)
-    assert call(L, (1, 1, 10000), mode=1) == H.ERR_UNSUPPORTED
-    assert b"no plan" in L.hyenand_last_error()
-    assert call(L, (1, 1, 12, 12, 12), mode=1) == H.ERR_UNSUPPORTED  # 3D: no single-pass plan
-    assert call(L, (1, 1, 300, 300)) == H.ERR_UNSUPPORTED  # 512 x 512 transform beyond the single pass
+    # extents that are not powers of two beyond the single-pass kernels run
+    # embedded in their transform grid, which needs a workspace
+    assert call(L, (1, 1, 10000), mode=1) == H.ERR_WORKSPACE_TOO_SMALL
+    assert call(L, (1, 1, 12, 12, 12), mode=1) == H.ERR_WORKSPACE_TOO_SMALL
+    assert call(L, (1, 1, 300, 300)) == H.ERR_WORKSPACE_TOO_SMALL  # a 1024 x 1024 grid
+    assert call(L, (1, 1, 300, 300), ws=FAKE + (40 << 36), ws_bytes=5 * (4 << 20)) == H.ERR_WORKSPACE_TOO_SMALL
+    assert call(L, (1, 1, 600, 600)) == H.ERR_UNSUPPORTED  # a 2048-point axis: beyond every plan
     assert b"no plan" in L.hyenand_last_error()
 
 
@@ -99,17 +101,21 @@ def test_workspace_queries_are_host_only():
     assert H.plan_name((1, 1, 3), "circular", "f32") == "fused1d_any"
     assert H.plan_name((2, 4, 14, 14), "circular", "f32") == "fused2d_any"
     assert H.workspace_size((1, 1, 3), "circular", "f32") == 0
-    with pytest.raises(H.HyenandError) as e:
-        H.workspace_size((1, 1, 10000), "circular", "f32")
-    assert e.value.status == H.ERR_UNSUPPORTED
+    assert H.plan_name((1, 1, 10000), "circular", "f32") == "embedded1d"
     # other extents in the non-circular modes: transforms on the smallest power
     # of two >= 2L - 1, single pass
     assert H.plan_name((1, 1, 3), "linear", "f32") == "fused1d_any"
     assert H.plan_name((2, 4, 14, 14), "centered", "f32") == "fused2d_any"
     assert H.plan_name((2, 4, 14, 16), "linear", "bf16") == "fused2d_any"
     assert H.workspace_size((2, 4, 14, 14), "linear", "f32") == 0
+    # beyond the single pass: embedded in the 256 x 256 grid; five embedded
+    # tensors of 256^2 floats, then the circular multi-pass plan's workspace
+    assert H.plan_name((1, 1, 100, 100), "linear", "f32") == "embedded2d"
+    assert H.plan_name((1, 2, 48, 48, 48), "centered", "bf16") == "embedded3d"
+    assert H.workspace_min((1, 1, 100, 100), "linear", "f32") == (
+        5 * 256 * 256 * 4 + H.workspace_min((1, 1, 256, 256), "circular", "f32"))
     with pytest.raises(H.HyenandError):
-        H.plan_name((1, 1, 100, 100), "linear", "f32")  # 256 x 256: beyond the single pass
+        H.plan_name((1, 1, 600, 600), "linear", "f32")
 
 
 def bcall(L, shape, mode=0, dtype=0, ptrs=None, ws=FAKE + (40 << 36), ws_bytes=1 << 20):
@@ -232,6 +238,7 @@ def test_operator_validation(L):
     assert ocall(L, (2, 3, 16), ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL  # 2 x 16 scales need 256 bytes
     assert ocall(L, (1, 1 << 15, 2)) == H.ERR_UNSUPPORTED  # more channels than the output norm's tile
     assert ocall(L, (1, 2, 10000), mode=1) == H.ERR_UNSUPPORTED  # circular, no single-pass plan
+    assert ocall(L, (1, 2, 100, 100)) == H.ERR_UNSUPPORTED  # embedded shapes: not in the operator
 
 
 def test_operator_workspace_size(L):

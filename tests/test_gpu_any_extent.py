@@ -112,3 +112,16 @@ def test_operator(grid, mode):
     err = rel_l2(from_device(y), ref)
     log(f"[any] operator {shape} {mode}: rel_l2={err:.3e}")
     assert err <= TOL["f32"]
+
+
+@pytest.mark.parametrize("shape,mode,dtype", [
+    ((1, 2, 20000), "linear", "f32"), ((1, 2, 10000), "circular", "f32"), ((2, 2, 9000), "centered", "bf16"),
+    ((1, 2, 100, 100), "linear", "f32"), ((1, 2, 300, 50), "centered", "f32"), ((2, 2, 70, 90), "circular", "bf16"),
+    ((1, 2, 48, 48, 48), "linear", "f32"), ((1, 2, 20, 24, 28), "centered", "bf16"), ((1, 2, 5, 6, 7), "circular", "f32"),
+])
+def test_embedded_plans(shape, mode, dtype):
+    """Shapes beyond the single-pass kernels (long 1D lines, large 2D images,
+    every 3D grid, e.g. the 48^3 volumes of the medical-imaging experiments):
+    x1, x2, v, k embedded in the transform grid, the circular plan there."""
+    plan = _check("embedded", shape[0], shape[1], shape[2:], mode, dtype, 70 + sum(shape))
+    assert plan.startswith("embedded")
