@@ -422,12 +422,15 @@ __device__ __forceinline__ void batched_copy(int tid, const Ld& ld, const St& st
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float ld1(const float* p) { return *p; }
 __device__ __forceinline__ float ld1(const uint16_t* p) { return __uint_as_float(((uint32_t)*p) << 16); }
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+// fp32 -> bf16 with round to nearest even (NaN stays NaN): gfx950 converts a
+// pair in one instruction (v_cvt_pk_bf16_f32)
+typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+typedef float f32x2_v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16_pack(float lo, float hi) {
+  const f32x2_v v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
 }
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 __device__ __forceinline__ void st1(float* p, float x) { *p = x; }
 __device__ __forceinline__ void st1(uint16_t* p, float x) { *p = f32_to_bf16_rne(x); }
 // four consecutive values (p aligned to four elements)
@@ -440,8 +443,8 @@ __device__ __forceinline__ float4 ld4(const uint16_t* p) {
 __device__ __forceinline__ void st4(float* p, float4 x) { *reinterpret_cast<float4*>(p) = x; }
 __device__ __forceinline__ void st4(uint16_t* p, float4 x) {
   uint2 u;
-  u.x = (uint32_t)f32_to_bf16_rne(x.x) | ((uint32_t)f32_to_bf16_rne(x.y) << 16);
-  u.y = (uint32_t)f32_to_bf16_rne(x.z) | ((uint32_t)f32_to_bf16_rne(x.w) << 16);
+  u.x = bf16_pack(x.x, x.y);
+  u.y = bf16_pack(x.z, x.w);
   *reinterpret_cast<uint2*>(p) = u;
 }
 // two consecutive values (p must be aligned to two elements)
@@ -452,7 +455,7 @@ __device__ __forceinline__ float2 ld2(const uint16_t* p) {
 }
 __device__ __forceinline__ void st2(float* p, float2 x) { *reinterpret_cast<float2*>(p) = x; }
 __device__ __forceinline__ void st2(uint16_t* p, float2 x) {
-  *reinterpret_cast<uint32_t*>(p) = (uint32_t)f32_to_bf16_rne(x.x) | ((uint32_t)f32_to_bf16_rne(x.y) << 16);
+  *reinterpret_cast<uint32_t*>(p) = bf16_pack(x.x, x.y);
 }
 
 // Line of k that line `line` (= b C + c) uses: its own, or with one kernel
