@@ -56,6 +56,10 @@ CASES = [
     ((1, 3, 8192), "linear", "f32"), ((2, 2, 16384), "circular", "bf16"),
     ((1, 3, 16384), "linear", "f32"), ((2, 2, 32768), "circular", "f32"), ((1, 2, 65536), "linear", "bf16"),
     ((1, 2, 1 << 20), "linear", "f32"),
+    # the largest transforms the plans take: 2^22 points in 1D, 1024 on an axis
+    ((1, 2, 1 << 21), "linear", "bf16"), ((1, 2, 1 << 22), "circular", "f32"), ((1, 2, 512, 512), "linear", "f32"),
+    ((1, 2, 1024, 1024), "circular", "bf16"), ((1, 2, 512, 4, 8), "linear", "f32"),
+    ((1, 2, 4, 1024, 16), "circular", "f32"), ((1, 2, 8, 4, 512), "linear", "bf16"),
 ]
 
 

@@ -202,3 +202,16 @@ def test_full_size_sampled_lines(full_inputs, name):
     err = rel_l2(got, ref)
     log(f"[full] {name}: lines={lines.tolist()} rel_l2={err:.3e} (tol {TOL[w.dtype]:.0e})")
     assert err <= TOL[w.dtype]
+
+
+@pytest.mark.parametrize("grid,mode,dtype", [((1 << 21,), "linear", "bf16"), ((1 << 22,), "circular", "f32"),
+                                             ((512, 512), "linear", "f32"), ((1024, 1024), "circular", "bf16"),
+                                             ((1024, 8), "circular", "f32"), ((512, 4, 8), "linear", "f32"),
+                                             ((4, 1024, 16), "circular", "bf16"), ((8, 4, 512), "linear", "f32")])
+def test_maximum_extents(grid, mode, dtype):
+    """The largest transforms the plans take: 2^22 points in 1D (N1 = 1024
+    columns of the four-step split), 1024 on any axis of a 2D or 3D grid;
+    every output element against the oracle."""
+    inp = W.random_case(1, 2, grid, mode, dtype, seed=600 + len(grid) + grid[0] % 13)
+    assert plan(inp) in ("fourstep1d", "multipass2d", "multipass3d")
+    check_full(inp, f"max {grid} {mode}")
