@@ -287,10 +287,12 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
  *   aligned; order = M in 1..256.
  * k (output, device, `dtype`, aligned to its element size) : [C, L]; must not
  *   overlap a parameter.  C in 1..65535, L in 1..2^29.
- * Accuracy: each point is generated from an exact (double) phase and
- * magnitude at most 31 fp32 steps back, so errors stay at a few fp32
- * roundings per mode.  Validation, stream and error conventions as for
- * hyenand_fftconv; no workspace.
+ * Accuracy: up to order 32 the sum runs as fp32 matrix-core products over
+ * tiles of 1024 points, each term formed from an exact (double) phase and
+ * magnitude at most 31 fp32 advances of lambda^1024 back; above order 32 each
+ * point's terms are at most 31 fp32 steps of lambda^64 from such a phase.
+ * Errors stay at a few fp32 roundings per mode.  Validation, stream and error
+ * conventions as for hyenand_fftconv; no workspace.
  */
 hyenand_status hyenand_modal_filter(const float* log_mag, const float* angle, const float* res_re,
                                     const float* res_im, int order, void* k, int64_t C, int64_t L, int dtype,

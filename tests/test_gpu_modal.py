@@ -36,7 +36,8 @@ def _run(C, M, L, dtype, seed, rows=None):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("C,M,L", [(1, 1, 1), (3, 16, 63), (3, 16, 64), (5, 16, 100), (2, 64, 8193),
-                                   (16, 16, 4096), (1, 256, 777)])
+                                   (16, 16, 4096), (1, 256, 777), (2, 5, 1025), (3, 24, 5000), (4, 17, 1 << 16),
+                                   (2, 32, 70001), (1, 33, 3000), (3, 16, (1 << 18) + 3)])
 def test_modal(C, M, L, dtype):
     got, ref, _, _ = _run(C, M, L, dtype, C * 1000 + M + L)
     err = rel_l2(got, ref)
@@ -58,7 +59,8 @@ def test_genomics_length(dtype):
 
 def test_undamped_pole_keeps_phase():
     """|lambda| = 1 over 2^20 points: the phase must not drift (each point is
-    at most 31 fp32 steps from an exact double-precision phase)."""
+    at most 31 fp32 advances of lambda^1024 from a factor formed from an exact
+    double-precision phase)."""
     import torch
     from paper_2607_19378_amd import hyenand as H
     L = 1 << 20
@@ -89,3 +91,23 @@ def test_filter_through_the_convolution():
     err = rel_l2(from_device(y), ref)
     log(f"[modal] through the convolution: rel_l2={err:.3e}")
     assert err <= TOL["f32"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_output_off_the_vector_boundary(dtype):
+    """k one element past a four-element boundary (the per-point store path)
+    gives the values of an aligned k, and leaves the element before it alone."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    C, M, L = 3, 16, 4096
+    p = W.modal_params(21, C, M, L)
+    d = [torch.from_numpy(p[n]).cuda() for n in ("log_mag", "angle", "res_re", "res_im")]
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    aligned = H.modal_filter(*d, L, dtype=tdt)
+    buf = torch.full((C * L + 1,), 7.0, dtype=tdt, device="cuda")
+    k = buf[1:].view(C, L)
+    H.PreparedModal(k, *d)()
+    torch.cuda.synchronize()
+    log(f"[modal] unaligned k {dtype}")
+    assert float(buf[0]) == 7.0
+    assert torch.equal(k, aligned)
