@@ -8,7 +8,8 @@ The three directories hold the CSV output of three rocprofv3 runs of one
 bench.py command: ``--kernel-trace --stats``, ``--pmc FETCH_SIZE`` and
 ``--pmc WRITE_SIZE``.  With ``--synth`` the runs are of ``bench.py --synth``
 and the summary, ``profiles/siren_synth_<workload>.md``, covers the kernel
-synthesis kernel.  N is the number of hyenand_fftconv calls the command
+synthesis kernel; with ``--modal`` they are of ``bench.py --modal`` and
+``profiles/modal_filter_<workload>.md`` covers the modal filter kernel.  N is the number of hyenand_fftconv calls the command
 made (bench.py: warmup + steps).  Writes
 
 * ``profiles/<plan>_<workload>.md``: per-kernel average durations, HBM bytes
@@ -149,6 +150,69 @@ def synth_summary(a, W, source_hash):
     print(md)
 
 
+def modal_summary(a, W, source_hash):
+    """profiles/modal_filter_<workload>.md from rocprofv3 runs of
+    ``bench.py --modal``: the modal filter kernel's duration, HBM bytes and
+    matrix-core rate, beside the convolution kernels of the same run."""
+    sys.path.insert(0, ROOT)
+    import bench
+    w = W.WORKLOADS[a.workload]
+    stats = [r for r in _rows(a.trace, "_kernel_stats.csv") if "hyenand" in r["Name"]]
+    stats.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    gen = [r for r in stats if "modal_" in r["Name"]]
+    if not gen:
+        raise SystemExit("no modal filter dispatches in the trace")
+    avg_ns = float(gen[0]["AverageNs"])
+    L = w.grid[0]
+    flops = 4.0 * bench.MODAL_ORDER * w.C * L
+    tf = flops / (avg_ns * 1e-9) / 1e12
+    k_bytes = w.C * L * w.storage_bytes
+
+    def per_dispatch(rows, counter):
+        tot, n, copy = 0.0, set(), 0.0
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            if "modal_" in r["Kernel_Name"]:
+                tot += float(r["Counter_Value"])
+                n.add(r["Dispatch_Id"])
+            elif COPY_KERNEL in r["Kernel_Name"]:
+                copy = max(copy, float(r["Counter_Value"]))
+        return tot / max(1, len(n)), copy
+
+    f_d, f_copy = per_dispatch(_rows(a.fetch, "_counter_collection.csv"), "FETCH_SIZE")
+    w_d, w_copy = per_dispatch(_rows(a.write, "_counter_collection.csv"), "WRITE_SIZE")
+    if f_copy <= 0 or w_copy <= 0:
+        raise SystemExit("copy calibration dispatch not found in the counter runs")
+    copy_kib = a.copy_mib * 1024.0
+    fb = f_d * 1024.0 * copy_kib / f_copy
+    wb = w_d * 1024.0 * copy_kib / w_copy
+    lines = [f"# modal filter on {w.name}", "",
+             f"Modal filter generation, order {bench.MODAL_ORDER}, one filter per channel over the length of "
+             f"{w.description}: {w.C} x {L} points.  Kernel source hash `{source_hash()}`.", "",
+             "Commands (run from /tmp with TMPDIR=/tmp on the MI355X box):", "",
+             "```", a.cmd_trace, a.cmd_fetch, a.cmd_write, "```", "",
+             "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",
+             "| kernel | dispatches | avg us | min us | max us |", "|---|---:|---:|---:|---:|"]
+    for r in stats:
+        lines.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    lines += ["", f"{short_name(gen[0]['Name'])}: {flops / 1e9:.3f} GFLOP (4 per mode and point) per call in "
+                  f"{avg_ns / 1e3:.2f} us = {tf:.1f} TFLOP/s, {100 * tf / bench.MFMA_F32_PEAK_TFLOPS:.1f}% of the "
+                  f"{bench.MFMA_F32_PEAK_TFLOPS} TFLOP/s fp32 matrix peak; the k write alone takes "
+                  f"{k_bytes / 8e12 * 1e6:.1f} us at 8 TB/s ({100 * k_bytes / (avg_ns * 1e-9) / 8e12:.1f}% of it "
+                  "achieved).", "",
+              "## HBM traffic per modal filter dispatch (rocprofv3 --pmc)", "",
+              f"Copy calibration: {a.copy_mib} MiB device copy read {f_copy:.1f} KiB (FETCH_SIZE) and wrote "
+              f"{w_copy:.1f} KiB (WRITE_SIZE).", "",
+              f"Read {fb / 1e6:.2f} MB (poles and residues), write {wb / 1e6:.2f} MB; the kernel tensor is "
+              f"{k_bytes / 1e6:.2f} MB (written once).", ""]
+    md = os.path.join(a.out, f"modal_filter_{w.name}.md")
+    with open(md, "w") as fh:
+        fh.write("\n".join(lines))
+    print(md)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", required=True)
@@ -162,6 +226,7 @@ def main(argv=None):
     ap.add_argument("--cmd-write", required=True)
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
     ap.add_argument("--synth", action="store_true", help="runs of bench.py --synth: summarise the synthesis kernel")
+    ap.add_argument("--modal", action="store_true", help="runs of bench.py --modal: summarise the modal filter kernel")
     a = ap.parse_args(argv)
 
     sys.path.insert(0, ROOT)
@@ -170,6 +235,9 @@ def main(argv=None):
     from paper_2607_19378_amd import hyenand as H
     if a.synth:
         synth_summary(a, W, source_hash)
+        return
+    if a.modal:
+        modal_summary(a, W, source_hash)
         return
 
     w = W.WORKLOADS[a.workload]
