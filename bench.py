@@ -509,31 +509,22 @@ def cpu_baseline(inp, budget_s: float):
     x1, x2, v, k, D = inp.as_f64()
     nl = w.B * w.C
     per_line = w.elems // nl
-    # probe with a few lines, then size the sample to about budget_s seconds:
-    # a subset of the lines, or whole passes over all of them when one pass
-    # takes less than the budget
-    probe = list(range(min(nl, max(1, nthreads))))
+    # chunks of lines, cycling over all of them, until budget_s has elapsed
+    # (after one warm-up chunk that starts the oracle's threads)
+    chunk = min(nl, max(nthreads, nl // 8))
+    oracle.conv_fft(x1, x2, v, k, D, w.pad_mode, lines=list(range(min(nl, nthreads))), nthreads=nthreads)
+    done, nxt = 0, 0
     t0 = time.perf_counter()
-    oracle.conv_fft(x1, x2, v, k, D, w.pad_mode, lines=probe, nthreads=nthreads)
-    dt = max(time.perf_counter() - t0, 1e-6)
-    want = len(probe) * budget_s / dt  # lines that fit the budget
-    if want >= nl:
-        # calibrate on one whole pass (the probe overstates the per-line cost)
-        t0 = time.perf_counter()
-        oracle.conv_fft(x1, x2, v, k, D, w.pad_mode, nthreads=nthreads)
-        dt_pass = max(time.perf_counter() - t0, 1e-6)
-        reps, lines = max(1, int(budget_s / dt_pass)), list(range(nl))
-    else:
-        n = max(len(probe), (int(want) // nthreads) * nthreads)
-        reps, lines = 1, list(range(min(n, nl)))
-    t0 = time.perf_counter()
-    for _ in range(reps):
+    while done == 0 or time.perf_counter() - t0 < budget_s:
+        lines = [(nxt + j) % nl for j in range(chunk)]
         oracle.conv_fft(x1, x2, v, k, D, w.pad_mode, lines=lines, nthreads=nthreads)
+        done += chunk
+        nxt = (nxt + chunk) % nl
     dt = time.perf_counter() - t0
-    n = len(lines)
-    sample = (f"{reps} passes over all {nl} (b,c) lines of {w.name}" if reps > 1 else f"{n} of {nl} (b,c) lines of {w.name}")
-    return {"value": round(reps * n * per_line / dt / 1e9, 6), "unit": "GElem/s", "cores": nthreads,
-            "kind": "oracle", "sample": f"{sample} (fp64 FFT oracle, {dt:.2f} s wall)", "seconds": round(dt, 3)}
+    sample = (f"{done} line evaluations cycling over the {nl} (b,c) lines of {w.name} ({done / nl:.1f} passes; "
+              f"fp64 FFT oracle, {dt:.2f} s wall)")
+    return {"value": round(done * per_line / dt / 1e9, 6), "unit": "GElem/s", "cores": nthreads,
+            "kind": "oracle", "sample": sample, "seconds": round(dt, 3)}
 
 
 def main():
