@@ -43,7 +43,7 @@ extern "C" {
 typedef enum {
   HYENAND_OK = 0,
   HYENAND_ERR_INVALID_ARGUMENT = 1,  /* null pointer, bad enum, dims <= 0, y aliasing an input */
-  HYENAND_ERR_UNSUPPORTED = 2,       /* extent not a power of two, or beyond the implemented plans */
+  HYENAND_ERR_UNSUPPORTED = 2,       /* a shape or size beyond the implemented plans */
   HYENAND_ERR_WORKSPACE_TOO_SMALL = 3,
   HYENAND_ERR_HIP = 4                /* a HIP launch failed; see hyenand_last_error() */
 } hyenand_status;
@@ -165,8 +165,8 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_
  * size.  gD is reduced in a fixed order, so results are deterministic and do
  * not depend on the workspace size.  Supported: every shape the forward
  * supports (1D transforms up to 2^22 points, 2D/3D up to 1024 per axis);
- * other shapes return HYENAND_ERR_UNSUPPORTED.  The multi-pass plans use the library's side
- * streams as hyenand_fftconv does.
+ * other shapes return HYENAND_ERR_UNSUPPORTED.  The multi-pass plans use the
+ * library's side streams as hyenand_fftconv does.
  *
  * Centred mode (k and gk [B, C, 2 L1 - 1, ...], gu[j] = sum_n k[n - j +
  * (L - 1)] h[n] + D h[j], gk[i] = sum_n h[n] u[n - i + (L - 1)]) and
