@@ -420,17 +420,19 @@ def bench_modal(args, w, inp):
     both_s, both_wall = timed([gen, conv])
     copy_calibration(args, dev)
     # Per point and mode the sum takes Re(z w) = Re z Re w - Im z Im w and
-    # accumulates it: two multiply-adds, 4 flops, run as an fp32 matrix-core
-    # product for orders up to 32.  The bound is the longer of that product
-    # at the fp32 matrix peak and the k write at the HBM peak.
+    # accumulates it: two multiply-adds, 4 flops, run as a matrix-core
+    # product for orders up to 32 (bf16 products for a bf16 kernel tensor,
+    # fp32 otherwise).  The bound is the longer of that product at its
+    # matrix peak and the k write at the HBM peak.
     flops = 4.0 * MODAL_ORDER * w.C * L
     tflops = flops / gen_s / 1e12
     k_bytes = k.numel() * k.element_size()
-    t_mfma = flops / (MFMA_F32_PEAK_TFLOPS * 1e12)
+    mpeak = MFMA_BF16_PEAK_TFLOPS if w.dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
+    t_mfma = flops / (mpeak * 1e12)
     t_write = k_bytes / (HBM_PEAK_GBS * 1e9)
     if t_mfma >= t_write:
-        roof = {"bound": "mfma", "achieved": round(tflops, 3), "peak": MFMA_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(tflops / MFMA_F32_PEAK_TFLOPS, 4)}
+        roof = {"bound": "mfma", "achieved": round(tflops, 3), "peak": mpeak, "unit": "TFLOP/s",
+                "frac": round(tflops / mpeak, 4)}
     else:
         gbs = k_bytes / gen_s / 1e9
         roof = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -454,7 +456,7 @@ def bench_modal(args, w, inp):
                    "storage": w.dtype},
         "roofline": dict(roof, traffic=None, kernel="modal_mfma_kernel", alg_flops_per_call=flops,
                          avg_call_us=round(gen_s * 1e6, 3), mfma_tflops=round(tflops, 3),
-                         mfma_frac=round(tflops / MFMA_F32_PEAK_TFLOPS, 4), k_bytes_written=k_bytes,
+                         mfma_frac=round(tflops / mpeak, 4), k_bytes_written=k_bytes,
                          hbm_frac_of_k_write=round(k_bytes / gen_s / 1e9 / HBM_PEAK_GBS, 4)),
         "modal_us": round(gen_s * 1e6, 3), "conv_us": round(conv_s * 1e6, 3),
         "modal_then_conv_us": round(both_s * 1e6, 3),

@@ -21,7 +21,7 @@
 //
 // i.e. one real [32 x 2M] x [2M x 32] product (Re z Re w - Im z Im w
 // summed over the modes), M v_mfma_f32_32x32x2f32 per tile with M rounded
-// up to 16 or 32.  The right factor lambda^n is fixed per channel; the left
+// up to 16 or 32 (for a bf16 kernel tensor, M / 8 bf16 products instead).  The right factor lambda^n is fixed per channel; the left
 // one advances by lambda^1024 from tile to tile (four VALU operations per
 // mode and row) and is recomputed exactly, as above, every kTilesPerWave
 // tiles.
@@ -106,6 +106,34 @@ __device__ __forceinline__ v16f tile_product(const float (&zr)[MH], const float 
   return acc;
 }
 
+// For a bf16 kernel tensor the same product runs on
+// v_mfma_f32_32x32x16_bf16 with both factors rounded to bf16 (the factors
+// still advance in fp32; the rounding is of the order of the output's own).
+// Lane half h supplies inner indices 16 s + 8 h + t (t < 8) of product s:
+// the real parts of its modes 8 s + t for s < NS / 2, then the imaginary
+// parts, NS = MH / 4 products per tile.
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+template <int MH>
+__device__ __forceinline__ v16f tile_product_bf(const float (&zr)[MH], const float (&zn)[MH],
+                                                const v8bf (&bq)[MH / 4]) {
+  constexpr int NS = MH / 4, NH = NS / 2;
+  v16f acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    v8bf av;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const int i = 8 * (s % NH) + t;
+      av[t] = (__bf16)(s < NH ? zr[i] : zn[i]);
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bq[s], acc, 0, 0, 0);
+  }
+  return acc;
+}
+
 // register e of a tile's result: row 8 (e / 4) + 4 h + e % 4, column r
 __device__ __forceinline__ int tile_pos(int e, int h, int r) { return 32 * (8 * (e >> 2) + 4 * h + (e & 3)) + r; }
 
@@ -180,13 +208,29 @@ __global__ void __launch_bounds__(64 * kMfmaWaves) __attribute__((amdgpu_waves_p
     wr[i] = st.x;
     wi[i] = st.y;
   }
+  constexpr bool BF = sizeof(TS) == 2;
+  v8bf bq[MH / 4];
+  if constexpr (BF) {
+    constexpr int NH = MH / 8;
+#pragma unroll
+    for (int q = 0; q < MH / 4; ++q)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int i = 8 * (q % NH) + t;
+        bq[q][t] = (__bf16)(q < NH ? br[i] : bi[i]);
+      }
+  }
+  auto product = [&]() {
+    if constexpr (BF) return tile_product_bf<MH>(zr, zn, bq);
+    else return tile_product<MH>(zr, zn, br, bi);
+  };
   TS* out = k + c * L + tw;
   int64_t nfull = (L - tw) / kTile;  // whole tiles of the wave
   if (nfull > ntile) nfull = ntile;
   // whole tiles, each one's stores issued with the next one's products
   v16f prev;
   for (int64_t j = 0; j < nfull; ++j) {
-    const v16f acc = tile_product<MH>(zr, zn, br, bi);
+    const v16f acc = product();
     if (j > 0) store_tile(out + (j - 1) * kTile, prev, h, r);
 #pragma unroll
     for (int i = 0; i < MH; ++i) {
@@ -199,7 +243,7 @@ __global__ void __launch_bounds__(64 * kMfmaWaves) __attribute__((amdgpu_waves_p
   if (nfull > 0) store_tile(out + (nfull - 1) * kTile, prev, h, r);
   // the part of a tile before the end of the line
   if (nfull < ntile && tw + nfull * kTile < L) {
-    const v16f acc = tile_product<MH>(zr, zn, br, bi);
+    const v16f acc = product();
     const int64_t t0 = tw + nfull * kTile;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {

@@ -197,9 +197,11 @@ def modal_summary(a, W, source_hash):
     for r in stats:
         lines.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    mpeak, mkind = ((bench.MFMA_BF16_PEAK_TFLOPS, "bf16") if w.dtype == "bf16"
+                    else (bench.MFMA_F32_PEAK_TFLOPS, "fp32"))
     lines += ["", f"{short_name(gen[0]['Name'])}: {flops / 1e9:.3f} GFLOP (4 per mode and point) per call in "
-                  f"{avg_ns / 1e3:.2f} us = {tf:.1f} TFLOP/s, {100 * tf / bench.MFMA_F32_PEAK_TFLOPS:.1f}% of the "
-                  f"{bench.MFMA_F32_PEAK_TFLOPS} TFLOP/s fp32 matrix peak; the k write alone takes "
+                  f"{avg_ns / 1e3:.2f} us = {tf:.1f} TFLOP/s, {100 * tf / mpeak:.1f}% of the "
+                  f"{mpeak} TFLOP/s {mkind} matrix peak; the k write alone takes "
                   f"{k_bytes / 8e12 * 1e6:.1f} us at 8 TB/s ({100 * k_bytes / (avg_ns * 1e-9) / 8e12:.1f}% of it "
                   "achieved).", "",
               "## HBM traffic per modal filter dispatch (rocprofv3 --pmc)", "",
