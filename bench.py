@@ -553,7 +553,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the operator shards by "
-              f"independent (b, c) lines and this build runs on a single MI355X.", file=sys.stderr)
+              f"independent (b, c) lines; this benchmark runs on a single MI355X.", file=sys.stderr)
         sys.exit(2)
 
     import torch
