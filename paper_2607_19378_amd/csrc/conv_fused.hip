@@ -418,6 +418,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   }
   __syncthreads();
 
+  // outer gate values of the row pairs this lane stores, fetched before the
+  // inverse rows so that their latency hides behind them (when they take
+  // few registers)
+  constexpr int NP = L0 * L1 / 2, JX = (NP + NT - 1) / NT;
+  constexpr bool kPre = JX <= 4;
+  float2 gpre[kPre ? JX : 1];
+  if constexpr (kPre) {
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+      const int i = tid + NT * j;
+      if (NP % NT == 0 || i < NP) gpre[j] = G.g2(ld2(x2 + base + 2 * i));
+    }
+  }
+
   // 3. inverse row transforms: c2r_pair turns row r's half spectrum (slot 0
   //    holding DC + i Nyquist) into the length-M1 transform of its even/odd
   //    output pairs; the inverse leaves y[r][2m] + i y[r][2m+1] in slot m.
@@ -457,13 +471,25 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   __syncthreads();
 
   // 4. outer gate and store (coalesced along rows)
-  batched_copy<L0 * L1 / 2, NT, 8>(
-      tid, [&](int i) { return G.g2(ld2(x2 + base + 2 * i)); },
-      [&](int i, float2 g) {
+  if constexpr (kPre) {
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+      const int i = tid + NT * j;
+      if (NP % NT == 0 || i < NP) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-        const float2 q = Uh[r * RP + m];
+        const float2 q = Uh[r * RP + m], g = gpre[j];
         st2(y + base + 2 * i, make_float2(g.x * q.x, g.y * q.y));
-      });
+      }
+    }
+  } else {
+    batched_copy<L0 * L1 / 2, NT, 8>(
+        tid, [&](int i) { return G.g2(ld2(x2 + base + 2 * i)); },
+        [&](int i, float2 g) {
+          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+          const float2 q = Uh[r * RP + m];
+          st2(y + base + 2 * i, make_float2(g.x * q.x, g.y * q.y));
+        });
+  }
 }
 
 // Centered kernel, single pass: the K half spectrum fills all P0 rows, so U
