@@ -279,42 +279,100 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 
   // 0. stage the real rows of u = x1 v and k (coalesced along rows); row r of
   //    Uh holds the even/odd packed line u[r][2m] + i u[r][2m+1].
-  batched_copy<L0 * L1 / 2, NT, 8>(
-      tid,
-      [&](int i) {
-        const float2 u = G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i);
-        const float2 kk = ld2(k + kbase + 2 * i);
-        return make_float4(u.x, u.y, kk.x * scale, kk.y * scale);
-      },
-      [&](int i, float4 z) {
-        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-        Uh[r * RP + m] = make_float2(z.x, z.y);
-        Kh[r * RP + m] = make_float2(z.z, z.w);
-      });
-  __syncthreads();
-
   // 1. forward row transforms (lanes run across rows), then untangle each row
-  {
-    constexpr int E = F::ER, T = F::TR, LR = F::LR;
-    for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
-      using Map = LaneMap<T, NT>;
-      static_assert(Map::kLines == LR, "lines per round");
-      const int l = l0 + Map::line(tid), t = Map::t(tid);
-      const bool act = (2 * L0) % LR == 0 || l < 2 * L0;  // all lanes busy when rounds are full
-      float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
-      float2 w[E];
+  constexpr int NPS = L0 * L1 / 2, JS = (NPS + NT - 1) / NT;
+  constexpr int ES = imin(8, M1), TRS = M1 / ES;
+  // split staging: all loads issued at once, k's rows transformed while x1
+  // and v are still arriving (where the loads fit in a few registers and one
+  // round of 8-point lanes covers the L0 rows of a signal)
+  constexpr bool kSplit = JS <= 4 && TRS * L0 == NT;
+  if constexpr (kSplit) {
+    float2 kr[JS], ar[JS], br[JS];
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int m = t + T * e;
-        w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
+    for (int j = 0; j < JS; ++j) {
+      const int i = tid + NT * j;
+      if (NPS % NT == 0 || i < NPS) kr[j] = ld2(k + kbase + 2 * i);
+    }
+#pragma unroll
+    for (int j = 0; j < JS; ++j) {
+      const int i = tid + NT * j;
+      if (NPS % NT == 0 || i < NPS) {
+        ar[j] = ld2(x1 + base + 2 * i);
+        br[j] = ld2(v + base + 2 * i);
       }
-      BlockFFT<M1, E, false>::run(w, t, ScrS<1>{row}, act);
-      if (act) {
+    }
 #pragma unroll
-        for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
+    for (int j = 0; j < JS; ++j) {
+      const int i = tid + NT * j;
+      if (NPS % NT == 0 || i < NPS) {
+        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+        Kh[r * RP + m] = make_float2(kr[j].x * scale, kr[j].y * scale);
       }
     }
     __syncthreads();
+    using Map = LaneMap<TRS, NT>;
+    static_assert(Map::kLines == L0, "one round per signal");
+    const int l = Map::line(tid), t = Map::t(tid);
+    auto rows = [&](float2* rowp) {
+      float2 w[ES];
+#pragma unroll
+      for (int e = 0; e < ES; ++e) {
+        const int m = t + TRS * e;
+        w[e] = (CIRC || m < MNZ) ? rowp[m] : czero();
+      }
+      BlockFFT<M1, ES, false>::run(w, t, ScrS<1>{rowp}, true);
+#pragma unroll
+      for (int e = 0; e < ES; ++e) rowp[t + TRS * e] = w[e];
+    };
+    rows(Kh + l * RP);
+#pragma unroll
+    for (int j = 0; j < JS; ++j) {
+      const int i = tid + NT * j;
+      if (NPS % NT == 0 || i < NPS) {
+        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+        Uh[r * RP + m] = G.u2(ar[j], br[j], 2 * i);
+      }
+    }
+    __syncthreads();
+    rows(Uh + l * RP);
+  } else {
+    batched_copy<L0 * L1 / 2, NT, 8>(
+        tid,
+        [&](int i) {
+          const float2 u = G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i);
+          const float2 kk = ld2(k + kbase + 2 * i);
+          return make_float4(u.x, u.y, kk.x * scale, kk.y * scale);
+        },
+        [&](int i, float4 z) {
+          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+          Uh[r * RP + m] = make_float2(z.x, z.y);
+          Kh[r * RP + m] = make_float2(z.z, z.w);
+        });
+    __syncthreads();
+    {
+      constexpr int E = F::ER, T = F::TR, LR = F::LR;
+      for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
+        using Map = LaneMap<T, NT>;
+        static_assert(Map::kLines == LR, "lines per round");
+        const int l = l0 + Map::line(tid), t = Map::t(tid);
+        const bool act = (2 * L0) % LR == 0 || l < 2 * L0;  // all lanes busy when rounds are full
+        float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+        float2 w[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int m = t + T * e;
+          w[e] = (act && (CIRC || m < MNZ)) ? row[m] : czero();
+        }
+        BlockFFT<M1, E, false>::run(w, t, ScrS<1>{row}, act);
+        if (act) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) row[t + T * e] = w[e];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  {
     // Untangling, in place: item (row l, g) for 0 < g < M1/2 owns bins g and
     // M1 - g; bins 0 and M1/2 are their own mirrors and share the item g = 0
     // of their row.  The DC and Nyquist bins of a real row are real: slot 0
