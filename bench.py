@@ -139,6 +139,7 @@ def bench_backward(args, w, inp):
     ws = torch.empty(H.backward_workspace_size(w.shape, w.pad_mode, w.dtype), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     calls = [H.PreparedBackward(*o, *st, w.pad_mode, ws, stream) for o, st in zip(outs, sets)]
+    settle_clocks(lambda i: calls[i % rot](), settle_count(alg_flops_backward(w), set_bytes, args.settle_ms))
     for i in range(args.warmup):
         calls[i % rot]()
     torch.cuda.synchronize()
@@ -236,6 +237,7 @@ def bench_operator(args, w, inp):
     ws = torch.empty(H.operator_workspace_size(w.shape, w.pad_mode, w.dtype), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     calls = [H.PreparedOperator(y, *st, 1e-6, 1e-6, w.pad_mode, ws, stream) for y, st in zip(ys, sets)]
+    settle_clocks(lambda i: calls[i % rot](), settle_count(alg_flops(w), alg_bytes(w), args.settle_ms))
     for i in range(args.warmup):
         calls[i % rot]()
     torch.cuda.synchronize()
@@ -313,6 +315,7 @@ def bench_synth(args, w, inp):
     conv = H.Prepared(y, x1, x2, v, k, D, w.pad_mode, ws, stream)
 
     def timed(fns, steps):
+        settle_clocks(lambda i: [f() for f in fns], settle_count(alg_flops(w), alg_bytes(w), args.settle_ms))
         for _ in range(args.warmup):
             for f in fns:
                 f()
@@ -403,6 +406,7 @@ def bench_modal(args, w, inp):
     conv = H.Prepared(y, x1, x2, v, k, D, w.pad_mode, ws, stream, shared_k=True)
 
     def timed(fns):
+        settle_clocks(lambda i: [f() for f in fns], settle_count(alg_flops(w), alg_bytes(w), args.settle_ms))
         for _ in range(args.warmup):
             for f in fns:
                 f()
