@@ -89,3 +89,21 @@ def test_bench_algorithmic_flops():
     n = 2 ** 21
     per_line = 3 * 2.5 * n * 21 + 6 * (n // 2 + 1) + 4 * 2 ** 20
     assert abs(bench.alg_flops(w) - per_line * 256) < 1e-6 * per_line
+
+
+def test_bench_settle_count():
+    """The untimed settling calls: a fixed count per workload worth about the
+    requested time at the rough per-call rate, at least one, at most 2000,
+    none when switched off."""
+    import bench
+    w = W.WORKLOADS["conv2d_64"]
+    f, b = bench.alg_flops(w), bench.alg_bytes(w)
+    n = bench.settle_count(f, b, 30.0)
+    per_call = max(b / 5e12, f / (0.5 * bench.FP32_VALU_TFLOPS * 1e12))
+    assert n == int(np.ceil(0.030 / per_call)) and 100 < n < 2000
+    assert bench.settle_count(f, b, 60.0) >= 2 * n - 1
+    assert bench.settle_count(f, b, 0.0) == 0
+    tiny = W.WORKLOADS["conv1d_4k"]
+    assert bench.settle_count(bench.alg_flops(tiny), bench.alg_bytes(tiny), 30.0) == 2000
+    big = W.WORKLOADS["conv3d_128"]
+    assert 1 <= bench.settle_count(bench.alg_flops(big), bench.alg_bytes(big), 30.0) < 50
