@@ -263,6 +263,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
   // line of 2 L0 >= P0 slots, the exchange scratch of that column's transforms
   __shared__ float2 UK[2 * L0 * RP];
+  __shared__ float2 NQ[2][P0];  // column group 0's U and K spectra (DC + i Nyquist)
   float2* const Uh = UK;
   float2* const Kh = UK + L0 * RP;
   const int img = blockIdx.x;
@@ -428,12 +429,12 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       BlockFFT<P0, E, false>::run(wk, t, su, act);
       // Group 0 holds A + i B with A, B the spectra of the real columns 0
       // and M1: A = (Z[f] + conj Z[-f]) / 2, B = -i (Z[f] - conj Z[-f]) / 2
-      // need the mirror bin, so its spectra go through LDS and the bin pairs
-      // (f, P0 - f) are multiplied by lanes of the first two wavefronts; the
-      // other groups multiply in registers.
-      const ScrS<RP> u0{UK};
-      const ScrS<RP> k0{CIRC ? Kh : UK + M1};
-      __syncthreads();  // exchange reads of the forward transforms are done
+      // need the mirror bin, so its spectra go through LDS (slots of their
+      // own, outside every group's exchange scratch, so no barrier precedes
+      // the writes) and the bin pairs (f, P0 - f) are multiplied by lanes of
+      // the first two wavefronts; the other groups multiply in registers.
+      const ScrS<1> u0{NQ[0]};
+      const ScrS<1> k0{NQ[1]};
       if (nyq) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
