@@ -351,7 +351,8 @@ __global__ void __launch_bounds__(512)
       BlockFFT<P0, E, false>::run(wu, t, sc, act);
       BlockFFT<P0, E, false>::run(wk, t, sc, act);
       BlockFFT<P0, E, false>::run(wh, t, sc, act);
-      __syncthreads();  // exchange reads of the forward transforms are done
+      // NQ lies outside every group's exchange scratch: no barrier before
+      // group 0 writes it
       if (nyq) {
 #pragma unroll
         for (int e = 0; e < E; ++e) {

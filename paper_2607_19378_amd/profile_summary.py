@@ -219,6 +219,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", required=True)
     ap.add_argument("--calls", type=int, required=True)
+    ap.add_argument("--steps", type=int, default=10, help="timed steps of the bench.py command (the last calls)")
     ap.add_argument("--trace", required=True)
     ap.add_argument("--fetch", required=True)
     ap.add_argument("--write", required=True)
@@ -288,7 +289,24 @@ def main(argv=None):
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{100.0 * float(r['TotalDurationNs']) / total_ns:.1f}% |")
     busy = busy_ns / a.calls
-    lines += ["", f"GPU busy time per call (union of the kernels' intervals): {busy / 1e3:.2f} us "
+    # the timed steps alone: the dispatches of the last a.steps calls, whose
+    # union per call is what bench.py's HIP events see (the earlier calls
+    # include the untimed settling calls, some at idle clocks)
+    tail = iv[-max(1, round(len(iv) * a.steps / a.calls)):]
+    tail_ns, cs, ce = 0, None, None
+    for s0, e0 in tail:
+        if ce is None or s0 > ce:
+            if ce is not None:
+                tail_ns += ce - cs
+            cs, ce = s0, e0
+        else:
+            ce = max(ce, e0)
+    if ce is not None:
+        tail_ns += ce - cs
+    tail_busy = tail_ns / a.steps
+    lines += ["", f"GPU busy time per call over the last {a.steps} calls (the timed steps): "
+                  f"{tail_busy / 1e3:.2f} us ({alg / tail_busy:.1f} GB/s of algorithmic bytes).", ""]
+    lines += [f"GPU busy time per call over all calls (union of the kernels' intervals): {busy / 1e3:.2f} us "
                   f"({alg / busy:.1f} GB/s of algorithmic bytes, {100.0 * alg / busy / 8000.0:.2f}% of 8 TB/s).  "
                   f"Sum of kernel durations per call: {total_ns / a.calls / 1e3:.2f} us"
                   + (" (kernels of chunks on different side streams overlap, and each one's duration includes "
