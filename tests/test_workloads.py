@@ -107,3 +107,16 @@ def test_bench_settle_count():
     assert bench.settle_count(bench.alg_flops(tiny), bench.alg_bytes(tiny), 30.0) == 2000
     big = W.WORKLOADS["conv3d_128"]
     assert 1 <= bench.settle_count(bench.alg_flops(big), bench.alg_bytes(big), 30.0) < 50
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus above 1 exits with a message and
+    status 2 before touching a device."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
