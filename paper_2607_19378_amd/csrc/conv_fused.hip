@@ -565,6 +565,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   using F = Fused2D<P0, P1, false, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
   __shared__ float2 S[P0 * RP];  // U rows [0, L0), then K rows [0, P0); column exchange scratch
+  __shared__ float2 NQ[2][P0];   // column group 0's U and K spectra (DC + i Nyquist)
   const int img = blockIdx.x;
   const int c = img % C;
   const size_t base = (size_t)img * L0 * L1;
@@ -676,9 +677,10 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     const ScrS<RP> su{S + col};
     BlockFFT<P0, E, false>::run(wu, t, su, act);
     BlockFFT<P0, E, false>::run(wk, t, su, act);
-    const ScrS<RP> u0{S};
-    const ScrS<RP> k0{S + M1};
-    __syncthreads();  // exchange reads of the forward transforms are done
+    // group 0's spectra go through slots of their own, outside every
+    // group's exchange scratch: no barrier precedes the writes
+    const ScrS<1> u0{NQ[0]};
+    const ScrS<1> k0{NQ[1]};
     if (nyq) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {
@@ -719,6 +721,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   }
   __syncthreads();
 
+  // outer gate values of the row pairs this lane stores, fetched before the
+  // inverse rows so that their latency hides behind them (when they take
+  // few registers)
+  constexpr int NP = L0 * L1 / 2, JX = (NP + NT - 1) / NT;
+  constexpr bool kPre = JX <= 4;
+  float2 gpre[kPre ? JX : 1];
+  if constexpr (kPre) {
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+      const int i = tid + NT * j;
+      if (NP % NT == 0 || i < NP) gpre[j] = G.g2(ld2(x2 + base + 2 * i));
+    }
+  }
+
   // 5. inverse row transforms (two real output values per complex point)
   {
     constexpr int EI = F::EI, TI = F::TI, RI = F::RI;
@@ -755,13 +771,25 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   __syncthreads();
 
   // 6. outer gate and store
-  batched_copy<L0 * L1 / 2, NT, 8>(
-      tid, [&](int i) { return G.g2(ld2(x2 + base + 2 * i)); },
-      [&](int i, float2 g) {
+  if constexpr (kPre) {
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+      const int i = tid + NT * j;
+      if (NP % NT == 0 || i < NP) {
         const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-        const float2 q = S[r * RP + m];
+        const float2 q = S[r * RP + m], g = gpre[j];
         st2(y + base + 2 * i, make_float2(g.x * q.x, g.y * q.y));
-      });
+      }
+    }
+  } else {
+    batched_copy<L0 * L1 / 2, NT, 8>(
+        tid, [&](int i) { return G.g2(ld2(x2 + base + 2 * i)); },
+        [&](int i, float2 g) {
+          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+          const float2 q = S[r * RP + m];
+          st2(y + base + 2 * i, make_float2(g.x * q.x, g.y * q.y));
+        });
+  }
 }
 
 template <int P0, int P1, typename TS>
