@@ -669,6 +669,9 @@ def main():
         "alg_bytes_per_call": set_bytes, "alg_flops_per_call": round(flops),
         "kernel_plan": plan, "launches_per_call": "1" if plan.startswith("fused") else "3-5 (chunked)",
         "avg_call_us": round(avg_call_s * 1e6, 3)})
+    prof = os.path.join("profiles", f"{plan}_{w.name}.md")
+    if os.path.exists(os.path.join(ROOT, prof)):
+        roofline["profile"] = prof  # rocprofv3 kernel trace and counter summary of this command
 
     copy_calibration(args, dev)
 
