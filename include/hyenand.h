@@ -27,8 +27,11 @@
  * so every displacement between two grid points has its own weight; the
  * transform is 2 L_d per axis and the output is cropped as in "linear".
  *
- * The library computes this with fused FFT kernels on the GPU (fp32 compute);
- * it allocates nothing on the call path and keeps no pointer after a call.
+ * The library computes this with fused FFT kernels on the GPU (fp32 compute).
+ * It allocates no memory on the call path and keeps no pointer after a call;
+ * the only driver objects it creates are the side streams and events of the
+ * multi-pass plans, once per (host thread, device), on that thread's first
+ * multi-pass call (see hyenand_fftconv).
  */
 #ifndef HYENAND_H
 #define HYENAND_H
@@ -65,7 +68,9 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  * D               : device pointer, [C] of `dtype`.
  * ndim            : N in {1, 2, 3}.
  * dims            : host pointer to ndim + 2 int64 values {B, C, L1, ..., LN},
- *                   all >= 1.  Transform extents: L_d circular, 2 L_d
+ *                   all >= 1, with B * C < 2^22 (one workgroup per (b, c)
+ *                   line; a launch holds fewer than 2^32 work-items).
+ *                   Transform extents: L_d circular, 2 L_d
  *                   linear and centered; supported up to 2^22 points in 1D
  *                   and 1024 per axis in 2D/3D.  Other extents run on the
  *                   smallest power of two >= 2 L_d - 1 (exact for a
@@ -80,8 +85,8 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  *                   its displacements: x1, x2, v and k are copied into the
  *                   workspace on that grid, the circular plan runs there and
  *                   y is copied back (the workspace queries include the five
- *                   embedded tensors).  The operator takes the single-pass
- *                   shapes only.
+ *                   embedded tensors; at most 2^31 elements per embedded
+ *                   tensor).  The operator takes the single-pass shapes only.
  * pad_mode        : hyenand_pad_mode.
  * dtype           : hyenand_dtype.
  * workspace       : device scratch of workspace_bytes (16-byte aligned), owned
@@ -100,16 +105,17 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
  * not depend on the workspace size.
  *
  * The multi-pass plans (the ones with a nonzero workspace) fork onto two or
- * three side streams of the library (created once per device, default
- * priority, kept until the process ends) that wait for `stream` and that
- * `stream` waits for before anything enqueued after the call; a graph
- * captured on `stream` therefore takes them in.  Calls from several host
- * threads share those side streams: they stay correct but their multi-pass
- * work runs one call after the other.
+ * three side streams of the library that wait for `stream` and that `stream`
+ * waits for before anything enqueued after the call; a graph captured on
+ * `stream` therefore takes them in.  Each host thread has its own side
+ * streams and fork/join events per device (default priority, created on the
+ * thread's first multi-pass call there, kept until the process ends), so
+ * calls from several threads run concurrently and a capture on one thread
+ * never takes in another thread's work.
  */
 hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k,
                                const void* D, void* y, int ndim, const int64_t* dims,
-                               int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                               hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace, size_t workspace_bytes,
                                void* stream);
 
 /*
@@ -122,23 +128,23 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
  */
 hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const void* v, const void* k,
                                         const void* D, void* y, int ndim, const int64_t* dims,
-                                        int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                                        hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace, size_t workspace_bytes,
                                         void* stream);
 
 /* Recommended workspace size (bytes) for a call with these arguments; 0 for
  * plans that keep everything on chip.  Pure host function. */
-hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, int pad_mode,
-                                              int dtype, size_t* bytes_out);
+hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                              hyenand_dtype dtype, size_t* bytes_out);
 
 /* Smallest workspace (bytes) hyenand_fftconv accepts for these arguments. */
-hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int pad_mode,
-                                             int dtype, size_t* bytes_out);
+hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                             hyenand_dtype dtype, size_t* bytes_out);
 
 /* Name of the plan the call would use ("fused1d", "fused2d", "multipass2d",
  * "multipass3d", "fourstep1d"; for extents that are not powers of two
  * "fused1d_any", "fused2d_any" or "embedded1d/2d/3d"), written
  * NUL-terminated into buf (at most n bytes).  Pure host function. */
-hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                          char* buf, size_t n);
 
 /*
@@ -181,18 +187,18 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_
  */
 hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,
                                         const void* D, const void* gy, void* gx1, void* gx2, void* gv,
-                                        void* gk, void* gD, int ndim, const int64_t* dims, int pad_mode,
-                                        int dtype, void* workspace, size_t workspace_bytes, void* stream);
+                                        void* gk, void* gD, int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                        hyenand_dtype dtype, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Recommended workspace bytes for hyenand_fftconv_backward with these
  * arguments. */
-hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, int pad_mode,
-                                                       int dtype, size_t* bytes_out);
+hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                                       hyenand_dtype dtype, size_t* bytes_out);
 
 /* Smallest workspace (bytes) hyenand_fftconv_backward accepts for these
  * arguments. */
-hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, int pad_mode,
-                                                      int dtype, size_t* bytes_out);
+hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                                      hyenand_dtype dtype, size_t* bytes_out);
 
 /*
  * hyenand_operator -- the whole HyenaND operator of Eq. (HyenaND), section
@@ -219,11 +225,11 @@ hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* d
  */
 hyenand_status hyenand_operator(const void* q, const void* kin, const void* vin, const void* k, const void* D,
                                 const void* w_in, const void* w_out, float eps_l2, float eps_rms, void* y,
-                                int ndim, const int64_t* dims, int pad_mode, int dtype, void* workspace,
+                                int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace,
                                 size_t workspace_bytes, void* stream);
 
 /* Recommended workspace bytes for hyenand_operator. */
-hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                                size_t* bytes_out);
 
 /*
@@ -270,7 +276,7 @@ hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, in
 hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const float* Wh, const float* bias,
                                     const float* gamma, const float* beta, const float* Wout, const float* window,
                                     int window_kind, int hidden, int layers, void* k, int ndim,
-                                    const int64_t* dims, int pad_mode, int dtype, void* stream);
+                                    const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream);
 
 /*
  * hyenand_modal_filter -- the implicit long filter of order M of the appendix
@@ -295,11 +301,11 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
  * conventions as for hyenand_fftconv; no workspace.
  */
 hyenand_status hyenand_modal_filter(const float* log_mag, const float* angle, const float* res_re,
-                                    const float* res_im, int order, void* k, int64_t C, int64_t L, int dtype,
+                                    const float* res_im, int order, void* k, int64_t C, int64_t L, hyenand_dtype dtype,
                                     void* stream);
 
 /* Static text for a status code. */
-const char* hyenand_status_string(int status);
+const char* hyenand_status_string(hyenand_status status);
 
 /* Detail of the last non-OK return on the calling host thread ("" if none). */
 const char* hyenand_last_error(void);

@@ -7,7 +7,6 @@
 #include <string.h>
 
 #include <cmath>
-#include <mutex>
 #include <string>
 
 #include "../../include/hyenand.h"
@@ -45,6 +44,11 @@ const char* plan_name(Plan p, int ndim) {
 
 bool pow2(int64_t n) { return n >= 1 && (n & (n - 1)) == 0; }
 
+constexpr int64_t kMaxLines = (int64_t(1) << 22) - 1;
+// elementwise kernels of the embedded plans: 256 lanes per element block,
+// fewer than 2^32 work-items per launch
+constexpr int64_t kMaxEmbedElems = (int64_t(1) << 31);
+
 // Shape checks shared by every entry point.  Fills a (pointers left null).
 hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtype, FftConvArgs* a) {
   memset(a, 0, sizeof *a);
@@ -64,6 +68,11 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   }
   a->lines = dims[0] * dims[1];
   a->C = dims[1];
+  // one workgroup per (b, c) line in the single-pass kernels, up to 1024
+  // lanes each, and a launch holds fewer than 2^32 work-items
+  if (a->lines > kMaxLines)
+    return fail(HYENAND_ERR_UNSUPPORTED, "B * C = %lld (b, c) lines exceed the %lld one call takes",
+                (long long)a->lines, (long long)kMaxLines);
   a->circular = pad_mode == HYENAND_PAD_CIRCULAR;
   a->centered = pad_mode == HYENAND_PAD_CENTERED;
   a->bf16 = dtype == HYENAND_DTYPE_BF16;
@@ -125,7 +134,7 @@ bool grid_problem(const FftConvArgs& a, GridProblem* m) {
                                         a.bf16 ? HYENAND_DTYPE_BF16 : HYENAND_DTYPE_F32, &m->e);
   g_last_error = keep;
   m->tensor = ((size_t)embed_grid_elems(a) * (a.bf16 ? 2 : 4) + 255) / 256 * 256;
-  return st == HYENAND_OK;
+  return st == HYENAND_OK && embed_grid_elems(a) <= kMaxEmbedElems;
 }
 
 Plan choose_plan(const FftConvArgs& a);
@@ -240,35 +249,58 @@ size_t embed_fwd_ws(const FftConvArgs& a, bool recommended) {
   return 5 * m.tensor + (recommended ? recommended_ws(m.e, pi) : bytes_per_line(m.e, pi));
 }
 
-// Non-blocking side streams per device, created on first use and kept for
-// the life of the process (default priority).
+// Side streams of the multi-pass plans, and the events that fork them off
+// the caller's stream and join them back: one set per (host thread, device),
+// created on that thread's first multi-pass call on the device (default
+// priority, non-blocking) and kept until the process ends.  Later calls
+// create nothing.  Each host thread has its own set, so calls from several
+// threads neither serialise on shared streams nor enter another thread's
+// graph capture.
 constexpr int kMaxDevices = 64;
-struct SideStreams {
-  std::once_flag once;
-  hipError_t err = hipSuccess;
+struct SideSet {
+  bool ready = false;
   hipStream_t s[kMaxSide] = {};
+  hipEvent_t fork = nullptr;
+  hipEvent_t join[kMaxSide] = {};
 };
-SideStreams g_side[kMaxDevices];
+thread_local SideSet t_side[kMaxDevices];
 
-hipError_t side_streams(hipStream_t caller, hipStream_t** out) {
+hipError_t create_side_set(SideSet& st, int dev) {
+  int prev = 0;
+  hipError_t e = hipGetDevice(&prev);
+  if (e == hipSuccess && prev != dev) e = hipSetDevice(dev);
+  for (int i = 0; i < kMaxSide && e == hipSuccess; ++i) e = hipStreamCreateWithFlags(&st.s[i], hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&st.fork, hipEventDisableTiming);
+  for (int i = 0; i < kMaxSide && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&st.join[i], hipEventDisableTiming);
+  if (e != hipSuccess) {  // leave nothing half made: the next call tries again
+    for (int i = 0; i < kMaxSide; ++i) {
+      if (st.s[i]) (void)hipStreamDestroy(st.s[i]);
+      if (st.join[i]) (void)hipEventDestroy(st.join[i]);
+      st.s[i] = nullptr;
+      st.join[i] = nullptr;
+    }
+    if (st.fork) (void)hipEventDestroy(st.fork);
+    st.fork = nullptr;
+  }
+  if (prev != dev) {
+    const hipError_t r = hipSetDevice(prev);
+    if (e == hipSuccess) e = r;
+  }
+  st.ready = e == hipSuccess;
+  return e;
+}
+
+hipError_t side_set(hipStream_t caller, SideSet** out) {
   int dev = 0;
   hipError_t e = caller ? hipStreamGetDevice(caller, &dev) : hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  SideStreams& sd = g_side[dev];
-  std::call_once(sd.once, [&sd, dev] {
-    int prev = 0;
-    sd.err = hipGetDevice(&prev);
-    if (sd.err == hipSuccess && prev != dev) sd.err = hipSetDevice(dev);
-    for (int i = 0; i < kMaxSide && sd.err == hipSuccess; ++i)
-      sd.err = hipStreamCreateWithFlags(&sd.s[i], hipStreamNonBlocking);
-    if (prev != dev) {
-      const hipError_t r = hipSetDevice(prev);
-      if (sd.err == hipSuccess) sd.err = r;
-    }
-  });
-  if (sd.err != hipSuccess) return sd.err;
-  *out = sd.s;
+  SideSet& st = t_side[dev];
+  if (!st.ready) {
+    e = create_side_set(st, dev);
+    if (e != hipSuccess) return e;
+  }
+  *out = &st;
   return hipSuccess;
 }
 
@@ -289,36 +321,28 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
     return hipSuccess;
   }
   const int S = c.streams;
-  hipStream_t* side = nullptr;
-  hipError_t e = side_streams(caller, &side);
+  SideSet* side = nullptr;
+  hipError_t e = side_set(caller, &side);
   if (e != hipSuccess) return e;
-  hipEvent_t ev[1 + kMaxSide] = {};
-  for (int i = 0; i <= S && e == hipSuccess; ++i) e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventRecord(ev[0], caller);
-  for (int i = 0; i < S && e == hipSuccess; ++i) e = hipStreamWaitEvent(side[i], ev[0], 0);
-  if (e == hipSuccess) {
-    for (int64_t j = 0; j < c.nchunks; ++j) {
-      const int64_t line0 = j * c.chunk;
-      const int64_t nl = a.lines - line0 < c.chunk ? a.lines - line0 : c.chunk;
-      if (nl <= 0) break;
-      const int q = (int)(j % S);
-      void* ws = (char*)a.ws + (size_t)q * (size_t)c.chunk * per;
-      e = launch(line0, nl, ws, side[q]);
-      if (e != hipSuccess) break;
-    }
-    // join even after a failed launch, so that no work is left unordered
-    // with the caller's stream
-    for (int i = 0; i < S; ++i) {
-      hipError_t r = hipEventRecord(ev[1 + i], side[i]);
-      if (r == hipSuccess) r = hipStreamWaitEvent(caller, ev[1 + i], 0);
-      if (e == hipSuccess) e = r;
-    }
+  e = hipEventRecord(side->fork, caller);
+  for (int i = 0; i < S && e == hipSuccess; ++i) e = hipStreamWaitEvent(side->s[i], side->fork, 0);
+  if (e != hipSuccess) return e;
+  for (int64_t j = 0; j < c.nchunks; ++j) {
+    const int64_t line0 = j * c.chunk;
+    const int64_t nl = a.lines - line0 < c.chunk ? a.lines - line0 : c.chunk;
+    if (nl <= 0) break;
+    const int q = (int)(j % S);
+    void* ws = (char*)a.ws + (size_t)q * (size_t)c.chunk * per;
+    e = launch(line0, nl, ws, side->s[q]);
+    if (e != hipSuccess) break;
   }
-  for (int i = 0; i <= S; ++i)
-    if (ev[i]) {
-      const hipError_t r = hipEventDestroy(ev[i]);
-      if (e == hipSuccess) e = r;
-    }
+  // join even after a failed launch, so that no work is left unordered with
+  // the caller's stream
+  for (int i = 0; i < S; ++i) {
+    hipError_t r = hipEventRecord(side->join[i], side->s[i]);
+    if (r == hipSuccess) r = hipStreamWaitEvent(caller, side->join[i], 0);
+    if (e == hipSuccess) e = r;
+  }
   return e;
 }
 
@@ -357,7 +381,7 @@ bool embedded_problem(const FftConvArgs& a, Embedded* m) {
   if (st != HYENAND_OK) return false;
   m->p = choose_bwd_plan(m->e);
   m->tensor = ((size_t)embed_grid_elems(a) * (a.bf16 ? 2 : 4) + 255) / 256 * 256;
-  return m->p != BWD_NONE && m->p != BWD_EMBED;
+  return m->p != BWD_NONE && m->p != BWD_EMBED && embed_grid_elems(a) <= kMaxEmbedElems;
 }
 
 BwdPlan choose_bwd_plan(const FftConvArgs& a) {
@@ -411,7 +435,7 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 extern "C" {
 
-hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                               size_t* bytes_out) {
   if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
   FftConvArgs a;
@@ -423,7 +447,7 @@ hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, int
   return HYENAND_OK;
 }
 
-hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                              size_t* bytes_out) {
   if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
   FftConvArgs a;
@@ -435,7 +459,7 @@ hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, int 
   return HYENAND_OK;
 }
 
-hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, int pad_mode, int dtype, char* buf,
+hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype, char* buf,
                                          size_t n) {
   if (!buf || n == 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "buf is NULL or empty");
   FftConvArgs a;
@@ -614,18 +638,18 @@ hyenand_status operator_fwd(const void* q, const void* kin, const void* vin, con
 extern "C" {
 
 hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, const void* k, const void* D,
-                               void* y, int ndim, const int64_t* dims, int pad_mode, int dtype,
+                               void* y, int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                void* workspace, size_t workspace_bytes, void* stream) {
   return forward(x1, x2, v, k, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, false);
 }
 
 hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const void* v, const void* k,
-                                        const void* D, void* y, int ndim, const int64_t* dims, int pad_mode,
-                                        int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+                                        const void* D, void* y, int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                        hyenand_dtype dtype, void* workspace, size_t workspace_bytes, void* stream) {
   return forward(x1, x2, v, k, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, true);
 }
 
-hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                                        size_t* bytes_out) {
   if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
   FftConvArgs a;
@@ -643,7 +667,7 @@ hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* 
   return HYENAND_OK;
 }
 
-hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                                       size_t* bytes_out) {
   if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
   FftConvArgs a;
@@ -663,7 +687,7 @@ hyenand_status hyenand_fftconv_backward_workspace_min(int ndim, const int64_t* d
 
 hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,
                                         const void* D, const void* gy, void* gx1, void* gx2, void* gv, void* gk,
-                                        void* gD, int ndim, const int64_t* dims, int pad_mode, int dtype,
+                                        void* gD, int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                         void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   FftConvArgs a;
@@ -760,7 +784,7 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
   return HYENAND_OK;
 }
 
-const char* hyenand_status_string(int status) {
+const char* hyenand_status_string(hyenand_status status) {
   switch (status) {
     case HYENAND_OK: return "ok";
     case HYENAND_ERR_INVALID_ARGUMENT: return "invalid argument";
@@ -775,13 +799,13 @@ const char* hyenand_last_error(void) { return g_last_error.c_str(); }
 
 hyenand_status hyenand_operator(const void* q, const void* kin, const void* vin, const void* k, const void* D,
                                 const void* w_in, const void* w_out, float eps_l2, float eps_rms, void* y, int ndim,
-                                const int64_t* dims, int pad_mode, int dtype, void* workspace, size_t workspace_bytes,
+                                const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace, size_t workspace_bytes,
                                 void* stream) {
   return operator_fwd(q, kin, vin, k, D, w_in, w_out, eps_l2, eps_rms, y, ndim, dims, pad_mode, dtype, workspace,
                       workspace_bytes, stream);
 }
 
-hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, int pad_mode, int dtype,
+hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                                size_t* bytes_out) {
   if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
   FftConvArgs a;
@@ -797,7 +821,7 @@ hyenand_status hyenand_operator_workspace_size(int ndim, const int64_t* dims, in
 hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const float* Wh, const float* bias,
                                     const float* gamma, const float* beta, const float* Wout, const float* window,
                                     int window_kind, int hidden, int layers, void* k, int ndim, const int64_t* dims,
-                                    int pad_mode, int dtype, void* stream) {
+                                    hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream) {
   if (ndim < 1 || ndim > 3) return fail(HYENAND_ERR_INVALID_ARGUMENT, "ndim must be 1, 2 or 3 (got %d)", ndim);
   if (!dims) return fail(HYENAND_ERR_INVALID_ARGUMENT, "dims is NULL");
   if (pad_mode != HYENAND_PAD_LINEAR && pad_mode != HYENAND_PAD_CIRCULAR && pad_mode != HYENAND_PAD_CENTERED)
@@ -871,7 +895,7 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
 }
 
 hyenand_status hyenand_modal_filter(const float* log_mag, const float* angle, const float* res_re,
-                                    const float* res_im, int order, void* k, int64_t C, int64_t L, int dtype,
+                                    const float* res_im, int order, void* k, int64_t C, int64_t L, hyenand_dtype dtype,
                                     void* stream) {
   if (dtype != HYENAND_DTYPE_F32 && dtype != HYENAND_DTYPE_BF16)
     return fail(HYENAND_ERR_INVALID_ARGUMENT, "dtype must be 0 (f32) or 1 (bf16), got %d", dtype);

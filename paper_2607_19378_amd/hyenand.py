@@ -16,7 +16,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhyenand.so")
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = range(5)
-PAD_LINEAR, PAD_CIRCULAR = 0, 1
+PAD_LINEAR, PAD_CIRCULAR, PAD_CENTERED = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
 EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_workspace_size",
@@ -158,6 +158,19 @@ def _ptr(t) -> int:
     return int(t.data_ptr())
 
 
+def _keep_for_stream(stream, *tensors) -> None:
+    """Tensors this module allocates on the current stream but hands to work
+    on another `stream`: mark them used there, so that torch's caching
+    allocator does not give their memory to a later allocation on the
+    current stream while that work is still pending."""
+    import torch
+    if stream is None:
+        return
+    for t in tensors:
+        if t is not None and stream != torch.cuda.current_stream(t.device):
+            t.record_stream(stream)
+
+
 class Prepared:
     """One hyenand_fftconv call with its arguments checked and marshalled
     once; calling the object enqueues the work again on the same buffers and
@@ -207,11 +220,13 @@ def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=No
     """Allocate y (and, unless given, the workspace) with torch and run the op."""
     import torch
     y = torch.empty_like(x1)
+    own = None
     if workspace is None:
         nbytes = workspace_size(tuple(x1.shape), pad_mode, x1.dtype)
         if nbytes:
-            workspace = torch.empty(nbytes, dtype=torch.uint8, device=x1.device)
+            workspace = own = torch.empty(nbytes, dtype=torch.uint8, device=x1.device)
     fftconv_into(y, x1, x2, v, k, D, pad_mode, workspace, stream, shared_k)
+    _keep_for_stream(stream, y, own)
     return y
 
 
@@ -248,10 +263,11 @@ class PreparedBackward:
         for t in (D, gD):
             if not t.is_cuda or t.dtype != x1.dtype or tuple(t.shape) != (shape[1],) or not t.is_contiguous():
                 raise ValueError("D and gD must be contiguous [C] GPU tensors of the same dtype")
+        nd, dims = _dims(shape)
         if workspace is None:
             workspace = torch.empty(backward_workspace_size(shape, pad_mode, x1.dtype), dtype=torch.uint8,
                                     device=x1.device)
-        nd, dims = _dims(shape)
+            _keep_for_stream(stream, workspace)
         if stream is None:
             stream = torch.cuda.current_stream(x1.device)
         self._fn = lib().hyenand_fftconv_backward
@@ -281,6 +297,7 @@ def backward(x1, x2, v, k, D, gy, pad_mode: str = "linear", workspace=None, stre
     gk = torch.empty_like(k)
     gD = torch.empty_like(D)
     backward_into(gx1, gx2, gv, gk, gD, x1, x2, v, k, D, gy, pad_mode, workspace, stream)
+    _keep_for_stream(stream, gx1, gx2, gv, gk, gD)
     return gx1, gx2, gv, gk, gD
 
 
@@ -310,6 +327,7 @@ class PreparedOperator:
         if workspace is None:
             workspace = torch.empty(operator_workspace_size(shape, pad_mode, q.dtype), dtype=torch.uint8,
                                     device=q.device)
+            _keep_for_stream(stream, workspace)
         nd, dims = _dims(shape)
         if stream is None:
             stream = torch.cuda.current_stream(q.device)
@@ -332,6 +350,7 @@ def operator(q, kin, vin, k, D, w_in, w_out, eps_l2: float = 1e-6, eps_rms: floa
     import torch
     y = torch.empty_like(q)
     PreparedOperator(y, q, kin, vin, k, D, w_in, w_out, eps_l2, eps_rms, pad_mode, workspace, stream)()
+    _keep_for_stream(stream, y)
     return y
 
 
@@ -395,6 +414,7 @@ def kernel_synth(shape, omega0, W1, Wh, Wout, window, gamma=None, beta=None, bia
     kshape = kernel_shape(shape, pad_mode, shared_k=gamma is None)
     k = torch.empty(kshape, dtype=dtype, device=omega0.device)
     PreparedSynth(k, shape, omega0, W1, Wh, Wout, window, gamma, beta, bias, window_kind, pad_mode, stream)()
+    _keep_for_stream(stream, k)
     return k
 
 
@@ -429,4 +449,5 @@ def modal_filter(log_mag, angle, res_re, res_im, L: int, dtype=None, stream=None
     import torch
     k = torch.empty((log_mag.shape[0], int(L)), dtype=dtype or torch.float32, device=log_mag.device)
     PreparedModal(k, log_mag, angle, res_re, res_im, stream)()
+    _keep_for_stream(stream, k)
     return k

@@ -341,3 +341,26 @@ def test_embedded_backward_validation(L):
     assert b"gD overlaps gk" in L.hyenand_last_error() or b"gk overlaps" in L.hyenand_last_error()
     assert bcall(L, (1, 2, 8), mode=2, ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 5, 7), mode=0, ws_bytes=64) == H.ERR_WORKSPACE_TOO_SMALL
+
+
+def test_line_count_bounded(L):
+    """B * C beyond what one launch of one workgroup per line can hold is
+    refused on the host (no index or grid overflow on the GPU)."""
+    assert call(L, (1 << 31, 1, 2)) == H.ERR_UNSUPPORTED
+    assert b"lines" in L.hyenand_last_error()
+    assert call(L, (1, 1 << 31, 2)) == H.ERR_UNSUPPORTED
+    assert call(L, (1 << 11, 1 << 11, 2)) == H.ERR_UNSUPPORTED  # exactly 2^22 lines
+    with pytest.raises(H.HyenandError):
+        H.workspace_size((1 << 12, 1 << 10, 4), "linear", "f32")
+    assert H.plan_name(((1 << 22) - 1, 1, 4), "linear", "f32") == "fused1d"
+
+
+def test_embedded_grid_bounded():
+    """An embedded plan whose grid tensor would exceed 2^31 elements has no
+    plan (its elementwise launches would exceed 2^32 work-items)."""
+    # 300 x 300 runs on a 1024 x 1024 grid: 2048 lines hold exactly 2^31
+    # elements, 2049 one line more
+    assert H.plan_name((1, 2048, 300, 300), "linear", "f32") == "embedded2d"
+    with pytest.raises(H.HyenandError) as e:
+        H.plan_name((1, 2049, 300, 300), "linear", "f32")
+    assert e.value.status == H.ERR_UNSUPPORTED

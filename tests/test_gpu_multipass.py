@@ -215,3 +215,77 @@ def test_maximum_extents(grid, mode, dtype):
     inp = W.random_case(1, 2, grid, mode, dtype, seed=600 + len(grid) + grid[0] % 13)
     assert plan(inp) in ("fourstep1d", "multipass2d", "multipass3d")
     check_full(inp, f"max {grid} {mode}")
+
+
+def test_other_stream_outside_its_context():
+    """fftconv(stream=s) called while another stream is current: the binding
+    allocates y and the workspace on the current stream and hands them to s.
+    Allocations made on the current stream right after the call (before s
+    finishes) must not take their memory: y matches a call on the current
+    stream bitwise, and the filler tensors keep their values."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    from gpu_util import to_device
+    inp = W.random_case(2, 6, (256, 128), "circular", "f32", seed=45)
+    w = inp.workload
+    assert plan(inp) == "multipass2d"
+    dev = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+    ref = H.fftconv(*dev, pad_mode=w.pad_mode)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    for rep in range(3):
+        y = H.fftconv(*dev, pad_mode=w.pad_mode, stream=s)
+        fill = [torch.full((H.workspace_size(w.shape, w.pad_mode, w.dtype) // 4 + 1024,), float(rep + j),
+                           device="cuda") for j in range(3)]
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        log(f"[other stream] rep {rep}")
+        assert torch.equal(y, ref)
+        for j, f in enumerate(fill):
+            assert bool((f == float(rep + j)).all())
+
+
+def test_host_threads_each_with_own_side_streams():
+    """Four host threads call multi-pass plans at once, each on a stream of
+    its own (ctypes releases the GIL inside the library, so the calls overlap
+    on the host); every result matches the single-thread one bitwise."""
+    import threading
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    from gpu_util import to_device
+    cases = []
+    for j, (grid, mode) in enumerate((((256, 128), "circular"), ((32768,), "linear"), ((8, 16, 8), "linear"),
+                                      ((128, 256), "linear"))):
+        inp = W.random_case(1, 5, grid, mode, "f32", seed=70 + j)
+        w = inp.workload
+        dev = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+        ref = H.fftconv(*dev, pad_mode=w.pad_mode)
+        cases.append((w, dev, ref))
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(j):
+        try:
+            w, dev, ref = cases[j]
+            s = torch.cuda.Stream()
+            ws = torch.empty(H.workspace_size(w.shape, w.pad_mode, w.dtype), dtype=torch.uint8, device="cuda")
+            ys = [torch.empty_like(dev[0]) for _ in range(4)]
+            torch.cuda.synchronize()
+            for y in ys:
+                H.fftconv_into(y, *dev, pad_mode=w.pad_mode, workspace=ws, stream=s)
+            s.synchronize()
+            for y in ys:
+                if not torch.equal(y, ref):
+                    errors.append(f"case {j}: mismatch")
+        except Exception as e:  # reported below
+            errors.append(f"case {j}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(j,)) for j in range(len(cases))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=60)
+    log(f"[threads] {len(cases)} threads done, errors={errors}")
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
