@@ -9,9 +9,14 @@ independent input sets are rotated so the working set exceeds the 256 MiB
 Infinity Cache and every step streams its inputs from HBM.  Before the W
 warmup steps the same calls run untimed for --settle-ms (30 ms), so that the
 GPU has left the low clocks of the idle time spent generating inputs; then
-exactly K steps are timed.  Prints one JSON line: GElem/s (output elements per second), the HBM-roofline fraction of the
-dominant kernel from HIP events on the launch stream, and the CPU oracle timed
-on a bounded sample of the same workload on the host cores.
+exactly K steps are timed.
+
+With no --workload, the headline workload (8 x 256 images of 64 x 64, fp32)
+and then each of the five workload configurations are timed in turn; one
+JSON line reports the headline (GElem/s, its HBM-roofline fraction from HIP
+events on the launch stream, the CPU oracle on a bounded sample) and a
+per_config list with the same figures for every configuration.  Progress
+goes to stderr.
 """
 from __future__ import annotations
 
@@ -37,6 +42,8 @@ FP32_VALU_TFLOPS = 78.6
 FP32_PACKED_TFLOPS = 157.3
 MALL_BYTES = 256 << 20
 DEFAULT_WORKLOAD = "conv2d_64"
+# the five configurations of the metric, in the order they are reported
+CONFIG_ORDER = ["conv1d_4k", "conv2d_64", "conv2d_512c", "conv3d_128", "conv1d_1m"]
 
 
 def alg_bytes(w: W.Workload) -> int:
@@ -209,7 +216,7 @@ def bench_backward(args, w, inp):
         "metric": "gated N-D FFT-conv backward GElem/s and % of roofline on 1 MI355X",
         "value": round(w.elems / (ms_per_step * 1e-3) / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage_dtype": w.dtype,
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads; gy seeded normal)",
         "config": {"workload": w.name, "pass": "backward", "B": w.B, "C": w.C, "grid": list(w.grid),
                    "pad_mode": w.pad_mode, "storage": w.dtype, "rotated_input_sets": rot},
@@ -268,7 +275,7 @@ def bench_operator(args, w, inp):
         "metric": "HyenaND operator (Eq. HyenaND) GElem/s on 1 MI355X",
         "value": round(w.elems / (ms_per_step * 1e-3) / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage_dtype": w.dtype,
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
         "config": {"workload": w.name, "pass": "operator", "B": w.B, "C": w.C, "grid": list(w.grid),
                    "pad_mode": w.pad_mode, "storage": w.dtype, "rotated_input_sets": rot},
@@ -366,7 +373,7 @@ def bench_synth(args, w, inp):
         "metric": "input-dependent kernel synthesis + gated N-D FFT conv GElem/s on 1 MI355X",
         "value": round(w.elems / both_wall / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(both_wall * 1e3, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage_dtype": w.dtype,
         "data": "synthetic (seeded parameters drawn by the paper's initialisation recipe)",
         "synth_products": "bf16 matrix cores, fp32 accumulate" if w.dtype == "bf16" else "fp32 matrix cores",
         "config": {"workload": w.name, "pass": "synth+conv", "B": w.B, "C": w.C, "grid": list(w.grid),
@@ -456,7 +463,7 @@ def bench_modal(args, w, inp):
         "metric": "modal filter generation + gated 1D FFT conv GElem/s on 1 MI355X",
         "value": round(w.elems / both_wall / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(both_wall * 1e3, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage_dtype": w.dtype,
         "data": "synthetic (seeded poles and residues)",
         "config": {"workload": w.name, "pass": "modal+conv", "B": w.B, "C": w.C, "L": L, "order": MODAL_ORDER,
                    "storage": w.dtype},
@@ -528,30 +535,200 @@ def settle_clocks(step, n: int) -> None:
     torch.cuda.synchronize()
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(inp, budget_s: float):
-    """The oracle (convolution theorem, fp64, own FFT) on a bounded sample of lines."""
+    """The oracle (convolution theorem, fp64, own FFT) on a bounded sample of
+    lines: chunks of lines cycling over all of them until budget_s has
+    elapsed (at least one chunk), after one warm-up chunk."""
     import oracle
     w = inp.workload
     nthreads = oracle.default_threads()
-    x1, x2, v, k, D = inp.as_f64()
     nl = w.B * w.C
     per_line = w.elems // nl
-    # chunks of lines, cycling over all of them, until budget_s has elapsed
-    # (after one warm-up chunk that starts the oracle's threads)
-    chunk = min(nl, max(nthreads, nl // 8))
-    oracle.conv_fft(x1, x2, v, k, D, w.pad_mode, lines=list(range(min(nl, nthreads))), nthreads=nthreads)
+    chunk = min(nl, max(nthreads, nl // 8)) if per_line <= (1 << 16) else min(nl, nthreads)
+    warm = list(range(min(nl, nthreads if per_line <= (1 << 16) else 1)))
+    _oracle_on_lines(inp, warm, nthreads)
     done, nxt = 0, 0
     t0 = time.perf_counter()
     while done == 0 or time.perf_counter() - t0 < budget_s:
         lines = [(nxt + j) % nl for j in range(chunk)]
-        oracle.conv_fft(x1, x2, v, k, D, w.pad_mode, lines=lines, nthreads=nthreads)
+        _oracle_on_lines(inp, lines, nthreads)
         done += chunk
         nxt = (nxt + chunk) % nl
     dt = time.perf_counter() - t0
-    sample = (f"{done} line evaluations cycling over the {nl} (b,c) lines of {w.name} ({done / nl:.1f} passes; "
+    sample = (f"{done} line evaluations cycling over the {nl} (b,c) lines of {w.name} ({done / nl:.2f} passes; "
               f"fp64 FFT oracle, {dt:.2f} s wall)")
     return {"value": round(done * per_line / dt / 1e9, 6), "unit": "GElem/s", "cores": nthreads,
-            "kind": "oracle", "sample": sample, "seconds": round(dt, 3)}
+            "cpu_model": cpu_model(), "kind": "oracle", "sample": sample, "seconds": round(dt, 3)}
+
+
+def _oracle_on_lines(inp, lines, nthreads=None):
+    """The oracle's y on the given flat (b * C + c) lines, each run as one
+    channel of a one-sample problem (only those lines are upcast)."""
+    import oracle
+    w = inp.workload
+    nl = w.B * w.C
+    lines = np.asarray(lines, dtype=np.int64)
+    sub = [W.storage_to_f64(a.reshape((nl,) + tuple(a.shape[2:]))[lines], w.dtype)[None]
+           for a in (inp.x1, inp.x2, inp.v, inp.k)]
+    Dsub = W.storage_to_f64(inp.D, w.dtype)[lines % w.C]
+    return oracle.conv_fft(*sub, Dsub, w.pad_mode, nthreads=nthreads)[0]
+
+
+def measure_stream_peak(dev, stream):
+    """A 1 GiB device-to-device copy (read + write), best of 6: GB/s."""
+    import torch
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    best = None
+    for _ in range(6):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dst.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    del src, dst
+    return 2.0 * (1 << 28) * 4 / (best * 1e-3) / 1e9
+
+
+def bench_forward(args, w, inp, cpu_budget, stream_gbs=None):
+    """Time hyenand_fftconv on one workload: exactly args.steps calls after
+    the settling calls and args.warmup warmup steps.  Returns the workload's
+    entry: throughput from the wall clock over the timed steps, per-call
+    times from HIP events on the launch stream (mean over the bracket; median
+    and min of the per-step intervals), the HBM- and ALU-roofline fractions
+    of the algorithmic work, the counter traffic when it was taken on these
+    kernel sources, parity on sampled lines and the CPU oracle baseline."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    set_bytes = alg_bytes(w)
+    rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
+    dev = torch.device("cuda:0")
+    base = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+    sets = [base]
+    for r in range(1, rot):
+        # distinct buffers with the same values: the cache cannot serve one set from another
+        sets.append([t.clone() for t in base])
+    ys = [torch.empty_like(base[0]) for _ in range(rot)]
+    ws_bytes = H.workspace_size(w.shape, w.pad_mode, w.dtype)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None
+    plan = H.plan_name(w.shape, w.pad_mode, w.dtype)
+    stream = torch.cuda.current_stream(dev)
+    # one prepared call per input set: the timed loop only enqueues
+    calls = [H.Prepared(ys[r], s[0], s[1], s[2], s[3], s[4], w.pad_mode, ws, stream) for r, s in enumerate(sets)]
+
+    def step(i):
+        calls[i % rot]()
+
+    # The GPU sits idle while the host generates the inputs and comes back
+    # at low clocks; a few milliseconds of the same calls, untimed, bring it
+    # to its working clock before the warmup steps.
+    n_settle = settle_count(alg_flops(w), alg_bytes(w), args.settle_ms)
+    settle_clocks(step, n_settle)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # HIP events on the launch stream: one before every timed step and one
+    # after the last.  Recording an event between launches leaves them
+    # queued back to back.
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        evs[i].record(stream)
+        step(i)
+    evs[-1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    per_step = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    avg_call_s = evs[0].elapsed_time(evs[-1]) * 1e-3 / args.steps
+    flops = alg_flops(w)
+    hbm_gbs = set_bytes / avg_call_s / 1e9
+    alu_tflops = flops / avg_call_s / 1e12
+    traffic = stored_traffic(w.name)
+    entry = {
+        "workload": w.name, "desc": w.description, "B": w.B, "C": w.C, "grid": list(w.grid),
+        "pad_mode": w.pad_mode, "storage_dtype": w.dtype, "compute_dtype": "f32", "plan": plan,
+        "value": round(w.elems / (ms_per_step * 1e-3) / 1e9, 3), "unit": "GElem/s",
+        "ms_per_step": round(ms_per_step, 5),
+        "call_us_mean": round(avg_call_s * 1e6, 3), "call_us_median": round(float(np.median(per_step)) * 1e3, 3),
+        "call_us_min": round(float(per_step.min()) * 1e3, 3),
+        "alg_bytes_per_call": set_bytes, "alg_flops_per_call": round(flops),
+        "hbm_achieved_gbs": round(hbm_gbs, 2), "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
+        "hbm_frac_wall": round(set_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "alu_achieved_tflops": round(alu_tflops, 3), "alu_frac": round(alu_tflops / FP32_VALU_TFLOPS, 4),
+        "alu_frac_of_packed_peak": round(alu_tflops / FP32_PACKED_TFLOPS, 4),
+        "first_bound": ("alu" if flops / (FP32_VALU_TFLOPS * 1e12) > set_bytes / (HBM_PEAK_GBS * 1e9) else "hbm"),
+        "counter_bytes_per_call": traffic,
+        "counter_to_alg_bytes": None if traffic is None else round(traffic / set_bytes, 3),
+        "rotated_input_sets": rot, "untimed_calls": {"settle": n_settle, "warmup": args.warmup},
+    }
+    if stream_gbs:
+        entry["hbm_frac_of_stream_peak"] = round(hbm_gbs / stream_gbs, 4)
+    prof = os.path.join("profiles", f"{plan}_{w.name}.md")
+    if os.path.exists(os.path.join(ROOT, prof)):
+        entry["profile"] = prof  # rocprofv3 kernel trace and counter summary of this workload
+
+    copy_calibration(args, dev)
+
+    if not args.no_parity:
+        # the last output against the oracle on sampled (b, c) lines; every
+        # element of every workload is compared in the GPU tests
+        nl = w.B * w.C
+        chk = np.array(sorted(set([0, nl // 2, nl - 1])), dtype=np.int64)
+        ref = _oracle_on_lines(inp, chk).reshape(len(chk), -1)
+        yv = ys[(args.steps - 1) % rot].reshape(nl, -1)[torch.as_tensor(chk, device=dev)]
+        if yv.dtype == torch.bfloat16:
+            got = W.bf16_bits_to_f64(yv.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+        else:
+            got = yv.cpu().numpy().astype(np.float64)
+        entry["parity_rel_l2_sampled_lines"] = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        entry["parity_lines"] = chk.tolist()
+    del calls, sets, base, ys, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    entry["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(inp, cpu_budget)
+    return entry
+
+
+def headline_roofline(e):
+    """The roofline object of the JSON line: the HBM roofline of the metric,
+    algorithmic bytes of one call over the mean call time under HIP events;
+    the ALU fraction beside it."""
+    r = {"bound": "hbm", "achieved": e["hbm_achieved_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+         "frac": e["hbm_frac"], "traffic": e["counter_bytes_per_call"],
+         "kernel_plan": e["plan"], "alg_bytes_per_call": e["alg_bytes_per_call"],
+         "avg_call_us": e["call_us_mean"], "median_call_us": e["call_us_median"], "min_call_us": e["call_us_min"],
+         "alu_achieved_tflops": e["alu_achieved_tflops"], "alu_peak_tflops": FP32_VALU_TFLOPS,
+         "alu_frac": e["alu_frac"], "alu_frac_of_packed_peak": e["alu_frac_of_packed_peak"],
+         "alg_flops_per_call": e["alg_flops_per_call"], "first_bound": e["first_bound"],
+         "counter_to_alg_bytes": e["counter_to_alg_bytes"]}
+    for k in ("profile", "hbm_frac_of_stream_peak"):
+        if k in e:
+            r[k] = e[k]
+    return r
+
+
+def progress(msg: str) -> None:
+    sys.stderr.write(f"[bench] {msg}\n")
+    sys.stderr.flush()
 
 
 def main():
@@ -562,9 +739,13 @@ def main():
     ap.add_argument("--settle-ms", type=float, default=30.0,
                     help="untimed calls worth about this long before the warmup steps, to leave the GPU's idle "
                          "clocks (0: none)")
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=list(W.WORKLOADS))
+    ap.add_argument("--workload", default=None, choices=list(W.WORKLOADS),
+                    help="time this workload only (default: the headline conv2d_64 plus every configuration)")
     ap.add_argument("--rotate", type=int, default=0, help="input sets to rotate (0: enough to exceed 2x the MALL)")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the headline's cpu_baseline")
+    ap.add_argument("--cpu-budget-other", type=float, default=5.0,
+                    help="seconds of oracle work for each other configuration's cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true", help="skip the sampled oracle check (profiling runs)")
     ap.add_argument("--no-stream-peak", action="store_true", help="skip the 1 GiB copy that measures the stream peak")
@@ -585,149 +766,53 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2607_19378_amd import hyenand as H
 
-    w = W.WORKLOADS[args.workload]
-    inp = W.generate(w)
-    if args.backward:
-        bench_backward(args, w, inp)
-        return
-    if args.operator:
-        bench_operator(args, w, inp)
-        return
-    if args.synth:
-        bench_synth(args, w, inp)
-        return
-    if args.modal:
-        bench_modal(args, w, inp)
-        return
-    set_bytes = alg_bytes(w)
-    rot = args.rotate or max(1, min(8, int(np.ceil(2 * MALL_BYTES / set_bytes))))
-    dev = torch.device("cuda:0")
-    base = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
-    sets = [base]
-    for r in range(1, rot):
-        # distinct buffers with the same values: the cache cannot serve one set from another
-        sets.append([t.clone() for t in base])
-    ys = [torch.empty_like(base[0]) for _ in range(rot)]
-    ws_bytes = H.workspace_size(w.shape, w.pad_mode, w.dtype)
-    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None
-    plan = H.plan_name(w.shape, w.pad_mode, w.dtype)
-    stream = torch.cuda.current_stream(dev)
-
-    # one prepared call per input set: the timed loop only enqueues
-    calls = [H.Prepared(ys[r], s[0], s[1], s[2], s[3], s[4], w.pad_mode, ws, stream) for r, s in enumerate(sets)]
-
-    def step(i):
-        calls[i % rot]()
-
-    # The GPU sits idle while the host generates the inputs and comes back
-    # at low clocks; a few milliseconds of the same calls, untimed, bring it
-    # to its working clock before the warmup steps (measured: 80 against
-    # 74 us per conv2d_64 call after 5 warmup steps without this).
-    n_settle = settle_count(alg_flops(w), alg_bytes(w), args.settle_ms)
-    settle_clocks(step, n_settle)
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    # HIP events on the launch stream bracket the timed steps; with no event
-    # between steps the launches queue back to back.
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0.record(stream)
-    for i in range(args.steps):
-        step(i)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
-    gelems = w.elems / (ms_per_step * 1e-3) / 1e9
-    per_call_ms = np.array([ev0.elapsed_time(ev1) / args.steps])
-
-    # One call = the whole path over the workload (one launch for the fused
-    # plans; three or five for the multi-pass plans, timed together).
-    avg_call_s = float(per_call_ms.mean()) * 1e-3
-    flops = alg_flops(w)
-    hbm_gbs = set_bytes / avg_call_s / 1e9
-    alu_tflops = flops / avg_call_s / 1e12
-    # the bound is whichever peak the algorithmic work reaches first
-    alu_bound = flops / (FP32_VALU_TFLOPS * 1e12) > set_bytes / (HBM_PEAK_GBS * 1e9)
-    if alu_bound:
-        roofline = {"bound": "alu", "achieved": round(alu_tflops, 3), "peak": FP32_VALU_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(alu_tflops / FP32_VALU_TFLOPS, 4)}
-    else:
-        roofline = {"bound": "hbm", "achieved": round(hbm_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(hbm_gbs / HBM_PEAK_GBS, 4)}
-    roofline.update({
-        "traffic": stored_traffic(w.name),
-        "hbm_achieved_gbs": round(hbm_gbs, 2), "hbm_frac": round(hbm_gbs / HBM_PEAK_GBS, 4),
-        "alu_achieved_tflops": round(alu_tflops, 3), "alu_frac": round(alu_tflops / FP32_VALU_TFLOPS, 4),
-        "alu_frac_of_packed_peak": round(alu_tflops / FP32_PACKED_TFLOPS, 4),
-        "alg_bytes_per_call": set_bytes, "alg_flops_per_call": round(flops),
-        "kernel_plan": plan, "launches_per_call": "1" if plan.startswith("fused") else "3-5 (chunked)",
-        "avg_call_us": round(avg_call_s * 1e6, 3)})
-    prof = os.path.join("profiles", f"{plan}_{w.name}.md")
-    if os.path.exists(os.path.join(ROOT, prof)):
-        roofline["profile"] = prof  # rocprofv3 kernel trace and counter summary of this command
-
-    copy_calibration(args, dev)
-
-    # measured stream peak: a 1 GiB device-to-device copy (read + write), best of 5
-    stream_gbs = None
-    if not args.no_stream_peak:
-        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-        best = None
-        for _ in range(6):
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            dst.copy_(src)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1)
-            best = ms if best is None else min(best, ms)
-        stream_gbs = 2.0 * src.numel() * 4 / (best * 1e-3) / 1e9
-        del src, dst
-        roofline["stream_peak_gbs"] = round(stream_gbs, 1)
-        roofline["hbm_frac_of_stream_peak"] = round(hbm_gbs / stream_gbs, 4)
-
-    parity = None
-    if not args.no_parity:
-        # the last output against the oracle on a few (b, c) lines
-        import oracle
-        nl = w.B * w.C
-        chk = np.array(sorted(set([0, nl // 2, nl - 1])), dtype=np.int64)
-        sub = [W.storage_to_f64(a.reshape((nl, -1))[chk].reshape((len(chk),) + a.shape[2:]), w.dtype)[None]
-               for a in (inp.x1, inp.x2, inp.v, inp.k)]
-        Dsub = W.storage_to_f64(inp.D, w.dtype)[chk % w.C]
-        ref = oracle.conv_fft(*sub, Dsub, w.pad_mode)[0].reshape(len(chk), -1)
-        yv = ys[(args.steps - 1) % rot]
-        if yv.dtype == torch.bfloat16:
-            got = W.bf16_bits_to_f64(yv.view(torch.int16).cpu().numpy().view(np.uint16))
+    if args.backward or args.operator or args.synth or args.modal:
+        w = W.WORKLOADS[args.workload or DEFAULT_WORKLOAD]
+        inp = W.generate(w)
+        if args.backward:
+            bench_backward(args, w, inp)
+        elif args.operator:
+            bench_operator(args, w, inp)
+        elif args.synth:
+            bench_synth(args, w, inp)
         else:
-            got = yv.cpu().numpy().astype(np.float64)
-        got = got.reshape(nl, -1)[chk]
-        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+            bench_modal(args, w, inp)
+        return
 
-    cpu = None if args.no_cpu_baseline else cpu_baseline(inp, args.cpu_budget)
-
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    stream_gbs = None if args.no_stream_peak else measure_stream_peak(dev, stream)
+    head_name = args.workload or DEFAULT_WORKLOAD
+    names = [head_name] if args.workload else [head_name] + [n for n in CONFIG_ORDER if n != head_name]
+    entries = {}
+    for n in names:
+        w = W.WORKLOADS[n]
+        progress(f"{n}: generating inputs {w.shape} {w.pad_mode} {w.dtype}")
+        inp = W.generate(w)
+        progress(f"{n}: timing {args.steps} steps")
+        entries[n] = bench_forward(args, w, inp, args.cpu_budget if n == head_name else args.cpu_budget_other,
+                                   stream_gbs)
+        e = entries[n]
+        progress(f"{n}: {e['value']} GElem/s, {e['call_us_mean']} us per call, hbm_frac {e['hbm_frac']}")
+        del inp
+    h = entries[head_name]
+    w = W.WORKLOADS[head_name]
     out = {
         "metric": "gated N-D FFT-conv GElem/s and % of HBM roofline on 1 MI355X",
-        "value": round(gelems, 3), "unit": "GElem/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "value": h["value"], "unit": "GElem/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": h["ms_per_step"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage_dtype": w.dtype,
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
         "config": {"workload": w.name, "desc": w.description, "B": w.B, "C": w.C, "grid": list(w.grid),
-                   "pad_mode": w.pad_mode, "storage": w.dtype, "plan": plan, "rotated_input_sets": rot},
-        "roofline": roofline,
-        "cpu_baseline": cpu,
-        "hbm_frac_alg": round(alg_bytes(w) / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-        "parity_rel_l2_sampled": parity,
-        "untimed_calls": {"settle": n_settle, "warmup": args.warmup},
+                   "pad_mode": w.pad_mode, "storage": w.dtype, "plan": h["plan"],
+                   "rotated_input_sets": h["rotated_input_sets"]},
+        "roofline": headline_roofline(h),
+        "cpu_baseline": h["cpu_baseline"],
+        "parity_rel_l2_sampled": h.get("parity_rel_l2_sampled_lines"),
+        "untimed_calls": h["untimed_calls"],
+        "stream_peak_gbs": None if stream_gbs is None else round(stream_gbs, 1),
+        "per_config": [entries[n] for n in names],
         "kernel_source_hash": kernel_source_hash(),
     }
     print(json.dumps(out))

@@ -89,8 +89,7 @@ __device__ __forceinline__ float2 twiddle_rt(uint32_t m, int log2n) {
 template <int NS, int R, bool INV>
 __device__ __forceinline__ float2 pass_twiddle(uint32_t jm, int r) {
   static_assert(NS >= 2 && R >= 2 && R <= 16 && NS * R <= 8192, "pass table range");
-  constexpr uint32_t off = (uint32_t)kPassOff[ilog2(NS)][ilog2(R)];
-  const float2 w = kPassTw[off + (uint32_t)(r - 1) * NS + jm];
+  const float2 w = pass_table<ilog2(NS), ilog2(R)>()[(uint32_t)(r - 1) * NS + jm];
   return INV ? c_conj(w) : w;
 }
 
@@ -216,11 +215,11 @@ struct PassTw {
       constexpr int R = radix(NS);
       if constexpr (NS > 1) {
         constexpr int off = offset(NS), cnt = rows(NS) * NS;
-        constexpr uint32_t g = (uint32_t)kPassOff[ilog2(NS)][ilog2(R)];
+        const float2* tab = pass_table<ilog2(NS), ilog2(R)>();
         for (int i = tid; i < cnt; i += nt) {
           const int q = i / NS, jm = i - q * NS;
           const int r = full(NS) ? q + 1 : (1 << q);
-          lds[off + i] = kPassTw[g + (uint32_t)(r - 1) * NS + jm];
+          lds[off + i] = tab[(uint32_t)(r - 1) * NS + jm];
         }
       }
       fill<NS * R>(lds, tid, nt);

@@ -85,6 +85,35 @@ def counter_per_call(rows, counter: str, calls: int):
     return op / calls, copy, {k: v / calls for k, v in per_kernel.items()}
 
 
+SQ_COUNTERS = ("SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_ACTIVE_INST_VALU", "SQ_BUSY_CYCLES",
+               "SQ_WAVES", "SQ_LDS_IDX_ACTIVE", "SQ_WAIT_INST_LDS", "GRBM_GUI_ACTIVE")
+DRAM_COUNTERS = ("TCC_EA0_RDREQ_DRAM_32B_sum", "TCC_EA0_WRREQ_WRITE_DRAM_32B_sum", "TCC_EA0_RDREQ_sum",
+                 "TCC_EA0_WRREQ_sum")
+
+
+def timed_counters(rows, counters, calls: int, steps: int):
+    """Per-call sums of each counter over the library's dispatches of the
+    last `steps` calls (the timed steps), and per kernel.  The library's
+    dispatches are taken in Dispatch_Id order; a call is the same number of
+    them throughout the command."""
+    lib = sorted({int(r["Dispatch_Id"]) for r in rows if "hyenand" in r["Kernel_Name"]})
+    per_call = len(lib) // calls
+    keep = set(lib[-per_call * steps:])
+    tot = {c: 0.0 for c in counters}
+    per_kernel = {}
+    for r in rows:
+        c = r["Counter_Name"]
+        if c not in tot or int(r["Dispatch_Id"]) not in keep:
+            continue
+        v = float(r["Counter_Value"])
+        tot[c] += v
+        k = short_name(r["Kernel_Name"])
+        per_kernel.setdefault(k, {}).setdefault(c, 0.0)
+        per_kernel[k][c] += v
+    return ({c: v / steps for c, v in tot.items()},
+            {k: {c: v / steps for c, v in d.items()} for k, d in per_kernel.items()}, per_call)
+
+
 def synth_summary(a, W, source_hash):
     """profiles/siren_synth_<workload>.md from rocprofv3 runs of
     ``bench.py --synth``: the synthesis kernel's duration, HBM bytes and
@@ -227,6 +256,10 @@ def main(argv=None):
     ap.add_argument("--cmd-trace", required=True)
     ap.add_argument("--cmd-fetch", required=True)
     ap.add_argument("--cmd-write", required=True)
+    ap.add_argument("--sq", default=None, help="counter run of SQ_* (and GRBM_GUI_ACTIVE) on the same command")
+    ap.add_argument("--dram", default=None, help="counter run of TCC_EA0_*DRAM* requests on the same command")
+    ap.add_argument("--cmd-sq", default="")
+    ap.add_argument("--cmd-dram", default="")
     ap.add_argument("--out", default=os.path.join(ROOT, "profiles"))
     ap.add_argument("--synth", action="store_true", help="runs of bench.py --synth: summarise the synthesis kernel")
     ap.add_argument("--modal", action="store_true", help="runs of bench.py --modal: summarise the modal filter kernel")
@@ -279,7 +312,7 @@ def main(argv=None):
     lines = [f"# {plan} on {w.name}", "",
              f"{w.description}.  Plan `{plan}`; kernel source hash `{h}`.", "",
              "Commands (run from /tmp with TMPDIR=/tmp on the MI355X box; bench.py made "
-             f"{a.calls} hyenand_fftconv calls in each):", "",
+             f"{a.calls} hyenand_fftconv calls in each, the last {a.steps} timed):", "",
              "```", a.cmd_trace, a.cmd_fetch, a.cmd_write, "```", "",
              "## Kernel durations (rocprofv3 --kernel-trace --stats)", "",
              "| kernel | dispatches | avg us | min us | max us | share of op time |",
@@ -305,7 +338,21 @@ def main(argv=None):
         tail_ns += ce - cs
     tail_busy = tail_ns / a.steps
     lines += ["", f"GPU busy time per call over the last {a.steps} calls (the timed steps): "
-                  f"{tail_busy / 1e3:.2f} us ({alg / tail_busy:.1f} GB/s of algorithmic bytes).", ""]
+                  f"{tail_busy / 1e3:.2f} us ({alg / tail_busy:.1f} GB/s of algorithmic bytes, "
+                  f"{100.0 * alg / tail_busy / 8000.0:.2f}% of 8 TB/s).", ""]
+    # per-kernel averages over the timed steps alone
+    tr = sorted(((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), short_name(r["Kernel_Name"]))
+                 for r in _rows(a.trace, "_kernel_trace.csv") if "hyenand" in r["Kernel_Name"]))
+    tr = tr[-max(1, round(len(tr) * a.steps / a.calls)):]
+    agg = {}
+    for s0, e0, k in tr:
+        d = agg.setdefault(k, [])
+        d.append(e0 - s0)
+    lines += [f"Per-kernel durations over the timed steps only ({a.steps} calls):", "",
+              "| kernel | dispatches | avg us | min us | max us |", "|---|---:|---:|---:|---:|"]
+    for k, d in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        lines.append(f"| `{k}` | {len(d)} | {np.mean(d) / 1e3:.2f} | {np.min(d) / 1e3:.2f} | {np.max(d) / 1e3:.2f} |")
+    lines.append("")
     lines += [f"GPU busy time per call over all calls (union of the kernels' intervals): {busy / 1e3:.2f} us "
                   f"({alg / busy:.1f} GB/s of algorithmic bytes, {100.0 * alg / busy / 8000.0:.2f}% of 8 TB/s).  "
                   f"Sum of kernel durations per call: {total_ns / a.calls / 1e3:.2f} us"
@@ -321,6 +368,44 @@ def main(argv=None):
               f"Total: read {fetch_b / 1e6:.2f} MB + write {write_b / 1e6:.2f} MB = {(fetch_b + write_b) / 1e6:.2f} MB "
               f"per call; algorithmic minimum {alg / 1e6:.2f} MB (x1, x2, v, k read and y written once); "
               f"ratio {(fetch_b + write_b) / alg:.3f}.", ""]
+    cmds = [a.cmd_trace, a.cmd_fetch, a.cmd_write]
+    sq_rec = None
+    if a.sq:
+        cmds.append(a.cmd_sq)
+        tot, per_k, per_call = timed_counters(_rows(a.sq, "_counter_collection.csv"), SQ_COUNTERS, a.calls,
+                                              a.steps)
+        sq_rec = tot
+        lines += ["## Instruction and LDS counters per call, timed steps only (rocprofv3 --pmc)", "",
+                  "`" + a.cmd_sq + "`", "",
+                  f"{per_call} library dispatches per call.  SQ_INSTS_* count wave instructions; "
+                  "SQ_ACTIVE_INST_VALU and SQ_WAIT_INST_LDS are in quad-cycles summed over waves; "
+                  "SQ_LDS_BANK_CONFLICT and SQ_LDS_IDX_ACTIVE are cycles summed over CUs; SQ_BUSY_CYCLES "
+                  "sums the shader engines' busy cycles; GRBM_GUI_ACTIVE is the GPU's busy clock count "
+                  "(counter runs serialise the dispatches).", "",
+                  "| kernel | " + " | ".join(SQ_COUNTERS) + " |", "|---|" + "---:|" * len(SQ_COUNTERS)]
+        for k, d in sorted(per_k.items()):
+            lines.append(f"| `{k}` | " + " | ".join(f"{d.get(c, 0.0):.4g}" for c in SQ_COUNTERS) + " |")
+        lines.append("| **per call** | " + " | ".join(f"{tot[c]:.4g}" for c in SQ_COUNTERS) + " |")
+        valu_floor_us = tot["SQ_INSTS_VALU"] * 4 / (256 * 4) / 2.4e3
+        lines += ["", f"VALU issue floor: {tot['SQ_INSTS_VALU'] / 1e6:.2f} M wave instructions x 4 cycles over "
+                      f"1024 SIMDs = {valu_floor_us:.1f} us at 2.4 GHz.  LDS bank-conflict cycles are "
+                      f"{100.0 * tot['SQ_LDS_BANK_CONFLICT'] / max(1.0, tot['SQ_LDS_IDX_ACTIVE']):.2f}% of the "
+                      "LDS-active cycles.", ""]
+    dram_rec = None
+    if a.dram:
+        cmds.append(a.cmd_dram)
+        tot, per_k, _ = timed_counters(_rows(a.dram, "_counter_collection.csv"), DRAM_COUNTERS, a.calls, a.steps)
+        rd = 32.0 * tot["TCC_EA0_RDREQ_DRAM_32B_sum"]
+        wr = 32.0 * tot["TCC_EA0_WRREQ_WRITE_DRAM_32B_sum"]
+        dram_rec = {"read_bytes_per_call": round(rd), "write_bytes_per_call": round(wr)}
+        lines += ["## Requests from the L2 to the memory controller per call, timed steps only", "",
+                  "`" + a.cmd_dram + "`", "",
+                  f"Read {rd / 1e6:.2f} MB and write {wr / 1e6:.2f} MB in 32-byte units "
+                  f"(TCC_EA0_RDREQ_DRAM_32B, TCC_EA0_WRREQ_WRITE_DRAM_32B); {tot['TCC_EA0_RDREQ_sum']:.4g} read "
+                  f"and {tot['TCC_EA0_WRREQ_sum']:.4g} write requests in all.  These requests go to the "
+                  "memory controller's side of the data fabric, where the 256 MiB Infinity Cache sits, so they "
+                  "too count Infinity-Cache hits as well as HBM accesses; no counter exposed to rocprofv3 on "
+                  "gfx950 separates the two.", ""]
     os.makedirs(a.out, exist_ok=True)
     md = os.path.join(a.out, f"{plan}_{w.name}.md")
     with open(md, "w") as fh:
@@ -328,7 +413,7 @@ def main(argv=None):
     rec = {"workload": w.name, "plan": plan, "source_hash": h, "bytes_per_call": round(fetch_b + write_b),
            "fetch_bytes_per_call": round(fetch_b), "write_bytes_per_call": round(write_b),
            "alg_bytes_per_call": alg, "fetch_scale": round(f_scale, 5), "write_scale": round(w_scale, 5),
-           "calls": a.calls, "commands": [a.cmd_fetch, a.cmd_write]}
+           "calls": a.calls, "steps": a.steps, "commands": cmds, "sq_per_call": sq_rec, "dram_per_call": dram_rec}
     with open(os.path.join(a.out, f"traffic_{w.name}.json"), "w") as fh:
         json.dump(rec, fh, indent=1)
         fh.write("\n")

@@ -17,3 +17,13 @@ def oracle_mod():
     import oracle
     oracle.build()
     return oracle
+
+
+def pytest_terminal_summary(terminalreporter, exitstatus, config):
+    """Print the whole-tensor parity figures the GPU tests recorded."""
+    mod = sys.modules.get("gpu_util")
+    lines = getattr(mod, "SUMMARY", None) if mod else None
+    if lines:
+        terminalreporter.section("whole-tensor parity against the fp64 oracle")
+        for line in lines:
+            terminalreporter.write_line(line)

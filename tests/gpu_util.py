@@ -14,6 +14,16 @@ def log(msg):
     sys.stdout.flush()
 
 
+# result lines printed in the terminal summary of the run (pytest keeps a
+# passing test's own output to itself)
+SUMMARY = []
+
+
+def summary(msg):
+    log(msg)
+    SUMMARY.append(msg)
+
+
 def to_device(arr, dtype):
     import torch
     if dtype == "f32":

@@ -1,7 +1,8 @@
 """GPU backward on the multi-pass plans (2D/3D grids beyond LDS and long 1D
 lines) against the oracle's backward, through the C ABI: every gradient
-element by element on small and ragged cases, sampled lines on the full
-workload shapes, and bitwise the same result for every workspace size."""
+element by element on small and ragged cases and bitwise the same result
+for every workspace size (the full workload shapes are compared element by
+element in test_gpu_full_workloads.py)."""
 import numpy as np
 import pytest
 
@@ -95,40 +96,3 @@ def test_backward_workspace_sizes_bitwise(shape, mode, dtype):
     for other in runs[1:]:
         for a, b in zip(runs[0], other):
             assert np.array_equal(a, b)
-
-
-def _sampled(name, channels):
-    """Full workload shape on the GPU; parity of every gradient on the lines of
-    the given channels (all samples, so gD[c] is complete)."""
-    import torch
-    w = W.WORKLOADS[name]
-    log(f"[bwd-full] generating {name}")
-    inp = W.generate(w)
-    gy = _gy(w.shape, w.dtype, 4321)
-    got = _gpu_backward(inp, gy)
-    nl = w.B * w.C
-    lines = np.array([b * w.C + c for b in range(w.B) for c in channels], dtype=np.int64)
-    idx = torch.as_tensor(lines, device="cuda")
-    got_lines = [from_device(g.reshape(nl, -1).index_select(0, idx)) for g in got[:4]]
-    gD = from_device(got[4])[list(channels)]
-    for g in got[:4]:
-        assert bool(torch.isfinite(g.float()).all())
-    del got
-    torch.cuda.empty_cache()
-    sub = []
-    for a in (inp.x1, inp.x2, inp.v, inp.k, gy):
-        flat = a.reshape((nl,) + tuple(w.grid))[lines]
-        sub.append(W.storage_to_f64(flat, w.dtype).reshape((w.B, len(channels)) + tuple(w.grid)))
-    Dsub = W.storage_to_f64(inp.D, w.dtype)[list(channels)]
-    ref = oracle.backward_fft(sub[0], sub[1], sub[2], sub[3], Dsub, sub[4], w.pad_mode)
-    ref_lines = [r.reshape(len(lines), -1) for r in ref[:4]] + [ref[4]]
-    errs = _errs(got_lines + [gD], ref_lines)
-    log(f"[bwd-full] {name} channels {list(channels)}: " + " ".join(f"{n}={e:.2e}" for n, e in errs))
-    for n, e in errs:
-        assert e <= TOL[w.dtype], (n, e)
-
-
-@pytest.mark.parametrize("name,channels", [("conv2d_512c", (0, 77)), ("conv3d_128", (5,)),
-                                           ("conv1d_1m", (0, 200))])
-def test_backward_full_size_sampled(name, channels):
-    _sampled(name, channels)
