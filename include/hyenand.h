@@ -48,14 +48,22 @@ typedef enum {
   HYENAND_ERR_INVALID_ARGUMENT = 1,  /* null pointer, bad enum, dims <= 0, y aliasing an input */
   HYENAND_ERR_UNSUPPORTED = 2,       /* a shape or size beyond the implemented plans */
   HYENAND_ERR_WORKSPACE_TOO_SMALL = 3,
-  HYENAND_ERR_HIP = 4                /* a HIP launch failed; see hyenand_last_error() */
+  HYENAND_ERR_HIP = 4,               /* a HIP launch failed; see hyenand_last_error() */
+  HYENAND_STATUS_MAX_ENUM = 0x7fffffff
 } hyenand_status;
 
-typedef enum { HYENAND_PAD_LINEAR = 0, HYENAND_PAD_CIRCULAR = 1, HYENAND_PAD_CENTERED = 2 } hyenand_pad_mode;
+/* Each enum ends with a 0x7fffffff member so that it spans every int: the
+ * library validates the values it receives, whatever int a caller passes. */
+typedef enum {
+  HYENAND_PAD_LINEAR = 0,
+  HYENAND_PAD_CIRCULAR = 1,
+  HYENAND_PAD_CENTERED = 2,
+  HYENAND_PAD_MAX_ENUM = 0x7fffffff
+} hyenand_pad_mode;
 
 /* Storage type of x1, x2, v, k, D and y.  Compute is fp32 in both cases;
  * bf16 values are widened on load and rounded to nearest-even on store. */
-typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1 } hyenand_dtype;
+typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1, HYENAND_DTYPE_MAX_ENUM = 0x7fffffff } hyenand_dtype;
 
 /*
  * hyenand_fftconv -- y = x2 * (k conv (x1*v) + D*(x1*v)) on the GPU.

@@ -44,6 +44,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _SO = os.path.join(_HERE, "liboracle.so")
+# HYENAND_ORACLE_LIBRARY: a sanitizer build of the same oracle.c to load instead
+_SO_OVERRIDE = os.environ.get("HYENAND_ORACLE_LIBRARY")
 _lock = threading.Lock()
 _lib = None
 
@@ -66,9 +68,12 @@ def lib():
     global _lib
     with _lock:
         if _lib is None:
-            if not os.path.exists(_SO):
-                build()
-            L = ctypes.CDLL(_SO)
+            if _SO_OVERRIDE:
+                L = ctypes.CDLL(_SO_OVERRIDE)
+            else:
+                if not os.path.exists(_SO):
+                    build()
+                L = ctypes.CDLL(_SO)
             sig = [_f64p] * 5
             L.oracle_direct.argtypes = sig + [_f64p, ctypes.c_int, _i64p, ctypes.c_int, _i64p,
                                               ctypes.c_int64, ctypes.c_int]

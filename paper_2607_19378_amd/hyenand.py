@@ -13,7 +13,9 @@ import threading
 from typing import Optional, Sequence
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libhyenand.so")
+# HYENAND_LIBRARY selects another build of the same library (the sanitizer
+# build of paper_2607_19378_amd.build --sanitize)
+LIB_PATH = os.environ.get("HYENAND_LIBRARY") or os.path.join(_PKG, "libhyenand.so")
 
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = range(5)
 PAD_LINEAR, PAD_CIRCULAR, PAD_CENTERED = 0, 1, 2
