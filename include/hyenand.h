@@ -139,6 +139,27 @@ hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const vo
                                         hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace, size_t workspace_bytes,
                                         void* stream);
 
+/*
+ * hyenand_fftconv_noalloc -- hyenand_fftconv for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Arguments, layouts, validation, stream
+ * semantics and results are those of hyenand_fftconv, with no workspace
+ * argument: the multi-pass plans use the library's own device scratch of
+ * 128 MiB (128 << 20 bytes) per GPU instead, a static array reserved when the
+ * library's code is loaded on that GPU and held until the process ends.
+ * Shapes whose least workspace (hyenand_fftconv_workspace_min) exceeds it
+ * return HYENAND_ERR_UNSUPPORTED before anything runs.  The call allocates
+ * no memory; the first call on a device looks the array up there once.
+ * Every call on one GPU shares that GPU's scratch: two calls whose work may
+ * overlap in time on the same GPU (on different streams, or from different
+ * host threads without ordering) race on it and give wrong results; order
+ * them on one stream or use hyenand_fftconv with a workspace each.  The
+ * scratch keeps the last call's contents, which no call reads before writing.
+ */
+hyenand_status hyenand_fftconv_noalloc(const void* x1, const void* x2, const void* v, const void* k,
+                                       const void* D, void* y, int ndim, const int64_t* dims,
+                                       hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream);
+
 /* Recommended workspace size (bytes) for a call with these arguments; 0 for
  * plans that keep everything on chip.  Pure host function. */
 hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,

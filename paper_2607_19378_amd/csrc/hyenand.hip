@@ -433,6 +433,12 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 }  // namespace
 
+namespace hyenand {
+// the calling thread's last-error text, for entry points in other
+// translation units
+hyenand_status set_last_error(hyenand_status s, const char* msg) { return fail(s, "%s", msg); }
+}  // namespace hyenand
+
 extern "C" {
 
 hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,

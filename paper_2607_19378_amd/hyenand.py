@@ -21,7 +21,7 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = ra
 PAD_LINEAR, PAD_CIRCULAR, PAD_CENTERED = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
-EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_workspace_size",
+EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_noalloc", "hyenand_fftconv_workspace_size",
             "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
@@ -52,6 +52,9 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv.restype = ctypes.c_int
             L.hyenand_fftconv_shared_k.argtypes = L.hyenand_fftconv.argtypes
             L.hyenand_fftconv_shared_k.restype = ctypes.c_int
+            L.hyenand_fftconv_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
+                                                  ctypes.c_int, vp]
+            L.hyenand_fftconv_noalloc.restype = ctypes.c_int
             for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min"):
                 f = getattr(L, name)
                 f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
@@ -216,6 +219,29 @@ def fftconv_into(y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None,
     """y <- x2 * (k conv (x1*v) + D*(x1*v)); all tensors already allocated on
     the GPU.  shared_k: k is [C, L...], one kernel per channel for every sample."""
     Prepared(y, x1, x2, v, k, D, pad_mode, workspace, stream, shared_k)()
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def fftconv_noalloc_into(y, x1, x2, v, k, D, pad_mode: str = "linear", stream=None) -> None:
+    """y <- x2 * (k conv (x1*v) + D*(x1*v)) through hyenand_fftconv_noalloc:
+    no workspace argument, the library's static device scratch instead
+    (calls overlapping on one GPU race on it)."""
+    import torch
+    shape = tuple(x1.shape)
+    for t, want in ((x1, shape), (x2, shape), (v, shape), (k, kernel_shape(shape, pad_mode)), (y, shape)):
+        if not t.is_cuda or tuple(t.shape) != want or t.dtype != x1.dtype or not t.is_contiguous():
+            raise ValueError("x1, x2, v, y must be contiguous GPU tensors of one shape and dtype; "
+                             f"k must be {kernel_shape(shape, pad_mode)}")
+    if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():
+        raise ValueError("D must be a contiguous [C] GPU tensor of the same dtype")
+    if stream is None:
+        stream = torch.cuda.current_stream(x1.device)
+    nd, dims = _dims(shape)
+    _check(lib().hyenand_fftconv_noalloc(_ptr(x1), _ptr(x2), _ptr(v), _ptr(k), _ptr(D), _ptr(y), nd, dims,
+                                         _mode(pad_mode), _dtype_code(x1.dtype),
+                                         ctypes.c_void_p(stream.cuda_stream)))
 
 
 def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=None, shared_k: bool = False):

@@ -364,3 +364,16 @@ def test_embedded_grid_bounded():
     with pytest.raises(H.HyenandError) as e:
         H.plan_name((1, 2049, 300, 300), "linear", "f32")
     assert e.value.status == H.ERR_UNSUPPORTED
+
+
+def test_noalloc_rejects_beyond_its_scratch(L):
+    """The no-allocation entry point refuses, on the host, shapes whose least
+    workspace exceeds its static scratch (128 MiB per GPU)."""
+    dims = (ctypes.c_int64 * 5)(1, 1, 256, 256, 256)
+    p = [ctypes.c_void_p(FAKE + i * (1 << 36)) for i in range(6)]
+    assert L.hyenand_fftconv_noalloc(*p, 3, dims, 0, 0, None) == H.ERR_UNSUPPORTED
+    assert b"scratch" in L.hyenand_last_error()
+    assert H.workspace_min((1, 1, 128, 128, 128), "linear", "bf16") <= H.NOALLOC_SCRATCH_BYTES
+    assert H.workspace_min((1, 1, 1 << 20), "linear", "bf16") <= H.NOALLOC_SCRATCH_BYTES
+    dims = (ctypes.c_int64 * 3)(1, 0, 64)
+    assert L.hyenand_fftconv_noalloc(*p, 1, dims, 0, 0, None) == H.ERR_INVALID_ARGUMENT
