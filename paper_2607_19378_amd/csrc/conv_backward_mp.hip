@@ -79,9 +79,11 @@ __global__ void __launch_bounds__(256)
   __shared__ float2 S[3][RPW * HP];  // u, k, h rows
   __shared__ float2 twl[imax(1, PassTw<ML, E>::kCount)];
   __shared__ float red[NT / 64];
+  __shared__ int64_t roff[RPW];
   const int64_t row0 = (int64_t)blockIdx.x * rpw;  // rows of one line (rpw divides rows)
   const int tid = threadIdx.x;
   PassTw<ML, E>::fill(twl, tid, NT);
+  ws_row_offsets<RPW, NT>(roff, row0, rpw, rows, L1, P1, HS, per_line, tid);
 
   // stage the real rows as packed pairs; every lane adds h u over the
   // elements it stages
@@ -195,10 +197,7 @@ __global__ void __launch_bounds__(256)
       [&](int i, const Bin3& z) {
         const int r = i / H, f = i - r * H;
         if (r < rpw) {
-          const int64_t gr = row0 + r;
-          const int64_t line = gr / rows;
-          const int rr = (int)(gr - line * rows);
-          float2* U = ws + line * per_line + ws_row(rr, L1, P1, HS) + f;
+          float2* U = ws + roff[r] + f;
           U[0] = z.u;
           U[half] = z.k;
           U[2 * half] = z.h;
@@ -307,11 +306,14 @@ __global__ void __launch_bounds__(256)
   constexpr int ML = PL / 2;
   __shared__ float2 reg[3][PPW * PRP];  // z, gu, gk pair regions
   __shared__ float2 twl[imax(1, PassTw<PL, E>::kCount)];
+  __shared__ int64_t roff[2 * PPW];
   const int64_t total_pairs = (int64_t)nlines * rows / 2;
   const int64_t pair0 = (int64_t)blockIdx.x * PPW;
   const int npair = (int)((total_pairs - pair0) < PPW ? (total_pairs - pair0) : PPW);
   const int tid = threadIdx.x;
   PassTw<PL, E>::fill(twl, tid, NT);
+  ws_row_offsets<2 * PPW, NT>(roff, 2 * pair0, 2 * npair, rows, L1, P1, HS, per_line, tid);
+  __syncthreads();
 
   // load the half-spectrum rows of each pair: row a at [0, H), row b at [H, 2H)
   struct Bin3 {
@@ -325,10 +327,7 @@ __global__ void __launch_bounds__(256)
         Bin3 z;
         z.z = z.gu = z.gk = czero();
         if (q < npair) {
-          const int64_t gr = 2 * (pair0 + q) + ab;
-          const int64_t line = gr / rows;
-          const int rr = (int)(gr - line * rows);
-          const float2* src = ws + line * per_line + ws_row(rr, L1, P1, HS) + f;
+          const float2* src = ws + roff[2 * q + ab] + f;
           z.z = src[0];
           z.gu = src[half];
           z.gk = src[2 * half];

@@ -53,11 +53,13 @@ __global__ void __launch_bounds__(256)
   __shared__ float2 Ur[RPW * HP];
   __shared__ float2 Kr[RPW * HP];
   __shared__ float2 twl[imax(1, PassTw<ML, E>::kCount)];
+  __shared__ int64_t roff[RPW];
   const int64_t total_rows = (int64_t)nlines * rows;
   const int64_t row0 = (int64_t)blockIdx.x * RPW;
   const int nrow = (int)((total_rows - row0) < RPW ? (total_rows - row0) : RPW);
   const int tid = threadIdx.x;
   PassTw<ML, E>::fill(twl, tid, NT);
+  ws_row_offsets<RPW, NT>(roff, row0, nrow, rows, L1, P1, HS, per_line, tid);
 
   // stage real rows (the input rows of the chunk are contiguous), four
   // samples per global load, written to LDS as two 8-byte pairs
@@ -175,13 +177,9 @@ __global__ void __launch_bounds__(256)
       [&](int i, float4 z) {
         const int r = i / H, f = i - r * H;
         if (r < nrow) {
-          const int64_t gr = row0 + r;
-          const int64_t line = gr / rows;
-          const int rr = (int)(gr - line * rows);
-          float2* U = ws + line * per_line;
-          const int64_t off = ws_row(rr, L1, P1, HS) + f;
-          U[off] = make_float2(z.x, z.y);
-          if (nsig > 1) U[half + off] = make_float2(z.z, z.w);
+          float2* U = ws + roff[r] + f;
+          U[0] = make_float2(z.x, z.y);
+          if (nsig > 1) U[half] = make_float2(z.z, z.w);
         }
       });
 }
@@ -375,11 +373,14 @@ __global__ void __launch_bounds__(256)
   constexpr int ML = PL / 2;
   __shared__ float2 reg[PPW * PRP];
   __shared__ float2 twl[imax(1, PassTw<PL, E>::kCount)];
+  __shared__ int64_t roff[2 * PPW];
   const int64_t total_pairs = (int64_t)nlines * rows / 2;
   const int64_t pair0 = (int64_t)blockIdx.x * PPW;
   const int npair = (int)((total_pairs - pair0) < PPW ? (total_pairs - pair0) : PPW);
   const int tid = threadIdx.x;
   PassTw<PL, E>::fill(twl, tid, NT);
+  ws_row_offsets<2 * PPW, NT>(roff, 2 * pair0, 2 * npair, rows, L1, P1, HS, per_line, tid);
+  __syncthreads();
 
   // load the half-spectrum rows of each pair: row a at [0, H), row b at [H, 2H)
   batched_copy<PPW * 2 * H, NT, 8>(
@@ -388,12 +389,7 @@ __global__ void __launch_bounds__(256)
         const int q = i / (2 * H), rem = i - q * 2 * H;
         const int ab = rem / H, f = rem - ab * H;
         float2 z = czero();
-        if (q < npair) {
-          const int64_t gr = 2 * (pair0 + q) + ab;
-          const int64_t line = gr / rows;
-          const int rr = (int)(gr - line * rows);
-          z = ws[line * per_line + ws_row(rr, L1, P1, HS) + f];
-        }
+        if (q < npair) z = ws[roff[2 * q + ab] + f];
         return z;
       },
       [&](int i, float2 z) {

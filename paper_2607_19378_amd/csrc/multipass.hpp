@@ -50,6 +50,27 @@ __device__ __forceinline__ int64_t ws_row(int r, int L1, int P1, int HS) {
   return ((int64_t)(r / L1) * P1 + (r % L1)) * HS;
 }
 
+// Workspace offsets (complex entries from ws) of the NR consecutive chunk
+// rows grow0 .. grow0 + NR - 1 that one workgroup moves, written to off[] by
+// its NT lanes (NR may exceed NT: short rows pack many per workgroup): the
+// divisions by the run-time row counts happen once per row here instead of
+// once per element in the copy loops.  Rows at or beyond nrow get offset 0
+// (never used).  The caller synchronises before reading off[].
+template <int NR, int NT>
+__device__ __forceinline__ void ws_row_offsets(int64_t* off, int64_t grow0, int nrow, int rows, int L1, int P1,
+                                               int HS, int64_t per_line, int tid) {
+  for (int r = tid; r < NR; r += NT) {
+    int64_t o = 0;
+    if (r < nrow) {
+      const int64_t gr = grow0 + r;
+      const int64_t line = gr / rows;
+      const int rr = (int)(gr - line * rows);
+      o = line * per_line + ws_row(rr, L1, P1, HS);
+    }
+    off[r] = o;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // strided tiles: TL adjacent columns of a [rows][stride] complex matrix,
 // transformed along the rows index.  LDS tile [P][TLP].  Columns whose index
