@@ -627,6 +627,11 @@ hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, voi
   L.nl = (int)nl;
   const bool three = a.ndim == 3;
   hipError_t e;
+  if (three && slab3d_supported(a)) {  // slab, line, slab
+    if ((e = launch_slab3d(a, line0, nl, ws, false, s)) != hipSuccess) return e;
+    if ((e = d_core(L.g.P0, L)) != hipSuccess) return e;
+    return launch_slab3d(a, line0, nl, ws, true, s);
+  }
   if ((e = d_rows_fwd(L.g.PL, L)) != hipSuccess) return e;
   if (L.g.kc && (e = d_rows_kc(L.g.PL, L)) != hipSuccess) return e;
   if (three && (e = d_axis1_fwd(L.g.P1, L)) != hipSuccess) return e;

@@ -30,11 +30,12 @@ hyenand_status fail(hyenand_status s, const char* fmt, ...) {
 
 enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP, PLAN_FUSED_RL, PLAN_EMBED };
 
-const char* plan_name(Plan p, int ndim) {
+const char* plan_name(Plan p, const FftConvArgs& a) {
+  const int ndim = a.ndim;
   switch (p) {
     case PLAN_FUSED1D: return "fused1d";
     case PLAN_FUSED2D: return "fused2d";
-    case PLAN_MULTIPASS: return ndim == 3 ? "multipass3d" : "multipass2d";
+    case PLAN_MULTIPASS: return ndim == 3 ? (slab3d_supported(a) ? "slab3d" : "multipass3d") : "multipass2d";
     case PLAN_FOURSTEP: return "fourstep1d";
     case PLAN_FUSED_RL: return ndim == 1 ? "fused1d_any" : "fused2d_any";
     case PLAN_EMBED: return ndim == 1 ? "embedded1d" : (ndim == 2 ? "embedded2d" : "embedded3d");
@@ -473,7 +474,7 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, hyenand_
   if (st != HYENAND_OK) return st;
   const Plan p = choose_plan(a);
   if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
-  snprintf(buf, n, "%s", plan_name(p, a.ndim));
+  snprintf(buf, n, "%s", plan_name(p, a));
   return HYENAND_OK;
 }
 
@@ -540,7 +541,7 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   if (per > 0) {
     if (!workspace || workspace_bytes < per)
       return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "plan %s needs at least %zu workspace bytes, got %zu",
-                  plan_name(p, a.ndim), per, workspace ? workspace_bytes : (size_t)0);
+                  plan_name(p, a), per, workspace ? workspace_bytes : (size_t)0);
     if (overlaps(workspace, workspace_bytes, y, nb)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps y");
     for (int i = 0; i < 4; ++i)
       if (overlaps(workspace, workspace_bytes, ins[i], in_bytes[i]))

@@ -47,6 +47,12 @@ hipError_t launch_fused_rl(const FftConvArgs& a, hipStream_t s);
 bool multipass_supported(const FftConvArgs& a);
 size_t multipass_bytes_per_line(const FftConvArgs& a);
 hipError_t launch_multipass(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, hipStream_t s);
+// three-pass 3D plan (conv_slab.hip) for grids whose planes fit in LDS: the
+// slab passes before (inverse = false) and after (inverse = true) the
+// multi-pass core, on the same workspace layout; launch_multipass takes it
+// where slab3d_supported (HYENAND_SLAB=0 turns it off)
+bool slab3d_supported(const FftConvArgs& a);
+hipError_t launch_slab3d(const FftConvArgs& a, int64_t line0, int64_t nl, void* ws, bool inverse, hipStream_t s);
 
 // backward
 struct FftConvBwdArgs {

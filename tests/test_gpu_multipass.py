@@ -258,3 +258,59 @@ def test_host_threads_each_with_own_side_streams():
     log(f"[threads] {len(cases)} threads done, errors={errors}")
     assert not any(t.is_alive() for t in threads)
     assert not errors, errors
+
+
+SLAB = [((4, 32, 32), "linear"), ((2, 64, 64), "linear"), ((4, 128, 128), "linear"), ((2, 64, 64), "circular"),
+        ((4, 128, 128), "circular"), ((8, 128, 128), "linear")]
+
+
+@pytest.mark.parametrize("grid,mode", SLAB)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_slab3d(grid, mode, dtype):
+    """The three-pass 3D plan (planes transformed on chip along both inner
+    axes, the multi-pass core along axis 0) against the oracle, every
+    element."""
+    inp = W.random_case(2, 3, grid, mode, dtype, seed=800 + sum(grid))
+    assert plan(inp) == "slab3d"
+    check_full(inp, f"slab3d {grid}")
+
+
+@pytest.mark.parametrize("grid,mode", [((4, 128, 128), "linear"), ((2, 128, 128), "circular")])
+def test_slab3d_and_five_pass_agree_with_oracle(monkeypatch, grid, mode):
+    """The same shapes on the five-pass plan (slab plan switched off) also
+    match the oracle, and the two plans agree to rounding."""
+    inp = W.random_case(1, 3, grid, mode, "f32", seed=850 + grid[0])
+    y_slab = check_full(inp, f"slab {grid}")
+    monkeypatch.setenv("HYENAND_SLAB", "0")
+    assert plan(inp) == "multipass3d"
+    y_five = check_full(inp, f"five-pass {grid}")
+    assert rel_l2(y_slab, y_five) <= 1e-6
+
+
+def test_slab3d_chunking_and_shared_k():
+    """Chunked workspaces give bitwise the recommended one's result; one
+    kernel per channel (k as [C, ...]) through the slab plan."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    from gpu_util import to_device
+    inp = W.random_case(2, 3, (4, 128, 128), "linear", "bf16", seed=861)
+    w = inp.workload
+    assert plan(inp) == "slab3d"
+    wmin = H.workspace_min(w.shape, w.pad_mode, w.dtype)
+    y1 = run_gpu(inp, workspace_bytes=wmin)
+    y2 = run_gpu(inp)
+    assert np.array_equal(y1, y2)
+    assert rel_l2(y2, oracle_ref(inp)) <= TOL["bf16"]
+    # shared k: every sample uses k[0]'s channels
+    ksh = inp.k[0]
+    dev = [to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, ksh, inp.D)]
+    y = H.fftconv(*dev, pad_mode=w.pad_mode, shared_k=True)
+    torch.cuda.synchronize()
+    import oracle
+    x1, x2, v, k, D = inp.as_f64()
+    kb = np.broadcast_to(k[:1], k.shape).copy()
+    ref = oracle.conv_fft(x1, x2, v, kb, D, w.pad_mode)
+    from gpu_util import from_device
+    err = rel_l2(from_device(y), ref)
+    log(f"[slab shared k] rel_l2={err:.3e}")
+    assert err <= TOL["bf16"]
