@@ -428,9 +428,12 @@ def bench_modal(args, w, inp):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e-3 / args.steps, (time.perf_counter() - t0) / args.steps
 
+    y2 = torch.empty_like(x1)
+    fused = H.PreparedModalConv(y2, x1, x2, v, *d, D, w.pad_mode, ws, stream)
     gen_s, _ = timed([gen])
     conv_s, _ = timed([conv])
     both_s, both_wall = timed([gen, conv])
+    fused_s, fused_wall = timed([fused])
     copy_calibration(args, dev)
     # Per point and mode the sum takes Re(z w) = Re z Re w - Im z Im w and
     # accumulates it: two multiply-adds, 4 flops, run as a matrix-core
@@ -459,6 +462,20 @@ def bench_modal(args, w, inp):
         got = (W.bf16_bits_to_f64(got.view(torch.int16).cpu().numpy().view(np.uint16)) if got.dtype == torch.bfloat16
                else got.cpu().numpy().astype(np.float64))
         parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+    fused_parity = None
+    if not args.no_parity:
+        # the fused call's output on three channels' lines against the
+        # oracle's filter through the oracle's convolution
+        import oracle
+        rows = [0, w.C // 2, w.C - 1]
+        kf = oracle.modal_filter(*[p[n][rows].astype(np.float64) for n in ("log_mag", "angle", "res_re", "res_im")], L)
+        sub = [W.storage_to_f64(a[0, rows], w.dtype)[None] for a in (inp.x1, inp.x2, inp.v)]
+        ref = oracle.conv_fft(sub[0], sub[1], sub[2], kf[None], W.storage_to_f64(inp.D, w.dtype)[rows],
+                              w.pad_mode)[0]
+        got = y2[0, rows]
+        got = (W.bf16_bits_to_f64(got.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+               if got.dtype == torch.bfloat16 else got.cpu().numpy().astype(np.float64))
+        fused_parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
     out = {
         "metric": "modal filter generation + gated 1D FFT conv GElem/s on 1 MI355X",
         "value": round(w.elems / both_wall / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
@@ -473,7 +490,12 @@ def bench_modal(args, w, inp):
                          hbm_frac_of_k_write=round(k_bytes / gen_s / 1e9 / HBM_PEAK_GBS, 4)),
         "modal_us": round(gen_s * 1e6, 3), "conv_us": round(conv_s * 1e6, 3),
         "modal_then_conv_us": round(both_s * 1e6, 3),
-        "cpu_baseline": None, "parity_rel_l2_sampled_channels": parity, "kernel_source_hash": kernel_source_hash(),
+        "fused_modal_conv_us": round(fused_s * 1e6, 3),
+        "fused_modal_conv_gelems": round(w.elems / fused_wall / 1e9, 3),
+        "fused_alg_bytes_per_call": 4 * w.elems * w.storage_bytes,
+        "fused_hbm_frac": round(4 * w.elems * w.storage_bytes / fused_s / 1e9 / HBM_PEAK_GBS, 4),
+        "cpu_baseline": None, "parity_rel_l2_sampled_channels": parity, "fused_parity_rel_l2_sampled_lines": fused_parity,
+        "kernel_source_hash": kernel_source_hash(),
     }
     print(json.dumps(out))
 

@@ -160,6 +160,38 @@ hyenand_status hyenand_fftconv_noalloc(const void* x1, const void* x2, const voi
                                        const void* D, void* y, int ndim, const int64_t* dims,
                                        hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream);
 
+/*
+ * hyenand_fftconv_modal -- hyenand_fftconv_shared_k with the kernel of every
+ * channel generated inside the transform kernels instead of read: the
+ * implicit long filter of order M of the appendix "Filter Generation",
+ *
+ *     k[c, t] = Re sum_{m < M} R[c, m] lambda[c, m]^t,  t = 0 .. L - 1,
+ *     lambda = exp(log_mag + i angle),  R = res_re + i res_im
+ *
+ * (the filter hyenand_modal_filter writes), evaluated where the FFT kernel
+ * would load k -- the paper fuses kernel evaluation into its FFT kernel
+ * (section 3.2.1, "Support for circular and non-circular convolutions";
+ * section 4, "CUDA Implementation: nSubQ") -- so no k tensor exists.  Every
+ * sample of channel c uses filter c.
+ * log_mag, angle, res_re, res_im : device pointers, [C, M] fp32, 4-byte
+ *   aligned; order = M in 1..32.
+ * Other arguments, layouts, workspace (the sizes hyenand_fftconv_workspace_*
+ * report for the same dims), stream and error conventions as for
+ * hyenand_fftconv.  Runs on the four-step plan only: 1D lines with a
+ * transform of 2^15 .. 2^22 points (linear: L = 2^14 .. 2^21; circular:
+ * L = 2^15 .. 2^22), pad_mode linear or circular; other shapes return
+ * HYENAND_ERR_UNSUPPORTED (hyenand_modal_filter and
+ * hyenand_fftconv_shared_k cover them).  Each point of the filter is at most
+ * N1 / T - 1 fp32 steps (7 for 2^20-point lines) from terms formed exactly
+ * from a double phase, and stays in fp32 (it is not rounded to the storage
+ * type).
+ */
+hyenand_status hyenand_fftconv_modal(const void* x1, const void* x2, const void* v, const float* log_mag,
+                                     const float* angle, const float* res_re, const float* res_im, int order,
+                                     const void* D, void* y, int ndim, const int64_t* dims,
+                                     hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+
 /* Recommended workspace size (bytes) for a call with these arguments; 0 for
  * plans that keep everything on chip.  Pure host function. */
 hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,

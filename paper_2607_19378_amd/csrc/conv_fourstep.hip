@@ -32,7 +32,7 @@ template <int N1, bool CIRC, typename TS, bool KC = false, bool ACT = false>
 __global__ void __launch_bounds__(512)
     fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int kC, ActIn ain,
-                int C) {
+                int C, int u_only) {
   static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
@@ -42,8 +42,10 @@ __global__ void __launch_bounds__(512)
   __shared__ float2 twl[imax(1, PassTw<N1, E>::kCount)];
   PassTw<N1, E>::fill(twl, threadIdx.x, NT);
   const int ntile = N2 / TL;
-  const int sig = (int)(blockIdx.x & 1);  // 0: u = x1 v, 1: k
-  const int64_t rest = blockIdx.x >> 1;
+  // 0: u = x1 v, 1: k (u_only: every workgroup takes u; k comes from
+  // fs_cols_modal)
+  const int sig = u_only ? 0 : (int)(blockIdx.x & 1);
+  const int64_t rest = u_only ? (int64_t)blockIdx.x : (int64_t)(blockIdx.x >> 1);
   const int64_t line = rest / ntile;
   const int c0 = (int)(rest % ntile) * TL;
   const int64_t M = (int64_t)N1 * N2;
@@ -94,6 +96,90 @@ __global__ void __launch_bounds__(512)
     const uint32_t m2 = (uint32_t)(c0 + cc);
     twiddle_run<E>(w, twiddle_rt<false>(m2 * (uint32_t)t, log2M), twiddle_rt<false>(m2 * (uint32_t)T, log2M));
     float2* A = ws + line * per_line + (sig ? M : 0) + c0 + cc;
+#pragma unroll
+    for (int e = 0; e < E; ++e) A[(size_t)(t + T * e) * N2] = w[e];
+  }
+}
+
+// Columns of the packed kernel line for a modal filter generated in place of
+// the k read (section 3.2.1's kernel evaluated inside the FFT kernel, here the
+// implicit modal filter of the appendix "Filter Generation"): for line
+// (b, c) the lane holding rows m1 = t + T e of column m2 needs
+// k[2m] + i k[2m + 1], m = m1 N2 + m2, with k[s] = Re sum_j R_j lambda_j^s.
+// The workgroup first tabulates, exactly (polar: double phase), A_j[cc] =
+// R_j lambda_j^(2 m2) for its TL columns, B_j[t] = lambda_j^(2 N2 t) for the
+// T lane rows, the step lambda_j^(2 N2 T) and lambda_j; a lane's first point
+// is A_j[cc] B_j[t] and each further row one fp32 step on, at most
+// N1 / T - 1 steps from an exact anchor.  Then the same column transform,
+// twiddle and store as the k columns of fs_cols_fwd.
+template <int N1, bool CIRC>
+__global__ void __launch_bounds__(512)
+    fs_cols_modal(ModalIn md, float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int C) {
+  using Cf = ColCfg<N1>;
+  constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
+  constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1 of the kernel
+  constexpr int MX = kMaxFusedModalOrder;
+  static_assert(NT / T >= TL, "one round covers the tile");
+  __shared__ float2 tile[N1 * TLP];
+  __shared__ float2 twl[imax(1, PassTw<N1, E>::kCount)];
+  __shared__ float2 tA[MX * TL];
+  __shared__ float2 tB[MX * T];
+  __shared__ float2 tS[MX], tL[MX];
+  const int tid = threadIdx.x;
+  PassTw<N1, E>::fill(twl, tid, NT);
+  const int ntile = N2 / TL;
+  const int64_t line = blockIdx.x / ntile;
+  const int c0 = (int)(blockIdx.x % ntile) * TL;
+  const int64_t M = (int64_t)N1 * N2;
+  const int64_t ch = (line0 + line) % C;
+  const int nm = md.M;
+  const float* pa = md.a + ch * nm;
+  const float* pt = md.th + ch * nm;
+  for (int i = tid; i < nm * (TL + T + 2); i += NT) {
+    int j, kind, idx;
+    if (i < nm * TL) {
+      j = i / TL, idx = i - j * TL, kind = 0;
+    } else if (i < nm * (TL + T)) {
+      j = (i - nm * TL) / T, idx = i - nm * TL - j * T, kind = 1;
+    } else {
+      j = (i - nm * (TL + T)) >> 1, idx = 0, kind = 2 + ((i - nm * (TL + T)) & 1);
+    }
+    const double s = kind == 0 ? 2.0 * (double)(c0 + idx)
+                               : (kind == 1 ? 2.0 * (double)N2 * idx : (kind == 2 ? 2.0 * (double)N2 * T : 1.0));
+    float cs, sn, mg;
+    polar(s * (double)pa[j], s * (double)pt[j], cs, sn, mg);
+    float2 z = make_float2(mg * cs, mg * sn);
+    if (kind == 0) z = c_mul(make_float2(md.re[ch * nm + j], md.im[ch * nm + j]), z);
+    if (kind == 0) tA[j * TL + idx] = z;
+    else if (kind == 1) tB[j * T + idx] = z;
+    else if (kind == 2) tS[j] = z;
+    else tL[j] = z;
+  }
+  __syncthreads();
+  const int cc = tid % (NT / T), t = tid / (NT / T);
+  const bool act = cc < TL;
+  float2 w[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) w[e] = czero();
+  if (act) {
+    for (int j = 0; j < nm; ++j) {
+      float2 z = c_mul(tA[j * TL + cc], tB[j * T + t]);
+      const float2 st = tS[j], l1 = tL[j];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        if (CIRC || t + T * e < NZ) {
+          w[e].x += z.x;                                  // k[2m]
+          w[e].y = fmaf(z.x, l1.x, fmaf(-z.y, l1.y, w[e].y));  // k[2m + 1] = Re(z lambda)
+          z = c_mul(z, st);
+        }
+      }
+    }
+  }
+  BlockFFT<N1, E, false>::run(w, t, ScrS<TLP>{tile + (act ? cc : 0)}, act, twl);
+  if (act) {
+    const uint32_t m2 = (uint32_t)(c0 + cc);
+    twiddle_run<E>(w, twiddle_rt<false>(m2 * (uint32_t)t, log2M), twiddle_rt<false>(m2 * (uint32_t)T, log2M));
+    float2* A = ws + line * per_line + M + c0 + cc;
 #pragma unroll
     for (int e = 0; e < E; ++e) A[(size_t)(t + T * e) * N2] = w[e];
   }
@@ -251,10 +337,22 @@ struct FsLaunch {
 template <int N1>
 hipError_t cols_fwd(const FsLaunch& L) {
   constexpr int TL = ColCfg<N1>::TL;
-  const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * 2));
   const FftConvArgs& a = *L.a;
+  const int u_only = a.modal.M > 0;  // the kernel's columns come from fs_cols_modal
+  const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * (u_only ? 1 : 2)));
+  if (u_only) {
+    const dim3 kgrid((unsigned)((int64_t)L.nl * (kN2 / TL)));
+    if (a.circular)
+      hipLaunchKernelGGL((fs_cols_modal<N1, true>), kgrid, dim3(512), 0, L.s, a.modal, L.ws, L.line0, kN2, L.log2M,
+                         L.per, (int)a.C);
+    else
+      hipLaunchKernelGGL((fs_cols_modal<N1, false>), kgrid, dim3(512), 0, L.s, a.modal, L.ws, L.line0, kN2, L.log2M,
+                         L.per, (int)a.C);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
 #define HY_ARGS(TS) \
-  (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC, a.act_in, (int)a.C
+  (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC, a.act_in, (int)a.C, u_only
 #define HY_LAUNCH(CI, TS, KC)                                                                                     \
   if (a.act) hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, true>), grid, dim3(512), 0, L.s, HY_ARGS(TS)); \
   else hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, false>), grid, dim3(512), 0, L.s, HY_ARGS(TS));

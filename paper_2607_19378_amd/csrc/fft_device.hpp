@@ -589,6 +589,17 @@ __device__ __forceinline__ Gates<ACT> line_gates(const ActIn& act, int64_t line,
   return g;
 }
 
+// exp(mag_log) (cos phase, sin phase) from a phase and log-magnitude formed
+// in double: the phase is reduced to [-pi, pi] in double before the fp32
+// sine and cosine, so a mode's factor at a large power t stays exact to a
+// few fp32 roundings (modal filters).
+__device__ __forceinline__ void polar(double mag_log, double phase, float& c, float& s, float& m) {
+  const double two_pi = 6.283185307179586;
+  const float r = (float)(phase - two_pi * rint(phase * (1.0 / two_pi)));  // in [-pi, pi]
+  __sincosf(r, &s, &c);
+  m = __expf((float)mag_log);
+}
+
 // Spectral product with the shortcut folded in: U (K + D), D times the
 // transform of a unit impulse (1 at every bin).  Inputs are 2U and 2K.
 __device__ __forceinline__ float2 gated_product(float2 U2, float2 K2, float twoD) {

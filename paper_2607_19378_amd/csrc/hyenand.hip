@@ -501,18 +501,43 @@ hipError_t launch_plan(const FftConvArgs& a, Plan p, size_t per, hipStream_t s) 
   }
 }
 
+// modal: the kernel is generated from these modal-filter parameters instead
+// of read (k is NULL; one filter per channel).
 hyenand_status forward(const void* x1, const void* x2, const void* v, const void* k, const void* D, void* y,
                        int ndim, const int64_t* dims, int pad_mode, int dtype, void* workspace,
-                       size_t workspace_bytes, void* stream, bool shared_k) {
+                       size_t workspace_bytes, void* stream, bool shared_k, const ModalIn* modal = nullptr) {
   g_last_error.clear();
   FftConvArgs a;
   hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
   if (st != HYENAND_OK) return st;
   a.kC = shared_k ? (int)a.C : 0;
-  if (!x1 || !x2 || !v || !k || !D || !y)
+  if (!x1 || !x2 || !v || (!k && !modal) || !D || !y)
     return fail(HYENAND_ERR_INVALID_ARGUMENT, "a tensor pointer is NULL");
+  if (modal) {
+    const float* mp[4] = {modal->a, modal->th, modal->re, modal->im};
+    const char* mn[4] = {"log_mag", "angle", "res_re", "res_im"};
+    if (modal->M < 1 || modal->M > kMaxFusedModalOrder)
+      return fail(HYENAND_ERR_UNSUPPORTED, "order must be 1..%d for the fused modal filter (got %d)",
+                  kMaxFusedModalOrder, modal->M);
+    const size_t pb = (size_t)a.C * (size_t)modal->M * sizeof(float);
+    size_t nyb = (size_t)a.lines * (a.bf16 ? 2 : 4);
+    for (int d = 0; d < a.ndim; ++d) nyb *= (size_t)a.L[d];
+    for (int i = 0; i < 4; ++i) {
+      if (!mp[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", mn[i]);
+      if ((uintptr_t)mp[i] % 4 != 0) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not 4-byte aligned", mn[i]);
+      if (overlaps(y, nyb, mp[i], pb)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", mn[i]);
+      if (workspace && overlaps(workspace, workspace_bytes, mp[i], pb))
+        return fail(HYENAND_ERR_INVALID_ARGUMENT, "workspace overlaps %s", mn[i]);
+    }
+    if (a.centered || a.rl || a.periodic || choose_plan(a) != PLAN_FOURSTEP)
+      return fail(HYENAND_ERR_UNSUPPORTED,
+                  "the fused modal filter runs on the four-step plan only (1D lines, transform of 2^15 .. 2^22 "
+                  "points, linear or circular)");
+    a.modal = *modal;
+    a.kC = (int)a.C;
+  }
   {
-    const void* tens[5] = {x1, x2, v, k, y};
+    const void* tens[5] = {x1, x2, v, modal ? x1 : k, y};
     const char* tn[5] = {"x1", "x2", "v", "k", "y"};
     for (int i = 0; i < 5; ++i)
       if ((uintptr_t)tens[i] % 16 != 0)
@@ -530,7 +555,7 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   for (int d = 0; d < a.ndim; ++d) kpts *= (size_t)(a.centered ? 2 * a.L[d] - 1 : a.L[d]);
   const size_t kb = (size_t)(shared_k ? a.C : a.lines) * kpts * es;  // [C, K...] or [B, C, K...]
   const void* ins[4] = {x1, x2, v, k};
-  const size_t in_bytes[4] = {nb, nb, nb, kb};
+  const size_t in_bytes[4] = {nb, nb, nb, modal ? (size_t)0 : kb};
   const char* names[4] = {"x1", "x2", "v", "k"};
   for (int i = 0; i < 4; ++i)
     if (overlaps(y, nb, ins[i], in_bytes[i])) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", names[i]);
@@ -654,6 +679,16 @@ hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const vo
                                         const void* D, void* y, int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
                                         hyenand_dtype dtype, void* workspace, size_t workspace_bytes, void* stream) {
   return forward(x1, x2, v, k, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, true);
+}
+
+hyenand_status hyenand_fftconv_modal(const void* x1, const void* x2, const void* v, const float* log_mag,
+                                     const float* angle, const float* res_re, const float* res_im, int order,
+                                     const void* D, void* y, int ndim, const int64_t* dims,
+                                     hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  const ModalIn md{log_mag, angle, res_re, res_im, order};
+  return forward(x1, x2, v, nullptr, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, true,
+                 &md);
 }
 
 hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,

@@ -9,6 +9,15 @@
 
 namespace hyenand {
 
+// A modal filter generated inside the transform kernels instead of read:
+// k[c, t] = Re sum_{m < M} (re + i im)[c, m] exp((a + i th)[c, m] t), the
+// parameters [C, M] fp32 (hyenand_fftconv_modal).  M = 0: k is read.
+struct ModalIn {
+  const float *a, *th, *re, *im;
+  int M;
+};
+constexpr int kMaxFusedModalOrder = 32;
+
 // One validated call, after unit axes have been squeezed out.
 struct FftConvArgs {
   const void *x1, *x2, *v, *k, *D;
@@ -28,6 +37,7 @@ struct FftConvArgs {
   size_t ws_bytes;
   bool act;       // HyenaND operator: x1, v, x2 are q, kin, vin (see Gates)
   ActIn act_in;
+  ModalIn modal;  // modal.M > 0: k generated per channel (four-step plan only)
 };
 
 // single pass (the padded problem of one line fits in LDS)

@@ -34,12 +34,6 @@ namespace {
 constexpr int kModalWaves = 4;
 constexpr int kModalT = 32;  // points per lane (advances of lambda^64)
 
-__device__ __forceinline__ void polar(double mag_log, double phase, float& c, float& s, float& m) {
-  const double two_pi = 6.283185307179586;
-  const float r = (float)(phase - two_pi * rint(phase * (1.0 / two_pi)));  // in [-pi, pi]
-  __sincosf(r, &s, &c);
-  m = __expf((float)mag_log);
-}
 
 template <typename TS>
 __global__ void __launch_bounds__(64 * kModalWaves)

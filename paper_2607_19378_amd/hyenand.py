@@ -21,7 +21,7 @@ OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_WORKSPACE_TOO_SMALL, ERR_HIP = ra
 PAD_LINEAR, PAD_CIRCULAR, PAD_CENTERED = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
-EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_noalloc", "hyenand_fftconv_workspace_size",
+EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_noalloc", "hyenand_fftconv_modal", "hyenand_fftconv_workspace_size",
             "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
@@ -55,6 +55,9 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
                                                   ctypes.c_int, vp]
             L.hyenand_fftconv_noalloc.restype = ctypes.c_int
+            L.hyenand_fftconv_modal.argtypes = [vp] * 7 + [ctypes.c_int, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
+                                                           ctypes.c_int, vp, ctypes.c_size_t, vp]
+            L.hyenand_fftconv_modal.restype = ctypes.c_int
             for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min"):
                 f = getattr(L, name)
                 f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
@@ -219,6 +222,56 @@ def fftconv_into(y, x1, x2, v, k, D, pad_mode: str = "linear", workspace=None,
     """y <- x2 * (k conv (x1*v) + D*(x1*v)); all tensors already allocated on
     the GPU.  shared_k: k is [C, L...], one kernel per channel for every sample."""
     Prepared(y, x1, x2, v, k, D, pad_mode, workspace, stream, shared_k)()
+
+
+class PreparedModalConv:
+    """One hyenand_fftconv_modal call with its arguments checked and
+    marshalled once (see Prepared): y from x1, x2, v, D and the [C, M] modal
+    filter parameters, the filter generated inside the transform kernels."""
+
+    def __init__(self, y, x1, x2, v, log_mag, angle, res_re, res_im, D, pad_mode: str = "linear", workspace=None,
+                 stream=None):
+        import torch
+        shape = tuple(x1.shape)
+        for t in (x1, x2, v, y):
+            if not t.is_cuda or tuple(t.shape) != shape or t.dtype != x1.dtype or not t.is_contiguous():
+                raise ValueError("x1, x2, v, y must be contiguous GPU tensors of one shape and dtype")
+        C, M = (int(n) for n in log_mag.shape)
+        if C != shape[1]:
+            raise ValueError("the modal parameters must be [C, M]")
+        for t in (log_mag, angle, res_re, res_im):
+            if not t.is_cuda or t.dtype != torch.float32 or tuple(t.shape) != (C, M) or not t.is_contiguous():
+                raise ValueError("log_mag, angle, res_re, res_im must be contiguous fp32 [C, M] GPU tensors")
+        if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (C,) or not D.is_contiguous():
+            raise ValueError("D must be a contiguous [C] GPU tensor of the same dtype")
+        if workspace is None:
+            nbytes = workspace_size(shape, pad_mode, x1.dtype)
+            workspace = torch.empty(max(1, nbytes), dtype=torch.uint8, device=x1.device)
+            _keep_for_stream(stream, workspace)
+        if stream is None:
+            stream = torch.cuda.current_stream(x1.device)
+        nd, dims = _dims(shape)
+        self._fn = lib().hyenand_fftconv_modal
+        self._args = (_ptr(x1), _ptr(x2), _ptr(v), _ptr(log_mag), _ptr(angle), _ptr(res_re), _ptr(res_im), M,
+                      _ptr(D), _ptr(y), nd, dims, _mode(pad_mode), _dtype_code(x1.dtype), _ptr(workspace),
+                      workspace.numel() * workspace.element_size(), ctypes.c_void_p(stream.cuda_stream))
+        self._keep = (y, x1, x2, v, log_mag, angle, res_re, res_im, D, workspace, stream)
+
+    def __call__(self) -> None:
+        status = self._fn(*self._args)
+        if status != OK:
+            _check(status)
+
+
+def fftconv_modal(x1, x2, v, log_mag, angle, res_re, res_im, D, pad_mode: str = "linear", workspace=None,
+                  stream=None):
+    """y = x2 * (k conv (x1*v) + D*(x1*v)) with k[c] the order-M modal filter
+    of channel c (generated inside the transform kernels); torch-allocated y."""
+    import torch
+    y = torch.empty_like(x1)
+    PreparedModalConv(y, x1, x2, v, log_mag, angle, res_re, res_im, D, pad_mode, workspace, stream)()
+    _keep_for_stream(stream, y)
+    return y
 
 
 NOALLOC_SCRATCH_BYTES = 128 << 20

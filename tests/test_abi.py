@@ -377,3 +377,23 @@ def test_noalloc_rejects_beyond_its_scratch(L):
     assert H.workspace_min((1, 1, 1 << 20), "linear", "bf16") <= H.NOALLOC_SCRATCH_BYTES
     dims = (ctypes.c_int64 * 3)(1, 0, 64)
     assert L.hyenand_fftconv_noalloc(*p, 1, dims, 0, 0, None) == H.ERR_INVALID_ARGUMENT
+
+
+def test_fused_modal_validation(L):
+    """hyenand_fftconv_modal refuses, on the host, shapes beyond the
+    four-step plan, orders above 32 and missing parameters."""
+    p = [ctypes.c_void_p(FAKE + i * (1 << 36)) for i in range(10)]
+
+    def call_modal(shape, mode=0, order=16, params=None):
+        dims = (ctypes.c_int64 * len(shape))(*shape)
+        pr = params if params is not None else p[3:7]
+        return L.hyenand_fftconv_modal(p[0], p[1], p[2], *pr, order, p[7], p[8], len(shape) - 2, dims, mode, 0,
+                                       p[9], 1 << 30, None)
+    assert call_modal((1, 4, 4096)) == H.ERR_UNSUPPORTED      # single-pass shape
+    assert b"four-step" in L.hyenand_last_error()
+    assert call_modal((1, 4, 64, 64)) == H.ERR_UNSUPPORTED    # 2D
+    assert call_modal((1, 4, 1 << 20), mode=2) == H.ERR_UNSUPPORTED  # centred
+    assert call_modal((1, 4, 1 << 20), order=33) == H.ERR_UNSUPPORTED
+    assert call_modal((1, 4, 1 << 20), order=0) == H.ERR_UNSUPPORTED
+    assert call_modal((1, 4, 1 << 20), params=[p[3], None, p[5], p[6]]) == H.ERR_INVALID_ARGUMENT
+    assert b"angle" in L.hyenand_last_error()

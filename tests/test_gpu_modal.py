@@ -111,3 +111,56 @@ def test_output_off_the_vector_boundary(dtype):
     log(f"[modal] unaligned k {dtype}")
     assert float(buf[0]) == 7.0
     assert torch.equal(k, aligned)
+
+
+def _fused(B, C, M, L, mode, dtype, seed):
+    """hyenand_fftconv_modal on a seeded case, and the oracle's modal filter
+    (fp64, from the same fp32 parameters) through the oracle's convolution."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    inp = W.random_case(B, C, (L,), mode, dtype, seed=seed)
+    p = W.modal_params(seed + 1, C, M, L)
+    d = [torch.from_numpy(p[n]).cuda() for n in ("log_mag", "angle", "res_re", "res_im")]
+    dev = [to_device(a, dtype) for a in (inp.x1, inp.x2, inp.v, inp.D)]
+    y = H.fftconv_modal(dev[0], dev[1], dev[2], *d, dev[3], pad_mode=mode)
+    torch.cuda.synchronize()
+    got = from_device(y)
+    kf = oracle.modal_filter(*[p[n].astype(np.float64) for n in ("log_mag", "angle", "res_re", "res_im")], L)
+    x1, x2, v, _, D = inp.as_f64()
+    ref = oracle.conv_fft(x1, x2, v, np.broadcast_to(kf[None], (B, C, L)).copy(), D, mode)
+    return got, ref, inp, p, dev, d
+
+
+@pytest.mark.parametrize("B,C,M,L,mode,dtype", [
+    (1, 3, 4, 16384, "linear", "f32"), (2, 4, 16, 32768, "linear", "bf16"), (1, 3, 8, 65536, "circular", "f32"),
+    (2, 2, 32, 1 << 17, "linear", "f32"), (1, 2, 1, 1 << 15, "circular", "bf16"), (1, 3, 16, 1 << 21, "linear", "f32"),
+    (1, 2, 13, 1 << 22, "circular", "f32")])
+def test_fused_modal_conv(B, C, M, L, mode, dtype):
+    """The modal filter generated inside the four-step transform's kernel
+    column pass: every output element against the oracle."""
+    from paper_2607_19378_amd import hyenand as H
+    assert H.plan_name((B, C, L), mode, dtype) == "fourstep1d"
+    got, ref, _, _, _, _ = _fused(B, C, M, L, mode, dtype, 70 + M + L % 97)
+    err = rel_l2(got, ref)
+    log(f"[fused modal] B={B} C={C} M={M} L={L} {mode} {dtype}: rel_l2={err:.3e}")
+    assert np.all(np.isfinite(got)) and err <= TOL[dtype]
+
+
+def test_fused_modal_matches_two_kernels():
+    """The fused call against hyenand_modal_filter followed by the
+    one-kernel-per-channel convolution on the same fp32 filter: the two
+    agree to fp32 rounding; a shape beyond the four-step plan is refused."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    got, ref, inp, p, dev, d = _fused(2, 8, 16, 1 << 20, "linear", "f32", 5)
+    k = H.modal_filter(*d, 1 << 20)
+    y2 = H.fftconv(dev[0], dev[1], dev[2], k, dev[3], pad_mode="linear", shared_k=True)
+    torch.cuda.synchronize()
+    two = from_device(y2)
+    log(f"[fused modal] 2 x 8 x 2^20: fused {rel_l2(got, ref):.3e}, two kernels {rel_l2(two, ref):.3e}, "
+        f"between {rel_l2(got, two):.3e}")
+    assert rel_l2(got, ref) <= TOL["f32"] and rel_l2(got, two) <= TOL["f32"]
+    short = [t[..., :4096].contiguous() for t in dev[:3]]
+    with pytest.raises(H.HyenandError) as e:
+        H.fftconv_modal(short[0], short[1], short[2], *d, dev[3], pad_mode="linear")
+    assert e.value.status == H.ERR_UNSUPPORTED
