@@ -557,6 +557,39 @@ def settle_clocks(step, n: int) -> None:
     torch.cuda.synchronize()
 
 
+def bench_line_sweep(args):
+    """Latency floor of a single-pass workload: the same call on 1 .. 4096
+    (b, c) lines of the workload's shape (one workgroup per line), mean call
+    time over args.steps calls under HIP events; prints one JSON line.  With
+    fewer lines than CUs the call takes one line's latency."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    w0 = W.WORKLOADS[args.workload or "conv1d_4k"]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for n in (1, 8, 64, 256, 512, 1024, 4096):
+        inp = W.random_case(1, n, w0.grid, w0.pad_mode, w0.dtype, seed=w0.seed)
+        t = [to_device(a, w0.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+        y = torch.empty_like(t[0])
+        call = H.Prepared(y, *t, w0.pad_mode, None, stream)
+        for _ in range(200):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        rows.append({"lines": n, "call_us": round(us, 2), "gelems": round(n * int(np.prod(w0.grid)) / us / 1e3, 2)})
+        progress(f"line sweep {w0.name}: {n} lines {us:.2f} us")
+    print(json.dumps({"metric": "call time against (b, c) lines", "workload": w0.name, "grid": list(w0.grid),
+                      "plan": H.plan_name((1, 1) + tuple(w0.grid), w0.pad_mode, w0.dtype), "steps": args.steps,
+                      "rows": rows, "kernel_source_hash": kernel_source_hash()}))
+
+
 def cpu_model() -> str:
     """The host CPU's model name (from /proc/cpuinfo)."""
     try:
@@ -779,6 +812,8 @@ def main():
                     help="time kernel synthesis (FiLM-modulated SIREN + window) alone and followed by the conv")
     ap.add_argument("--modal", action="store_true",
                     help="time modal filter generation (order 16, one filter per channel) alone and with the conv")
+    ap.add_argument("--line-sweep", action="store_true",
+                    help="time the workload's single-pass call on 1 .. 4096 lines (latency floor)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the timed steps, run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -789,6 +824,9 @@ def main():
 
     import torch
 
+    if args.line_sweep:
+        bench_line_sweep(args)
+        return
     if args.backward or args.operator or args.synth or args.modal:
         w = W.WORKLOADS[args.workload or DEFAULT_WORKLOAD]
         inp = W.generate(w)

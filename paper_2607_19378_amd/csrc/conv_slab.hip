@@ -59,10 +59,12 @@ constexpr bool slab_fits() {
 // the packed DC + i Nyquist bin pair of a row from its two bins
 __device__ __forceinline__ float2 pack_dc_nyq(float2 dc, float2 nyq) { return make_float2(dc.x - nyq.y, dc.y + nyq.x); }
 
-template <int P, bool CIRC, typename TS>
+// ACT: the HyenaND operator's gates (x1, v, x2 hold q, kin, vin; see Gates)
+template <int P, bool CIRC, typename TS, bool ACT>
 __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
     mp_slab_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
-                float2* __restrict__ ws, int64_t line0, int L0, int HS, int64_t half, int64_t per_line, int kC) {
+                float2* __restrict__ ws, int64_t line0, int L0, int HS, int64_t half, int64_t per_line, int kC,
+                ActIn ain, int C) {
   using Cf = SlabCfg<P, CIRC>;
   constexpr int ML = Cf::ML, HP = Cf::HP, L1 = Cf::L1, LL = Cf::LL, MNZ = Cf::MNZ, NT = Cf::NT;
   __shared__ float2 pl[L1 * HP];
@@ -81,13 +83,13 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
   {
     const TS* a = sig ? k + k_line(gline, kC) * pts + pbase : x1 + gline * pts + pbase;
     const TS* b = v + gline * pts + pbase;
+    const Gates<ACT> G = line_gates<ACT, TS>(ain, gline, C);
     batched_copy<L1 * LL / 2, NT, 4>(
         tid,
         [&](int i) {
           const float2 p = ld2(a + 2 * i);
           if (sig) return p;
-          const float2 q = ld2(b + 2 * i);
-          return make_float2(p.x * q.x, p.y * q.y);
+          return G.u2(p, ld2(b + 2 * i), pbase + 2 * i);
         },
         [&](int i, float2 z) {
           const int r = i / (LL / 2), m = i - r * (LL / 2);
@@ -205,7 +207,7 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
   }
 }
 
-template <int P, bool CIRC, typename TS>
+template <int P, bool CIRC, typename TS, bool ACT>
 __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
     mp_slab_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0,
                 int L0, int HS, int64_t per_line) {
@@ -305,7 +307,7 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
   // 3. outer gate and store, coalesced along rows
   const int64_t gbase = (gline * L0 + n0) * (int64_t)L1 * LL;
   batched_copy<L1 * LL / 2, NT, 4>(
-      tid, [&](int i) { return ld2(x2 + gbase + 2 * i); },
+      tid, [&](int i) { return Gates<ACT>{}.g2(ld2(x2 + gbase + 2 * i)); },
       [&](int i, float2 g) {
         const int r = i / (LL / 2), m = i - r * (LL / 2);
         const float2 q = pl[r * HP + m];
@@ -322,20 +324,26 @@ hipError_t slab_launch(const FftConvArgs& a, const MpGeom& g, float2* ws, int64_
     constexpr int NT = SlabCfg<P, CIRC>::NT;
     if (!inverse) {
       const dim3 grid((unsigned)((int64_t)nl * g.L0 * 2));
-      if (a.bf16)
-        hipLaunchKernelGGL((mp_slab_fwd<P, CIRC, uint16_t>), grid, dim3(NT), 0, s, (const uint16_t*)a.x1,
-                           (const uint16_t*)a.v, (const uint16_t*)a.k, ws, line0, g.L0, g.HS, g.half, per, a.kC);
-      else
-        hipLaunchKernelGGL((mp_slab_fwd<P, CIRC, float>), grid, dim3(NT), 0, s, (const float*)a.x1,
-                           (const float*)a.v, (const float*)a.k, ws, line0, g.L0, g.HS, g.half, per, a.kC);
+#define HY_FWD(TS, ACT)                                                                                        \
+  hipLaunchKernelGGL((mp_slab_fwd<P, CIRC, TS, ACT>), grid, dim3(NT), 0, s, (const TS*)a.x1, (const TS*)a.v, \
+                     (const TS*)a.k, ws, line0, g.L0, g.HS, g.half, per, a.kC, a.act_in, (int)a.C)
+      if (a.bf16) {
+        if (a.act) HY_FWD(uint16_t, true); else HY_FWD(uint16_t, false);
+      } else {
+        if (a.act) HY_FWD(float, true); else HY_FWD(float, false);
+      }
+#undef HY_FWD
     } else {
       const dim3 grid((unsigned)((int64_t)nl * g.L0));
-      if (a.bf16)
-        hipLaunchKernelGGL((mp_slab_inv<P, CIRC, uint16_t>), grid, dim3(NT), 0, s, ws, (const uint16_t*)a.x2,
-                           (uint16_t*)a.y, line0, g.L0, g.HS, per);
-      else
-        hipLaunchKernelGGL((mp_slab_inv<P, CIRC, float>), grid, dim3(NT), 0, s, ws, (const float*)a.x2,
-                           (float*)a.y, line0, g.L0, g.HS, per);
+#define HY_INV(TS, ACT)                                                                                   \
+  hipLaunchKernelGGL((mp_slab_inv<P, CIRC, TS, ACT>), grid, dim3(NT), 0, s, ws, (const TS*)a.x2, (TS*)a.y, \
+                     line0, g.L0, g.HS, per)
+      if (a.bf16) {
+        if (a.act) HY_INV(uint16_t, true); else HY_INV(uint16_t, false);
+      } else {
+        if (a.act) HY_INV(float, true); else HY_INV(float, false);
+      }
+#undef HY_INV
     }
     return hipGetLastError();
   }
@@ -344,7 +352,7 @@ hipError_t slab_launch(const FftConvArgs& a, const MpGeom& g, float2* ws, int64_
 }  // namespace
 
 bool slab3d_supported(const FftConvArgs& a) {
-  if (a.ndim != 3 || a.centered || a.act || a.rl || a.periodic) return false;
+  if (a.ndim != 3 || a.centered || a.rl || a.periodic) return false;
   if (getenv("HYENAND_SLAB") && strcmp(getenv("HYENAND_SLAB"), "0") == 0) return false;
   const int64_t P = a.P[2];
   if (a.P[1] != P || a.L[1] != a.L[2]) return false;

@@ -62,12 +62,16 @@ def test_single_pass(grid, plan, mode, dtype):
 @pytest.mark.parametrize("mode", ["linear", "circular", "centered"])
 @pytest.mark.parametrize("grid,plan", [((32768,), "fourstep1d"), ((256, 128), "multipass2d"),
                                        ((256, 64), "multipass2d"), ((8, 16, 32), "multipass3d"),
-                                       ((32, 32, 32), "multipass3d")])
+                                       ((32, 32, 32), "slab3d")])
 def test_multi_pass(grid, plan, mode):
+    if plan == "slab3d" and mode != "linear":
+        # the slab plan takes linear 32^3 (64-point transforms); circular 32^3
+        # (32-point) and centred grids stay on the five-pass plan
+        plan = "multipass3d"
     _check("multi", 2, 6, grid, mode, "f32", 200 + sum(grid), expect_plan=plan)
 
 
-@pytest.mark.parametrize("grid", [(65536,), (64, 128), (16, 16, 32)])
+@pytest.mark.parametrize("grid", [(65536,), (64, 128), (16, 16, 32), (8, 64, 64)])
 def test_multi_pass_bf16(grid):
     _check("multi-bf16", 1, 5, grid, "linear", "bf16", 300 + sum(grid))
 
