@@ -500,6 +500,92 @@ def bench_modal(args, w, inp):
     print(json.dumps(out))
 
 
+def bench_shared_k(args, w, inp):
+    """One kernel per channel (hyenand_fftconv_shared_k, k[c] = the workload's
+    kernel of sample 0) on a single-pass 2D workload: each channel's spectrum
+    computed once and read by every image, against every image transforming
+    k itself (the same call without a workspace); prints one JSON line."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    if len(w.grid) != 2 or H.plan_name(w.shape, w.pad_mode, w.dtype) != "fused2d":
+        raise SystemExit("--shared-k takes a workload on the single-pass 2D plan")
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    x1, x2, v, D = (to_device(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.D))
+    kc = to_device(np.ascontiguousarray(inp.k[0]), w.dtype)
+    y_hat, y_img = torch.empty_like(x1), torch.empty_like(x1)
+    need = H.workspace_size(w.shape, w.pad_mode, w.dtype, shared_k=True)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    with_hat = H.Prepared(y_hat, x1, x2, v, kc, D, w.pad_mode, ws, stream, shared_k=True)
+    per_image = H.Prepared(y_img, x1, x2, v, kc, D, w.pad_mode, None, stream, shared_k=True)
+
+    def timed(fn):
+        settle_clocks(lambda i: fn(), settle_count(alg_flops(w), alg_bytes(w), args.settle_ms))
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / args.steps, (time.perf_counter() - t0) / args.steps
+
+    img_s, _ = timed(per_image)
+    hat_s, hat_wall = timed(with_hat)
+    diff = float((y_hat.float() - y_img.float()).abs().max().item())
+    # the same images repeated along the batch: B x 4 (inputs for timing only)
+    big = [t.repeat((4,) + (1,) * (t.dim() - 1)) for t in (x1, x2, v)]
+    shape4 = tuple(big[0].shape)
+    yb1, yb2 = torch.empty_like(big[0]), torch.empty_like(big[0])
+    ws4 = torch.empty(H.workspace_size(shape4, w.pad_mode, w.dtype, shared_k=True), dtype=torch.uint8, device=dev)
+    img4_s, _ = timed(H.Prepared(yb1, *big, kc, D, w.pad_mode, None, stream, shared_k=True))
+    hat4_s, _ = timed(H.Prepared(yb2, *big, kc, D, w.pad_mode, ws4, stream, shared_k=True))
+    del big, yb1, yb2, ws4
+    parity = None
+    if not args.no_parity:
+        import oracle
+        f = [W.storage_to_f64(a, w.dtype) for a in (inp.x1, inp.x2, inp.v, inp.k, inp.D)]
+        rng = np.random.default_rng(w.seed + 5)
+        worst = 0.0
+        got_all = y_hat
+        for b, c in zip(rng.integers(0, w.B, 6), rng.integers(0, w.C, 6)):
+            ref = oracle.conv_fft(f[0][b:b + 1, c:c + 1], f[1][b:b + 1, c:c + 1], f[2][b:b + 1, c:c + 1],
+                                  f[3][0:1, c:c + 1], f[4][c:c + 1], w.pad_mode)[0, 0]
+            got = got_all[b, c]
+            got = (W.bf16_bits_to_f64(got.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+                   if got.dtype == torch.bfloat16 else got.cpu().numpy().astype(np.float64))
+            worst = max(worst, float(np.linalg.norm(got - ref) / np.linalg.norm(ref)))
+        parity = worst
+    # x1, v, x2 read and y written per image, k read once per channel
+    kpts = int(np.prod(w.grid))
+    alg = (4 * w.elems + w.C * kpts) * w.storage_bytes
+    gbs = alg / hat_s / 1e9
+    out = {
+        "metric": "gated 2D FFT conv, one kernel per channel, GElem/s on 1 MI355X",
+        "value": round(w.elems / hat_wall / 1e9, 3), "unit": "GElem/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(hat_wall * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "storage_dtype": w.dtype,
+        "data": "synthetic (seeded; k[c] = the workload's kernel of sample 0)",
+        "config": {"workload": w.name, "pass": "forward, shared k", "B": w.B, "C": w.C, "grid": list(w.grid),
+                   "pad_mode": w.pad_mode, "storage": w.dtype},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "alg_bytes_per_call": alg},
+        "spectra_once_per_channel_us": round(hat_s * 1e6, 3),
+        "per_image_transform_us": round(img_s * 1e6, 3),
+        "speedup": round(img_s / hat_s, 3),
+        "batch_x4": {"B": 4 * w.B, "spectra_once_per_channel_us": round(hat4_s * 1e6, 3),
+                     "per_image_transform_us": round(img4_s * 1e6, 3), "speedup": round(img4_s / hat4_s, 3)},
+        "workspace_bytes": need,
+        "max_abs_diff_between_paths": diff,
+        "cpu_baseline": None, "parity_rel_l2_worst_sampled_line": parity,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    print(json.dumps(out))
+
+
 def copy_calibration(args, dev):
     """One plain device copy of --copy-calibration-mb MiB, whose FETCH_SIZE and
     WRITE_SIZE counters scale the library's own to HBM bytes."""
@@ -812,6 +898,9 @@ def main():
                     help="time kernel synthesis (FiLM-modulated SIREN + window) alone and followed by the conv")
     ap.add_argument("--modal", action="store_true",
                     help="time modal filter generation (order 16, one filter per channel) alone and with the conv")
+    ap.add_argument("--shared-k", action="store_true",
+                    help="one kernel per channel on a single-pass 2D workload: spectra once per channel "
+                         "against per-image transforms")
     ap.add_argument("--line-sweep", action="store_true",
                     help="time the workload's single-pass call on 1 .. 4096 lines (latency floor)")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
@@ -827,10 +916,12 @@ def main():
     if args.line_sweep:
         bench_line_sweep(args)
         return
-    if args.backward or args.operator or args.synth or args.modal:
+    if args.backward or args.operator or args.synth or args.modal or args.shared_k:
         w = W.WORKLOADS[args.workload or DEFAULT_WORKLOAD]
         inp = W.generate(w)
-        if args.backward:
+        if args.shared_k:
+            bench_shared_k(args, w, inp)
+        elif args.backward:
             bench_backward(args, w, inp)
         elif args.operator:
             bench_operator(args, w, inp)

@@ -48,7 +48,10 @@ typedef enum {
   HYENAND_ERR_INVALID_ARGUMENT = 1,  /* null pointer, bad enum, dims <= 0, y aliasing an input */
   HYENAND_ERR_UNSUPPORTED = 2,       /* a shape or size beyond the implemented plans */
   HYENAND_ERR_WORKSPACE_TOO_SMALL = 3,
-  HYENAND_ERR_HIP = 4,               /* a HIP launch failed; see hyenand_last_error() */
+  HYENAND_ERR_HIP = 4,               /* a HIP launch failed; see hyenand_last_error().  A call
+                                        clears the calling thread's pending HIP error (one that
+                                        earlier work left to be read by hipGetLastError) before
+                                        it launches, so only its own launches are reported. */
   HYENAND_STATUS_MAX_ENUM = 0x7fffffff
 } hyenand_status;
 
@@ -131,13 +134,27 @@ hyenand_status hyenand_fftconv(const void* x1, const void* x2, const void* v, co
  * shared by every sample: the Hyena operator's global kernel K of one row per
  * channel (Eq. (hyena), section "Background: Hyena and CKConv"), before
  * HyenaND makes the kernel input-dependent.  k is [C, L1, ..., LN] (centered:
- * [C, 2 L1 - 1, ...]) and sample b, channel c uses k[c].  Everything else, including the workspace sizes
- * below, is as for hyenand_fftconv.
+ * [C, 2 L1 - 1, ...]) and sample b, channel c uses k[c].  Everything else is
+ * as for hyenand_fftconv; its workspace sizes are enough.
+ * Since the kernel does not depend on the sample, its spectrum is the same
+ * for all B samples: on the single-pass 2D plan (power-of-two transform
+ * grids, linear or circular, B >= 2) a workspace of at least
+ * hyenand_fftconv_shared_k_workspace_size() bytes lets the call transform
+ * each channel's kernel once (C x P0 x P1/2 complex fp32 spectra at the
+ * start of the workspace) and every image read that spectrum, instead of
+ * transforming it once per image.  With a smaller or NULL workspace it
+ * does the latter.  The two give the same results up to rounding order.
  */
 hyenand_status hyenand_fftconv_shared_k(const void* x1, const void* x2, const void* v, const void* k,
                                         const void* D, void* y, int ndim, const int64_t* dims,
                                         hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* workspace, size_t workspace_bytes,
                                         void* stream);
+
+/* Recommended workspace size (bytes) for hyenand_fftconv_shared_k: that of
+ * hyenand_fftconv, or the per-channel spectra where the call can use them
+ * (see above).  Pure host function. */
+hyenand_status hyenand_fftconv_shared_k_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                                       hyenand_dtype dtype, size_t* bytes_out);
 
 /*
  * hyenand_fftconv_noalloc -- hyenand_fftconv for callers that cannot

@@ -253,11 +253,21 @@ struct Fused2D {
   static_assert(2 * L0 >= P0, "column scratch");
 };
 
-template <int P0, int P1, bool CIRC, typename TS, bool ACT = false>
+// KH selects how the kernel's spectrum is obtained when one kernel serves a
+// channel in every sample (kC = C):
+//   0: each image transforms its own k (every call shape);
+//   1: one workgroup per channel transforms k[c] and writes its column-pass
+//      spectrum, khat[c][n][g] (n < P0 along axis 0, g < P1/2 the column
+//      group, group 0 the DC + i Nyquist column), and stops there;
+//   2: each image reads that spectrum instead of transforming k.
+// Modes 1 and 2 together run the same arithmetic on k as mode 0, once per
+// channel instead of once per image.
+template <int P0, int P1, bool CIRC, typename TS, bool ACT = false, int KH = 0>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     conv2d_fused(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
                  const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int C, int kC,
-                 ActIn ain) {
+                 ActIn ain, float2* __restrict__ khat) {
+  static_assert(KH >= 0 && KH <= 2 && !(ACT && KH), "kernel spectrum mode");
   using F = Fused2D<P0, P1, CIRC, TS>;
   constexpr int L0 = F::L0, L1 = F::L1, M1 = F::M1, MNZ = F::MNZ, RP = F::RP, NT = F::NT;
   // U half spectrum rows [0, L0), then K's: column c of both is one stride-RP
@@ -266,7 +276,16 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   __shared__ float2 NQ[2][P0];  // column group 0's U and K spectra (DC + i Nyquist)
   float2* const Uh = UK;
   float2* const Kh = UK + L0 * RP;
-  const int img = blockIdx.x;
+  int img = blockIdx.x;
+  if constexpr (KH == 2) {
+    // Workgroup j runs on XCD j mod 8.  Renumber so that the B images of a
+    // channel take consecutive slots j, j + 8, ... of one XCD: its spectrum
+    // then comes into that XCD's L2 once for all of them.
+    if ((C & 7) == 0) {
+      const int nb = (int)gridDim.x / C, x = img & 7, q = img >> 3;
+      img = (q % nb) * C + (q / nb) * 8 + x;
+    }
+  }
   const int c = img % C;
   const size_t base = (size_t)img * L0 * L1;
   const size_t kbase = (size_t)k_line(img, kC) * L0 * L1;
@@ -289,28 +308,34 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   constexpr bool kSplit = JS <= 4 && TRS * L0 == NT;
   if constexpr (kSplit) {
     float2 kr[JS], ar[JS], br[JS];
+    if constexpr (KH != 2) {
 #pragma unroll
-    for (int j = 0; j < JS; ++j) {
-      const int i = tid + NT * j;
-      if (NPS % NT == 0 || i < NPS) kr[j] = ld2(k + kbase + 2 * i);
-    }
-#pragma unroll
-    for (int j = 0; j < JS; ++j) {
-      const int i = tid + NT * j;
-      if (NPS % NT == 0 || i < NPS) {
-        ar[j] = ld2(x1 + base + 2 * i);
-        br[j] = ld2(v + base + 2 * i);
+      for (int j = 0; j < JS; ++j) {
+        const int i = tid + NT * j;
+        if (NPS % NT == 0 || i < NPS) kr[j] = ld2(k + kbase + 2 * i);
       }
     }
+    if constexpr (KH != 1) {
 #pragma unroll
-    for (int j = 0; j < JS; ++j) {
-      const int i = tid + NT * j;
-      if (NPS % NT == 0 || i < NPS) {
-        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-        Kh[r * RP + m] = make_float2(kr[j].x * scale, kr[j].y * scale);
+      for (int j = 0; j < JS; ++j) {
+        const int i = tid + NT * j;
+        if (NPS % NT == 0 || i < NPS) {
+          ar[j] = ld2(x1 + base + 2 * i);
+          br[j] = ld2(v + base + 2 * i);
+        }
       }
     }
-    __syncthreads();
+    if constexpr (KH != 2) {
+#pragma unroll
+      for (int j = 0; j < JS; ++j) {
+        const int i = tid + NT * j;
+        if (NPS % NT == 0 || i < NPS) {
+          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+          Kh[r * RP + m] = make_float2(kr[j].x * scale, kr[j].y * scale);
+        }
+      }
+      __syncthreads();
+    }
     using Map = LaneMap<TRS, NT>;
     static_assert(Map::kLines == L0, "one round per signal");
     const int l = Map::line(tid), t = Map::t(tid);
@@ -325,39 +350,61 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
 #pragma unroll
       for (int e = 0; e < ES; ++e) rowp[t + TRS * e] = w[e];
     };
-    rows(Kh + l * RP);
+    if constexpr (KH != 2) rows(Kh + l * RP);
+    if constexpr (KH != 1) {
 #pragma unroll
-    for (int j = 0; j < JS; ++j) {
-      const int i = tid + NT * j;
-      if (NPS % NT == 0 || i < NPS) {
-        const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-        Uh[r * RP + m] = G.u2(ar[j], br[j], 2 * i);
+      for (int j = 0; j < JS; ++j) {
+        const int i = tid + NT * j;
+        if (NPS % NT == 0 || i < NPS) {
+          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+          Uh[r * RP + m] = G.u2(ar[j], br[j], 2 * i);
+        }
       }
+      __syncthreads();
+      rows(Uh + l * RP);
+    }
+  } else {
+    if constexpr (KH == 0) {
+      batched_copy<L0 * L1 / 2, NT, 8>(
+          tid,
+          [&](int i) {
+            const float2 u = G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i);
+            const float2 kk = ld2(k + kbase + 2 * i);
+            return make_float4(u.x, u.y, kk.x * scale, kk.y * scale);
+          },
+          [&](int i, float4 z) {
+            const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+            Uh[r * RP + m] = make_float2(z.x, z.y);
+            Kh[r * RP + m] = make_float2(z.z, z.w);
+          });
+    } else {
+      batched_copy<L0 * L1 / 2, NT, 8>(
+          tid,
+          [&](int i) {
+            if constexpr (KH == 1) {
+              const float2 kk = ld2(k + kbase + 2 * i);
+              return make_float2(kk.x * scale, kk.y * scale);
+            } else {
+              return G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i);
+            }
+          },
+          [&](int i, float2 z) {
+            const int r = i / (L1 / 2), m = i - r * (L1 / 2);
+            (KH == 1 ? Kh : Uh)[r * RP + m] = z;
+          });
     }
     __syncthreads();
-    rows(Uh + l * RP);
-  } else {
-    batched_copy<L0 * L1 / 2, NT, 8>(
-        tid,
-        [&](int i) {
-          const float2 u = G.u2(ld2(x1 + base + 2 * i), ld2(v + base + 2 * i), 2 * i);
-          const float2 kk = ld2(k + kbase + 2 * i);
-          return make_float4(u.x, u.y, kk.x * scale, kk.y * scale);
-        },
-        [&](int i, float4 z) {
-          const int r = i / (L1 / 2), m = i - r * (L1 / 2);
-          Uh[r * RP + m] = make_float2(z.x, z.y);
-          Kh[r * RP + m] = make_float2(z.z, z.w);
-        });
-    __syncthreads();
     {
+      // rows of U then K (KH = 0), or of the one signal this mode transforms
+      constexpr int NL = KH == 0 ? 2 * L0 : L0;
+      float2* const R0 = KH == 1 ? Kh : Uh;
       constexpr int E = F::ER, T = F::TR, LR = F::LR;
-      for (int l0 = 0; l0 < 2 * L0; l0 += LR) {
+      for (int l0 = 0; l0 < NL; l0 += LR) {
         using Map = LaneMap<T, NT>;
         static_assert(Map::kLines == LR, "lines per round");
         const int l = l0 + Map::line(tid), t = Map::t(tid);
-        const bool act = (2 * L0) % LR == 0 || l < 2 * L0;  // all lanes busy when rounds are full
-        float2* row = (l < L0) ? Uh + l * RP : Kh + (l - L0) * RP;
+        const bool act = NL % LR == 0 || l < NL;  // all lanes busy when rounds are full
+        float2* row = R0 + (act ? l : 0) * RP;
         float2 w[E];
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -380,11 +427,12 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     // keeps both, as DC + i Nyquist (column group 0 below).  Rows of U and K
     // are contiguous (Kh = Uh + L0 RP); with 2 L0 a multiple of 64 every
     // wavefront shares one g, so its twiddle is a scalar.
-    constexpr int NR = 2 * L0, NG = imax(1, M1 / 2);
+    constexpr int NR = KH == 0 ? 2 * L0 : L0, NG = imax(1, M1 / 2);
+    float2* const R0 = KH == 1 ? Kh : Uh;
     for (int it = tid; it < NR * NG; it += NT) {
       const int l = it % NR;
       const int g = NR % 64 == 0 ? __builtin_amdgcn_readfirstlane(it / NR) : it / NR;
-      float2* row = Uh + l * RP;
+      float2* row = R0 + l * RP;
       float2 xa, xb;
       if (g == 0) {
         r2c_pair(row[0], row[0], make_float2(1.f, 0.f), xa, xb);
@@ -408,7 +456,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
   //    complex column DC + i Nyquist of the two real columns 0 and M1.
   {
     constexpr int E = F::EC, T = F::TC, CR = F::CR;
-    const float twoD = 2.f * scale * ld1(Dp + c);
+    const float twoD = KH == 1 ? 0.f : 2.f * scale * ld1(Dp + c);
+    const float2* const kh = khat + (size_t)c * P0 * M1;  // modes 1 and 2
     for (int c0 = 0; c0 < M1; c0 += CR) {
       using Map = LaneMap<T, NT>;
       static_assert(Map::kLines == CR, "groups per round");
@@ -421,12 +470,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       for (int e = 0; e < E; ++e) {
         const int n = t + T * e;
         const bool nz = act && (CIRC || n < L0);
-        wu[e] = nz ? Uh[n * RP + col] : czero();
-        wk[e] = nz ? Kh[n * RP + col] : czero();
+        if constexpr (KH != 1) wu[e] = nz ? Uh[n * RP + col] : czero();
+        if constexpr (KH == 2) wk[e] = act ? kh[n * M1 + col] : czero();
+        else wk[e] = nz ? Kh[n * RP + col] : czero();
       }
       const ScrS<RP> su{UK + col};
-      BlockFFT<P0, E, false>::run(wu, t, su, act);
-      BlockFFT<P0, E, false>::run(wk, t, su, act);
+      if constexpr (KH != 1) BlockFFT<P0, E, false>::run(wu, t, su, act);
+      if constexpr (KH != 2) BlockFFT<P0, E, false>::run(wk, t, su, act);
+      if constexpr (KH == 1) {
+        if (act) {
+#pragma unroll
+          for (int e = 0; e < E; ++e) khat[(size_t)c * P0 * M1 + (t + T * e) * M1 + col] = wk[e];
+        }
+        continue;
+      }
       // Group 0 holds A + i B with A, B the spectra of the real columns 0
       // and M1: A = (Z[f] + conj Z[-f]) / 2, B = -i (Z[f] - conj Z[-f]) / 2
       // need the mirror bin, so its spectra go through LDS (slots of their
@@ -475,6 +532,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       }
     }
   }
+  if constexpr (KH == 1) return;
   __syncthreads();
 
   // outer gate values of the row pairs this lane stores, fetched before the
@@ -807,14 +865,23 @@ static hipError_t launch_2d_fused_kc_t(const FftConvArgs& a, hipStream_t s) {
 
 template <int P0, int P1, bool CIRC, typename TS>
 static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
-  if (a.act)
+  if (a.act) {
     hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, true>), dim3((unsigned)a.lines), dim3(512), 0, s,
                        (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, a.act_in);
-  else
+                       (int)a.C, a.kC, a.act_in, nullptr);
+  } else if (a.khat) {
+    // each channel's spectrum once, then the images read it
+    hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false, 1>), dim3((unsigned)a.C), dim3(512), 0, s,
+                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                       (int)a.C, a.kC, a.act_in, a.khat);
+    hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false, 2>), dim3((unsigned)a.lines), dim3(512), 0, s,
+                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                       (int)a.C, a.kC, a.act_in, a.khat);
+  } else {
     hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false>), dim3((unsigned)a.lines), dim3(512), 0, s,
                        (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, a.act_in);
+                       (int)a.C, a.kC, a.act_in, nullptr);
+  }
   return hipGetLastError();
 }
 
@@ -837,6 +904,13 @@ bool fused2d_supported(int64_t P0, int64_t P1) {
   HY_FUSED2D_SIZES(HY_CASE)
 #undef HY_CASE
   return false;
+}
+
+size_t fused2d_khat_bytes(const FftConvArgs& a) {
+  if (a.ndim != 2 || a.centered || a.rl || a.act || a.kC != a.C || a.lines / a.C < 2 ||
+      !fused2d_supported(a.P[0], a.P[1]))
+    return 0;
+  return ((size_t)a.C * (size_t)a.P[0] * (size_t)(a.P[1] / 2) * sizeof(float2) + 255) / 256 * 256;
 }
 
 hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s) {

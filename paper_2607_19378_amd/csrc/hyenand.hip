@@ -6,6 +6,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <cmath>
 #include <string>
 
@@ -454,6 +455,20 @@ hyenand_status hyenand_fftconv_workspace_size(int ndim, const int64_t* dims, hye
   return HYENAND_OK;
 }
 
+hyenand_status hyenand_fftconv_shared_k_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                                       hyenand_dtype dtype, size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  a.kC = (int)a.C;
+  const Plan p = choose_plan(a);
+  if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
+  const size_t khb = p == PLAN_FUSED2D ? fused2d_khat_bytes(a) : 0;
+  *bytes_out = std::max(recommended_ws(a, p), khb);
+  return HYENAND_OK;
+}
+
 hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                              size_t* bytes_out) {
   if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
@@ -563,7 +578,11 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   const Plan p = choose_plan(a);
   if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
   const size_t per = bytes_per_line(a, p);
-  if (per > 0) {
+  // one kernel per channel on the fused 2D plan: with room in the workspace,
+  // each channel's spectrum is computed once and read by all its images
+  const size_t khb = (shared_k && !modal && p == PLAN_FUSED2D) ? fused2d_khat_bytes(a) : 0;
+  const bool use_khat = khb > 0 && workspace && workspace_bytes >= khb;
+  if (per > 0 || use_khat) {
     if (!workspace || workspace_bytes < per)
       return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "plan %s needs at least %zu workspace bytes, got %zu",
                   plan_name(p, a), per, workspace ? workspace_bytes : (size_t)0);
@@ -575,6 +594,8 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   a.x1 = x1; a.x2 = x2; a.v = v; a.k = k; a.D = D; a.y = y;
   a.ws = workspace;
   a.ws_bytes = workspace_bytes;
+  a.khat = use_khat ? (float2*)workspace : nullptr;
+  clear_pending_error();
   if (p == PLAN_EMBED) {
     // x1, x2, v, k into the transform grid, the circular plan there, y back
     GridProblem m;
@@ -658,6 +679,7 @@ hyenand_status operator_fwd(const void* q, const void* kin, const void* vin, con
   a.act_in.w_in = w_in;
   a.act_in.npos = npos;
   const hipStream_t s = (hipStream_t)stream;
+  clear_pending_error();
   hipError_t err = launch_op_prologue(q, kin, sc, B, (int)a.C, npos, a.bf16, eps_l2, eps_rms, s);
   if (err == hipSuccess) err = launch_plan(a, p, per, s);
   if (err == hipSuccess) err = launch_op_rmsnorm(y, w_out, B, (int)a.C, npos, a.bf16, eps_rms, s);
@@ -791,6 +813,7 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
   b.partial = (float*)workspace;
   const hipStream_t s = (hipStream_t)stream;
   hipError_t err = hipSuccess;
+  clear_pending_error();
   if (p == BWD_EMBED) {
     char* w = (char*)workspace;
     void* e[9];
@@ -931,6 +954,7 @@ hyenand_status hyenand_kernel_synth(const float* omega0, const float* W1, const 
   a.J = layers;
   a.wkind = window_kind;
   a.hidden = hidden;
+  clear_pending_error();
   hipError_t err = launch_synth(a, dtype == HYENAND_DTYPE_BF16, (hipStream_t)stream);
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
   return HYENAND_OK;
@@ -957,6 +981,7 @@ hyenand_status hyenand_modal_filter(const float* log_mag, const float* angle, co
     if (overlaps(k, (size_t)C * L * es, ptrs[i], (size_t)C * order * 4))
       return fail(HYENAND_ERR_INVALID_ARGUMENT, "k overlaps %s", names[i]);
   }
+  clear_pending_error();
   hipError_t err = launch_modal(log_mag, angle, res_re, res_im, k, C, order, L, dtype == HYENAND_DTYPE_BF16,
                                 (hipStream_t)stream);
   if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));

@@ -38,13 +38,24 @@ struct FftConvArgs {
   bool act;       // HyenaND operator: x1, v, x2 are q, kin, vin (see Gates)
   ActIn act_in;
   ModalIn modal;  // modal.M > 0: k generated per channel (four-step plan only)
+  float2* khat;   // non-null: the fused 2D plan transforms each channel's k
+                  // once into this workspace region (kC = C; fused2d_khat_bytes)
 };
+
+// Drop the calling thread's pending (non-sticky) HIP error, left by work
+// before a call, so that the hipGetLastError after each of the call's
+// launches reports that launch only.
+inline void clear_pending_error() { (void)hipGetLastError(); }
 
 // single pass (the padded problem of one line fits in LDS)
 bool fused1d_supported(int64_t P);
 hipError_t launch_fused1d(const FftConvArgs& a, hipStream_t s);
 bool fused2d_supported(int64_t P0, int64_t P1);
 hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s);
+// bytes of the per-channel kernel spectra of a fused 2D call with one kernel
+// per channel (C x P0 x P1/2 complex fp32); 0 where that path does not apply
+// (centered or non-power-of-two grids, the operator, a single sample)
+size_t fused2d_khat_bytes(const FftConvArgs& a);
 
 // single pass for grid extents that are not powers of two (linear and
 // centered modes, transform P_d = the smallest power of two >= 2 L_d - 1)

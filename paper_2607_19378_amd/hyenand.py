@@ -22,7 +22,7 @@ PAD_LINEAR, PAD_CIRCULAR, PAD_CENTERED = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
 
 EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_noalloc", "hyenand_fftconv_modal", "hyenand_fftconv_workspace_size",
-            "hyenand_fftconv_workspace_min",
+            "hyenand_fftconv_shared_k_workspace_size", "hyenand_fftconv_workspace_min",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
             "hyenand_kernel_synth", "hyenand_modal_filter", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
@@ -44,6 +44,12 @@ def lib() -> ctypes.CDLL:
         if _lib is None:
             if not os.path.exists(LIB_PATH):
                 raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2607_19378_amd.build`")
+            # torch first: its HIP runtime then satisfies the library's
+            # dependency on libamdhip64.so.7, so the process holds one HIP
+            # runtime.  Loaded before torch, the library would bring in the
+            # system one beside torch's, and whichever of the two initialises
+            # second finds no device.
+            import torch  # noqa: F401
             L = ctypes.CDLL(LIB_PATH)
             i64p = ctypes.POINTER(ctypes.c_int64)
             vp = ctypes.c_void_p
@@ -58,7 +64,8 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv_modal.argtypes = [vp] * 7 + [ctypes.c_int, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
                                                            ctypes.c_int, vp, ctypes.c_size_t, vp]
             L.hyenand_fftconv_modal.restype = ctypes.c_int
-            for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_workspace_min"):
+            for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_shared_k_workspace_size",
+                         "hyenand_fftconv_workspace_min"):
                 f = getattr(L, name)
                 f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                               ctypes.POINTER(ctypes.c_size_t)]
@@ -135,11 +142,14 @@ def _dtype_code(dtype) -> int:
     raise ValueError(f"unsupported dtype {dtype}")
 
 
-def workspace_size(shape, pad_mode: str, dtype) -> int:
+def workspace_size(shape, pad_mode: str, dtype, shared_k: bool = False) -> int:
+    """Recommended workspace bytes of hyenand_fftconv (shared_k: of
+    hyenand_fftconv_shared_k, which may use more to transform each channel's
+    kernel once)."""
     nd, dims = _dims(shape)
     out = ctypes.c_size_t(0)
-    _check(lib().hyenand_fftconv_workspace_size(nd, dims, _mode(pad_mode), _dtype_code(dtype),
-                                                ctypes.byref(out)))
+    fn = lib().hyenand_fftconv_shared_k_workspace_size if shared_k else lib().hyenand_fftconv_workspace_size
+    _check(fn(nd, dims, _mode(pad_mode), _dtype_code(dtype), ctypes.byref(out)))
     return int(out.value)
 
 
@@ -303,7 +313,7 @@ def fftconv(x1, x2, v, k, D, pad_mode: str = "linear", workspace=None, stream=No
     y = torch.empty_like(x1)
     own = None
     if workspace is None:
-        nbytes = workspace_size(tuple(x1.shape), pad_mode, x1.dtype)
+        nbytes = workspace_size(tuple(x1.shape), pad_mode, x1.dtype, shared_k)
         if nbytes:
             workspace = own = torch.empty(nbytes, dtype=torch.uint8, device=x1.device)
     fftconv_into(y, x1, x2, v, k, D, pad_mode, workspace, stream, shared_k)

@@ -118,6 +118,22 @@ def test_workspace_queries_are_host_only():
         H.plan_name((1, 1, 600, 600), "linear", "f32")
 
 
+def test_shared_kernel_workspace_query():
+    """hyenand_fftconv_shared_k_workspace_size: room for C spectra of P0 x P1/2
+    complex fp32 on the single-pass 2D plan with B >= 2, else the plain
+    query's size."""
+    assert H.workspace_size((8, 256, 64, 64), "linear", "f32", shared_k=True) == 256 * 128 * 64 * 8
+    assert H.workspace_size((2, 3, 32, 64), "circular", "bf16", shared_k=True) == 3 * 32 * 32 * 8
+    assert H.workspace_size((2, 1, 4, 4), "circular", "f32", shared_k=True) == 256  # rounded up
+    for shape, mode in (((1, 256, 64, 64), "linear"),      # one sample: nothing to share
+                        ((2, 4, 14, 14), "linear"),        # non-power-of-two grid
+                        ((2, 4, 32, 32), "centered"),      # centred kernels
+                        ((2, 4, 4096), "linear"),          # 1D
+                        ((2, 3, 256, 256), "linear"),      # multi-pass
+                        ((2, 3, 1 << 16), "linear")):      # four-step
+        assert H.workspace_size(shape, mode, "f32", shared_k=True) == H.workspace_size(shape, mode, "f32")
+
+
 def bcall(L, shape, mode=0, dtype=0, ptrs=None, ws=FAKE + (40 << 36), ws_bytes=1 << 20):
     nd = len(shape) - 2
     dims = (ctypes.c_int64 * len(shape))(*shape)
