@@ -207,8 +207,9 @@ __global__ void __launch_bounds__(512)
   __shared__ float red[NT / 64];
   PassTw<N1, E>::fill(twl, threadIdx.x, NT);
   const int ntile = N2 / TL;
-  const int64_t line = blockIdx.x / ntile;
-  const int c0 = (int)(blockIdx.x % ntile) * TL;
+  const uint32_t bid = fs_pair_tiles<1>(blockIdx.x);
+  const int64_t line = bid / ntile;
+  const int c0 = (int)(bid % ntile) * TL;
   const int64_t M = (int64_t)N1 * N2;
   const int64_t L = CIRC ? 2 * M : M;
   const int tid = threadIdx.x;
@@ -246,7 +247,7 @@ __global__ void __launch_bounds__(512)
     }
   }
   const float tot = fs_wg_sum<NT>(hu, red, tid);
-  if (tid == 0) partial[(line0 + line) * ntile + (blockIdx.x % ntile)] = tot;
+  if (tid == 0) partial[(line0 + line) * ntile + (bid % ntile)] = tot;
 }
 
 struct FsbLaunch {

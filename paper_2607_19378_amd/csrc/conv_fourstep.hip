@@ -44,8 +44,9 @@ __global__ void __launch_bounds__(512)
   const int ntile = N2 / TL;
   // 0: u = x1 v, 1: k (u_only: every workgroup takes u; k comes from
   // fs_cols_modal)
-  const int sig = u_only ? 0 : (int)(blockIdx.x & 1);
-  const int64_t rest = u_only ? (int64_t)blockIdx.x : (int64_t)(blockIdx.x >> 1);
+  const uint32_t bid = u_only ? blockIdx.x : fs_pair_tiles<2>(blockIdx.x);
+  const int sig = u_only ? 0 : (int)(bid & 1);
+  const int64_t rest = u_only ? (int64_t)bid : (int64_t)(bid >> 1);
   const int64_t line = rest / ntile;
   const int c0 = (int)(rest % ntile) * TL;
   const int64_t M = (int64_t)N1 * N2;

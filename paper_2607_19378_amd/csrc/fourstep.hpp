@@ -39,6 +39,22 @@ __device__ __forceinline__ void twiddle_run(float2 (&v)[E], float2 w, float2 s) 
   }
 }
 
+// Workgroup numbering of the column passes over NSIG signals: the logical
+// index b' = NSIG rest + sig (rest = line * ntile + tile) would put the tiles
+// 2q and 2q + 1 of one signal, which share every 128-byte row run of a
+// 16-column bf16 tile (64 bytes each), on different XCDs.  Workgroup b runs
+// on XCD b mod 8, so pairing b and b + 8 (one XCD, consecutive slots) on those
+// two tiles fetches each run once, while workgroups near in b stay near in
+// rest.  A bijection of [0, n) when n is a multiple of 16 NSIG and ntile is
+// even.  Used by fs_cols_fwd (u, k) and fsb_cols_inv; in the three-signal
+// fsb_cols_fwd the same numbering measured slower than the plain one.
+template <uint32_t NSIG>
+__device__ __forceinline__ uint32_t fs_pair_tiles(uint32_t b) {
+  const uint32_t s = b >> 3, x = b & 7u, h = s & 1u;
+  const uint32_t g = (s >> 1) * 8u + x;
+  return ((g / NSIG) * 2u + h) * NSIG + g % NSIG;
+}
+
 inline int ilog2_rt(int64_t n) {
   int r = 0;
   while ((int64_t(1) << r) < n) ++r;
