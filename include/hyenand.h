@@ -157,6 +157,40 @@ hyenand_status hyenand_fftconv_shared_k_workspace_size(int ndim, const int64_t* 
                                                        hyenand_dtype dtype, size_t* bytes_out);
 
 /*
+ * Kernel spectra kept across calls.  A static kernel (the Hyena operator's
+ * global kernel K, one row per channel: Eq. (hyena), section "Background:
+ * Hyena and CKConv"; at inference it does not change between calls) has the
+ * same spectrum in every call, so it can be transformed once:
+ *
+ *   hyenand_kernel_spectrum_size(ndim, dims, ...)  bytes of the spectra
+ *   hyenand_kernel_spectrum(k, khat, ...)          k [C, L1, L2] -> khat
+ *   hyenand_fftconv_spectrum(x1, x2, v, khat, ...) y as hyenand_fftconv_shared_k
+ *                                                  gives for that k
+ *
+ * dims, pad_mode, dtype: those of the convolution calls ([B, C, L1, L2];
+ * only C, the grid and the mode fix the spectra, so one khat serves every B).
+ * Runs on the single-pass 2D plan only: linear or circular mode with a
+ * power-of-two transform grid of up to 128 x 128 (hyenand_fftconv_plan_name
+ * "fused2d"); other shapes return HYENAND_ERR_UNSUPPORTED.
+ * khat: device buffer of at least the reported size (C x P0 x P1/2 complex
+ * fp32 values), 16-byte aligned, owned by the caller; its layout is private
+ * to the library and valid only for calls with the same C, grid, pad mode
+ * and library version.  k, x1, x2, v, y: 16-byte aligned, as for
+ * hyenand_fftconv; D element-aligned.  hyenand_kernel_spectrum reads k and
+ * writes khat (which must not overlap); hyenand_fftconv_spectrum reads khat
+ * and must not write it through y.  Validation, stream and error
+ * conventions as for hyenand_fftconv; the results are bitwise those of
+ * hyenand_fftconv_shared_k with the same k.
+ */
+hyenand_status hyenand_kernel_spectrum_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                            hyenand_dtype dtype, size_t* bytes_out);
+hyenand_status hyenand_kernel_spectrum(const void* k, void* khat, size_t khat_bytes, int ndim, const int64_t* dims,
+                                       hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream);
+hyenand_status hyenand_fftconv_spectrum(const void* x1, const void* x2, const void* v, const void* khat,
+                                        size_t khat_bytes, const void* D, void* y, int ndim, const int64_t* dims,
+                                        hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream);
+
+/*
  * hyenand_fftconv_noalloc -- hyenand_fftconv for callers that cannot
  * allocate device memory: code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc.  Arguments, layouts, validation, stream

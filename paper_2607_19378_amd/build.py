@@ -35,8 +35,11 @@ BUILD_DIR = os.path.join(os.path.dirname(PKG), "_build", "hyenand")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed fp32 VALU forms are disabled on purpose: hipcc would otherwise emit
-# v_pk_{add,mul,fma}_f32 from plain float code.
-FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall",
+# v_pk_{add,mul,fma}_f32 from plain float code.  -fno-signed-zeros lets the
+# compiler drop x + 0 where a transform's input is a compile-time zero (the
+# zero-padded half of every linear-mode first pass); it changes no value, at
+# most the sign of an exact zero.
+FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-fno-signed-zeros",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wno-pass-failed", "-I", os.path.join(os.path.dirname(PKG), "include")]
 

@@ -871,12 +871,14 @@ static hipError_t launch_2d_fused_t(const FftConvArgs& a, hipStream_t s) {
                        (int)a.C, a.kC, a.act_in, nullptr);
   } else if (a.khat) {
     // each channel's spectrum once, then the images read it
-    hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false, 1>), dim3((unsigned)a.C), dim3(512), 0, s,
-                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, a.act_in, a.khat);
-    hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false, 2>), dim3((unsigned)a.lines), dim3(512), 0, s,
-                       (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
-                       (int)a.C, a.kC, a.act_in, a.khat);
+    if (a.khat_pass != 2)
+      hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false, 1>), dim3((unsigned)a.C), dim3(512), 0, s,
+                         (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                         (int)a.C, a.kC, a.act_in, a.khat);
+    if (a.khat_pass != 1)
+      hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false, 2>), dim3((unsigned)a.lines), dim3(512), 0, s,
+                         (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
+                         (int)a.C, a.kC, a.act_in, a.khat);
   } else {
     hipLaunchKernelGGL((conv2d_fused<P0, P1, CIRC, TS, false>), dim3((unsigned)a.lines), dim3(512), 0, s,
                        (const TS*)a.x1, (const TS*)a.x2, (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y,
@@ -907,9 +909,7 @@ bool fused2d_supported(int64_t P0, int64_t P1) {
 }
 
 size_t fused2d_khat_bytes(const FftConvArgs& a) {
-  if (a.ndim != 2 || a.centered || a.rl || a.act || a.kC != a.C || a.lines / a.C < 2 ||
-      !fused2d_supported(a.P[0], a.P[1]))
-    return 0;
+  if (a.ndim != 2 || a.centered || a.rl || a.act || !fused2d_supported(a.P[0], a.P[1])) return 0;
   return ((size_t)a.C * (size_t)a.P[0] * (size_t)(a.P[1] / 2) * sizeof(float2) + 255) / 256 * 256;
 }
 

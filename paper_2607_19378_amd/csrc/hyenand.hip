@@ -433,6 +433,19 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return a0 < b0 + nb && b0 < a0 + na;
 }
 
+// Shape of a call that keeps kernel spectra (one kernel per channel, the
+// single-pass 2D plan): parsed, with the plan checked.
+hyenand_status spectrum_shape(int ndim, const int64_t* dims, int pad_mode, int dtype, FftConvArgs* a) {
+  const hyenand_status st = parse_shape(ndim, dims, pad_mode, dtype, a);
+  if (st != HYENAND_OK) return st;
+  a->kC = (int)a->C;
+  if (choose_plan(*a) != PLAN_FUSED2D || fused2d_khat_bytes(*a) == 0)
+    return fail(HYENAND_ERR_UNSUPPORTED,
+                "kernel spectra are kept for the single-pass 2D plan only (power-of-two transform grids up to "
+                "128 x 128, linear or circular)");
+  return HYENAND_OK;
+}
+
 }  // namespace
 
 namespace hyenand {
@@ -464,7 +477,7 @@ hyenand_status hyenand_fftconv_shared_k_workspace_size(int ndim, const int64_t* 
   a.kC = (int)a.C;
   const Plan p = choose_plan(a);
   if (p == PLAN_NONE) return fail(HYENAND_ERR_UNSUPPORTED, "no plan for this shape");
-  const size_t khb = p == PLAN_FUSED2D ? fused2d_khat_bytes(a) : 0;
+  const size_t khb = (p == PLAN_FUSED2D && a.lines / a.C >= 2) ? fused2d_khat_bytes(a) : 0;
   *bytes_out = std::max(recommended_ws(a, p), khb);
   return HYENAND_OK;
 }
@@ -580,7 +593,7 @@ hyenand_status forward(const void* x1, const void* x2, const void* v, const void
   const size_t per = bytes_per_line(a, p);
   // one kernel per channel on the fused 2D plan: with room in the workspace,
   // each channel's spectrum is computed once and read by all its images
-  const size_t khb = (shared_k && !modal && p == PLAN_FUSED2D) ? fused2d_khat_bytes(a) : 0;
+  const size_t khb = (shared_k && !modal && p == PLAN_FUSED2D && a.lines / a.C >= 2) ? fused2d_khat_bytes(a) : 0;
   const bool use_khat = khb > 0 && workspace && workspace_bytes >= khb;
   if (per > 0 || use_khat) {
     if (!workspace || workspace_bytes < per)
@@ -711,6 +724,70 @@ hyenand_status hyenand_fftconv_modal(const void* x1, const void* x2, const void*
   const ModalIn md{log_mag, angle, res_re, res_im, order};
   return forward(x1, x2, v, nullptr, D, y, ndim, dims, pad_mode, dtype, workspace, workspace_bytes, stream, true,
                  &md);
+}
+
+hyenand_status hyenand_kernel_spectrum_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode,
+                                            hyenand_dtype dtype, size_t* bytes_out) {
+  if (!bytes_out) return fail(HYENAND_ERR_INVALID_ARGUMENT, "bytes_out is NULL");
+  FftConvArgs a;
+  const hyenand_status st = spectrum_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  *bytes_out = fused2d_khat_bytes(a);
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_kernel_spectrum(const void* k, void* khat, size_t khat_bytes, int ndim, const int64_t* dims,
+                                       hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream) {
+  g_last_error.clear();
+  FftConvArgs a;
+  const hyenand_status st = spectrum_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  if (!k || !khat) return fail(HYENAND_ERR_INVALID_ARGUMENT, "k or khat is NULL");
+  if ((uintptr_t)k % 16 != 0 || (uintptr_t)khat % 16 != 0)
+    return fail(HYENAND_ERR_INVALID_ARGUMENT, "k and khat must be 16-byte aligned");
+  const size_t need = fused2d_khat_bytes(a);
+  if (khat_bytes < need)
+    return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "khat needs %zu bytes, got %zu", need, khat_bytes);
+  const size_t kb = (size_t)a.C * (size_t)a.L[0] * (size_t)a.L[1] * (a.bf16 ? 2 : 4);
+  if (overlaps(k, kb, khat, need)) return fail(HYENAND_ERR_INVALID_ARGUMENT, "khat overlaps k");
+  a.k = k;
+  a.khat = (float2*)khat;
+  a.khat_pass = 1;
+  clear_pending_error();
+  const hipError_t err = launch_fused2d(a, (hipStream_t)stream);
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
+}
+
+hyenand_status hyenand_fftconv_spectrum(const void* x1, const void* x2, const void* v, const void* khat,
+                                        size_t khat_bytes, const void* D, void* y, int ndim, const int64_t* dims,
+                                        hyenand_pad_mode pad_mode, hyenand_dtype dtype, void* stream) {
+  g_last_error.clear();
+  FftConvArgs a;
+  const hyenand_status st = spectrum_shape(ndim, dims, pad_mode, dtype, &a);
+  if (st != HYENAND_OK) return st;
+  const void* ptrs[6] = {x1, x2, v, khat, D, y};
+  const char* pn[6] = {"x1", "x2", "v", "khat", "D", "y"};
+  const size_t es = a.bf16 ? 2 : 4;
+  for (int i = 0; i < 6; ++i) {
+    if (!ptrs[i]) return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is NULL", pn[i]);
+    if ((uintptr_t)ptrs[i] % (i == 4 ? es : 16) != 0)
+      return fail(HYENAND_ERR_INVALID_ARGUMENT, "%s is not aligned", pn[i]);
+  }
+  const size_t need = fused2d_khat_bytes(a);
+  if (khat_bytes < need)
+    return fail(HYENAND_ERR_WORKSPACE_TOO_SMALL, "khat needs %zu bytes, got %zu", need, khat_bytes);
+  const size_t nb = (size_t)a.lines * (size_t)a.L[0] * (size_t)a.L[1] * es;
+  const size_t bytes[5] = {nb, nb, nb, need, (size_t)a.C * es};
+  for (int i = 0; i < 5; ++i)
+    if (overlaps(y, nb, ptrs[i], bytes[i])) return fail(HYENAND_ERR_INVALID_ARGUMENT, "y overlaps %s", pn[i]);
+  a.x1 = x1; a.x2 = x2; a.v = v; a.D = D; a.y = y;
+  a.khat = (float2*)const_cast<void*>(khat);
+  a.khat_pass = 2;
+  clear_pending_error();
+  const hipError_t err = launch_fused2d(a, (hipStream_t)stream);
+  if (err != hipSuccess) return fail(HYENAND_ERR_HIP, "HIP error %d: %s", (int)err, hipGetErrorString(err));
+  return HYENAND_OK;
 }
 
 hyenand_status hyenand_fftconv_backward_workspace_size(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,

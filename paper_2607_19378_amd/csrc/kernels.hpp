@@ -39,7 +39,9 @@ struct FftConvArgs {
   ActIn act_in;
   ModalIn modal;  // modal.M > 0: k generated per channel (four-step plan only)
   float2* khat;   // non-null: the fused 2D plan transforms each channel's k
-                  // once into this workspace region (kC = C; fused2d_khat_bytes)
+                  // once into this region (kC = C; fused2d_khat_bytes)
+  int khat_pass;  // with khat: 0 spectra then images, 1 spectra only,
+                  // 2 images only (spectra written by an earlier call)
 };
 
 // Drop the calling thread's pending (non-sticky) HIP error, left by work
@@ -54,7 +56,7 @@ bool fused2d_supported(int64_t P0, int64_t P1);
 hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s);
 // bytes of the per-channel kernel spectra of a fused 2D call with one kernel
 // per channel (C x P0 x P1/2 complex fp32); 0 where that path does not apply
-// (centered or non-power-of-two grids, the operator, a single sample)
+// (centered or non-power-of-two grids, the operator)
 size_t fused2d_khat_bytes(const FftConvArgs& a);
 
 // single pass for grid extents that are not powers of two (linear and

@@ -23,6 +23,7 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 
 EXPORTED = ("hyenand_fftconv", "hyenand_fftconv_shared_k", "hyenand_fftconv_noalloc", "hyenand_fftconv_modal", "hyenand_fftconv_workspace_size",
             "hyenand_fftconv_shared_k_workspace_size", "hyenand_fftconv_workspace_min",
+            "hyenand_kernel_spectrum_size", "hyenand_kernel_spectrum", "hyenand_fftconv_spectrum",
             "hyenand_fftconv_plan_name", "hyenand_fftconv_backward", "hyenand_fftconv_backward_workspace_size",
             "hyenand_fftconv_backward_workspace_min", "hyenand_operator", "hyenand_operator_workspace_size",
             "hyenand_kernel_synth", "hyenand_modal_filter", "hyenand_status_string", "hyenand_last_error", "hyenand_version")
@@ -64,8 +65,14 @@ def lib() -> ctypes.CDLL:
             L.hyenand_fftconv_modal.argtypes = [vp] * 7 + [ctypes.c_int, vp, vp, ctypes.c_int, i64p, ctypes.c_int,
                                                            ctypes.c_int, vp, ctypes.c_size_t, vp]
             L.hyenand_fftconv_modal.restype = ctypes.c_int
+            L.hyenand_kernel_spectrum.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, i64p, ctypes.c_int,
+                                                  ctypes.c_int, vp]
+            L.hyenand_kernel_spectrum.restype = ctypes.c_int
+            L.hyenand_fftconv_spectrum.argtypes = [vp, vp, vp, vp, ctypes.c_size_t, vp, vp, ctypes.c_int, i64p,
+                                                   ctypes.c_int, ctypes.c_int, vp]
+            L.hyenand_fftconv_spectrum.restype = ctypes.c_int
             for name in ("hyenand_fftconv_workspace_size", "hyenand_fftconv_shared_k_workspace_size",
-                         "hyenand_fftconv_workspace_min"):
+                         "hyenand_fftconv_workspace_min", "hyenand_kernel_spectrum_size"):
                 f = getattr(L, name)
                 f.argtypes = [ctypes.c_int, i64p, ctypes.c_int, ctypes.c_int,
                               ctypes.POINTER(ctypes.c_size_t)]
@@ -280,6 +287,56 @@ def fftconv_modal(x1, x2, v, log_mag, angle, res_re, res_im, D, pad_mode: str = 
     import torch
     y = torch.empty_like(x1)
     PreparedModalConv(y, x1, x2, v, log_mag, angle, res_re, res_im, D, pad_mode, workspace, stream)()
+    _keep_for_stream(stream, y)
+    return y
+
+
+def kernel_spectrum_size(shape, pad_mode: str, dtype) -> int:
+    """Bytes of the kept spectra of one kernel per channel for convolutions of
+    this [B, C, L1, L2] shape (single-pass 2D plan only)."""
+    nd, dims = _dims(shape)
+    out = ctypes.c_size_t(0)
+    _check(lib().hyenand_kernel_spectrum_size(nd, dims, _mode(pad_mode), _dtype_code(dtype), ctypes.byref(out)))
+    return int(out.value)
+
+
+def kernel_spectrum(k, shape, pad_mode: str = "linear", stream=None):
+    """Transform a static kernel k [C, L1, L2] once for convolutions of the
+    given [B, C, L1, L2] shape; returns the spectra as a torch uint8 tensor
+    (layout private to the library) for fftconv_spectrum."""
+    import torch
+    shape = tuple(shape)
+    if not k.is_cuda or not k.is_contiguous() or tuple(k.shape) != (shape[1],) + shape[2:]:
+        raise ValueError(f"k must be a contiguous GPU tensor of shape {(shape[1],) + shape[2:]}")
+    khat = torch.empty(kernel_spectrum_size(shape, pad_mode, k.dtype), dtype=torch.uint8, device=k.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(k.device)
+    nd, dims = _dims(shape)
+    _check(lib().hyenand_kernel_spectrum(_ptr(k), _ptr(khat), khat.numel(), nd, dims, _mode(pad_mode),
+                                         _dtype_code(k.dtype), ctypes.c_void_p(stream.cuda_stream)))
+    _keep_for_stream(stream, khat)
+    return khat
+
+
+def fftconv_spectrum(x1, x2, v, khat, D, pad_mode: str = "linear", stream=None):
+    """y = x2 * (k conv (x1*v) + D*(x1*v)) for the static kernel whose spectra
+    kernel_spectrum returned; torch-allocated y."""
+    import torch
+    shape = tuple(x1.shape)
+    for t in (x1, x2, v):
+        if not t.is_cuda or tuple(t.shape) != shape or t.dtype != x1.dtype or not t.is_contiguous():
+            raise ValueError("x1, x2, v must be contiguous GPU tensors of one shape and dtype")
+    if not D.is_cuda or D.dtype != x1.dtype or tuple(D.shape) != (shape[1],) or not D.is_contiguous():
+        raise ValueError("D must be a contiguous [C] GPU tensor of the same dtype")
+    if not khat.is_cuda or khat.dtype != torch.uint8:
+        raise ValueError("khat must be the uint8 GPU tensor kernel_spectrum returned")
+    y = torch.empty_like(x1)
+    if stream is None:
+        stream = torch.cuda.current_stream(x1.device)
+    nd, dims = _dims(shape)
+    _check(lib().hyenand_fftconv_spectrum(_ptr(x1), _ptr(x2), _ptr(v), _ptr(khat), khat.numel(), _ptr(D), _ptr(y),
+                                          nd, dims, _mode(pad_mode), _dtype_code(x1.dtype),
+                                          ctypes.c_void_p(stream.cuda_stream)))
     _keep_for_stream(stream, y)
     return y
 

@@ -279,6 +279,49 @@ def test_shared_kernel_validation(L):
     assert L.hyenand_fftconv_shared_k(*q, 1, dims, 0, 0, None, 0, None) == H.ERR_INVALID_ARGUMENT
 
 
+def test_kernel_spectrum_validation(L):
+    """Kept kernel spectra: sizes on the single-pass 2D plan (any B, since only
+    C, the grid and the mode fix them), UNSUPPORTED elsewhere, and argument
+    checks that fail before anything launches (fake pointers)."""
+    assert H.kernel_spectrum_size((8, 256, 64, 64), "linear", "f32") == 256 * 128 * 64 * 8
+    assert H.kernel_spectrum_size((1, 3, 32, 64), "circular", "bf16") == 3 * 32 * 32 * 8
+    for shape, mode in (((2, 4, 4096), "linear"), ((2, 4, 32, 32), "centered"), ((2, 4, 14, 14), "linear"),
+                        ((1, 3, 256, 256), "linear"), ((1, 2, 8, 8, 8), "circular")):
+        with pytest.raises(H.HyenandError) as e:
+            H.kernel_spectrum_size(shape, mode, "f32")
+        assert e.value.status == H.ERR_UNSUPPORTED
+    shape = (2, 3, 32, 32)
+    dims = (ctypes.c_int64 * 4)(*shape)
+    need = 3 * 64 * 32 * 8  # C x P0 x P1/2 complex fp32, P = 2 L (linear)
+    k, khat = FAKE, FAKE + (1 << 36)
+    vp = ctypes.c_void_p
+    assert L.hyenand_kernel_spectrum(vp(k), vp(khat), need - 1, 2, dims, 0, 0, None) == H.ERR_WORKSPACE_TOO_SMALL
+    assert L.hyenand_kernel_spectrum(None, vp(khat), need, 2, dims, 0, 0, None) == H.ERR_INVALID_ARGUMENT
+    assert L.hyenand_kernel_spectrum(vp(k), vp(khat + 8), need, 2, dims, 0, 0, None) == H.ERR_INVALID_ARGUMENT
+    assert L.hyenand_kernel_spectrum(vp(k), vp(k + 64), need, 2, dims, 0, 0, None) == H.ERR_INVALID_ARGUMENT
+    assert b"khat overlaps k" in L.hyenand_last_error()
+    d3 = (ctypes.c_int64 * 5)(2, 3, 8, 8, 8)
+    assert L.hyenand_kernel_spectrum(vp(k), vp(khat), 1 << 30, 3, d3, 1, 0, None) == H.ERR_UNSUPPORTED
+    p = [FAKE + i * (1 << 36) for i in range(6)]  # x1, x2, v, khat, D, y
+
+    def conv(ptrs, nbytes=need, d=dims, nd=2, mode=0):
+        return L.hyenand_fftconv_spectrum(*[vp(x) if x else None for x in ptrs[:4]], nbytes,
+                                          *[vp(x) if x else None for x in ptrs[4:]], nd, d, mode, 0, None)
+    assert conv(p, need - 256) == H.ERR_WORKSPACE_TOO_SMALL
+    for i in range(6):
+        q = list(p)
+        q[i] = 0
+        assert conv(q) == H.ERR_INVALID_ARGUMENT
+    q = list(p)
+    q[5] = p[3] + 16  # y over khat
+    assert conv(q) == H.ERR_INVALID_ARGUMENT
+    assert b"y overlaps khat" in L.hyenand_last_error()
+    q = list(p)
+    q[0] += 4
+    assert conv(q) == H.ERR_INVALID_ARGUMENT
+    assert conv(p, mode=2) == H.ERR_UNSUPPORTED
+
+
 def synth(L, shape=(2, 4, 16), hidden=32, layers=1, wkind=0, mode=0, dtype=0, ptrs=None, k=None):
     """hyenand_kernel_synth with fake pointers: every call here must fail
     validation (nothing may launch)."""

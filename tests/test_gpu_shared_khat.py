@@ -3,7 +3,9 @@ hyenand_fftconv_shared_k_workspace_size reports, each channel's kernel is
 transformed once and every image of that channel reads the spectrum.  Checked
 against the oracle (k repeated for every sample) on every instantiated
 transform grid, against the same call without the workspace (each image
-transforms k itself), and on the fallbacks (one sample, a short workspace)."""
+transforms k itself), and on the fallbacks (one sample, a short workspace).
+Kernel spectra kept across calls (hyenand_kernel_spectrum and
+hyenand_fftconv_spectrum) against the one-call path and the oracle."""
 import numpy as np
 import pytest
 
@@ -148,3 +150,36 @@ def test_khat_workload_size():
     assert diff <= 1e-6 * float(np.abs(per_image).max())
     del dev
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("mode,grid", [("linear", (64, 64)), ("circular", (32, 64)), ("linear", (16, 16))])
+def test_kept_spectra_serve_several_calls(mode, grid, dtype):
+    """One kernel_spectrum, then convolutions of two input sets and of a
+    different batch size from the same spectra: bitwise the one-call shared-k
+    results, and the oracle's within the tolerance."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    from gpu_util import from_device, log, to_device
+    C = 8
+    log(f"kept spectra {mode} {grid} {dtype}")
+    arrs = _inputs((3, C) + grid, dtype, 31 + grid[0])
+    kc_dev = to_device(arrs[3], dtype)
+    D_dev = to_device(arrs[4], dtype)
+    khat = H.kernel_spectrum(kc_dev, (3, C) + grid, mode)
+    assert khat.numel() == H.kernel_spectrum_size((1, C) + grid, mode, dtype)
+    rng = np.random.default_rng(5)
+    for B in (3, 3, 1):
+        shape = (B, C) + grid
+        x1, x2, v = (W.quantise(rng.standard_normal(shape), dtype) for _ in range(3))
+        dev = [to_device(a, dtype) for a in (x1, x2, v)]
+        y = H.fftconv_spectrum(dev[0], dev[1], dev[2], khat, D_dev, mode)
+        torch.cuda.synchronize()
+        got = from_device(y)
+        one_call = from_device(H.fftconv(dev[0], dev[1], dev[2], kc_dev, D_dev, pad_mode=mode, shared_k=True))
+        ref = _oracle((x1, x2, v, arrs[3], arrs[4]), shape, mode, dtype)
+        err = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        print(f"kept spectra {mode} {grid} {dtype} B={B}: rel_l2={err:.2e}")
+        assert err <= TOL[dtype]
+        if B >= 2:  # the one-call path uses the spectra too (B = 1 transforms k per image)
+            assert np.array_equal(got, one_call)
