@@ -29,12 +29,12 @@ namespace {
 // KC: k is the centered kernel of 2L - 1 points (linear transform grid); its
 // column lines have no zero half.
 template <int N1, bool CIRC, typename TS, bool KC = false, bool ACT = false>
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(ColCfgFwd<N1>::NT) __attribute__((amdgpu_waves_per_eu(ColCfgFwd<N1>::kWaves)))
     fs_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                 float2* __restrict__ ws, int64_t line0, int N2, int log2M, int64_t per_line, int kC, ActIn ain,
                 int C, int u_only) {
   static_assert(!(KC && CIRC), "centered kernels use the linear transform grid");
-  using Cf = ColCfg<N1>;
+  using Cf = ColCfgFwd<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1 of u (and of k unless centered)
   static_assert(NT / T >= TL, "one round covers the tile");
@@ -338,6 +338,7 @@ struct FsLaunch {
 template <int N1>
 hipError_t cols_fwd(const FsLaunch& L) {
   constexpr int TL = ColCfg<N1>::TL;
+  static_assert(ColCfgFwd<N1>::TL == TL, "the modal and forward column passes share the tiling");
   const FftConvArgs& a = *L.a;
   const int u_only = a.modal.M > 0;  // the kernel's columns come from fs_cols_modal
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * (u_only ? 1 : 2)));
@@ -355,8 +356,8 @@ hipError_t cols_fwd(const FsLaunch& L) {
 #define HY_ARGS(TS) \
   (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, L.ws, L.line0, kN2, L.log2M, L.per, a.kC, a.act_in, (int)a.C, u_only
 #define HY_LAUNCH(CI, TS, KC)                                                                                     \
-  if (a.act) hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, true>), grid, dim3(512), 0, L.s, HY_ARGS(TS)); \
-  else hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, false>), grid, dim3(512), 0, L.s, HY_ARGS(TS));
+  if (a.act) hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, true>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(TS)); \
+  else hipLaunchKernelGGL((fs_cols_fwd<N1, CI, TS, KC, false>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(TS));
   if (a.centered) {
     if (a.bf16) { HY_LAUNCH(false, uint16_t, true) } else { HY_LAUNCH(false, float, true) }
   } else if (a.bf16) {

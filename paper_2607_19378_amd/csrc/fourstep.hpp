@@ -29,6 +29,24 @@ struct ColCfg {
   static constexpr int TLP = TL + 1;
 };
 
+// The forward column pass with 512-point columns: 1024 lanes of 8 points on
+// the same 16-column tiles, so that two workgroups per CU (the LDS limit)
+// keep 32 wavefronts, and twice the memory requests, in flight.
+template <int N1>
+struct ColCfgFwd : ColCfg<N1> {
+  static constexpr int kWaves = 4;  // per SIMD, for amdgpu_waves_per_eu
+};
+template <>
+struct ColCfgFwd<512> {
+  static constexpr int NT = 1024;
+  static constexpr int TL = 16;
+  static constexpr int E = 8;
+  static constexpr int T = 512 / E;
+  static constexpr int TLP = TL + 1;
+  static constexpr int kWaves = 8;
+  static_assert(TL * T == NT, "every lane busy");
+};
+
 // w, w s, w s^2, ... (E values): twiddles of one lane by recurrence
 template <int E>
 __device__ __forceinline__ void twiddle_run(float2 (&v)[E], float2 w, float2 s) {
