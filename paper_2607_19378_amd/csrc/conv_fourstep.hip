@@ -278,10 +278,10 @@ __global__ void __launch_bounds__(512)
 }
 
 template <int N1, bool CIRC, typename TS, bool ACT = false>
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(ColCfgFwd<N1>::NT) __attribute__((amdgpu_waves_per_eu(ColCfgFwd<N1>::kWaves)))
     fs_cols_inv(const float2* __restrict__ ws, const TS* __restrict__ x2, TS* __restrict__ y, int64_t line0, int N2,
                 int64_t per_line) {
-  using Cf = ColCfg<N1>;
+  using Cf = ColCfgFwd<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NOUT = CIRC ? N1 : N1 / 2;  // cropped rows m1
   static_assert(NT / T >= TL, "one round covers the tile");
@@ -372,13 +372,13 @@ hipError_t cols_fwd(const FsLaunch& L) {
 
 template <int N1>
 hipError_t cols_inv(const FsLaunch& L) {
-  constexpr int TL = ColCfg<N1>::TL;
+  constexpr int TL = ColCfgFwd<N1>::TL;
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL)));
   const FftConvArgs& a = *L.a;
 #define HY_ARGS(TS) L.ws, (const TS*)a.x2, (TS*)a.y, L.line0, kN2, L.per
 #define HY_LAUNCH(CI, TS)                                                                                  \
-  if (a.act) hipLaunchKernelGGL((fs_cols_inv<N1, CI, TS, true>), grid, dim3(512), 0, L.s, HY_ARGS(TS)); \
-  else hipLaunchKernelGGL((fs_cols_inv<N1, CI, TS, false>), grid, dim3(512), 0, L.s, HY_ARGS(TS));
+  if (a.act) hipLaunchKernelGGL((fs_cols_inv<N1, CI, TS, true>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(TS)); \
+  else hipLaunchKernelGGL((fs_cols_inv<N1, CI, TS, false>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(TS));
   if (a.bf16) {
     if (a.circular) { HY_LAUNCH(true, uint16_t) } else { HY_LAUNCH(false, uint16_t) }
   } else {
