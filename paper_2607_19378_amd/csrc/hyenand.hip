@@ -184,9 +184,9 @@ size_t bytes_per_line(const FftConvArgs& a, Plan p) {
 // side streams, each with its own part of the workspace, so that the passes
 // of one chunk run in the launch tails of the others'; a chunk's spectra are
 // kept near 1/S of a 160 MiB budget so that the next pass over them still
-// finds most of them in the 256 MiB Infinity Cache.  S is 2, or 3 where a
-// chunk is a single line (measured best on the MI355X for 512^2, 2^20 and
-// 128^3 lines).  The recommended workspace is S such chunks;
+// finds most of them in the 256 MiB Infinity Cache.  S is 2 (measured best
+// or equal on the MI355X for 512^2, 2^20 and 128^3 lines against 1, 3 and 4,
+// at 160 to 640 MiB budgets).  The recommended workspace is S such chunks;
 // HYENAND_WS_TARGET_MB sets the budget and HYENAND_CHUNK_STREAMS fixes S.
 size_t ws_target_bytes() {
   size_t target = (size_t)160 << 20;
@@ -205,7 +205,8 @@ int chunk_streams(size_t per) {
     const long n = strtol(e, nullptr, 10);
     if (n >= 1 && n <= kMaxSide) return (int)n;
   }
-  return ws_target_bytes() / 2 / per < 2 ? 3 : 2;
+  (void)per;
+  return 2;
 }
 
 struct ChunkPlan {
