@@ -21,6 +21,8 @@
 // contiguous run of TL complex values and no explicit transpose is stored.
 // Tiles are sized so that two 512-lane (core pass: up to four 256-lane)
 // workgroups share a CU.
+#include <type_traits>
+
 #include "multipass.hpp"
 
 namespace hyenand {
@@ -281,6 +283,12 @@ __global__ void __launch_bounds__(256)
 // One workgroup per (line, tile of TL adjacent columns of the [L0][ncols]
 // view).  Only one signal tile lives in LDS: K's tile is prefetched into
 // registers while U's tile loads and transforms, then takes its place.
+// The view has ncols / HS rows of HS slots, of which bins 0 .. H - 1 are
+// valid.  With nyq set ((H - 1) a multiple of TL, several rows), a row's
+// first H - 1 bins make whole aligned tiles and the last bin of every row
+// (the Nyquist bin) goes into tiles of its own, TL rows each, so that no
+// lane transforms the padding slots; else tiles run over every slot and the
+// padding lanes idle.
 // ---------------------------------------------------------------------------
 template <int P0, bool CIRC>
 struct CoreCfg {
@@ -295,15 +303,16 @@ struct CoreCfg {
 template <int P0, bool CIRC>
 __global__ void __launch_bounds__(mp_core_nt(P0))
     mp_core(float2* __restrict__ ws, const void* __restrict__ Dp, int dbf16, int64_t line0, int C,
-            int ncols, int HS, int H, int64_t half, int64_t per_line, float scale, int krows) {
+            int ncols, int HS, int H, int64_t half, int64_t per_line, float scale, int krows, int nyq) {
   using Cf = CoreCfg<P0, CIRC>;
   constexpr int TL = Cf::TL, TLP = Cf::TLP, E = Cf::E, T = Cf::T, NT = Cf::NT, L0 = Cf::L0;
   __shared__ float2 tile[P0 * TLP];
   __shared__ float2 twl[imax(1, PassTw<P0, E>::kCount)];
-  const int ntile = (ncols + TL - 1) / TL;
+  const int vrows = ncols / HS;
+  const int rtiles = (H - 1) / TL;  // aligned tiles per row (nyq)
+  const int ntile = nyq ? vrows * rtiles + (vrows + TL - 1) / TL : (ncols + TL - 1) / TL;
   const int tl = (int)(blockIdx.x % ntile);
   const int64_t line = blockIdx.x / ntile;
-  const int col0 = tl * TL;
   const int tid = threadIdx.x;
   PassTw<P0, E>::fill(twl, tid, NT);
   const int c = (int)((line0 + line) % C);
@@ -313,16 +322,28 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
   const float2* K = U + half;
 
   // Column points of U and K straight from global memory into registers
-  // (lane (cc, t) holds rows n = t + T e of column col0 + cc; consecutive
-  // lanes read consecutive columns).  K's loads are issued right after U's
+  // (lane (cc, t) holds rows n = t + T e of column col; consecutive lanes
+  // read consecutive columns, except in Nyquist tiles).  K's loads are issued right after U's
   // and arrive while U is transformed.  The LDS tile is only the exchange
   // scratch; the result goes back to U's rows straight from registers.
   static_assert(NT / T >= TL, "one round of columns");
   const int cc = tid % TL, t = tid / TL;
   const bool act = t < T;
-  const bool cv = act && col_valid(col0 + cc, ncols, HS, H);
-  float2* const uc = U + col0 + cc;
-  const float2* const kc = K + col0 + cc;
+  int col;
+  bool cv;
+  if (!nyq) {
+    col = tl * TL + cc;
+    cv = act && col_valid(col, ncols, HS, H);
+  } else if (tl < vrows * rtiles) {  // aligned bins of one row
+    col = (tl / rtiles) * HS + (tl % rtiles) * TL + cc;
+    cv = act;
+  } else {  // the Nyquist bins of TL rows
+    const int r = (tl - vrows * rtiles) * TL + cc;
+    cv = act && r < vrows;
+    col = cv ? r * HS + (H - 1) : 0;
+  }
+  float2* const uc = U + col;
+  const float2* const kc = K + col;
   const ScrS<TLP> sc{tile + cc};
   float2 wu[E], wk[E];
 #pragma unroll
@@ -545,17 +566,18 @@ template <int P0>
 hipError_t core(const MpLaunch& L) {
   const FftConvArgs& a = *L.a;
   const int ncols = L.g.P1 * L.g.HS;
-  if (a.circular) {
-    constexpr int TL = CoreCfg<P0, true>::TL;
-    const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
-    hipLaunchKernelGGL((mp_core<P0, true>), grid, dim3(CoreCfg<P0, true>::NT), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
-                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale, L.g.krows0);
-  } else {
-    constexpr int TL = CoreCfg<P0, false>::TL;
-    const dim3 grid((unsigned)((int64_t)L.nl * ((ncols + TL - 1) / TL)));
-    hipLaunchKernelGGL((mp_core<P0, false>), grid, dim3(CoreCfg<P0, false>::NT), 0, L.s, L.ws, a.D, (int)a.bf16, L.line0, (int)a.C,
-                       ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale, L.g.krows0);
-  }
+  auto launch = [&](auto circ) {
+    constexpr bool CI = decltype(circ)::value;
+    constexpr int TL = CoreCfg<P0, CI>::TL;
+    const int rows = ncols / L.g.HS;
+    const int nyq = rows > 1 && (L.g.H - 1) % TL == 0 && L.g.H - 1 >= TL;
+    const int64_t ntile = nyq ? (int64_t)rows * ((L.g.H - 1) / TL) + (rows + TL - 1) / TL : (ncols + TL - 1) / TL;
+    hipLaunchKernelGGL((mp_core<P0, CI>), dim3((unsigned)(L.nl * ntile)), dim3(CoreCfg<P0, CI>::NT), 0, L.s, L.ws,
+                       a.D, (int)a.bf16, L.line0, (int)a.C, ncols, L.g.HS, L.g.H, L.g.half, L.per, L.scale,
+                       L.g.krows0, nyq);
+  };
+  if (a.circular) launch(std::true_type{});
+  else launch(std::false_type{});
   return hipGetLastError();
 }
 
