@@ -267,6 +267,20 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
   }
   __syncthreads();
 
+  // outer gate values of the items this lane stores in step 3, as raw storage
+  // words, fetched now so that their latency hides behind the row transforms
+  const int64_t gbase = (gline * L0 + n0) * (int64_t)L1 * LL;
+  constexpr int NI = L1 * LL / 2, IT = (NI + NT - 1) / NT;
+  constexpr bool kPre = IT <= 8;
+  typename Raw2<TS>::type g2r[kPre ? IT : 1];
+  if constexpr (kPre) {
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int i = tid + NT * j;
+      if (NI % NT == 0 || i < NI) g2r[j] = ld2_raw(x2 + gbase + 2 * i);
+    }
+  }
+
   // 2. complex-to-real rows: c2r_pair turns row n1's half spectrum (slot 0
   //    holding DC + i Nyquist) into the length-ML transform of its even/odd
   //    output pairs; the inverse leaves y[2m] + i y[2m + 1] in slot m
@@ -305,14 +319,26 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
   __syncthreads();
 
   // 3. outer gate and store, coalesced along rows
-  const int64_t gbase = (gline * L0 + n0) * (int64_t)L1 * LL;
-  batched_copy<L1 * LL / 2, NT, 4>(
-      tid, [&](int i) { return Gates<ACT>{}.g2(ld2(x2 + gbase + 2 * i)); },
-      [&](int i, float2 g) {
+  if constexpr (kPre) {
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int i = tid + NT * j;
+      if (NI % NT == 0 || i < NI) {
+        const float2 g = Gates<ACT>{}.g2(widen2(g2r[j]));
         const int r = i / (LL / 2), m = i - r * (LL / 2);
         const float2 q = pl[r * HP + m];
         st2(y + gbase + 2 * i, make_float2(g.x * q.x, g.y * q.y));
-      });
+      }
+    }
+  } else {
+    batched_copy<L1 * LL / 2, NT, 4>(
+        tid, [&](int i) { return Gates<ACT>{}.g2(ld2(x2 + gbase + 2 * i)); },
+        [&](int i, float2 g) {
+          const int r = i / (LL / 2), m = i - r * (LL / 2);
+          const float2 q = pl[r * HP + m];
+          st2(y + gbase + 2 * i, make_float2(g.x * q.x, g.y * q.y));
+        });
+  }
 }
 
 template <int P, bool CIRC>
