@@ -104,6 +104,20 @@ __global__ void __launch_bounds__(fused1d_nt(P))
     Ub[0] = make_float2(G.u1(ld1(x1 + base), ld1(v + base), 0), 0.f);
     Kb[0] = make_float2(ld1(k + kbase), 0.f);
   }
+  // outer gate values of the output pairs this lane stores at the end, as
+  // raw storage words, fetched now so that their latency hides behind the
+  // transforms (a short line is one launch latency, nothing to hide it in)
+  constexpr bool kGpre = L >= 2;
+  typename Raw2<TS>::type gpre[kGpre ? F::EI : 1];
+  if constexpr (kGpre) {
+    if (tid < F::TI) {
+#pragma unroll
+      for (int e = 0; e < F::EI; ++e) {
+        const int n = 2 * (tid + F::TI * e);
+        if (n < L) gpre[e] = ld2_raw(x2 + base + n);
+      }
+    }
+  }
   __syncthreads();
 
   // forward half-length transforms of both packed lines
@@ -162,8 +176,15 @@ __global__ void __launch_bounds__(fused1d_nt(P))
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int n = 2 * (t + T * e);
-        if (n < L) st1(y + base + n, G.g1(ld1(x2 + base + n)) * w[e].x);
-        if (n + 1 < L) st1(y + base + n + 1, G.g1(ld1(x2 + base + n + 1)) * w[e].y);
+        if constexpr (kGpre) {  // L even: n < L holds both outputs of the pair
+          if (n < L) {
+            const float2 g = G.g2(widen2(gpre[e]));
+            st2(y + base + n, make_float2(g.x * w[e].x, g.y * w[e].y));
+          }
+        } else {
+          if (n < L) st1(y + base + n, G.g1(ld1(x2 + base + n)) * w[e].x);
+          if (n + 1 < L) st1(y + base + n + 1, G.g1(ld1(x2 + base + n + 1)) * w[e].y);
+        }
       }
     }
   }
