@@ -38,11 +38,11 @@ __device__ __forceinline__ float fs_wg_sum(float x, float* red, int tid) {
 }
 
 template <int N1, bool CIRC, typename TS>
-__global__ void __launch_bounds__(512)
+__global__ void __launch_bounds__(ColCfgFwd<N1>::NT) __attribute__((amdgpu_waves_per_eu(ColCfgFwd<N1>::kWaves)))
     fsb_cols_fwd(const TS* __restrict__ x1, const TS* __restrict__ v, const TS* __restrict__ k,
                  const TS* __restrict__ gy, const TS* __restrict__ x2, float2* __restrict__ ws, int64_t line0,
                  int N2, int log2M, int64_t per_line) {
-  using Cf = ColCfg<N1>;
+  using Cf = ColCfgFwd<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1
   static_assert(NT / T >= TL, "one round covers the tile");
@@ -263,17 +263,17 @@ struct FsbLaunch {
 
 template <int N1>
 hipError_t b_cols_fwd(const FsbLaunch& L) {
-  constexpr int TL = ColCfg<N1>::TL;
+  constexpr int TL = ColCfgFwd<N1>::TL;
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * 3));
   const FftConvArgs& a = L.b->f;
 #define HY_ARGS(TS) \
   (const TS*)a.x1, (const TS*)a.v, (const TS*)a.k, (const TS*)L.b->gy, (const TS*)a.x2, L.ws, L.line0, kN2, L.log2M, L.per
   if (a.bf16) {
-    if (a.circular) hipLaunchKernelGGL((fsb_cols_fwd<N1, true, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
-    else hipLaunchKernelGGL((fsb_cols_fwd<N1, false, uint16_t>), grid, dim3(512), 0, L.s, HY_ARGS(uint16_t));
+    if (a.circular) hipLaunchKernelGGL((fsb_cols_fwd<N1, true, uint16_t>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(uint16_t));
+    else hipLaunchKernelGGL((fsb_cols_fwd<N1, false, uint16_t>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(uint16_t));
   } else {
-    if (a.circular) hipLaunchKernelGGL((fsb_cols_fwd<N1, true, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
-    else hipLaunchKernelGGL((fsb_cols_fwd<N1, false, float>), grid, dim3(512), 0, L.s, HY_ARGS(float));
+    if (a.circular) hipLaunchKernelGGL((fsb_cols_fwd<N1, true, float>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(float));
+    else hipLaunchKernelGGL((fsb_cols_fwd<N1, false, float>), grid, dim3(ColCfgFwd<N1>::NT), 0, L.s, HY_ARGS(float));
   }
 #undef HY_ARGS
   return hipGetLastError();

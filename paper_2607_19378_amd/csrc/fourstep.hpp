@@ -29,9 +29,10 @@ struct ColCfg {
   static constexpr int TLP = TL + 1;
 };
 
-// The forward and inverse column passes with 512-point columns: 1024 lanes of
-// 8 points on the same 16-column tiles, so that two workgroups per CU (the LDS
-// limit) keep 32 wavefronts, and twice the memory requests, in flight.
+// The forward and inverse column passes with 512-point columns (and the
+// backward's forward column pass): 1024 lanes of 8 points on the same
+// 16-column tiles, so that two workgroups per CU (the LDS limit) keep 32
+// wavefronts, and twice the memory requests, in flight.  Same TL as ColCfg.
 template <int N1>
 struct ColCfgFwd : ColCfg<N1> {
   static constexpr int kWaves = 4;  // per SIMD, for amdgpu_waves_per_eu
