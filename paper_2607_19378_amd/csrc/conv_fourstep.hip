@@ -119,13 +119,17 @@ __global__ void __launch_bounds__(512)
   using Cf = ColCfg<N1>;
   constexpr int E = Cf::E, T = Cf::T, NT = Cf::NT, TL = Cf::TL, TLP = Cf::TLP;
   constexpr int NZ = CIRC ? N1 : N1 / 2;  // nonzero rows m1 of the kernel
-  constexpr int MX = kMaxFusedModalOrder;
   static_assert(NT / T >= TL, "one round covers the tile");
   __shared__ float2 tile[N1 * TLP];
   __shared__ float2 twl[imax(1, PassTw<N1, E>::kCount)];
-  __shared__ float2 tA[MX * TL];
-  __shared__ float2 tB[MX * T];
-  __shared__ float2 tS[MX], tL[MX];
+  // the mode tables, sized by the order at launch (modal_lds_bytes): two
+  // workgroups share a CU up to order 16 with 512-point columns
+  extern __shared__ float2 mtab[];
+  const int nm = md.M;
+  float2* const tA = mtab;            // [nm][TL]
+  float2* const tB = tA + nm * TL;    // [nm][T]
+  float2* const tS = tB + nm * T;     // [nm]
+  float2* const tL = tS + nm;         // [nm]
   const int tid = threadIdx.x;
   PassTw<N1, E>::fill(twl, tid, NT);
   const int ntile = N2 / TL;
@@ -133,7 +137,6 @@ __global__ void __launch_bounds__(512)
   const int c0 = (int)(blockIdx.x % ntile) * TL;
   const int64_t M = (int64_t)N1 * N2;
   const int64_t ch = (line0 + line) % C;
-  const int nm = md.M;
   const float* pa = md.a + ch * nm;
   const float* pt = md.th + ch * nm;
   for (int i = tid; i < nm * (TL + T + 2); i += NT) {
@@ -344,12 +347,13 @@ hipError_t cols_fwd(const FsLaunch& L) {
   const dim3 grid((unsigned)((int64_t)L.nl * (kN2 / TL) * (u_only ? 1 : 2)));
   if (u_only) {
     const dim3 kgrid((unsigned)((int64_t)L.nl * (kN2 / TL)));
+    const size_t mbytes = (size_t)a.modal.M * (TL + ColCfg<N1>::T + 2) * sizeof(float2);
     if (a.circular)
-      hipLaunchKernelGGL((fs_cols_modal<N1, true>), kgrid, dim3(512), 0, L.s, a.modal, L.ws, L.line0, kN2, L.log2M,
-                         L.per, (int)a.C);
+      hipLaunchKernelGGL((fs_cols_modal<N1, true>), kgrid, dim3(512), mbytes, L.s, a.modal, L.ws, L.line0, kN2,
+                         L.log2M, L.per, (int)a.C);
     else
-      hipLaunchKernelGGL((fs_cols_modal<N1, false>), kgrid, dim3(512), 0, L.s, a.modal, L.ws, L.line0, kN2, L.log2M,
-                         L.per, (int)a.C);
+      hipLaunchKernelGGL((fs_cols_modal<N1, false>), kgrid, dim3(512), mbytes, L.s, a.modal, L.ws, L.line0, kN2,
+                         L.log2M, L.per, (int)a.C);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
