@@ -441,7 +441,15 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
     }
   }
   __syncthreads();
-  {
+  // The real rows' spectra come out of the packed row transforms Z by
+  // untangling (r2c_pair: bin g from Z[g] and Z[M1 - g]).  When one round of
+  // column groups covers every column, each column lane untangles the bins it
+  // loads (the bin and its mirror are both read before the first exchange
+  // barrier of the column transforms, which is the first write to either
+  // slot), so no pass rewrites the rows; in linear mode it then untangles
+  // only the L0 nonzero rows.  Otherwise a pass over the rows does it first.
+  constexpr bool kColUntangle = M1 <= F::CR;
+  if constexpr (!kColUntangle) {
     // Untangling, in place: item (row l, g) for 0 < g < M1/2 owns bins g and
     // M1 - g; bins 0 and M1/2 are their own mirrors and share the item g = 0
     // of their row.  The DC and Nyquist bins of a real row are real: slot 0
@@ -469,8 +477,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
         row[M1 - g] = xb;
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // 2. column groups: forward transforms of U and K, gated product with the
   //    folded shortcut, inverse transform; keep rows < L0.  Group 0 is the
@@ -486,14 +494,21 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4)))
       const bool act = M1 % CR == 0 || grp < M1;
       const bool nyq = act && grp == 0;
       const int col = act ? grp : 0;
+      const int mcol = (M1 - col) & (M1 - 1);          // mirror bin (0 for 0)
+      const float2 twc = twiddle<ilog2(P1), false>(col);  // (1, 0) for column 0
+      // bin col of row n: untangled from the packed row spectrum, or as stored
+      auto bin = [&](const float2* R, int n) -> float2 {
+        if constexpr (kColUntangle) return untangle_bin(R + n * RP, col, mcol, twc);
+        else return R[n * RP + col];
+      };
       float2 wu[E], wk[E];
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int n = t + T * e;
         const bool nz = act && (CIRC || n < L0);
-        if constexpr (KH != 1) wu[e] = nz ? Uh[n * RP + col] : czero();
+        if constexpr (KH != 1) wu[e] = nz ? bin(Uh, n) : czero();
         if constexpr (KH == 2) wk[e] = act ? kh[n * M1 + col] : czero();
-        else wk[e] = nz ? Kh[n * RP + col] : czero();
+        else wk[e] = nz ? bin(Kh, n) : czero();
       }
       const ScrS<RP> su{UK + col};
       if constexpr (KH != 1) BlockFFT<P0, E, false>::run(wu, t, su, act);

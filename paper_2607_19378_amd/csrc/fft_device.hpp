@@ -493,6 +493,15 @@ __device__ __forceinline__ void r2c_pair(float2 A, float2 B, float2 w, float2& X
   Xmg = make_float2(e.x - t.x, t.y - e.y);  // conj(e - t)
 }
 
+// Bin g of a real row's doubled R2C spectrum from its packed transform Z
+// (r2c_pair's first output, w = exp(-2 pi i g / P)); for g = 0 the DC and
+// Nyquist bins, both real, packed as DC + i Nyquist (w = 1).  gm = (M - g) mod M.
+__device__ __forceinline__ float2 untangle_bin(const float2* row, int g, int gm, float2 w) {
+  float2 xa, xb;
+  r2c_pair(row[g], row[gm], w, xa, xb);
+  return g == 0 ? make_float2(xa.x, xb.x) : xa;
+}
+
 // Complex-to-real pre-pass, the inverse of r2c_pair: from the Hermitian
 // spectrum values Yg = Y[g], Ymg = Y[M-g] of a real length-P signal y and
 // w = exp(-2 pi i g / P), returns  Yg + conj Ymg + i w^-1 (Yg - conj Ymg)
