@@ -120,9 +120,16 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
     }
   }
   __syncthreads();
-  // untangle in place: item (row, g) owns bins g and ML - g; slot 0 of a row
-  // keeps its DC and Nyquist bins (both real) as DC + i Nyquist
-  {
+  // The rows' real spectra come out of their packed transforms by untangling
+  // (bin g from packed bins g and ML - g).  When one round of column lanes
+  // covers the ML bin columns, each lane untangles the bins it loads (the
+  // bin and its mirror are read before the first exchange barrier of the
+  // axis-1 transforms, the first write to either slot); otherwise a pass
+  // over the rows does it in place first.
+  constexpr bool kColUntangle = ML <= NT / Cf::TC;
+  if constexpr (!kColUntangle) {
+    // untangle in place: item (row, g) owns bins g and ML - g; slot 0 of a
+    // row keeps its DC and Nyquist bins (both real) as DC + i Nyquist
     constexpr int NG = imax(1, ML / 2);
     for (int it = tid; it < L1 * NG; it += NT) {
       const int l = it % L1, g = it / L1;
@@ -142,8 +149,8 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
         row[ML - g] = xb;
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // 2. axis-1 transforms of the ML bin columns, straight to the workspace:
   //    bin row f1 of plane n0 at ((n0 P + f1) HS) of this signal's half
@@ -157,9 +164,15 @@ __global__ void __launch_bounds__((SlabCfg<P, CIRC>::NT))
       const bool act = ML % CR == 0 || col < ML;
       const int cc = act ? col : 0;
       const ScrS<HP> sc{pl + cc};
+      const int mc = (ML - cc) & (ML - 1);                // mirror bin (0 for 0)
+      const float2 twc = twiddle<ilog2(P), false>(cc);   // (1, 0) for column 0
       float2 x[E];
 #pragma unroll
-      for (int e = 0; e < E; ++e) x[e] = act ? pl[(t + T * e) * HP + cc] : czero();
+      for (int e = 0; e < E; ++e) {
+        const float2* row = pl + (t + T * e) * HP;
+        if constexpr (kColUntangle) x[e] = act ? untangle_bin(row, cc, mc, twc) : czero();
+        else x[e] = act ? row[cc] : czero();
+      }
       if constexpr (CIRC) {
         BlockFFT<NC, E, false>::run(x, t, sc, act);
         if (act) {
