@@ -197,15 +197,14 @@ size_t ws_target_bytes() {
   return target;
 }
 
-// side streams for lines of `per` workspace bytes: 1 (the caller's stream
-// only) up to kMaxSide
+// side streams of a chunked call: 1 (the caller's stream only) up to
+// kMaxSide, 2 unless HYENAND_CHUNK_STREAMS says otherwise
 constexpr int kMaxSide = 4;
-int chunk_streams(size_t per) {
+int chunk_streams() {
   if (const char* e = getenv("HYENAND_CHUNK_STREAMS")) {
     const long n = strtol(e, nullptr, 10);
     if (n >= 1 && n <= kMaxSide) return (int)n;
   }
-  (void)per;
   return 2;
 }
 
@@ -218,7 +217,7 @@ struct ChunkPlan {
 ChunkPlan plan_chunks(int64_t lines, size_t per, size_t ws_bytes) {
   ChunkPlan c;
   const int64_t fit = (int64_t)(ws_bytes / per);  // >= 1, checked by the caller
-  const int want = chunk_streams(per);
+  const int want = chunk_streams();
   c.streams = want;
   if (c.streams > fit) c.streams = (int)fit;
   if (c.streams > lines) c.streams = (int)lines;
@@ -237,7 +236,7 @@ size_t recommended_ws(const FftConvArgs& a, Plan p) {
   if (p == PLAN_EMBED) return embed_fwd_ws(a, true);
   const size_t per = bytes_per_line(a, p);
   if (per == 0) return 0;
-  const int ns = chunk_streams(per);
+  const int ns = chunk_streams();
   int64_t n = (int64_t)(ws_target_bytes() / (size_t)ns / per);
   if (n < 1) n = 1;
   n *= ns;
@@ -421,7 +420,7 @@ size_t bwd_bytes_per_line(const FftConvArgs& a, BwdPlan p) {
 size_t bwd_recommended_spectra(const FftConvArgs& a, BwdPlan p) {
   const size_t per = bwd_bytes_per_line(a, p);
   if (per == 0) return 0;
-  const int ns = chunk_streams(per);
+  const int ns = chunk_streams();
   int64_t n = (int64_t)(ws_target_bytes() / (size_t)ns / per);
   if (n < 1) n = 1;
   n *= ns;
