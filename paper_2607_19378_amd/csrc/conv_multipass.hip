@@ -377,7 +377,9 @@ __global__ void __launch_bounds__(mp_core_nt(P0))
 template <int PL>
 struct RowsInvCfg {
   static constexpr int H = PL / 2 + 1;
-  static constexpr int PRP = PL + 18;  // pair region pitch (holds 2H and the scratch; = 2 mod 16)
+  // pair region pitch: the two half spectra (2H entries), then the exchange
+  // scratch and the outputs with one pad slot per 16 entries
+  static constexpr int PRP = imax(2 * H, pad16_size(PL));
   static constexpr int E = imin(16, PL);
   static constexpr int T = PL / E;
   static constexpr int NT = 256;
@@ -419,8 +421,11 @@ __global__ void __launch_bounds__(256)
       });
   __syncthreads();
 
+  // the T lanes of a pair are consecutive (a wavefront holds 64 / T pairs):
+  // with the padded scratch every exchange of the 512-point transform reaches
+  // 32 distinct bank pairs
   for (int q0 = 0; q0 < PPW; q0 += NT / T) {
-    const int q = q0 + tid % (NT / T), t = tid / (NT / T);
+    const int q = q0 + tid / T, t = tid % T;
     const bool act = q < npair;
     float2* R = reg + (act ? q : 0) * PRP;
     float2 w[E];
@@ -440,12 +445,13 @@ __global__ void __launch_bounds__(256)
       w[e] = make_float2(ya.x - yb.y, ya.y + yb.x);  // ya + i yb
     }
     if constexpr (T == 1) __syncthreads();
-    BlockFFT<PL, E, true>::run(w, t, ScrS<1>{R}, act, twl);
+    const ScrPad16 sc{R};
+    BlockFFT<PL, E, true>::run(w, t, sc, act, twl);
     if (act) {
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const int n = t + T * e;
-        if (CIRC || n < LL) R[n] = w[e];
+        if (CIRC || n < LL) *sc(n) = w[e];
       }
     }
   }
@@ -464,7 +470,8 @@ __global__ void __launch_bounds__(256)
           const int i = 4 * i4;
           const int row = i / LL, n = i - row * LL;
           if (row < 2 * npair) {
-            const float2* R = reg + (row >> 1) * PRP + n;
+            // n is a multiple of 4, so n .. n + 3 share one 16-entry block
+            const float2* R = reg + (row >> 1) * PRP + n + (n >> 4);
             float4 o;
             if (row & 1)
               o = make_float4(g.x * R[0].y, g.y * R[1].y, g.z * R[2].y, g.w * R[3].y);
@@ -476,7 +483,7 @@ __global__ void __launch_bounds__(256)
   } else {
     for (int i = tid; i < npair * 2 * LL; i += NT) {
       const int row = i / LL, n = i - row * LL;
-      const float2 qv = reg[(row >> 1) * PRP + n];
+      const float2 qv = reg[(row >> 1) * PRP + n + (n >> 4)];
       st1(y + gbase + i, Gates<ACT>{}.g1(ld1(x2 + gbase + i)) * ((row & 1) ? qv.y : qv.x));
     }
   }
