@@ -83,14 +83,20 @@ typedef enum { HYENAND_DTYPE_F32 = 0, HYENAND_DTYPE_BF16 = 1, HYENAND_DTYPE_MAX_
  *                   line; a launch holds fewer than 2^32 work-items).
  *                   Transform extents: L_d circular, 2 L_d
  *                   linear and centered; supported up to 2^22 points in 1D
- *                   and 1024 per axis in 2D/3D.  Other extents run on the
- *                   smallest power of two >= 2 L_d - 1 (exact for a
- *                   non-circular convolution; in circular mode the kernel is
- *                   repeated periodically over the displacements
- *                   -(L_d - 1) .. L_d - 1, which makes the circular
- *                   convolution a non-circular one): in one pass per line
- *                   for 1D up to L = 8192 and 2D up to 128-point transforms
- *                   per axis; beyond that (and in 3D) embedded in the
+ *                   and 1024 per axis in 2D/3D.  Other extents (section
+ *                   3.2.2: patch grids such as 14 x 14, register rows):
+ *                   grids of up to 4096 transform points in one pass on
+ *                   mixed-radix transforms (radix 2, 3, 4, 5, 7, 8), a
+ *                   circular axis whose extent has no prime factor above 7
+ *                   on its own L_d points, every other axis on the smallest
+ *                   such P_d >= 2 L_d - 1; or on the smallest power of two
+ *                   >= 2 L_d - 1, whichever is the faster for the shape (a
+ *                   non-circular convolution is exact on any such P_d; a
+ *                   circular axis of another extent repeats the kernel
+ *                   periodically over the displacements -(L_d - 1) ..
+ *                   L_d - 1, which makes it a non-circular one): in one pass
+ *                   per line for 1D up to L = 8192 and 2D up to 128-point
+ *                   transforms per axis; beyond that embedded in the
  *                   transform grid, where the call is the circular
  *                   convolution of the zero-padded inputs and of k placed at
  *                   its displacements: x1, x2, v and k are copied into the
@@ -254,7 +260,7 @@ hyenand_status hyenand_fftconv_workspace_min(int ndim, const int64_t* dims, hyen
 
 /* Name of the plan the call would use ("fused1d", "fused2d", "multipass2d",
  * "multipass3d", "fourstep1d"; for extents that are not powers of two
- * "fused1d_any", "fused2d_any" or "embedded1d/2d/3d"), written
+ * "mixed1d/2d/3d", "fused1d_any", "fused2d_any" or "embedded1d/2d/3d"), written
  * NUL-terminated into buf (at most n bytes).  Pure host function. */
 hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, hyenand_pad_mode pad_mode, hyenand_dtype dtype,
                                          char* buf, size_t n);

@@ -29,7 +29,7 @@ hyenand_status fail(hyenand_status s, const char* fmt, ...) {
   return s;
 }
 
-enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP, PLAN_FUSED_RL, PLAN_EMBED };
+enum Plan { PLAN_NONE = 0, PLAN_FUSED1D, PLAN_FUSED2D, PLAN_MULTIPASS, PLAN_FOURSTEP, PLAN_FUSED_RL, PLAN_MIXED, PLAN_EMBED };
 
 const char* plan_name(Plan p, const FftConvArgs& a) {
   const int ndim = a.ndim;
@@ -39,6 +39,7 @@ const char* plan_name(Plan p, const FftConvArgs& a) {
     case PLAN_MULTIPASS: return ndim == 3 ? (slab3d_supported(a) ? "slab3d" : "multipass3d") : "multipass2d";
     case PLAN_FOURSTEP: return "fourstep1d";
     case PLAN_FUSED_RL: return ndim == 1 ? "fused1d_any" : "fused2d_any";
+    case PLAN_MIXED: return ndim == 1 ? "mixed1d" : (ndim == 2 ? "mixed2d" : "mixed3d");
     case PLAN_EMBED: return ndim == 1 ? "embedded1d" : (ndim == 2 ? "embedded2d" : "embedded3d");
     default: return "none";
   }
@@ -148,13 +149,21 @@ Plan embedded_inner_plan(const FftConvArgs& a, GridProblem* m) {
   return p == PLAN_EMBED ? PLAN_NONE : p;
 }
 
+// Extents that are not powers of two: the mixed-radix kernels where they are
+// the faster (mixed_preferred), the power-of-two single-pass kernels, then the
+// mixed-radix ones for the shapes those do not take, then the embedded plans.
+// HYENAND_PLAN=mixed prefers, =nomixed avoids, the mixed-radix kernels.
 Plan choose_plan(const FftConvArgs& a) {
+  const char* force = getenv("HYENAND_PLAN");
   if (a.rl) {
+    const bool want = force && strcmp(force, "mixed") == 0;
+    const bool avoid = force && strcmp(force, "nomixed") == 0;
+    if (!avoid && (want ? mixed_supported(a) : mixed_preferred(a))) return PLAN_MIXED;
     if (fused_rl_supported(a)) return PLAN_FUSED_RL;
+    if (!avoid && mixed_supported(a)) return PLAN_MIXED;
     GridProblem m;
     return embedded_inner_plan(a, &m) != PLAN_NONE ? PLAN_EMBED : PLAN_NONE;
   }
-  const char* force = getenv("HYENAND_PLAN");
   const bool no_fused = force && (strcmp(force, "multipass") == 0 || strcmp(force, "fourstep") == 0);
   if (a.ndim == 1) {
     if (!no_fused && fused1d_supported(a.P[0])) return PLAN_FUSED1D;
@@ -525,6 +534,7 @@ hipError_t launch_plan(const FftConvArgs& a, Plan p, size_t per, hipStream_t s) 
         return launch_fourstep(a, l0, nl, ws, st);
       });
     case PLAN_FUSED_RL: return launch_fused_rl(a, s);
+    case PLAN_MIXED: return launch_mixed(a, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -64,6 +64,13 @@ size_t fused2d_khat_bytes(const FftConvArgs& a);
 bool fused_rl_supported(const FftConvArgs& a);
 hipError_t launch_fused_rl(const FftConvArgs& a, hipStream_t s);
 
+// single pass on mixed-radix transform grids (extents with prime factors 2,
+// 3, 5, 7 up to 4096 points per image): circular axes of such extents on
+// their own points, the others on the smallest such P_d >= 2 L_d - 1
+bool mixed_supported(const FftConvArgs& a);
+bool mixed_preferred(const FftConvArgs& a);  // faster than the power-of-two kernels
+hipError_t launch_mixed(const FftConvArgs& a, hipStream_t s);
+
 // multi-pass 2D/3D (lines along each axis; spectra staged in the workspace).
 // One call runs every pass over lines [line0, line0 + nl) with their spectra
 // in ws (nl times the bytes per line), all on stream s.

@@ -64,7 +64,7 @@ def test_invalid_arguments(L):
     # extents that are not powers of two beyond the single-pass kernels run
     # embedded in their transform grid, which needs a workspace
     assert call(L, (1, 1, 10000), mode=1) == H.ERR_WORKSPACE_TOO_SMALL
-    assert call(L, (1, 1, 12, 12, 12), mode=1) == H.ERR_WORKSPACE_TOO_SMALL
+    assert call(L, (1, 1, 20, 20, 20), mode=1) == H.ERR_WORKSPACE_TOO_SMALL  # 8000 points: no mixed radix
     assert call(L, (1, 1, 300, 300)) == H.ERR_WORKSPACE_TOO_SMALL  # a 1024 x 1024 grid
     assert call(L, (1, 1, 300, 300), ws=FAKE + (40 << 36), ws_bytes=5 * (4 << 20)) == H.ERR_WORKSPACE_TOO_SMALL
     assert call(L, (1, 1, 600, 600)) == H.ERR_UNSUPPORTED  # a 2048-point axis: beyond every plan
@@ -97,16 +97,34 @@ def test_workspace_queries_are_host_only():
     assert H.plan_name((8, 256, 64, 64), "linear", "f32") == "fused2d"
     assert H.plan_name((2, 2, 1, 64), "linear", "bf16") == "fused1d"      # unit axis squeezed
     assert H.plan_name((2, 2, 1, 1, 1), "circular", "f32") == "fused1d"  # single point
-    # circular, not a power of two: the periodic kernel on the centred grid
-    assert H.plan_name((1, 1, 3), "circular", "f32") == "fused1d_any"
-    assert H.plan_name((2, 4, 14, 14), "circular", "f32") == "fused2d_any"
+    # circular, extents with prime factors 2, 3, 5, 7: mixed-radix transforms
+    # on the grid's own points
+    assert H.plan_name((2, 4, 14, 14), "circular", "f32") == "mixed2d"
+    assert H.plan_name((1, 1, 300), "circular", "f32") == "mixed1d"      # 300 points against 1024
+    assert H.plan_name((1, 1, 3), "circular", "f32") == "mixed1d"        # short lines
+    # lines beyond 128 points with more than a third of the power-of-two
+    # points: that kernel
+    assert H.plan_name((1, 1, 500), "circular", "f32") == "fused1d_any"
+    assert H.plan_name((1, 2, 5, 6, 7), "circular", "bf16") == "mixed3d"
+    assert H.plan_name((1, 2, 63, 64), "circular", "f32") == "mixed2d"    # 4032 points
     assert H.workspace_size((1, 1, 3), "circular", "f32") == 0
+    # a circular axis of 13 points: k repeated periodically on 25 points, the
+    # 14-point axis on its own; half the points of the 32 x 32 power-of-two grid
+    assert H.plan_name((2, 3, 13, 14), "circular", "f32") == "mixed2d"
+    # 13 alone: 25 points, a short line
+    assert H.plan_name((2, 3, 13), "circular", "f32") == "mixed1d"
+    # beyond 4096 mixed-radix points
     assert H.plan_name((1, 1, 10000), "circular", "f32") == "embedded1d"
+    assert H.plan_name((1, 1, 65, 65), "circular", "f32") == "embedded2d"   # 135 x 135 mixed, 256 x 256 pow2
     # other extents in the non-circular modes: transforms on the smallest power
     # of two >= 2L - 1, single pass
-    assert H.plan_name((1, 1, 3), "linear", "f32") == "fused1d_any"
-    assert H.plan_name((2, 4, 14, 14), "centered", "f32") == "fused2d_any"
-    assert H.plan_name((2, 4, 14, 16), "linear", "bf16") == "fused2d_any"
+    assert H.plan_name((1, 1, 3), "linear", "f32") == "mixed1d"
+    assert H.plan_name((1, 1, 100), "linear", "f32") == "fused1d_any"      # 200 points against 256
+    assert H.plan_name((1, 1, 1000), "linear", "f32") == "fused1d_any"
+    # 2D grids up to 2048 mixed-radix points: those kernels (27 x 27, 27 x 32)
+    assert H.plan_name((2, 4, 14, 14), "centered", "f32") == "mixed2d"
+    assert H.plan_name((2, 4, 14, 16), "linear", "bf16") == "mixed2d"
+    assert H.plan_name((2, 4, 24, 40), "linear", "f32") == "fused2d_any"   # 48 x 80 against 64 x 128
     assert H.workspace_size((2, 4, 14, 14), "linear", "f32") == 0
     # beyond the single pass: embedded in the 256 x 256 grid; five embedded
     # tensors of 256^2 floats, then the circular multi-pass plan's workspace
@@ -116,6 +134,20 @@ def test_workspace_queries_are_host_only():
         5 * 256 * 256 * 4 + H.workspace_min((1, 1, 256, 256), "circular", "f32"))
     with pytest.raises(H.HyenandError):
         H.plan_name((1, 1, 600, 600), "linear", "f32")
+
+
+def test_mixed_radix_plan_choice(monkeypatch):
+    """HYENAND_PLAN=mixed prefers the mixed-radix kernels wherever they take
+    the shape (4096 transform points at most), =nomixed avoids them."""
+    monkeypatch.setenv("HYENAND_PLAN", "mixed")
+    assert H.plan_name((2, 4, 14, 14), "centered", "f32") == "mixed2d"    # 27 x 27
+    assert H.plan_name((2, 4, 1000), "linear", "bf16") == "mixed1d"       # 2000 points
+    assert H.plan_name((2, 4, 13), "circular", "f32") == "mixed1d"
+    assert H.plan_name((2, 4, 3000), "linear", "f32") == "fused1d_any"    # 6000 > 4096
+    assert H.plan_name((2, 4, 64, 64), "linear", "f32") == "fused2d"      # powers of two: unchanged
+    monkeypatch.setenv("HYENAND_PLAN", "nomixed")
+    assert H.plan_name((2, 4, 14, 14), "circular", "f32") == "fused2d_any"
+    assert H.plan_name((1, 2, 5, 6, 7), "circular", "f32") == "embedded3d"
 
 
 def test_shared_kernel_workspace_query():

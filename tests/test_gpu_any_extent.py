@@ -3,7 +3,10 @@ on the smallest power of two >= 2L - 1 and crop L points (linear and centered
 modes; the circular mode as the centred convolution of the periodically
 repeated kernel); parity with the fp64 oracle (which takes any extent) on 1D
 and 2D grids, fp32 and bf16, one kernel per channel and the HyenaND
-operator."""
+operator.  These tests keep the library off the mixed-radix kernels
+(HYENAND_PLAN=nomixed), which tests/test_gpu_mixed_radix.py covers."""
+import os
+
 import numpy as np
 import pytest
 
@@ -20,6 +23,13 @@ def _gpu():
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
+    prev = os.environ.get("HYENAND_PLAN")
+    os.environ["HYENAND_PLAN"] = "nomixed"
+    yield
+    if prev is None:
+        del os.environ["HYENAND_PLAN"]
+    else:
+        os.environ["HYENAND_PLAN"] = prev
 
 
 def _case(B, C, grid, mode, dtype, seed, shared=False):
