@@ -21,8 +21,10 @@
 // both.  Odd extents need no half-length packing this way, and each image
 // costs one and a half complex transforms of the grid.
 //
-// Each axis runs Stockham passes of radix 8, 4, 2, 7, 5 or 3 between two LDS
-// buffers (one barrier per pass).  A pass of radix r over an axis of P points
+// Each axis runs Stockham passes between two LDS buffers (one barrier per
+// pass), of the largest radix up to 16 that divides what is left of the axis
+// (16, 15, 14, 12, 10, 9, 8, 7, 6, 5, 4, 3, 2: one pass for a 14-point axis,
+// three for 1000 points), each butterfly an in-register DFT.  A pass of radix r over an axis of P points
 // with stride S, after passes whose radices multiply to Ns: butterfly j of a
 // line reads the r points j + t P/r, multiplies point t by the twiddle
 // exp(-2 pi i t (j mod Ns) / (Ns r)), takes the r-point DFT and writes output
@@ -77,8 +79,9 @@ struct MrPlan {
   int Q;          // image pairs per workgroup
   int twoff[3], ntw;
   int nt;         // lanes per workgroup
+  int fam;        // radix family of the passes
   int npass;      // forward passes; the inverse runs the same list
-  FastDiv dN, dP1, dP2, dL1, dL2, dLd;
+  FastDiv dN, dP1, dP2, dL1, dL2, dLd, dC, dKC;
   MrPass pass[kMrMaxPass];
 };
 
@@ -129,10 +132,91 @@ __device__ __forceinline__ void dft_odd(float2 (&x)[R]) {
   x[0] = x0;
 }
 
+// exp(-2 pi i m / R) for m < R, R <= 16, evaluated at compile time (Taylor
+// series in double on the angle reduced to [-pi, pi]).
+constexpr double kPiD = 3.141592653589793238462643;
+constexpr double cx_sin(double x) {
+  double term = x, sum = x;
+  for (int n = 1; n < 24; ++n) {
+    term *= -x * x / ((2.0 * n) * (2.0 * n + 1.0));
+    sum += term;
+  }
+  return sum;
+}
+constexpr double cx_cos(double x) {
+  double term = 1.0, sum = 1.0;
+  for (int n = 1; n < 24; ++n) {
+    term *= -x * x / ((2.0 * n - 1.0) * (2.0 * n));
+    sum += term;
+  }
+  return sum;
+}
 template <int R>
-__device__ __forceinline__ void dft_any(float2 (&x)[R]) {
-  if constexpr (R == 3 || R == 5 || R == 7) dft_odd<R>(x);
-  else dft<R, false>(x);
+struct RootTab {
+  float c[R], s[R];
+  constexpr RootTab() : c(), s() {
+    for (int m = 0; m < R; ++m) {
+      const int mm = 2 * m > R ? m - R : m;
+      const double th = 2.0 * kPiD * mm / R;
+      c[m] = (float)cx_cos(th);
+      s[m] = (float)(-cx_sin(th));
+    }
+  }
+};
+template <int R>
+constexpr RootTab<R> kRoots{};
+
+// a * exp(-2 pi i m / R), m a compile-time constant after unrolling; exact
+// for the quarter turns
+template <int R>
+__device__ __forceinline__ float2 mul_root_c(float2 a, int m) {
+  m %= R;
+  if (m == 0) return a;
+  if (4 * m == R) return make_float2(a.y, -a.x);
+  if (2 * m == R) return make_float2(-a.x, -a.y);
+  if (4 * m == 3 * R) return make_float2(-a.y, a.x);
+  const float c = kRoots<R>.c[m], s = kRoots<R>.s[m];
+  return make_float2(fmaf(a.x, c, -a.y * s), fmaf(a.x, s, a.y * c));
+}
+
+// largest base radix (8, 7, 5, 4, 3, 2) that divides R and is below it
+constexpr int split_radix(int R) {
+  for (int a : {8, 7, 5, 4, 3, 2})
+    if (a < R && R % a == 0) return a;
+  return R;
+}
+constexpr bool base_radix(int R) { return R == 2 || R == 3 || R == 4 || R == 5 || R == 7 || R == 8; }
+
+// In-register DFT of R points (R <= 16, prime factors <= 7), natural order in
+// and out.  Composite R = A B by decimation in time: n = n1 + A n2,
+// k = k1 + B k2; B-point DFTs of the A decimated sequences, the twiddles
+// exp(-2 pi i n1 k1 / R), then A-point DFTs across them.
+template <int R>
+__device__ __forceinline__ void dft_reg(float2 (&x)[R]) {
+  if constexpr (base_radix(R)) {
+    if constexpr (R == 3 || R == 5 || R == 7) dft_odd<R>(x);
+    else dft<R, false>(x);
+  } else {
+    constexpr int A = split_radix(R), B = R / A;
+    float2 t[A][B];
+#pragma unroll
+    for (int n1 = 0; n1 < A; ++n1) {
+#pragma unroll
+      for (int n2 = 0; n2 < B; ++n2) t[n1][n2] = x[n1 + A * n2];
+      dft_reg<B>(t[n1]);
+#pragma unroll
+      for (int k1 = 0; k1 < B; ++k1) t[n1][k1] = mul_root_c<R>(t[n1][k1], n1 * k1);
+    }
+#pragma unroll
+    for (int k1 = 0; k1 < B; ++k1) {
+      float2 u[A];
+#pragma unroll
+      for (int n1 = 0; n1 < A; ++n1) u[n1] = t[n1][k1];
+      dft_reg<A>(u);
+#pragma unroll
+      for (int k2 = 0; k2 < A; ++k2) x[k1 + B * k2] = u[k2];
+    }
+  }
 }
 
 // One Stockham pass of radix R over `items` butterflies (all images); TW:
@@ -156,7 +240,7 @@ __device__ __forceinline__ void mr_pass_t(const float2* src, float2* dst, const 
 #pragma unroll
       for (int t = 1; t < R; ++t) x[t] = c_mul(x[t], tp[t * tws]);
     }
-    dft_any<R>(x);
+    dft_reg<R>(x);
     float2* dp = dst + base + (jn * (uint32_t)(ps.ns * R) + kk) * (uint32_t)ps.sa;
 #pragma unroll
     for (int t = 0; t < R; ++t) dp[t * nss] = x[t];
@@ -170,20 +254,35 @@ __device__ __forceinline__ void mr_pass(const float2* src, float2* dst, const fl
   else mr_pass_t<R, NT, true>(src, dst, tw, ps, items, tid);
 }
 
+// Radix families: every kernel takes 8, 7, 5, 4, 3 and 2, and family f adds
+// kFamRadix[f] (more composite radices in one kernel and the compiler keeps
+// their arrays in scratch memory instead of registers).
+constexpr int kNumFam = 4;
+constexpr int kFamRadix[kNumFam][2] = {{0, 0}, {14, 12}, {16, 10}, {15, 9}};
+constexpr bool fam_has(int f, int r) {
+  return r == 8 || r == 7 || r == 5 || r == 4 || r == 3 || r == 2 || kFamRadix[f][0] == r || kFamRadix[f][1] == r;
+}
+
 // every pass of the plan over n points (whole images), ping-ponging src/dst;
 // returns with the result in src
-template <int NT>
-__device__ __forceinline__ void mr_transform(float2*& src, float2*& dst, const float2* tw, const MrPlan& pl,
-                                             uint32_t n, uint32_t tid) {
-  for (int i = 0; i < pl.npass; ++i) {
-    const MrPass& ps = pl.pass[i];
+template <int NT, int FAM>
+__device__ __forceinline__ void mr_transform(float2*& src, float2*& dst, const float2* tw, const MrPass* passes,
+                                             int npass, uint32_t n, uint32_t tid) {
+  for (int i = 0; i < npass; ++i) {
+    const MrPass ps = passes[i];
     switch (ps.r) {
+      case 16: if constexpr (fam_has(FAM, 16)) mr_pass<16, NT>(src, dst, tw, ps, n / 16, tid); break;
+      case 15: if constexpr (fam_has(FAM, 15)) mr_pass<15, NT>(src, dst, tw, ps, n / 15, tid); break;
+      case 14: if constexpr (fam_has(FAM, 14)) mr_pass<14, NT>(src, dst, tw, ps, n / 14, tid); break;
+      case 12: if constexpr (fam_has(FAM, 12)) mr_pass<12, NT>(src, dst, tw, ps, n / 12, tid); break;
+      case 10: if constexpr (fam_has(FAM, 10)) mr_pass<10, NT>(src, dst, tw, ps, n / 10, tid); break;
+      case 9: if constexpr (fam_has(FAM, 9)) mr_pass<9, NT>(src, dst, tw, ps, n / 9, tid); break;
       case 8: mr_pass<8, NT>(src, dst, tw, ps, n / 8, tid); break;
-      case 4: mr_pass<4, NT>(src, dst, tw, ps, n / 4, tid); break;
-      case 2: mr_pass<2, NT>(src, dst, tw, ps, n / 2, tid); break;
       case 7: mr_pass<7, NT>(src, dst, tw, ps, n / 7, tid); break;
       case 5: mr_pass<5, NT>(src, dst, tw, ps, n / 5, tid); break;
-      default: mr_pass<3, NT>(src, dst, tw, ps, n / 3, tid); break;
+      case 4: mr_pass<4, NT>(src, dst, tw, ps, n / 4, tid); break;
+      case 3: mr_pass<3, NT>(src, dst, tw, ps, n / 3, tid); break;
+      default: mr_pass<2, NT>(src, dst, tw, ps, n / 2, tid); break;
     }
     __syncthreads();
     float2* t = src;
@@ -194,13 +293,13 @@ __device__ __forceinline__ void mr_transform(float2*& src, float2*& dst, const f
 
 // exp(-2 pi i m / P), 0 <= m < P: the nearest quarter turn q = round(4m / P)
 // is taken exactly in integers, and the remainder angle
-// 2 pi m / P - q pi / 2 = pi (4m - qP) / (2P), at most pi / 4, goes to sincospif,
-// so the only rounding before it is that of (4m - qP) / 2P (|x| <= 1/4).
+// 2 pi m / P - q pi / 2 = pi (4m - qP) / (2P), at most pi / 4, goes to sinpif
+// and cospif, so the only rounding before them is that of (4m - qP) / 2P
+// (|x| <= 1/4).
 __device__ __forceinline__ float2 mr_root(int m, int P) {
   const int q = (8 * m + P) / (2 * P);  // round(4m / P), half up
   const float x = (float)(4 * m - q * P) / (float)(2 * P);
-  float s, c;
-  sincospif(x, &s, &c);
+  const float s = sinpif(x), c = cospif(x);
   // exp(-i (q pi / 2 + pi x)) = (-i)^q (c - i s)
   switch (q & 3) {
     case 0: return make_float2(c, -s);
@@ -228,21 +327,46 @@ __device__ __forceinline__ float2 mr_product(float2 z, float2 zm, float D, float
   return c_mul(u, make_float2(fmaf(0.5f, d.y, D), -0.5f * d.x));
 }
 
-template <typename TS, bool ACT, int NT>
+// Gates of image img (the operator's s row and w_in[c]), without 64-bit division.
+template <bool ACT, typename TS>
+__device__ __forceinline__ Gates<ACT> mr_gates(const ActIn& ain, uint32_t img, uint32_t C, FastDiv dC) {
+  Gates<ACT> g;
+  if constexpr (ACT) {
+    const uint32_t b = fdiv(img, dC);
+    g.s = ain.s + (size_t)b * ain.npos;
+    g.w = ld1(reinterpret_cast<const TS*>(ain.w_in) + (img - b * C));
+  } else {
+    g.s = nullptr;
+    g.w = 1.f;
+  }
+  return g;
+}
+
+// One workgroup per group of 2Q images (img0 = 2Q blockIdx.x).
+template <typename TS, bool ACT, int NT, int FAM>
 __global__ void __launch_bounds__(NT)
     conv_mixed(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
-               const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int64_t lines, int C,
-               int kC, ActIn ain, MrPlan pl) {
+               const TS* __restrict__ k, const TS* __restrict__ Dp, TS* __restrict__ y, int lines, int C, int kC,
+               ActIn ain, MrPlan pl) {
   extern __shared__ float2 mr_lds[];
   const uint32_t tid = threadIdx.x;
-  const uint32_t N = (uint32_t)pl.N;
-  const int64_t img0 = (int64_t)blockIdx.x * 2 * pl.Q;
-  const int nimg = (int)(lines - img0 < 2 * pl.Q ? lines - img0 : 2 * pl.Q);
-  const uint32_t np = (uint32_t)(nimg + 1) / 2;  // pairs in this workgroup
+  const uint32_t N = (uint32_t)pl.N, Ld = (uint32_t)pl.Ld;
+  const uint32_t G2 = 2 * (uint32_t)pl.Q;  // images per group
+  const uint32_t i0 = blockIdx.x * G2;
+  const uint32_t nimg = imin((int)G2, lines - (int)i0);
+  const uint32_t np = (nimg + 1) / 2;  // pairs in this group
   float2* const tw = mr_lds;
   float2* src = mr_lds + pl.ntw;
-  float2* dst = src + (size_t)2 * pl.Q * N;
+  float2* dst = src + (size_t)G2 * N;
+  float* const Dl = reinterpret_cast<float*>(dst + (size_t)G2 * N);  // D of the group's images
   const bool exact = pl.N == pl.Ld;  // every axis exact: transform point = data point
+
+  // the pass descriptors, copied with compile-time indices (a run-time index
+  // into the plan argument would make the compiler copy all of it to scratch)
+  __shared__ MrPass spass[kMrMaxPass];
+#pragma unroll
+  for (int i = 0; i < kMrMaxPass; ++i)
+    if (tid == (uint32_t)i && i < pl.npass) spass[i] = pl.pass[i];
 
   // twiddles exp(-2 pi i m / P) of each transformed axis
 #pragma unroll
@@ -250,30 +374,41 @@ __global__ void __launch_bounds__(NT)
     if (pl.P[d] < 2) continue;
     for (int m = tid; m < pl.P[d]; m += NT) tw[pl.twoff[d] + m] = mr_root(m, pl.P[d]);
   }
+  for (uint32_t i = tid; i < G2; i += NT) {
+    const uint32_t img = i0 + i;
+    Dl[i] = i < nimg ? ld1(Dp + (img - fdiv(img, pl.dC) * (uint32_t)C)) : 0.f;
+  }
 
   // stage z = u + i k of every image on the transform grid
+  const uint32_t nval = nimg * N;
   for (uint32_t f = tid; f < 2 * np * N; f += NT) {
-    const uint32_t i = fdiv(f, pl.dN), p = f - i * N;
     float2 z = czero();
-    if ((int)i < nimg) {
-      const int64_t img = img0 + i;
-      const Gates<ACT> G = line_gates<ACT, TS>(ain, img, C);
-      const TS* kl = k + (size_t)k_line(img, kC) * pl.Kd;
-      const size_t base = (size_t)img * pl.Ld;
-      if (exact) {
-        z.x = G.u1(ld1(x1 + base + p), ld1(v + base + p), p);
-        z.y = ld1(kl + p);
+    if (f < nval) {
+      if (exact && kC == 0 && !ACT) {  // the group's x1, v, k: one run from i0 N
+        const size_t o = (size_t)i0 * N + f;
+        z = make_float2(ld1(x1 + o) * ld1(v + o), ld1(k + o));
       } else {
-        const uint32_t t = fdiv(p, pl.dP2), g2 = p - t * pl.P[2];
-        const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
-        if ((int)g0 < pl.L[0] && (int)g1 < pl.L[1] && (int)g2 < pl.L[2]) {
-          const uint32_t n = (g0 * pl.L[1] + g1) * pl.L[2] + g2;
-          z.x = G.u1(ld1(x1 + base + n), ld1(v + base + n), n);
+        const uint32_t i = fdiv(f, pl.dN), p = f - i * N;
+        const uint32_t img = i0 + i;
+        const size_t base = (size_t)img * Ld;
+        const uint32_t kl = kC ? img - fdiv(img, pl.dKC) * (uint32_t)kC : img;
+        const TS* kp = k + (size_t)kl * (uint32_t)pl.Kd;
+        const Gates<ACT> G = mr_gates<ACT, TS>(ain, img, (uint32_t)C, pl.dC);
+        if (exact) {
+          z.x = G.u1(ld1(x1 + base + p), ld1(v + base + p), p);
+          z.y = ld1(kp + p);
+        } else {
+          const uint32_t t = fdiv(p, pl.dP2), g2 = p - t * pl.P[2];
+          const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
+          if ((int)g0 < pl.L[0] && (int)g1 < pl.L[1] && (int)g2 < pl.L[2]) {
+            const uint32_t n = (g0 * pl.L[1] + g1) * pl.L[2] + g2;
+            z.x = G.u1(ld1(x1 + base + n), ld1(v + base + n), n);
+          }
+          const int j0 = mr_kidx(g0, pl.kind[0], pl.L[0], pl.P[0]);
+          const int j1 = mr_kidx(g1, pl.kind[1], pl.L[1], pl.P[1]);
+          const int j2 = mr_kidx(g2, pl.kind[2], pl.L[2], pl.P[2]);
+          if (j0 >= 0 && j1 >= 0 && j2 >= 0) z.y = ld1(kp + (j0 * pl.KL[1] + j1) * pl.KL[2] + j2);
         }
-        const int j0 = mr_kidx(g0, pl.kind[0], pl.L[0], pl.P[0]);
-        const int j1 = mr_kidx(g1, pl.kind[1], pl.L[1], pl.P[1]);
-        const int j2 = mr_kidx(g2, pl.kind[2], pl.L[2], pl.P[2]);
-        if (j0 >= 0 && j1 >= 0 && j2 >= 0) z.y = ld1(kl + (j0 * pl.KL[1] + j1) * pl.KL[2] + j2);
       }
     }
     src[f] = z;
@@ -281,7 +416,7 @@ __global__ void __launch_bounds__(NT)
   __syncthreads();
 
   // forward transforms of the 2 np images
-  mr_transform<NT>(src, dst, tw, pl, 2 * np * N, tid);
+  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, 2 * np * N, tid);
 
   // products of each pair, conjugated: conj(Ya + i Yb)
   {
@@ -294,11 +429,8 @@ __global__ void __launch_bounds__(NT)
       const uint32_t pm = (m0 * pl.P[1] + m1) * pl.P[2] + m2;
       const float2* za = src + 2 * q * N;
       const float2* zb = za + N;
-      const int64_t ia = img0 + 2 * q, ib = ia + 1;
-      const float Da = ld1(Dp + ia % C);
-      const float Db = ib < lines ? ld1(Dp + ib % C) : 0.f;
-      const float2 ya = mr_product(za[p], za[pm], Da, scale);
-      const float2 yb = mr_product(zb[p], zb[pm], Db, scale);
+      const float2 ya = mr_product(za[p], za[pm], Dl[2 * q], scale);
+      const float2 yb = mr_product(zb[p], zb[pm], Dl[2 * q + 1], scale);
       dst[f] = make_float2(ya.x - yb.y, -(ya.y + yb.x));
     }
     __syncthreads();
@@ -308,11 +440,12 @@ __global__ void __launch_bounds__(NT)
   }
 
   // one transform per pair: the conjugate of both inverses
-  mr_transform<NT>(src, dst, tw, pl, np * N, tid);
+  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, np * N, tid);
 
   // crop, outer gate, store: ya = Re, yb = -Im
-  for (uint32_t f = tid; f < (uint32_t)nimg * (uint32_t)pl.Ld; f += NT) {
-    const uint32_t i = fdiv(f, pl.dLd), n = f - i * (uint32_t)pl.Ld;
+  const Gates<ACT> G{};  // the outer gate depends on x2 only
+  for (uint32_t f = tid; f < nimg * Ld; f += NT) {
+    const uint32_t i = fdiv(f, pl.dLd), n = f - i * Ld;
     uint32_t p = n;
     if (!exact) {
       const uint32_t t = fdiv(n, pl.dL2), n2 = n - t * pl.L[2];
@@ -320,9 +453,7 @@ __global__ void __launch_bounds__(NT)
       p = (n0 * pl.P[1] + n1) * pl.P[2] + n2;
     }
     const float2 r = src[(i >> 1) * N + p];
-    const int64_t img = img0 + i;
-    const Gates<ACT> G = line_gates<ACT, TS>(ain, img, C);
-    const size_t o = (size_t)img * pl.Ld + n;
+    const size_t o = (size_t)i0 * Ld + f;
     st1(y + o, G.g1(ld1(x2 + o)) * ((i & 1) ? -r.y : r.x));
   }
 }
@@ -339,9 +470,55 @@ int64_t smooth7_ceil(int64_t n) {
   return n;
 }
 
+// twiddles, the two buffers of 2Q images' grids, D of the 2Q images
+size_t mr_lds_bytes(const MrPlan& pl, int Q) {
+  return ((size_t)pl.ntw + (size_t)4 * Q * pl.N) * sizeof(float2) + (size_t)2 * Q * sizeof(float);
+}
+
 int env_int(const char* name) {
   const char* e = getenv(name);
   return e ? (int)strtol(e, nullptr, 10) : 0;
+}
+
+// Passes of every axis with the radices of family f, the twiddle table layout.
+bool mr_passes(MrPlan* pl, int f) {
+  if (f < 0 || f >= kNumFam) return false;
+  int np = 0, tw = 0;
+  for (int d = 0; d < 3; ++d) {
+    const int P = pl->P[d];
+    if (P < 2) continue;
+    int S = 1;
+    for (int e = d + 1; e < 3; ++e) S *= pl->P[e];
+    pl->twoff[d] = tw;
+    tw += P;
+    int rest = P, ns = 1;
+    while (rest > 1) {
+      int r = 0;
+      for (int c : {16, 15, 14, 12, 10, 9, 8, 7, 5, 4, 3, 2})
+        if (fam_has(f, c) && rest % c == 0) {
+          r = c;
+          break;
+        }
+      if (r == 0 || np == kMrMaxPass) return false;
+      MrPass& ps = pl->pass[np++];
+      ps.r = r;
+      ps.q = P / r;
+      ps.ns = ns;
+      ps.sa = S;
+      ps.pasa = P * S;
+      ps.twoff = pl->twoff[d];
+      ps.twstep = P / (ns * r);
+      ps.dsa = make_fastdiv((uint32_t)S);
+      ps.dq = make_fastdiv((uint32_t)ps.q);
+      ps.dns = make_fastdiv((uint32_t)ns);
+      ns *= r;
+      rest /= r;
+    }
+  }
+  pl->npass = np;
+  pl->ntw = tw;
+  pl->fam = f;
+  return true;
 }
 
 // The plan of a call, or false where these kernels do not take it.
@@ -379,58 +556,44 @@ bool mixed_plan(const FftConvArgs& a, MrPlan* pl) {
   pl->N = (int)N;
   pl->Ld = (int)Ld;
   pl->Kd = (int)Kd;
-  // passes: each axis, radices 8, 4, 2, 7, 5, 3 in that order
-  int np = 0, tw = 0;
-  for (int d = 0; d < 3; ++d) {
-    const int P = pl->P[d];
-    if (P < 2) continue;
-    int S = 1;
-    for (int e = d + 1; e < 3; ++e) S *= pl->P[e];
-    pl->twoff[d] = tw;
-    tw += P;
-    int rest = P, ns = 1;
-    while (rest > 1) {
-      int r = 0;
-      for (int c : {8, 4, 2, 7, 5, 3})
-        if (rest % c == 0) {
-          r = c;
-          break;
-        }
-      if (r == 0 || np == kMrMaxPass) return false;
-      MrPass& ps = pl->pass[np++];
-      ps.r = r;
-      ps.q = P / r;
-      ps.ns = ns;
-      ps.sa = S;
-      ps.pasa = P * S;
-      ps.twoff = pl->twoff[d];
-      ps.twstep = P / (ns * r);
-      ps.dsa = make_fastdiv((uint32_t)S);
-      ps.dq = make_fastdiv((uint32_t)ps.q);
-      ps.dns = make_fastdiv((uint32_t)ns);
-      ns *= r;
-      rest /= r;
+  // passes: each axis, the largest radix of the family that divides what is
+  // left; the family with the fewest passes (ties: the lower family)
+  int best = -1;
+  for (int f = 0; f < kNumFam; ++f) {
+    MrPlan t = *pl;
+    if (!mr_passes(&t, f)) continue;
+    if (best < 0 || t.npass < pl->npass) {
+      *pl = t;
+      best = f;
     }
   }
-  pl->npass = np;
-  pl->ntw = tw;
-  // Lanes and image pairs per workgroup, from a sweep of 64 .. 1024 lanes and
-  // 1 .. 12 pairs on 14^2 to 48 x 64 grids and 300- and 1000-point lines
-  // (MI355X): about 3 points of the images' grids per lane below 512
-  // transform points, 6 from there, 1024 lanes on one pair from 1536 points.
+  if (best < 0) return false;
+  if (const char* e = getenv("HYENAND_MIXED_FAMILY")) {  // force a family (sweeps)
+    MrPlan t = *pl;
+    if (mr_passes(&t, (int)strtol(e, nullptr, 10))) *pl = t;
+  }
+  // Lanes and image pairs per workgroup, from sweeps of 256 .. 1024 lanes and
+  // 1 .. 8 pairs on 12- to 1000-point lines, 14^2 to 48 x 64 grids and 12^3
+  // (MI355X): about 3 points of the images' grids per lane below 256
+  // transform points and 6 from there, at least 512 workgroups where the
+  // lines allow, 256 lanes for groups of at most 768 points, one pair from
+  // 1536 points on 1024 lanes (512 for lines below 2560 points: 87 us against
+  // 120 for 64 x 64 lines of 2000).
   int nt = 512, Q = 1;
   if (pl->N < 1536) {
-    const int target = pl->N >= 512 ? 3072 : 1536;  // grid points per workgroup
+    const int target = pl->N >= 256 ? 3072 : 1536;  // grid points per workgroup
     Q = imax(1, (target + pl->N) / (2 * pl->N));
+    Q = imax(1, imin(Q, (int)(a.lines / 1024)));
+    if (2 * Q * pl->N <= 768) nt = 256;
   } else {
-    nt = 1024;
+    nt = (a.ndim == 1 && pl->N < 2560) ? 512 : 1024;
   }
   if (const int o = env_int("HYENAND_MIXED_PAIRS"); o > 0) Q = o;
-  if (const int o = env_int("HYENAND_MIXED_LANES"); o == 64 || o == 128 || o == 256 || o == 512 || o == 1024) nt = o;
+  if (const int o = env_int("HYENAND_MIXED_LANES"); o == 256 || o == 512 || o == 1024) nt = o;
   const int64_t pairs = (a.lines + 1) / 2;
   if (Q > pairs) Q = (int)pairs;
-  while (Q > 1 && ((size_t)pl->ntw + (size_t)4 * Q * pl->N) * sizeof(float2) > kMrMaxLds) --Q;
-  if (((size_t)pl->ntw + (size_t)4 * Q * pl->N) * sizeof(float2) > kMrMaxLds) return false;
+  while (Q > 1 && mr_lds_bytes(*pl, Q) > kMrMaxLds) --Q;
+  if (mr_lds_bytes(*pl, Q) > kMrMaxLds) return false;
   pl->Q = Q;
   pl->nt = nt;
   pl->dN = make_fastdiv((uint32_t)pl->N);
@@ -439,32 +602,44 @@ bool mixed_plan(const FftConvArgs& a, MrPlan* pl) {
   pl->dL1 = make_fastdiv((uint32_t)pl->L[1]);
   pl->dL2 = make_fastdiv((uint32_t)pl->L[2]);
   pl->dLd = make_fastdiv((uint32_t)pl->Ld);
+  pl->dC = make_fastdiv((uint32_t)a.C);
+  pl->dKC = make_fastdiv((uint32_t)(a.kC ? a.kC : 1));
   return true;
 }
 
-template <typename TS, bool ACT, int NT>
+template <typename TS, bool ACT, int NT, int FAM>
 hipError_t launch_mixed_t(const FftConvArgs& a, const MrPlan& pl, hipStream_t s) {
-  const size_t lds = ((size_t)pl.ntw + (size_t)4 * pl.Q * pl.N) * sizeof(float2);
+  const size_t lds = mr_lds_bytes(pl, pl.Q);
   const unsigned nblk = (unsigned)((a.lines + 2 * pl.Q - 1) / (2 * pl.Q));
   // the kernel may take more than the default 64 KB of dynamic LDS
   static std::once_flag once;
   static hipError_t attr = hipSuccess;
   std::call_once(once, [] {
-    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(conv_mixed<TS, ACT, NT>),
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(conv_mixed<TS, ACT, NT, FAM>),
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMrMaxLds);
   });
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((conv_mixed<TS, ACT, NT>), dim3(nblk), dim3(NT), lds, s, (const TS*)a.x1, (const TS*)a.x2,
-                     (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int64_t)a.lines, (int)a.C, a.kC,
+  hipLaunchKernelGGL((conv_mixed<TS, ACT, NT, FAM>), dim3(nblk), dim3(NT), lds, s, (const TS*)a.x1, (const TS*)a.x2,
+                     (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (TS*)a.y, (int)a.lines, (int)a.C, a.kC,
                      a.act_in, pl);
   return hipGetLastError();
 }
 
+template <int NT, int FAM>
+hipError_t launch_mixed_f(const FftConvArgs& a, const MrPlan& pl, hipStream_t s) {
+  if (a.bf16)
+    return a.act ? launch_mixed_t<uint16_t, true, NT, FAM>(a, pl, s) : launch_mixed_t<uint16_t, false, NT, FAM>(a, pl, s);
+  return a.act ? launch_mixed_t<float, true, NT, FAM>(a, pl, s) : launch_mixed_t<float, false, NT, FAM>(a, pl, s);
+}
+
 template <int NT>
 hipError_t launch_mixed_nt(const FftConvArgs& a, const MrPlan& pl, hipStream_t s) {
-  if (a.bf16)
-    return a.act ? launch_mixed_t<uint16_t, true, NT>(a, pl, s) : launch_mixed_t<uint16_t, false, NT>(a, pl, s);
-  return a.act ? launch_mixed_t<float, true, NT>(a, pl, s) : launch_mixed_t<float, false, NT>(a, pl, s);
+  switch (pl.fam) {
+    case 1: return launch_mixed_f<NT, 1>(a, pl, s);
+    case 2: return launch_mixed_f<NT, 2>(a, pl, s);
+    case 3: return launch_mixed_f<NT, 3>(a, pl, s);
+    default: return launch_mixed_f<NT, 0>(a, pl, s);
+  }
 }
 
 }  // namespace
@@ -476,13 +651,15 @@ bool mixed_supported(const FftConvArgs& a) {
 
 // Where these kernels beat the power-of-two ones (measured on the MI355X):
 // 3D grids (which those do not take), 2D grids up to 2048 transform points
-// (14 x 14: 14.7 us against 105 us for 16 x 384 images; 27 x 27 centred:
-// 44 us against 111 us) and larger ones with at most a quarter of the
-// power-of-two points (48 x 64: 21 us against 60 us; 48 x 80 at half: 91 us
-// against 62 us), lines of at most 128 points (64 x 256 lines of 12: 6.7 us
-// against 20.6 us; 64 x 64 of 100: 8.6 against 11.0) or a third of the
-// power-of-two points (300: 15.5 us against 17.9 us; 500 and 1000 at half:
-// 23.6 and 44 us against 20.5 and 40 us).
+// (14 x 14: 12.6 us against 106 us for 16 x 384 images; 27 x 27 centred:
+// 39 us against 111 us) and larger ones with at most a quarter of the
+// power-of-two points (48 x 64: 18.4 us against 60 us; 48 x 80 at half: 89 us
+// against 62 us), lines of at most 128 points (64 x 256 lines of 12: 6.1 us
+// against 20.6 us), of at most 1024 with half the power-of-two points (64 x 64
+// lines of 300, 500 and 1000: 13.4, 19.1 and 36.2 us against 17.4, 20.6 and
+// 40.0 us; 100-point linear lines on 200 points: 12.4 us against 10.6 on 256)
+// and longer ones with at most 5/12 of them (3000: 137 us against 158 us on
+// 8192 points; 2000: 87 us against 78 us on 4096).
 bool mixed_preferred(const FftConvArgs& a) {
   MrPlan pl;
   if (!mixed_plan(a, &pl)) return false;
@@ -490,15 +667,13 @@ bool mixed_preferred(const FftConvArgs& a) {
   for (int d = 0; d < a.ndim; ++d) pow2_points *= a.P[d];
   if (a.ndim == 3) return true;
   if (a.ndim == 2) return pl.N <= 2048 || 4 * (int64_t)pl.N <= pow2_points;
-  return pl.N <= 128 || 3 * (int64_t)pl.N <= pow2_points;
+  return pl.N <= 128 || (pl.N <= 1024 && 2 * (int64_t)pl.N <= pow2_points) || 12 * (int64_t)pl.N <= 5 * pow2_points;
 }
 
 hipError_t launch_mixed(const FftConvArgs& a, hipStream_t s) {
   MrPlan pl;
   if (!mixed_plan(a, &pl)) return hipErrorInvalidValue;
   switch (pl.nt) {
-    case 64: return launch_mixed_nt<64>(a, pl, s);
-    case 128: return launch_mixed_nt<128>(a, pl, s);
     case 512: return launch_mixed_nt<512>(a, pl, s);
     case 1024: return launch_mixed_nt<1024>(a, pl, s);
     default: return launch_mixed_nt<256>(a, pl, s);

@@ -83,8 +83,7 @@ def _mixed(nd):
     return {1: "mixed1d", 2: "mixed2d", 3: "mixed3d"}[nd]
 
 
-# circular extents with prime factors 2, 3, 5, 7, on their own points (lines:
-# the default where the power-of-two transform has 3 times the points)
+# circular extents with prime factors 2, 3, 5, 7, on their own points
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("L", [3, 5, 7, 12, 15, 100, 300, 1000, 3000])
 def test_1d_circular(L, dtype):
@@ -96,7 +95,9 @@ def test_1d_default_choice():
     assert H.plan_name((2, 3, 300), "circular", "f32") == "mixed1d"
     assert H.plan_name((2, 3, 5), "circular", "f32") == "mixed1d"
     assert H.plan_name((2, 3, 100), "circular", "f32") == "mixed1d"
-    assert H.plan_name((2, 3, 1000), "circular", "f32") == "fused1d_any"
+    assert H.plan_name((2, 3, 1000), "circular", "f32") == "mixed1d"
+    assert H.plan_name((2, 3, 67), "circular", "f32") == "fused1d_any"
+    assert H.plan_name((2, 3, 100), "linear", "f32") == "fused1d_any"
     _check("1d-default", 4, 16, (300,), "circular", "f32", 77)
 
 
@@ -136,6 +137,16 @@ def test_pairs_per_workgroup(pairs, lines):
     env = {"HYENAND_MIXED_PAIRS": pairs} if pairs else {}
     _check("pairs", lines[0], lines[1], (14, 14), "circular", "f32", 600 + pairs, **env)
     _check("pairs", lines[0], lines[1], (15,), "centered", "f32", 610 + pairs, HYENAND_PLAN="mixed", **env)
+
+
+# every radix family (the base radices 8, 7, 5, 4, 3, 2 and 14 + 12, 16 + 10,
+# 15 + 9), forced on grids whose axes factor differently under each
+@pytest.mark.parametrize("family", [0, 1, 2, 3])
+@pytest.mark.parametrize("grid,mode", [((30, 28), "circular"), ((720,), "circular"), ((12, 10, 9), "circular"),
+                                       ((14, 20), "centered"), ((2160,), "circular")])
+def test_radix_families(family, grid, mode):
+    assert _check("family", 2, 3, grid, mode, "f32", 800 + family, HYENAND_PLAN="mixed",
+                  HYENAND_MIXED_FAMILY=family) == _mixed(len(grid))
 
 
 @pytest.mark.parametrize("grid,mode", [((14, 14), "circular"), ((100,), "circular"), ((14, 14), "centered")])
