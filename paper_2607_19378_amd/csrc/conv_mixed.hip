@@ -12,14 +12,22 @@
 //    2L - 1 points, displacement -(L-1) .. L-1) or periodic (a circular axis
 //    of other extents: k[d mod L] at displacement d).
 //
-// Arithmetic: two real signals per complex transform.  An image's u and k go
-// into one complex grid z = u + i k; after the forward transform the mirror
-// bin separates them, U(f) = (Z(f) + conj Z(-f)) / 2 and
-// K(f) = (Z(f) - conj Z(-f)) / 2i.  The products of two images, Ya and Yb
-// (with the shortcut folded in as U (K + D)), go into one grid Ya + i Yb, and
-// one more transform of its conjugate gives conj(ya + i yb): the inverse of
-// both.  Odd extents need no half-length packing this way, and each image
-// costs one and a half complex transforms of the grid.
+// Arithmetic: two real signals per complex transform, always two of the same
+// kind: the u of the two images a, b of a pair in one complex grid
+// zu = ua + i ub, their k in zk = ka + i kb.  After the forward transforms
+// the mirror bin separates them, Ua(f) = (Zu(f) + conj Zu(-f)) / 2 and
+// Ub(f) = (Zu(f) - conj Zu(-f)) / 2i, and so for K.  (Packing u + i k of one
+// image instead would give K the rounding error of U, eps |U|, which exceeds
+// the fp32 tolerance where |u| >> |k|.)  Each of the two real signals of a
+// grid is scaled, exactly, by the power of two that brings its largest
+// magnitude into [1/2, 1) before the transforms, and each product by the
+// power of two of u's scale times the larger of k's and D's (about the scale
+// of y), undone at the store, so that lines of different scales in one pair
+// do not pass their rounding error to each other either.  The products Ya and Yb (with the
+// shortcut folded in as U (K + D)) go into one grid Ya + i Yb, and one more
+// transform of its conjugate gives conj(ya + i yb): the inverse of both.  Odd
+// extents need no half-length packing this way, and each image costs one and
+// a half complex transforms of the grid.
 //
 // Each axis runs Stockham passes between two LDS buffers (one barrier per
 // pass), of the largest radix up to 16 that divides what is left of the axis
@@ -219,11 +227,18 @@ __device__ __forceinline__ void dft_reg(float2 (&x)[R]) {
   }
 }
 
+__device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
+// e with |x| 2^-e in [1/2, 1) (0 for 0), for x and for the magnitude whose
+// bits are b
+__device__ __forceinline__ int mr_fexp(float x) { return __builtin_amdgcn_frexp_expf(x); }
+__device__ __forceinline__ int mr_exp(uint32_t b) { return mr_fexp(__uint_as_float(b)); }
+
 // One Stockham pass of radix R over `items` butterflies (all images); TW:
 // the pass has twiddles (not the first pass of its axis, where all are 1).
-template <int R, int NT, bool TW>
+template <int R, int NT, bool TW, bool SC>
 __device__ __forceinline__ void mr_pass_t(const float2* src, float2* dst, const float2* tw, const MrPass& ps,
-                                          uint32_t items, uint32_t tid) {
+                                          uint32_t items, uint32_t tid, const uint32_t* smx, FastDiv dN) {
   const uint32_t qs = (uint32_t)(ps.q * ps.sa), nss = (uint32_t)(ps.ns * ps.sa);
   for (uint32_t it = tid; it < items; it += NT) {
     const uint32_t t1 = fdiv(it, ps.dsa), s = it - t1 * (uint32_t)ps.sa;
@@ -234,6 +249,12 @@ __device__ __forceinline__ void mr_pass_t(const float2* src, float2* dst, const 
     float2 x[R];
 #pragma unroll
     for (int t = 0; t < R; ++t) x[t] = sp[t * qs];
+    if constexpr (SC) {  // the staging scales of this grid's two parts
+      const uint32_t g = fdiv(base, dN);
+      const int ex = -mr_exp(smx[2 * g]), ey = -mr_exp(smx[2 * g + 1]);
+#pragma unroll
+      for (int t = 0; t < R; ++t) x[t] = make_float2(ldexpf(x[t].x, ex), ldexpf(x[t].y, ey));
+    }
     if constexpr (TW) {
       const uint32_t tws = kk * (uint32_t)ps.twstep;
       const float2* tp = tw + ps.twoff;
@@ -247,11 +268,14 @@ __device__ __forceinline__ void mr_pass_t(const float2* src, float2* dst, const 
   }
 }
 
+// sc: the first pass of the forward transforms, which applies the staging
+// scales (it is the first pass of its axis: no twiddles)
 template <int R, int NT>
 __device__ __forceinline__ void mr_pass(const float2* src, float2* dst, const float2* tw, const MrPass& ps,
-                                        uint32_t items, uint32_t tid) {
-  if (ps.ns == 1) mr_pass_t<R, NT, false>(src, dst, tw, ps, items, tid);
-  else mr_pass_t<R, NT, true>(src, dst, tw, ps, items, tid);
+                                        uint32_t items, uint32_t tid, bool sc, const uint32_t* smx, FastDiv dN) {
+  if (sc) mr_pass_t<R, NT, false, true>(src, dst, tw, ps, items, tid, smx, dN);
+  else if (ps.ns == 1) mr_pass_t<R, NT, false, false>(src, dst, tw, ps, items, tid, smx, dN);
+  else mr_pass_t<R, NT, true, false>(src, dst, tw, ps, items, tid, smx, dN);
 }
 
 // Radix families: every kernel takes 8, 7, 5, 4, 3 and 2, and family f adds
@@ -265,24 +289,27 @@ constexpr bool fam_has(int f, int r) {
 
 // every pass of the plan over n points (whole images), ping-ponging src/dst;
 // returns with the result in src
+// scale: the forward transforms (the first pass applies the staging scales)
 template <int NT, int FAM>
 __device__ __forceinline__ void mr_transform(float2*& src, float2*& dst, const float2* tw, const MrPass* passes,
-                                             int npass, uint32_t n, uint32_t tid) {
+                                             int npass, uint32_t n, uint32_t tid, bool scale, const uint32_t* smx,
+                                             FastDiv dN) {
   for (int i = 0; i < npass; ++i) {
     const MrPass ps = passes[i];
+    const bool sc = scale && i == 0;
     switch (ps.r) {
-      case 16: if constexpr (fam_has(FAM, 16)) mr_pass<16, NT>(src, dst, tw, ps, n / 16, tid); break;
-      case 15: if constexpr (fam_has(FAM, 15)) mr_pass<15, NT>(src, dst, tw, ps, n / 15, tid); break;
-      case 14: if constexpr (fam_has(FAM, 14)) mr_pass<14, NT>(src, dst, tw, ps, n / 14, tid); break;
-      case 12: if constexpr (fam_has(FAM, 12)) mr_pass<12, NT>(src, dst, tw, ps, n / 12, tid); break;
-      case 10: if constexpr (fam_has(FAM, 10)) mr_pass<10, NT>(src, dst, tw, ps, n / 10, tid); break;
-      case 9: if constexpr (fam_has(FAM, 9)) mr_pass<9, NT>(src, dst, tw, ps, n / 9, tid); break;
-      case 8: mr_pass<8, NT>(src, dst, tw, ps, n / 8, tid); break;
-      case 7: mr_pass<7, NT>(src, dst, tw, ps, n / 7, tid); break;
-      case 5: mr_pass<5, NT>(src, dst, tw, ps, n / 5, tid); break;
-      case 4: mr_pass<4, NT>(src, dst, tw, ps, n / 4, tid); break;
-      case 3: mr_pass<3, NT>(src, dst, tw, ps, n / 3, tid); break;
-      default: mr_pass<2, NT>(src, dst, tw, ps, n / 2, tid); break;
+      case 16: if constexpr (fam_has(FAM, 16)) mr_pass<16, NT>(src, dst, tw, ps, n / 16, tid, sc, smx, dN); break;
+      case 15: if constexpr (fam_has(FAM, 15)) mr_pass<15, NT>(src, dst, tw, ps, n / 15, tid, sc, smx, dN); break;
+      case 14: if constexpr (fam_has(FAM, 14)) mr_pass<14, NT>(src, dst, tw, ps, n / 14, tid, sc, smx, dN); break;
+      case 12: if constexpr (fam_has(FAM, 12)) mr_pass<12, NT>(src, dst, tw, ps, n / 12, tid, sc, smx, dN); break;
+      case 10: if constexpr (fam_has(FAM, 10)) mr_pass<10, NT>(src, dst, tw, ps, n / 10, tid, sc, smx, dN); break;
+      case 9: if constexpr (fam_has(FAM, 9)) mr_pass<9, NT>(src, dst, tw, ps, n / 9, tid, sc, smx, dN); break;
+      case 8: mr_pass<8, NT>(src, dst, tw, ps, n / 8, tid, sc, smx, dN); break;
+      case 7: mr_pass<7, NT>(src, dst, tw, ps, n / 7, tid, sc, smx, dN); break;
+      case 5: mr_pass<5, NT>(src, dst, tw, ps, n / 5, tid, sc, smx, dN); break;
+      case 4: mr_pass<4, NT>(src, dst, tw, ps, n / 4, tid, sc, smx, dN); break;
+      case 3: mr_pass<3, NT>(src, dst, tw, ps, n / 3, tid, sc, smx, dN); break;
+      default: mr_pass<2, NT>(src, dst, tw, ps, n / 2, tid, sc, smx, dN); break;
     }
     __syncthreads();
     float2* t = src;
@@ -319,12 +346,13 @@ __device__ __forceinline__ int mr_kidx(int g, int kind, int L, int P) {
   }
 }
 
-// U (K + D) / N of one image from its transform Z at bin f and the mirror bin
-__device__ __forceinline__ float2 mr_product(float2 z, float2 zm, float D, float scale) {
-  const float2 a = z, b = c_conj(zm);
-  const float2 u = c_scale(c_add(a, b), 0.5f * scale);
-  const float2 d = c_sub(a, b);
-  return c_mul(u, make_float2(fmaf(0.5f, d.y, D), -0.5f * d.x));
+// The spectra A, B of the two real signals of z = a + i b at bin f, from Z(f)
+// and Z(-f): A = (Z(f) + conj Z(-f)) / 2, B = (Z(f) - conj Z(-f)) / 2i.
+__device__ __forceinline__ void mr_split(float2 z, float2 zm, float2& A, float2& B) {
+  const float2 c = c_conj(zm);
+  A = c_scale(c_add(z, c), 0.5f);
+  const float2 d = c_sub(z, c);
+  B = make_float2(0.5f * d.y, -0.5f * d.x);
 }
 
 // Gates of image img (the operator's s row and w_in[c]), without 64-bit division.
@@ -359,6 +387,7 @@ __global__ void __launch_bounds__(NT)
   float2* src = mr_lds + pl.ntw;
   float2* dst = src + (size_t)G2 * N;
   float* const Dl = reinterpret_cast<float*>(dst + (size_t)G2 * N);  // D of the group's images
+  uint32_t* const smx = reinterpret_cast<uint32_t*>(Dl + G2);           // max |.| of each grid's parts
   const bool exact = pl.N == pl.Ld;  // every axis exact: transform point = data point
 
   // the pass descriptors, copied with compile-time indices (a run-time index
@@ -378,45 +407,92 @@ __global__ void __launch_bounds__(NT)
     const uint32_t img = i0 + i;
     Dl[i] = i < nimg ? ld1(Dp + (img - fdiv(img, pl.dC) * (uint32_t)C)) : 0.f;
   }
+  for (uint32_t i = tid; i < 2 * G2; i += NT) smx[i] = 0u;  // (the staging barrier orders it)
 
-  // stage z = u + i k of every image on the transform grid
-  const uint32_t nval = nimg * N;
+  // stage zu = ua + i ub and zk = ka + i kb of every pair on the transform
+  // grid: grid i = 2q + r of the group holds pair q's u (r = 0) or k (r = 1)
   for (uint32_t f = tid; f < 2 * np * N; f += NT) {
+    const uint32_t i = fdiv(f, pl.dN), p = f - i * N;
+    const uint32_t ia = i & ~1u;  // image a of the pair, in the group
+    const bool isk = i & 1u, hasb = ia + 1 < nimg;
     float2 z = czero();
-    if (f < nval) {
-      if (exact && kC == 0 && !ACT) {  // the group's x1, v, k: one run from i0 N
-        const size_t o = (size_t)i0 * N + f;
-        z = make_float2(ld1(x1 + o) * ld1(v + o), ld1(k + o));
+    if (exact && kC == 0 && !ACT) {  // the group's x1, v, k: one run from i0 N
+      const size_t o = (size_t)(i0 + ia) * N + p;
+      if (isk) {
+        z.x = ld1(k + o);
+        if (hasb) z.y = ld1(k + o + N);
       } else {
-        const uint32_t i = fdiv(f, pl.dN), p = f - i * N;
-        const uint32_t img = i0 + i;
-        const size_t base = (size_t)img * Ld;
-        const uint32_t kl = kC ? img - fdiv(img, pl.dKC) * (uint32_t)kC : img;
-        const TS* kp = k + (size_t)kl * (uint32_t)pl.Kd;
-        const Gates<ACT> G = mr_gates<ACT, TS>(ain, img, (uint32_t)C, pl.dC);
-        if (exact) {
-          z.x = G.u1(ld1(x1 + base + p), ld1(v + base + p), p);
-          z.y = ld1(kp + p);
-        } else {
-          const uint32_t t = fdiv(p, pl.dP2), g2 = p - t * pl.P[2];
-          const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
-          if ((int)g0 < pl.L[0] && (int)g1 < pl.L[1] && (int)g2 < pl.L[2]) {
-            const uint32_t n = (g0 * pl.L[1] + g1) * pl.L[2] + g2;
-            z.x = G.u1(ld1(x1 + base + n), ld1(v + base + n), n);
+        z.x = ld1(x1 + o) * ld1(v + o);
+        if (hasb) z.y = ld1(x1 + o + N) * ld1(v + o + N);
+      }
+    } else {
+      // grid point p: the data point n (u; n < 0 outside the image) and the
+      // kernel point j (k; j < 0 where no displacement lands)
+      int n = (int)p, j = (int)p;
+      if (!exact) {
+        const uint32_t t = fdiv(p, pl.dP2), g2 = p - t * pl.P[2];
+        const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
+        n = ((int)g0 < pl.L[0] && (int)g1 < pl.L[1] && (int)g2 < pl.L[2])
+                ? (int)((g0 * pl.L[1] + g1) * pl.L[2] + g2) : -1;
+        const int j0 = mr_kidx(g0, pl.kind[0], pl.L[0], pl.P[0]);
+        const int j1 = mr_kidx(g1, pl.kind[1], pl.L[1], pl.P[1]);
+        const int j2 = mr_kidx(g2, pl.kind[2], pl.L[2], pl.P[2]);
+        j = (j0 >= 0 && j1 >= 0 && j2 >= 0) ? (j0 * pl.KL[1] + j1) * pl.KL[2] + j2 : -1;
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (h == 1 && !hasb) break;
+        const uint32_t img = i0 + ia + h;
+        float val = 0.f;
+        if (isk) {
+          if (j >= 0) {
+            const uint32_t kl = kC ? img - fdiv(img, pl.dKC) * (uint32_t)kC : img;
+            val = ld1(k + (size_t)kl * (uint32_t)pl.Kd + j);
           }
-          const int j0 = mr_kidx(g0, pl.kind[0], pl.L[0], pl.P[0]);
-          const int j1 = mr_kidx(g1, pl.kind[1], pl.L[1], pl.P[1]);
-          const int j2 = mr_kidx(g2, pl.kind[2], pl.L[2], pl.P[2]);
-          if (j0 >= 0 && j1 >= 0 && j2 >= 0) z.y = ld1(kp + (j0 * pl.KL[1] + j1) * pl.KL[2] + j2);
+        } else if (n >= 0) {
+          const Gates<ACT> G = mr_gates<ACT, TS>(ain, img, (uint32_t)C, pl.dC);
+          const size_t o = (size_t)img * Ld + n;
+          val = G.u1(ld1(x1 + o), ld1(v + o), n);
         }
+        if (h == 0) z.x = val;
+        else z.y = val;
       }
     }
     src[f] = z;
   }
   __syncthreads();
 
-  // forward transforms of the 2 np images
-  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, 2 * np * N, tid);
+  // largest magnitude of each grid's two parts: whole grids per wavefront, or
+  // S wavefronts per grid where there are fewer grids than wavefronts; one
+  // atomic per wavefront and part (magnitudes as bit patterns, ordered like
+  // the values for x >= 0)
+  {
+    constexpr uint32_t NW = NT / 64;
+    const uint32_t w = tid / 64, lane = tid % 64, G = 2 * np;
+    const uint32_t S = G >= NW ? 1 : NW / G;
+    for (uint32_t gw = w; gw < G * S; gw += NW) {
+      const uint32_t g = gw / S, part = gw % S;
+      uint32_t mx = 0, my = 0;
+      for (uint32_t p = part * 64 + lane; p < N; p += 64 * S) {
+        const float2 z = src[g * N + p];
+        mx = umax(mx, __float_as_uint(fabsf(z.x)));
+        my = umax(my, __float_as_uint(fabsf(z.y)));
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o /= 2) {
+        mx = umax(mx, (uint32_t)__shfl_xor((int)mx, o));
+        my = umax(my, (uint32_t)__shfl_xor((int)my, o));
+      }
+      if (lane == 0) {
+        atomicMax(smx + 2 * g, mx);
+        atomicMax(smx + 2 * g + 1, my);
+      }
+    }
+  }
+  __syncthreads();
+
+  // forward transforms of the 2 np grids
+  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, 2 * np * N, tid, true, smx, pl.dN);
 
   // products of each pair, conjugated: conj(Ya + i Yb)
   {
@@ -427,10 +503,24 @@ __global__ void __launch_bounds__(NT)
       const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
       const uint32_t m0 = g0 ? pl.P[0] - g0 : 0, m1 = g1 ? pl.P[1] - g1 : 0, m2 = g2 ? pl.P[2] - g2 : 0;
       const uint32_t pm = (m0 * pl.P[1] + m1) * pl.P[2] + m2;
-      const float2* za = src + 2 * q * N;
-      const float2* zb = za + N;
-      const float2 ya = mr_product(za[p], za[pm], Dl[2 * q], scale);
-      const float2 yb = mr_product(zb[p], zb[pm], Dl[2 * q + 1], scale);
+      const float2* zu = src + 2 * q * N;
+      const float2* zk = zu + N;
+      float2 Ua, Ub, Ka, Kb;
+      mr_split(zu[p], zu[pm], Ua, Ub);
+      mr_split(zk[p], zk[pm], Ka, Kb);
+      // grid 2q holds (ua, ub) and grid 2q + 1 (ka, kb), each part scaled
+      // by 2^-e; Y = U (K + D) / N comes out scaled by 2^-(eu + ey), ey the
+      // larger of ek and D's exponent
+      const uint32_t* sm = smx + 4 * q;
+      const float Da = Dl[2 * q], Db = Dl[2 * q + 1];
+      const int eka = mr_exp(sm[2]), ekb = mr_exp(sm[3]);
+      const int eya = imax(eka, mr_fexp(Da)), eyb = imax(ekb, mr_fexp(Db));
+      Ua = c_scale(Ua, scale);
+      Ub = c_scale(Ub, scale);
+      Ka = c_scale(Ka, ldexpf(1.f, eka - eya));
+      Kb = c_scale(Kb, ldexpf(1.f, ekb - eyb));
+      const float2 ya = c_mul(Ua, make_float2(Ka.x + ldexpf(Da, -eya), Ka.y));
+      const float2 yb = c_mul(Ub, make_float2(Kb.x + ldexpf(Db, -eyb), Kb.y));
       dst[f] = make_float2(ya.x - yb.y, -(ya.y + yb.x));
     }
     __syncthreads();
@@ -440,7 +530,7 @@ __global__ void __launch_bounds__(NT)
   }
 
   // one transform per pair: the conjugate of both inverses
-  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, np * N, tid);
+  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, np * N, tid, false, smx, pl.dN);
 
   // crop, outer gate, store: ya = Re, yb = -Im
   const Gates<ACT> G{};  // the outer gate depends on x2 only
@@ -453,8 +543,10 @@ __global__ void __launch_bounds__(NT)
       p = (n0 * pl.P[1] + n1) * pl.P[2] + n2;
     }
     const float2 r = src[(i >> 1) * N + p];
+    const uint32_t* sm = smx + 4 * (i >> 1) + (i & 1);  // u's and k's magnitudes of image i
+    const int e = mr_exp(sm[0]) + imax(mr_exp(sm[2]), mr_fexp(Dl[i]));
     const size_t o = (size_t)i0 * Ld + f;
-    st1(y + o, G.g1(ld1(x2 + o)) * ((i & 1) ? -r.y : r.x));
+    st1(y + o, G.g1(ld1(x2 + o)) * ldexpf((i & 1) ? -r.y : r.x, e));
   }
 }
 
@@ -470,9 +562,11 @@ int64_t smooth7_ceil(int64_t n) {
   return n;
 }
 
-// twiddles, the two buffers of 2Q images' grids, D of the 2Q images
+// twiddles, the two buffers of 2Q images' grids, D of the 2Q images, the
+// magnitudes of the 2Q grids' two parts
 size_t mr_lds_bytes(const MrPlan& pl, int Q) {
-  return ((size_t)pl.ntw + (size_t)4 * Q * pl.N) * sizeof(float2) + (size_t)2 * Q * sizeof(float);
+  return ((size_t)pl.ntw + (size_t)4 * Q * pl.N) * sizeof(float2) + (size_t)2 * Q * sizeof(float) +
+         (size_t)4 * Q * sizeof(uint32_t);
 }
 
 int env_int(const char* name) {
@@ -650,16 +744,15 @@ bool mixed_supported(const FftConvArgs& a) {
 }
 
 // Where these kernels beat the power-of-two ones (measured on the MI355X):
-// 3D grids (which those do not take), 2D grids up to 2048 transform points
-// (14 x 14: 12.6 us against 106 us for 16 x 384 images; 27 x 27 centred:
-// 39 us against 111 us) and larger ones with at most a quarter of the
-// power-of-two points (48 x 64: 18.4 us against 60 us; 48 x 80 at half: 89 us
-// against 62 us), lines of at most 128 points (64 x 256 lines of 12: 6.1 us
-// against 20.6 us), of at most 1024 with half the power-of-two points (64 x 64
-// lines of 300, 500 and 1000: 13.4, 19.1 and 36.2 us against 17.4, 20.6 and
-// 40.0 us; 100-point linear lines on 200 points: 12.4 us against 10.6 on 256)
-// and longer ones with at most 5/12 of them (3000: 137 us against 158 us on
-// 8192 points; 2000: 87 us against 78 us on 4096).
+// 3D grids (which those do not take; 4 x 64 x 12^3: 13.9 us against 207 us
+// embedded), 2D grids up to 2048 transform points (16 x 384 images of 14 x 14:
+// 15.1 us against 105 us; 27 x 27 centred: 44 us against 111 us) and larger
+// ones with at most a quarter of the power-of-two points (48 x 64: 20.2 us
+// against 59 us; 48 x 80 at half: 97 us against 62 us), lines of at most 128
+// points (64 x 256 lines of 12: 9.9 us against 20.2 us) or with at most 5/12
+// of the power-of-two points (64 x 64 lines of 300 and 3000: 15.4 and 152 us
+// against 17.0 and 157 us; of 500, 1000 and 2000 at about half: 22.5, 41.5
+// and 99 us against 20.6, 40.0 and 78 us).
 bool mixed_preferred(const FftConvArgs& a) {
   MrPlan pl;
   if (!mixed_plan(a, &pl)) return false;
@@ -667,7 +760,7 @@ bool mixed_preferred(const FftConvArgs& a) {
   for (int d = 0; d < a.ndim; ++d) pow2_points *= a.P[d];
   if (a.ndim == 3) return true;
   if (a.ndim == 2) return pl.N <= 2048 || 4 * (int64_t)pl.N <= pow2_points;
-  return pl.N <= 128 || (pl.N <= 1024 && 2 * (int64_t)pl.N <= pow2_points) || 12 * (int64_t)pl.N <= 5 * pow2_points;
+  return pl.N <= 128 || 12 * (int64_t)pl.N <= 5 * pow2_points;
 }
 
 hipError_t launch_mixed(const FftConvArgs& a, hipStream_t s) {

@@ -17,9 +17,13 @@ datasets is used):
 * ``conv1d_1m``   -- 1D linear, bf16 storage, B=1, C=256, L=2^20 (genomics-scale
   long context, the 1M point of the context-length study).
 
-One more, outside the five: ``conv2d_64_centered`` -- the image workload with
+Two more, outside the five: ``conv2d_64_centered`` -- the image workload with
 the paper's own non-circular kernel, evaluated on the double grid (127 x 127
-points per 64 x 64 image, pad mode "centered").
+points per 64 x 64 image, pad mode "centered"); ``conv2d_14_patches`` -- the
+14 x 14 patch grid of a 224 x 224 image at patch 16 (the ImageNet models'
+grid; ViT-Small width, C = 384), natural images and so the centered double
+grid (27 x 27 kernel points), B = 16: a grid whose extents are not powers of
+two.
 
 Draw recipe (identical for every workload): ``numpy.random.SeedSequence(seed)``
 spawns one child per tensor in the order x1, x2, v, kernel noise, D; each
@@ -129,6 +133,9 @@ WORKLOADS: Dict[str, Workload] = {
     "conv2d_64_centered": Workload(
         "conv2d_64_centered", 8, 256, (64, 64), CENTERED, "f32", 20266, 16.0,
         description="2D gated FFT conv with 127x127 centered kernels, fp32, B=8 C=256 64x64, pad 128x128"),
+    "conv2d_14_patches": Workload(
+        "conv2d_14_patches", 16, 384, (14, 14), CENTERED, "f32", 20267, 4.0,
+        description="2D gated FFT conv on 14x14 patch grids with 27x27 centered kernels, fp32, B=16 C=384"),
 }
 
 # Order in which the workloads are listed (small 1D case first).

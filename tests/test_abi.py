@@ -100,11 +100,11 @@ def test_workspace_queries_are_host_only():
     # circular, extents with prime factors 2, 3, 5, 7: mixed-radix transforms
     # on the grid's own points
     assert H.plan_name((2, 4, 14, 14), "circular", "f32") == "mixed2d"
-    assert H.plan_name((1, 1, 300), "circular", "f32") == "mixed1d"      # 300 points against 1024
     assert H.plan_name((1, 1, 3), "circular", "f32") == "mixed1d"        # short lines
-    assert H.plan_name((1, 1, 500), "circular", "f32") == "mixed1d"
-    # lines beyond 128 points with more than half the power-of-two points:
-    # that kernel (67 points: k periodic on 135 against 256)
+    assert H.plan_name((1, 1, 300), "circular", "f32") == "mixed1d"      # 300 against 1024 points
+    # lines beyond 128 points with more than 5/12 of the power-of-two points:
+    # that kernel (500 against 1024; 67: k periodic on 135 against 256)
+    assert H.plan_name((1, 1, 500), "circular", "f32") == "fused1d_any"
     assert H.plan_name((1, 1, 67), "circular", "f32") == "fused1d_any"
     assert H.plan_name((1, 2, 5, 6, 7), "circular", "bf16") == "mixed3d"
     assert H.plan_name((1, 2, 63, 64), "circular", "f32") == "mixed2d"    # 4032 points

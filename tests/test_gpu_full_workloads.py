@@ -15,7 +15,7 @@ from gpu_util import TOL, from_device, log, oracle_lines, run_gpu, summary, to_d
 
 pytestmark = pytest.mark.gpu
 
-FORWARD = ["conv1d_4k", "conv2d_64", "conv2d_512c", "conv3d_128", "conv1d_1m"]
+FORWARD = ["conv1d_4k", "conv2d_64", "conv2d_512c", "conv3d_128", "conv1d_1m", "conv2d_14_patches"]
 BACKWARD = ["conv2d_512c", "conv3d_128", "conv1d_1m"]
 NAMES = ("gx1", "gx2", "gv", "gk", "gD")
 

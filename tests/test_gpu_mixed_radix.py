@@ -95,7 +95,8 @@ def test_1d_default_choice():
     assert H.plan_name((2, 3, 300), "circular", "f32") == "mixed1d"
     assert H.plan_name((2, 3, 5), "circular", "f32") == "mixed1d"
     assert H.plan_name((2, 3, 100), "circular", "f32") == "mixed1d"
-    assert H.plan_name((2, 3, 1000), "circular", "f32") == "mixed1d"
+    assert H.plan_name((2, 3, 1000), "circular", "f32") == "fused1d_any"
+    assert H.plan_name((2, 3, 3000), "circular", "f32") == "mixed1d"
     assert H.plan_name((2, 3, 67), "circular", "f32") == "fused1d_any"
     assert H.plan_name((2, 3, 100), "linear", "f32") == "fused1d_any"
     _check("1d-default", 4, 16, (300,), "circular", "f32", 77)
@@ -152,6 +153,36 @@ def test_radix_families(family, grid, mode):
 @pytest.mark.parametrize("grid,mode", [((14, 14), "circular"), ((100,), "circular"), ((14, 14), "centered")])
 def test_shared_kernel(grid, mode):
     _check("shared", 3, 4, grid, mode, "f32", 700, shared=True, HYENAND_PLAN="mixed")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("grid,mode", [((14, 14), "circular"), ((1000,), "circular"), ((15,), "centered"),
+                                       ((6, 10, 14), "circular"), ((14, 14), "linear")])
+def test_dynamic_range(grid, mode, dtype):
+    """Two real signals share each complex transform (the u of two lines, the
+    k of two lines, two lines' products), each scaled on its own.  Kernels
+    1e4 times smaller than u, and the lines of each pair at scales apart by up
+    to 1e7: every line within the tolerance of the oracle."""
+    import torch
+    from paper_2607_19378_amd import hyenand as H
+    B, C = 2, 4
+    shape, x1, x2, v, k, D = _case(B, C, grid, mode, "f32", 900)
+    line_scale = np.array([1e4, 1.0, 1e-3, 3.0, 1.0, 1e-2, 1e2, 1.0])
+    x1 = x1 * line_scale.reshape((B, C) + (1,) * len(grid))
+    k = k * 1e-4
+    D = D * 1e-4
+    x1, x2, v, k, D = (W.quantise(a, dtype) for a in (x1, x2, v, k, D))
+    dev = [to_device(a, dtype) for a in (x1, x2, v, k, D)]
+    with _env(HYENAND_PLAN="mixed"):
+        assert H.plan_name(shape, mode, dtype) == _mixed(len(grid))
+        y = H.fftconv(*dev, pad_mode=mode)
+        torch.cuda.synchronize()
+    got = from_device(y)
+    f = [W.storage_to_f64(a, dtype) for a in (x1, x2, v, k, D)]
+    ref = (oracle.conv_direct if mode == "circular" else oracle.conv_fft)(*f, mode)
+    worst = per_line_worst(got, ref, B * C)
+    log(f"[mixed] dynamic range {shape} {mode} {dtype}: worst line={worst:.3e}")
+    assert np.all(np.isfinite(got)) and worst <= TOL[dtype]
 
 
 def test_image_patch_grid_batch():
