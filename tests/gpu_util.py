@@ -85,7 +85,7 @@ def oracle_lines(inp, lines):
     lines = np.asarray(lines, dtype=np.int64)
     sub = []
     for a in (inp.x1, inp.x2, inp.v, inp.k):
-        flat = a.reshape((nl,) + tuple(w.grid))[lines]
+        flat = a.reshape((nl,) + tuple(a.shape[2:]))[lines]  # k: the double grid when centered
         sub.append(W.storage_to_f64(flat, w.dtype)[None])
     Dsub = W.storage_to_f64(inp.D, w.dtype)[lines % w.C]
     return oracle.conv_fft(sub[0], sub[1], sub[2], sub[3], Dsub, w.pad_mode)[0]
