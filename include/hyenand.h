@@ -295,13 +295,16 @@ hyenand_status hyenand_fftconv_plan_name(int ndim, const int64_t* dims, hyenand_
  * Centred mode (k and gk [B, C, 2 L1 - 1, ...], gu[j] = sum_n k[n - j +
  * (L - 1)] h[n] + D h[j], gk[i] = sum_n h[n] u[n - i + (L - 1)]) and
  * extents that are not powers of two: both are circular convolutions on
- * their transform grid (a power of two >= 2 L_d - 1 per axis) once u is
- * zero-padded and k placed at its displacements, so the library embeds x1,
- * x2, v, gy and k in that grid, runs the circular backward there and
- * extracts the gradients.  The workspace then starts with the nine embedded
- * tensors (each B * C * prod P elements of dtype, 256-byte aligned); the
- * workspace queries include them.  Extents that are not powers of two may
- * also be 3D here.
+ * their transform grid once u is zero-padded and k placed at its
+ * displacements.  Extents that are not powers of two run in one pass on the
+ * forward's mixed-radix grid where it fits (about 3000 transform points per
+ * image; the workspace holds the gD sums only).  The other shapes, and the
+ * centred mode on power-of-two extents, are embedded: the library copies x1,
+ * x2, v, gy and k into the transform grid (a power of two >= 2 L_d - 1 per
+ * axis), runs the circular backward there and extracts the gradients.  The
+ * workspace then starts with the nine embedded tensors (each B * C * prod P
+ * elements of dtype, 256-byte aligned); the workspace queries include them.
+ * Extents that are not powers of two may also be 3D here.
  */
 hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const void* v, const void* k,
                                         const void* D, const void* gy, void* gx1, void* gx2, void* gv,

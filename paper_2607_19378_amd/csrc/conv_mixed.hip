@@ -89,7 +89,7 @@ struct MrPlan {
   int nt;         // lanes per workgroup
   int fam;        // radix family of the passes
   int npass;      // forward passes; the inverse runs the same list
-  FastDiv dN, dP1, dP2, dL1, dL2, dLd, dC, dKC;
+  FastDiv dN, dP1, dP2, dL1, dL2, dLd, dC, dKC, dKL1, dKL2, dKd;
   MrPass pass[kMrMaxPass];
 };
 
@@ -550,6 +550,251 @@ __global__ void __launch_bounds__(NT)
   }
 }
 
+// ---------------------------------------------------------------------------
+// Backward (hyenand_fftconv_backward) on the same transform grid.  With
+// u = x1 v and h = gy x2, zero outside the image, and k at its
+// displacements, the convolution is circular on the grid, so per bin
+//   Z = U (K + D)           z = k conv u + D u       -> gx2 = gy z
+//   Gu = H (conj K + D)     gu, the adjoint applied  -> gx1 = gu v, gv = gu x1
+//   Gk = H conj U           gk at the displacements of k's points (both
+//                           displacements of a periodic axis' point summed)
+// and gD[c] = sum over the samples and points of h u (one fp32 sum per line,
+// added over the samples in order afterwards).  A pair of images has three
+// staged grids, u, k and h (grid 3q + 0, 1, 2: a's part real, b's
+// imaginary), and three products, each scaled as in the forward (Z by
+// 2^-(eu + ey), Gu by 2^-(eh + ey), Gk by 2^-(eh + eu)).
+// ---------------------------------------------------------------------------
+
+// grid coordinate(s) on one axis of kernel index j: one, or two for a
+// periodic axis (displacements j and j - L); returns how many
+__device__ __forceinline__ int mr_kpos(int j, int kind, int L, int P, int (&g)[2]) {
+  switch (kind) {
+    case MR_EXACT:
+    case MR_LINEAR: g[0] = j; return 1;
+    case MR_CENTERED: {
+      const int d = j - (L - 1);
+      g[0] = d >= 0 ? d : d + P;
+      return 1;
+    }
+    default:
+      g[0] = j;
+      g[1] = P - L + j;
+      return j >= 1 ? 2 : 1;
+  }
+}
+
+template <typename TS, int NT, int FAM>
+__global__ void __launch_bounds__(NT)
+    conv_mixed_bwd(const TS* __restrict__ x1, const TS* __restrict__ x2, const TS* __restrict__ v,
+                   const TS* __restrict__ k, const TS* __restrict__ Dp, const TS* __restrict__ gy,
+                   TS* __restrict__ gx1, TS* __restrict__ gx2, TS* __restrict__ gv, TS* __restrict__ gk,
+                   float* __restrict__ partial, int lines, int C, MrPlan pl) {
+  extern __shared__ float2 mr_lds[];
+  constexpr uint32_t NW = NT / 64;
+  const uint32_t tid = threadIdx.x;
+  const uint32_t N = (uint32_t)pl.N, Ld = (uint32_t)pl.Ld, Kd = (uint32_t)pl.Kd;
+  const uint32_t G2 = 2 * (uint32_t)pl.Q;  // images per group
+  const uint32_t i0 = blockIdx.x * G2;
+  const uint32_t nimg = imin((int)G2, lines - (int)i0);
+  const uint32_t np = (nimg + 1) / 2;
+  float2* const tw = mr_lds;
+  float2* src = mr_lds + pl.ntw;
+  float2* dst = src + (size_t)3 * pl.Q * N;
+  float* const Dl = reinterpret_cast<float*>(dst + (size_t)3 * pl.Q * N);
+  uint32_t* const smx = reinterpret_cast<uint32_t*>(Dl + G2);         // 6 per pair
+  float2* const wsum = reinterpret_cast<float2*>(smx + 6 * pl.Q);    // 16 per pair
+  const bool exact = pl.N == pl.Ld;
+
+  __shared__ MrPass spass[kMrMaxPass];
+#pragma unroll
+  for (int i = 0; i < kMrMaxPass; ++i)
+    if (tid == (uint32_t)i && i < pl.npass) spass[i] = pl.pass[i];
+#pragma unroll
+  for (int d = 0; d < 3; ++d) {
+    if (pl.P[d] < 2) continue;
+    for (int m = tid; m < pl.P[d]; m += NT) tw[pl.twoff[d] + m] = mr_root(m, pl.P[d]);
+  }
+  for (uint32_t i = tid; i < G2; i += NT) {
+    const uint32_t img = i0 + i;
+    Dl[i] = i < nimg ? ld1(Dp + (img - fdiv(img, pl.dC) * (uint32_t)C)) : 0.f;
+  }
+  for (uint32_t i = tid; i < 6 * (uint32_t)pl.Q; i += NT) smx[i] = 0u;  // (the staging barrier orders it)
+
+  // stage the pairs' u, k and h grids
+  for (uint32_t f = tid; f < 3 * np * N; f += NT) {
+    const uint32_t gi = fdiv(f, pl.dN), p = f - gi * N;
+    const uint32_t q = gi / 3, role = gi - 3 * q;  // 0 u, 1 k, 2 h
+    const uint32_t ia = 2 * q;
+    const bool hasb = ia + 1 < nimg;
+    int n = (int)p, j = (int)p;
+    if (!exact) {
+      const uint32_t t = fdiv(p, pl.dP2), g2 = p - t * pl.P[2];
+      const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
+      n = ((int)g0 < pl.L[0] && (int)g1 < pl.L[1] && (int)g2 < pl.L[2]) ? (int)((g0 * pl.L[1] + g1) * pl.L[2] + g2)
+                                                                          : -1;
+      const int j0 = mr_kidx(g0, pl.kind[0], pl.L[0], pl.P[0]);
+      const int j1 = mr_kidx(g1, pl.kind[1], pl.L[1], pl.P[1]);
+      const int j2 = mr_kidx(g2, pl.kind[2], pl.L[2], pl.P[2]);
+      j = (j0 >= 0 && j1 >= 0 && j2 >= 0) ? (j0 * pl.KL[1] + j1) * pl.KL[2] + j2 : -1;
+    }
+    float2 z = czero();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h == 1 && !hasb) break;
+      const size_t img = i0 + ia + h;
+      float val = 0.f;
+      if (role == 1) {
+        if (j >= 0) val = ld1(k + img * Kd + j);
+      } else if (n >= 0) {
+        const size_t o = img * Ld + n;
+        val = role == 0 ? ld1(x1 + o) * ld1(v + o) : ld1(gy + o) * ld1(x2 + o);
+      }
+      if (h == 0) z.x = val;
+      else z.y = val;
+    }
+    src[f] = z;
+  }
+  __syncthreads();
+
+  // per pair: the largest magnitude of each grid part (scales) and the sums
+  // of h u of its two lines (gD), whole pairs per wavefront or S wavefronts
+  // per pair; the sums are combined in a fixed order
+  const uint32_t S = np >= NW ? 1 : NW / np;
+  {
+    const uint32_t w = tid / 64, lane = tid % 64;
+    for (uint32_t gw = w; gw < np * S; gw += NW) {
+      const uint32_t q = gw / S, part = gw % S;
+      uint32_t mx[6] = {0, 0, 0, 0, 0, 0};
+      float sa = 0.f, sb = 0.f;
+      for (uint32_t p = part * 64 + lane; p < N; p += 64 * S) {
+        const float2 zu = src[(3 * q) * N + p], zk = src[(3 * q + 1) * N + p], zh = src[(3 * q + 2) * N + p];
+        mx[0] = umax(mx[0], __float_as_uint(fabsf(zu.x)));
+        mx[1] = umax(mx[1], __float_as_uint(fabsf(zu.y)));
+        mx[2] = umax(mx[2], __float_as_uint(fabsf(zk.x)));
+        mx[3] = umax(mx[3], __float_as_uint(fabsf(zk.y)));
+        mx[4] = umax(mx[4], __float_as_uint(fabsf(zh.x)));
+        mx[5] = umax(mx[5], __float_as_uint(fabsf(zh.y)));
+        sa = fmaf(zh.x, zu.x, sa);
+        sb = fmaf(zh.y, zu.y, sb);
+      }
+#pragma unroll
+      for (int o = 32; o >= 1; o /= 2) {
+#pragma unroll
+        for (int e = 0; e < 6; ++e) mx[e] = umax(mx[e], (uint32_t)__shfl_xor((int)mx[e], o));
+        sa += __shfl_xor(sa, o);
+        sb += __shfl_xor(sb, o);
+      }
+      if (lane == 0) {
+#pragma unroll
+        for (int e = 0; e < 6; ++e) atomicMax(smx + 6 * q + e, mx[e]);
+        wsum[16 * q + part] = make_float2(sa, sb);
+      }
+    }
+  }
+  __syncthreads();
+  for (uint32_t i = tid; i < nimg; i += NT) {
+    float acc = 0.f;
+    for (uint32_t part = 0; part < S; ++part) {
+      const float2 w2 = wsum[16 * (i >> 1) + part];
+      acc += (i & 1) ? w2.y : w2.x;
+    }
+    partial[i0 + i] = acc;
+  }
+
+  // forward transforms of the 3 np grids (the first pass applies the scales)
+  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, 3 * np * N, tid, true, smx, pl.dN);
+
+  // the three products of each pair, conjugated
+  {
+    const float scale = 1.f / (float)pl.N;
+    for (uint32_t f = tid; f < np * N; f += NT) {
+      const uint32_t q = fdiv(f, pl.dN), p = f - q * N;
+      const uint32_t t = fdiv(p, pl.dP2), g2 = p - t * pl.P[2];
+      const uint32_t g0 = fdiv(t, pl.dP1), g1 = t - g0 * pl.P[1];
+      const uint32_t m0 = g0 ? pl.P[0] - g0 : 0, m1 = g1 ? pl.P[1] - g1 : 0, m2 = g2 ? pl.P[2] - g2 : 0;
+      const uint32_t pm = (m0 * pl.P[1] + m1) * pl.P[2] + m2;
+      const float2* zu = src + 3 * q * N;
+      const float2* zk = zu + N;
+      const float2* zh = zk + N;
+      float2 U[2], K[2], H[2];
+      mr_split(zu[p], zu[pm], U[0], U[1]);
+      mr_split(zk[p], zk[pm], K[0], K[1]);
+      mr_split(zh[p], zh[pm], H[0], H[1]);
+      const uint32_t* sm = smx + 6 * q;
+      float2 Z[2], Gu[2], Gk[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float D = Dl[2 * q + h];
+        const int ek = mr_exp(sm[2 + h]), ey = imax(ek, mr_fexp(D));
+        const float2 Kn = c_scale(K[h], ldexpf(1.f, ek - ey));  // K 2^-ey
+        const float Dn = ldexpf(D, -ey);
+        const float2 Us = c_scale(U[h], scale), Hs = c_scale(H[h], scale);
+        Z[h] = c_mul(Us, make_float2(Kn.x + Dn, Kn.y));
+        Gu[h] = c_mul(Hs, make_float2(Kn.x + Dn, -Kn.y));
+        Gk[h] = c_mul(Hs, c_conj(U[h]));
+      }
+      float2* out = dst + 3 * q * N;
+      out[p] = make_float2(Z[0].x - Z[1].y, -(Z[0].y + Z[1].x));
+      out[N + p] = make_float2(Gu[0].x - Gu[1].y, -(Gu[0].y + Gu[1].x));
+      out[2 * N + p] = make_float2(Gk[0].x - Gk[1].y, -(Gk[0].y + Gk[1].x));
+    }
+    __syncthreads();
+    float2* t = src;
+    src = dst;
+    dst = t;
+  }
+
+  // inverse transforms of the 3 np grids
+  mr_transform<NT, FAM>(src, dst, tw, spass, pl.npass, 3 * np * N, tid, false, smx, pl.dN);
+
+  // data points: gx2 = gy z, gx1 = gu v, gv = gu x1
+  for (uint32_t f = tid; f < nimg * Ld; f += NT) {
+    const uint32_t i = fdiv(f, pl.dLd), n = f - i * Ld;
+    uint32_t p = n;
+    if (!exact) {
+      const uint32_t t = fdiv(n, pl.dL2), n2 = n - t * pl.L[2];
+      const uint32_t n0 = fdiv(t, pl.dL1), n1 = t - n0 * pl.L[1];
+      p = (n0 * pl.P[1] + n1) * pl.P[2] + n2;
+    }
+    const uint32_t q = i >> 1, h = i & 1;
+    const uint32_t* sm = smx + 6 * q + h;  // u, k, h parts of image i: sm[0], sm[2], sm[4]
+    const int ey = imax(mr_exp(sm[2]), mr_fexp(Dl[i]));
+    const float2 rz = src[3 * q * N + p], ru = src[(3 * q + 1) * N + p];
+    const float z = ldexpf(h ? -rz.y : rz.x, mr_exp(sm[0]) + ey);
+    const float gu = ldexpf(h ? -ru.y : ru.x, mr_exp(sm[4]) + ey);
+    const size_t o = (size_t)i0 * Ld + f;
+    st1(gx2 + o, ld1(gy + o) * z);
+    st1(gx1 + o, gu * ld1(v + o));
+    st1(gv + o, gu * ld1(x1 + o));
+  }
+  // kernel points: gk at the displacement(s) of each
+  for (uint32_t f = tid; f < nimg * Kd; f += NT) {
+    const uint32_t i = fdiv(f, pl.dKd), j = f - i * Kd;
+    const uint32_t q = i >> 1, h = i & 1;
+    const float2* rg = src + (3 * q + 2) * N;
+    float acc = 0.f;
+    if (exact) {
+      const float2 r = rg[j];
+      acc = h ? -r.y : r.x;
+    } else {
+      const uint32_t t = fdiv(j, pl.dKL2), j2 = j - t * pl.KL[2];
+      const uint32_t j0 = fdiv(t, pl.dKL1), j1 = t - j0 * pl.KL[1];
+      int a0[2], a1[2], a2[2];
+      const int c0 = mr_kpos(j0, pl.kind[0], pl.L[0], pl.P[0], a0);
+      const int c1 = mr_kpos(j1, pl.kind[1], pl.L[1], pl.P[1], a1);
+      const int c2 = mr_kpos(j2, pl.kind[2], pl.L[2], pl.P[2], a2);
+      for (int e0 = 0; e0 < c0; ++e0)
+        for (int e1 = 0; e1 < c1; ++e1)
+          for (int e2 = 0; e2 < c2; ++e2) {
+            const float2 r = rg[(a0[e0] * pl.P[1] + a1[e1]) * pl.P[2] + a2[e2]];
+            acc += h ? -r.y : r.x;
+          }
+    }
+    const uint32_t* sm = smx + 6 * q + h;
+    st1(gk + (size_t)i0 * Kd + f, ldexpf(acc, mr_exp(sm[4]) + mr_exp(sm[0])));
+  }
+}
+
 bool smooth7(int64_t n) {
   if (n < 1) return false;
   for (int r : {2, 3, 5, 7})
@@ -567,6 +812,13 @@ int64_t smooth7_ceil(int64_t n) {
 size_t mr_lds_bytes(const MrPlan& pl, int Q) {
   return ((size_t)pl.ntw + (size_t)4 * Q * pl.N) * sizeof(float2) + (size_t)2 * Q * sizeof(float) +
          (size_t)4 * Q * sizeof(uint32_t);
+}
+
+// the backward's: twiddles, two buffers of 3 grids per pair, D, 6 scales and
+// 16 partial sums per pair
+size_t mr_lds_bytes_bwd(const MrPlan& pl, int Q) {
+  return ((size_t)pl.ntw + (size_t)6 * Q * pl.N) * sizeof(float2) + (size_t)2 * Q * sizeof(float) +
+         (size_t)6 * Q * sizeof(uint32_t) + (size_t)16 * Q * sizeof(float2);
 }
 
 int env_int(const char* name) {
@@ -698,6 +950,9 @@ bool mixed_plan(const FftConvArgs& a, MrPlan* pl) {
   pl->dLd = make_fastdiv((uint32_t)pl->Ld);
   pl->dC = make_fastdiv((uint32_t)a.C);
   pl->dKC = make_fastdiv((uint32_t)(a.kC ? a.kC : 1));
+  pl->dKL1 = make_fastdiv((uint32_t)pl->KL[1]);
+  pl->dKL2 = make_fastdiv((uint32_t)pl->KL[2]);
+  pl->dKd = make_fastdiv((uint32_t)pl->Kd);
   return true;
 }
 
@@ -736,6 +991,66 @@ hipError_t launch_mixed_nt(const FftConvArgs& a, const MrPlan& pl, hipStream_t s
   }
 }
 
+// The backward's plan: the forward's grid and passes, its own workgroup
+// shape (three grids per pair: about 2304 grid points per workgroup below
+// 256 transform points and 4608 from there, at least 512 workgroups where
+// the lines allow, 256 lanes for groups of at most 1152 points; one pair from
+// 1536 points on 1024 lanes, 512 for lines below 2560).
+bool mixed_bwd_plan(const FftConvArgs& a, MrPlan* pl) {
+  if (a.act || a.kC || !mixed_plan(a, pl)) return false;
+  int nt = 512, Q = 1;
+  if (pl->N < 1536) {
+    const int target = pl->N >= 256 ? 4608 : 2304;
+    Q = imax(1, (2 * target + 3 * pl->N) / (6 * pl->N));
+    Q = imax(1, imin(Q, (int)(a.lines / 1024)));
+    if (6 * Q * pl->N <= 1152) nt = 256;
+  } else {
+    nt = (a.ndim == 1 && pl->N < 2560) ? 512 : 1024;
+  }
+  if (const int o = env_int("HYENAND_MIXED_PAIRS"); o > 0) Q = o;
+  if (const int o = env_int("HYENAND_MIXED_LANES"); o == 256 || o == 512 || o == 1024) nt = o;
+  const int64_t pairs = (a.lines + 1) / 2;
+  if (Q > pairs) Q = (int)pairs;
+  while (Q > 1 && mr_lds_bytes_bwd(*pl, Q) > kMrMaxLds) --Q;
+  if (mr_lds_bytes_bwd(*pl, Q) > kMrMaxLds) return false;
+  pl->Q = Q;
+  pl->nt = nt;
+  return true;
+}
+
+template <typename TS, int NT, int FAM>
+hipError_t launch_mixed_bwd_t(const FftConvBwdArgs& b, const MrPlan& pl, hipStream_t s) {
+  const FftConvArgs& a = b.f;
+  const size_t lds = mr_lds_bytes_bwd(pl, pl.Q);
+  const unsigned nblk = (unsigned)((a.lines + 2 * pl.Q - 1) / (2 * pl.Q));
+  static std::once_flag once;
+  static hipError_t attr = hipSuccess;
+  std::call_once(once, [] {
+    attr = hipFuncSetAttribute(reinterpret_cast<const void*>(conv_mixed_bwd<TS, NT, FAM>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMrMaxLds);
+  });
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((conv_mixed_bwd<TS, NT, FAM>), dim3(nblk), dim3(NT), lds, s, (const TS*)a.x1, (const TS*)a.x2,
+                     (const TS*)a.v, (const TS*)a.k, (const TS*)a.D, (const TS*)b.gy, (TS*)b.gx1, (TS*)b.gx2,
+                     (TS*)b.gv, (TS*)b.gk, b.partial, (int)a.lines, (int)a.C, pl);
+  return hipGetLastError();
+}
+
+template <int NT, int FAM>
+hipError_t launch_mixed_bwd_f(const FftConvBwdArgs& b, const MrPlan& pl, hipStream_t s) {
+  return b.f.bf16 ? launch_mixed_bwd_t<uint16_t, NT, FAM>(b, pl, s) : launch_mixed_bwd_t<float, NT, FAM>(b, pl, s);
+}
+
+template <int NT>
+hipError_t launch_mixed_bwd_nt(const FftConvBwdArgs& b, const MrPlan& pl, hipStream_t s) {
+  switch (pl.fam) {
+    case 1: return launch_mixed_bwd_f<NT, 1>(b, pl, s);
+    case 2: return launch_mixed_bwd_f<NT, 2>(b, pl, s);
+    case 3: return launch_mixed_bwd_f<NT, 3>(b, pl, s);
+    default: return launch_mixed_bwd_f<NT, 0>(b, pl, s);
+  }
+}
+
 }  // namespace
 
 bool mixed_supported(const FftConvArgs& a) {
@@ -770,6 +1085,21 @@ hipError_t launch_mixed(const FftConvArgs& a, hipStream_t s) {
     case 512: return launch_mixed_nt<512>(a, pl, s);
     case 1024: return launch_mixed_nt<1024>(a, pl, s);
     default: return launch_mixed_nt<256>(a, pl, s);
+  }
+}
+
+bool mixed_backward_supported(const FftConvArgs& a) {
+  MrPlan pl;
+  return mixed_bwd_plan(a, &pl);
+}
+
+hipError_t launch_mixed_backward(const FftConvBwdArgs& b, hipStream_t s) {
+  MrPlan pl;
+  if (!mixed_bwd_plan(b.f, &pl)) return hipErrorInvalidValue;
+  switch (pl.nt) {
+    case 512: return launch_mixed_bwd_nt<512>(b, pl, s);
+    case 1024: return launch_mixed_bwd_nt<1024>(b, pl, s);
+    default: return launch_mixed_bwd_nt<256>(b, pl, s);
   }
 }
 

@@ -368,7 +368,7 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
 // tensors extracted from it (conv_embed.hip); gD comes out directly.  Their
 // workspace holds the nine embedded tensors (each 256-byte aligned) and then
 // the circular backward's own.
-enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP, BWD_EMBED };
+enum BwdPlan { BWD_NONE = 0, BWD_FUSED, BWD_MULTIPASS, BWD_FOURSTEP, BWD_MIXED, BWD_EMBED };
 
 BwdPlan choose_bwd_plan(const FftConvArgs& a);
 
@@ -397,6 +397,10 @@ bool embedded_problem(const FftConvArgs& a, Embedded* m) {
 
 BwdPlan choose_bwd_plan(const FftConvArgs& a) {
   if (a.centered || a.rl) {
+    // extents that are not powers of two: the mixed-radix single pass on the
+    // forward's grid where it fits (HYENAND_PLAN=nomixed avoids it)
+    const char* force = getenv("HYENAND_PLAN");
+    if (a.rl && !(force && strcmp(force, "nomixed") == 0) && mixed_backward_supported(a)) return BWD_MIXED;
     Embedded m;
     return embedded_problem(a, &m) ? BWD_EMBED : BWD_NONE;
   }
@@ -409,6 +413,7 @@ BwdPlan choose_bwd_plan(const FftConvArgs& a) {
 int64_t bwd_partials_per_line(const FftConvArgs& a, BwdPlan p) {
   switch (p) {
     case BWD_FUSED: return 1;
+    case BWD_MIXED: return 1;
     case BWD_MULTIPASS: return backward_mp_partials_per_line(a);
     case BWD_FOURSTEP: return backward_fs_partials_per_line(a);
     default: return 0;
@@ -916,6 +921,9 @@ hyenand_status hyenand_fftconv_backward(const void* x1, const void* x2, const vo
     err = launch_extract(b.f, eout, gx1, gx2, gv, gk, s);
   } else if (p == BWD_FUSED) {
     err = launch_backward(b, s);
+  } else if (p == BWD_MIXED) {
+    err = launch_mixed_backward(b, s);
+    if (err == hipSuccess) err = launch_backward_reduce(b, 1, s);
   } else {
     // the spectra of each chunk follow the gD sums in the workspace
     FftConvArgs sa = b.f;

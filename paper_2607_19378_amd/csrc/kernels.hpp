@@ -106,6 +106,10 @@ size_t backward_fs_bytes_per_line(const FftConvArgs& a);
 int64_t backward_fs_partials_per_line(const FftConvArgs& a);
 hipError_t launch_backward_fs(const FftConvBwdArgs& b, int64_t line0, int64_t nl, void* ws, hipStream_t s);
 hipError_t launch_backward_reduce(const FftConvBwdArgs& b, int64_t partials_per_line, hipStream_t s);
+// mixed-radix single pass (conv_mixed.hip) on the forward's transform grid,
+// grids of up to about 3000 points; one float of partial per line
+bool mixed_backward_supported(const FftConvArgs& a);
+hipError_t launch_mixed_backward(const FftConvBwdArgs& b, hipStream_t s);
 // centred and non-power-of-two extents (conv_embed.hip): embed x1, x2, v, gy
 // and k in the transform grid (e[0..4], lines * prod P elements each), run
 // the circular backward there, extract gx1, gx2, gv, gk (from e[0..3])

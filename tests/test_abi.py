@@ -195,12 +195,14 @@ def test_backward_validation(L):
     assert bcall(L, (2, 3, 16), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 1 << 22)) == H.ERR_UNSUPPORTED       # 2^23 transform points
     assert bcall(L, (1, 2, 2048, 4)) == H.ERR_UNSUPPORTED       # 4096 points on an axis of a 2D grid
-    # circular, not a power of two: embedded in the 32-point grid (nine
-    # tensors of 2 x 32 floats, 256 bytes each, then the gD sums)
-    assert bcall(L, (1, 2, 12), mode=1, ws_bytes=9 * 256) == H.ERR_WORKSPACE_TOO_SMALL
-    # other extents (linear) run embedded in their transform grid: nine
-    # embedded tensors of 2 x 32 floats (256 bytes each) plus the gD sums
-    assert bcall(L, (1, 2, 12), ws_bytes=9 * 256) == H.ERR_WORKSPACE_TOO_SMALL
+    # circular and linear, not a power of two: the mixed-radix single pass
+    # needs the gD sums only (one float per line, a 256-byte block)
+    assert bcall(L, (1, 2, 12), mode=1, ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
+    assert bcall(L, (1, 2, 12), ws_bytes=16) == H.ERR_WORKSPACE_TOO_SMALL
+    assert H.backward_workspace_min((1, 2, 12), "circular", "f32") == 256
+    # beyond the mixed-radix grids (10000 points): embedded in the 32768-point
+    # grid, nine embedded tensors of 2 x 32768 floats before the gD sums
+    assert bcall(L, (1, 2, 10000), mode=1, ws_bytes=9 * 2 * 32768 * 4) == H.ERR_WORKSPACE_TOO_SMALL
     # multi-pass plans: the gD sums plus one line of three spectra at least
     assert bcall(L, (1, 2, 1 << 20)) == H.ERR_WORKSPACE_TOO_SMALL
     assert bcall(L, (1, 2, 128, 128), mode=1, ws_bytes=4096) == H.ERR_WORKSPACE_TOO_SMALL

@@ -2,7 +2,11 @@
 two, every pad mode (hyenand_fftconv_backward running the circular backward
 on the transform grid of the embedded tensors) against the oracle's direct-sum backward, every
 gradient, fp32 and bf16, 1D/2D/3D, and each circular plan underneath (single
-pass, multi-pass, four-step)."""
+pass, multi-pass, four-step).  The mixed-radix backward, which takes most
+of these shapes by default, is kept off here (HYENAND_PLAN=nomixed;
+tests/test_gpu_backward_mixed.py covers it)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -19,6 +23,13 @@ def _gpu():
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
+    prev = os.environ.get("HYENAND_PLAN")
+    os.environ["HYENAND_PLAN"] = "nomixed"
+    yield
+    if prev is None:
+        del os.environ["HYENAND_PLAN"]
+    else:
+        os.environ["HYENAND_PLAN"] = prev
 
 
 def _check(shape, mode, dtype, seed):
