@@ -15,8 +15,9 @@ With no --workload, the headline workload (8 x 256 images of 64 x 64, fp32)
 and then each of the five workload configurations are timed in turn; one
 JSON line reports the headline (GElem/s, its HBM-roofline fraction from HIP
 events on the launch stream, the CPU oracle on a bounded sample) and a
-per_config list with the same figures for every configuration.  Progress
-goes to stderr.
+per_config list with the same figures for every configuration, then an
+extra_workloads list with the 14 x 14 patch-grid workload (extents that are
+not powers of two, on the mixed-radix kernels).  Progress goes to stderr.
 """
 from __future__ import annotations
 
@@ -45,6 +46,9 @@ MALL_BYTES = 256 << 20
 DEFAULT_WORKLOAD = "conv2d_64"
 # the five configurations of the metric, in the order they are reported
 CONFIG_ORDER = ["conv1d_4k", "conv2d_64", "conv2d_512c", "conv3d_128", "conv1d_1m"]
+# timed after the five in the default run and listed apart: the 14 x 14 patch
+# grid, whose extents are not powers of two (the mixed-radix kernels)
+EXTRA_ORDER = ["conv2d_14_patches"]
 
 
 def alg_bytes(w: W.Workload) -> int:
@@ -949,8 +953,9 @@ def main():
     stream_gbs = None if args.no_stream_peak else measure_stream_peak(dev, stream)
     head_name = args.workload or DEFAULT_WORKLOAD
     names = [head_name] if args.workload else [head_name] + [n for n in CONFIG_ORDER if n != head_name]
+    extra = [] if args.workload else [n for n in EXTRA_ORDER if n not in names]
     entries = {}
-    for n in names:
+    for n in names + extra:
         w = W.WORKLOADS[n]
         progress(f"{n}: generating inputs {w.shape} {w.pad_mode} {w.dtype}")
         inp = W.generate(w)
@@ -977,6 +982,7 @@ def main():
         "untimed_calls": h["untimed_calls"],
         "stream_peak_gbs": None if stream_gbs is None else round(stream_gbs, 1),
         "per_config": [entries[n] for n in names],
+        "extra_workloads": [entries[n] for n in extra],
         "kernel_source_hash": kernel_source_hash(),
     }
     print(json.dumps(out))
