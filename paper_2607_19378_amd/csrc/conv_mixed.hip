@@ -23,22 +23,25 @@
 // magnitude into [1/2, 1) before the transforms, and each product by the
 // power of two of u's scale times the larger of k's and D's (about the scale
 // of y), undone at the store, so that lines of different scales in one pair
-// do not pass their rounding error to each other either.  The products Ya and Yb (with the
-// shortcut folded in as U (K + D)) go into one grid Ya + i Yb, and one more
-// transform of its conjugate gives conj(ya + i yb): the inverse of both.  Odd
-// extents need no half-length packing this way, and each image costs one and
-// a half complex transforms of the grid.
+// do not pass their rounding error to each other either.  The products Ya
+// and Yb (with the shortcut folded in as U (K + D)) go into one grid
+// Ya + i Yb, and one more transform of its conjugate gives conj(ya + i yb):
+// the inverse of both.  Odd extents need no half-length packing this way, and
+// each image costs one and a half complex transforms of the grid.
 //
 // Each axis runs Stockham passes between two LDS buffers (one barrier per
-// pass), of the largest radix up to 16 that divides what is left of the axis
-// (16, 15, 14, 12, 10, 9, 8, 7, 6, 5, 4, 3, 2: one pass for a 14-point axis,
-// three for 1000 points), each butterfly an in-register DFT.  A pass of radix r over an axis of P points
-// with stride S, after passes whose radices multiply to Ns: butterfly j of a
-// line reads the r points j + t P/r, multiplies point t by the twiddle
-// exp(-2 pi i t (j mod Ns) / (Ns r)), takes the r-point DFT and writes output
-// t to (j div Ns) Ns r + (j mod Ns) + t Ns; after the last pass the axis is in
-// natural order.  Every pass sees the images of the workgroup as one list of
-// butterflies, so the lanes stay busy whatever the grid.
+// pass), each of the largest radix of the kernel's family that divides what
+// is left of the axis (every family has 8, 7, 5, 4, 3, 2, and one pair of
+// 14 + 12, 16 + 10 or 15 + 9: one pass for a 14-point axis, three for 1000
+// points), each butterfly an in-register DFT.  A pass of radix r over an axis
+// of P points with stride S, after passes whose radices multiply to Ns:
+// butterfly j of a line reads the r points j + t P/r, multiplies point t by
+// the twiddle exp(-2 pi i t (j mod Ns) / (Ns r)), takes the r-point DFT and
+// writes output t to (j div Ns) Ns r + (j mod Ns) + t Ns; after the last pass
+// the axis is in natural order.  Every pass sees the images of the workgroup
+// as one list of butterflies, so the lanes stay busy whatever the grid.
+//
+// The backward (conv_mixed_bwd, further down) runs on the same grids.
 #include <stdlib.h>
 #include <string.h>
 
@@ -977,7 +980,8 @@ hipError_t launch_mixed_t(const FftConvArgs& a, const MrPlan& pl, hipStream_t s)
 template <int NT, int FAM>
 hipError_t launch_mixed_f(const FftConvArgs& a, const MrPlan& pl, hipStream_t s) {
   if (a.bf16)
-    return a.act ? launch_mixed_t<uint16_t, true, NT, FAM>(a, pl, s) : launch_mixed_t<uint16_t, false, NT, FAM>(a, pl, s);
+    return a.act ? launch_mixed_t<uint16_t, true, NT, FAM>(a, pl, s)
+                 : launch_mixed_t<uint16_t, false, NT, FAM>(a, pl, s);
   return a.act ? launch_mixed_t<float, true, NT, FAM>(a, pl, s) : launch_mixed_t<float, false, NT, FAM>(a, pl, s);
 }
 
