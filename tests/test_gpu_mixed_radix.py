@@ -150,6 +150,15 @@ def test_radix_families(family, grid, mode):
                   HYENAND_MIXED_FAMILY=family) == _mixed(len(grid))
 
 
+# the largest grids these kernels take (3600 points, 144 KB of LDS, and 3840
+# of at most 4096 points; one pair per workgroup) and unit axes squeezed away
+@pytest.mark.parametrize("grid,mode", [((3600,), "circular"), ((16, 16, 15), "circular"), ((1, 14), "circular"),
+                                       ((14, 1), "centered"), ((1, 1, 21), "linear")])
+def test_extremes(grid, mode):
+    plan = _check("extreme", 2, 3, grid, mode, "f32", 950 + sum(grid), HYENAND_PLAN="mixed")
+    assert plan == _mixed(sum(1 for g in grid if g > 1))
+
+
 @pytest.mark.parametrize("grid,mode", [((14, 14), "circular"), ((100,), "circular"), ((14, 14), "centered")])
 def test_shared_kernel(grid, mode):
     _check("shared", 3, 4, grid, mode, "f32", 700, shared=True, HYENAND_PLAN="mixed")
