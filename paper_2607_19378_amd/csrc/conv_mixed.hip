@@ -996,18 +996,22 @@ hipError_t launch_mixed_nt(const FftConvArgs& a, const MrPlan& pl, hipStream_t s
 }
 
 // The backward's plan: the forward's grid and passes, its own workgroup
-// shape (three grids per pair: about 2304 grid points per workgroup below
-// 256 transform points and 4608 from there, at least 512 workgroups where
-// the lines allow, 256 lanes for groups of at most 1152 points; one pair from
-// 1536 points on 1024 lanes, 512 for lines below 2560).
+// shape, from a sweep of 256 .. 1024 lanes and 1 .. 4 pairs (three grids per
+// pair): about 2304 grid points per workgroup below 512 transform points, at
+// least 512 workgroups where the lines allow, 256 lanes for groups of at most
+// 1152 points; one pair from 512 points (64 x 64 lines of 1000: 101 us
+// against 127 with two), on 256 lanes for 2D and 3D grids below 1024 points
+// (16 x 384 centred 14 x 14: 88 us against 93 on 512); from 1536 points on
+// 1024 lanes, 512 for lines below 2560.
 bool mixed_bwd_plan(const FftConvArgs& a, MrPlan* pl) {
   if (a.act || a.kC || !mixed_plan(a, pl)) return false;
   int nt = 512, Q = 1;
-  if (pl->N < 1536) {
-    const int target = pl->N >= 256 ? 4608 : 2304;
-    Q = imax(1, (2 * target + 3 * pl->N) / (6 * pl->N));
+  if (pl->N < 512) {
+    Q = imax(1, (2 * 2304 + 3 * pl->N) / (6 * pl->N));
     Q = imax(1, imin(Q, (int)(a.lines / 1024)));
     if (6 * Q * pl->N <= 1152) nt = 256;
+  } else if (pl->N < 1536) {
+    nt = (a.ndim >= 2 && pl->N < 1024) ? 256 : 512;
   } else {
     nt = (a.ndim == 1 && pl->N < 2560) ? 512 : 1024;
   }
