@@ -113,9 +113,10 @@ hyenand_status parse_shape(int ndim, const int64_t* dims, int pad_mode, int dtyp
   return HYENAND_OK;
 }
 
-// A shape whose extents are not powers of two and that no single-pass kernel
-// takes runs embedded in its transform grid (P_d >= 2 L_d - 1, a power of
-// two): on that grid the call is the circular convolution of the zero-padded
+// A shape whose extents are not powers of two and that neither the
+// power-of-two single-pass kernels nor the mixed-radix ones take runs
+// embedded in its transform grid (P_d >= 2 L_d - 1, a power of two): on that
+// grid the call is the circular convolution of the zero-padded
 // inputs and of k placed at its displacements (conv_embed.hip), so x1, x2, v
 // and k are embedded, the circular plan of the grid runs, and y is extracted.
 // The workspace holds the five embedded tensors (x1, x2, v, k, y; each
@@ -362,9 +363,11 @@ hipError_t run_chunked(const FftConvArgs& a, size_t per, hipStream_t caller, Lau
 // with three signals.  The workspace holds the gD sums (256-byte aligned
 // block) and then the spectra of a chunk of lines per side stream.
 //
-// The centred mode and extents that are not powers of two (BWD_EMBED) run the
-// circular backward on their transform grid (P_d >= 2 L_d - 1, a power of
-// two): the five inputs are embedded in that grid and the four gradient
+// Extents that are not powers of two run the mixed-radix single pass
+// (BWD_MIXED, conv_mixed.hip) where their grid fits; those beyond it and the
+// centred mode on power-of-two extents (BWD_EMBED) run the circular backward
+// on their transform grid (P_d >= 2 L_d - 1, a power of two): the five
+// inputs are embedded in that grid and the four gradient
 // tensors extracted from it (conv_embed.hip); gD comes out directly.  Their
 // workspace holds the nine embedded tensors (each 256-byte aligned) and then
 // the circular backward's own.

@@ -59,8 +59,9 @@ hipError_t launch_fused2d(const FftConvArgs& a, hipStream_t s);
 // (centered or non-power-of-two grids, the operator)
 size_t fused2d_khat_bytes(const FftConvArgs& a);
 
-// single pass for grid extents that are not powers of two (linear and
-// centered modes, transform P_d = the smallest power of two >= 2 L_d - 1)
+// single pass for grid extents that are not powers of two on power-of-two
+// transforms (P_d = the smallest power of two >= 2 L_d - 1; a circular axis
+// as the centred convolution of the periodically repeated kernel)
 bool fused_rl_supported(const FftConvArgs& a);
 hipError_t launch_fused_rl(const FftConvArgs& a, hipStream_t s);
 
